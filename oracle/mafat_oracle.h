@@ -1,0 +1,107 @@
+/*
+ * mafat_oracle.h -- CPU reference ("oracle") for fused tile partitioning (FTP)
+ * of a stack of convolution / max-pool layers, as used by MAFAT
+ * (Farley & Gerstlauer, "MAFAT: Memory-Aware Fusing and Tiling of Neural
+ * Networks for Accelerated Edge Inference", arXiv 2107.06960).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This library exists to check the GPU library
+ * against; nothing in the product path may link, load or call it.  It shares
+ * no code, header or table with the GPU library.
+ *
+ * Everything here is plain, slow and written to be checked by eye:
+ *   - tensors are float64 ("double"), NHWC, frame-major;
+ *   - convolution weights are [c_out][f][f][c_in];
+ *   - one fixed summation order per output element (ky, kx, ci), in double.
+ *
+ * Rectangles are half-open, in the coordinates of the tensor they index:
+ *   rect = {y0, y1, x0, x1}  covers rows [y0, y1) and columns [x0, x1).
+ *
+ * Return values: 0 on success, negative on error (see ORC_E*).
+ */
+#ifndef MAFAT_ORACLE_H
+#define MAFAT_ORACLE_H
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { ORC_CONV = 0, ORC_MAXPOOL = 1 };
+enum { ORC_ACT_LINEAR = 0, ORC_ACT_LEAKY01 = 1 };
+enum {
+  ORC_OK = 0,
+  ORC_EINVAL = -1,     /* bad argument or layer description          */
+  ORC_EREGION = -2,    /* a tile read outside the region it was given */
+  ORC_ENOMEM = -3,
+  ORC_ENOTRECT = -4    /* brute-force receptive field is not a rectangle */
+};
+
+/* One layer.  c_out is ignored for max-pool (channels pass through). */
+typedef struct {
+  int op, c_out, f, s, p, act;
+} orc_layer;
+
+/* Shape inference (paper section 4.1: each layer has width, height, filter
+ * size and stride; padding and channel counts are added here).
+ * dims[6*l + 0..5] = in_h, in_w, in_c, out_h, out_w, out_c of layer l. */
+int orc_shapes(const orc_layer* layers, int n, int h, int w, int c, int* dims);
+
+/* Untiled, layer-by-layer forward of layers [l0, l1] for `batch` frames.
+ * x is the input of layer l0, y receives the output of layer l1.
+ * w/scale/bias are indexed by global layer number (NULL entries for pools).
+ * round_bf16 != 0 rounds every layer output to bfloat16 (round to nearest
+ * even), emulating a bf16-activation execution. */
+int orc_forward_layers(const orc_layer* layers, int n, int h, int w, int c,
+                       int l0, int l1, int batch, const double* x,
+                       const double* const* wt, const double* const* scale,
+                       const double* const* bias, int round_bf16, double* y);
+
+/* Number of ints orc_regions / orc_regions_bruteforce write:
+ * sum over groups of tiles(g) * layers(g) * 8. */
+int orc_regions_size(int n, const int* group_start, int n_groups,
+                     const int* grid_rows, const int* grid_cols);
+
+/* Per-group, per-tile, per-layer regions by interval back-projection
+ * (the "Grid"/traversal function of section 4.1).  Layout, concatenated over
+ * groups g: [tile t (row-major)][layer l - g0][in y0,y1,x0,x1, out y0,y1,x0,x1].
+ * Group g covers layers [group_start[g], group_start[g+1]) (last: to n). */
+int orc_regions(const orc_layer* layers, int n, int h, int w, int c,
+                const int* group_start, int n_groups, const int* grid_rows,
+                const int* grid_cols, int* out);
+
+/* The same table, built by enumerating every contributing input element of
+ * every output element of each tile (receptive fields), layer by layer.
+ * Returns ORC_ENOTRECT if a receptive field is not a full rectangle. */
+int orc_regions_bruteforce(const orc_layer* layers, int n, int h, int w, int c,
+                           const int* group_start, int n_groups,
+                           const int* grid_rows, const int* grid_cols, int* out);
+
+/* FTP execution (sections 3-4): every group is split into its own output tile
+ * grid, every tile is pushed through all layers of the group using only its
+ * own input region, and tile outputs are stitched into the group output,
+ * which is the next group's input.  y receives the network output;
+ * cut_out[g] (if cut_out and cut_out[g] are non-NULL) receives the output of
+ * group g < n_groups-1.  Returns ORC_EREGION if a tile needed an element
+ * outside its region. */
+int orc_forward_tiled(const orc_layer* layers, int n, int h, int w, int c,
+                      int batch, const int* group_start, int n_groups,
+                      const int* grid_rows, const int* grid_cols,
+                      const double* x, const double* const* wt,
+                      const double* const* scale, const double* const* bias,
+                      int round_bf16, double* y, double* const* cut_out);
+
+/* Output of the whole stack [0, n) on one output rectangle of one frame,
+ * computed from that rectangle's receptive field only (a one-tile FTP).
+ * y holds (oy1-oy0) x (ox1-ox0) x c_out values, NHWC. */
+int orc_forward_rect(const orc_layer* layers, int n, int h, int w, int c,
+                     const double* x, const double* const* wt,
+                     const double* const* scale, const double* const* bias,
+                     int round_bf16, int oy0, int oy1, int ox0, int ox1,
+                     double* y);
+
+/* bfloat16 round-to-nearest-even of a value (via float32), as a double. */
+double orc_round_bf16(double v);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

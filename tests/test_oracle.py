@@ -1,0 +1,339 @@
+"""Pins of the CPU oracle against things other than itself: hand-computed
+cases, closed forms, brute-force receptive fields, library routines (numpy
+matmul, torch conv2d/max_pool2d in float64 on the CPU) and the numbers the
+paper prints about its workload.  No GPU."""
+import os
+
+import numpy as np
+import pytest
+
+from paper_2107_06960_amd import workloads as W
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _params_single(w, scale, bias):
+    return {"w": [np.asarray(w, np.float64)], "scale": [np.asarray(scale, np.float64)],
+            "bias": [np.asarray(bias, np.float64)]}
+
+
+def _read_golden(name):
+    lines = []
+    with open(os.path.join(GOLD, name)) as fh:
+        for ln in fh:
+            ln = ln.strip()
+            if not ln or ln.startswith("#"):
+                continue
+            lines.append(ln.split())
+    return lines
+
+
+# --------------------------------------------------------------- closed forms
+
+def test_ones_kernel_counts_in_image_neighbours(orc):
+    # all-ones 3x3 kernel on an all-ones image: 4 at corners, 6 on edges, 9 inside
+    L = [W.conv(1, 3, act=W.LINEAR)]
+    x = np.ones((1, 6, 7, 1))
+    y = orc.forward_layers(L, 6, 7, 1, x, _params_single(np.ones((1, 3, 3, 1)), [1.0], [0.0]))[0, :, :, 0]
+    exp = np.full((6, 7), 9.0)
+    exp[0, :] = exp[-1, :] = 6
+    exp[:, 0] = exp[:, -1] = 6
+    exp[0, 0] = exp[0, -1] = exp[-1, 0] = exp[-1, -1] = 4
+    assert np.array_equal(y, exp)
+
+
+def test_leaky_on_negative_input(orc):
+    # input -1 -> sums -4/-6/-9 -> leaky 0.1 -> -0.4/-0.6/-0.9
+    L = [W.conv(1, 3, act=W.LEAKY)]
+    x = -np.ones((1, 3, 3, 1))
+    y = orc.forward_layers(L, 3, 3, 1, x, _params_single(np.ones((1, 3, 3, 1)), [1.0], [0.0]))[0, :, :, 0]
+    exp = np.array([[-0.4, -0.6, -0.4], [-0.6, -0.9, -0.6], [-0.4, -0.6, -0.4]])
+    np.testing.assert_allclose(y, exp, rtol=0, atol=1e-15)
+
+
+def test_leaky_at_zero_is_zero(orc):
+    L = [W.conv(1, 1, act=W.LEAKY)]
+    y = orc.forward_layers(L, 1, 2, 1, np.array([[[[0.0], [5.0]]]]), _params_single([[[[1.0]]]], [1.0], [0.0]))
+    assert y[0, 0, 0, 0] == 0.0 and y[0, 0, 1, 0] == 5.0
+
+
+def test_two_layer_ramp_golden(orc):
+    g = {ln[0]: np.array([float(v) for v in ln[1:]]) for ln in _read_golden("ramp4_conv_pool.txt")}
+    x = (4 * np.arange(4)[:, None] + np.arange(4)[None, :]).astype(np.float64).reshape(1, 4, 4, 1)
+    w = np.ones((1, 3, 3, 1))
+    for case, scale, bias, act in (("A", 1.0, 0.0, W.LINEAR), ("B", 0.5, -20.0, W.LEAKY)):
+        L = [W.conv(1, 3, act=act), W.maxpool()]
+        p = {"w": [w, None], "scale": [np.array([scale]), None], "bias": [np.array([bias]), None]}
+        conv_out = orc.forward_layers(L, 4, 4, 1, x, p, 0, 0)
+        pool_out = orc.forward_layers(L, 4, 4, 1, x, p)
+        np.testing.assert_allclose(conv_out.ravel(), g[case + "_CONV"], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(pool_out.ravel(), g[case + "_POOL"], rtol=0, atol=1e-12)
+
+
+def test_conv1x1_is_matmul(orc):
+    rng = np.random.default_rng(3)
+    B, H, Wd, Ci, Co = 2, 5, 7, 6, 4
+    x = rng.standard_normal((B, H, Wd, Ci))
+    w = rng.standard_normal((Co, 1, 1, Ci))
+    s = rng.uniform(0.5, 1.5, Co)
+    b = rng.standard_normal(Co)
+    L = [W.conv(Co, 1, act=W.LINEAR)]
+    y = orc.forward_layers(L, H, Wd, Ci, x, _params_single(w, s, b))
+    ref = (x.reshape(-1, Ci) @ w.reshape(Co, Ci).T) * s + b
+    np.testing.assert_allclose(y.reshape(-1, Co), ref, rtol=1e-12, atol=1e-12)
+
+
+def test_conv3x3_is_im2col_matmul(orc):
+    # Darknet's formulation (the paper's "scratch space", section 2): unfold
+    # every 3x3 zero-padded window into a row, then one matrix product.
+    rng = np.random.default_rng(4)
+    H, Wd, Ci, Co = 6, 5, 3, 7
+    x = rng.standard_normal((1, H, Wd, Ci))
+    w = rng.standard_normal((Co, 3, 3, Ci))
+    xp = np.zeros((H + 2, Wd + 2, Ci))
+    xp[1:-1, 1:-1] = x[0]
+    cols = np.stack([xp[yy:yy + 3, xx:xx + 3, :].ravel() for yy in range(H) for xx in range(Wd)])
+    ref = cols @ w.reshape(Co, -1).T
+    L = [W.conv(Co, 3, act=W.LINEAR)]
+    y = orc.forward_layers(L, H, Wd, Ci, x, _params_single(w, np.ones(Co), np.zeros(Co)))
+    np.testing.assert_allclose(y.reshape(-1, Co), ref, rtol=1e-12, atol=1e-12)
+
+
+def _torch_forward(layers, x, params):
+    import torch
+    import torch.nn.functional as F
+    t = torch.from_numpy(np.asarray(x, np.float64)).permute(0, 3, 1, 2)
+    for k, L in enumerate(layers):
+        if L["op"] == W.CONV:
+            wt = torch.from_numpy(np.asarray(params["w"][k], np.float64)).permute(0, 3, 1, 2)
+            t = F.conv2d(t, wt, stride=L["s"], padding=L["p"])
+            t = t * torch.from_numpy(np.asarray(params["scale"][k], np.float64))[None, :, None, None]
+            t = t + torch.from_numpy(np.asarray(params["bias"][k], np.float64))[None, :, None, None]
+            if L["act"] == W.LEAKY:
+                t = F.leaky_relu(t, 0.1)
+        else:
+            t = F.max_pool2d(t, L["f"], L["s"], L["p"])
+    return t.permute(0, 2, 3, 1).numpy()
+
+
+def test_untiled_matches_torch_fp64_tiny(orc):
+    wl = W.WORKLOADS["tiny"]
+    p = W.workload_inputs(wl)
+    y = orc.forward_layers(wl.layers, wl.h, wl.w, wl.c, p["x"], p)
+    ref = _torch_forward(wl.layers, p["x"], p)
+    assert np.max(np.abs(y - ref)) <= 1e-12 * max(1.0, np.max(np.abs(ref)))
+
+
+@pytest.mark.slow
+def test_untiled_matches_torch_fp64_yolo_small_image(orc):
+    # the full 16-layer YOLOv2 stack on a 48x48 image (all layer kinds, 512 ch)
+    p = W.make_inputs(W.YOLOV2_16, 48, 48, 3, 1, seed=7)
+    y = orc.forward_layers(W.YOLOV2_16, 48, 48, 3, p["x"], p)
+    ref = _torch_forward(W.YOLOV2_16, p["x"], p)
+    assert np.max(np.abs(y - ref)) <= 1e-10 * np.max(np.abs(ref))
+
+
+def test_strided_and_padded_layers_match_torch(orc):
+    rng = np.random.default_rng(5)
+    L = [{"op": "conv", "c_out": 5, "f": 3, "s": 2, "p": 1, "act": "leaky"},
+         {"op": "max", "c_out": 0, "f": 3, "s": 1, "p": 1, "act": "linear"},
+         {"op": "conv", "c_out": 3, "f": 5, "s": 1, "p": 2, "act": "linear"},
+         {"op": "max", "c_out": 0, "f": 2, "s": 2, "p": 0, "act": "linear"}]
+    p = W.make_inputs(L, 13, 11, 2, 2, seed=11)
+    y = orc.forward_layers(L, 13, 11, 2, p["x"], p)
+    ref = _torch_forward(L, p["x"], p)
+    assert y.shape == ref.shape
+    assert np.max(np.abs(y - ref)) <= 1e-12 * np.max(np.abs(ref))
+
+
+def test_bf16_rounding_matches_torch(orc):
+    import torch
+    rng = np.random.default_rng(0)
+    vals = np.concatenate([rng.standard_normal(2000) * 10.0 ** rng.integers(-6, 6, 2000),
+                           [0.0, -0.0, 1.0, 1.00390625, 1.01171875, 3.0e38, -2.5e-38]]).astype(np.float32)
+    ref = torch.from_numpy(vals).to(torch.bfloat16).to(torch.float64).numpy()
+    got = np.array([orc.round_bf16(float(v)) for v in vals])
+    assert np.array_equal(got, ref)
+    assert np.array_equal(W.bf16_round(vals).astype(np.float64), ref)
+
+
+# --------------------------------------------------------------- regions
+
+def test_tiny_regions_golden(orc):
+    wl = W.WORKLOADS["tiny"]
+    gs, r, c = wl.groups()
+    R = orc.regions(wl.layers, wl.h, wl.w, wl.c, gs, r, c)[0]
+    for ln in _read_golden("tiny_regions.txt"):
+        ti, tj, l, *rect = map(int, ln)
+        assert list(R[ti * 2 + tj, l]) == rect, (ti, tj, l)
+
+
+def _random_stack(rng, max_layers=4):
+    n = int(rng.integers(1, max_layers + 1))
+    layers = []
+    for _ in range(n):
+        if rng.random() < 0.6:
+            f = int(rng.choice([1, 2, 3, 5]))
+            s = 1 if f == 1 else int(rng.choice([1, 1, 2]))   # stride <= filter: gap-free fields
+            layers.append({"op": "conv", "c_out": int(rng.integers(1, 4)), "f": f,
+                           "s": s, "p": int(rng.integers(0, f)), "act": "leaky"})
+        else:
+            f = int(rng.choice([2, 3]))
+            layers.append({"op": "max", "c_out": 0, "f": f, "s": int(rng.choice([1, 2])),
+                           "p": int(rng.integers(0, (f + 1) // 2)), "act": "linear"})
+    return layers
+
+
+def _random_case(orc, rng):
+    while True:
+        layers = _random_stack(rng)
+        h, w = int(rng.integers(4, 24)), int(rng.integers(4, 24))
+        try:
+            dims = orc.shapes(layers, h, w, 2)
+        except orc.OracleError:
+            continue
+        n = len(layers)
+        ng = int(rng.integers(1, min(3, n) + 1))
+        cuts = sorted(rng.choice(np.arange(1, n), size=ng - 1, replace=False).tolist()) if ng > 1 else []
+        gs = [0] + [int(v) for v in cuts]
+        rows, cols = [], []
+        for g in range(ng):
+            last = (gs[g + 1] if g + 1 < ng else n) - 1
+            rows.append(int(rng.integers(1, min(5, dims[last, 3]) + 1)))
+            cols.append(int(rng.integers(1, min(5, dims[last, 4]) + 1)))
+        return layers, h, w, gs, rows, cols
+
+
+def test_regions_equal_bruteforce_random(orc):
+    rng = np.random.default_rng(2024)
+    for _ in range(300):
+        layers, h, w, gs, rows, cols = _random_case(orc, rng)
+        A = orc.regions(layers, h, w, 2, gs, rows, cols)
+        B = orc.regions_bruteforce(layers, h, w, 2, gs, rows, cols)
+        for a, b in zip(A, B):
+            assert np.array_equal(a, b), (layers, h, w, gs, rows, cols)
+
+
+def test_regions_equal_bruteforce_yolo_configs(orc):
+    # the YOLOv2 stack at a reduced 96x96 image with the paper's cut points
+    for spec in ("1x1/NoCut", "3x3/NoCut", "2x2/12/2x2", "5x5/8/2x2", "3x3/4/2x2", "4x4/12/1x1"):
+        gs, r, c = W.parse_tiling(spec, 16)
+        A = orc.regions(W.YOLOV2_16, 96, 96, 3, gs, r, c)
+        B = orc.regions_bruteforce(W.YOLOV2_16, 96, 96, 3, gs, r, c)
+        for a, b in zip(A, B):
+            assert np.array_equal(a, b), spec
+
+
+def test_region_invariants_full_size(orc):
+    dims = orc.shapes(W.YOLOV2_16, 608, 608, 3)
+    for spec in ("5x5/8/2x2", "4x4/12/1x1", "6x6/4/2x2", "3x3/NoCut"):
+        gs, r, c = W.parse_tiling(spec, 16)
+        for g, R in enumerate(orc.regions(W.YOLOV2_16, 608, 608, 3, gs, r, c)):
+            g0 = gs[g]
+            last = (gs[g + 1] if g + 1 < len(gs) else 16) - 1
+            cover = np.zeros((dims[last, 3], dims[last, 4]), np.int32)
+            for t in range(R.shape[0]):
+                o = R[t, -1, 4:]
+                cover[o[0]:o[1], o[2]:o[3]] += 1
+                for k in range(R.shape[1]):
+                    l = g0 + k
+                    iy0, iy1, ix0, ix1, oy0, oy1, ox0, ox1 = R[t, k]
+                    assert 0 <= iy0 < iy1 <= dims[l, 0] and 0 <= ix0 < ix1 <= dims[l, 1]
+                    assert 0 <= oy0 < oy1 <= dims[l, 3] and 0 <= ox0 < ox1 <= dims[l, 4]
+                    if k > 0:
+                        assert list(R[t, k, :4]) == list(R[t, k - 1, 4:])
+            assert np.all(cover == 1), spec   # tiles partition the group output
+
+
+def test_one_by_one_grid_is_whole_tensor(orc):
+    dims = orc.shapes(W.YOLOV2_16, 96, 96, 3)
+    R = orc.regions(W.YOLOV2_16, 96, 96, 3, [0], [1], [1])[0]
+    for l in range(16):
+        assert list(R[0, l]) == [0, dims[l, 0], 0, dims[l, 1], 0, dims[l, 3], 0, dims[l, 4]]
+
+
+# --------------------------------------------------------------- tiled == untiled
+
+def test_tiled_equals_untiled_random(orc):
+    rng = np.random.default_rng(77)
+    for _ in range(120):
+        layers, h, w, gs, rows, cols = _random_case(orc, rng)
+        p = W.make_inputs(layers, h, w, 2, 2, seed=int(rng.integers(1 << 30)))
+        ref = orc.forward_layers(layers, h, w, 2, p["x"], p)
+        got = orc.forward_tiled(layers, h, w, 2, p["x"], p, gs, rows, cols)
+        assert np.array_equal(ref, got), (layers, h, w, gs, rows, cols)
+
+
+def test_tiled_equals_untiled_yolo_small(orc):
+    p = W.make_inputs(W.YOLOV2_16, 64, 64, 3, 1, seed=1)
+    ref = orc.forward_layers(W.YOLOV2_16, 64, 64, 3, p["x"], p)
+    for spec in ("4x4/NoCut", "3x3/8/2x2", "2x2/4/3x3"):
+        gs, r, c = W.parse_tiling(spec, 16)
+        got, cuts = orc.forward_tiled(W.YOLOV2_16, 64, 64, 3, p["x"], p, gs, r, c, want_cuts=True)
+        assert np.array_equal(ref, got), spec
+        if len(gs) > 1:
+            cut_ref = orc.forward_layers(W.YOLOV2_16, 64, 64, 3, p["x"], p, 0, gs[1] - 1)
+            assert np.array_equal(cut_ref, cuts[0]), spec
+
+
+def test_tiled_equals_untiled_bf16_emulation(orc):
+    wl = W.WORKLOADS["tiny"]
+    p = W.make_inputs(wl.layers, wl.h, wl.w, wl.c, 2, 0, "bf16")
+    ref = orc.forward_layers(wl.layers, wl.h, wl.w, wl.c, p["x"], p, round_bf16=True)
+    got = orc.forward_tiled(wl.layers, wl.h, wl.w, wl.c, p["x"], p, [0], [2], [3], round_bf16=True)
+    assert np.array_equal(ref, got)
+    # every emulated activation is a bfloat16 value
+    assert np.array_equal(W.bf16_round(ref.astype(np.float32)).astype(np.float64), ref)
+
+
+def test_forward_rect_equals_untiled_crop(orc):
+    p = W.make_inputs(W.YOLOV2_16, 64, 64, 3, 1, seed=2)
+    ref = orc.forward_layers(W.YOLOV2_16, 64, 64, 3, p["x"], p)
+    for (a, b, c, d) in ((0, 1, 0, 1), (1, 3, 2, 4), (3, 4, 0, 4)):
+        got = orc.forward_rect(W.YOLOV2_16, 64, 64, 3, p["x"][0], p, a, b, c, d)
+        assert np.array_equal(got, ref[0, a:b, c:d])
+
+
+def test_bad_arguments_are_errors(orc):
+    with pytest.raises(orc.OracleError):
+        orc.shapes([W.conv(4, 3)], 0, 5, 1)
+    with pytest.raises(orc.OracleError):      # grid finer than the output
+        orc.regions(W.TINY, 8, 8, 3, [0], [5], [1])
+    with pytest.raises(orc.OracleError):      # group start not 0
+        orc.regions(W.TINY, 8, 8, 3, [1], [1], [1])
+
+
+# --------------------------------------------------------------- the paper's workload
+
+def test_layer2_memory_matches_paper_135MB(orc):
+    """Section 2: layer 2 of YOLOv2 has the largest combined memory, at least
+    135 MB, with per-layer scratch up to about 100 MB.  Darknet's scratch is
+    the unfolded (im2col) input, out_h*out_w*c_in*f*f elements; with float32
+    at 608x608 the oracle's shapes give 135.38 MiB at layer 2, and layer 2 is
+    the largest of the 16 layers."""
+    dims = orc.shapes(W.YOLOV2_16, 608, 608, 3)
+    mib = []
+    for l, L in enumerate(W.YOLOV2_16):
+        ih, iw, ic, oh, ow, oc = dims[l]
+        scratch = oh * ow * ic * L["f"] ** 2 if L["op"] == W.CONV else 0
+        mib.append((ih * iw * ic + oh * ow * oc + scratch) * 4 / 2 ** 20)
+    assert int(np.argmax(mib)) == 2
+    assert 135.0 <= mib[2] < 136.0
+    ih, iw, ic, oh, ow, oc = dims[2]
+    assert 95 <= oh * ow * ic * 9 * 4 / 2 ** 20 <= 105       # "as high as 100MB"
+    assert list(dims[-1]) == [38, 38, 512, 38, 38, 256]
+
+
+def test_cut_candidates_follow_maxpools():
+    """Section 4: the YOLOv2 cut candidates 2, 4, 8 and 12 lie directly after
+    max-pool layers."""
+    pools = [l for l, L in enumerate(W.YOLOV2_16) if L["op"] == W.MAXPOOL]
+    assert [p + 1 for p in pools] == [2, 4, 8, 12]
+
+
+def test_parse_tiling():
+    assert W.parse_tiling("5x5/8/2x2", 16) == ([0, 8], [5, 2], [5, 2])
+    assert W.parse_tiling("1x1/NoCut", 16) == ([0], [1], [1])
+    assert W.parse_tiling("3x4", 16) == ([0], [3], [4])
+    with pytest.raises(ValueError):
+        W.parse_tiling("5x5/16/2x2", 16)
