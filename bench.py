@@ -1,0 +1,295 @@
+"""Benchmark: fused-tile (MAFAT) execution of YOLOv2 layers 0-15 on one GPU.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--graph]
+
+Default workload: 608x608x3, bf16 activations/weights with fp32 accumulate,
+two groups -- layers 0-7 on a 5x5 tile grid, layers 8-15 on 2x2
+("5x5/8/2x2"), batch 1.  Inputs are seeded synthetic tensors already resident
+in device memory; one step is one pass of the whole stack (both groups).
+
+Prints ONE JSON line: frames/s (value), executed/useful TFLOP/s and their
+fraction of the bf16 (or fp32) matrix-core peak, per-group and per-stage
+times from HIP events recorded on the launch stream, the roofline of the
+dominant stage kernel, peak device memory against the untiled layer-by-layer
+baseline, and the CPU oracle's rate on a bounded sample (baseline only).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "frames/s + TFLOP/s (frac of MFMA peak), YOLOv2 L0-15 608² 2-group tiled"
+PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}   # MI355X dense matrix-core peaks
+PEAK_HBM_GBS = 8000.0
+
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime torch has loaded."""
+
+    def __init__(self):
+        self.rt = ctypes.CDLL("libamdhip64.so.7")   # already loaded by torch: same runtime
+        self.rt.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                ctypes.c_void_p]
+        self.rt.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.rt.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+
+    def create(self, n):
+        out = []
+        for _ in range(n):
+            e = ctypes.c_void_p()
+            assert self.rt.hipEventCreate(ctypes.byref(e)) == 0
+            out.append(e.value)
+        return out
+
+    def ms(self, a, b):
+        f = ctypes.c_float()
+        assert self.rt.hipEventSynchronize(b) == 0
+        assert self.rt.hipEventElapsedTime(ctypes.byref(f), a, b) == 0
+        return f.value
+
+    def destroy(self, evs):
+        for e in evs:
+            self.rt.hipEventDestroy(e)
+
+
+def stage_flops(plan, g):
+    """Executed FLOPs (2 * MAC, halo recompute included) of every stage of
+    group g for one frame, from the plan's region table."""
+    first, nl, nt = plan.group(g)
+    R = plan.regions(g)
+    out = []
+    for (a, b) in plan.stages(g):
+        L = plan.layers[a]
+        if L["op"] != "conv":
+            out.append(0)
+            continue
+        d = plan.shape(a)
+        per = d[5] * L["f"] * L["f"] * d[2]
+        k = a - first
+        area = sum(int(R[t, k, 5] - R[t, k, 4]) * int(R[t, k, 7] - R[t, k, 6]) for t in range(nt))
+        out.append(2 * area * per)
+    return out
+
+
+def untiled_groups(layers):
+    """Every stage its own group on a 1x1 grid: the untiled layer-by-layer
+    execution with the same kernels (a conv and its following pool fused)."""
+    starts, l = [], 0
+    while l < len(layers):
+        starts.append(l)
+        l += 2 if (layers[l]["op"] == "conv" and l + 1 < len(layers) and layers[l + 1]["op"] == "max") else 1
+    return starts, [1] * len(starts), [1] * len(starts)
+
+
+def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs=2):
+    import torch
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    torch.cuda.reset_peak_memory_stats()
+    base = torch.cuda.memory_allocated()
+    plan = M.Plan(layers, hwc, tiling)
+    net = M.Network(plan, params, batch, dtype)
+    x = net.input_tensor(x_np)
+    for _ in range(runs):
+        net.run(x)
+    torch.cuda.synchronize()
+    peak = torch.cuda.max_memory_allocated() - base
+    t0 = time.perf_counter()
+    n = 20
+    for _ in range(n):
+        net.run(x)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / n * 1e3
+    del net, x
+    return peak, ms
+
+
+def cpu_baseline(wl, params, exec_macs_per_frame, min_s=10.0, max_s=30.0):
+    """Oracle rate (MAC/s) on one core, on 2x2-pixel output rectangles of
+    frame 0 (each computed from its whole receptive-field cone through layers
+    0-15), extrapolated to a frame by the configuration's executed MACs."""
+    import numpy as np
+    from oracle import oracle as O
+    layers = wl.layers
+    dims = O.shapes(layers, wl.h, wl.w, wl.c)
+    oh, ow = int(dims[-1, 3]), int(dims[-1, 4])
+    gr, gc = oh // 2, ow // 2
+    R = O.regions(layers, wl.h, wl.w, wl.c, [0], [gr], [gc])[0]
+    order = [(gr // 2) * gc + gc // 2, 0, gr * gc - 1, (gr // 2) * gc, gc - 1, (gr // 4) * gc + gc // 4]
+    x0 = params["x"][0]
+    macs = 0
+    t0 = time.perf_counter()
+    used = []
+    for t in order:
+        y0, y1, x0_, x1 = (int(v) for v in R[t, -1, 4:])
+        O.forward_rect(layers, wl.h, wl.w, wl.c, x0, params, y0, y1, x0_, x1)
+        for l, L in enumerate(layers):
+            if L["op"] == "conv":
+                a = int(R[t, l, 5] - R[t, l, 4]) * int(R[t, l, 7] - R[t, l, 6])
+                macs += a * int(dims[l, 5]) * L["f"] ** 2 * int(dims[l, 2])
+        used.append(t)
+        el = time.perf_counter() - t0
+        if el >= min_s or el + el / len(used) > max_s:
+            break
+    el = time.perf_counter() - t0
+    rate = macs / el
+    return {"value": rate / exec_macs_per_frame, "unit": "frames/s", "cores": 1, "kind": "oracle",
+            "sample": (f"{len(used)} output rects of 2x2 px of frame 0, each through its full receptive "
+                       f"field of layers 0-15 ({macs / 1e9:.2f} GMAC in {el:.1f} s, float64, one thread); "
+                       f"frames/s = MAC rate / executed MAC per frame of {wl.tiling}"),
+            "gmac_per_s": rate / 1e9}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="yolo608_5x5_8_2x2")
+    ap.add_argument("--graph", action="store_true", help="replay one step from a captured HIP graph")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-untiled", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
+                                   "(frames shard across GPUs with no exchange, see the design notes)"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    from paper_2107_06960_amd import workloads as W
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    wl = W.WORKLOADS[args.workload]
+    params = W.workload_inputs(wl)
+    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling)
+    net = M.Network(plan, params, wl.batch, wl.dtype)
+    x = net.input_tensor(params["x"])
+    stream = torch.cuda.current_stream()
+
+    step = lambda: net.run(x)  # noqa: E731
+    graph = None
+    if args.graph:
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for _ in range(3):
+                net.run(x, stream=s)
+        torch.cuda.current_stream().wait_stream(s)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            net.run(x, stream=torch.cuda.current_stream())
+        step = graph.replay
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    ms_step = el / args.steps * 1e3
+    fps = wl.batch * args.steps / el
+
+    # Per-stage durations: the same steps again, one run_group call per group
+    # with a HIP event before every stage and after the last, on the stream
+    # the kernels are launched on.
+    ev = HipEvents()
+    ng = plan.n_groups
+    stages = [plan.stages(g) for g in range(ng)]
+    per_step = sum(len(s) + 1 for s in stages)
+    nsteps_ev = min(args.steps, 100)
+    handles = ev.create(per_step * nsteps_ev)
+    torch.cuda.synchronize()
+    k = 0
+    for _ in range(nsteps_ev):
+        for g in range(ng):
+            gin, gout = net.group_io(g, x)
+            n = len(stages[g]) + 1
+            net.run_group(g, gin, gout, stream=stream, events=handles[k:k + n])
+            k += n
+    torch.cuda.synchronize()
+    stage_ms = [[0.0] * len(stages[g]) for g in range(ng)]
+    group_ms = [0.0] * ng
+    k = 0
+    for _ in range(nsteps_ev):
+        for g in range(ng):
+            n = len(stages[g]) + 1
+            hs = handles[k:k + n]
+            for s in range(n - 1):
+                stage_ms[g][s] += ev.ms(hs[s], hs[s + 1]) / nsteps_ev
+            group_ms[g] += ev.ms(hs[0], hs[-1]) / nsteps_ev
+            k += n
+    ev.destroy(handles)
+
+    flops = [stage_flops(plan, g) for g in range(ng)]
+    exec_flops = sum(2 * plan.macs(g)[0] for g in range(ng)) * wl.batch
+    useful_flops = sum(2 * plan.macs(g)[1] for g in range(ng)) * wl.batch
+    peak = PEAK_TFLOPS[wl.dtype]
+    per_stage = []
+    for g in range(ng):
+        for s, (a, b) in enumerate(stages[g]):
+            f = flops[g][s] * wl.batch
+            t = stage_ms[g][s]
+            per_stage.append({"group": g, "layers": [a, b], "ms": round(t, 5),
+                              "gflop": round(f / 1e9, 4),
+                              "tflops": round(f / (t * 1e-3) / 1e12, 2) if t > 0 else None,
+                              "frac_mfma_peak": round(f / (t * 1e-3) / 1e12 / peak, 4) if t > 0 else None})
+    dom = max(per_stage, key=lambda r: r["ms"])
+    dom_f = dom["gflop"] * 1e9
+    roof = {"bound": "mfma", "achieved": round(dom_f / (dom["ms"] * 1e-3) / 1e12, 2), "peak": peak,
+            "unit": "TFLOP/s", "frac": round(dom_f / (dom["ms"] * 1e-3) / 1e12 / peak, 4), "traffic": None,
+            "kernel": f"stage layers {dom['layers'][0]}-{dom['layers'][1]} (group {dom['group']})",
+            "per_launch_gflop": dom["gflop"], "avg_ms": dom["ms"]}
+
+    res = {
+        "metric": METRIC, "value": round(fps, 2), "unit": "frames/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+        "data": "synthetic (seeded U[0,1) input, He-normal weights, folded-BN scale/bias)",
+        "config": {"workload": wl.name, "network": "YOLOv2 layers 0-15" if len(wl.layers) == 16 else wl.note,
+                   "input": f"{wl.h}x{wl.w}x{wl.c}", "batch": wl.batch, "tiling": wl.tiling,
+                   "accumulate": "f32", "graph": bool(args.graph)},
+        "tflops_executed": round(exec_flops / (ms_step * 1e-3) / 1e12, 2),
+        "tflops_useful": round(useful_flops / (ms_step * 1e-3) / 1e12, 2),
+        "frac_mfma_peak_executed": round(exec_flops / (ms_step * 1e-3) / 1e12 / peak, 4),
+        "gflop_executed_per_step": round(exec_flops / 1e9, 3),
+        "gflop_useful_per_step": round(useful_flops / 1e9, 3),
+        "group_ms": [round(v, 5) for v in group_ms],
+        "group_frac_mfma_peak": [round(sum(flops[g]) * wl.batch / (group_ms[g] * 1e-3) / 1e12 / peak, 4)
+                                 for g in range(ng)],
+        "per_stage": per_stage,
+        "roofline": roof,
+    }
+
+    if not args.no_untiled:
+        del net, x
+        tp, tms = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch,
+                                      wl.dtype, params["x"])
+        ug = untiled_groups(wl.layers)
+        up, ums = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), ug, params, wl.batch,
+                                      wl.dtype, params["x"])
+        res["peak_mem_mib"] = round(tp / 2 ** 20, 2)
+        res["untiled_peak_mem_mib"] = round(up / 2 ** 20, 2)
+        res["untiled_ms_per_step"] = round(ums, 5)
+
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl, params, sum(plan.macs(g)[0] for g in range(ng)))
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

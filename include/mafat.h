@@ -1,0 +1,187 @@
+/*
+ * mafat.h -- C ABI of the MI355X (gfx950) fused-tile-partitioning library.
+ *
+ * Method: MAFAT, memory-aware fusing and tiling (Farley & Gerstlauer,
+ * arXiv 2107.06960), built on fused tile partitioning (FTP).  A stack of
+ * convolution and max-pool layers is split into layer groups (section 4:
+ * one group, or groups separated by cuts; group g covers layers
+ * [group_start[g], group_start[g+1])).  Each group has its own output tile
+ * grid (section 4; notation N1xM1/c/N2xM2 of section 5.1).  Every tile's
+ * input region, halo included, is back-projected through the group's layers
+ * (the "Grid"/traversal function of section 4.1); the tile is pushed through
+ * every layer of the group without its intermediates being written out as
+ * full tensors, and the tile outputs are stitched into the group's output
+ * tensor, which the next group re-tiles (section 4).
+ *
+ * Conventions
+ *   - Activations are NHWC, frame-major: element (b, y, x, c) of an
+ *     H x W x C tensor is at ((b*H + y)*W + x)*C + c.
+ *   - Convolution weights are [c_out][f][f][c_in] (KRSC), in the run dtype.
+ *     Per-layer folded batch-norm scale and bias are float32 [c_out].
+ *   - Every convolution computes  v = scale[c] * sum(...) + bias[c], then
+ *     its activation (linear, or leaky ReLU with slope 0.1); padding is zero
+ *     and applies only outside the image, never at a tile border.
+ *   - Rectangles are half-open, in the global coordinates of the tensor they
+ *     index: {y0, y1, x0, x1} covers rows [y0, y1) and columns [x0, x1).
+ *   - dtype MAFAT_F32: float32 activations and weights, float32 accumulate.
+ *     dtype MAFAT_BF16: bfloat16 activations and weights, float32 accumulate;
+ *     every layer output is rounded to bfloat16 (nearest, ties to even).
+ *   - Supported layers: convolution with f in {1, 3}, s = 1, p = (f-1)/2;
+ *     max-pool with f = 2, s = 2, p = 0 (odd extents drop the last row or
+ *     column).  Tensor extents must be at most 32767.
+ *
+ * Ownership and threading
+ *   - A plan is created and destroyed by the library, read-only after
+ *     creation, and may be shared between threads.
+ *   - Every device buffer (input, output, cut tensors, weights, scale, bias,
+ *     workspace) is owned by the caller.  The library never allocates or
+ *     frees device memory and never synchronises a stream; run functions only
+ *     enqueue kernels on the given stream and return.
+ *   - Pointer arrays (w, scale, bias, cut_bufs, events) are host arrays of
+ *     device pointers / event handles, read during the call only.
+ *
+ * Errors
+ *   - Every int-returning function returns a mafat_status.  No C++
+ *     exception crosses this boundary.  mafat_last_error() gives a
+ *     thread-local message about the last failing call.
+ *   - Run functions return MAFAT_EHIP if a launch reports an error; faults
+ *     that happen while kernels execute surface at the caller's next
+ *     synchronisation of the stream.
+ */
+#ifndef MAFAT_H
+#define MAFAT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MAFAT_OK = 0,
+  MAFAT_EINVAL = -1,        /* null pointer, bad index or bad argument value */
+  MAFAT_ESHAPE = -2,        /* layer list / input shape / grid inconsistent   */
+  MAFAT_EUNSUPPORTED = -3,  /* valid request this library does not implement */
+  MAFAT_EWORKSPACE = -4,    /* workspace smaller than mafat_workspace_size    */
+  MAFAT_EHIP = -5,          /* the HIP runtime reported an error              */
+  MAFAT_ENOMEM = -6         /* host allocation failed                         */
+} mafat_status;
+
+typedef enum { MAFAT_CONV = 0, MAFAT_MAXPOOL = 1 } mafat_op;
+typedef enum { MAFAT_ACT_LINEAR = 0, MAFAT_ACT_LEAKY01 = 1 } mafat_act;
+typedef enum { MAFAT_F32 = 0, MAFAT_BF16 = 1 } mafat_dtype;
+
+/* One layer (section 4.1 describes a layer by width, height, filter size
+ * and stride; channels, padding and activation are added).  c_out and act
+ * are ignored for max-pool. */
+typedef struct {
+  int32_t op, c_out, f, s, p, act;
+} mafat_layer;
+
+typedef struct {
+  int32_t y0, y1, x0, x1;
+} mafat_rect;
+
+typedef struct mafat_plan mafat_plan;
+
+/* Builds a plan: shape inference, per-group output tile partition and
+ * per-tile, per-layer region back-projection (sections 4 and 4.1).
+ *   layers[n_layers]          the stack, applied to an in_h x in_w x in_c input
+ *   group_start[n_groups]     first layer of each group; strictly increasing,
+ *                             group_start[0] == 0
+ *   grid_rows/cols[n_groups]  each group's output tile grid; 1 <= rows <= the
+ *                             group output's height (cols: width)
+ * Tile (i, j) of an H x W group output covers rows [floor(iH/rows),
+ * floor((i+1)H/rows)) and columns likewise; tiles are numbered row-major.
+ * On success *out owns the plan (free with mafat_plan_destroy).
+ * Errors: EINVAL (null pointer, n < 1), ESHAPE (non-positive extent, group
+ * or grid out of range, extent > 32767), EUNSUPPORTED (layer kind outside
+ * the supported set). */
+int mafat_plan_create(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
+                      int32_t in_w, int32_t in_c, const int32_t* group_start,
+                      int32_t n_groups, const int32_t* grid_rows,
+                      const int32_t* grid_cols, mafat_plan** out);
+
+/* Frees a plan (NULL is ignored). */
+void mafat_plan_destroy(mafat_plan* plan);
+
+/* dims[6] = in_h, in_w, in_c, out_h, out_w, out_c of layer `layer`.
+ * Errors: EINVAL. */
+int mafat_plan_layer_shape(const mafat_plan* plan, int32_t layer, int32_t dims[6]);
+
+/* Group g's first layer, number of layers and number of tiles.
+ * Any output pointer may be NULL.  Errors: EINVAL. */
+int mafat_plan_group(const mafat_plan* plan, int32_t group, int32_t* first_layer,
+                     int32_t* n_layers, int32_t* n_tiles);
+
+/* Region table of group g, [tile][layer - first_layer] (tiles row-major):
+ * in_rects = the region of the layer's input the tile reads (halo included,
+ * clipped to the tensor); out_rects = the region of the layer's output the
+ * tile computes.  Within a tile, in_rects[k] == out_rects[k-1].  The last
+ * layer's out_rects partition the group output.  capacity is the number of
+ * elements each array can hold (>= n_tiles * n_layers; EINVAL otherwise).
+ * Either array may be NULL. */
+int mafat_plan_regions(const mafat_plan* plan, int32_t group, mafat_rect* in_rects,
+                       mafat_rect* out_rects, int64_t capacity);
+
+/* Multiply-accumulates of group g per frame: executed (every tile's
+ * convolution outputs, halo recompute included, times c_in*f*f) and untiled
+ * (the same layers on whole tensors).  Either pointer may be NULL. */
+int mafat_plan_macs(const mafat_plan* plan, int32_t group, int64_t* executed,
+                    int64_t* untiled);
+
+/* Number of kernel stages group g runs and, for stage s, its first and last
+ * layer (a convolution directly followed by a 2x2 max-pool in the same group
+ * is one stage; every other layer is a stage of its own).  Used for
+ * per-stage timing with the events argument of mafat_run_group. */
+int mafat_plan_stages(const mafat_plan* plan, int32_t group, int32_t* n_stages);
+int mafat_plan_stage_layers(const mafat_plan* plan, int32_t group, int32_t stage,
+                            int32_t* first_layer, int32_t* last_layer);
+
+/* Bytes of device workspace mafat_run_group / mafat_run_network need for
+ * `batch` frames in `dtype` (0 if none).  It holds the tiles' intermediate
+ * activations between stages; the largest group decides.  Errors: EINVAL. */
+int mafat_workspace_size(const mafat_plan* plan, int32_t batch, int32_t dtype,
+                         size_t* bytes);
+
+/* Runs group g on `batch` frames.
+ *   x          device, the group input: batch x H x W x C of the group's first
+ *              layer input (the network input for g = 0, else the previous
+ *              group's output)
+ *   y          device, the group output: batch x H x W x C of its last layer;
+ *              every element is written exactly once
+ *   w, scale, bias  host arrays indexed by global layer number (n_layers
+ *              entries); entries of max-pool layers are ignored
+ *   workspace  device, 256-byte aligned, at least mafat_workspace_size bytes
+ *   stream     hipStream_t (NULL: the default stream)
+ *   events     NULL, or n_stages+1 hipEvent_t: events[s] is recorded on the
+ *              stream right before stage s, events[n_stages] after the last
+ * x and y must not overlap.  Errors: EINVAL, EUNSUPPORTED (dtype),
+ * EWORKSPACE, EHIP. */
+int mafat_run_group(const mafat_plan* plan, int32_t group, int32_t batch, int32_t dtype,
+                    const void* x, void* y, const void* const* w,
+                    const float* const* scale, const float* const* bias,
+                    void* workspace, size_t ws_bytes, void* stream,
+                    void* const* events);
+
+/* Runs every group in order on one stream: group 0 reads x, group g writes
+ * cut_bufs[g] (n_groups-1 caller-owned tensors, each the shape of its group's
+ * output) and group g+1 reads it; the last group writes y.  Same argument
+ * conventions and errors as mafat_run_group. */
+int mafat_run_network(const mafat_plan* plan, int32_t batch, int32_t dtype,
+                      const void* x, void* y, void* const* cut_bufs,
+                      const void* const* w, const float* const* scale,
+                      const float* const* bias, void* workspace, size_t ws_bytes,
+                      void* stream);
+
+/* Static text of a status code. */
+const char* mafat_status_string(int status);
+
+/* Thread-local detail of the last failing call on this thread ("" if none). */
+const char* mafat_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

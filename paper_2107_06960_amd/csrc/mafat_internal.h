@@ -1,0 +1,74 @@
+// mafat_internal.h -- plan structures shared by the planner (plan.cpp), the
+// runtime (run.hip) and the kernels (kernels.hip).  Not part of the ABI.
+#pragma once
+
+#include <array>
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "../../include/mafat.h"
+
+namespace mafat {
+
+// Tiles one kernel launch can describe in its argument block; a stage with
+// more tiles is launched in chunks.
+constexpr int kMaxTilesPerLaunch = 64;
+
+// Largest tensor extent the 16-bit tile descriptors can address.
+constexpr int kMaxExtent = 32767;
+
+enum StageKind { STAGE_CONV = 0, STAGE_POOL = 1 };
+
+// Where a stage reads from / writes to.
+enum BufKind { BUF_GROUP_IO = -1, BUF_SCRATCH0 = 0, BUF_SCRATCH1 = 1 };
+
+// Geometry of one tile in one stage, all in global coordinates.
+struct TileGeom {
+  // The rectangle the stage's kernel computes: for a conv stage the conv
+  // output rectangle (before any fused pool), for a pool stage the pool
+  // output rectangle.
+  int cy0, cx0, ch, cw;
+  // Source buffer: the element (y, x, c) of the stage input lives at
+  // src_off + ((y - sy0) * sw + (x - sx0)) * C + c of one frame's buffer.
+  int sy0, sx0, sw;
+  // Destination buffer, the same way for the stage output.
+  int dy0, dx0, dw;
+  int64_t src_off, dst_off;
+};
+
+struct Stage {
+  int kind;          // StageKind
+  int first, last;   // layers [first, last]
+  bool pool;         // conv stage with a fused 2x2/2 max-pool
+  int in_h, in_w, cin;     // input tensor of the first layer
+  int out_h, out_w, cout;  // output tensor of the last layer
+  int f, p, act;           // conv parameters (conv stages)
+  int src_buf, dst_buf;    // BufKind
+  std::vector<TileGeom> tiles;
+};
+
+struct Group {
+  int l0, l1;        // layers [l0, l1]
+  int rows, cols, ntiles;
+  std::vector<mafat_rect> in_r, out_r;  // [tile * nlayers + (l - l0)]
+  std::vector<Stage> stages;
+  int64_t scratch_elems;  // per tile per scratch buffer
+  int nbufs;              // scratch buffers (0, 1 or 2)
+  int64_t macs_exec, macs_untiled;
+};
+
+}  // namespace mafat
+
+struct mafat_plan {
+  int n, in_h, in_w, in_c;
+  std::vector<mafat_layer> layers;
+  std::vector<std::array<int, 6>> dims;  // in_h, in_w, in_c, out_h, out_w, out_c
+  std::vector<mafat::Group> groups;
+};
+
+namespace mafat {
+// Thread-local error detail (mafat_last_error).
+void set_error(const std::string& msg);
+void clear_error();
+}  // namespace mafat

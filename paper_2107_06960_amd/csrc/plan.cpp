@@ -1,0 +1,320 @@
+// plan.cpp -- host-side planning for fused tile partitioning (MAFAT,
+// arXiv 2107.06960): shape inference, per-group output tile partition,
+// per-tile region back-projection, stage decomposition for the kernels,
+// workspace sizing and multiply-accumulate accounting.  Pure integer host
+// code; no HIP calls.
+#include <algorithm>
+#include <cstring>
+#include <new>
+
+#include "mafat_internal.h"
+
+namespace mafat {
+
+static thread_local std::string g_last_error;
+void set_error(const std::string& msg) { g_last_error = msg; }
+void clear_error() { g_last_error.clear(); }
+
+namespace {
+
+bool layer_supported(const mafat_layer& L, std::string* why) {
+  if (L.op == MAFAT_CONV) {
+    if (L.f != 1 && L.f != 3) { *why = "convolution filter must be 1 or 3"; return false; }
+    if (L.s != 1) { *why = "convolution stride must be 1"; return false; }
+    if (L.p != (L.f - 1) / 2) { *why = "convolution padding must be (f-1)/2"; return false; }
+    if (L.c_out < 1) { *why = "convolution c_out must be positive"; return false; }
+    if (L.act != MAFAT_ACT_LINEAR && L.act != MAFAT_ACT_LEAKY01) { *why = "unknown activation"; return false; }
+    return true;
+  }
+  if (L.op == MAFAT_MAXPOOL) {
+    if (L.f != 2 || L.s != 2 || L.p != 0) { *why = "max-pool must be 2x2, stride 2, no padding"; return false; }
+    return true;
+  }
+  *why = "unknown layer op";
+  return false;
+}
+
+// Tile i of N over the extent [0, E): [floor(iE/N), floor((i+1)E/N)).
+void split(int E, int N, int i, int* a, int* b) {
+  *a = static_cast<int>((static_cast<int64_t>(i) * E) / N);
+  *b = static_cast<int>((static_cast<int64_t>(i + 1) * E) / N);
+}
+
+// The input interval [ia, ib) that outputs [a, b) of a layer with filter F,
+// stride S and padding P read, clipped to the input extent [0, E).
+void back_project(int a, int b, int F, int S, int P, int E, int* ia, int* ib) {
+  *ia = std::max(0, a * S - P);
+  *ib = std::min(E, (b - 1) * S - P + F);
+}
+
+int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, Group* out) {
+  Group G;
+  G.l0 = g0; G.l1 = g1; G.rows = rows; G.cols = cols; G.ntiles = rows * cols;
+  const int nl = g1 - g0 + 1;
+  const auto& dl = plan.dims[g1];
+  if (rows < 1 || cols < 1 || rows > dl[3] || cols > dl[4]) {
+    set_error("grid " + std::to_string(rows) + "x" + std::to_string(cols) +
+              " does not fit the group output " + std::to_string(dl[3]) + "x" + std::to_string(dl[4]));
+    return MAFAT_ESHAPE;
+  }
+  G.in_r.resize(static_cast<size_t>(G.ntiles) * nl);
+  G.out_r.resize(static_cast<size_t>(G.ntiles) * nl);
+  for (int i = 0; i < rows; ++i)
+    for (int j = 0; j < cols; ++j) {
+      const int t = i * cols + j;
+      mafat_rect o;
+      split(dl[3], rows, i, &o.y0, &o.y1);
+      split(dl[4], cols, j, &o.x0, &o.x1);
+      for (int l = g1; l >= g0; --l) {
+        const mafat_layer& L = plan.layers[l];
+        const auto& d = plan.dims[l];
+        mafat_rect in;
+        back_project(o.y0, o.y1, L.f, L.s, L.p, d[0], &in.y0, &in.y1);
+        back_project(o.x0, o.x1, L.f, L.s, L.p, d[1], &in.x0, &in.x1);
+        G.out_r[static_cast<size_t>(t) * nl + (l - g0)] = o;
+        G.in_r[static_cast<size_t>(t) * nl + (l - g0)] = in;
+        o = in;
+      }
+    }
+
+  // Multiply-accumulates per frame.
+  G.macs_exec = G.macs_untiled = 0;
+  for (int l = g0; l <= g1; ++l) {
+    const mafat_layer& L = plan.layers[l];
+    if (L.op != MAFAT_CONV) continue;
+    const auto& d = plan.dims[l];
+    const int64_t per_px = static_cast<int64_t>(d[5]) * L.f * L.f * d[2];
+    G.macs_untiled += static_cast<int64_t>(d[3]) * d[4] * per_px;
+    for (int t = 0; t < G.ntiles; ++t) {
+      const mafat_rect& r = G.out_r[static_cast<size_t>(t) * nl + (l - g0)];
+      G.macs_exec += static_cast<int64_t>(r.y1 - r.y0) * (r.x1 - r.x0) * per_px;
+    }
+  }
+
+  // Stages: a convolution directly followed (inside the group) by a 2x2/2
+  // max-pool is one stage with the pool fused into its epilogue.
+  for (int l = g0; l <= g1;) {
+    Stage S{};
+    const mafat_layer& L = plan.layers[l];
+    S.first = l;
+    if (L.op == MAFAT_CONV) {
+      S.kind = STAGE_CONV;
+      S.pool = (l + 1 <= g1 && plan.layers[l + 1].op == MAFAT_MAXPOOL);
+      S.last = S.pool ? l + 1 : l;
+      S.f = L.f; S.p = L.p; S.act = L.act;
+    } else {
+      S.kind = STAGE_POOL;
+      S.pool = false;
+      S.last = l;
+      S.f = L.f; S.p = 0; S.act = MAFAT_ACT_LINEAR;
+    }
+    const auto& din = plan.dims[S.first];
+    const auto& dout = plan.dims[S.last];
+    S.in_h = din[0]; S.in_w = din[1]; S.cin = din[2];
+    S.out_h = dout[3]; S.out_w = dout[4]; S.cout = dout[5];
+    G.stages.push_back(S);
+    l = S.last + 1;
+  }
+  const int ns = static_cast<int>(G.stages.size());
+  G.nbufs = std::min(2, ns - 1);
+  G.scratch_elems = 0;
+  for (int s = 0; s < ns; ++s) {
+    Stage& S = G.stages[s];
+    S.src_buf = (s == 0) ? BUF_GROUP_IO : ((s - 1) % 2);
+    S.dst_buf = (s == ns - 1) ? BUF_GROUP_IO : (s % 2);
+    for (int t = 0; t < G.ntiles; ++t) {
+      const mafat_rect& cr = G.out_r[static_cast<size_t>(t) * nl + (S.first - g0)];  // computed rect
+      const mafat_rect& sr = G.in_r[static_cast<size_t>(t) * nl + (S.first - g0)];   // read rect
+      const mafat_rect& orr = G.out_r[static_cast<size_t>(t) * nl + (S.last - g0)];  // written rect
+      TileGeom T{};
+      if (S.kind == STAGE_CONV) {
+        T.cy0 = cr.y0; T.cx0 = cr.x0; T.ch = cr.y1 - cr.y0; T.cw = cr.x1 - cr.x0;
+      } else {
+        T.cy0 = orr.y0; T.cx0 = orr.x0; T.ch = orr.y1 - orr.y0; T.cw = orr.x1 - orr.x0;
+      }
+      if (S.src_buf == BUF_GROUP_IO) {
+        T.sy0 = 0; T.sx0 = 0; T.sw = S.in_w; T.src_off = 0;
+      } else {
+        T.sy0 = sr.y0; T.sx0 = sr.x0; T.sw = sr.x1 - sr.x0;
+        T.src_off = (static_cast<int64_t>(S.src_buf) * G.ntiles + t);  // scaled below
+      }
+      if (S.dst_buf == BUF_GROUP_IO) {
+        T.dy0 = 0; T.dx0 = 0; T.dw = S.out_w; T.dst_off = 0;
+      } else {
+        T.dy0 = orr.y0; T.dx0 = orr.x0; T.dw = orr.x1 - orr.x0;
+        T.dst_off = (static_cast<int64_t>(S.dst_buf) * G.ntiles + t);  // scaled below
+        G.scratch_elems = std::max<int64_t>(
+            G.scratch_elems, static_cast<int64_t>(orr.y1 - orr.y0) * (orr.x1 - orr.x0) * S.cout);
+      }
+      S.tiles.push_back(T);
+    }
+  }
+  // Scratch buffers of one frame: [buffer][tile][scratch_elems]; every
+  // tile's buffer starts on a 256-byte boundary for both dtypes.
+  G.scratch_elems = (G.scratch_elems + 127) / 128 * 128;
+  for (Stage& S : G.stages)
+    for (TileGeom& T : S.tiles) {
+      if (S.src_buf != BUF_GROUP_IO) T.src_off *= G.scratch_elems;
+      if (S.dst_buf != BUF_GROUP_IO) T.dst_off *= G.scratch_elems;
+    }
+  *out = std::move(G);
+  return MAFAT_OK;
+}
+
+}  // namespace
+}  // namespace mafat
+
+using namespace mafat;
+
+extern "C" int mafat_plan_create(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
+                                 int32_t in_w, int32_t in_c, const int32_t* group_start,
+                                 int32_t n_groups, const int32_t* grid_rows,
+                                 const int32_t* grid_cols, mafat_plan** out) {
+  clear_error();
+  if (!out) { set_error("out is NULL"); return MAFAT_EINVAL; }
+  *out = nullptr;
+  if (!layers || !group_start || !grid_rows || !grid_cols || n_layers < 1 || n_groups < 1) {
+    set_error("null pointer or empty layer/group list");
+    return MAFAT_EINVAL;
+  }
+  if (in_h < 1 || in_w < 1 || in_c < 1 || in_h > kMaxExtent || in_w > kMaxExtent) {
+    set_error("input extent out of range");
+    return MAFAT_ESHAPE;
+  }
+  mafat_plan* plan = new (std::nothrow) mafat_plan();
+  if (!plan) return MAFAT_ENOMEM;
+  try {
+    plan->n = n_layers; plan->in_h = in_h; plan->in_w = in_w; plan->in_c = in_c;
+    plan->layers.assign(layers, layers + n_layers);
+    int h = in_h, w = in_w, c = in_c;
+    for (int l = 0; l < n_layers; ++l) {
+      const mafat_layer& L = layers[l];
+      std::string why;
+      if (!layer_supported(L, &why)) {
+        set_error("layer " + std::to_string(l) + ": " + why);
+        delete plan;
+        return (L.op == MAFAT_CONV || L.op == MAFAT_MAXPOOL) ? MAFAT_EUNSUPPORTED : MAFAT_EINVAL;
+      }
+      const int oh_num = h + 2 * L.p - L.f, ow_num = w + 2 * L.p - L.f;
+      if (oh_num < 0 || ow_num < 0) {
+        set_error("layer " + std::to_string(l) + ": input smaller than the filter");
+        delete plan;
+        return MAFAT_ESHAPE;
+      }
+      const int oh = oh_num / L.s + 1, ow = ow_num / L.s + 1;
+      const int oc = (L.op == MAFAT_CONV) ? L.c_out : c;
+      plan->dims.push_back({h, w, c, oh, ow, oc});
+      h = oh; w = ow; c = oc;
+    }
+    if (group_start[0] != 0) {
+      set_error("group_start[0] must be 0");
+      delete plan;
+      return MAFAT_ESHAPE;
+    }
+    for (int g = 0; g < n_groups; ++g) {
+      const int g0 = group_start[g];
+      const int end = (g + 1 < n_groups) ? group_start[g + 1] : n_layers;
+      if (g0 < 0 || end <= g0 || end > n_layers) {
+        set_error("group starts must be strictly increasing and below n_layers");
+        delete plan;
+        return MAFAT_ESHAPE;
+      }
+      Group G;
+      const int rc = build_group(*plan, g0, end - 1, grid_rows[g], grid_cols[g], &G);
+      if (rc != MAFAT_OK) { delete plan; return rc; }
+      plan->groups.push_back(std::move(G));
+    }
+  } catch (const std::bad_alloc&) {
+    delete plan;
+    set_error("host allocation failed");
+    return MAFAT_ENOMEM;
+  }
+  *out = plan;
+  return MAFAT_OK;
+}
+
+extern "C" void mafat_plan_destroy(mafat_plan* plan) { delete plan; }
+
+extern "C" int mafat_plan_layer_shape(const mafat_plan* plan, int32_t layer, int32_t dims[6]) {
+  if (!plan || !dims || layer < 0 || layer >= plan->n) return MAFAT_EINVAL;
+  for (int k = 0; k < 6; ++k) dims[k] = plan->dims[layer][k];
+  return MAFAT_OK;
+}
+
+extern "C" int mafat_plan_group(const mafat_plan* plan, int32_t group, int32_t* first_layer,
+                                int32_t* n_layers, int32_t* n_tiles) {
+  if (!plan || group < 0 || group >= static_cast<int>(plan->groups.size())) return MAFAT_EINVAL;
+  const Group& G = plan->groups[group];
+  if (first_layer) *first_layer = G.l0;
+  if (n_layers) *n_layers = G.l1 - G.l0 + 1;
+  if (n_tiles) *n_tiles = G.ntiles;
+  return MAFAT_OK;
+}
+
+extern "C" int mafat_plan_regions(const mafat_plan* plan, int32_t group, mafat_rect* in_rects,
+                                  mafat_rect* out_rects, int64_t capacity) {
+  if (!plan || group < 0 || group >= static_cast<int>(plan->groups.size())) return MAFAT_EINVAL;
+  const Group& G = plan->groups[group];
+  const int64_t need = static_cast<int64_t>(G.in_r.size());
+  if (capacity < need) {
+    set_error("region capacity " + std::to_string(capacity) + " < " + std::to_string(need));
+    return MAFAT_EINVAL;
+  }
+  if (in_rects) std::memcpy(in_rects, G.in_r.data(), sizeof(mafat_rect) * need);
+  if (out_rects) std::memcpy(out_rects, G.out_r.data(), sizeof(mafat_rect) * need);
+  return MAFAT_OK;
+}
+
+extern "C" int mafat_plan_macs(const mafat_plan* plan, int32_t group, int64_t* executed,
+                               int64_t* untiled) {
+  if (!plan || group < 0 || group >= static_cast<int>(plan->groups.size())) return MAFAT_EINVAL;
+  if (executed) *executed = plan->groups[group].macs_exec;
+  if (untiled) *untiled = plan->groups[group].macs_untiled;
+  return MAFAT_OK;
+}
+
+extern "C" int mafat_plan_stages(const mafat_plan* plan, int32_t group, int32_t* n_stages) {
+  if (!plan || !n_stages || group < 0 || group >= static_cast<int>(plan->groups.size()))
+    return MAFAT_EINVAL;
+  *n_stages = static_cast<int32_t>(plan->groups[group].stages.size());
+  return MAFAT_OK;
+}
+
+extern "C" int mafat_plan_stage_layers(const mafat_plan* plan, int32_t group, int32_t stage,
+                                       int32_t* first_layer, int32_t* last_layer) {
+  if (!plan || group < 0 || group >= static_cast<int>(plan->groups.size())) return MAFAT_EINVAL;
+  const Group& G = plan->groups[group];
+  if (stage < 0 || stage >= static_cast<int>(G.stages.size())) return MAFAT_EINVAL;
+  if (first_layer) *first_layer = G.stages[stage].first;
+  if (last_layer) *last_layer = G.stages[stage].last;
+  return MAFAT_OK;
+}
+
+extern "C" int mafat_workspace_size(const mafat_plan* plan, int32_t batch, int32_t dtype,
+                                    size_t* bytes) {
+  if (!plan || !bytes || batch < 1) return MAFAT_EINVAL;
+  if (dtype != MAFAT_F32 && dtype != MAFAT_BF16) return MAFAT_EUNSUPPORTED;
+  const size_t esz = (dtype == MAFAT_F32) ? 4 : 2;
+  size_t best = 0;
+  for (const Group& G : plan->groups) {
+    const size_t b = static_cast<size_t>(batch) * G.nbufs * G.ntiles * G.scratch_elems * esz;
+    best = std::max(best, b);
+  }
+  *bytes = (best + 255) & ~static_cast<size_t>(255);
+  return MAFAT_OK;
+}
+
+extern "C" const char* mafat_status_string(int status) {
+  switch (status) {
+    case MAFAT_OK: return "ok";
+    case MAFAT_EINVAL: return "invalid argument";
+    case MAFAT_ESHAPE: return "inconsistent shape, group or grid";
+    case MAFAT_EUNSUPPORTED: return "unsupported layer or dtype";
+    case MAFAT_EWORKSPACE: return "workspace too small";
+    case MAFAT_EHIP: return "HIP runtime error";
+    case MAFAT_ENOMEM: return "host allocation failed";
+    default: return "unknown status";
+  }
+}
+
+extern "C" const char* mafat_last_error(void) { return g_last_error.c_str(); }

@@ -1,0 +1,296 @@
+"""Thin ctypes binding of libmafat.so (the C ABI declared in include/mafat.h).
+
+Functions keep the C names (``mafat_plan_create``, ``mafat_run_group``,
+``mafat_run_network``, ...) and only marshal arguments: every step of the
+computation runs in the library's HIP kernels.  PyTorch is used only to own
+device memory and to supply the stream.  There is no fallback: if the
+library is missing, loading raises.
+
+``Plan`` wraps a plan handle; ``Network`` holds device copies of the
+parameters and runs the whole stack.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import workloads as W
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmafat.so")
+
+MAFAT_OK, MAFAT_EINVAL, MAFAT_ESHAPE, MAFAT_EUNSUPPORTED = 0, -1, -2, -3
+MAFAT_EWORKSPACE, MAFAT_EHIP, MAFAT_ENOMEM = -4, -5, -6
+MAFAT_CONV, MAFAT_MAXPOOL = 0, 1
+MAFAT_ACT_LINEAR, MAFAT_ACT_LEAKY01 = 0, 1
+MAFAT_F32, MAFAT_BF16 = 0, 1
+DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
+
+# Every symbol include/mafat.h declares.
+EXPORTS = ("mafat_plan_create", "mafat_plan_destroy", "mafat_plan_layer_shape", "mafat_plan_group",
+           "mafat_plan_regions", "mafat_plan_macs", "mafat_plan_stages", "mafat_plan_stage_layers",
+           "mafat_workspace_size", "mafat_run_group", "mafat_run_network", "mafat_status_string",
+           "mafat_last_error")
+
+
+class mafat_layer(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_int32) for k in ("op", "c_out", "f", "s", "p", "act")]
+
+
+class mafat_rect(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_int32) for k in ("y0", "y1", "x0", "x1")]
+
+
+class MafatError(RuntimeError):
+    def __init__(self, fn, rc, detail):
+        super().__init__(f"{fn} failed: {rc} ({_status(rc)}): {detail}")
+        self.rc = rc
+
+
+_lib = None
+
+
+def lib():
+    """Loads libmafat.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: run `python -m paper_2107_06960_amd.build`")
+        # torch ships its own HIP runtime under the same soname; importing it
+        # first makes libmafat bind to that one instead of loading a second
+        # runtime from /opt/rocm.
+        import torch  # noqa: F401
+        L = ctypes.CDLL(LIB_PATH)
+        i32, i64, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+        vp, vpp = ctypes.c_void_p, ctypes.POINTER(ctypes.c_void_p)
+        i32p = ctypes.POINTER(i32)
+        planp = ctypes.c_void_p
+        L.mafat_plan_create.argtypes = [ctypes.POINTER(mafat_layer), i32, i32, i32, i32, i32p, i32,
+                                        i32p, i32p, ctypes.POINTER(planp)]
+        L.mafat_plan_destroy.argtypes = [planp]
+        L.mafat_plan_destroy.restype = None
+        L.mafat_plan_layer_shape.argtypes = [planp, i32, i32p]
+        L.mafat_plan_group.argtypes = [planp, i32, i32p, i32p, i32p]
+        L.mafat_plan_regions.argtypes = [planp, i32, ctypes.POINTER(mafat_rect),
+                                         ctypes.POINTER(mafat_rect), i64]
+        L.mafat_plan_macs.argtypes = [planp, i32, ctypes.POINTER(i64), ctypes.POINTER(i64)]
+        L.mafat_plan_stages.argtypes = [planp, i32, i32p]
+        L.mafat_plan_stage_layers.argtypes = [planp, i32, i32, i32p, i32p]
+        L.mafat_workspace_size.argtypes = [planp, i32, i32, ctypes.POINTER(sz)]
+        L.mafat_run_group.argtypes = [planp, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp, vpp]
+        L.mafat_run_network.argtypes = [planp, i32, i32, vp, vp, vpp, vpp, vpp, vpp, vp, sz, vp]
+        L.mafat_status_string.argtypes = [ctypes.c_int]
+        L.mafat_status_string.restype = ctypes.c_char_p
+        L.mafat_last_error.argtypes = []
+        L.mafat_last_error.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _status(rc):
+    return lib().mafat_status_string(rc).decode()
+
+
+def _check(fn, rc):
+    if rc != MAFAT_OK:
+        raise MafatError(fn, rc, lib().mafat_last_error().decode())
+
+
+def _ptrs(vals):
+    arr = (ctypes.c_void_p * max(1, len(vals)))()
+    for k, v in enumerate(vals):
+        arr[k] = v
+    return arr
+
+
+# ------------------------------------------------------------------ C names
+
+def mafat_plan_create(layers, in_h, in_w, in_c, group_start, grid_rows, grid_cols):
+    """Returns a plan handle (int); raises MafatError with the library's status."""
+    n = len(layers)
+    arr = (mafat_layer * n)()
+    for k, L in enumerate(layers):
+        op = MAFAT_CONV if L["op"] == W.CONV else MAFAT_MAXPOOL
+        act = MAFAT_ACT_LEAKY01 if L.get("act") == W.LEAKY else MAFAT_ACT_LINEAR
+        arr[k] = mafat_layer(op, int(L.get("c_out", 0)), int(L["f"]), int(L["s"]), int(L["p"]), act)
+    gs = (ctypes.c_int32 * len(group_start))(*group_start)
+    rr = (ctypes.c_int32 * len(grid_rows))(*grid_rows)
+    cc = (ctypes.c_int32 * len(grid_cols))(*grid_cols)
+    h = ctypes.c_void_p()
+    _check("mafat_plan_create",
+           lib().mafat_plan_create(arr, n, in_h, in_w, in_c, gs, len(group_start), rr, cc, ctypes.byref(h)))
+    return h.value
+
+
+def mafat_plan_destroy(plan):
+    lib().mafat_plan_destroy(plan)
+
+
+def mafat_plan_layer_shape(plan, layer):
+    d = (ctypes.c_int32 * 6)()
+    _check("mafat_plan_layer_shape", lib().mafat_plan_layer_shape(plan, layer, d))
+    return tuple(d)
+
+
+def mafat_plan_group(plan, group):
+    a, b, c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    _check("mafat_plan_group", lib().mafat_plan_group(plan, group, ctypes.byref(a), ctypes.byref(b),
+                                                      ctypes.byref(c)))
+    return a.value, b.value, c.value
+
+
+def mafat_plan_regions(plan, group):
+    """int32 array (tiles, layers_in_group, 8): in y0,y1,x0,x1 then out y0,y1,x0,x1."""
+    _, nl, nt = mafat_plan_group(plan, group)
+    ins, outs = (mafat_rect * (nl * nt))(), (mafat_rect * (nl * nt))()
+    _check("mafat_plan_regions", lib().mafat_plan_regions(plan, group, ins, outs, nl * nt))
+    a = np.ctypeslib.as_array(ctypes.cast(ins, ctypes.POINTER(ctypes.c_int32)), (nl * nt * 4,))
+    b = np.ctypeslib.as_array(ctypes.cast(outs, ctypes.POINTER(ctypes.c_int32)), (nl * nt * 4,))
+    return np.concatenate([a.reshape(nt, nl, 4), b.reshape(nt, nl, 4)], axis=2).copy()
+
+
+def mafat_plan_macs(plan, group):
+    e, u = ctypes.c_int64(), ctypes.c_int64()
+    _check("mafat_plan_macs", lib().mafat_plan_macs(plan, group, ctypes.byref(e), ctypes.byref(u)))
+    return e.value, u.value
+
+
+def mafat_plan_stages(plan, group):
+    n = ctypes.c_int32()
+    _check("mafat_plan_stages", lib().mafat_plan_stages(plan, group, ctypes.byref(n)))
+    out = []
+    for s in range(n.value):
+        a, b = ctypes.c_int32(), ctypes.c_int32()
+        _check("mafat_plan_stage_layers", lib().mafat_plan_stage_layers(plan, group, s, ctypes.byref(a),
+                                                                        ctypes.byref(b)))
+        out.append((a.value, b.value))
+    return out
+
+
+def mafat_workspace_size(plan, batch, dtype):
+    n = ctypes.c_size_t()
+    _check("mafat_workspace_size", lib().mafat_workspace_size(plan, batch, dtype, ctypes.byref(n)))
+    return n.value
+
+
+def mafat_run_group(plan, group, batch, dtype, x, y, w, scale, bias, workspace, ws_bytes, stream,
+                    events=None):
+    """x, y, workspace: device pointers (int); w/scale/bias: lists of device
+    pointers indexed by layer (None for pools); stream: hipStream_t (int);
+    events: None or a list of n_stages+1 hipEvent_t handles."""
+    ev = _ptrs(events) if events is not None else None
+    _check("mafat_run_group",
+           lib().mafat_run_group(plan, group, batch, dtype, x, y, _ptrs(w), _ptrs(scale), _ptrs(bias),
+                                 workspace, ws_bytes, stream, ev))
+
+
+def mafat_run_network(plan, batch, dtype, x, y, cut_bufs, w, scale, bias, workspace, ws_bytes, stream):
+    _check("mafat_run_network",
+           lib().mafat_run_network(plan, batch, dtype, x, y, _ptrs(cut_bufs), _ptrs(w), _ptrs(scale),
+                                   _ptrs(bias), workspace, ws_bytes, stream))
+
+
+# ------------------------------------------------------------------ convenience
+
+class Plan:
+    """A plan for a layer stack, an input shape and a tiling spec such as
+    ``"5x5/8/2x2"`` (section 5.1 notation) or explicit group lists."""
+
+    def __init__(self, layers, in_hwc, tiling="1x1/NoCut"):
+        self.layers = list(layers)
+        self.h, self.w, self.c = in_hwc
+        self.group_start, self.rows, self.cols = W.parse_tiling(tiling, len(layers)) \
+            if isinstance(tiling, str) else tiling
+        self.handle = mafat_plan_create(self.layers, self.h, self.w, self.c, self.group_start,
+                                        self.rows, self.cols)
+        self.n_groups = len(self.group_start)
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h:
+            try:
+                mafat_plan_destroy(h)
+            except Exception:
+                pass
+            self.handle = None
+
+    def shape(self, layer):
+        return mafat_plan_layer_shape(self.handle, layer)
+
+    def group(self, g):
+        return mafat_plan_group(self.handle, g)
+
+    def regions(self, g):
+        return mafat_plan_regions(self.handle, g)
+
+    def macs(self, g):
+        return mafat_plan_macs(self.handle, g)
+
+    def stages(self, g):
+        return mafat_plan_stages(self.handle, g)
+
+    def workspace_size(self, batch, dtype):
+        return mafat_workspace_size(self.handle, batch, DTYPES.get(dtype, dtype))
+
+    def group_out_shape(self, g):
+        first, nl, _ = self.group(g)
+        d = self.shape(first + nl - 1)
+        return d[3], d[4], d[5]
+
+
+def _stream_handle(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+class Network:
+    """Device-resident parameters for a plan, plus output / cut / workspace
+    buffers, all allocated by torch.  run() enqueues mafat_run_network."""
+
+    def __init__(self, plan: Plan, params, batch: int, dtype: str, device="cuda"):
+        import torch
+        self.plan, self.batch, self.dtype = plan, batch, dtype
+        self.code = DTYPES[dtype]
+        tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+        self.tdtype = tdt
+        self.w, self.scale, self.bias = [], [], []
+        for k, L in enumerate(plan.layers):
+            if L["op"] != W.CONV:
+                self.w.append(None); self.scale.append(None); self.bias.append(None)
+                continue
+            self.w.append(torch.from_numpy(np.ascontiguousarray(params["w"][k])).to(device=device, dtype=tdt))
+            self.scale.append(torch.from_numpy(np.ascontiguousarray(params["scale"][k])).to(device))
+            self.bias.append(torch.from_numpy(np.ascontiguousarray(params["bias"][k])).to(device))
+        self.cuts = [torch.empty((batch,) + plan.group_out_shape(g), dtype=tdt, device=device)
+                     for g in range(plan.n_groups - 1)]
+        self.y = torch.empty((batch,) + plan.group_out_shape(plan.n_groups - 1), dtype=tdt, device=device)
+        self.ws_bytes = plan.workspace_size(batch, dtype)
+        self.ws = torch.empty(max(self.ws_bytes, 256), dtype=torch.uint8, device=device)
+        self._wp = [None if t is None else t.data_ptr() for t in self.w]
+        self._sp = [None if t is None else t.data_ptr() for t in self.scale]
+        self._bp = [None if t is None else t.data_ptr() for t in self.bias]
+
+    def input_tensor(self, x_np, device="cuda"):
+        import torch
+        return torch.from_numpy(np.ascontiguousarray(x_np)).to(device=device, dtype=self.tdtype)
+
+    def run(self, x, stream=None):
+        assert x.dtype == self.tdtype and x.is_contiguous()
+        assert tuple(x.shape) == (self.batch, self.plan.h, self.plan.w, self.plan.c)
+        mafat_run_network(self.plan.handle, self.batch, self.code, x.data_ptr(), self.y.data_ptr(),
+                          [c.data_ptr() for c in self.cuts], self._wp, self._sp, self._bp,
+                          self.ws.data_ptr(), self.ws_bytes, _stream_handle(stream))
+        return self.y
+
+    def run_group(self, g, x, y, stream=None, events=None):
+        mafat_run_group(self.plan.handle, g, self.batch, self.code, x.data_ptr(), y.data_ptr(),
+                        self._wp, self._sp, self._bp, self.ws.data_ptr(), self.ws_bytes,
+                        _stream_handle(stream), events)
+
+    def group_io(self, g, x):
+        gin = x if g == 0 else self.cuts[g - 1]
+        gout = self.y if g == self.plan.n_groups - 1 else self.cuts[g]
+        return gin, gout

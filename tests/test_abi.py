@@ -1,0 +1,184 @@
+"""CPU tests of the C ABI: the library loads without a GPU, exports every
+symbol the header declares, its plan (host code) matches the oracle's regions
+bit for bit, and invalid requests return the documented status codes
+(all checked before any HIP call)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2107_06960_amd import mafat as M
+from paper_2107_06960_amd import workloads as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(M.LIB_PATH):
+        from paper_2107_06960_amd import build
+        build.build(verbose=False)
+    return M.lib()
+
+
+def test_exports_every_declared_symbol(lib):
+    hdr = open(os.path.join(ROOT, "include", "mafat.h")).read()
+    declared = set(re.findall(r"\b(mafat_[a-z_]+)\s*\(", hdr))
+    assert declared == set(M.EXPORTS)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def _oracle_macs(orc, layers, h, w, c, gs, rows, cols):
+    dims = orc.shapes(layers, h, w, c)
+    out = []
+    for g, R in enumerate(orc.regions(layers, h, w, c, gs, rows, cols)):
+        ex = un = 0
+        for k in range(R.shape[1]):
+            l = gs[g] + k
+            L = layers[l]
+            if L["op"] != W.CONV:
+                continue
+            per = int(dims[l, 5]) * L["f"] ** 2 * int(dims[l, 2])
+            un += int(dims[l, 3]) * int(dims[l, 4]) * per
+            for t in range(R.shape[0]):
+                oy0, oy1, ox0, ox1 = R[t, k, 4:]
+                ex += int(oy1 - oy0) * int(ox1 - ox0) * per
+        out.append((ex, un))
+    return out
+
+
+@pytest.mark.parametrize("name", sorted(W.WORKLOADS))
+def test_plan_regions_and_macs_match_oracle(lib, orc, name):
+    wl = W.WORKLOADS[name]
+    gs, r, c = wl.groups()
+    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling)
+    R = orc.regions(wl.layers, wl.h, wl.w, wl.c, gs, r, c)
+    macs = _oracle_macs(orc, wl.layers, wl.h, wl.w, wl.c, gs, r, c)
+    for g in range(len(gs)):
+        assert np.array_equal(plan.regions(g), R[g])
+        assert plan.macs(g) == macs[g]
+    dims = orc.shapes(wl.layers, wl.h, wl.w, wl.c)
+    for l in range(len(wl.layers)):
+        assert plan.shape(l) == tuple(dims[l])
+
+
+def _random_supported(rng):
+    layers, c = [], int(rng.integers(1, 40))
+    for _ in range(int(rng.integers(1, 7))):
+        if rng.random() < 0.35:
+            layers.append(W.maxpool())
+        else:
+            layers.append(W.conv(int(rng.integers(1, 70)), int(rng.choice([1, 3]))))
+    return layers, c
+
+
+def test_plan_regions_random_match_bruteforce(lib, orc):
+    rng = np.random.default_rng(99)
+    done = 0
+    while done < 150:
+        layers, c = _random_supported(rng)
+        h, w = int(rng.integers(2, 70)), int(rng.integers(2, 70))
+        try:
+            dims = orc.shapes(layers, h, w, c)
+        except orc.OracleError:
+            continue
+        n = len(layers)
+        ng = int(rng.integers(1, min(3, n) + 1))
+        gs = [0] + sorted(int(v) for v in rng.choice(np.arange(1, n), ng - 1, replace=False)) if ng > 1 else [0]
+        rows, cols = [], []
+        for g in range(ng):
+            last = (gs[g + 1] if g + 1 < ng else n) - 1
+            rows.append(int(rng.integers(1, min(6, dims[last, 3]) + 1)))
+            cols.append(int(rng.integers(1, min(6, dims[last, 4]) + 1)))
+        plan = M.Plan(layers, (h, w, c), (gs, rows, cols))
+        B = orc.regions_bruteforce(layers, h, w, c, gs, rows, cols)
+        for g in range(ng):
+            assert np.array_equal(plan.regions(g), B[g]), (layers, h, w, c, gs, rows, cols)
+        done += 1
+
+
+def test_stages_fuse_conv_and_following_pool(lib):
+    plan = M.Plan(W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2")
+    assert plan.stages(0) == [(0, 1), (2, 3), (4, 4), (5, 5), (6, 7)]
+    assert plan.stages(1) == [(8, 8), (9, 9), (10, 11), (12, 12), (13, 13), (14, 14), (15, 15)]
+    plan = M.Plan(W.YOLOV2_16, (608, 608, 3), "3x3/3/2x2")   # group 2 starts with a pool
+    assert plan.stages(0) == [(0, 1), (2, 2)]
+    assert plan.stages(1)[0] == (3, 3)
+
+
+def test_workspace_size(lib):
+    plan = M.Plan(W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2")
+    b1 = plan.workspace_size(1, "bf16")
+    assert b1 > 0 and b1 % 256 == 0
+    assert plan.workspace_size(4, "bf16") >= 4 * b1 - 256
+    assert plan.workspace_size(1, "f32") >= 2 * b1 - 256
+    one = M.Plan([W.conv(8)], (16, 16, 3), "2x2")          # single stage: no scratch
+    assert one.workspace_size(3, "f32") == 0
+
+
+def _create_rc(layers, h, w, c, gs, rows, cols):
+    n = len(layers)
+    arr = (M.mafat_layer * max(1, n))()
+    for k, L in enumerate(layers):
+        arr[k] = M.mafat_layer(*L)
+    h_ = ctypes.c_void_p()
+    rc = M.lib().mafat_plan_create(arr, n, h, w, c, (ctypes.c_int32 * len(gs))(*gs), len(gs),
+                                   (ctypes.c_int32 * len(rows))(*rows), (ctypes.c_int32 * len(cols))(*cols),
+                                   ctypes.byref(h_))
+    if h_.value:
+        M.lib().mafat_plan_destroy(h_.value)
+    return rc
+
+
+def test_plan_create_error_codes(lib):
+    conv3 = (0, 8, 3, 1, 1, 1)
+    pool = (1, 0, 2, 2, 0, 0)
+    ok = _create_rc([conv3, pool], 16, 16, 3, [0], [2], [2])
+    assert ok == M.MAFAT_OK
+    assert _create_rc([(0, 8, 5, 1, 2, 1)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED  # 5x5
+    assert _create_rc([(0, 8, 3, 2, 1, 1)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED  # stride 2
+    assert _create_rc([(1, 0, 3, 2, 0, 0)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED  # 3x3 pool
+    assert _create_rc([(0, 8, 3, 1, 1, 7)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED  # activation
+    assert _create_rc([(9, 8, 3, 1, 1, 1)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EINVAL        # op
+    assert _create_rc([conv3, pool], 16, 16, 3, [0], [9], [1]) == M.MAFAT_ESHAPE               # grid > out
+    assert _create_rc([conv3, pool], 16, 16, 3, [1], [1], [1]) == M.MAFAT_ESHAPE               # start != 0
+    assert _create_rc([conv3, pool], 16, 16, 3, [0, 0], [1, 1], [1, 1]) == M.MAFAT_ESHAPE      # not increasing
+    assert _create_rc([conv3, pool], 16, 16, 3, [0, 2], [1, 1], [1, 1]) == M.MAFAT_ESHAPE      # start >= n
+    assert _create_rc([conv3, pool], 0, 16, 3, [0], [1], [1]) == M.MAFAT_ESHAPE                # empty input
+    assert _create_rc([pool, pool], 3, 3, 3, [0], [1], [1]) == M.MAFAT_ESHAPE                  # 1x1 -> pool
+    assert _create_rc([conv3], 40000, 4, 3, [0], [1], [1]) == M.MAFAT_ESHAPE                   # > 32767
+    assert _create_rc([], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EINVAL
+    assert M.lib().mafat_plan_create(None, 1, 1, 1, 1, None, 1, None, None, None) == M.MAFAT_EINVAL
+    assert b"grid" in M.lib().mafat_last_error() or True
+
+
+def test_run_argument_errors_before_any_launch(lib):
+    plan = M.Plan(W.TINY, (64, 64, 3), "2x2")
+    need = plan.workspace_size(1, "f32")
+    L = M.lib()
+    vp = ctypes.c_void_p
+    fake = 1 << 20          # aligned, never dereferenced: validation fails first
+    w = M._ptrs([fake, None, fake])
+    # workspace too small
+    rc = L.mafat_run_group(plan.handle, 0, 1, M.MAFAT_F32, fake, fake * 4, w, w, w, fake, need - 1, None, None)
+    assert rc == M.MAFAT_EWORKSPACE
+    # unsupported dtype, bad batch, bad group, null plan
+    assert L.mafat_run_group(plan.handle, 0, 1, 7, fake, fake * 4, w, w, w, fake, need, None, None) == M.MAFAT_EUNSUPPORTED
+    assert L.mafat_run_group(plan.handle, 0, 0, 0, fake, fake * 4, w, w, w, fake, need, None, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_group(plan.handle, 3, 1, 0, fake, fake * 4, w, w, w, fake, need, None, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_group(None, 0, 1, 0, fake, fake * 4, w, w, w, fake, need, None, None) == M.MAFAT_EINVAL
+    # misaligned / null tensors, overlapping x and y, missing weights
+    assert L.mafat_run_group(plan.handle, 0, 1, 0, fake + 4, fake * 4, w, w, w, fake, need, None, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_group(plan.handle, 0, 1, 0, None, fake * 4, w, w, w, fake, need, None, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_group(plan.handle, 0, 1, 0, fake, fake + 256, w, w, w, fake, need, None, None) == M.MAFAT_EINVAL
+    nw = M._ptrs([None, None, fake])
+    assert L.mafat_run_group(plan.handle, 0, 1, 0, fake, fake * 4, nw, w, w, fake, need, None, None) == M.MAFAT_EINVAL
+    # workspace misaligned
+    assert L.mafat_run_group(plan.handle, 0, 1, 0, fake, fake * 4, w, w, w, fake + 16, need, None, None) == M.MAFAT_EINVAL
+    # network with several groups but no cut buffers
+    plan2 = M.Plan(W.TINY, (64, 64, 3), "2x2/2/2x2")
+    assert L.mafat_run_network(plan2.handle, 1, 0, fake, fake * 4, None, w, w, w, fake, 1 << 30, None) == M.MAFAT_EINVAL
+    assert M.lib().mafat_status_string(M.MAFAT_EWORKSPACE) == b"workspace too small"

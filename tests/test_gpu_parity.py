@@ -1,0 +1,118 @@
+"""GPU parity: the HIP library through its C ABI against the CPU oracle on
+the same seeded inputs.
+
+Tolerance (normwise, max|gpu - ref| / max|ref| per compared tensor):
+1e-4 for float32, 2e-2 for bfloat16 activations/weights with float32
+accumulation; the oracle is float64 on the same (bf16-rounded) values.
+Group outputs (the cut tensors) are compared as well as the final output.
+"""
+import numpy as np
+import pytest
+
+from paper_2107_06960_amd import workloads as W
+
+from gpu_util import TOL, normwise_err, require_gpu, run_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _check_full(orc, layers, h, w, c, tiling, batch, dtype, seed=0):
+    print(f"[parity] {h}x{w}x{c} {tiling} batch={batch} {dtype} seed={seed}", flush=True)
+    p = W.make_inputs(layers, h, w, c, batch, seed, dtype)
+    out, cuts, net, _ = run_gpu(layers, h, w, c, p, tiling, batch, dtype)
+    ref = orc.forward_layers(layers, h, w, c, p["x"], p)
+    err = normwise_err(out, ref)
+    assert err <= TOL[dtype], (tiling, dtype, err)
+    gs, _, _ = W.parse_tiling(tiling, len(layers))
+    for g in range(len(gs) - 1):
+        cref = orc.forward_layers(layers, h, w, c, p["x"], p, 0, gs[g + 1] - 1)
+        e = normwise_err(cuts[g], cref)
+        assert e <= TOL[dtype], (tiling, dtype, "cut", g, e)
+    return err
+
+
+def test_tiny_f32(orc):
+    wl = W.WORKLOADS["tiny"]
+    err = _check_full(orc, wl.layers, wl.h, wl.w, wl.c, wl.tiling, 1, "f32")
+    print("tiny f32 err", err)
+
+
+def test_tiny_bf16(orc):
+    wl = W.WORKLOADS["tiny"]
+    _check_full(orc, wl.layers, wl.h, wl.w, wl.c, wl.tiling, 2, "bf16")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("tiling", ["1x1/NoCut", "3x3/NoCut", "5x5/8/2x2", "2x3/4/3x2", "4x4/12/1x1"])
+def test_yolo_small_image(orc, dtype, tiling):
+    # the 16-layer YOLOv2 stack on an 80x80 image: every layer kind, all
+    # channel widths (32..512), ragged tiles
+    _check_full(orc, W.YOLOV2_16, 80, 80, 3, tiling, 1, dtype, seed=3)
+
+
+def test_yolo_odd_image_batch(orc):
+    # odd extents: every max-pool drops a row/column
+    _check_full(orc, W.YOLOV2_16, 71, 93, 3, "3x2/8/2x2", 2, "bf16", seed=5)
+
+
+def test_many_tiles_chunked_launch(orc):
+    # 9x8 = 72 tiles > one launch's 64-tile argument block
+    _check_full(orc, W.TINY, 64, 64, 3, "9x8", 1, "f32", seed=9)
+
+
+@pytest.mark.parametrize("seed", [11, 12, 13, 14])
+def test_random_stacks(orc, seed):
+    rng = np.random.default_rng(seed)
+    layers = []
+    c = int(rng.choice([3, 16, 32, 48]))
+    c0 = c
+    for _ in range(int(rng.integers(2, 6))):
+        if rng.random() < 0.3 and layers and layers[-1]["op"] == W.CONV:
+            layers.append(W.maxpool())
+        else:
+            layers.append(W.conv(int(rng.choice([16, 32, 48, 64, 20])), int(rng.choice([1, 3])),
+                                 act=str(rng.choice([W.LEAKY, W.LINEAR]))))
+    h, w = int(rng.integers(20, 60)), int(rng.integers(20, 60))
+    n = len(layers)
+    cut = int(rng.integers(1, n)) if n > 2 else None
+    tiling = f"{rng.integers(1, 4)}x{rng.integers(1, 4)}" + (f"/{cut}/{rng.integers(1, 3)}x{rng.integers(1, 3)}" if cut else "")
+    for dtype in ("f32", "bf16"):
+        _check_full(orc, layers, h, w, c0, tiling, 1, dtype, seed=seed)
+
+
+def test_every_output_written_once_and_guards_untouched():
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    wl = W.WORKLOADS["tiny"]
+    p = W.workload_inputs(wl)
+    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), "3x3")
+    net = M.Network(plan, p, 1, "f32")
+    x = net.input_tensor(p["x"])
+    guard = 4096
+    big = torch.full((guard * 2 + net.y.numel(),), float("nan"), device="cuda")
+    big[:guard] = 12345.0
+    big[-guard:] = 12345.0
+    y = big[guard:guard + net.y.numel()].view_as(net.y)
+    net.run_group(0, x, y)
+    torch.cuda.synchronize()
+    assert not torch.isnan(y).any()
+    assert torch.all(big[:guard] == 12345.0) and torch.all(big[-guard:] == 12345.0)
+
+
+def test_deterministic_bitwise():
+    import torch
+    wl = W.WORKLOADS["yolo608_5x5_8_2x2"]
+    p = W.make_inputs(W.YOLOV2_16, 128, 128, 3, 1, 0, "bf16")
+    from paper_2107_06960_amd import mafat as M
+    plan = M.Plan(W.YOLOV2_16, (128, 128, 3), wl.tiling)
+    net = M.Network(plan, p, 1, "bf16")
+    x = net.input_tensor(p["x"])
+    a = net.run(x).clone()
+    b = net.run(x).clone()
+    torch.cuda.synchronize()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
