@@ -17,16 +17,33 @@
 //                       channel count does not fill a K chunk (the 3-channel
 //                       first layer): one thread per output pixel (or per
 //                       2x2 pool window), weights through the scalar cache.
+//   conv_rgb_kernel     the 3-channel first layer on the vector ALUs
+//                       (bf16: packed dot products), patch in registers.
 //   pool_kernel         a max-pool stage that does not follow a convolution.
 #include <hip/hip_runtime.h>
 
 #include "kernel_args.h"
 
 namespace mafat {
+#ifdef MAFAT_TUNING
+// Tuning builds only: phase timestamps of a few workgroups.
+__device__ long long g_trace[4][64];
+#define MAFAT_TRACE(slot_)                                                                     \
+  do {                                                                                         \
+    if (threadIdx.x == 0 && (blockIdx.x == 0 || blockIdx.x == gridDim.x - 1 ||                 \
+                             blockIdx.x == gridDim.x / 2) && (slot_) < 64)                     \
+      g_trace[blockIdx.x == 0 ? 0 : (blockIdx.x == gridDim.x - 1 ? 1 : 2)][(slot_)] = wall_clock64(); \
+  } while (0)
+#else
+#define MAFAT_TRACE(slot_) do {} while (0)
+#endif
 namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+// Native 16-byte vector (HIP's uint4 is a struct; selects between structs
+// compile to stack copies, so the kernels use this type for 16-byte data).
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 template <int DT> struct Elt;
 template <> struct Elt<MAFAT_F32> { using T = float; };
@@ -65,19 +82,27 @@ __device__ __forceinline__ int xcd_remap(int bid, int total) {
 }
 
 struct BlockPos {
-  int frame, tile, mb, nb;
+  int frame, tile, mb, nb, ks, blk;  // blk: block index within the frame (mg * nblk_n + nb)
 };
 
 __device__ __forceinline__ BlockPos decode_block(const StageArgs& a) {
   int bid = xcd_remap(static_cast<int>(blockIdx.x), a.total_blocks);
-  const int per_frame = a.mblk_total * a.nblk_n;
+  const int per_frame = a.mblk_total * a.nblk_n * a.nsplit;
   BlockPos p;
   p.frame = bid / per_frame;
   bid -= p.frame * per_frame;
-  const int mg = bid / a.nblk_n;
-  p.nb = bid - mg * a.nblk_n;
+  // splits of one output block are adjacent (same XCD after the remap), then
+  // channel blocks, then pixel blocks
+  const int blk = bid / a.nsplit;
+  p.ks = bid - blk * a.nsplit;
+  p.blk = blk;
+  const int mg = blk / a.nblk_n;
+  p.nb = blk - mg * a.nblk_n;
+  // Tile lookup without a chain of dependent loads: every prefix entry is
+  // read with a constant offset (the loads issue together), then counted.
   int t = 0;
-  while (t + 1 < a.ntiles && a.mblk_prefix[t + 1] <= mg) ++t;
+#pragma unroll
+  for (int k = 1; k < kMaxTilesPerLaunch; ++k) t += (k < a.ntiles && a.mblk_prefix[k] <= mg) ? 1 : 0;
   p.tile = t;
   p.mb = mg - a.mblk_prefix[t];
   return p;
@@ -103,10 +128,10 @@ __device__ __forceinline__ void row_pixel(const KTile& t, int m, int* oy, int* o
 }
 
 template <int DT>
-__device__ __forceinline__ void mma(f32x4& c, const uint4& a, const uint4& b);
+__device__ __forceinline__ void mma(f32x4& c, const u32x4& a, const u32x4& b);
 
 template <>
-__device__ __forceinline__ void mma<MAFAT_BF16>(f32x4& c, const uint4& a, const uint4& b) {
+__device__ __forceinline__ void mma<MAFAT_BF16>(f32x4& c, const u32x4& a, const u32x4& b) {
   c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                               __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
@@ -115,7 +140,7 @@ __device__ __forceinline__ void mma<MAFAT_BF16>(f32x4& c, const uint4& a, const 
 // four 16x16x4 MFMAs each take one of them.  A and B lanes use the same K
 // assignment, so the sum runs over all 16 K elements of the chunk.
 template <>
-__device__ __forceinline__ void mma<MAFAT_F32>(f32x4& c, const uint4& a, const uint4& b) {
+__device__ __forceinline__ void mma<MAFAT_F32>(f32x4& c, const u32x4& a, const u32x4& b) {
   c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
   c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
   c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
@@ -123,25 +148,47 @@ __device__ __forceinline__ void mma<MAFAT_F32>(f32x4& c, const uint4& a, const u
 }
 
 // Implicit-GEMM convolution, block tile BM pixels x BN channels, 4 waves in
-// a 2x2 arrangement, K consumed in 64-byte chunks (32 bf16 or 16 fp32
-// channels of one filter tap).  Requires c_in % (64 / sizeof(T)) == 0 and
-// c_out % 16 == 0 (checked by the host).
-template <int DT, int F, int BM, int BN, bool POOL>
+// a 2x2 arrangement (wave tile BM/2 x BN/2 of 16x16 accumulator tiles).
+//
+// K runs over (tap, channel) in 64-byte sub-chunks (32 bf16 or 16 fp32
+// channels of one filter tap); a pipeline stage holds two sub-chunks
+// (128 bytes of every A and B row).  Each thread issues its 16-byte loads for
+// stage s+DEPTH while the waves run the MFMAs of stage s from LDS, so DEPTH
+// stages are in flight per workgroup; LDS is double buffered with one
+// barrier per stage.  Rows are padded to 144 bytes so the 16-lane fragment
+// reads of consecutive rows hit distinct banks.
+//
+// Epilogue: scale, bias, activation, the optional 2x2 max (the 4 accumulator
+// rows a lane holds are one pool window), rounding to the output type, then
+// the block's output tile is transposed through LDS and written with 16-byte
+// stores along channels.
+//
+// Requires c_in % (64 / sizeof(T)) == 0 and c_out % 16 == 0 (host-checked).
+template <int DT, int F, int BM, int BN, bool POOL, int DEPTH>
 __global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
   using T = typename Elt<DT>::T;
   constexpr int P = (F - 1) / 2;
-  constexpr int KC = 64 / static_cast<int>(sizeof(T));   // channels per K chunk
+  constexpr int KC = 64 / static_cast<int>(sizeof(T));   // channels per sub-chunk
   constexpr int EPV = 16 / static_cast<int>(sizeof(T));  // channels per 16 bytes
-  constexpr int ALD = BM / 64, BLD = BN / 64;            // staging loads per thread
+  constexpr int ROWQ = 9;                                 // u32x4 per LDS row
+  constexpr int ALD = BM / 32, BLD = BN / 32;             // loads per thread per stage
   constexpr int WM = BM / 2, WN = BN / 2, MT = WM / 16, NT = WN / 16;
-  constexpr int LROW = 5;  // uint4 per LDS row: 64 data bytes + 16 pad bytes
-  __shared__ uint4 sA[2][BM * LROW];
-  __shared__ uint4 sB[2][BN * LROW];
+  static_assert(DEPTH >= 2 && DEPTH <= 6, "pipeline depth");
+  constexpr int OPND_BYTES = 2 * (BM + BN) * ROWQ * 16;
+  constexpr int OROWS = POOL ? BM / 4 : BM;
+  constexpr int OROW_BYTES = BN * static_cast<int>(sizeof(T)) + 16;
+  constexpr int OUT_BYTES = OROWS * OROW_BYTES;
+  constexpr int SMEM = OPND_BYTES > OUT_BYTES ? OPND_BYTES : OUT_BYTES;
+  __shared__ __align__(16) unsigned char smem[SMEM];
+  u32x4* sA = reinterpret_cast<u32x4*>(smem);                 // [2][BM][ROWQ]
+  u32x4* sB = sA + 2 * BM * ROWQ;                             // [2][BN][ROWQ]
 
+  MAFAT_TRACE(0);
   const BlockPos bp = decode_block(a);
   const KTile tl = a.tiles[bp.tile];
   const int tid = static_cast<int>(threadIdx.x), lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
+  MAFAT_TRACE(4 + (tl.ch > 30000 ? 1 : 0));
   const int M = tl.ch * tl.cw;
   const int m0 = bp.mb * BM, n0 = bp.nb * BN;
   const int cin = a.cin, cout = a.cout;
@@ -150,51 +197,90 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
   const T* wgt = static_cast<const T*>(a.w);
   const int K = F * F * cin;
   const int cblocks = cin / KC;
-  const int ksteps = F * F * cblocks;
-  const int chunk = tid & 3;
+  const int nsub_all = F * F * cblocks;  // 64-byte sub-chunks along K
+  const int nstage_all = (nsub_all + 1) >> 1;
+  // This block's share of K: stages [st0, st0 + nstage) of 128 bytes.
+  const int sps = (nstage_all + a.nsplit - 1) / a.nsplit;
+  const int st0 = bp.ks * sps;
+  const int nstage = min(nstage_all, st0 + sps) - st0;
+  const int nsub = min(nsub_all, 2 * (st0 + nstage));  // sub-chunks at or past this are zero
 
-  int a_oy[ALD], a_ox[ALD];
-  bool a_ok[ALD];
+  // This thread stages rows r0 + 32 i, 16-byte piece `pc` of sub-chunk `hh`.
+  // Per A row: the element offset of its pixel in the source buffer and a
+  // mask of the filter taps that land inside the image (zero padding).
+  const int r0 = tid >> 3, q = tid & 7, hh = q >> 2, pc = q & 3;
+  int a_base[ALD];
+  unsigned a_taps[ALD];
 #pragma unroll
   for (int i = 0; i < ALD; ++i) {
-    const int m = m0 + (tid >> 2) + 64 * i;
-    a_ok[i] = m < M;
-    row_pixel<POOL>(tl, a_ok[i] ? m : 0, &a_oy[i], &a_ox[i]);
+    const int m = m0 + r0 + 32 * i;
+    int oy, ox;
+    row_pixel<POOL>(tl, m < M ? m : 0, &oy, &ox);
+    a_base[i] = ((oy - tl.sy0) * tl.sw + (ox - tl.sx0)) * cin + pc * EPV;
+    unsigned mask = 0;
+#pragma unroll
+    for (int t = 0; t < F * F; ++t) {
+      const int iy = oy + t / F - P, ix = ox + t % F - P;
+      const bool in = static_cast<unsigned>(iy) < static_cast<unsigned>(a.in_h) &&
+                      static_cast<unsigned>(ix) < static_cast<unsigned>(a.in_w);
+      mask |= in ? (1u << t) : 0u;
+    }
+    a_taps[i] = (m < M) ? mask : 0u;
   }
-  const T* b_ptr[BLD];
+  int b_off[BLD];
   bool b_ok[BLD];
 #pragma unroll
   for (int i = 0; i < BLD; ++i) {
-    const int co = n0 + (tid >> 2) + 64 * i;
+    const int co = n0 + r0 + 32 * i;
     b_ok[i] = co < cout;
-    b_ptr[i] = wgt + static_cast<int64_t>(b_ok[i] ? co : 0) * K + chunk * EPV;
+    b_off[i] = (b_ok[i] ? co : 0) * K + pc * EPV;
   }
 
-  uint4 ra[ALD], rb[BLD];
-  const uint4 zero = make_uint4(0, 0, 0, 0);
-  auto gload = [&](int ks) {
-    const int tap = ks / cblocks, cb = ks - tap * cblocks;
-    const int ky = tap / F, kx = tap - ky * F;
-    const int ci0 = cb * KC + chunk * EPV;
-#pragma unroll
-    for (int i = 0; i < ALD; ++i) {
-      const int iy = a_oy[i] + ky - P, ix = a_ox[i] + kx - P;
-      const bool ok = a_ok[i] && static_cast<unsigned>(iy) < static_cast<unsigned>(a.in_h) &&
-                      static_cast<unsigned>(ix) < static_cast<unsigned>(a.in_w);
-      ra[i] = ok ? *reinterpret_cast<const uint4*>(
-                       src + ((iy - tl.sy0) * tl.sw + (ix - tl.sx0)) * cin + ci0)
-                 : zero;
-    }
-#pragma unroll
-    for (int i = 0; i < BLD; ++i)
-      rb[i] = b_ok[i] ? *reinterpret_cast<const uint4*>(b_ptr[i] + tap * cin + cb * KC) : zero;
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < ALD; ++i) sA[buf][((tid >> 2) + 64 * i) * LROW + chunk] = ra[i];
-#pragma unroll
-    for (int i = 0; i < BLD; ++i) sB[buf][((tid >> 2) + 64 * i) * LROW + chunk] = rb[i];
-  };
+  u32x4 ra[DEPTH][ALD], rb[DEPTH][BLD];
+  unsigned okm[DEPTH];  // bit i: A load i valid; bit ALD + i: B load i valid
+  // Load cursor: filter tap and channel block of the first sub-chunk of the
+  // next stage to load (uniform across the workgroup); advanced by two
+  // sub-chunks per load.
+  int lc_kc = 2 * st0, lc_tap = lc_kc / cblocks, lc_cb = lc_kc - lc_tap * cblocks;
+  // Global -> registers, next stage into register set d_.  Every load is
+  // issued unconditionally from a clamped, valid address; invalid ones are
+  // zeroed when the set is written to LDS.  (Zeroing here, or a guarded
+  // load, would make the compiler wait for the load right away and nothing
+  // would stay in flight.)
+#define MAFAT_GLOAD(d_)                                                                        \
+  do {                                                                                         \
+    const int tap1_ = (lc_cb + 1 < cblocks) ? lc_tap : lc_tap + 1;                             \
+    const int cb1_ = (lc_cb + 1 < cblocks) ? lc_cb + 1 : lc_cb + 1 - cblocks;                  \
+    const int tap_ = hh ? tap1_ : lc_tap, cb_ = hh ? cb1_ : lc_cb;                             \
+    const bool kok_ = lc_kc + hh < nsub;                                                       \
+    const int ky_ = tap_ / F, kx_ = tap_ - ky_ * F;                                            \
+    const int aoff_ = ((ky_ - P) * tl.sw + (kx_ - P)) * cin + cb_ * KC;                       \
+    const int boff_ = tap_ * cin + cb_ * KC;                                                   \
+    unsigned m_ = 0;                                                                           \
+    _Pragma("unroll") for (int i = 0; i < ALD; ++i) {                                          \
+      const bool ok = kok_ && ((a_taps[i] >> tap_) & 1u);                                      \
+      m_ |= ok ? (1u << i) : 0u;                                                               \
+      ra[d_][i] = *reinterpret_cast<const u32x4*>(src + (ok ? a_base[i] + aoff_ : 0));         \
+    }                                                                                          \
+    _Pragma("unroll") for (int i = 0; i < BLD; ++i) {                                          \
+      const bool ok = kok_ && b_ok[i];                                                         \
+      m_ |= ok ? (1u << (ALD + i)) : 0u;                                                       \
+      rb[d_][i] = *reinterpret_cast<const u32x4*>(wgt + (ok ? b_off[i] + boff_ : 0));         \
+    }                                                                                          \
+    okm[d_] = m_;                                                                              \
+    lc_kc += 2;                                                                                \
+    lc_cb += 2;                                                                                \
+    while (lc_cb >= cblocks) { lc_cb -= cblocks; ++lc_tap; }                                   \
+  } while (0)
+  // Registers (set d_) -> LDS buffer buf_, zeroing the invalid loads.
+#define MAFAT_LSTORE(d_, buf_)                                                                     \
+  do {                                                                                             \
+    _Pragma("unroll") for (int i = 0; i < ALD; ++i)                                                \
+      sA[((buf_) * BM + r0 + 32 * i) * ROWQ + q] = ra[d_][i] & ((okm[d_] >> i) & 1u ? ~0u : 0u);   \
+    _Pragma("unroll") for (int i = 0; i < BLD; ++i)                                                \
+      sB[((buf_) * BN + r0 + 32 * i) * ROWQ + q] =                                                 \
+          rb[d_][i] & ((okm[d_] >> (ALD + i)) & 1u ? ~0u : 0u);                                     \
+  } while (0)
 
   f32x4 acc[MT][NT];
 #pragma unroll
@@ -202,59 +288,139 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
 #pragma unroll
     for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  gload(0);
-  lstore(0);
+  // The stage count is padded to a multiple of DEPTH so that the loop body
+  // has no branches: padded stages load from a valid address, are masked to
+  // zero and add nothing.  (Branches around the loads would create joins
+  // at which the compiler waits for every outstanding load.)
+  const int nst_pad = (nstage + DEPTH - 1) / DEPTH * DEPTH;
+  MAFAT_TRACE(5);
+  MAFAT_GLOAD(0);
+  MAFAT_GLOAD(1);
+  if constexpr (DEPTH >= 3) MAFAT_GLOAD(2);
+  if constexpr (DEPTH >= 4) MAFAT_GLOAD(3);
+  if constexpr (DEPTH >= 5) MAFAT_GLOAD(4);
+  if constexpr (DEPTH >= 6) MAFAT_GLOAD(5);
+  MAFAT_TRACE(6);
+  MAFAT_LSTORE(0, 0);
+  MAFAT_TRACE(7);
   __syncthreads();
-  for (int ks = 0; ks < ksteps; ++ks) {
-    const int cur = ks & 1;
-    if (ks + 1 < ksteps) gload(ks + 1);
-    uint4 af[MT], bf[NT];
-#pragma unroll
-    for (int i = 0; i < MT; ++i) af[i] = sA[cur][(wm * WM + i * 16 + (lane & 15)) * LROW + (lane >> 4)];
-#pragma unroll
-    for (int j = 0; j < NT; ++j) bf[j] = sB[cur][(wn * WN + j * 16 + (lane & 15)) * LROW + (lane >> 4)];
+  MAFAT_TRACE(1);
+  // One pipeline step on stage s0 + d_, held in LDS buffer (s0 + d_) & 1:
+  // issue the loads of stage s0 + d_ + DEPTH into register set d_ (written
+  // to LDS in the previous step), run the MFMAs, write register set dn_
+  // (stage s0 + d_ + 1) to the other LDS buffer, barrier.
+#define MAFAT_STEP(d_, dn_)                                                                      \
+  do {                                                                                           \
+    const int st = s0 + (d_);                                                                    \
+    const int buf = st & 1;                                                                      \
+    MAFAT_GLOAD(d_);                                                                             \
+    _Pragma("unroll") for (int h = 0; h < 2; ++h) {                                              \
+      u32x4 af[MT], bfr[NT];                                                                     \
+      _Pragma("unroll") for (int i = 0; i < MT; ++i)                                             \
+        af[i] = sA[(buf * BM + wm * WM + i * 16 + (lane & 15)) * ROWQ + h * 4 + (lane >> 4)];     \
+      _Pragma("unroll") for (int j = 0; j < NT; ++j)                                             \
+        bfr[j] = sB[(buf * BN + wn * WN + j * 16 + (lane & 15)) * ROWQ + h * 4 + (lane >> 4)];    \
+      _Pragma("unroll") for (int i = 0; i < MT; ++i)                                             \
+        _Pragma("unroll") for (int j = 0; j < NT; ++j) mma<DT>(acc[i][j], af[i], bfr[j]);        \
+    }                                                                                            \
+    MAFAT_LSTORE(dn_, buf ^ 1);                                                                  \
+    __syncthreads();                                                                             \
+    MAFAT_TRACE(8 + st);                                                                         \
+  } while (0)
+  for (int s0 = 0; s0 < nst_pad; s0 += DEPTH) {
+    if constexpr (DEPTH == 2) {
+      MAFAT_STEP(0, 1); MAFAT_STEP(1, 0);
+    } else if constexpr (DEPTH == 3) {
+      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 0);
+    } else if constexpr (DEPTH == 4) {
+      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 3); MAFAT_STEP(3, 0);
+    } else if constexpr (DEPTH == 5) {
+      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 3); MAFAT_STEP(3, 4); MAFAT_STEP(4, 0);
+    } else {
+      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 3); MAFAT_STEP(3, 4); MAFAT_STEP(4, 5);
+      MAFAT_STEP(5, 0);
+    }
+  }
+#undef MAFAT_STEP
+#undef MAFAT_GLOAD
+#undef MAFAT_LSTORE
+
+  MAFAT_TRACE(2);
+  // Split K: every block writes its partial sums; the last of the nsplit
+  // blocks of an output tile to arrive adds them in split order (the same
+  // order whatever the arrival order, so results are reproducible) and runs
+  // the epilogue; it also resets the counter for the next use.
+  if (a.nsplit > 1) {
+    __shared__ uint32_t s_arrival;
+    const int64_t bidx = static_cast<int64_t>(bp.frame) * (a.mblk_total * a.nblk_n) + bp.blk;
+    f32x4* part = reinterpret_cast<f32x4*>(a.partials) + bidx * a.nsplit * (MT * NT * 256);
 #pragma unroll
     for (int i = 0; i < MT; ++i)
 #pragma unroll
-      for (int j = 0; j < NT; ++j) mma<DT>(acc[i][j], af[i], bf[j]);
-    if (ks + 1 < ksteps) lstore(cur ^ 1);
+      for (int j = 0; j < NT; ++j) part[(bp.ks * MT * NT + i * NT + j) * 256 + tid] = acc[i][j];
+    __threadfence();
     __syncthreads();
+    if (tid == 0) s_arrival = atomicAdd(&a.counters[bidx], 1u);
+    __syncthreads();
+    if (s_arrival != static_cast<uint32_t>(a.nsplit - 1)) return;
+    __threadfence();
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int k = 0; k < a.nsplit; ++k)
+          sum += (k == bp.ks) ? acc[i][j] : part[(k * MT * NT + i * NT + j) * 256 + tid];
+        acc[i][j] = sum;
+      }
+    if (tid == 0) atomicExch(&a.counters[bidx], 0u);
   }
 
-  // Epilogue: lane holds rows 4*(lane/16) .. +3 of each 16x16 accumulator
-  // tile, column lane % 16.
-  const int rbase = (lane >> 4) * 4;
+  // Epilogue.  Lane holds rows 4*(lane/16) .. +3 of each 16x16 accumulator
+  // tile, column lane % 16.  Results go to LDS as [output row][channel].
+  T* sO = reinterpret_cast<T*>(smem);
+  constexpr int OSTRIDE = OROW_BYTES / static_cast<int>(sizeof(T));
+  const int rq = (lane >> 4) * 4;
 #pragma unroll
   for (int j = 0; j < NT; ++j) {
-    const int co = n0 + wn * WN + j * 16 + (lane & 15);
-    if (co >= cout) continue;
-    const float s = a.scale[co], b = a.bias[co];
+    const int cl = wn * WN + j * 16 + (lane & 15);
+    const int co = n0 + cl;
+    const float s = co < cout ? a.scale[co] : 0.f, b = co < cout ? a.bias[co] : 0.f;
 #pragma unroll
     for (int i = 0; i < MT; ++i) {
-      const int mrow = m0 + wm * WM + i * 16 + rbase;
-      if (mrow >= M) continue;
+      const int ml = wm * WM + i * 16 + rq;
       float v[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) v[r] = activate(acc[i][j][r] * s + b, a.act);
       if (POOL) {
         const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-        const int pw = tl.cw >> 1;
-        const int q = mrow >> 2, qy = q / pw, qx = q - qy * pw;
-        const int py = (tl.cy0 >> 1) + qy, px = (tl.cx0 >> 1) + qx;
-        put(dst + ((py - tl.dy0) * tl.dw + (px - tl.dx0)) * cout + co, mx);
+        put(sO + (ml >> 2) * OSTRIDE + cl, mx);
       } else {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = mrow + r;
-          if (m < M) {
-            int oy, ox;
-            row_pixel<false>(tl, m, &oy, &ox);
-            put(dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * cout + co, v[r]);
-          }
-        }
+        for (int r = 0; r < 4; ++r) put(sO + (ml + r) * OSTRIDE + cl, v[r]);
       }
     }
   }
+  __syncthreads();
+  constexpr int CPR = BN / EPV;  // 16-byte pieces per output row
+  const int pw = tl.cw >> 1;
+  for (int c = tid; c < OROWS * CPR; c += 256) {
+    const int row = c / CPR, piece = c - row * CPR;
+    const int m = m0 + (POOL ? 4 * row : row);
+    const int co = n0 + piece * EPV;
+    if (m >= M || co >= cout) continue;
+    int oy, ox;
+    if (POOL) {
+      const int qq = m >> 2, qy = qq / pw;
+      oy = (tl.cy0 >> 1) + qy;
+      ox = (tl.cx0 >> 1) + (qq - qy * pw);
+    } else {
+      row_pixel<false>(tl, m, &oy, &ox);
+    }
+    *reinterpret_cast<u32x4*>(dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * cout + co) =
+        *reinterpret_cast<const u32x4*>(sO + row * OSTRIDE + piece * EPV);
+  }
+  MAFAT_TRACE(3);
 }
 
 // Direct convolution on the vector ALUs, one thread per output pixel (or per
@@ -328,6 +494,141 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const StageArgs a) {
   }
 }
 
+// First layer of an image network: 3 input channels, 3x3 filter.  A K of 27
+// does not fill the matrix cores' K chunk, so this runs on the vector ALUs.
+// A thread owns one output pixel (or one 2x2 pool window) and one group of 8
+// output channels: its (Q+2)x(Q+2)x3 input patch is loaded into registers
+// (neighbouring threads of the same pixel hit the same cache lines), the
+// weights of its 8 channels are broadcast from LDS, and its result leaves in
+// one 16-byte store (the channel groups of a pixel are adjacent threads, so
+// the stores of a pixel are contiguous).  bf16 uses the packed dot product
+// v_dot2_f32_bf16 on channel pairs (c0,c1) and (c2,0): two multiply-adds per
+// instruction with float32 accumulation.
+// Requires c_out in {8, 16, 32, 64} (checked by the host).
+template <int DT, bool POOL>
+__global__ __launch_bounds__(256) 
+void conv_rgb_kernel(const StageArgs a) {
+  using T = typename Elt<DT>::T;
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  constexpr int Q = POOL ? 2 : 1;   // output pixels per thread along each axis
+  constexpr int PR = Q + 2;         // input patch extent
+  constexpr int CO = 8;
+  constexpr int NJ = (DT == MAFAT_BF16) ? 2 : 3;  // weight words per tap
+  __shared__ __align__(16) uint32_t wl[9 * 3 * 64];
+  const int cout = a.cout;
+  const int cg_n = cout / CO;                     // channel groups per pixel
+  const T* wgt = static_cast<const T*>(a.w);
+  // LDS weights, [tap][j][co]: bf16 j=0 holds (w_c0, w_c1), j=1 (w_c2, 0);
+  // fp32 j is the input channel.
+  for (int i = static_cast<int>(threadIdx.x); i < 9 * NJ * cout; i += 256) {
+    const int co = i % cout, rest = i / cout, j = rest % NJ, tap = rest / NJ;
+    const T* wr = wgt + co * 27 + tap * 3;
+    if constexpr (DT == MAFAT_BF16) {
+      wl[i] = (j == 0) ? (static_cast<uint32_t>(wr[0]) | (static_cast<uint32_t>(wr[1]) << 16))
+                       : static_cast<uint32_t>(wr[2]);
+    } else {
+      wl[i] = __float_as_uint(to_f(wr[j]));
+    }
+  }
+  __syncthreads();
+
+  const BlockPos bp = decode_block(a);
+  const KTile tl = a.tiles[bp.tile];
+  const int units = POOL ? (tl.ch >> 1) * (tl.cw >> 1) : tl.ch * tl.cw;
+  const int per_block = 256 / cg_n;
+  const int u = bp.mb * per_block + static_cast<int>(threadIdx.x) / cg_n;
+  const int co0 = (static_cast<int>(threadIdx.x) % cg_n) * CO;
+  if (u >= units) return;
+  int oy0, ox0;
+  if (POOL) {
+    const int pw = tl.cw >> 1, qy = u / pw;
+    oy0 = tl.cy0 + 2 * qy;
+    ox0 = tl.cx0 + 2 * (u - qy * pw);
+  } else {
+    const int yy = u / tl.cw;
+    oy0 = tl.cy0 + yy;
+    ox0 = tl.cx0 + (u - yy * tl.cw);
+  }
+  const T* src = static_cast<const T*>(a.src) + bp.frame * a.src_fstride + tl.src_off;
+  T* dst = static_cast<T*>(a.dst) + bp.frame * a.dst_fstride + tl.dst_off;
+
+  // input patch, zero outside the image
+  uint32_t pin[PR][PR][NJ];
+#pragma unroll
+  for (int r = 0; r < PR; ++r)
+#pragma unroll
+    for (int c = 0; c < PR; ++c) {
+      const int iy = oy0 - 1 + r, ix = ox0 - 1 + c;
+      const bool ok = static_cast<unsigned>(iy) < static_cast<unsigned>(a.in_h) &&
+                      static_cast<unsigned>(ix) < static_cast<unsigned>(a.in_w);
+      const T* p = src + (ok ? ((iy - tl.sy0) * tl.sw + (ix - tl.sx0)) * 3 : 0);
+      if constexpr (DT == MAFAT_BF16) {
+        const uint32_t e0 = p[0], e1 = p[1], e2 = p[2];
+        pin[r][c][0] = ok ? (e0 | (e1 << 16)) : 0u;
+        pin[r][c][1] = ok ? e2 : 0u;
+      } else {
+#pragma unroll
+        for (int j = 0; j < 3; ++j) {
+          const uint32_t e = __float_as_uint(to_f(p[j]));
+          pin[r][c][j] = ok ? e : 0u;
+        }
+      }
+    }
+
+  float acc[Q * Q][CO];
+#pragma unroll
+  for (int q = 0; q < Q * Q; ++q)
+#pragma unroll
+    for (int c = 0; c < CO; ++c) acc[q][c] = 0.f;
+#pragma unroll
+  for (int tap = 0; tap < 9; ++tap) {
+    const int ky = tap / 3, kx = tap % 3;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const u32x4 w0 = *reinterpret_cast<const u32x4*>(&wl[(tap * NJ + j) * cout + co0]);
+      const u32x4 w1 = *reinterpret_cast<const u32x4*>(&wl[(tap * NJ + j) * cout + co0 + 4]);
+      const uint32_t wv[CO] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
+#pragma unroll
+      for (int q = 0; q < Q * Q; ++q) {
+        const uint32_t v = pin[q / Q + ky][q % Q + kx][j];
+#pragma unroll
+        for (int c = 0; c < CO; ++c) {
+          if constexpr (DT == MAFAT_BF16)
+            acc[q][c] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, v),
+                                                        __builtin_bit_cast(bf16x2, wv[c]), acc[q][c], false);
+          else
+            acc[q][c] = fmaf(__uint_as_float(v), __uint_as_float(wv[c]), acc[q][c]);
+        }
+      }
+    }
+  }
+  float r[CO];
+#pragma unroll
+  for (int c = 0; c < CO; ++c) {
+    const float s = a.scale[co0 + c], b = a.bias[co0 + c];
+    float v = activate(acc[0][c] * s + b, a.act);
+#pragma unroll
+    for (int q = 1; q < Q * Q; ++q) v = fmaxf(v, activate(acc[q][c] * s + b, a.act));
+    r[c] = v;
+  }
+  int py = oy0, px = ox0;
+  if (POOL) { py >>= 1; px >>= 1; }
+  T* out = dst + ((py - tl.dy0) * tl.dw + (px - tl.dx0)) * cout + co0;
+  if constexpr (DT == MAFAT_BF16) {
+    u32x4 o;
+    o.x = f2bf(r[0]) | (static_cast<uint32_t>(f2bf(r[1])) << 16);
+    o.y = f2bf(r[2]) | (static_cast<uint32_t>(f2bf(r[3])) << 16);
+    o.z = f2bf(r[4]) | (static_cast<uint32_t>(f2bf(r[5])) << 16);
+    o.w = f2bf(r[6]) | (static_cast<uint32_t>(f2bf(r[7])) << 16);
+    *reinterpret_cast<u32x4*>(out) = o;
+  } else {
+    *reinterpret_cast<u32x4*>(out) = u32x4{__float_as_uint(r[0]), __float_as_uint(r[1]),
+                                           __float_as_uint(r[2]), __float_as_uint(r[3])};
+    *reinterpret_cast<u32x4*>(out + 4) = u32x4{__float_as_uint(r[4]), __float_as_uint(r[5]),
+                                               __float_as_uint(r[6]), __float_as_uint(r[7])};
+  }
+}
+
 // Lone 2x2/2 max-pool: 64 output pixels per block, 4 threads per pixel
 // striding over channels.  The computed rectangle is in pool-output
 // coordinates.
@@ -353,23 +654,40 @@ __global__ __launch_bounds__(256) void pool_kernel(const StageArgs a) {
   }
 }
 
+template <int DT, int F, bool POOL, int DEPTH>
+hipError_t launch_mfma(MfmaShape sh, const StageArgs& args, hipStream_t stream) {
+  const dim3 grid(static_cast<unsigned>(args.total_blocks)), block(256);
+#define MAFAT_SHAPE(bm_, bn_)                                                                  \
+  if (sh.bm == (bm_) && sh.bn == (bn_)) {                                                      \
+    hipLaunchKernelGGL((conv_mfma_kernel<DT, F, bm_, bn_, POOL, DEPTH>), grid, block, 0, stream, args); \
+    return hipGetLastError();                                                                  \
+  }
+  MAFAT_SHAPE(128, 128) MAFAT_SHAPE(128, 64) MAFAT_SHAPE(64, 128) MAFAT_SHAPE(64, 64)
+  MAFAT_SHAPE(64, 32) MAFAT_SHAPE(32, 64) MAFAT_SHAPE(32, 32)
+#undef MAFAT_SHAPE
+  return hipErrorInvalidValue;
+}
+
 template <int DT, int F, bool POOL>
 hipError_t launch_conv(int kind, MfmaShape sh, const StageArgs& args, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>(args.total_blocks)), block(256);
   if (kind == K_CONV_DIRECT) {
     hipLaunchKernelGGL((conv_direct_kernel<DT, F, POOL>), grid, block, 0, stream, args);
-  } else if (sh.bm == 64 && sh.bn == 64) {
-    hipLaunchKernelGGL((conv_mfma_kernel<DT, F, 64, 64, POOL>), grid, block, 0, stream, args);
-  } else if (sh.bm == 128 && sh.bn == 64) {
-    hipLaunchKernelGGL((conv_mfma_kernel<DT, F, 128, 64, POOL>), grid, block, 0, stream, args);
-  } else if (sh.bm == 64 && sh.bn == 128) {
-    hipLaunchKernelGGL((conv_mfma_kernel<DT, F, 64, 128, POOL>), grid, block, 0, stream, args);
-  } else if (sh.bm == 128 && sh.bn == 128) {
-    hipLaunchKernelGGL((conv_mfma_kernel<DT, F, 128, 128, POOL>), grid, block, 0, stream, args);
-  } else {
-    return hipErrorInvalidValue;
+    return hipGetLastError();
   }
-  return hipGetLastError();
+  if (kind == K_CONV_RGB) {
+    if (F != 3) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((conv_rgb_kernel<DT, POOL>), grid, block, 0, stream, args);
+    return hipGetLastError();
+  }
+  switch (sh.depth) {
+    case 2: return launch_mfma<DT, F, POOL, 2>(sh, args, stream);
+    case 3: return launch_mfma<DT, F, POOL, 3>(sh, args, stream);
+    case 4: return launch_mfma<DT, F, POOL, 4>(sh, args, stream);
+    case 5: return launch_mfma<DT, F, POOL, 5>(sh, args, stream);
+    case 6: return launch_mfma<DT, F, POOL, 6>(sh, args, stream);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 template <int DT>
@@ -387,11 +705,28 @@ hipError_t launch_dt(int kind, int f, bool pool, MfmaShape sh, const StageArgs& 
   return hipErrorInvalidValue;
 }
 
+__global__ __launch_bounds__(256) void zero_kernel(uint32_t* p, int64_t n) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
 }  // namespace
+
+#ifdef MAFAT_TUNING
+extern "C" int mafat_debug_trace(long long* host_out) {
+  return hipMemcpyFromSymbol(host_out, HIP_SYMBOL(g_trace), sizeof(g_trace)) == hipSuccess ? 0 : -1;
+}
+#endif
+
+hipError_t launch_zero(uint32_t* p, int64_t n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(zero_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, p, n);
+  return hipGetLastError();
+}
 
 int block_units(int kind, MfmaShape shape) {
   if (kind == K_CONV_MFMA) return shape.bm;
-  if (kind == K_CONV_DIRECT) return 256;
+  if (kind == K_CONV_DIRECT || kind == K_CONV_RGB) return 256;
   return 64;
 }
 

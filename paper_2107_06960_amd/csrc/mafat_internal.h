@@ -68,6 +68,24 @@ struct mafat_plan {
 };
 
 namespace mafat {
+
+// How one stage runs for a given batch and dtype (chosen by the runtime,
+// also used to size the workspace).
+struct StageConfig {
+  int kind;          // KernelKind
+  int bm, bn, depth; // matrix-core kernel block tile and pipeline depth
+  int nsplit;        // K splits per output block
+  int64_t blocks;    // output blocks per frame (pixel blocks x channel blocks)
+};
+StageConfig choose_config(const Stage& S, int batch, int dtype);
+
+// Workspace layout for one group: [scratch][partials][counters], each part
+// 256-byte aligned.  Sizes in bytes.
+struct WorkspaceLayout {
+  size_t scratch, partials, counters, total;
+};
+WorkspaceLayout workspace_layout(const Group& G, int batch, int dtype);
+
 // Thread-local error detail (mafat_last_error).
 void set_error(const std::string& msg);
 void clear_error();

@@ -294,13 +294,9 @@ extern "C" int mafat_workspace_size(const mafat_plan* plan, int32_t batch, int32
                                     size_t* bytes) {
   if (!plan || !bytes || batch < 1) return MAFAT_EINVAL;
   if (dtype != MAFAT_F32 && dtype != MAFAT_BF16) return MAFAT_EUNSUPPORTED;
-  const size_t esz = (dtype == MAFAT_F32) ? 4 : 2;
   size_t best = 0;
-  for (const Group& G : plan->groups) {
-    const size_t b = static_cast<size_t>(batch) * G.nbufs * G.ntiles * G.scratch_elems * esz;
-    best = std::max(best, b);
-  }
-  *bytes = (best + 255) & ~static_cast<size_t>(255);
+  for (const Group& G : plan->groups) best = std::max(best, workspace_layout(G, batch, dtype).total);
+  *bytes = best;
   return MAFAT_OK;
 }
 

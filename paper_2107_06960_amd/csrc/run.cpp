@@ -4,11 +4,18 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 
 #include "kernel_args.h"
 #include "mafat_internal.h"
+
+#ifdef MAFAT_TUNING
+extern "C" int mafat_debug_trace(long long* host_out);
+#endif
 
 namespace mafat {
 namespace {
@@ -27,10 +34,117 @@ bool mfma_ok(const Stage& S, int dtype) {
   return S.kind == STAGE_CONV && S.cin % kc == 0 && S.cout % 16 == 0;
 }
 
-MfmaShape pick_shape(const Stage& S, int /*dtype*/) {
-  (void)S;
-  return MfmaShape{64, 64};
+// The vector first-layer kernel: 3 input channels, 3x3, 8/16/32/64 outputs.
+bool rgb_ok(const Stage& S) {
+  return S.kind == STAGE_CONV && S.cin == 3 && S.f == 3 &&
+         (S.cout == 8 || S.cout == 16 || S.cout == 32 || S.cout == 64);
 }
+
+}  // namespace
+
+// Block tile, split count and pipeline depth for the matrix-core kernel,
+// from a small time model of one CU: a workgroup costs a fixed ~2 us
+// (first loads, epilogue) plus the larger of its MFMA time at the CU's
+// peak (4096 flop/clock) and its operand traffic at the CU's L2 bandwidth
+// (64 bytes/clock); workgroups beyond 256 queue on the CUs; a split adds
+// one reduction pass over the partial sums.  Larger tiles re-read fewer
+// operands; splitting K restores parallelism when there are few tiles.
+StageConfig choose_config(const Stage& S, int batch, int dtype) {
+  StageConfig c{};
+  c.nsplit = 1;
+  c.bm = 64; c.bn = 64; c.depth = 3;
+  if (S.kind == STAGE_POOL) { c.kind = K_POOL; return c; }
+  if (!mfma_ok(S, dtype)) {
+    c.kind = rgb_ok(S) ? K_CONV_RGB : K_CONV_DIRECT;
+    return c;
+  }
+  c.kind = K_CONV_MFMA;
+  const int esz = (dtype == MAFAT_BF16) ? 2 : 4;
+  const int kcs = 64 / esz;                                   // channels per sub-chunk
+  const int nstage = (S.f * S.f * (S.cin / kcs) + 1) / 2;     // 128-byte K stages
+  const double K = static_cast<double>(S.f) * S.f * S.cin;
+  const double clk = 2.4e9, mfma_rate = 4096.0 * clk, l2_rate = 64.0 * clk, t0 = 2e-6;
+  static const int kShapes[][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}, {64, 32}, {32, 64}};
+  double best = 1e30;
+  for (const auto& sh : kShapes) {
+    const int bm = sh[0], bn = sh[1];
+    if (bn > S.cout && bn > 32) continue;
+    int64_t mb = 0;
+    for (const TileGeom& T : S.tiles) mb += (static_cast<int64_t>(T.ch) * T.cw + bm - 1) / bm;
+    const int64_t blocks = mb * ((S.cout + bn - 1) / bn);
+    // Split K is off: combining partial sums across workgroups needs a
+    // device-scope fence, which writes back and invalidates the XCD's whole
+    // L2 and stalls every other workgroup on it (measured: 2.7x slower
+    // at two splits).
+    for (int split = 1; split <= 1 && split <= nstage; ++split) {
+      const int sps = (nstage + split - 1) / split;
+      const int eff = (nstage + sps - 1) / sps;  // splits that are not empty
+      if (eff != split) continue;
+      const double wgs = static_cast<double>(blocks) * split * batch;
+      const double k_share = K * sps / nstage;
+      const double flops = 2.0 * bm * bn * k_share, bytes = (bm + bn) * k_share * esz;
+      const double per_wg = std::max(flops / mfma_rate, bytes / l2_rate);
+      const double rounds = std::ceil(wgs / 256.0);
+      double t = t0 + rounds * per_wg;
+      if (split > 1) t += 1e-6 + (split - 1) * bm * bn * 4.0 / l2_rate;
+      if (t < best * 0.97) {
+        best = t;
+        c.bm = bm; c.bn = bn; c.nsplit = split; c.blocks = blocks;
+      }
+    }
+  }
+  // Pipeline depth: stages of K in flight per workgroup.  Deeper keeps more
+  // loads outstanding (per-CU L2 bandwidth grows with them); the stage count
+  // is padded to a multiple of the depth, so take the deepest one whose
+  // padding is at most one stage (or none for short K).
+  c.depth = 2;
+  for (int d = 6; d >= 2; --d) {
+    const int pad = (nstage + d - 1) / d * d - nstage;
+    if (pad == 0 || (pad <= 1 && nstage >= 4 * d)) { c.depth = d; break; }
+  }
+#ifdef MAFAT_TUNING
+  // Tuning builds only: MAFAT_TUNE="first_layer:bm,bn,split,depth;..." forces
+  // the configuration of the stage starting at first_layer.
+  if (const char* env = std::getenv("MAFAT_TUNE")) {
+    std::string e(env);
+    size_t pos = 0;
+    while (pos < e.size()) {
+      size_t end = e.find(';', pos);
+      if (end == std::string::npos) end = e.size();
+      int l, bm, bn, sp, dp;
+      if (std::sscanf(e.substr(pos, end - pos).c_str(), "%d:%d,%d,%d,%d", &l, &bm, &bn, &sp, &dp) == 5 &&
+          l == S.first) {
+        c.bm = bm; c.bn = bn; c.nsplit = sp; c.depth = dp;
+        int64_t mb = 0;
+        for (const TileGeom& T : S.tiles) mb += (static_cast<int64_t>(T.ch) * T.cw + bm - 1) / bm;
+        c.blocks = mb * ((S.cout + bn - 1) / bn);
+      }
+      pos = end + 1;
+    }
+  }
+#endif
+  return c;
+}
+
+WorkspaceLayout workspace_layout(const Group& G, int batch, int dtype) {
+  const size_t esz = (dtype == MAFAT_F32) ? 4 : 2;
+  auto up = [](size_t v) { return (v + 255) & ~static_cast<size_t>(255); };
+  WorkspaceLayout L{};
+  L.scratch = up(static_cast<size_t>(batch) * G.nbufs * G.ntiles * G.scratch_elems * esz);
+  size_t part = 0, cnt = 0;
+  for (const Stage& S : G.stages) {
+    const StageConfig c = choose_config(S, batch, dtype);
+    if (c.kind != K_CONV_MFMA || c.nsplit <= 1) continue;
+    part = std::max(part, static_cast<size_t>(batch) * c.blocks * c.nsplit * c.bm * c.bn * 4);
+    cnt = std::max(cnt, static_cast<size_t>(batch) * c.blocks * 4);
+  }
+  L.partials = up(part);
+  L.counters = up(cnt);
+  L.total = L.scratch + L.partials + L.counters;
+  return L;
+}
+
+namespace {
 
 int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const void* x, void* y,
                    const void* const* w, const float* const* scale, const float* const* bias,
@@ -39,6 +153,7 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
   const size_t esz = (dtype == MAFAT_F32) ? 4 : 2;
   size_t need = 0;
   mafat_workspace_size(plan, batch, dtype, &need);
+  const WorkspaceLayout WL = workspace_layout(G, batch, dtype);
   if (ws_bytes < need)
     return fail(MAFAT_EWORKSPACE, "workspace " + std::to_string(ws_bytes) + " < " + std::to_string(need) + " bytes");
   if (need > 0 && (!ws || (reinterpret_cast<uintptr_t>(ws) & 255u)))
@@ -65,14 +180,21 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
       if (!aligned16(w[l])) return fail(MAFAT_EINVAL, "layer " + std::to_string(l) + ": weights not 16-byte aligned");
     }
 
+  float* partials = reinterpret_cast<float*>(static_cast<char*>(ws) + WL.scratch);
+  uint32_t* counters = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + WL.scratch + WL.partials);
+  if (WL.counters > 0) {
+    const hipError_t e = launch_zero(counters, static_cast<int64_t>(WL.counters / 4), stream);
+    if (e != hipSuccess) return fail(MAFAT_EHIP, std::string("counter reset failed: ") + hipGetErrorString(e));
+  }
   const int ns = static_cast<int>(G.stages.size());
   for (int s = 0; s < ns; ++s) {
     const Stage& S = G.stages[s];
     if (events && events[s] && hipEventRecord(static_cast<hipEvent_t>(events[s]), stream) != hipSuccess)
       return fail(MAFAT_EHIP, "hipEventRecord failed");
-    const int kind = (S.kind == STAGE_POOL) ? K_POOL : (mfma_ok(S, dtype) ? K_CONV_MFMA : K_CONV_DIRECT);
-    const MfmaShape shape = pick_shape(S, dtype);
-    const int bu = block_units(kind, shape);
+    const StageConfig cfg = choose_config(S, batch, dtype);
+    const int kind = cfg.kind;
+    const MfmaShape shape{cfg.bm, cfg.bn, cfg.depth};
+    const int bu = (kind == K_CONV_RGB) ? 256 / (S.cout / 8) : block_units(kind, shape);
     StageArgs A;
     std::memset(&A, 0, sizeof(A));
     A.src = (S.src_buf == BUF_GROUP_IO) ? x : ws;
@@ -88,6 +210,11 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
     A.cin = S.cin; A.cout = S.cout;
     A.act = S.act;
     A.nblk_n = (kind == K_CONV_MFMA) ? (S.cout + shape.bn - 1) / shape.bn : 1;
+    A.nsplit = (kind == K_CONV_MFMA) ? cfg.nsplit : 1;
+    A.partials = partials;
+    A.counters = counters;
+    if (A.nsplit > 1 && G.ntiles > kMaxTilesPerLaunch)
+      return fail(MAFAT_EUNSUPPORTED, "split K with more than one launch chunk");
     for (int t0 = 0; t0 < G.ntiles; t0 += kMaxTilesPerLaunch) {
       const int t1 = std::min(G.ntiles, t0 + kMaxTilesPerLaunch);
       A.ntiles = t1 - t0;
@@ -105,17 +232,35 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
         k.src_off = static_cast<int32_t>(T.src_off);
         k.dst_off = static_cast<int32_t>(T.dst_off);
         int64_t units = static_cast<int64_t>(T.ch) * T.cw;
-        if (kind == K_CONV_DIRECT && S.pool) units /= 4;
+        if ((kind == K_CONV_DIRECT || kind == K_CONV_RGB) && S.pool) units /= 4;
         total += (units + bu - 1) / bu;
         A.mblk_prefix[t - t0 + 1] = static_cast<int32_t>(total);
       }
       A.mblk_total = static_cast<int32_t>(total);
-      const int64_t blocks = total * A.nblk_n * batch;
+      const int64_t blocks = total * A.nblk_n * A.nsplit * batch;
       if (blocks >= (1ll << 31)) return fail(MAFAT_EUNSUPPORTED, "grid too large");
       A.total_blocks = static_cast<int32_t>(blocks);
       const hipError_t e = launch_stage(kind, dtype, S.f, S.pool, shape, A, stream);
       if (e != hipSuccess)
         return fail(MAFAT_EHIP, std::string("stage launch failed: ") + hipGetErrorString(e));
+#ifdef MAFAT_TUNING
+      if (std::getenv("MAFAT_TRACE_DUMP") && kind == K_CONV_MFMA) {
+        long long tr[4][64];
+        hipStreamSynchronize(stream);
+        mafat_debug_trace(&tr[0][0]);
+        std::fprintf(stderr, "TRACE stage %d-%d tile %dx%d split %d depth %d grid %d\n", S.first, S.last,
+                     shape.bm, shape.bn, A.nsplit, shape.depth, A.total_blocks);
+        for (int w = 0; w < 3; ++w) {
+          std::fprintf(stderr, "  wg%d decoded +%lld addr +%lld issued +%lld lstored +%lld barrier +%lld loop +%lld end +%lld steps:", w,
+                       (tr[w][4] - tr[w][0]) * 10, (tr[w][5] - tr[w][0]) * 10, (tr[w][6] - tr[w][0]) * 10,
+                       (tr[w][7] - tr[w][0]) * 10, (tr[w][1] - tr[w][0]) * 10, (tr[w][2] - tr[w][0]) * 10,
+                       (tr[w][3] - tr[w][0]) * 10);
+          for (int k = 8; k < 20; ++k) std::fprintf(stderr, " %lld", (tr[w][k] - tr[w][0]) * 10);
+          std::fprintf(stderr, "\n");
+        }
+        std::fprintf(stderr, "  start spread wg-last minus wg0: %lld ns\n", (tr[1][0] - tr[0][0]) * 10);
+      }
+#endif
     }
   }
   if (events && events[ns] && hipEventRecord(static_cast<hipEvent_t>(events[ns]), stream) != hipSuccess)
