@@ -32,10 +32,9 @@ struct StageArgs {
   int32_t ntiles;
   int32_t nblk_n;       // blocks along output channels
   int32_t mblk_total;   // blocks along pixels, summed over tiles
-  int32_t total_blocks; // batch * mblk_total * nblk_n * nsplit
-  int32_t nsplit;       // K splits per output block (matrix-core kernel)
-  float* partials;      // nsplit > 1: [frame][block][split][BM*BN] fp32 partial sums
-  uint32_t* counters;   // nsplit > 1: [frame][block] arrival counters (zero between uses)
+  int32_t total_blocks; // batch * mblk_total * nblk_n
+  int32_t chan_major;   // 1: blocks ordered channel-block-major (each XCD gets a slice of
+                        //    the weights); 0: pixel-block-major (a slice of the pixels)
   int32_t mblk_prefix[kMaxTilesPerLaunch + 1];
   KTile tiles[kMaxTilesPerLaunch];
 };
@@ -44,13 +43,10 @@ struct StageArgs {
 enum KernelKind { K_CONV_MFMA = 0, K_CONV_DIRECT = 1, K_POOL = 2, K_CONV_RGB = 3 };
 
 // Block shape of the MFMA kernel: output pixels x output channels, and the
-// depth of its load pipeline (2 or 3 stages of 128 bytes of K in flight).
+// depth of its load pipeline (3 to 6 stages of 128 bytes of K in flight).
 struct MfmaShape {
   int bm, bn, depth;
 };
-
-// Zero `n` 32-bit words (the split-K arrival counters) on the stream.
-hipError_t launch_zero(uint32_t* p, int64_t n, hipStream_t stream);
 
 // Launch one stage chunk.  `units_per_block` is what the kernel covers per
 // block along the pixel axis (used to fill mblk_prefix by the caller).

@@ -71,9 +71,11 @@ __device__ __forceinline__ float activate(float v, int act) {
 
 // Workgroups are dispatched round-robin over the 8 XCDs (workgroup b runs
 // on XCD b % 8).  Renumber so that each XCD gets one contiguous range of
-// logical blocks: neighbouring pixel blocks of a tile (which share halo rows)
-// and the channel blocks of one pixel block (which share the input rows)
-// then hit the same L2.
+// logical blocks, which then share that XCD's L2: in pixel-block-major order
+// an XCD owns a band of pixels (and streams all the weights), in
+// channel-block-major order it owns a slice of the output channels (and
+// streams all the input) -- the runtime picks the order with fewer
+// compulsory L2 misses.
 __device__ __forceinline__ int xcd_remap(int bid, int total) {
   constexpr int X = 8;
   const int per = total / X, rem = total % X;
@@ -82,29 +84,52 @@ __device__ __forceinline__ int xcd_remap(int bid, int total) {
 }
 
 struct BlockPos {
-  int frame, tile, mb, nb, ks, blk;  // blk: block index within the frame (mg * nblk_n + nb)
+  int frame, tile, mb, nb;
 };
 
-__device__ __forceinline__ BlockPos decode_block(const StageArgs& a) {
+// Block -> (frame, tile, pixel block, channel block), and the tile's
+// geometry.  The per-tile tables are read with vector loads straight from
+// the kernel argument segment, lane k reading entry k, issued before
+// anything else so they arrive together with the scalar header fields (a
+// dynamic index into the argument block would be a chain of dependent
+// scalar loads).  The tile is then found with a ballot over the block
+// prefix and its fields are taken with readlane.
+__device__ __forceinline__ BlockPos decode_block(const StageArgs& a, KTile* tile) {
+  static_assert(kMaxTilesPerLaunch == 64 && sizeof(KTile) == 28, "one tile per lane of a wave");
+  const int lane = static_cast<int>(threadIdx.x) & 63;
+  // (C-style cast: converts from the constant address space.)
+  const StageArgs* ka = (const StageArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  const int pre = ka->mblk_prefix[lane];
+  const uint32_t* tw = reinterpret_cast<const uint32_t*>(&ka->tiles[lane]);
+  uint32_t w[7];
+#pragma unroll
+  for (int k = 0; k < 7; ++k) w[k] = tw[k];
+
   int bid = xcd_remap(static_cast<int>(blockIdx.x), a.total_blocks);
-  const int per_frame = a.mblk_total * a.nblk_n * a.nsplit;
+  MAFAT_TRACE(60 + (bid < 0 ? 1 : 0));
+  const int per_frame = a.mblk_total * a.nblk_n;
   BlockPos p;
   p.frame = bid / per_frame;
-  bid -= p.frame * per_frame;
-  // splits of one output block are adjacent (same XCD after the remap), then
-  // channel blocks, then pixel blocks
-  const int blk = bid / a.nsplit;
-  p.ks = bid - blk * a.nsplit;
-  p.blk = blk;
-  const int mg = blk / a.nblk_n;
-  p.nb = blk - mg * a.nblk_n;
-  // Tile lookup without a chain of dependent loads: every prefix entry is
-  // read with a constant offset (the loads issue together), then counted.
-  int t = 0;
-#pragma unroll
-  for (int k = 1; k < kMaxTilesPerLaunch; ++k) t += (k < a.ntiles && a.mblk_prefix[k] <= mg) ? 1 : 0;
+  const int blk = bid - p.frame * per_frame;
+  // channel blocks then pixel blocks (or the other way round)
+  int mg;
+  if (a.chan_major) {
+    p.nb = blk / a.mblk_total;
+    mg = blk - p.nb * a.mblk_total;
+  } else {
+    mg = blk / a.nblk_n;
+    p.nb = blk - mg * a.nblk_n;
+  }
+  MAFAT_TRACE(61 + (mg < 0 ? 1 : 0));
+  // Tiles whose first block is at or before mg, not counting tile 0.
+  const int t = __popcll(__builtin_amdgcn_ballot_w64(lane >= 1 && lane < a.ntiles && pre <= mg));
   p.tile = t;
-  p.mb = mg - a.mblk_prefix[t];
+  p.mb = mg - __builtin_amdgcn_readlane(pre, t);
+  uint32_t tw_t[7];
+#pragma unroll
+  for (int k = 0; k < 7; ++k) tw_t[k] = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(w[k]), t));
+  __builtin_memcpy(tile, tw_t, sizeof(KTile));
+  MAFAT_TRACE(62 + (t < 0 ? 1 : 0));
   return p;
 }
 
@@ -147,239 +172,39 @@ __device__ __forceinline__ void mma<MAFAT_F32>(f32x4& c, const u32x4& a, const u
   c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
 }
 
-// Implicit-GEMM convolution, block tile BM pixels x BN channels, 4 waves in
-// a 2x2 arrangement (wave tile BM/2 x BN/2 of 16x16 accumulator tiles).
-//
-// K runs over (tap, channel) in 64-byte sub-chunks (32 bf16 or 16 fp32
-// channels of one filter tap); a pipeline stage holds two sub-chunks
-// (128 bytes of every A and B row).  Each thread issues its 16-byte loads for
-// stage s+DEPTH while the waves run the MFMAs of stage s from LDS, so DEPTH
-// stages are in flight per workgroup; LDS is double buffered with one
-// barrier per stage.  Rows are padded to 144 bytes so the 16-lane fragment
-// reads of consecutive rows hit distinct banks.
-//
-// Epilogue: scale, bias, activation, the optional 2x2 max (the 4 accumulator
-// rows a lane holds are one pool window), rounding to the output type, then
-// the block's output tile is transposed through LDS and written with 16-byte
-// stores along channels.
-//
-// Requires c_in % (64 / sizeof(T)) == 0 and c_out % 16 == 0 (host-checked).
-template <int DT, int F, int BM, int BN, bool POOL, int DEPTH>
-__global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
-  using T = typename Elt<DT>::T;
-  constexpr int P = (F - 1) / 2;
-  constexpr int KC = 64 / static_cast<int>(sizeof(T));   // channels per sub-chunk
-  constexpr int EPV = 16 / static_cast<int>(sizeof(T));  // channels per 16 bytes
-  constexpr int ROWQ = 9;                                 // u32x4 per LDS row
-  constexpr int ALD = BM / 32, BLD = BN / 32;             // loads per thread per stage
-  constexpr int WM = BM / 2, WN = BN / 2, MT = WM / 16, NT = WN / 16;
-  static_assert(DEPTH >= 2 && DEPTH <= 6, "pipeline depth");
-  constexpr int OPND_BYTES = 2 * (BM + BN) * ROWQ * 16;
-  constexpr int OROWS = POOL ? BM / 4 : BM;
-  constexpr int OROW_BYTES = BN * static_cast<int>(sizeof(T)) + 16;
-  constexpr int OUT_BYTES = OROWS * OROW_BYTES;
-  constexpr int SMEM = OPND_BYTES > OUT_BYTES ? OPND_BYTES : OUT_BYTES;
-  __shared__ __align__(16) unsigned char smem[SMEM];
-  u32x4* sA = reinterpret_cast<u32x4*>(smem);                 // [2][BM][ROWQ]
-  u32x4* sB = sA + 2 * BM * ROWQ;                             // [2][BN][ROWQ]
+// 16-byte load through a buffer descriptor.  The hardware range check returns
+// zero for a byte offset at or past the descriptor's size, which the matrix-core
+// kernel uses for its zero padding: an operand that must read as
+// zero gets bit 31 set in its offset (sizes stay below 2^31 bytes).
+__device__ __forceinline__ u32x4 buf_load16(__amdgpu_buffer_rsrc_t r, unsigned off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, 0));
+}
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, unsigned bytes) {
+  // Word 3: 32-bit data format (required non-zero for untyped loads).
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), 0x00020000);
+}
 
-  MAFAT_TRACE(0);
-  const BlockPos bp = decode_block(a);
-  const KTile tl = a.tiles[bp.tile];
+// Epilogue of the matrix-core kernels for a BM x BN block computed by 4
+// waves in a 2x2 arrangement: scale, bias, activation, the optional 2x2 max
+// (the 4 accumulator rows a lane holds are one pool window), rounding to the
+// output type; the block is then transposed through LDS (`smem`, at least
+// OROWS * (BN * sizeof(T) + 16) bytes, free for use) and written with
+// 16-byte stores along channels.  Lane l holds rows 4*(l/16) .. +3 of each
+// 16x16 accumulator tile, column l % 16.
+template <int DT, int BM, int BN, bool POOL>
+__device__ __forceinline__ void store_block(const f32x4 (&acc)[BM / 32][BN / 32],
+                                            unsigned char* smem, const StageArgs& a,
+                                            const KTile& tl, int m0, int n0,
+                                            typename Elt<DT>::T* dst) {
+  using T = typename Elt<DT>::T;
+  constexpr int EPV = 16 / static_cast<int>(sizeof(T));
+  constexpr int WM = BM / 2, WN = BN / 2, MT = WM / 16, NT = WN / 16;
+  constexpr int OROWS = POOL ? BM / 4 : BM;
+  constexpr int OSTRIDE = (BN * static_cast<int>(sizeof(T)) + 16) / static_cast<int>(sizeof(T));
   const int tid = static_cast<int>(threadIdx.x), lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
-  MAFAT_TRACE(4 + (tl.ch > 30000 ? 1 : 0));
-  const int M = tl.ch * tl.cw;
-  const int m0 = bp.mb * BM, n0 = bp.nb * BN;
-  const int cin = a.cin, cout = a.cout;
-  const T* src = static_cast<const T*>(a.src) + bp.frame * a.src_fstride + tl.src_off;
-  T* dst = static_cast<T*>(a.dst) + bp.frame * a.dst_fstride + tl.dst_off;
-  const T* wgt = static_cast<const T*>(a.w);
-  const int K = F * F * cin;
-  const int cblocks = cin / KC;
-  const int nsub_all = F * F * cblocks;  // 64-byte sub-chunks along K
-  const int nstage_all = (nsub_all + 1) >> 1;
-  // This block's share of K: stages [st0, st0 + nstage) of 128 bytes.
-  const int sps = (nstage_all + a.nsplit - 1) / a.nsplit;
-  const int st0 = bp.ks * sps;
-  const int nstage = min(nstage_all, st0 + sps) - st0;
-  const int nsub = min(nsub_all, 2 * (st0 + nstage));  // sub-chunks at or past this are zero
-
-  // This thread stages rows r0 + 32 i, 16-byte piece `pc` of sub-chunk `hh`.
-  // Per A row: the element offset of its pixel in the source buffer and a
-  // mask of the filter taps that land inside the image (zero padding).
-  const int r0 = tid >> 3, q = tid & 7, hh = q >> 2, pc = q & 3;
-  int a_base[ALD];
-  unsigned a_taps[ALD];
-#pragma unroll
-  for (int i = 0; i < ALD; ++i) {
-    const int m = m0 + r0 + 32 * i;
-    int oy, ox;
-    row_pixel<POOL>(tl, m < M ? m : 0, &oy, &ox);
-    a_base[i] = ((oy - tl.sy0) * tl.sw + (ox - tl.sx0)) * cin + pc * EPV;
-    unsigned mask = 0;
-#pragma unroll
-    for (int t = 0; t < F * F; ++t) {
-      const int iy = oy + t / F - P, ix = ox + t % F - P;
-      const bool in = static_cast<unsigned>(iy) < static_cast<unsigned>(a.in_h) &&
-                      static_cast<unsigned>(ix) < static_cast<unsigned>(a.in_w);
-      mask |= in ? (1u << t) : 0u;
-    }
-    a_taps[i] = (m < M) ? mask : 0u;
-  }
-  int b_off[BLD];
-  bool b_ok[BLD];
-#pragma unroll
-  for (int i = 0; i < BLD; ++i) {
-    const int co = n0 + r0 + 32 * i;
-    b_ok[i] = co < cout;
-    b_off[i] = (b_ok[i] ? co : 0) * K + pc * EPV;
-  }
-
-  u32x4 ra[DEPTH][ALD], rb[DEPTH][BLD];
-  unsigned okm[DEPTH];  // bit i: A load i valid; bit ALD + i: B load i valid
-  // Load cursor: filter tap and channel block of the first sub-chunk of the
-  // next stage to load (uniform across the workgroup); advanced by two
-  // sub-chunks per load.
-  int lc_kc = 2 * st0, lc_tap = lc_kc / cblocks, lc_cb = lc_kc - lc_tap * cblocks;
-  // Global -> registers, next stage into register set d_.  Every load is
-  // issued unconditionally from a clamped, valid address; invalid ones are
-  // zeroed when the set is written to LDS.  (Zeroing here, or a guarded
-  // load, would make the compiler wait for the load right away and nothing
-  // would stay in flight.)
-#define MAFAT_GLOAD(d_)                                                                        \
-  do {                                                                                         \
-    const int tap1_ = (lc_cb + 1 < cblocks) ? lc_tap : lc_tap + 1;                             \
-    const int cb1_ = (lc_cb + 1 < cblocks) ? lc_cb + 1 : lc_cb + 1 - cblocks;                  \
-    const int tap_ = hh ? tap1_ : lc_tap, cb_ = hh ? cb1_ : lc_cb;                             \
-    const bool kok_ = lc_kc + hh < nsub;                                                       \
-    const int ky_ = tap_ / F, kx_ = tap_ - ky_ * F;                                            \
-    const int aoff_ = ((ky_ - P) * tl.sw + (kx_ - P)) * cin + cb_ * KC;                       \
-    const int boff_ = tap_ * cin + cb_ * KC;                                                   \
-    unsigned m_ = 0;                                                                           \
-    _Pragma("unroll") for (int i = 0; i < ALD; ++i) {                                          \
-      const bool ok = kok_ && ((a_taps[i] >> tap_) & 1u);                                      \
-      m_ |= ok ? (1u << i) : 0u;                                                               \
-      ra[d_][i] = *reinterpret_cast<const u32x4*>(src + (ok ? a_base[i] + aoff_ : 0));         \
-    }                                                                                          \
-    _Pragma("unroll") for (int i = 0; i < BLD; ++i) {                                          \
-      const bool ok = kok_ && b_ok[i];                                                         \
-      m_ |= ok ? (1u << (ALD + i)) : 0u;                                                       \
-      rb[d_][i] = *reinterpret_cast<const u32x4*>(wgt + (ok ? b_off[i] + boff_ : 0));         \
-    }                                                                                          \
-    okm[d_] = m_;                                                                              \
-    lc_kc += 2;                                                                                \
-    lc_cb += 2;                                                                                \
-    while (lc_cb >= cblocks) { lc_cb -= cblocks; ++lc_tap; }                                   \
-  } while (0)
-  // Registers (set d_) -> LDS buffer buf_, zeroing the invalid loads.
-#define MAFAT_LSTORE(d_, buf_)                                                                     \
-  do {                                                                                             \
-    _Pragma("unroll") for (int i = 0; i < ALD; ++i)                                                \
-      sA[((buf_) * BM + r0 + 32 * i) * ROWQ + q] = ra[d_][i] & ((okm[d_] >> i) & 1u ? ~0u : 0u);   \
-    _Pragma("unroll") for (int i = 0; i < BLD; ++i)                                                \
-      sB[((buf_) * BN + r0 + 32 * i) * ROWQ + q] =                                                 \
-          rb[d_][i] & ((okm[d_] >> (ALD + i)) & 1u ? ~0u : 0u);                                     \
-  } while (0)
-
-  f32x4 acc[MT][NT];
-#pragma unroll
-  for (int i = 0; i < MT; ++i)
-#pragma unroll
-    for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // The stage count is padded to a multiple of DEPTH so that the loop body
-  // has no branches: padded stages load from a valid address, are masked to
-  // zero and add nothing.  (Branches around the loads would create joins
-  // at which the compiler waits for every outstanding load.)
-  const int nst_pad = (nstage + DEPTH - 1) / DEPTH * DEPTH;
-  MAFAT_TRACE(5);
-  MAFAT_GLOAD(0);
-  MAFAT_GLOAD(1);
-  if constexpr (DEPTH >= 3) MAFAT_GLOAD(2);
-  if constexpr (DEPTH >= 4) MAFAT_GLOAD(3);
-  if constexpr (DEPTH >= 5) MAFAT_GLOAD(4);
-  if constexpr (DEPTH >= 6) MAFAT_GLOAD(5);
-  MAFAT_TRACE(6);
-  MAFAT_LSTORE(0, 0);
-  MAFAT_TRACE(7);
-  __syncthreads();
-  MAFAT_TRACE(1);
-  // One pipeline step on stage s0 + d_, held in LDS buffer (s0 + d_) & 1:
-  // issue the loads of stage s0 + d_ + DEPTH into register set d_ (written
-  // to LDS in the previous step), run the MFMAs, write register set dn_
-  // (stage s0 + d_ + 1) to the other LDS buffer, barrier.
-#define MAFAT_STEP(d_, dn_)                                                                      \
-  do {                                                                                           \
-    const int st = s0 + (d_);                                                                    \
-    const int buf = st & 1;                                                                      \
-    MAFAT_GLOAD(d_);                                                                             \
-    _Pragma("unroll") for (int h = 0; h < 2; ++h) {                                              \
-      u32x4 af[MT], bfr[NT];                                                                     \
-      _Pragma("unroll") for (int i = 0; i < MT; ++i)                                             \
-        af[i] = sA[(buf * BM + wm * WM + i * 16 + (lane & 15)) * ROWQ + h * 4 + (lane >> 4)];     \
-      _Pragma("unroll") for (int j = 0; j < NT; ++j)                                             \
-        bfr[j] = sB[(buf * BN + wn * WN + j * 16 + (lane & 15)) * ROWQ + h * 4 + (lane >> 4)];    \
-      _Pragma("unroll") for (int i = 0; i < MT; ++i)                                             \
-        _Pragma("unroll") for (int j = 0; j < NT; ++j) mma<DT>(acc[i][j], af[i], bfr[j]);        \
-    }                                                                                            \
-    MAFAT_LSTORE(dn_, buf ^ 1);                                                                  \
-    __syncthreads();                                                                             \
-    MAFAT_TRACE(8 + st);                                                                         \
-  } while (0)
-  for (int s0 = 0; s0 < nst_pad; s0 += DEPTH) {
-    if constexpr (DEPTH == 2) {
-      MAFAT_STEP(0, 1); MAFAT_STEP(1, 0);
-    } else if constexpr (DEPTH == 3) {
-      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 0);
-    } else if constexpr (DEPTH == 4) {
-      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 3); MAFAT_STEP(3, 0);
-    } else if constexpr (DEPTH == 5) {
-      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 3); MAFAT_STEP(3, 4); MAFAT_STEP(4, 0);
-    } else {
-      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 3); MAFAT_STEP(3, 4); MAFAT_STEP(4, 5);
-      MAFAT_STEP(5, 0);
-    }
-  }
-#undef MAFAT_STEP
-#undef MAFAT_GLOAD
-#undef MAFAT_LSTORE
-
-  MAFAT_TRACE(2);
-  // Split K: every block writes its partial sums; the last of the nsplit
-  // blocks of an output tile to arrive adds them in split order (the same
-  // order whatever the arrival order, so results are reproducible) and runs
-  // the epilogue; it also resets the counter for the next use.
-  if (a.nsplit > 1) {
-    __shared__ uint32_t s_arrival;
-    const int64_t bidx = static_cast<int64_t>(bp.frame) * (a.mblk_total * a.nblk_n) + bp.blk;
-    f32x4* part = reinterpret_cast<f32x4*>(a.partials) + bidx * a.nsplit * (MT * NT * 256);
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int j = 0; j < NT; ++j) part[(bp.ks * MT * NT + i * NT + j) * 256 + tid] = acc[i][j];
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) s_arrival = atomicAdd(&a.counters[bidx], 1u);
-    __syncthreads();
-    if (s_arrival != static_cast<uint32_t>(a.nsplit - 1)) return;
-    __threadfence();
-#pragma unroll
-    for (int i = 0; i < MT; ++i)
-#pragma unroll
-      for (int j = 0; j < NT; ++j) {
-        f32x4 sum = f32x4{0.f, 0.f, 0.f, 0.f};
-        for (int k = 0; k < a.nsplit; ++k)
-          sum += (k == bp.ks) ? acc[i][j] : part[(k * MT * NT + i * NT + j) * 256 + tid];
-        acc[i][j] = sum;
-      }
-    if (tid == 0) atomicExch(&a.counters[bidx], 0u);
-  }
-
-  // Epilogue.  Lane holds rows 4*(lane/16) .. +3 of each 16x16 accumulator
-  // tile, column lane % 16.  Results go to LDS as [output row][channel].
+  const int M = tl.ch * tl.cw, cout = a.cout;
   T* sO = reinterpret_cast<T*>(smem);
-  constexpr int OSTRIDE = OROW_BYTES / static_cast<int>(sizeof(T));
   const int rq = (lane >> 4) * 4;
 #pragma unroll
   for (int j = 0; j < NT; ++j) {
@@ -420,8 +245,204 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
     *reinterpret_cast<u32x4*>(dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * cout + co) =
         *reinterpret_cast<const u32x4*>(sO + row * OSTRIDE + piece * EPV);
   }
+}
+
+// Implicit-GEMM convolution, block tile BM pixels x BN channels, 4 waves in
+// a 2x2 arrangement (wave tile BM/2 x BN/2 of 16x16 accumulator tiles).
+//
+// K runs over (tap, channel) in 64-byte sub-chunks (32 bf16 or 16 fp32
+// channels of one filter tap); a pipeline stage holds two sub-chunks
+// (128 bytes of every A and B row).  Each thread issues its 16-byte loads for
+// stage s+DEPTH while the waves run the MFMAs of stage s from LDS, so DEPTH
+// stages are in flight per workgroup; LDS is double buffered with one
+// barrier per stage.  Rows are padded to 144 bytes so the 16-lane fragment
+// reads of consecutive rows hit distinct banks.
+//
+// Operands are read through buffer descriptors with 32-bit byte offsets:
+// the zero padding of the convolution (taps outside the image), padded
+// sub-chunks past the last tap and weight rows past c_out all read as zero
+// through the descriptor's range check, so the loop has no masking work.
+//
+// Epilogue: see store_block.
+//
+// Requires c_in % (64 / sizeof(T)) == 0, c_out % 16 == 0 and byte offsets
+// below 2^31 within a frame's source buffer and the weights (host-checked).
+template <int DT, int F, int BM, int BN, bool POOL, int DEPTH>
+__global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
+  using T = typename Elt<DT>::T;
+  constexpr int ESZ = static_cast<int>(sizeof(T));
+  constexpr int P = (F - 1) / 2;
+  constexpr int KC = 64 / ESZ;   // channels per sub-chunk
+  constexpr int EPV = 16 / ESZ;  // channels per 16 bytes
+  constexpr int ROWQ = 9;        // u32x4 per LDS row
+  constexpr int ALD = BM / 32, BLD = BN / 32;  // loads per thread per stage
+  constexpr int WM = BM / 2, WN = BN / 2, MT = WM / 16, NT = WN / 16;
+  static_assert(DEPTH >= 3 && DEPTH <= 6, "pipeline depth");
+  static_assert(F * F + 2 * DEPTH + 2 < 32, "tap mask width (taps of computed stages)");
+  constexpr int NBUF = 2;  // LDS stage buffers
+  constexpr int OPND_BYTES = NBUF * (BM + BN) * ROWQ * 16;
+  constexpr int OROWS = POOL ? BM / 4 : BM;
+  constexpr int OUT_BYTES = OROWS * (BN * ESZ + 16);
+  constexpr int SMEM = OPND_BYTES > OUT_BYTES ? OPND_BYTES : OUT_BYTES;
+  __shared__ __align__(16) unsigned char smem[SMEM];
+  u32x4* sA = reinterpret_cast<u32x4*>(smem);  // [NBUF][BM][ROWQ]
+  u32x4* sB = sA + NBUF * BM * ROWQ;           // [NBUF][BN][ROWQ]
+
+  MAFAT_TRACE(0);
+  KTile tl;
+  const BlockPos bp = decode_block(a, &tl);
+  const int tid = static_cast<int>(threadIdx.x), lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  MAFAT_TRACE(4 + (tl.ch > 30000 ? 1 : 0));
+  const int M = tl.ch * tl.cw;
+  const int m0 = bp.mb * BM, n0 = bp.nb * BN;
+  const int cin = a.cin, cout = a.cout, sw = tl.sw;
+  const int64_t sbase = bp.frame * a.src_fstride + tl.src_off;
+  T* dst = static_cast<T*>(a.dst) + bp.frame * a.dst_fstride + tl.dst_off;
+  const int K = F * F * cin;
+  const int cblocks = cin / KC;
+  const int nsub = F * F * cblocks;    // 64-byte sub-chunks along K
+  const int nstage = (nsub + 1) >> 1;  // 128-byte stages
+  const __amdgpu_buffer_rsrc_t rsa =
+      make_rsrc(static_cast<const T*>(a.src) + sbase, static_cast<unsigned>((a.src_fstride - tl.src_off) * ESZ));
+  const __amdgpu_buffer_rsrc_t rsb = make_rsrc(a.w, static_cast<unsigned>(cout * K * ESZ));
+
+  // This thread stages rows r0 + 32 i, 16-byte piece `pc` of sub-chunk `hh`
+  // of every stage.  Per A row: the byte offset of its pixel in the source
+  // buffer and a mask of the filter taps that read zero (outside the image;
+  // bits past the last tap are set, so padded sub-chunks read zero).  Loads
+  // that must read zero get bit 31 set in their offset.
+  const int r0 = tid >> 3, q = tid & 7, hh = q >> 2, pc = q & 3;
+  unsigned a_off[ALD], a_inv[ALD], b_off[BLD];
+#pragma unroll
+  for (int i = 0; i < ALD; ++i) {
+    const int m = m0 + r0 + 32 * i;
+    int oy, ox;
+    row_pixel<POOL>(tl, m < M ? m : 0, &oy, &ox);
+    a_off[i] = static_cast<unsigned>((((oy - tl.sy0) * sw + (ox - tl.sx0)) * cin + pc * EPV) * ESZ);
+    unsigned inv = ~0u << (F * F);
+#pragma unroll
+    for (int t = 0; t < F * F; ++t) {
+      const int iy = oy + t / F - P, ix = ox + t % F - P;
+      const bool in = static_cast<unsigned>(iy) < static_cast<unsigned>(a.in_h) &&
+                      static_cast<unsigned>(ix) < static_cast<unsigned>(a.in_w);
+      inv |= in ? 0u : (1u << t);
+    }
+    a_inv[i] = (m < M) ? inv : ~0u;
+  }
+#pragma unroll
+  for (int i = 0; i < BLD; ++i) {
+    const int co = n0 + r0 + 32 * i;
+    b_off[i] = co < cout ? static_cast<unsigned>((co * K + pc * EPV) * ESZ) : 0x80000000u;
+  }
+
+  u32x4 ra[DEPTH][ALD], rb[DEPTH][BLD];
+  // Load cursor (uniform): filter tap and channel block of the first
+  // sub-chunk of the next stage to load, advanced by two sub-chunks per load
+  // (readfirstlane keeps its arithmetic on the scalar unit).  Padded
+  // sub-chunks (tap past the last) re-read the last tap's weights, which
+  // meet zero A rows.
+  int lc_tap = 0, lc_cb = 0;
+#define MAFAT_GLOAD(d_)                                                                        \
+  do {                                                                                         \
+    const int tap0_ = __builtin_amdgcn_readfirstlane(lc_tap);                                  \
+    const int cb0_ = __builtin_amdgcn_readfirstlane(lc_cb);                                    \
+    const int w0_ = (cblocks - 2 - cb0_) >> 31; /* -1: the next sub-chunk starts a new tap */  \
+    const int tap1_ = tap0_ - w0_, cb1_ = (cb0_ + 1) & ~w0_;                                   \
+    const int w1_ = (cblocks - 2 - cb1_) >> 31;                                                \
+    const int ky0_ = tap0_ / F, kx0_ = tap0_ - ky0_ * F;                                       \
+    const int ky1_ = tap1_ / F, kx1_ = tap1_ - ky1_ * F;                                       \
+    const int ao0_ = (((ky0_ - P) * sw + (kx0_ - P)) * cin + cb0_ * KC) * ESZ;                 \
+    const int ao1_ = (((ky1_ - P) * sw + (kx1_ - P)) * cin + cb1_ * KC) * ESZ;                 \
+    const int bo0_ = (min(tap0_, F * F - 1) * cin + cb0_ * KC) * ESZ;                          \
+    const int bo1_ = (min(tap1_, F * F - 1) * cin + cb1_ * KC) * ESZ;                          \
+    const int t0c_ = min(tap0_, 31), t1c_ = min(tap1_, 31);                                    \
+    const unsigned tap_ = static_cast<unsigned>(hh ? t1c_ : t0c_);                             \
+    const unsigned aoff_ = static_cast<unsigned>(hh ? ao1_ : ao0_);                            \
+    const unsigned boff_ = static_cast<unsigned>(hh ? bo1_ : bo0_);                            \
+    _Pragma("unroll") for (int i = 0; i < ALD; ++i) {                                          \
+      const unsigned bad_ = (a_inv[i] >> tap_) & 1u;                                           \
+      ra[d_][i] = buf_load16(rsa, (a_off[i] + aoff_) | (bad_ << 31));                         \
+    }                                                                                          \
+    _Pragma("unroll") for (int i = 0; i < BLD; ++i) rb[d_][i] = buf_load16(rsb, b_off[i] + boff_); \
+    lc_tap = tap1_ - w1_;                                                                      \
+    lc_cb = (cb1_ + 1) & ~w1_;                                                                 \
+  } while (0)
+  // Registers (set d_) -> LDS buffer buf_.
+#define MAFAT_LSTORE(d_, buf_)                                                                 \
+  do {                                                                                         \
+    _Pragma("unroll") for (int i = 0; i < ALD; ++i)                                            \
+      sA[((buf_) * BM + r0 + 32 * i) * ROWQ + q] = ra[d_][i];                                  \
+    _Pragma("unroll") for (int i = 0; i < BLD; ++i)                                            \
+      sB[((buf_) * BN + r0 + 32 * i) * ROWQ + q] = rb[d_][i];                                  \
+  } while (0)
+
+  f32x4 acc[MT][NT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // Pipeline, per step st (computing stage st from LDS buffer st % 2):
+  //   barrier (stage st is in LDS; every wave is done reading stage st - 1);
+  //   read both K-halves' fragments of stage st; issue the global loads of
+  //   stage st + DEPTH into the register set stage st came from; MFMAs;
+  //   write stage st + 1 (loaded DEPTH - 1 steps ago) to the other buffer.
+  // The stage count is padded to a multiple of DEPTH so the loop body has no
+  // branches (padded stages read zero A rows).
+  const int nst_pad = (nstage + DEPTH - 1) / DEPTH * DEPTH;
+  MAFAT_TRACE(5);
+  MAFAT_GLOAD(0);
+  MAFAT_GLOAD(1);
+  MAFAT_GLOAD(2);
+  if constexpr (DEPTH >= 4) MAFAT_GLOAD(3);
+  if constexpr (DEPTH >= 5) MAFAT_GLOAD(4);
+  if constexpr (DEPTH >= 6) MAFAT_GLOAD(5);
+  MAFAT_TRACE(6);
+  MAFAT_LSTORE(0, 0);
+  MAFAT_TRACE(7);
+  int rbuf = 0;   // LDS buffer holding stage st
+#define MAFAT_STEP(d_, dn_)                                                                      \
+  do {                                                                                           \
+    __syncthreads();                                                                             \
+    u32x4 af[2][MT], bfr[2][NT];                                                                 \
+    _Pragma("unroll") for (int h = 0; h < 2; ++h) {                                              \
+      _Pragma("unroll") for (int i = 0; i < MT; ++i)                                             \
+        af[h][i] = sA[(rbuf * BM + wm * WM + i * 16 + (lane & 15)) * ROWQ + h * 4 + (lane >> 4)]; \
+      _Pragma("unroll") for (int j = 0; j < NT; ++j)                                             \
+        bfr[h][j] = sB[(rbuf * BN + wn * WN + j * 16 + (lane & 15)) * ROWQ + h * 4 + (lane >> 4)]; \
+    }                                                                                            \
+    MAFAT_GLOAD(d_);                                                                             \
+    _Pragma("unroll") for (int h = 0; h < 2; ++h)                                                \
+      _Pragma("unroll") for (int i = 0; i < MT; ++i)                                             \
+        _Pragma("unroll") for (int j = 0; j < NT; ++j) mma<DT>(acc[i][j], af[h][i], bfr[h][j]);  \
+    rbuf ^= 1;                                                                                   \
+    MAFAT_LSTORE(dn_, rbuf);                                                                     \
+    MAFAT_TRACE(8 + s0 + (d_));                                                                  \
+  } while (0)
+  for (int s0 = 0; s0 < nst_pad; s0 += DEPTH) {
+    if constexpr (DEPTH == 3) {
+      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 0);
+    } else if constexpr (DEPTH == 4) {
+      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 3); MAFAT_STEP(3, 0);
+    } else if constexpr (DEPTH == 5) {
+      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 3); MAFAT_STEP(3, 4); MAFAT_STEP(4, 0);
+    } else {
+      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 3); MAFAT_STEP(3, 4); MAFAT_STEP(4, 5);
+      MAFAT_STEP(5, 0);
+    }
+  }
+  MAFAT_TRACE(1);
+  __syncthreads();
+#undef MAFAT_STEP
+#undef MAFAT_GLOAD
+#undef MAFAT_LSTORE
+
+  MAFAT_TRACE(2);
+  store_block<DT, BM, BN, POOL>(acc, smem, a, tl, m0, n0, dst);
   MAFAT_TRACE(3);
 }
+
 
 // Direct convolution on the vector ALUs, one thread per output pixel (or per
 // 2x2 pool window), all output channels in chunks of 8.  Weights are read
@@ -432,8 +453,8 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const StageArgs a) {
   constexpr int P = (F - 1) / 2;
   constexpr int NP = POOL ? 4 : 1;
   constexpr int CO = 8;
-  const BlockPos bp = decode_block(a);
-  const KTile tl = a.tiles[bp.tile];
+  KTile tl;
+  const BlockPos bp = decode_block(a, &tl);
   const int units = POOL ? (tl.ch >> 1) * (tl.cw >> 1) : tl.ch * tl.cw;
   const int u = bp.mb * 256 + static_cast<int>(threadIdx.x);
   if (u >= units) return;
@@ -532,8 +553,8 @@ void conv_rgb_kernel(const StageArgs a) {
   }
   __syncthreads();
 
-  const BlockPos bp = decode_block(a);
-  const KTile tl = a.tiles[bp.tile];
+  KTile tl;
+  const BlockPos bp = decode_block(a, &tl);
   const int units = POOL ? (tl.ch >> 1) * (tl.cw >> 1) : tl.ch * tl.cw;
   const int per_block = 256 / cg_n;
   const int u = bp.mb * per_block + static_cast<int>(threadIdx.x) / cg_n;
@@ -635,8 +656,8 @@ void conv_rgb_kernel(const StageArgs a) {
 template <int DT>
 __global__ __launch_bounds__(256) void pool_kernel(const StageArgs a) {
   using T = typename Elt<DT>::T;
-  const BlockPos bp = decode_block(a);
-  const KTile tl = a.tiles[bp.tile];
+  KTile tl;
+  const BlockPos bp = decode_block(a, &tl);
   const int u = bp.mb * 64 + (static_cast<int>(threadIdx.x) >> 2);
   if (u >= tl.ch * tl.cw) return;
   const int yy = u / tl.cw;
@@ -681,7 +702,6 @@ hipError_t launch_conv(int kind, MfmaShape sh, const StageArgs& args, hipStream_
     return hipGetLastError();
   }
   switch (sh.depth) {
-    case 2: return launch_mfma<DT, F, POOL, 2>(sh, args, stream);
     case 3: return launch_mfma<DT, F, POOL, 3>(sh, args, stream);
     case 4: return launch_mfma<DT, F, POOL, 4>(sh, args, stream);
     case 5: return launch_mfma<DT, F, POOL, 5>(sh, args, stream);
@@ -705,11 +725,6 @@ hipError_t launch_dt(int kind, int f, bool pool, MfmaShape sh, const StageArgs& 
   return hipErrorInvalidValue;
 }
 
-__global__ __launch_bounds__(256) void zero_kernel(uint32_t* p, int64_t n) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (i < n) p[i] = 0u;
-}
-
 }  // namespace
 
 #ifdef MAFAT_TUNING
@@ -717,12 +732,6 @@ extern "C" int mafat_debug_trace(long long* host_out) {
   return hipMemcpyFromSymbol(host_out, HIP_SYMBOL(g_trace), sizeof(g_trace)) == hipSuccess ? 0 : -1;
 }
 #endif
-
-hipError_t launch_zero(uint32_t* p, int64_t n, hipStream_t stream) {
-  if (n <= 0) return hipSuccess;
-  hipLaunchKernelGGL(zero_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, p, n);
-  return hipGetLastError();
-}
 
 int block_units(int kind, MfmaShape shape) {
   if (kind == K_CONV_MFMA) return shape.bm;

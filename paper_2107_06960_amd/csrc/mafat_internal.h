@@ -74,15 +74,15 @@ namespace mafat {
 struct StageConfig {
   int kind;          // KernelKind
   int bm, bn, depth; // matrix-core kernel block tile and pipeline depth
-  int nsplit;        // K splits per output block
+  int chan_major;    // block order (see StageArgs::chan_major)
   int64_t blocks;    // output blocks per frame (pixel blocks x channel blocks)
 };
 StageConfig choose_config(const Stage& S, int batch, int dtype);
 
-// Workspace layout for one group: [scratch][partials][counters], each part
-// 256-byte aligned.  Sizes in bytes.
+// Workspace layout for one group: the ping-pong scratch buffers of every
+// tile of every frame, 256-byte aligned.  Sizes in bytes.
 struct WorkspaceLayout {
-  size_t scratch, partials, counters, total;
+  size_t scratch, total;
 };
 WorkspaceLayout workspace_layout(const Group& G, int batch, int dtype);
 

@@ -28,10 +28,14 @@ int fail(int status, const std::string& msg) {
 }
 
 // The matrix-core kernel needs whole 64-byte K chunks (32 bf16 or 16 fp32
-// input channels) and output channels in multiples of 16.
+// input channels), output channels in multiples of 16, and its weights
+// addressable with 32-bit byte offsets (the source buffer is checked per
+// launch).
 bool mfma_ok(const Stage& S, int dtype) {
   const int kc = (dtype == MAFAT_BF16) ? 32 : 16;
-  return S.kind == STAGE_CONV && S.cin % kc == 0 && S.cout % 16 == 0;
+  const int64_t esz = (dtype == MAFAT_BF16) ? 2 : 4;
+  return S.kind == STAGE_CONV && S.cin % kc == 0 && S.cout % 16 == 0 &&
+         static_cast<int64_t>(S.cout) * S.f * S.f * S.cin * esz < (1ll << 31);
 }
 
 // The vector first-layer kernel: 3 input channels, 3x3, 8/16/32/64 outputs.
@@ -40,18 +44,46 @@ bool rgb_ok(const Stage& S) {
          (S.cout == 8 || S.cout == 16 || S.cout == 32 || S.cout == 64);
 }
 
+// Tuning builds only: MAFAT_TUNE="first_layer:bm,bn,depth[,chan_major[,kind]];..."
+// forces the configuration of the stage starting at first_layer.
+StageConfig tune_override(const Stage& S, StageConfig c) {
+#ifdef MAFAT_TUNING
+  if (const char* env = std::getenv("MAFAT_TUNE")) {
+    std::string e(env);
+    size_t pos = 0;
+    while (pos < e.size()) {
+      size_t end = e.find(';', pos);
+      if (end == std::string::npos) end = e.size();
+      int l, bm, bn, dp, cm = -1, kd = -1;
+      const int got = std::sscanf(e.substr(pos, end - pos).c_str(), "%d:%d,%d,%d,%d,%d", &l, &bm, &bn, &dp,
+                                  &cm, &kd);
+      if (got >= 4 && l == S.first) {
+        c.bm = bm; c.bn = bn; c.depth = dp;
+        if (cm >= 0) c.chan_major = cm;
+        if (kd >= 0) c.kind = kd;
+        int64_t mb = 0;
+        for (const TileGeom& T : S.tiles) mb += (static_cast<int64_t>(T.ch) * T.cw + bm - 1) / bm;
+        c.blocks = mb * ((S.cout + bn - 1) / bn);
+      }
+      pos = end + 1;
+    }
+  }
+#else
+  (void)S;
+#endif
+  return c;
+}
+
 }  // namespace
 
-// Block tile, split count and pipeline depth for the matrix-core kernel,
-// from a small time model of one CU: a workgroup costs a fixed ~2 us
-// (first loads, epilogue) plus the larger of its MFMA time at the CU's
-// peak (4096 flop/clock) and its operand traffic at the CU's L2 bandwidth
-// (64 bytes/clock); workgroups beyond 256 queue on the CUs; a split adds
-// one reduction pass over the partial sums.  Larger tiles re-read fewer
-// operands; splitting K restores parallelism when there are few tiles.
+// Block tile and pipeline depth for the matrix-core kernel, from a small
+// time model of one CU: a workgroup costs a fixed ~2 us (first loads,
+// epilogue) plus the larger of its MFMA time at the CU's peak (4096
+// flop/clock) and its operand traffic at the CU's L2 bandwidth (64
+// bytes/clock); workgroups beyond 256 queue on the CUs.  Larger tiles
+// re-read fewer operands, smaller ones give more workgroups.
 StageConfig choose_config(const Stage& S, int batch, int dtype) {
   StageConfig c{};
-  c.nsplit = 1;
   c.bm = 64; c.bn = 64; c.depth = 3;
   if (S.kind == STAGE_POOL) { c.kind = K_POOL; return c; }
   if (!mfma_ok(S, dtype)) {
@@ -72,75 +104,46 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
     int64_t mb = 0;
     for (const TileGeom& T : S.tiles) mb += (static_cast<int64_t>(T.ch) * T.cw + bm - 1) / bm;
     const int64_t blocks = mb * ((S.cout + bn - 1) / bn);
-    // Split K is off: combining partial sums across workgroups needs a
-    // device-scope fence, which writes back and invalidates the XCD's whole
-    // L2 and stalls every other workgroup on it (measured: 2.7x slower
-    // at two splits).
-    for (int split = 1; split <= 1 && split <= nstage; ++split) {
-      const int sps = (nstage + split - 1) / split;
-      const int eff = (nstage + sps - 1) / sps;  // splits that are not empty
-      if (eff != split) continue;
-      const double wgs = static_cast<double>(blocks) * split * batch;
-      const double k_share = K * sps / nstage;
-      const double flops = 2.0 * bm * bn * k_share, bytes = (bm + bn) * k_share * esz;
-      const double per_wg = std::max(flops / mfma_rate, bytes / l2_rate);
-      const double rounds = std::ceil(wgs / 256.0);
-      double t = t0 + rounds * per_wg;
-      if (split > 1) t += 1e-6 + (split - 1) * bm * bn * 4.0 / l2_rate;
-      if (t < best * 0.97) {
-        best = t;
-        c.bm = bm; c.bn = bn; c.nsplit = split; c.blocks = blocks;
-      }
+    const double wgs = static_cast<double>(blocks) * batch;
+    const double flops = 2.0 * bm * bn * K, bytes = (bm + bn) * K * esz;
+    const double per_wg = std::max(flops / mfma_rate, bytes / l2_rate);
+    const double t = t0 + std::ceil(wgs / 256.0) * per_wg;
+    if (t < best * 0.97) {
+      best = t;
+      c.bm = bm; c.bn = bn; c.blocks = blocks;
     }
   }
-  // Pipeline depth: stages of K in flight per workgroup.  Deeper keeps more
-  // loads outstanding (per-CU L2 bandwidth grows with them); the stage count
-  // is padded to a multiple of the depth, so take the deepest one whose
-  // padding is at most one stage (or none for short K).
-  c.depth = 2;
-  for (int d = 6; d >= 2; --d) {
+  // Block order.  Each of the 8 XCDs (own L2) reads, at least once, every
+  // operand byte its blocks touch.  Pixel-major: each XCD reads all weights
+  // and about 1/8 of the input; channel-major: 1/8 of the weights (when
+  // there are at least 8 channel blocks) and all the input.
+  {
+    const double w_bytes = static_cast<double>(S.cout) * K * esz;
+    double a_bytes = 0;
+    for (const TileGeom& T : S.tiles)
+      a_bytes += static_cast<double>(T.ch + S.f - 1) * (T.cw + S.f - 1) * S.cin * esz;
+    a_bytes *= batch;
+    const double nb = static_cast<double>((S.cout + c.bn - 1) / c.bn);
+    const double pix_major = 8.0 * w_bytes + a_bytes;
+    const double chan_major = w_bytes * std::max(1.0, 8.0 / nb) + a_bytes * std::min(8.0, nb);
+    c.chan_major = chan_major < pix_major ? 1 : 0;
+  }
+  // Pipeline depth: stages of K loaded ahead (3 to 6).  The stage count is
+  // padded to a multiple of the depth, so take the deepest one whose padding
+  // is at most one stage, or none for short K.
+  c.depth = 3;
+  for (int d = 6; d >= 3; --d) {
     const int pad = (nstage + d - 1) / d * d - nstage;
     if (pad == 0 || (pad <= 1 && nstage >= 4 * d)) { c.depth = d; break; }
   }
-#ifdef MAFAT_TUNING
-  // Tuning builds only: MAFAT_TUNE="first_layer:bm,bn,split,depth;..." forces
-  // the configuration of the stage starting at first_layer.
-  if (const char* env = std::getenv("MAFAT_TUNE")) {
-    std::string e(env);
-    size_t pos = 0;
-    while (pos < e.size()) {
-      size_t end = e.find(';', pos);
-      if (end == std::string::npos) end = e.size();
-      int l, bm, bn, sp, dp;
-      if (std::sscanf(e.substr(pos, end - pos).c_str(), "%d:%d,%d,%d,%d", &l, &bm, &bn, &sp, &dp) == 5 &&
-          l == S.first) {
-        c.bm = bm; c.bn = bn; c.nsplit = sp; c.depth = dp;
-        int64_t mb = 0;
-        for (const TileGeom& T : S.tiles) mb += (static_cast<int64_t>(T.ch) * T.cw + bm - 1) / bm;
-        c.blocks = mb * ((S.cout + bn - 1) / bn);
-      }
-      pos = end + 1;
-    }
-  }
-#endif
-  return c;
+  return tune_override(S, c);
 }
 
 WorkspaceLayout workspace_layout(const Group& G, int batch, int dtype) {
   const size_t esz = (dtype == MAFAT_F32) ? 4 : 2;
-  auto up = [](size_t v) { return (v + 255) & ~static_cast<size_t>(255); };
   WorkspaceLayout L{};
-  L.scratch = up(static_cast<size_t>(batch) * G.nbufs * G.ntiles * G.scratch_elems * esz);
-  size_t part = 0, cnt = 0;
-  for (const Stage& S : G.stages) {
-    const StageConfig c = choose_config(S, batch, dtype);
-    if (c.kind != K_CONV_MFMA || c.nsplit <= 1) continue;
-    part = std::max(part, static_cast<size_t>(batch) * c.blocks * c.nsplit * c.bm * c.bn * 4);
-    cnt = std::max(cnt, static_cast<size_t>(batch) * c.blocks * 4);
-  }
-  L.partials = up(part);
-  L.counters = up(cnt);
-  L.total = L.scratch + L.partials + L.counters;
+  L.scratch = (static_cast<size_t>(batch) * G.nbufs * G.ntiles * G.scratch_elems * esz + 255) & ~static_cast<size_t>(255);
+  L.total = L.scratch;
   return L;
 }
 
@@ -153,7 +156,6 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
   const size_t esz = (dtype == MAFAT_F32) ? 4 : 2;
   size_t need = 0;
   mafat_workspace_size(plan, batch, dtype, &need);
-  const WorkspaceLayout WL = workspace_layout(G, batch, dtype);
   if (ws_bytes < need)
     return fail(MAFAT_EWORKSPACE, "workspace " + std::to_string(ws_bytes) + " < " + std::to_string(need) + " bytes");
   if (need > 0 && (!ws || (reinterpret_cast<uintptr_t>(ws) & 255u)))
@@ -180,19 +182,18 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
       if (!aligned16(w[l])) return fail(MAFAT_EINVAL, "layer " + std::to_string(l) + ": weights not 16-byte aligned");
     }
 
-  float* partials = reinterpret_cast<float*>(static_cast<char*>(ws) + WL.scratch);
-  uint32_t* counters = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + WL.scratch + WL.partials);
-  if (WL.counters > 0) {
-    const hipError_t e = launch_zero(counters, static_cast<int64_t>(WL.counters / 4), stream);
-    if (e != hipSuccess) return fail(MAFAT_EHIP, std::string("counter reset failed: ") + hipGetErrorString(e));
-  }
   const int ns = static_cast<int>(G.stages.size());
   for (int s = 0; s < ns; ++s) {
     const Stage& S = G.stages[s];
     if (events && events[s] && hipEventRecord(static_cast<hipEvent_t>(events[s]), stream) != hipSuccess)
       return fail(MAFAT_EHIP, "hipEventRecord failed");
     const StageConfig cfg = choose_config(S, batch, dtype);
-    const int kind = cfg.kind;
+    int kind = cfg.kind;
+    // The matrix-core kernel addresses a frame's source buffer with 32-bit
+    // byte offsets; the generic kernel covers larger frames.
+    const int64_t src_frame_elems = (S.src_buf == BUF_GROUP_IO) ? in_frame : scr_frame;
+    if (kind == K_CONV_MFMA && src_frame_elems * static_cast<int64_t>(esz) >= (1ll << 31)) kind = K_CONV_DIRECT;
+    const bool matrix = (kind == K_CONV_MFMA);
     const MfmaShape shape{cfg.bm, cfg.bn, cfg.depth};
     const int bu = (kind == K_CONV_RGB) ? 256 / (S.cout / 8) : block_units(kind, shape);
     StageArgs A;
@@ -209,12 +210,8 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
     A.in_h = S.in_h; A.in_w = S.in_w;
     A.cin = S.cin; A.cout = S.cout;
     A.act = S.act;
-    A.nblk_n = (kind == K_CONV_MFMA) ? (S.cout + shape.bn - 1) / shape.bn : 1;
-    A.nsplit = (kind == K_CONV_MFMA) ? cfg.nsplit : 1;
-    A.partials = partials;
-    A.counters = counters;
-    if (A.nsplit > 1 && G.ntiles > kMaxTilesPerLaunch)
-      return fail(MAFAT_EUNSUPPORTED, "split K with more than one launch chunk");
+    A.nblk_n = matrix ? (S.cout + shape.bn - 1) / shape.bn : 1;
+    A.chan_major = matrix ? cfg.chan_major : 0;
     for (int t0 = 0; t0 < G.ntiles; t0 += kMaxTilesPerLaunch) {
       const int t1 = std::min(G.ntiles, t0 + kMaxTilesPerLaunch);
       A.ntiles = t1 - t0;
@@ -237,7 +234,7 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
         A.mblk_prefix[t - t0 + 1] = static_cast<int32_t>(total);
       }
       A.mblk_total = static_cast<int32_t>(total);
-      const int64_t blocks = total * A.nblk_n * A.nsplit * batch;
+      const int64_t blocks = total * A.nblk_n * batch;
       if (blocks >= (1ll << 31)) return fail(MAFAT_EUNSUPPORTED, "grid too large");
       A.total_blocks = static_cast<int32_t>(blocks);
       const hipError_t e = launch_stage(kind, dtype, S.f, S.pool, shape, A, stream);
@@ -248,14 +245,16 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
         long long tr[4][64];
         hipStreamSynchronize(stream);
         mafat_debug_trace(&tr[0][0]);
-        std::fprintf(stderr, "TRACE stage %d-%d tile %dx%d split %d depth %d grid %d\n", S.first, S.last,
-                     shape.bm, shape.bn, A.nsplit, shape.depth, A.total_blocks);
+        std::fprintf(stderr, "TRACE stage %d-%d tile %dx%d depth %d grid %d\n", S.first, S.last,
+                     shape.bm, shape.bn, shape.depth, A.total_blocks);
         for (int w = 0; w < 3; ++w) {
           std::fprintf(stderr, "  wg%d decoded +%lld addr +%lld issued +%lld lstored +%lld barrier +%lld loop +%lld end +%lld steps:", w,
                        (tr[w][4] - tr[w][0]) * 10, (tr[w][5] - tr[w][0]) * 10, (tr[w][6] - tr[w][0]) * 10,
                        (tr[w][7] - tr[w][0]) * 10, (tr[w][1] - tr[w][0]) * 10, (tr[w][2] - tr[w][0]) * 10,
                        (tr[w][3] - tr[w][0]) * 10);
           for (int k = 8; k < 20; ++k) std::fprintf(stderr, " %lld", (tr[w][k] - tr[w][0]) * 10);
+          std::fprintf(stderr, " | remap +%lld divs +%lld prefix +%lld", (tr[w][60] - tr[w][0]) * 10,
+                       (tr[w][61] - tr[w][0]) * 10, (tr[w][62] - tr[w][0]) * 10);
           std::fprintf(stderr, "\n");
         }
         std::fprintf(stderr, "  start spread wg-last minus wg0: %lld ns\n", (tr[1][0] - tr[0][0]) * 10);
