@@ -153,6 +153,59 @@ def cpu_baseline(wl, params, exec_macs_per_frame, min_s=10.0, max_s=30.0):
             "gmac_per_s": rate / 1e9}
 
 
+def csrc_digest():
+    """SHA-256 over the library's kernel and runtime sources: a counter
+    measurement taken on other sources no longer describes the kernels."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2107_06960_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload, stage_layers):
+    """HBM bytes per launch of a stage from a committed counter summary
+    (profiles/traffic_*.txt, 'key: value' lines): FETCH_SIZE + WRITE_SIZE
+    per dispatch, each scaled by bytes / counter of a plain copy of known
+    size.  None if no summary matches this workload, stage and sources."""
+    import glob
+    digest = csrc_digest()
+    for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "traffic_*.txt"))):
+        kv = {}
+        with open(path) as fh:
+            for line in fh:
+                if ":" in line and not line.startswith("#"):
+                    k, v = line.split(":", 1)
+                    kv[k.strip()] = v.strip()
+        try:
+            if (kv.get("workload") != workload or kv.get("stage_layers") != f"{stage_layers[0]}-{stage_layers[1]}"
+                    or kv.get("csrc_sha256") != digest):
+                continue
+            cb = float(kv["copy_bytes"])
+            fetch = float(kv["fetch_kib_per_dispatch"]) * cb / float(kv["copy_fetch_kib"])
+            write = float(kv["write_kib_per_dispatch"]) * cb / float(kv["copy_write_kib"])
+        except (KeyError, ValueError, ZeroDivisionError):
+            continue
+        return {"bytes": round(fetch + write), "fetch_bytes": round(fetch), "write_bytes": round(write),
+                "source": os.path.relpath(path, ROOT)}
+    return None
+
+
+def copy_calibration(mib, reps=5):
+    """A plain device copy of a known size, for scaling the HBM byte counters."""
+    import torch
+    n = mib << 20
+    src = torch.randint(0, 255, (n,), dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n, "reps": reps, "kernel": "torch uint8 device-to-device copy_"}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -162,7 +215,12 @@ def main():
     ap.add_argument("--graph", action="store_true", help="replay one step from a captured HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-untiled", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "only the one-GPU path is built: --gpus must be 1 (frames, and the "
                                    "tiles of a group, would shard across GPUs without exchange)"}))
@@ -264,6 +322,10 @@ def main():
             "frac": round(dom_f / (dom["ms"] * 1e-3) / 1e12 / dom["peak_tflops"], 4), "traffic": None,
             "kernel": f"stage layers {dom['layers'][0]}-{dom['layers'][1]} (group {dom['group']})",
             "per_launch_gflop": dom["gflop"], "avg_ms": dom["ms"]}
+    tr = measured_traffic(wl.name, dom["layers"])
+    if tr is not None:
+        roof["traffic"] = tr["bytes"]
+        roof["traffic_detail"] = tr
 
     res = {
         "metric": METRIC, "value": round(fps, 2), "unit": "frames/s", "n_gpus": 1,

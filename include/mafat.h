@@ -39,6 +39,8 @@
  *     enqueue kernels on the given stream and return.
  *   - Pointer arrays (w, scale, bias, cut_bufs, events) are host arrays of
  *     device pointers / event handles, read during the call only.
+ *   - Device tensors (x, y, cut tensors, weights, scale, bias) must be
+ *     16-byte aligned (EINVAL otherwise); the workspace 256-byte aligned.
  *
  * Errors
  *   - Every int-returning function returns a mafat_status.  No C++

@@ -40,12 +40,18 @@ struct StageArgs {
 };
 
 // Kernel families the runtime picks from.
-enum KernelKind { K_CONV_MFMA = 0, K_CONV_DIRECT = 1, K_POOL = 2, K_CONV_RGB = 3 };
+enum KernelKind { K_CONV_MFMA = 0, K_CONV_DIRECT = 1, K_POOL = 2, K_CONV_RGB = 3, K_CONV_RGB_MFMA = 4 };
 
-// Block shape of the MFMA kernel: output pixels x output channels, and the
-// depth of its load pipeline (3 to 6 stages of 128 bytes of K in flight).
+// Conv outputs (rows x columns) per workgroup of the matrix-core first-layer
+// kernel.
+constexpr int kRgbBlockRows = 32, kRgbBlockCols = 32;
+
+// Block shape of the MFMA kernel: output pixels x output channels, the
+// depth of its load pipeline (3 to 6 stages of 128 bytes of K in flight) and
+// the number of K groups (1: 4 waves; 2: 8 waves, each group of 4 multiplies
+// one 64-byte half of every stage).
 struct MfmaShape {
-  int bm, bn, depth;
+  int bm, bn, depth, kg;
 };
 
 // Launch one stage chunk.  `units_per_block` is what the kernel covers per

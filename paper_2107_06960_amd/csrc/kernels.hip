@@ -18,7 +18,9 @@
 //                       first layer): one thread per output pixel (or per
 //                       2x2 pool window), weights through the scalar cache.
 //   conv_rgb_kernel     the 3-channel first layer on the vector ALUs
-//                       (bf16: packed dot products), patch in registers.
+//                       (fp32), patch in registers.
+//   conv_rgb_mfma_kernel  the 3-channel first layer in bf16 on the matrix
+//                       cores, K = 27 zero-padded to 32.
 //   pool_kernel         a max-pool stage that does not follow a convolution.
 #include <hip/hip_runtime.h>
 
@@ -184,66 +186,109 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, un
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, static_cast<int>(bytes), 0x00020000);
 }
 
-// Epilogue of the matrix-core kernels for a BM x BN block computed by 4
-// waves in a 2x2 arrangement: scale, bias, activation, the optional 2x2 max
-// (the 4 accumulator rows a lane holds are one pool window), rounding to the
-// output type; the block is then transposed through LDS (`smem`, at least
-// OROWS * (BN * sizeof(T) + 16) bytes, free for use) and written with
-// 16-byte stores along channels.  Lane l holds rows 4*(l/16) .. +3 of each
-// 16x16 accumulator tile, column l % 16.
-template <int DT, int BM, int BN, bool POOL>
-__device__ __forceinline__ void store_block(const f32x4 (&acc)[BM / 32][BN / 32],
-                                            unsigned char* smem, const StageArgs& a,
-                                            const KTile& tl, int m0, int n0,
-                                            typename Elt<DT>::T* dst) {
-  using T = typename Elt<DT>::T;
-  constexpr int EPV = 16 / static_cast<int>(sizeof(T));
-  constexpr int WM = BM / 2, WN = BN / 2, MT = WM / 16, NT = WN / 16;
-  constexpr int OROWS = POOL ? BM / 4 : BM;
-  constexpr int OSTRIDE = (BN * static_cast<int>(sizeof(T)) + 16) / static_cast<int>(sizeof(T));
-  const int tid = static_cast<int>(threadIdx.x), lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int M = tl.ch * tl.cw, cout = a.cout;
-  T* sO = reinterpret_cast<T*>(smem);
-  const int rq = (lane >> 4) * 4;
+// Epilogue of the matrix-core kernels.  Two MFMA orientations:
+//   - no pool: the weights are the A operand, so accumulator tile acc[j][i]
+//     holds output channels (rows) x pixels (columns): lane l has channels
+//     4*(l/16) .. +3 of column l % 16, i.e. 4 consecutive channels of one
+//     pixel, which leave in one 8-byte (bf16) or 16-byte (fp32) store;
+//   - fused 2x2 max-pool: the pixels are the A operand, quad-ordered (see
+//     row_pixel), so the 4 accumulator rows a lane holds (rows 4*(l/16) ..
+//     +3 of column l % 16) are one pool window of one channel.  The window
+//     is reduced in the lane: scale and bias per pixel, the maximum, then
+//     the activation -- which is non-decreasing, so applying it after the
+//     maximum gives the same value as pooling activated outputs.
+// Leaky ReLU(0.1) is max(v, 0.1 v); a linear layer uses slope 1.
+__device__ __forceinline__ float act_slope(int act) { return act == MAFAT_ACT_LEAKY01 ? 0.1f : 1.f; }
+
+template <int DT>
+__device__ __forceinline__ void store4(float* p, const float (&v)[4]) {
+  *reinterpret_cast<f32x4*>(p) = f32x4{v[0], v[1], v[2], v[3]};
+}
+template <int DT>
+__device__ __forceinline__ void store4(uint16_t* p, const float (&v)[4]) {
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  const bf16x4 h = {static_cast<__bf16>(v[0]), static_cast<__bf16>(v[1]), static_cast<__bf16>(v[2]),
+                    static_cast<__bf16>(v[3])};  // round to nearest even
+  *reinterpret_cast<uint2*>(p) = __builtin_bit_cast(uint2, h);
+}
+__device__ __forceinline__ void store1(float* p, float v) { *p = v; }
+__device__ __forceinline__ void store1(uint16_t* p, float v) {
+  *reinterpret_cast<__bf16*>(p) = static_cast<__bf16>(v);
+}
+
+// Scale and bias of a lane's channels of each of its NT channel tiles: 4
+// consecutive channels (no pool) or one channel (pool, in element 0).
+template <int BN, bool POOL>
+__device__ __forceinline__ void load_scale_bias(const StageArgs& a, int n0, f32x4 (&sc)[BN / 32],
+                                                f32x4 (&bi)[BN / 32]) {
+  constexpr int WN = BN / 2, NT = WN / 16;
+  const int lane = static_cast<int>(threadIdx.x) & 63, wn = (static_cast<int>(threadIdx.x) >> 6) & 1;  // any K group
 #pragma unroll
   for (int j = 0; j < NT; ++j) {
-    const int cl = wn * WN + j * 16 + (lane & 15);
-    const int co = n0 + cl;
-    const float s = co < cout ? a.scale[co] : 0.f, b = co < cout ? a.bias[co] : 0.f;
-#pragma unroll
-    for (int i = 0; i < MT; ++i) {
-      const int ml = wm * WM + i * 16 + rq;
-      float v[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = activate(acc[i][j][r] * s + b, a.act);
-      if (POOL) {
-        const float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-        put(sO + (ml >> 2) * OSTRIDE + cl, mx);
-      } else {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) put(sO + (ml + r) * OSTRIDE + cl, v[r]);
-      }
+    if (POOL) {
+      const int co = n0 + wn * WN + j * 16 + (lane & 15);
+      const int cc = co < a.cout ? co : 0;
+      sc[j] = f32x4{a.scale[cc], 0.f, 0.f, 0.f};
+      bi[j] = f32x4{a.bias[cc], 0.f, 0.f, 0.f};
+    } else {
+      const int co = n0 + wn * WN + j * 16 + 4 * (lane >> 4);
+      const int cc = co < a.cout ? co : 0;
+      sc[j] = *reinterpret_cast<const f32x4*>(a.scale + cc);
+      bi[j] = *reinterpret_cast<const f32x4*>(a.bias + cc);
     }
   }
-  __syncthreads();
-  constexpr int CPR = BN / EPV;  // 16-byte pieces per output row
-  const int pw = tl.cw >> 1;
-  for (int c = tid; c < OROWS * CPR; c += 256) {
-    const int row = c / CPR, piece = c - row * CPR;
-    const int m = m0 + (POOL ? 4 * row : row);
-    const int co = n0 + piece * EPV;
-    if (m >= M || co >= cout) continue;
+}
+
+// With KG == 2 K groups, group g stores channel tiles [g NT/2, (g+1) NT/2).
+template <int DT, int BM, int BN, bool POOL, int KG>
+__device__ __forceinline__ void store_direct(const f32x4 (&acc)[BN / 32][BM / 32], const f32x4 (&sc)[BN / 32],
+                                             const f32x4 (&bi)[BN / 32], const StageArgs& a,
+                                             const KTile& tl, int m0, int n0,
+                                             typename Elt<DT>::T* dst) {
+  constexpr int WM = BM / 2, WN = BN / 2, MT = WM / 16, NT = WN / 16;
+  const int tid = static_cast<int>(threadIdx.x), lane = tid & 63, wave = tid >> 6;
+  const int wm = (wave >> 1) & 1, wn = wave & 1, grp = wave >> 2;
+  const int M = tl.ch * tl.cw, cout = a.cout;
+  const float slope = act_slope(a.act);
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
     int oy, ox;
+    bool ok;
     if (POOL) {
-      const int qq = m >> 2, qy = qq / pw;
+      // this lane's window: GEMM rows m .. m+3
+      const int m = m0 + wm * WM + i * 16 + 4 * (lane >> 4);
+      const int pw = tl.cw >> 1, qq = m >> 2, qy = qq / pw;
       oy = (tl.cy0 >> 1) + qy;
       ox = (tl.cx0 >> 1) + (qq - qy * pw);
+      ok = m < M;
     } else {
-      row_pixel<false>(tl, m, &oy, &ox);
+      const int m = m0 + wm * WM + i * 16 + (lane & 15);
+      row_pixel<false>(tl, m < M ? m : 0, &oy, &ox);
+      ok = m < M;
     }
-    *reinterpret_cast<u32x4*>(dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * cout + co) =
-        *reinterpret_cast<const u32x4*>(sO + row * OSTRIDE + piece * EPV);
+    typename Elt<DT>::T* drow = dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * cout;
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      if (KG == 2 && (j < grp * (NT / 2) || j >= (grp + 1) * (NT / 2))) continue;
+      if (POOL) {
+        const int co = n0 + wn * WN + j * 16 + (lane & 15);
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = fmaf(acc[j][i][r], sc[j][0], bi[j][0]);
+        float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+        m = fmaxf(m, slope * m);
+        if (ok && co < cout) store1(drow + co, m);
+      } else {
+        const int co = n0 + wn * WN + j * 16 + 4 * (lane >> 4);
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          v[r] = fmaf(acc[j][i][r], sc[j][r], bi[j][r]);
+          v[r] = fmaxf(v[r], slope * v[r]);
+        }
+        if (ok && co < cout) store4<DT>(drow + co, v);
+      }
+    }
   }
 }
 
@@ -263,28 +308,30 @@ __device__ __forceinline__ void store_block(const f32x4 (&acc)[BM / 32][BN / 32]
 // sub-chunks past the last tap and weight rows past c_out all read as zero
 // through the descriptor's range check, so the loop has no masking work.
 //
-// Epilogue: see store_block.
+// Epilogue: see store_direct (no LDS).
 //
 // Requires c_in % (64 / sizeof(T)) == 0, c_out % 16 == 0 and byte offsets
 // below 2^31 within a frame's source buffer and the weights (host-checked).
-template <int DT, int F, int BM, int BN, bool POOL, int DEPTH>
-__global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
+template <int DT, int F, int BM, int BN, bool POOL, int DEPTH, int KG>
+__global__ __launch_bounds__(256 * KG) void conv_mfma_kernel(const StageArgs a) {
   using T = typename Elt<DT>::T;
   constexpr int ESZ = static_cast<int>(sizeof(T));
   constexpr int P = (F - 1) / 2;
   constexpr int KC = 64 / ESZ;   // channels per sub-chunk
   constexpr int EPV = 16 / ESZ;  // channels per 16 bytes
   constexpr int ROWQ = 9;        // u32x4 per LDS row
-  constexpr int ALD = BM / 32, BLD = BN / 32;  // loads per thread per stage
+  constexpr int RSTEP = 32 * KG;                     // rows staged per pass of the workgroup
+  constexpr int ALD = BM / RSTEP, BLD = BN / RSTEP;  // loads per thread per stage
   constexpr int WM = BM / 2, WN = BN / 2, MT = WM / 16, NT = WN / 16;
+  constexpr int NH = 2 / KG;  // 64-byte halves of a stage each wave multiplies
+  static_assert(KG == 1 || KG == 2, "K groups");
+  static_assert(ALD >= 1 && BLD >= 1 && ALD * RSTEP == BM && BLD * RSTEP == BN, "block shape");
+  static_assert(KG == 1 || NT % 2 == 0, "two K groups split the channel tiles in the epilogue");
   static_assert(DEPTH >= 3 && DEPTH <= 6, "pipeline depth");
   static_assert(F * F + 2 * DEPTH + 2 < 32, "tap mask width (taps of computed stages)");
   constexpr int NBUF = 2;  // LDS stage buffers
   constexpr int OPND_BYTES = NBUF * (BM + BN) * ROWQ * 16;
-  constexpr int OROWS = POOL ? BM / 4 : BM;
-  constexpr int OUT_BYTES = OROWS * (BN * ESZ + 16);
-  constexpr int SMEM = OPND_BYTES > OUT_BYTES ? OPND_BYTES : OUT_BYTES;
-  __shared__ __align__(16) unsigned char smem[SMEM];
+  __shared__ __align__(16) unsigned char smem[OPND_BYTES];
   u32x4* sA = reinterpret_cast<u32x4*>(smem);  // [NBUF][BM][ROWQ]
   u32x4* sB = sA + NBUF * BM * ROWQ;           // [NBUF][BN][ROWQ]
 
@@ -292,7 +339,10 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
   KTile tl;
   const BlockPos bp = decode_block(a, &tl);
   const int tid = static_cast<int>(threadIdx.x), lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  // Waves 4g .. 4g+3 form K group g (2x2 over the block); with two groups,
+  // group g multiplies the 64-byte half g of every stage.
+  const int grp = wave >> 2, wm = (wave >> 1) & 1, wn = wave & 1;
+  const int h0 = (KG == 2) ? grp : 0;
   MAFAT_TRACE(4 + (tl.ch > 30000 ? 1 : 0));
   const int M = tl.ch * tl.cw;
   const int m0 = bp.mb * BM, n0 = bp.nb * BN;
@@ -307,7 +357,7 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
       make_rsrc(static_cast<const T*>(a.src) + sbase, static_cast<unsigned>((a.src_fstride - tl.src_off) * ESZ));
   const __amdgpu_buffer_rsrc_t rsb = make_rsrc(a.w, static_cast<unsigned>(cout * K * ESZ));
 
-  // This thread stages rows r0 + 32 i, 16-byte piece `pc` of sub-chunk `hh`
+  // This thread stages rows r0 + RSTEP i, 16-byte piece `pc` of sub-chunk `hh`
   // of every stage.  Per A row: the byte offset of its pixel in the source
   // buffer and a mask of the filter taps that read zero (outside the image;
   // bits past the last tap are set, so padded sub-chunks read zero).  Loads
@@ -316,7 +366,7 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
   unsigned a_off[ALD], a_inv[ALD], b_off[BLD];
 #pragma unroll
   for (int i = 0; i < ALD; ++i) {
-    const int m = m0 + r0 + 32 * i;
+    const int m = m0 + r0 + RSTEP * i;
     int oy, ox;
     row_pixel<POOL>(tl, m < M ? m : 0, &oy, &ox);
     a_off[i] = static_cast<unsigned>((((oy - tl.sy0) * sw + (ox - tl.sx0)) * cin + pc * EPV) * ESZ);
@@ -332,7 +382,7 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
   }
 #pragma unroll
   for (int i = 0; i < BLD; ++i) {
-    const int co = n0 + r0 + 32 * i;
+    const int co = n0 + r0 + RSTEP * i;
     b_off[i] = co < cout ? static_cast<unsigned>((co * K + pc * EPV) * ESZ) : 0x80000000u;
   }
 
@@ -372,24 +422,24 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
 #define MAFAT_LSTORE(d_, buf_)                                                                 \
   do {                                                                                         \
     _Pragma("unroll") for (int i = 0; i < ALD; ++i)                                            \
-      sA[((buf_) * BM + r0 + 32 * i) * ROWQ + q] = ra[d_][i];                                  \
+      sA[((buf_) * BM + r0 + RSTEP * i) * ROWQ + q] = ra[d_][i];                               \
     _Pragma("unroll") for (int i = 0; i < BLD; ++i)                                            \
-      sB[((buf_) * BN + r0 + 32 * i) * ROWQ + q] = rb[d_][i];                                  \
+      sB[((buf_) * BN + r0 + RSTEP * i) * ROWQ + q] = rb[d_][i];                               \
   } while (0)
 
-  f32x4 acc[MT][NT];
+  f32x4 acc[NT][MT];  // [channel tile][pixel tile], orientation: see store_direct
 #pragma unroll
-  for (int i = 0; i < MT; ++i)
+  for (int j = 0; j < NT; ++j)
 #pragma unroll
-    for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int i = 0; i < MT; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // Pipeline, per step st (computing stage st from LDS buffer st % 2):
   //   barrier (stage st is in LDS; every wave is done reading stage st - 1);
   //   read both K-halves' fragments of stage st; issue the global loads of
   //   stage st + DEPTH into the register set stage st came from; MFMAs;
   //   write stage st + 1 (loaded DEPTH - 1 steps ago) to the other buffer.
-  // The stage count is padded to a multiple of DEPTH so the loop body has no
-  // branches (padded stages read zero A rows).
+  // The stage count is padded to a multiple of DEPTH so the unrolled loop
+  // body has no branches (padded stages read zero A rows).
   const int nst_pad = (nstage + DEPTH - 1) / DEPTH * DEPTH;
   MAFAT_TRACE(5);
   MAFAT_GLOAD(0);
@@ -402,44 +452,94 @@ __global__ __launch_bounds__(256) void conv_mfma_kernel(const StageArgs a) {
   MAFAT_LSTORE(0, 0);
   MAFAT_TRACE(7);
   int rbuf = 0;   // LDS buffer holding stage st
-#define MAFAT_STEP(d_, dn_)                                                                      \
+#define MAFAT_STEP(d_, dn_, load_)                                                               \
   do {                                                                                           \
     __syncthreads();                                                                             \
-    u32x4 af[2][MT], bfr[2][NT];                                                                 \
-    _Pragma("unroll") for (int h = 0; h < 2; ++h) {                                              \
+    u32x4 af[NH][MT], bfr[NH][NT];                                                               \
+    _Pragma("unroll") for (int h = 0; h < NH; ++h) {                                             \
       _Pragma("unroll") for (int i = 0; i < MT; ++i)                                             \
-        af[h][i] = sA[(rbuf * BM + wm * WM + i * 16 + (lane & 15)) * ROWQ + h * 4 + (lane >> 4)]; \
+        af[h][i] = sA[(rbuf * BM + wm * WM + i * 16 + (lane & 15)) * ROWQ + (h0 + h) * 4 + (lane >> 4)]; \
       _Pragma("unroll") for (int j = 0; j < NT; ++j)                                             \
-        bfr[h][j] = sB[(rbuf * BN + wn * WN + j * 16 + (lane & 15)) * ROWQ + h * 4 + (lane >> 4)]; \
+        bfr[h][j] = sB[(rbuf * BN + wn * WN + j * 16 + (lane & 15)) * ROWQ + (h0 + h) * 4 + (lane >> 4)]; \
     }                                                                                            \
-    MAFAT_GLOAD(d_);                                                                             \
-    _Pragma("unroll") for (int h = 0; h < 2; ++h)                                                \
+    if (load_) MAFAT_GLOAD(d_);                                                                  \
+    _Pragma("unroll") for (int h = 0; h < NH; ++h)                                               \
       _Pragma("unroll") for (int i = 0; i < MT; ++i)                                             \
-        _Pragma("unroll") for (int j = 0; j < NT; ++j) mma<DT>(acc[i][j], af[h][i], bfr[h][j]);  \
+        _Pragma("unroll") for (int j = 0; j < NT; ++j) {                                         \
+          if constexpr (POOL) mma<DT>(acc[j][i], af[h][i], bfr[h][j]);                           \
+          else mma<DT>(acc[j][i], bfr[h][j], af[h][i]);                                          \
+        }                                                                                        \
     rbuf ^= 1;                                                                                   \
     MAFAT_LSTORE(dn_, rbuf);                                                                     \
     MAFAT_TRACE(8 + s0 + (d_));                                                                  \
   } while (0)
-  for (int s0 = 0; s0 < nst_pad; s0 += DEPTH) {
-    if constexpr (DEPTH == 3) {
-      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 0);
-    } else if constexpr (DEPTH == 4) {
-      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 3); MAFAT_STEP(3, 0);
-    } else if constexpr (DEPTH == 5) {
-      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 3); MAFAT_STEP(3, 4); MAFAT_STEP(4, 0);
-    } else {
-      MAFAT_STEP(0, 1); MAFAT_STEP(1, 2); MAFAT_STEP(2, 3); MAFAT_STEP(3, 4); MAFAT_STEP(4, 5);
-      MAFAT_STEP(5, 0);
-    }
-  }
+#define MAFAT_STEPS(load_)                                                                       \
+  do {                                                                                           \
+    if constexpr (DEPTH == 3) {                                                                  \
+      MAFAT_STEP(0, 1, load_); MAFAT_STEP(1, 2, load_); MAFAT_STEP(2, 0, load_);                 \
+    } else if constexpr (DEPTH == 4) {                                                           \
+      MAFAT_STEP(0, 1, load_); MAFAT_STEP(1, 2, load_); MAFAT_STEP(2, 3, load_);                 \
+      MAFAT_STEP(3, 0, load_);                                                                   \
+    } else if constexpr (DEPTH == 5) {                                                           \
+      MAFAT_STEP(0, 1, load_); MAFAT_STEP(1, 2, load_); MAFAT_STEP(2, 3, load_);                 \
+      MAFAT_STEP(3, 4, load_); MAFAT_STEP(4, 0, load_);                                          \
+    } else {                                                                                     \
+      MAFAT_STEP(0, 1, load_); MAFAT_STEP(1, 2, load_); MAFAT_STEP(2, 3, load_);                 \
+      MAFAT_STEP(3, 4, load_); MAFAT_STEP(4, 5, load_); MAFAT_STEP(5, 0, load_);                 \
+    }                                                                                            \
+  } while (0)
+  // Steady state: every step loads the stage DEPTH ahead.  The last DEPTH
+  // steps load nothing (all their stages are in flight already), so nothing
+  // useless sits in the memory queue ahead of the epilogue's scale and bias,
+  // which are fetched before those steps.
+  int s0 = 0;
+  for (; s0 < nst_pad - DEPTH; s0 += DEPTH) MAFAT_STEPS(true);
+  f32x4 sc[NT], bi[NT];
+  load_scale_bias<BN, POOL>(a, n0, sc, bi);
+  MAFAT_STEPS(false);
   MAFAT_TRACE(1);
-  __syncthreads();
+#undef MAFAT_STEPS
 #undef MAFAT_STEP
 #undef MAFAT_GLOAD
 #undef MAFAT_LSTORE
 
   MAFAT_TRACE(2);
-  store_block<DT, BM, BN, POOL>(acc, smem, a, tl, m0, n0, dst);
+  if constexpr (KG == 2) {
+    // Each group keeps half of the channel tiles: it hands the other half of
+    // its partial sums to the partner wave (same 2x2 position) through LDS
+    // and adds the partner's partial sums for its own half.
+    constexpr int NH2 = NT / 2;
+    static_assert(8 * 64 * NH2 * MT * 16 <= OPND_BYTES, "partial sums fit in the operand buffers");
+    f32x4* sX = reinterpret_cast<f32x4*>(smem);  // [wave][NT/2][MT][64 lanes]
+    __syncthreads();  // every wave is done with the operand buffers
+    // (Two copies with constant indices: a wave-dependent index into acc
+    // would move it to scratch memory.)
+    const int partner = wave ^ 4;
+    if (grp == 0) {
+#pragma unroll
+      for (int j = 0; j < NH2; ++j)
+#pragma unroll
+        for (int i = 0; i < MT; ++i) sX[((wave * NH2 + j) * MT + i) * 64 + lane] = acc[NH2 + j][i];
+    } else {
+#pragma unroll
+      for (int j = 0; j < NH2; ++j)
+#pragma unroll
+        for (int i = 0; i < MT; ++i) sX[((wave * NH2 + j) * MT + i) * 64 + lane] = acc[j][i];
+    }
+    __syncthreads();
+    if (grp == 0) {
+#pragma unroll
+      for (int j = 0; j < NH2; ++j)
+#pragma unroll
+        for (int i = 0; i < MT; ++i) acc[j][i] += sX[((partner * NH2 + j) * MT + i) * 64 + lane];
+    } else {
+#pragma unroll
+      for (int j = 0; j < NH2; ++j)
+#pragma unroll
+        for (int i = 0; i < MT; ++i) acc[NH2 + j][i] += sX[((partner * NH2 + j) * MT + i) * 64 + lane];
+    }
+  }
+  store_direct<DT, BM, BN, POOL, KG>(acc, sc, bi, a, tl, m0, n0, dst);
   MAFAT_TRACE(3);
 }
 
@@ -650,6 +750,176 @@ void conv_rgb_kernel(const StageArgs a) {
   }
 }
 
+// First layer on the matrix cores (bf16).  Its K = 3x3x3 = 27 runs as three
+// v_mfma_f32_16x16x16_bf16, one per filter row ky, each with K = 16 = 4 kx
+// slots x 4 channel slots: (kx, c) for kx < 3, c < 3, and zeros (channel
+// slot 3, and the whole kx slot 3, have zero weights).  A workgroup computes
+// a BR x BC block of conv outputs (all c_out channels) of one tile:
+//   1. the (BR+2) x (BC+2) input patch is staged in LDS as 8-byte pixels
+//      (c0, c1, c2, 0), so the 4 K values of a lane's operand are one
+//      aligned 8-byte LDS read at a per-lane constant offset; the patch is
+//      fetched with coalesced 2-byte buffer loads (all of a thread's loads
+//      are issued before its first LDS write), zero outside the image and
+//      outside the tile's source region (those loads get an offset past
+//      the descriptor's range); the weights, scale and bias, the same for
+//      every workgroup, are staged with one 16-byte load per thread;
+//   2. each wave takes 16-pixel tiles (2 rows x 8 columns, ordered as 4
+//      windows of 2x2); lane l loads, for each ky, the pixel (kx = l / 16)
+//      of its pixel's (l % 16) filter window (kx slot 3 repeats kx = 2, which
+//      meets zero weights);
+//   3. the epilogue follows store_direct: without a pool the weights are
+//      the A operand (a lane ends with 4 consecutive channels of one pixel,
+//      one 8-byte store); with a fused 2x2 pool the pixels are (a lane's 4
+//      accumulator rows are one window of one channel: scale and bias, the
+//      window maximum, then the activation, which is monotone).
+// Requires c_out = 16 * NJ, c_in = 3, f = 3, s = 1, p = 1 (host-checked).
+template <bool POOL, int NJ>
+__global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+  constexpr int BR = kRgbBlockRows, BC = kRgbBlockCols;  // conv outputs per block, even
+  constexpr int SR = BR + 2, SC = BC + 2;    // staged input patch (pixels)
+  constexpr int RS = SC * 4 + 8;             // bf16 per LDS row (8-byte pixels + pad)
+  constexpr int NTILE = BR * BC / 16;        // 16-pixel MFMA tiles
+  constexpr int TPR = BC / 8;                // tiles per 2 rows
+  constexpr int COUT = 16 * NJ;
+  constexpr int W16 = COUT * 27 * 2 / 16;    // 16-byte pieces of the weights
+  constexpr int NEL = SR * SC * 4;           // staged elements (incl. the zero 4th channel)
+  constexpr int NLD = (NEL + 255) / 256;     // staging elements per thread
+  __shared__ __align__(16) uint16_t sx[SR * RS];
+  __shared__ __align__(16) uint16_t swt[COUT * 27];
+  __shared__ __align__(16) float ssb[2 * COUT];  // scale, bias
+
+  MAFAT_TRACE(0);
+  KTile tl;
+  const BlockPos bp = decode_block(a, &tl);
+  const int tid = static_cast<int>(threadIdx.x), lane = tid & 63, wave = tid >> 6;
+  MAFAT_TRACE(4 + (tl.ch > 30000 ? 1 : 0));
+  const int nbx = (tl.cw + BC - 1) / BC;
+  const int by = bp.mb / nbx, bx = bp.mb - by * nbx;
+  const int oy0 = tl.cy0 + by * BR, ox0 = tl.cx0 + bx * BC;
+  const uint16_t* src = static_cast<const uint16_t*>(a.src) + bp.frame * a.src_fstride + tl.src_off;
+  uint16_t* dst = static_cast<uint16_t*>(a.dst) + bp.frame * a.dst_fstride + tl.dst_off;
+  const int kq = lane >> 4;
+
+  // Weights, scale, bias -> LDS (16 bytes per thread).
+  if (tid < W16) {
+    reinterpret_cast<u32x4*>(swt)[tid] = reinterpret_cast<const u32x4*>(a.w)[tid];
+  } else if (tid < W16 + COUT / 4) {
+    const int i = tid - W16;
+    reinterpret_cast<f32x4*>(ssb)[i] = reinterpret_cast<const f32x4*>(a.scale)[i];
+  } else if (tid < W16 + COUT / 2) {
+    const int i = tid - W16 - COUT / 4;
+    reinterpret_cast<f32x4*>(ssb + COUT)[i] = reinterpret_cast<const f32x4*>(a.bias)[i];
+  }
+  // Input patch: rows oy0-1 .. oy0+BR, columns ox0-1 .. ox0+BC.  Elements
+  // outside the image, or outside this tile's source region (only outputs
+  // outside the tile's computed rectangle would read them), read 0.
+  const int ylo = max(0, tl.cy0 - 1), yhi = min(a.in_h, tl.cy0 + tl.ch + 1);
+  const int xlo = max(0, tl.cx0 - 1), xhi = min(a.in_w, tl.cx0 + tl.cw + 1);
+  const __amdgpu_buffer_rsrc_t rs =
+      make_rsrc(src, static_cast<unsigned>((a.src_fstride - tl.src_off) * 2));
+  uint32_t ld[NLD];
+#pragma unroll
+  for (int k = 0; k < NLD; ++k) {
+    const int e = tid + 256 * k;
+    const int r = e / (SC * 4), rem = e - r * (SC * 4);
+    const int px = rem >> 2, c = rem & 3;
+    const int iy = oy0 - 1 + r, ix = ox0 - 1 + px;
+    const bool ok = e < NEL && c < 3 && iy >= ylo && iy < yhi && ix >= xlo && ix < xhi;
+    const unsigned off = static_cast<unsigned>((((iy - tl.sy0) * tl.sw + (ix - tl.sx0)) * 3 + c) * 2);
+    ld[k] = __builtin_amdgcn_raw_buffer_load_b16(rs, static_cast<int>(ok ? off : 0x80000000u), 0, 0);
+  }
+#pragma unroll
+  for (int k = 0; k < NLD; ++k) {
+    const int e = tid + 256 * k;
+    const int r = e / (SC * 4), rem = e - r * (SC * 4);
+    if (e < NEL) sx[r * RS + rem] = static_cast<uint16_t>(ld[k]);
+  }
+  MAFAT_TRACE(6);
+  __syncthreads();
+  MAFAT_TRACE(7);
+
+  // Weight operand of a lane, per channel tile j and filter row ky: output
+  // channel 16 j + (lane & 15), kx slot kq: (w[c0], w[c1], w[c2], 0), zero
+  // for kq = 3.  (The same registers serve as A or B operand.)
+  u32x2 wf[NJ][3];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int ky = 0; ky < 3; ++ky) {
+      const int wr = (16 * j + (lane & 15)) * 27 + ky * 9 + 3 * min(kq, 2);
+      const uint32_t w0 = swt[wr], w1 = swt[wr + 1], w2 = swt[wr + 2];
+      wf[j][ky] = kq < 3 ? u32x2{w0 | (w1 << 16), w2} : u32x2{0u, 0u};
+    }
+  float sc[NJ][4], bi[NJ][4];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int co = POOL ? 16 * j + (lane & 15) : 16 * j + 4 * kq + r;
+      sc[j][r] = ssb[co];
+      bi[j][r] = ssb[COUT + co];
+    }
+  const float slope = act_slope(a.act);
+
+  const int p = lane & 15;  // pixel of the MFMA tile whose operand this lane loads
+  const int kx = min(kq, 2);
+  for (int t = wave; t < NTILE; t += 4) {
+    // tile t: rows 2 (t / TPR) .. +1, columns 8 (t % TPR) .. +7, as 4
+    // windows of 2x2: pixel p is window p >> 2, position p & 3 in it
+    const int py = 2 * (t / TPR) + ((p & 3) >> 1);
+    const int pxl = 8 * (t % TPR) + 2 * (p >> 2) + (p & 1);
+    const u32x2* xp = reinterpret_cast<const u32x2*>(sx + py * RS + (pxl + kx) * 4);
+    u32x2 xf[3];
+#pragma unroll
+    for (int ky = 0; ky < 3; ++ky) xf[ky] = xp[ky * (RS / 4)];
+    f32x4 acc[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ky = 0; ky < 3; ++ky) {
+        const bf16x4 xa = __builtin_bit_cast(bf16x4, xf[ky]), wa = __builtin_bit_cast(bf16x4, wf[j][ky]);
+        acc[j] = POOL ? __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(xa, wa, acc[j], 0, 0, 0)
+                      : __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(wa, xa, acc[j], 0, 0, 0);
+      }
+    }
+    if constexpr (POOL) {
+      // a lane's accumulator rows are window kq of the tile, column = channel
+      const int oy = oy0 + 2 * (t / TPR), ox = ox0 + 8 * (t % TPR) + 2 * kq;
+      const bool ok = (oy - tl.cy0) < tl.ch && (ox - tl.cx0) < tl.cw;
+      uint16_t* drow = dst + (((oy >> 1) - tl.dy0) * tl.dw + ((ox >> 1) - tl.dx0)) * COUT;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = fmaf(acc[j][r], sc[j][0], bi[j][0]);
+        float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+        m = fmaxf(m, slope * m);
+        if (ok) store1(drow + 16 * j + p, m);
+      }
+    } else {
+      // a lane's accumulator rows are channels 4 kq .. +3 of pixel p
+      const int oy = oy0 + py, ox = ox0 + pxl;
+      const bool ok = (oy - tl.cy0) < tl.ch && (ox - tl.cx0) < tl.cw;
+      uint16_t* drow = dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * COUT;
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          v[r] = fmaf(acc[j][r], sc[j][r], bi[j][r]);
+          v[r] = fmaxf(v[r], slope * v[r]);
+        }
+        if (ok) store4<MAFAT_BF16>(drow + 16 * j + 4 * kq, v);
+      }
+    }
+  }
+  MAFAT_TRACE(3);
+}
+
+
 // Lone 2x2/2 max-pool: 64 output pixels per block, 4 threads per pixel
 // striding over channels.  The computed rectangle is in pool-output
 // coordinates.
@@ -677,14 +947,16 @@ __global__ __launch_bounds__(256) void pool_kernel(const StageArgs a) {
 
 template <int DT, int F, bool POOL, int DEPTH>
 hipError_t launch_mfma(MfmaShape sh, const StageArgs& args, hipStream_t stream) {
-  const dim3 grid(static_cast<unsigned>(args.total_blocks)), block(256);
-#define MAFAT_SHAPE(bm_, bn_)                                                                  \
-  if (sh.bm == (bm_) && sh.bn == (bn_)) {                                                      \
-    hipLaunchKernelGGL((conv_mfma_kernel<DT, F, bm_, bn_, POOL, DEPTH>), grid, block, 0, stream, args); \
+  const dim3 grid(static_cast<unsigned>(args.total_blocks));
+#define MAFAT_SHAPE(bm_, bn_, kg_)                                                             \
+  if (sh.bm == (bm_) && sh.bn == (bn_) && sh.kg == (kg_)) {                                    \
+    hipLaunchKernelGGL((conv_mfma_kernel<DT, F, bm_, bn_, POOL, DEPTH, kg_>), grid, dim3(256 * (kg_)), 0, \
+                       stream, args);                                                          \
     return hipGetLastError();                                                                  \
   }
-  MAFAT_SHAPE(128, 128) MAFAT_SHAPE(128, 64) MAFAT_SHAPE(64, 128) MAFAT_SHAPE(64, 64)
-  MAFAT_SHAPE(64, 32) MAFAT_SHAPE(32, 64) MAFAT_SHAPE(32, 32)
+  MAFAT_SHAPE(128, 128, 1) MAFAT_SHAPE(128, 64, 1) MAFAT_SHAPE(64, 128, 1) MAFAT_SHAPE(64, 64, 1)
+  MAFAT_SHAPE(64, 32, 1) MAFAT_SHAPE(32, 64, 1) MAFAT_SHAPE(32, 32, 1)
+  MAFAT_SHAPE(128, 128, 2) MAFAT_SHAPE(128, 64, 2) MAFAT_SHAPE(64, 128, 2) MAFAT_SHAPE(64, 64, 2)
 #undef MAFAT_SHAPE
   return hipErrorInvalidValue;
 }
@@ -699,6 +971,16 @@ hipError_t launch_conv(int kind, MfmaShape sh, const StageArgs& args, hipStream_
   if (kind == K_CONV_RGB) {
     if (F != 3) return hipErrorInvalidValue;
     hipLaunchKernelGGL((conv_rgb_kernel<DT, POOL>), grid, block, 0, stream, args);
+    return hipGetLastError();
+  }
+  if (kind == K_CONV_RGB_MFMA) {
+    if (F != 3 || DT != MAFAT_BF16) return hipErrorInvalidValue;
+    switch (sh.bn) {  // c_out
+      case 16: hipLaunchKernelGGL((conv_rgb_mfma_kernel<POOL, 1>), grid, block, 0, stream, args); break;
+      case 32: hipLaunchKernelGGL((conv_rgb_mfma_kernel<POOL, 2>), grid, block, 0, stream, args); break;
+      case 64: hipLaunchKernelGGL((conv_rgb_mfma_kernel<POOL, 4>), grid, block, 0, stream, args); break;
+      default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
   }
   switch (sh.depth) {

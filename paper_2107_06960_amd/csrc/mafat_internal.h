@@ -74,6 +74,7 @@ namespace mafat {
 struct StageConfig {
   int kind;          // KernelKind
   int bm, bn, depth; // matrix-core kernel block tile and pipeline depth
+  int kg;            // matrix-core kernel K groups (1 or 2, see MfmaShape)
   int chan_major;    // block order (see StageArgs::chan_major)
   int64_t blocks;    // output blocks per frame (pixel blocks x channel blocks)
 };

@@ -44,7 +44,7 @@ bool rgb_ok(const Stage& S) {
          (S.cout == 8 || S.cout == 16 || S.cout == 32 || S.cout == 64);
 }
 
-// Tuning builds only: MAFAT_TUNE="first_layer:bm,bn,depth[,chan_major[,kind]];..."
+// Tuning builds only: MAFAT_TUNE="first_layer:bm,bn,depth[,chan_major[,kg]];..."
 // forces the configuration of the stage starting at first_layer.
 StageConfig tune_override(const Stage& S, StageConfig c) {
 #ifdef MAFAT_TUNING
@@ -54,13 +54,13 @@ StageConfig tune_override(const Stage& S, StageConfig c) {
     while (pos < e.size()) {
       size_t end = e.find(';', pos);
       if (end == std::string::npos) end = e.size();
-      int l, bm, bn, dp, cm = -1, kd = -1;
+      int l, bm, bn, dp, cm = -1, kg = -1;
       const int got = std::sscanf(e.substr(pos, end - pos).c_str(), "%d:%d,%d,%d,%d,%d", &l, &bm, &bn, &dp,
-                                  &cm, &kd);
+                                  &cm, &kg);
       if (got >= 4 && l == S.first) {
         c.bm = bm; c.bn = bn; c.depth = dp;
         if (cm >= 0) c.chan_major = cm;
-        if (kd >= 0) c.kind = kd;
+        if (kg >= 1) c.kg = kg;
         int64_t mb = 0;
         for (const TileGeom& T : S.tiles) mb += (static_cast<int64_t>(T.ch) * T.cw + bm - 1) / bm;
         c.blocks = mb * ((S.cout + bn - 1) / bn);
@@ -84,11 +84,16 @@ StageConfig tune_override(const Stage& S, StageConfig c) {
 // re-read fewer operands, smaller ones give more workgroups.
 StageConfig choose_config(const Stage& S, int batch, int dtype) {
   StageConfig c{};
-  c.bm = 64; c.bn = 64; c.depth = 3;
+  c.bm = 64; c.bn = 64; c.depth = 3; c.kg = 1;
   if (S.kind == STAGE_POOL) { c.kind = K_POOL; return c; }
   if (!mfma_ok(S, dtype)) {
     c.kind = rgb_ok(S) ? K_CONV_RGB : K_CONV_DIRECT;
-    return c;
+    // bf16 first layer with 16/32/64 outputs: K = 27 padded to one MFMA K.
+    if (c.kind == K_CONV_RGB && dtype == MAFAT_BF16 && (S.cout == 16 || S.cout == 32 || S.cout == 64)) {
+      c.kind = K_CONV_RGB_MFMA;
+      c.bn = S.cout;
+    }
+    return tune_override(S, c);
   }
   c.kind = K_CONV_MFMA;
   const int esz = (dtype == MAFAT_BF16) ? 2 : 4;
@@ -128,6 +133,11 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
     const double chan_major = w_bytes * std::max(1.0, 8.0 / nb) + a_bytes * std::min(8.0, nb);
     c.chan_major = chan_major < pix_major ? 1 : 0;
   }
+  // Two K groups (8 waves) when the grid gives a CU at most two workgroups
+  // and the block allows it: the second wave per SIMD hides the latency of
+  // the per-stage barrier / LDS / MFMA chain.  (Larger grids already put
+  // several workgroups on a CU.)
+  c.kg = (c.bm >= 64 && c.bn >= 64 && c.blocks * batch <= 2 * 256) ? 2 : 1;
   // Pipeline depth: stages of K loaded ahead (3 to 6).  The stage count is
   // padded to a multiple of the depth, so take the deepest one whose padding
   // is at most one stage, or none for short K.
@@ -179,7 +189,8 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
     if (plan->layers[l].op == MAFAT_CONV) {
       if (!w || !scale || !bias || !w[l] || !scale[l] || !bias[l])
         return fail(MAFAT_EINVAL, "layer " + std::to_string(l) + ": missing weights, scale or bias");
-      if (!aligned16(w[l])) return fail(MAFAT_EINVAL, "layer " + std::to_string(l) + ": weights not 16-byte aligned");
+      if (!aligned16(w[l]) || !aligned16(scale[l]) || !aligned16(bias[l]))
+        return fail(MAFAT_EINVAL, "layer " + std::to_string(l) + ": weights, scale or bias not 16-byte aligned");
     }
 
   const int ns = static_cast<int>(G.stages.size());
@@ -194,7 +205,7 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
     const int64_t src_frame_elems = (S.src_buf == BUF_GROUP_IO) ? in_frame : scr_frame;
     if (kind == K_CONV_MFMA && src_frame_elems * static_cast<int64_t>(esz) >= (1ll << 31)) kind = K_CONV_DIRECT;
     const bool matrix = (kind == K_CONV_MFMA);
-    const MfmaShape shape{cfg.bm, cfg.bn, cfg.depth};
+    const MfmaShape shape{cfg.bm, cfg.bn, cfg.depth, cfg.kg};
     const int bu = (kind == K_CONV_RGB) ? 256 / (S.cout / 8) : block_units(kind, shape);
     StageArgs A;
     std::memset(&A, 0, sizeof(A));
@@ -230,7 +241,11 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
         k.dst_off = static_cast<int32_t>(T.dst_off);
         int64_t units = static_cast<int64_t>(T.ch) * T.cw;
         if ((kind == K_CONV_DIRECT || kind == K_CONV_RGB) && S.pool) units /= 4;
-        total += (units + bu - 1) / bu;
+        if (kind == K_CONV_RGB_MFMA)  // 2-D blocks of conv outputs
+          total += static_cast<int64_t>((T.ch + kRgbBlockRows - 1) / kRgbBlockRows) *
+                   ((T.cw + kRgbBlockCols - 1) / kRgbBlockCols);
+        else
+          total += (units + bu - 1) / bu;
         A.mblk_prefix[t - t0 + 1] = static_cast<int32_t>(total);
       }
       A.mblk_total = static_cast<int32_t>(total);
@@ -241,7 +256,7 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
       if (e != hipSuccess)
         return fail(MAFAT_EHIP, std::string("stage launch failed: ") + hipGetErrorString(e));
 #ifdef MAFAT_TUNING
-      if (std::getenv("MAFAT_TRACE_DUMP") && kind == K_CONV_MFMA) {
+      if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_MFMA || kind == K_CONV_RGB_MFMA)) {
         long long tr[4][64];
         hipStreamSynchronize(stream);
         mafat_debug_trace(&tr[0][0]);
