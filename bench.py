@@ -167,25 +167,33 @@ def csrc_digest():
 
 def measured_traffic(workload, stage_layers):
     """HBM bytes per launch of a stage from a committed counter summary
-    (profiles/traffic_*.txt, 'key: value' lines): FETCH_SIZE + WRITE_SIZE
-    per dispatch, each scaled by bytes / counter of a plain copy of known
-    size.  None if no summary matches this workload, stage and sources."""
+    (profiles/traffic_*.txt): 'key: value' header lines (workload,
+    csrc_sha256, copy_bytes, copy_fetch_kib, copy_write_kib) and one line per
+    stage, 'stage A-B: fetch_kib=F write_kib=W' (FETCH_SIZE / WRITE_SIZE per
+    dispatch).  Each counter is scaled by the bytes of a plain copy of known
+    size over what the same counter reads for it.  None if no summary
+    matches this workload, stage and sources."""
     import glob
     digest = csrc_digest()
+    want = f"stage {stage_layers[0]}-{stage_layers[1]}"
     for path in sorted(glob.glob(os.path.join(ROOT, "profiles", "traffic_*.txt"))):
-        kv = {}
+        kv, stages = {}, {}
         with open(path) as fh:
             for line in fh:
-                if ":" in line and not line.startswith("#"):
-                    k, v = line.split(":", 1)
+                line = line.strip()
+                if not line or line.startswith("#") or ":" not in line:
+                    continue
+                k, v = line.split(":", 1)
+                if k.startswith("stage "):  # "stage A-B: fetch_kib=F write_kib=W  # kernel name"
+                    stages[k.strip()] = dict(f.split("=", 1) for f in v.split("#")[0].split())
+                else:
                     kv[k.strip()] = v.strip()
+        if kv.get("workload") != workload or kv.get("csrc_sha256") != digest or want not in stages:
+            continue
         try:
-            if (kv.get("workload") != workload or kv.get("stage_layers") != f"{stage_layers[0]}-{stage_layers[1]}"
-                    or kv.get("csrc_sha256") != digest):
-                continue
             cb = float(kv["copy_bytes"])
-            fetch = float(kv["fetch_kib_per_dispatch"]) * cb / float(kv["copy_fetch_kib"])
-            write = float(kv["write_kib_per_dispatch"]) * cb / float(kv["copy_write_kib"])
+            fetch = float(stages[want]["fetch_kib"]) * cb / float(kv["copy_fetch_kib"])
+            write = float(stages[want]["write_kib"]) * cb / float(kv["copy_write_kib"])
         except (KeyError, ValueError, ZeroDivisionError):
             continue
         return {"bytes": round(fetch + write), "fetch_bytes": round(fetch), "write_bytes": round(write),
@@ -307,9 +315,9 @@ def main():
         for s, (a, b) in enumerate(stages[g]):
             f = flops[g][s] * wl.batch
             t = stage_ms[g][s]
-            # the 3-channel first layer runs on the vector ALUs, the rest on
-            # the matrix cores
-            vec = plan.layers[a]["op"] == "conv" and plan.shape(a)[2] == 3
+            # the 3-channel first layer runs on the vector ALUs in fp32 (on
+            # the matrix cores in bf16), the rest on the matrix cores
+            vec = plan.layers[a]["op"] == "conv" and plan.shape(a)[2] == 3 and wl.dtype == "f32"
             pk, bound = (PEAK_VALU_TFLOPS, "alu") if vec else (peak, "mfma")
             per_stage.append({"group": g, "layers": [a, b], "ms": round(t, 5),
                               "gflop": round(f / 1e9, 4), "bound": bound, "peak_tflops": pk,
