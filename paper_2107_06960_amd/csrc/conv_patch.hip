@@ -1,0 +1,317 @@
+// conv_patch.hip -- bf16 3x3 convolution stage (stride 1, zero padding
+// outside the image, folded batch-norm scale/bias, activation, optional
+// fused 2x2/2 max-pool) on the matrix cores, with the input patch of a 2-D
+// block of output pixels staged in LDS once per channel chunk and shared by
+// all nine filter taps.
+//
+// Why: as an implicit GEMM with im2col rows, every input pixel is fetched
+// once per tap (nine times).  Here a workgroup owns a BR x BC block of conv
+// outputs of one tile (and BN output channels); for each chunk of 32 input
+// channels it loads the (BR+2) x (BC+2) input patch (64 bytes per pixel)
+// and the nine 64-byte tap slices of its BN weight rows, and runs the nine
+// taps' MFMAs from LDS, the A operand of tap (ky, kx) being the patch
+// shifted by (ky, kx).
+//
+// GEMM view per chunk and tap: M = the block's pixels (row r <-> pixel
+// (r / BC, r % BC), or with a fused pool every 4 consecutive rows one 2x2
+// window), N = BN output channels, K = 32 channels:
+// one v_mfma_f32_16x16x32_bf16 per 16x16 accumulator tile.
+//
+// Data movement: a ring of NS slots in LDS, slot = [patch pixels x 64 B]
+// [9 taps x BN rows x 64 B]; chunk c lives in slot c % NS.  Loads are
+// buffer_load_dwordx4 ... lds (global -> LDS, 64 lanes = 1 KiB = 16 rows of
+// 64 bytes per instruction): lane l writes row (l >> 2) of its 16-row group
+// at 16-byte position (l & 3) and fetches the row's 16-byte chunk
+// (l & 3) ^ ((row >> 1) & 3), so MFMA fragment reads of consecutive rows at
+// one K offset hit distinct LDS banks.  Patch pixels outside the image (the
+// zero padding), outside the tile's source region, or past the patch, and
+// weight rows past c_out, are fetched at an offset with bit 31 set, past the
+// buffer descriptor's range: the range check returns zeros.  Loads run NS-1
+// chunks ahead; every chunk costs one explicit vmcnt wait and one barrier.
+//
+// Requires f = 3, c_in % 32 == 0, c_out % 16 == 0, byte offsets below 2^31
+// within a frame's source buffer and within the weights (host-checked); a
+// fused pool needs even block sizes and even tile origins and extents.
+#include <hip/hip_runtime.h>
+
+#include "device_util.h"
+#include "kernel_args.h"
+
+namespace mafat {
+namespace {
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+template <int N>
+__device__ __forceinline__ void pwait_vmcnt() {
+  static_assert(N >= 0 && N <= 63, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+template <int L, int R>
+__device__ __forceinline__ void pwait_stage(int rem) {
+  if constexpr (R == 0) {
+    pwait_vmcnt<0>();
+  } else {
+    if (rem >= R) {
+      pwait_vmcnt<R * L>();
+    } else {
+      pwait_stage<L, R - 1>(rem);
+    }
+  }
+}
+__device__ __forceinline__ void pbarrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// Byte offset of 16-byte chunk q of 64-byte row `row` in a slot region.
+__device__ __forceinline__ int swz(int row, int q) { return row * 64 + ((q ^ ((row >> 1) & 3)) << 4); }
+
+// Block pixel (py, px) of GEMM row r.
+template <int BC, bool POOL>
+__device__ __forceinline__ void block_pixel(int r, int* py, int* px) {
+  if (POOL) {
+    constexpr int WC = BC / 2;  // windows per block row
+    const int q = r >> 2, s = r & 3, wy = q / WC;
+    *py = 2 * wy + (s >> 1);
+    *px = 2 * (q - wy * WC) + (s & 1);
+  } else {
+    *py = r / BC;
+    *px = r - (r / BC) * BC;
+  }
+}
+
+template <int BR, int BC, int BM, int BN, int WGM, int WGN, int NS, bool POOL>
+__global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageArgs a) {
+  constexpr int NWAVE = WGM * WGN;
+  constexpr int WM = BM / WGM, WN = BN / WGN, MT = WM / 16, NT = WN / 16;
+  constexpr int PR = BR + 2, PC = BC + 2;
+  constexpr int PPX = (PR * PC + 15) / 16 * 16;  // patch rows (pixels), whole 16-row groups
+  constexpr int A_BYTES = PPX * 64;
+  constexpr int B_ROWS = 9 * BN;
+  constexpr int SLOT = A_BYTES + B_ROWS * 64;
+  constexpr int NA = PPX / 16, NB = B_ROWS / 16;  // load instructions per chunk
+  constexpr int NAW = (NA + NWAVE - 1) / NWAVE, NBW = (NB + NWAVE - 1) / NWAVE;
+  constexpr bool SINK = (NAW * NWAVE != NA) || (NBW * NWAVE != NB);
+  constexpr int LPS = NAW + NBW;  // loads per thread per chunk
+  static_assert(MT >= 1 && NT >= 1 && MT * 16 == WM && NT * 16 == WN, "wave tile");
+  static_assert(BR * BC <= BM && BM % (16 * WGM) == 0, "block rows");
+  static_assert(!POOL || (BR % 2 == 0 && BC % 2 == 0), "pooled blocks cover whole windows");
+  static_assert(NS >= 2 && NS <= 6 && (NS - 2) * LPS <= 63, "ring depth");
+  __shared__ __align__(1024) unsigned char smem[NS * SLOT + (SINK ? 1024 : 0)];
+
+  KTile tl;
+  const BlockPos bp = decode_block(a, &tl);
+  const int tid = static_cast<int>(threadIdx.x), lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave - wm * WGN;
+  const int nbx = (tl.cw + BC - 1) / BC;
+  const int bby = bp.mb / nbx, bbx = bp.mb - bby * nbx;
+  const int by0 = tl.cy0 + bby * BR, bx0 = tl.cx0 + bbx * BC;  // block origin (conv outputs)
+  const int n0 = bp.nb * BN;
+  const int cin = a.cin, cout = a.cout, sw = tl.sw;
+  const int64_t sbase = bp.frame * a.src_fstride + tl.src_off;
+  uint16_t* dst = static_cast<uint16_t*>(a.dst) + bp.frame * a.dst_fstride + tl.dst_off;
+  const int K = 9 * cin;
+  const int nstage = cin >> 5;
+  const __amdgpu_buffer_rsrc_t rsa = make_rsrc(static_cast<const uint16_t*>(a.src) + sbase,
+                                               static_cast<unsigned>((a.src_fstride - tl.src_off) * 2));
+  const __amdgpu_buffer_rsrc_t rsb = make_rsrc(a.w, static_cast<unsigned>(cout * K * 2));
+
+  // Scale and bias of this lane's output channels.
+  float sc[NT][4], bi[NT][4];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    if (POOL) {
+      const int co = n0 + wn * WN + j * 16 + (lane & 15);
+      const int cc = co < cout ? co : 0;
+      sc[j][0] = a.scale[cc];
+      bi[j][0] = a.bias[cc];
+    } else {
+      const int co = n0 + wn * WN + j * 16 + 4 * (lane >> 4);
+      const int cc = co < cout ? co : 0;
+      const f32x4 s4 = *reinterpret_cast<const f32x4*>(a.scale + cc);
+      const f32x4 b4 = *reinterpret_cast<const f32x4*>(a.bias + cc);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) { sc[j][r] = s4[r]; bi[j][r] = b4[r]; }
+    }
+  }
+
+  // This lane's loads (chunk 0; chunk c adds 64 c bytes).  Instruction g of
+  // a chunk: g < NA fills patch rows [16 g, 16 g + 16), else weight rows
+  // [16 (g - NA), +16) (row = tap * BN + n); g past NA + NB fills the sink.
+  const int lrow = lane >> 2, lpos = lane & 3;
+  // Source region of the tile: the conv outputs [cy0, cy0 + ch) read rows
+  // [cy0 - 1, cy0 + ch] (columns likewise), clipped to the image.
+  const int ry0 = max(tl.cy0 - 1, 0), ry1 = min(tl.cy0 + tl.ch + 1, a.in_h);
+  const int rx0 = max(tl.cx0 - 1, 0), rx1 = min(tl.cx0 + tl.cw + 1, a.in_w);
+  unsigned a_off[NAW], b_off[NBW];
+#pragma unroll
+  for (int k = 0; k < NAW; ++k) {
+    const int g = k * NWAVE + wave;
+    const int p = 16 * g + lrow;
+    const int py = p / PC, px = p - (p / PC) * PC;
+    const int iy = by0 - 1 + py, ix = bx0 - 1 + px;
+    const bool ok = g < NA && p < PR * PC && iy >= ry0 && iy < ry1 && ix >= rx0 && ix < rx1;
+    const int chunk = lpos ^ ((p >> 1) & 3);
+    a_off[k] = ok ? static_cast<unsigned>((((iy - tl.sy0) * sw + (ix - tl.sx0)) * cin) * 2 + chunk * 16)
+                  : 0x80000000u;
+  }
+#pragma unroll
+  for (int k = 0; k < NBW; ++k) {
+    const int g = k * NWAVE + wave;
+    const int row = 16 * g + lrow;           // weight row within the slot
+    const int t = row / BN, n = row - t * BN;
+    const int co = n0 + n;
+    const int chunk = lpos ^ ((row >> 1) & 3);
+    b_off[k] = (g < NB && co < cout) ? static_cast<unsigned>((co * K + t * cin) * 2 + chunk * 16)
+                                     : 0x80000000u;
+  }
+  auto issue = [&](int c, int slot) {
+    unsigned char* sl = smem + slot * SLOT;
+    const unsigned coff = static_cast<unsigned>(c * 64);
+#pragma unroll
+    for (int k = 0; k < NAW; ++k) {
+      const int g = k * NWAVE + wave;
+      unsigned char* d = (g < NA) ? sl + g * 1024 : smem + NS * SLOT;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, (lds_ptr_t)d, 16,
+                                               static_cast<int>(a_off[k] + coff), 0, 0, 0);
+    }
+#pragma unroll
+    for (int k = 0; k < NBW; ++k) {
+      const int g = k * NWAVE + wave;
+      unsigned char* d = (g < NB) ? sl + A_BYTES + g * 1024 : smem + NS * SLOT;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, (lds_ptr_t)d, 16,
+                                               static_cast<int>(b_off[k] + coff), 0, 0, 0);
+    }
+  };
+
+  // Fragment reads.  A: lane l supplies GEMM row wm*WM + 16 i + (l & 15),
+  // i.e. block pixel (py, px), as patch row (py + ky) * PC + (px + kx) at
+  // 16-byte chunk q = l >> 4 (K elements 8q .. 8q+7 of the 32).  B: weight
+  // row tap * BN + wn*WN + 16 j + (l & 15), chunk q.
+  const int q = lane >> 4;
+  int p0[MT];
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    int r = wm * WM + i * 16 + (lane & 15);
+    r = (r < BR * BC) ? r : 0;  // padding rows: any valid pixel, result discarded
+    int py, px;
+    block_pixel<BC, POOL>(r, &py, &px);
+    p0[i] = py * PC + px;
+  }
+  const int rb = wn * WN + (lane & 15);
+  const int b_lane = A_BYTES + swz(rb, q);  // (tap * BN + 16 j) rows later: same swizzle
+
+  f32x4 acc[NT][MT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j)
+#pragma unroll
+    for (int i = 0; i < MT; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](int slot) {
+    const unsigned char* sp = smem + slot * SLOT;
+#pragma unroll
+    for (int t = 0; t < 9; ++t) {
+      const int toff = (t / 3) * PC + (t % 3);
+      u32x4 af[MT], bfr[NT];
+#pragma unroll
+      for (int i = 0; i < MT; ++i) af[i] = *reinterpret_cast<const u32x4*>(sp + swz(p0[i] + toff, q));
+#pragma unroll
+      for (int j = 0; j < NT; ++j)
+        bfr[j] = *reinterpret_cast<const u32x4*>(sp + b_lane + (t * BN + j * 16) * 64);
+#pragma unroll
+      for (int i = 0; i < MT; ++i)
+#pragma unroll
+        for (int j = 0; j < NT; ++j) {
+          if constexpr (POOL) mma<MAFAT_BF16>(acc[j][i], af[i], bfr[j]);
+          else mma<MAFAT_BF16>(acc[j][i], bfr[j], af[i]);
+        }
+    }
+  };
+
+#pragma unroll
+  for (int p = 0; p < NS - 1; ++p)
+    if (p < nstage) issue(p, p);
+  int slot = 0;
+  for (int s = 0; s < nstage; ++s) {
+    pwait_stage<LPS, NS - 2>(nstage - 1 - s);
+    pbarrier();
+    if (s + NS - 1 < nstage) issue(s + NS - 1, slot == 0 ? NS - 1 : slot - 1);
+    compute(slot);
+    slot = (slot == NS - 1) ? 0 : slot + 1;
+  }
+
+  // Epilogue: folded batch-norm, activation (leaky: max(v, 0.1 v)), the
+  // fused pool, round to bf16, store the pixels inside the tile's computed
+  // rectangle.
+  const float slope = act_slope(a.act);
+  const int vy = tl.cy0 + tl.ch - by0, vx = tl.cx0 + tl.cw - bx0;  // valid extent of this block
+#pragma unroll
+  for (int i = 0; i < MT; ++i) {
+    int oy, ox;
+    bool ok;
+    if (POOL) {
+      const int r = wm * WM + i * 16 + 4 * (lane >> 4);  // first row of this lane's window
+      int py, px;
+      block_pixel<BC, true>(r < BR * BC ? r : 0, &py, &px);
+      ok = r < BR * BC && py < vy && px < vx;
+      oy = (by0 + py) >> 1;
+      ox = (bx0 + px) >> 1;
+    } else {
+      const int r = wm * WM + i * 16 + (lane & 15);
+      int py, px;
+      block_pixel<BC, false>(r < BR * BC ? r : 0, &py, &px);
+      ok = r < BR * BC && py < vy && px < vx;
+      oy = by0 + py;
+      ox = bx0 + px;
+    }
+    uint16_t* drow = dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * cout;
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      if (POOL) {
+        const int co = n0 + wn * WN + j * 16 + (lane & 15);
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = fmaf(acc[j][i][r], sc[j][0], bi[j][0]);
+        float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+        mx = fmaxf(mx, slope * mx);
+        if (ok && co < cout) store1(drow + co, mx);
+      } else {
+        const int co = n0 + wn * WN + j * 16 + 4 * (lane >> 4);
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          v[r] = fmaf(acc[j][i][r], sc[j][r], bi[j][r]);
+          v[r] = fmaxf(v[r], slope * v[r]);
+        }
+        if (ok && co < cout) store4<MAFAT_BF16>(drow + co, v);
+      }
+    }
+  }
+}
+
+template <bool POOL>
+hipError_t launch_patch_p(const MfmaShape& sh, const StageArgs& args, hipStream_t stream) {
+  const dim3 grid(static_cast<unsigned>(args.total_blocks));
+#define MAFAT_PATCH(br_, bc_, bm_, bn_, wgm_, wgn_, ns_)                                               \
+  if (sh.br == (br_) && sh.bc == (bc_) && sh.bm == (bm_) && sh.bn == (bn_) && sh.wgm == (wgm_) &&      \
+      sh.wgn == (wgn_) && sh.depth == (ns_)) {                                                        \
+    if constexpr (!POOL || ((br_) % 2 == 0 && (bc_) % 2 == 0)) {                                      \
+      hipLaunchKernelGGL((conv_patch_kernel<br_, bc_, bm_, bn_, wgm_, wgn_, ns_, POOL>), grid,         \
+                         dim3(64 * (wgm_) * (wgn_)), 0, stream, args);                                 \
+      return hipGetLastError();                                                                       \
+    }                                                                                                 \
+    return hipErrorInvalidValue;                                                                      \
+  }
+  MAFAT_PATCH_SHAPES
+  MAFAT_PATCH_TUNE_SHAPES
+#undef MAFAT_PATCH
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs& args, hipStream_t stream) {
+  if (args.total_blocks <= 0) return hipSuccess;
+  return pool ? launch_patch_p<true>(shape, args, stream) : launch_patch_p<false>(shape, args, stream);
+}
+
+}  // namespace mafat

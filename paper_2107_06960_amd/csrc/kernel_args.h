@@ -40,7 +40,15 @@ struct StageArgs {
 };
 
 // Kernel families the runtime picks from.
-enum KernelKind { K_CONV_MFMA = 0, K_CONV_DIRECT = 1, K_POOL = 2, K_CONV_RGB = 3, K_CONV_RGB_MFMA = 4 };
+enum KernelKind {
+  K_CONV_MFMA = 0,      // matrix cores, operands staged through registers (fp32)
+  K_CONV_DIRECT = 1,    // vector ALUs, any shape
+  K_POOL = 2,           // lone max-pool
+  K_CONV_RGB = 3,       // 3-channel first layer, vector ALUs
+  K_CONV_RGB_MFMA = 4,  // 3-channel first layer, matrix cores (bf16)
+  K_CONV_RING = 5,      // matrix cores, operands streamed into an LDS ring (bf16)
+  K_CONV_PATCH = 6      // 3x3 on the matrix cores, input patch shared by the taps (bf16)
+};
 
 // Conv outputs (rows x columns) per workgroup of the matrix-core first-layer
 // kernel.
@@ -50,14 +58,63 @@ constexpr int kRgbBlockRows = 32, kRgbBlockCols = 32;
 // depth of its load pipeline (3 to 6 stages of 128 bytes of K in flight) and
 // the number of K groups (1: 4 waves; 2: 8 waves, each group of 4 multiplies
 // one 64-byte half of every stage).
+// For the LDS-ring kernel, depth is the number of ring slots, wgm x wgn
+// the wave arrangement of one K group and kord the K order (0: tap-major,
+// 1: channel-block-major).
 struct MfmaShape {
   int bm, bn, depth, kg;
+  int wgm, wgn, kord;
+  int br, bc;  // patch kernel: block of br x bc conv outputs (bm >= br * bc GEMM rows)
 };
+
+// Instantiated patch kernel shapes: (br, bc, bm, bn, wgm, wgn, ring slots).
+#define MAFAT_PATCH_SHAPES                \
+  MAFAT_PATCH(8, 16, 128, 64, 2, 2, 3)    \
+  MAFAT_PATCH(8, 8, 64, 64, 2, 2, 3)      \
+  MAFAT_PATCH(8, 16, 128, 32, 2, 2, 4)    \
+  MAFAT_PATCH(16, 16, 256, 64, 2, 2, 2)   \
+  MAFAT_PATCH(10, 10, 128, 32, 2, 2, 4)   \
+  MAFAT_PATCH(8, 8, 64, 32, 2, 2, 4)      \
+  MAFAT_PATCH(4, 16, 64, 64, 2, 2, 3)     \
+  MAFAT_PATCH(16, 16, 256, 32, 2, 2, 3)
+#ifdef MAFAT_TUNING
+#define MAFAT_PATCH_TUNE_SHAPES           \
+  MAFAT_PATCH(8, 16, 128, 64, 2, 2, 2)    \
+  MAFAT_PATCH(4, 8, 32, 64, 2, 2, 3)      \
+  MAFAT_PATCH(16, 32, 512, 32, 2, 2, 2)
+#else
+#define MAFAT_PATCH_TUNE_SHAPES
+#endif
+
+// Instantiated LDS-ring kernel shapes: (bm, bn, wgm, wgn, kg, ring slots, K order).
+#define MAFAT_RING_SHAPES             \
+  MAFAT_RING(32, 64, 2, 2, 1, 3, 1)   \
+  MAFAT_RING(64, 32, 2, 2, 1, 3, 1)   \
+  MAFAT_RING(64, 64, 2, 2, 1, 3, 1)   \
+  MAFAT_RING(128, 64, 2, 2, 2, 4, 1)  \
+  MAFAT_RING(128, 128, 2, 2, 2, 3, 1)
+#ifdef MAFAT_TUNING
+#define MAFAT_RING_TUNE_SHAPES        \
+  MAFAT_RING(64, 64, 2, 2, 2, 6, 1)   \
+  MAFAT_RING(64, 64, 2, 2, 1, 4, 1)   \
+  MAFAT_RING(32, 64, 2, 2, 1, 6, 1)   \
+  MAFAT_RING(32, 64, 2, 2, 1, 4, 1)   \
+  MAFAT_RING(32, 64, 2, 2, 1, 3, 0)
+#else
+#define MAFAT_RING_TUNE_SHAPES
+#endif
 
 // Launch one stage chunk.  `units_per_block` is what the kernel covers per
 // block along the pixel axis (used to fill mblk_prefix by the caller).
 hipError_t launch_stage(int kind, int dtype, int f, bool pool, MfmaShape shape,
                         const StageArgs& args, hipStream_t stream);
+
+// Launch one bf16 LDS-ring convolution stage chunk (conv_ring.hip).
+hipError_t launch_conv_ring(int f, bool pool, const MfmaShape& shape, const StageArgs& args,
+                            hipStream_t stream);
+
+// Launch one bf16 3x3 patch-kernel stage chunk (conv_patch.hip).
+hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs& args, hipStream_t stream);
 
 // Pixel-axis block size of each kernel family.
 int block_units(int kind, MfmaShape shape);

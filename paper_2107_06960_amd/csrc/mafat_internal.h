@@ -75,6 +75,9 @@ struct StageConfig {
   int kind;          // KernelKind
   int bm, bn, depth; // matrix-core kernel block tile and pipeline depth
   int kg;            // matrix-core kernel K groups (1 or 2, see MfmaShape)
+  int kord;          // LDS-ring kernel K order (see MfmaShape)
+  int br, bc;        // patch kernel block (see MfmaShape)
+  int wgm, wgn;      // wave arrangement (see MfmaShape)
   int chan_major;    // block order (see StageArgs::chan_major)
   int64_t blocks;    // output blocks per frame (pixel blocks x channel blocks)
 };

@@ -15,6 +15,7 @@
 
 #ifdef MAFAT_TUNING
 extern "C" int mafat_debug_trace(long long* host_out);
+extern "C" int mafat_debug_ring_trace(long long* host_out);
 #endif
 
 namespace mafat {
@@ -44,8 +45,10 @@ bool rgb_ok(const Stage& S) {
          (S.cout == 8 || S.cout == 16 || S.cout == 32 || S.cout == 64);
 }
 
-// Tuning builds only: MAFAT_TUNE="first_layer:bm,bn,depth[,chan_major[,kg]];..."
-// forces the configuration of the stage starting at first_layer.
+// Tuning builds only: MAFAT_TUNE="first_layer:bm,bn,depth[,chan_major[,kg[,kind[,kord[,br,bc]]]]];..."
+// forces the configuration of the stage starting at first_layer (kind: 0 the
+// register-staged matrix-core kernel, 5 the LDS-ring kernel, 6 the 3x3 patch
+// kernel).
 StageConfig tune_override(const Stage& S, StageConfig c) {
 #ifdef MAFAT_TUNING
   if (const char* env = std::getenv("MAFAT_TUNE")) {
@@ -54,16 +57,16 @@ StageConfig tune_override(const Stage& S, StageConfig c) {
     while (pos < e.size()) {
       size_t end = e.find(';', pos);
       if (end == std::string::npos) end = e.size();
-      int l, bm, bn, dp, cm = -1, kg = -1;
-      const int got = std::sscanf(e.substr(pos, end - pos).c_str(), "%d:%d,%d,%d,%d,%d", &l, &bm, &bn, &dp,
-                                  &cm, &kg);
+      int l, bm, bn, dp, cm = -1, kg = -1, kind = -1, ko = -1, br = -1, bc = -1;
+      const int got = std::sscanf(e.substr(pos, end - pos).c_str(), "%d:%d,%d,%d,%d,%d,%d,%d,%d,%d", &l, &bm,
+                                  &bn, &dp, &cm, &kg, &kind, &ko, &br, &bc);
       if (got >= 4 && l == S.first) {
         c.bm = bm; c.bn = bn; c.depth = dp;
         if (cm >= 0) c.chan_major = cm;
         if (kg >= 1) c.kg = kg;
-        int64_t mb = 0;
-        for (const TileGeom& T : S.tiles) mb += (static_cast<int64_t>(T.ch) * T.cw + bm - 1) / bm;
-        c.blocks = mb * ((S.cout + bn - 1) / bn);
+        if (kind >= 0) c.kind = kind;
+        if (ko >= 0) c.kord = ko;
+        if (br > 0 && bc > 0) { c.br = br; c.bc = bc; }
       }
       pos = end + 1;
     }
@@ -84,7 +87,7 @@ StageConfig tune_override(const Stage& S, StageConfig c) {
 // re-read fewer operands, smaller ones give more workgroups.
 StageConfig choose_config(const Stage& S, int batch, int dtype) {
   StageConfig c{};
-  c.bm = 64; c.bn = 64; c.depth = 3; c.kg = 1;
+  c.bm = 64; c.bn = 64; c.depth = 3; c.kg = 1; c.wgm = 2; c.wgn = 2;
   if (S.kind == STAGE_POOL) { c.kind = K_POOL; return c; }
   if (!mfma_ok(S, dtype)) {
     c.kind = rgb_ok(S) ? K_CONV_RGB : K_CONV_DIRECT;
@@ -95,27 +98,106 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
     }
     return tune_override(S, c);
   }
-  c.kind = K_CONV_MFMA;
   const int esz = (dtype == MAFAT_BF16) ? 2 : 4;
-  const int kcs = 64 / esz;                                   // channels per sub-chunk
-  const int nstage = (S.f * S.f * (S.cin / kcs) + 1) / 2;     // 128-byte K stages
   const double K = static_cast<double>(S.f) * S.f * S.cin;
-  const double clk = 2.4e9, mfma_rate = 4096.0 * clk, l2_rate = 64.0 * clk, t0 = 2e-6;
-  static const int kShapes[][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}, {64, 32}, {32, 64}};
-  double best = 1e30;
-  for (const auto& sh : kShapes) {
-    const int bm = sh[0], bn = sh[1];
-    if (bn > S.cout && bn > 32) continue;
+  if (dtype == MAFAT_BF16 && S.f == 3 && S.cin >= 256) {
+    // 3x3 patch kernel for the deep layers (many 32-channel chunks, few
+    // pixels): measured faster than the LDS-ring kernel there; on layers
+    // with fewer input channels the ring kernel's higher occupancy wins.
+    // Time model per workgroup (one per CU: the ring takes more than half
+    // the LDS) and chunk: the largest of its load bytes at ~27 bytes/clock
+    // (what one workgroup of 4 waves sustains from L2), its MFMA time at
+    // the CU's peak (4096 flop/clock) and its LDS fragment reads at 128
+    // bytes/clock; plus ~2 us per workgroup (decode, first loads,
+    // epilogue).  Edge blocks of a tile compute their full rectangle, so
+    // large blocks waste work on small tiles; rounds beyond 256 queue.
+    c.kind = K_CONV_PATCH;
+    c.wgm = 2; c.wgn = 2;
+    const int nstage = S.cin / 32;
+    struct PS { int br, bc, bm, bn, wgm, wgn, ns; };
+    static const PS kPatch[] = {
+#define MAFAT_PATCH(br_, bc_, bm_, bn_, wgm_, wgn_, ns_) {br_, bc_, bm_, bn_, wgm_, wgn_, ns_},
+        MAFAT_PATCH_SHAPES
+#undef MAFAT_PATCH
+    };
+    double best = 1e30;
+    for (const PS& r : kPatch) {
+      if (r.bn > S.cout && r.bn > 32) continue;
+      int64_t mb = 0;
+      for (const TileGeom& T : S.tiles)
+        mb += static_cast<int64_t>((T.ch + r.br - 1) / r.br) * ((T.cw + r.bc - 1) / r.bc);
+      const int64_t blocks = mb * ((S.cout + r.bn - 1) / r.bn);
+      const double wgs = static_cast<double>(blocks) * batch;
+      const int ppx = ((r.br + 2) * (r.bc + 2) + 15) / 16 * 16;
+      const double slot = (ppx + 9.0 * r.bn) * 64.0;
+      const int nw = r.wgm * r.wgn;
+      const double mt = r.bm / r.wgm / 16.0, nt = r.bn / r.wgn / 16.0;
+      const double loadc = slot / 27.0;
+      const double mfma = 2.0 * r.bm * r.bn * 288.0 / 4096.0;
+      const double ldsc = 9.0 * nw * (mt + nt) * 1024.0 / 128.0;
+      const double per = std::max(std::max(loadc, mfma), ldsc);
+      const double t = 2e-6 + std::ceil(wgs / 256.0) * nstage * per / 2.4e9;
+      if (t < best * 0.97) {
+        best = t;
+        c.br = r.br; c.bc = r.bc; c.bm = r.bm; c.bn = r.bn; c.wgm = r.wgm; c.wgn = r.wgn; c.depth = r.ns;
+        c.blocks = blocks;
+      }
+    }
+  } else if (dtype == MAFAT_BF16) {
+    // LDS-ring kernel.  Block shapes from a sweep over every YOLOv2 stage
+    // at 608x608 (tiling 5x5/8/2x2; blocks 32..128 x 32..128, ring depths
+    // 2..8, one or two K groups): the K loop of a workgroup is bound by LDS
+    // traffic and by the operand bytes it keeps in flight, so wide layers
+    // take large blocks with two K groups (8 waves), narrow ones small
+    // blocks with several workgroups per CU, and 1x1 layers with a long K
+    // the smallest block.
+    c.kind = K_CONV_RING;
+    c.depth = 3; c.kg = 1; c.kord = 1;
+    if (S.f == 1) {
+      c.bm = (S.cin >= 256 && S.cout >= 64) ? 32 : 64;
+      c.bn = (S.cout >= 64) ? 64 : 32;
+    } else if (S.cout >= 256) {
+      c.bm = 128; c.bn = 64; c.kg = 2; c.depth = 4;
+    } else if (S.cout >= 128) {
+      c.bm = 128; c.bn = 128; c.kg = 2; c.depth = 3;
+    } else {
+      c.bm = 64; c.bn = (S.cout >= 64) ? 64 : 32;
+    }
     int64_t mb = 0;
-    for (const TileGeom& T : S.tiles) mb += (static_cast<int64_t>(T.ch) * T.cw + bm - 1) / bm;
-    const int64_t blocks = mb * ((S.cout + bn - 1) / bn);
-    const double wgs = static_cast<double>(blocks) * batch;
-    const double flops = 2.0 * bm * bn * K, bytes = (bm + bn) * K * esz;
-    const double per_wg = std::max(flops / mfma_rate, bytes / l2_rate);
-    const double t = t0 + std::ceil(wgs / 256.0) * per_wg;
-    if (t < best * 0.97) {
-      best = t;
-      c.bm = bm; c.bn = bn; c.blocks = blocks;
+    for (const TileGeom& T : S.tiles) mb += (static_cast<int64_t>(T.ch) * T.cw + c.bm - 1) / c.bm;
+    c.blocks = mb * ((S.cout + c.bn - 1) / c.bn);
+  } else {
+    c.kind = K_CONV_MFMA;
+    const double clk = 2.4e9, mfma_rate = 4096.0 * clk, l2_rate = 64.0 * clk, t0 = 2e-6;
+    static const int kShapes[][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}, {64, 32}, {32, 64}};
+    double best = 1e30;
+    for (const auto& sh : kShapes) {
+      const int bm = sh[0], bn = sh[1];
+      if (bn > S.cout && bn > 32) continue;
+      int64_t mb = 0;
+      for (const TileGeom& T : S.tiles) mb += (static_cast<int64_t>(T.ch) * T.cw + bm - 1) / bm;
+      const int64_t blocks = mb * ((S.cout + bn - 1) / bn);
+      const double wgs = static_cast<double>(blocks) * batch;
+      const double flops = 2.0 * bm * bn * K, bytes = (bm + bn) * K * esz;
+      const double per_wg = std::max(flops / mfma_rate, bytes / l2_rate);
+      const double t = t0 + std::ceil(wgs / 256.0) * per_wg;
+      if (t < best * 0.97) {
+        best = t;
+        c.bm = bm; c.bn = bn; c.blocks = blocks;
+      }
+    }
+    // Two K groups (8 waves) when the grid gives a CU at most two
+    // workgroups and the block allows it: the second wave per SIMD hides
+    // the latency of the per-stage barrier / LDS / MFMA chain.
+    c.kg = (c.bm >= 64 && c.bn >= 64 && c.blocks * batch <= 2 * 256) ? 2 : 1;
+    // Pipeline depth: stages of K loaded ahead (3 to 6).  The stage count is
+    // padded to a multiple of the depth, so take the deepest one whose
+    // padding is at most one stage, or none for short K.
+    const int nstage = (S.f * S.f * (S.cin / (64 / esz)) + 1) / 2;  // 128-byte K stages
+    c.depth = 3;
+    for (int d = 6; d >= 3; --d) {
+      const int pad = (nstage + d - 1) / d * d - nstage;
+      if (pad == 0 || (pad <= 1 && nstage >= 4 * d)) { c.depth = d; break; }
     }
   }
   // Block order.  Each of the 8 XCDs (own L2) reads, at least once, every
@@ -132,19 +214,6 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
     const double pix_major = 8.0 * w_bytes + a_bytes;
     const double chan_major = w_bytes * std::max(1.0, 8.0 / nb) + a_bytes * std::min(8.0, nb);
     c.chan_major = chan_major < pix_major ? 1 : 0;
-  }
-  // Two K groups (8 waves) when the grid gives a CU at most two workgroups
-  // and the block allows it: the second wave per SIMD hides the latency of
-  // the per-stage barrier / LDS / MFMA chain.  (Larger grids already put
-  // several workgroups on a CU.)
-  c.kg = (c.bm >= 64 && c.bn >= 64 && c.blocks * batch <= 2 * 256) ? 2 : 1;
-  // Pipeline depth: stages of K loaded ahead (3 to 6).  The stage count is
-  // padded to a multiple of the depth, so take the deepest one whose padding
-  // is at most one stage, or none for short K.
-  c.depth = 3;
-  for (int d = 6; d >= 3; --d) {
-    const int pad = (nstage + d - 1) / d * d - nstage;
-    if (pad == 0 || (pad <= 1 && nstage >= 4 * d)) { c.depth = d; break; }
   }
   return tune_override(S, c);
 }
@@ -203,9 +272,11 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
     // The matrix-core kernel addresses a frame's source buffer with 32-bit
     // byte offsets; the generic kernel covers larger frames.
     const int64_t src_frame_elems = (S.src_buf == BUF_GROUP_IO) ? in_frame : scr_frame;
-    if (kind == K_CONV_MFMA && src_frame_elems * static_cast<int64_t>(esz) >= (1ll << 31)) kind = K_CONV_DIRECT;
-    const bool matrix = (kind == K_CONV_MFMA);
-    const MfmaShape shape{cfg.bm, cfg.bn, cfg.depth, cfg.kg};
+    if ((kind == K_CONV_MFMA || kind == K_CONV_RING || kind == K_CONV_PATCH) &&
+        src_frame_elems * static_cast<int64_t>(esz) >= (1ll << 31))
+      kind = K_CONV_DIRECT;
+    const bool matrix = (kind == K_CONV_MFMA || kind == K_CONV_RING || kind == K_CONV_PATCH);
+    const MfmaShape shape{cfg.bm, cfg.bn, cfg.depth, cfg.kg, cfg.wgm, cfg.wgn, cfg.kord, cfg.br, cfg.bc};
     const int bu = (kind == K_CONV_RGB) ? 256 / (S.cout / 8) : block_units(kind, shape);
     StageArgs A;
     std::memset(&A, 0, sizeof(A));
@@ -244,6 +315,8 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
         if (kind == K_CONV_RGB_MFMA)  // 2-D blocks of conv outputs
           total += static_cast<int64_t>((T.ch + kRgbBlockRows - 1) / kRgbBlockRows) *
                    ((T.cw + kRgbBlockCols - 1) / kRgbBlockCols);
+        else if (kind == K_CONV_PATCH)
+          total += static_cast<int64_t>((T.ch + shape.br - 1) / shape.br) * ((T.cw + shape.bc - 1) / shape.bc);
         else
           total += (units + bu - 1) / bu;
         A.mblk_prefix[t - t0 + 1] = static_cast<int32_t>(total);
@@ -252,10 +325,28 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
       const int64_t blocks = total * A.nblk_n * batch;
       if (blocks >= (1ll << 31)) return fail(MAFAT_EUNSUPPORTED, "grid too large");
       A.total_blocks = static_cast<int32_t>(blocks);
-      const hipError_t e = launch_stage(kind, dtype, S.f, S.pool, shape, A, stream);
+      hipError_t e;
+      if (kind == K_CONV_RING) e = launch_conv_ring(S.f, S.pool, shape, A, stream);
+      else if (kind == K_CONV_PATCH) e = launch_conv_patch(S.pool, shape, A, stream);
+      else e = launch_stage(kind, dtype, S.f, S.pool, shape, A, stream);
       if (e != hipSuccess)
         return fail(MAFAT_EHIP, std::string("stage launch failed: ") + hipGetErrorString(e));
 #ifdef MAFAT_TUNING
+      if (std::getenv("MAFAT_TRACE_DUMP") && kind == K_CONV_RING) {
+        long long tr[3][64];
+        hipStreamSynchronize(stream);
+        mafat_debug_ring_trace(&tr[0][0]);
+        std::fprintf(stderr, "RTRACE stage %d-%d %dx%d kg%d ns%d grid %d\n", S.first, S.last, shape.bm, shape.bn,
+                     shape.kg, shape.depth, A.total_blocks);
+        for (int w = 0; w < 3; ++w) {
+          std::fprintf(stderr, "  wg%d decode +%lld loopend +%lld end +%lld iters:", w, (tr[w][1] - tr[w][0]) * 10,
+                       (tr[w][4] - tr[w][0]) * 10, (tr[w][5] - tr[w][0]) * 10);
+          for (int k = 8; k < 44; ++k) std::fprintf(stderr, " %lld", (tr[w][k] - tr[w][0]) * 10);
+          std::fprintf(stderr, "\n");
+        }
+        std::fprintf(stderr, "  start spread: mid-first %lld last-first %lld ns\n", (tr[1][0] - tr[0][0]) * 10,
+                     (tr[2][0] - tr[0][0]) * 10);
+      }
       if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_MFMA || kind == K_CONV_RGB_MFMA)) {
         long long tr[4][64];
         hipStreamSynchronize(stream);
@@ -327,3 +418,16 @@ extern "C" int mafat_run_network(const mafat_plan* plan, int32_t batch, int32_t 
   }
   return MAFAT_OK;
 }
+
+#ifdef MAFAT_TUNING
+// Tuning builds only: the configuration the runtime picks for stage s of
+// group g: kind, bm, bn, depth, kg, kord, br, bc.
+extern "C" int mafat_debug_config(const mafat_plan* plan, int32_t g, int32_t s, int32_t batch, int32_t dtype,
+                                  int32_t* out) {
+  const mafat::Stage& S = plan->groups[g].stages[s];
+  const mafat::StageConfig c = mafat::choose_config(S, batch, dtype);
+  const int32_t v[8] = {c.kind, c.bm, c.bn, c.depth, c.kg, c.kord, c.br, c.bc};
+  for (int k = 0; k < 8; ++k) out[k] = v[k];
+  return 0;
+}
+#endif
