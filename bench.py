@@ -43,6 +43,7 @@ class HipEvents:
                                                 ctypes.c_void_p]
         self.rt.hipEventDestroy.argtypes = [ctypes.c_void_p]
         self.rt.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.rt.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
 
     def create(self, n):
         out = []
@@ -51,6 +52,9 @@ class HipEvents:
             assert self.rt.hipEventCreate(ctypes.byref(e)) == 0
             out.append(e.value)
         return out
+
+    def record(self, e, stream):
+        assert self.rt.hipEventRecord(ctypes.c_void_p(e), ctypes.c_void_p(stream.cuda_stream)) == 0
 
     def ms(self, a, b):
         f = ctypes.c_float()
@@ -79,6 +83,24 @@ def stage_flops(plan, g):
         k = a - first
         area = sum(int(R[t, k, 5] - R[t, k, 4]) * int(R[t, k, 7] - R[t, k, 6]) for t in range(nt))
         out.append(2 * area * per)
+    return out
+
+
+def stage_bytes(plan, g, esz):
+    """Algorithmic HBM bytes of every stage of group g for one frame: each
+    tile's input region (halo included) read once, the weights (and scale,
+    bias) once, each tile's output rectangle written once."""
+    first, nl, nt = plan.group(g)
+    R = plan.regions(g)
+    out = []
+    for (a, b) in plan.stages(g):
+        da, db = plan.shape(a), plan.shape(b)
+        ka, kb = a - first, b - first
+        rd = sum(int(R[t, ka, 1] - R[t, ka, 0]) * int(R[t, ka, 3] - R[t, ka, 2]) for t in range(nt)) * da[2] * esz
+        wr = sum(int(R[t, kb, 5] - R[t, kb, 4]) * int(R[t, kb, 7] - R[t, kb, 6]) for t in range(nt)) * db[5] * esz
+        L = plan.layers[a]
+        w = (da[5] * L["f"] * L["f"] * da[2] * esz + 8 * da[5]) if L["op"] == "conv" else 0
+        out.append(rd + wr + w)
     return out
 
 
@@ -275,38 +297,44 @@ def main():
     ms_step = el / args.steps * 1e3
     fps = wl.batch * args.steps / el
 
-    # Per-stage durations: the same steps again, one run_group call per group
-    # with a HIP event before every stage and after the last, on the stream
-    # the kernels are launched on.
+    # Per-stage and per-group durations: the same steps again, one run_group
+    # call per group, with start/stop events recorded on the launch stream by
+    # the kernel dispatches themselves (hipExtLaunchKernel: nothing is
+    # inserted between the kernels).  Groups: events only on the start of the
+    # first and the end of the last kernel.  Stages: a start and a stop event
+    # on every stage's kernel.  All events are created before the timed loops.
     ev = HipEvents()
     ng = plan.n_groups
     stages = [plan.stages(g) for g in range(ng)]
-    per_step = sum(len(s) + 1 for s in stages)
     nsteps_ev = min(args.steps, 100)
-    handles = ev.create(per_step * nsteps_ev)
-    torch.cuda.synchronize()
-    k = 0
-    for _ in range(nsteps_ev):
-        for g in range(ng):
-            gin, gout = net.group_io(g, x)
-            n = len(stages[g]) + 1
-            net.run_group(g, gin, gout, stream=stream, events=handles[k:k + n])
-            k += n
-    torch.cuda.synchronize()
     stage_ms = [[0.0] * len(stages[g]) for g in range(ng)]
     group_ms = [0.0] * ng
-    k = 0
-    for _ in range(nsteps_ev):
+    gev = [[ev.create(2) for _ in range(ng)] for _ in range(nsteps_ev)]
+    sev = [[ev.create(2 * len(stages[g])) for g in range(ng)] for _ in range(nsteps_ev)]
+    io = [net.group_io(g, x) for g in range(ng)]
+    torch.cuda.synchronize()
+    for r in range(nsteps_ev):
         for g in range(ng):
-            n = len(stages[g]) + 1
-            hs = handles[k:k + n]
-            for s in range(n - 1):
-                stage_ms[g][s] += ev.ms(hs[s], hs[s + 1]) / nsteps_ev
-            group_ms[g] += ev.ms(hs[0], hs[-1]) / nsteps_ev
-            k += n
-    ev.destroy(handles)
+            lst = [None] * (2 * len(stages[g]))
+            lst[0], lst[-1] = gev[r][g]
+            net.run_group(g, io[g][0], io[g][1], stream=stream, events=lst)
+    torch.cuda.synchronize()
+    for r in range(nsteps_ev):
+        for g in range(ng):
+            net.run_group(g, io[g][0], io[g][1], stream=stream, events=sev[r][g])
+    torch.cuda.synchronize()
+    for r in range(nsteps_ev):
+        for g in range(ng):
+            group_ms[g] += ev.ms(gev[r][g][0], gev[r][g][1]) / nsteps_ev
+            hs = sev[r][g]
+            for s_ in range(len(stages[g])):
+                stage_ms[g][s_] += ev.ms(hs[2 * s_], hs[2 * s_ + 1]) / nsteps_ev
+            ev.destroy(gev[r][g])
+            ev.destroy(hs)
 
     flops = [stage_flops(plan, g) for g in range(ng)]
+    esz = 2 if wl.dtype == "bf16" else 4
+    sbytes = [stage_bytes(plan, g, esz) for g in range(ng)]
     exec_flops = sum(2 * plan.macs(g)[0] for g in range(ng)) * wl.batch
     useful_flops = sum(2 * plan.macs(g)[1] for g in range(ng)) * wl.batch
     peak = PEAK_TFLOPS[wl.dtype]
@@ -319,17 +347,23 @@ def main():
             # the matrix cores in bf16), the rest on the matrix cores
             vec = plan.layers[a]["op"] == "conv" and plan.shape(a)[2] == 3 and wl.dtype == "f32"
             pk, bound = (PEAK_VALU_TFLOPS, "alu") if vec else (peak, "mfma")
+            nb = sbytes[g][s] * wl.batch
             per_stage.append({"group": g, "layers": [a, b], "ms": round(t, 5),
                               "gflop": round(f / 1e9, 4), "bound": bound, "peak_tflops": pk,
                               "tflops": round(f / (t * 1e-3) / 1e12, 2) if t > 0 else None,
-                              "frac": round(f / (t * 1e-3) / 1e12 / pk, 4) if t > 0 else None})
+                              "frac": round(f / (t * 1e-3) / 1e12 / pk, 4) if t > 0 else None,
+                              "hbm_mb": round(nb / 1e6, 3),
+                              "gbs": round(nb / (t * 1e-3) / 1e9, 1) if t > 0 else None,
+                              "hbm_frac": round(nb / (t * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) if t > 0 else None})
     dom = max(per_stage, key=lambda r: r["ms"])
     dom_f = dom["gflop"] * 1e9
     roof = {"bound": dom["bound"], "achieved": round(dom_f / (dom["ms"] * 1e-3) / 1e12, 2),
             "peak": dom["peak_tflops"], "unit": "TFLOP/s",
             "frac": round(dom_f / (dom["ms"] * 1e-3) / 1e12 / dom["peak_tflops"], 4), "traffic": None,
             "kernel": f"stage layers {dom['layers'][0]}-{dom['layers'][1]} (group {dom['group']})",
-            "per_launch_gflop": dom["gflop"], "avg_ms": dom["ms"]}
+            "per_launch_gflop": dom["gflop"], "avg_ms": dom["ms"],
+            "timing": "kernel start/stop HIP events of the dispatch (hipExtLaunchKernel) on the launch stream, "
+                      "averaged over the event-timed steps of the whole network"}
     tr = measured_traffic(wl.name, dom["layers"])
     if tr is not None:
         roof["traffic"] = tr["bytes"]

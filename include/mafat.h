@@ -157,8 +157,11 @@ int mafat_workspace_size(const mafat_plan* plan, int32_t batch, int32_t dtype,
  *              entries); entries of max-pool layers are ignored
  *   workspace  device, 256-byte aligned, at least mafat_workspace_size bytes
  *   stream     hipStream_t (NULL: the default stream)
- *   events     NULL, or n_stages+1 hipEvent_t: events[s] is recorded on the
- *              stream right before stage s, events[n_stages] after the last
+ *   events     NULL, or 2 * n_stages hipEvent_t: events[2s] is recorded when
+ *              the first kernel of stage s starts and events[2s+1] when its
+ *              last kernel ends (timestamps of the kernel dispatches
+ *              themselves, so timing adds nothing between kernels); entries
+ *              may be NULL
  * x and y must not overlap.  Errors: EINVAL, EUNSUPPORTED (dtype),
  * EWORKSPACE, EHIP. */
 int mafat_run_group(const mafat_plan* plan, int32_t group, int32_t batch, int32_t dtype,
@@ -166,6 +169,18 @@ int mafat_run_group(const mafat_plan* plan, int32_t group, int32_t batch, int32_
                     const float* const* scale, const float* const* bias,
                     void* workspace, size_t ws_bytes, void* stream,
                     void* const* events);
+
+/* Runs only stage `stage` of group g (see mafat_plan_stages): the stage
+ * reads the group input x (first stage) or the workspace, and writes the
+ * group output y (last stage) or the workspace.  Calling it for stages 0 ..
+ * n_stages-1 in order on one stream with the same workspace computes what
+ * mafat_run_group computes; one stage alone can be launched repeatedly
+ * (e.g. to time its kernel).  Same arguments, conventions and errors as
+ * mafat_run_group, plus EINVAL for a stage index out of range. */
+int mafat_run_stage(const mafat_plan* plan, int32_t group, int32_t stage, int32_t batch,
+                    int32_t dtype, const void* x, void* y, const void* const* w,
+                    const float* const* scale, const float* const* bias, void* workspace,
+                    size_t ws_bytes, void* stream);
 
 /* Runs every group in order on one stream: group 0 reads x, group g writes
  * cut_bufs[g] (n_groups-1 caller-owned tensors, each the shape of its group's

@@ -206,24 +206,44 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
 #pragma unroll
     for (int i = 0; i < MT; ++i) acc[j][i] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  // Nine taps per chunk, software-pipelined: the fragments of tap t + 1 are
+  // read from LDS (into the other register set) before the MFMAs of tap t
+  // are issued, and a scheduling barrier keeps the compiler from
+  // interleaving them, so each tap's LDS latency hides behind the previous
+  // tap's MFMAs.
+  auto load_frags = [&](const unsigned char* sp, int t, u32x4 (&af)[MT], u32x4 (&bfr)[NT]) {
+    const int toff = (t / 3) * PC + (t % 3);
+#pragma unroll
+    for (int i = 0; i < MT; ++i) af[i] = *reinterpret_cast<const u32x4*>(sp + swz(p0[i] + toff, q));
+#pragma unroll
+    for (int j = 0; j < NT; ++j)
+      bfr[j] = *reinterpret_cast<const u32x4*>(sp + b_lane + (t * BN + j * 16) * 64);
+  };
+  auto mfmas = [&](const u32x4 (&af)[MT], const u32x4 (&bfr)[NT]) {
+#pragma unroll
+    for (int i = 0; i < MT; ++i)
+#pragma unroll
+      for (int j = 0; j < NT; ++j) {
+        if constexpr (POOL) mma<MAFAT_BF16>(acc[j][i], af[i], bfr[j]);
+        else mma<MAFAT_BF16>(acc[j][i], bfr[j], af[i]);
+      }
+  };
   auto compute = [&](int slot) {
     const unsigned char* sp = smem + slot * SLOT;
+    u32x4 af0[MT], bf0[NT], af1[MT], bf1[NT];
+    load_frags(sp, 0, af0, bf0);
 #pragma unroll
-    for (int t = 0; t < 9; ++t) {
-      const int toff = (t / 3) * PC + (t % 3);
-      u32x4 af[MT], bfr[NT];
-#pragma unroll
-      for (int i = 0; i < MT; ++i) af[i] = *reinterpret_cast<const u32x4*>(sp + swz(p0[i] + toff, q));
-#pragma unroll
-      for (int j = 0; j < NT; ++j)
-        bfr[j] = *reinterpret_cast<const u32x4*>(sp + b_lane + (t * BN + j * 16) * 64);
-#pragma unroll
-      for (int i = 0; i < MT; ++i)
-#pragma unroll
-        for (int j = 0; j < NT; ++j) {
-          if constexpr (POOL) mma<MAFAT_BF16>(acc[j][i], af[i], bfr[j]);
-          else mma<MAFAT_BF16>(acc[j][i], bfr[j], af[i]);
-        }
+    for (int t = 0; t < 9; t += 2) {
+      if (t + 1 < 9) load_frags(sp, t + 1, af1, bf1);
+      __builtin_amdgcn_sched_barrier(0);
+      mfmas(af0, bf0);
+      __builtin_amdgcn_sched_barrier(0);
+      if (t + 1 < 9) {
+        if (t + 2 < 9) load_frags(sp, t + 2, af0, bf0);
+        __builtin_amdgcn_sched_barrier(0);
+        mfmas(af1, bf1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   };
 
@@ -289,14 +309,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
 }
 
 template <bool POOL>
-hipError_t launch_patch_p(const MfmaShape& sh, const StageArgs& args, hipStream_t stream) {
+hipError_t launch_patch_p(const MfmaShape& sh, const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
   const dim3 grid(static_cast<unsigned>(args.total_blocks));
 #define MAFAT_PATCH(br_, bc_, bm_, bn_, wgm_, wgn_, ns_)                                               \
   if (sh.br == (br_) && sh.bc == (bc_) && sh.bm == (bm_) && sh.bn == (bn_) && sh.wgm == (wgm_) &&      \
       sh.wgn == (wgn_) && sh.depth == (ns_)) {                                                        \
     if constexpr (!POOL || ((br_) % 2 == 0 && (bc_) % 2 == 0)) {                                      \
-      hipLaunchKernelGGL((conv_patch_kernel<br_, bc_, bm_, bn_, wgm_, wgn_, ns_, POOL>), grid,         \
-                         dim3(64 * (wgm_) * (wgn_)), 0, stream, args);                                 \
+      hipExtLaunchKernelGGL((conv_patch_kernel<br_, bc_, bm_, bn_, wgm_, wgn_, ns_, POOL>), grid,      \
+                            dim3(64 * (wgm_) * (wgn_)), 0, stream, ev.start, ev.stop, 0, args);       \
       return hipGetLastError();                                                                       \
     }                                                                                                 \
     return hipErrorInvalidValue;                                                                      \
@@ -309,9 +329,10 @@ hipError_t launch_patch_p(const MfmaShape& sh, const StageArgs& args, hipStream_
 
 }  // namespace
 
-hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs& args, hipStream_t stream) {
+hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs& args, hipStream_t stream,
+                             LaunchEvents ev) {
   if (args.total_blocks <= 0) return hipSuccess;
-  return pool ? launch_patch_p<true>(shape, args, stream) : launch_patch_p<false>(shape, args, stream);
+  return pool ? launch_patch_p<true>(shape, args, stream, ev) : launch_patch_p<false>(shape, args, stream, ev);
 }
 
 }  // namespace mafat

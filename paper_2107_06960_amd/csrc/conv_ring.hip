@@ -363,13 +363,13 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void conv_ring_kernel(const St
 }
 
 template <int F, bool POOL>
-hipError_t launch_ring_fp(const MfmaShape& sh, const StageArgs& args, hipStream_t stream) {
+hipError_t launch_ring_fp(const MfmaShape& sh, const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
   const dim3 grid(static_cast<unsigned>(args.total_blocks));
 #define MAFAT_RING(bm_, bn_, wgm_, wgn_, kg_, ns_, ko_)                                             \
   if (sh.bm == (bm_) && sh.bn == (bn_) && sh.wgm == (wgm_) && sh.wgn == (wgn_) && sh.kg == (kg_) && \
       sh.depth == (ns_) && sh.kord == (ko_)) {                                                     \
-    hipLaunchKernelGGL((conv_ring_kernel<F, bm_, bn_, wgm_, wgn_, kg_, ns_, ko_, POOL>), grid,      \
-                       dim3(64 * (wgm_) * (wgn_) * (kg_)), 0, stream, args);                        \
+    hipExtLaunchKernelGGL((conv_ring_kernel<F, bm_, bn_, wgm_, wgn_, kg_, ns_, ko_, POOL>), grid,   \
+                          dim3(64 * (wgm_) * (wgn_) * (kg_)), 0, stream, ev.start, ev.stop, 0, args); \
     return hipGetLastError();                                                                      \
   }
   MAFAT_RING_SHAPES
@@ -387,10 +387,10 @@ extern "C" int mafat_debug_ring_trace(long long* host_out) {
 #endif
 
 hipError_t launch_conv_ring(int f, bool pool, const MfmaShape& shape, const StageArgs& args,
-                            hipStream_t stream) {
+                            hipStream_t stream, LaunchEvents ev) {
   if (args.total_blocks <= 0) return hipSuccess;
-  if (f == 3) return pool ? launch_ring_fp<3, true>(shape, args, stream) : launch_ring_fp<3, false>(shape, args, stream);
-  if (f == 1) return pool ? launch_ring_fp<1, true>(shape, args, stream) : launch_ring_fp<1, false>(shape, args, stream);
+  if (f == 3) return pool ? launch_ring_fp<3, true>(shape, args, stream, ev) : launch_ring_fp<3, false>(shape, args, stream, ev);
+  if (f == 1) return pool ? launch_ring_fp<1, true>(shape, args, stream, ev) : launch_ring_fp<1, false>(shape, args, stream, ev);
   return hipErrorInvalidValue;
 }
 

@@ -1,6 +1,7 @@
 // kernel_args.h -- argument blocks passed by value to the stage kernels.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -69,19 +70,15 @@ struct MfmaShape {
 
 // Instantiated patch kernel shapes: (br, bc, bm, bn, wgm, wgn, ring slots).
 #define MAFAT_PATCH_SHAPES                \
-  MAFAT_PATCH(8, 16, 128, 64, 2, 2, 3)    \
-  MAFAT_PATCH(8, 8, 64, 64, 2, 2, 3)      \
-  MAFAT_PATCH(8, 16, 128, 32, 2, 2, 4)    \
-  MAFAT_PATCH(16, 16, 256, 64, 2, 2, 2)   \
-  MAFAT_PATCH(10, 10, 128, 32, 2, 2, 4)   \
-  MAFAT_PATCH(8, 8, 64, 32, 2, 2, 4)      \
-  MAFAT_PATCH(4, 16, 64, 64, 2, 2, 3)     \
-  MAFAT_PATCH(16, 16, 256, 32, 2, 2, 3)
+  MAFAT_PATCH(16, 16, 256, 64, 4, 1, 2)   \
+  MAFAT_PATCH(10, 10, 128, 32, 4, 1, 4)   \
+  MAFAT_PATCH(8, 8, 64, 32, 4, 1, 4)
 #ifdef MAFAT_TUNING
 #define MAFAT_PATCH_TUNE_SHAPES           \
-  MAFAT_PATCH(8, 16, 128, 64, 2, 2, 2)    \
-  MAFAT_PATCH(4, 8, 32, 64, 2, 2, 3)      \
-  MAFAT_PATCH(16, 32, 512, 32, 2, 2, 2)
+  MAFAT_PATCH(10, 10, 128, 32, 2, 2, 4)   \
+  MAFAT_PATCH(16, 16, 256, 64, 2, 2, 2)   \
+  MAFAT_PATCH(8, 16, 128, 64, 2, 2, 3)    \
+  MAFAT_PATCH(16, 16, 256, 32, 2, 2, 3)
 #else
 #define MAFAT_PATCH_TUNE_SHAPES
 #endif
@@ -106,15 +103,22 @@ struct MfmaShape {
 
 // Launch one stage chunk.  `units_per_block` is what the kernel covers per
 // block along the pixel axis (used to fill mblk_prefix by the caller).
+// Optional kernel timestamps: `start` is recorded when the launched kernel
+// starts and `stop` when it ends (hipExtLaunchKernel: timestamps of the
+// dispatch itself, no extra packets between kernels); null for none.
+struct LaunchEvents {
+  hipEvent_t start, stop;
+};
 hipError_t launch_stage(int kind, int dtype, int f, bool pool, MfmaShape shape,
-                        const StageArgs& args, hipStream_t stream);
+                        const StageArgs& args, hipStream_t stream, LaunchEvents ev);
 
 // Launch one bf16 LDS-ring convolution stage chunk (conv_ring.hip).
 hipError_t launch_conv_ring(int f, bool pool, const MfmaShape& shape, const StageArgs& args,
-                            hipStream_t stream);
+                            hipStream_t stream, LaunchEvents ev);
 
 // Launch one bf16 3x3 patch-kernel stage chunk (conv_patch.hip).
-hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs& args, hipStream_t stream);
+hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs& args, hipStream_t stream,
+                             LaunchEvents ev);
 
 // Pixel-axis block size of each kernel family.
 int block_units(int kind, MfmaShape shape);

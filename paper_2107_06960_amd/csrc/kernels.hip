@@ -773,12 +773,12 @@ __global__ __launch_bounds__(256) void pool_kernel(const StageArgs a) {
 }
 
 template <int DT, int F, bool POOL, int DEPTH>
-hipError_t launch_mfma(MfmaShape sh, const StageArgs& args, hipStream_t stream) {
+hipError_t launch_mfma(MfmaShape sh, const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
   const dim3 grid(static_cast<unsigned>(args.total_blocks));
 #define MAFAT_SHAPE(bm_, bn_, kg_)                                                             \
   if (sh.bm == (bm_) && sh.bn == (bn_) && sh.kg == (kg_)) {                                    \
-    hipLaunchKernelGGL((conv_mfma_kernel<DT, F, bm_, bn_, POOL, DEPTH, kg_>), grid, dim3(256 * (kg_)), 0, \
-                       stream, args);                                                          \
+    hipExtLaunchKernelGGL((conv_mfma_kernel<DT, F, bm_, bn_, POOL, DEPTH, kg_>), grid, dim3(256 * (kg_)), 0, \
+                          stream, ev.start, ev.stop, 0, args);                                 \
     return hipGetLastError();                                                                  \
   }
   MAFAT_SHAPE(128, 128, 1) MAFAT_SHAPE(128, 64, 1) MAFAT_SHAPE(64, 128, 1) MAFAT_SHAPE(64, 64, 1)
@@ -789,23 +789,23 @@ hipError_t launch_mfma(MfmaShape sh, const StageArgs& args, hipStream_t stream) 
 }
 
 template <int DT, int F, bool POOL>
-hipError_t launch_conv(int kind, MfmaShape sh, const StageArgs& args, hipStream_t stream) {
+hipError_t launch_conv(int kind, MfmaShape sh, const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
   const dim3 grid(static_cast<unsigned>(args.total_blocks)), block(256);
   if (kind == K_CONV_DIRECT) {
-    hipLaunchKernelGGL((conv_direct_kernel<DT, F, POOL>), grid, block, 0, stream, args);
+    hipExtLaunchKernelGGL((conv_direct_kernel<DT, F, POOL>), grid, block, 0, stream, ev.start, ev.stop, 0, args);
     return hipGetLastError();
   }
   if (kind == K_CONV_RGB) {
     if (F != 3) return hipErrorInvalidValue;
-    hipLaunchKernelGGL((conv_rgb_kernel<DT, POOL>), grid, block, 0, stream, args);
+    hipExtLaunchKernelGGL((conv_rgb_kernel<DT, POOL>), grid, block, 0, stream, ev.start, ev.stop, 0, args);
     return hipGetLastError();
   }
   if (kind == K_CONV_RGB_MFMA) {
     if (F != 3 || DT != MAFAT_BF16) return hipErrorInvalidValue;
     switch (sh.bn) {  // c_out
-      case 16: hipLaunchKernelGGL((conv_rgb_mfma_kernel<POOL, 1>), grid, block, 0, stream, args); break;
-      case 32: hipLaunchKernelGGL((conv_rgb_mfma_kernel<POOL, 2>), grid, block, 0, stream, args); break;
-      case 64: hipLaunchKernelGGL((conv_rgb_mfma_kernel<POOL, 4>), grid, block, 0, stream, args); break;
+      case 16: hipExtLaunchKernelGGL((conv_rgb_mfma_kernel<POOL, 1>), grid, block, 0, stream, ev.start, ev.stop, 0, args); break;
+      case 32: hipExtLaunchKernelGGL((conv_rgb_mfma_kernel<POOL, 2>), grid, block, 0, stream, ev.start, ev.stop, 0, args); break;
+      case 64: hipExtLaunchKernelGGL((conv_rgb_mfma_kernel<POOL, 4>), grid, block, 0, stream, ev.start, ev.stop, 0, args); break;
       default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -814,26 +814,26 @@ hipError_t launch_conv(int kind, MfmaShape sh, const StageArgs& args, hipStream_
   // register-staged kernel serves float32.
   if constexpr (DT != MAFAT_F32) return hipErrorInvalidValue;
   else switch (sh.depth) {
-    case 3: return launch_mfma<DT, F, POOL, 3>(sh, args, stream);
-    case 4: return launch_mfma<DT, F, POOL, 4>(sh, args, stream);
-    case 5: return launch_mfma<DT, F, POOL, 5>(sh, args, stream);
-    case 6: return launch_mfma<DT, F, POOL, 6>(sh, args, stream);
+    case 3: return launch_mfma<DT, F, POOL, 3>(sh, args, stream, ev);
+    case 4: return launch_mfma<DT, F, POOL, 4>(sh, args, stream, ev);
+    case 5: return launch_mfma<DT, F, POOL, 5>(sh, args, stream, ev);
+    case 6: return launch_mfma<DT, F, POOL, 6>(sh, args, stream, ev);
     default: return hipErrorInvalidValue;
   }
 }
 
 template <int DT>
 hipError_t launch_dt(int kind, int f, bool pool, MfmaShape sh, const StageArgs& args,
-                     hipStream_t stream) {
+                     hipStream_t stream, LaunchEvents ev) {
   if (kind == K_POOL) {
-    hipLaunchKernelGGL((pool_kernel<DT>), dim3(static_cast<unsigned>(args.total_blocks)), dim3(256),
-                       0, stream, args);
+    hipExtLaunchKernelGGL((pool_kernel<DT>), dim3(static_cast<unsigned>(args.total_blocks)), dim3(256),
+                          0, stream, ev.start, ev.stop, 0, args);
     return hipGetLastError();
   }
-  if (f == 3) return pool ? launch_conv<DT, 3, true>(kind, sh, args, stream)
-                          : launch_conv<DT, 3, false>(kind, sh, args, stream);
-  if (f == 1) return pool ? launch_conv<DT, 1, true>(kind, sh, args, stream)
-                          : launch_conv<DT, 1, false>(kind, sh, args, stream);
+  if (f == 3) return pool ? launch_conv<DT, 3, true>(kind, sh, args, stream, ev)
+                          : launch_conv<DT, 3, false>(kind, sh, args, stream, ev);
+  if (f == 1) return pool ? launch_conv<DT, 1, true>(kind, sh, args, stream, ev)
+                          : launch_conv<DT, 1, false>(kind, sh, args, stream, ev);
   return hipErrorInvalidValue;
 }
 
@@ -852,10 +852,10 @@ int block_units(int kind, MfmaShape shape) {
 }
 
 hipError_t launch_stage(int kind, int dtype, int f, bool pool, MfmaShape shape,
-                        const StageArgs& args, hipStream_t stream) {
+                        const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
   if (args.total_blocks <= 0) return hipSuccess;
-  if (dtype == MAFAT_BF16) return launch_dt<MAFAT_BF16>(kind, f, pool, shape, args, stream);
-  if (dtype == MAFAT_F32) return launch_dt<MAFAT_F32>(kind, f, pool, shape, args, stream);
+  if (dtype == MAFAT_BF16) return launch_dt<MAFAT_BF16>(kind, f, pool, shape, args, stream, ev);
+  if (dtype == MAFAT_F32) return launch_dt<MAFAT_F32>(kind, f, pool, shape, args, stream, ev);
   return hipErrorInvalidValue;
 }
 

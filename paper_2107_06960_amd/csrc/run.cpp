@@ -45,7 +45,7 @@ bool rgb_ok(const Stage& S) {
          (S.cout == 8 || S.cout == 16 || S.cout == 32 || S.cout == 64);
 }
 
-// Tuning builds only: MAFAT_TUNE="first_layer:bm,bn,depth[,chan_major[,kg[,kind[,kord[,br,bc]]]]];..."
+// Tuning builds only: MAFAT_TUNE="first_layer:bm,bn,depth[,chan_major[,kg[,kind[,kord[,br,bc[,wgm,wgn]]]]]];..."
 // forces the configuration of the stage starting at first_layer (kind: 0 the
 // register-staged matrix-core kernel, 5 the LDS-ring kernel, 6 the 3x3 patch
 // kernel).
@@ -57,9 +57,9 @@ StageConfig tune_override(const Stage& S, StageConfig c) {
     while (pos < e.size()) {
       size_t end = e.find(';', pos);
       if (end == std::string::npos) end = e.size();
-      int l, bm, bn, dp, cm = -1, kg = -1, kind = -1, ko = -1, br = -1, bc = -1;
-      const int got = std::sscanf(e.substr(pos, end - pos).c_str(), "%d:%d,%d,%d,%d,%d,%d,%d,%d,%d", &l, &bm,
-                                  &bn, &dp, &cm, &kg, &kind, &ko, &br, &bc);
+      int l, bm, bn, dp, cm = -1, kg = -1, kind = -1, ko = -1, br = -1, bc = -1, wgm = -1, wgn = -1;
+      const int got = std::sscanf(e.substr(pos, end - pos).c_str(), "%d:%d,%d,%d,%d,%d,%d,%d,%d,%d,%d,%d", &l,
+                                  &bm, &bn, &dp, &cm, &kg, &kind, &ko, &br, &bc, &wgm, &wgn);
       if (got >= 4 && l == S.first) {
         c.bm = bm; c.bn = bn; c.depth = dp;
         if (cm >= 0) c.chan_major = cm;
@@ -67,6 +67,7 @@ StageConfig tune_override(const Stage& S, StageConfig c) {
         if (kind >= 0) c.kind = kind;
         if (ko >= 0) c.kord = ko;
         if (br > 0 && bc > 0) { c.br = br; c.bc = bc; }
+        if (wgm > 0 && wgn > 0) { c.wgm = wgm; c.wgn = wgn; }
       }
       pos = end + 1;
     }
@@ -100,48 +101,35 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
   }
   const int esz = (dtype == MAFAT_BF16) ? 2 : 4;
   const double K = static_cast<double>(S.f) * S.f * S.cin;
-  if (dtype == MAFAT_BF16 && S.f == 3 && S.cin >= 256) {
-    // 3x3 patch kernel for the deep layers (many 32-channel chunks, few
-    // pixels): measured faster than the LDS-ring kernel there; on layers
-    // with fewer input channels the ring kernel's higher occupancy wins.
-    // Time model per workgroup (one per CU: the ring takes more than half
-    // the LDS) and chunk: the largest of its load bytes at ~27 bytes/clock
-    // (what one workgroup of 4 waves sustains from L2), its MFMA time at
-    // the CU's peak (4096 flop/clock) and its LDS fragment reads at 128
-    // bytes/clock; plus ~2 us per workgroup (decode, first loads,
-    // epilogue).  Edge blocks of a tile compute their full rectangle, so
-    // large blocks waste work on small tiles; rounds beyond 256 queue.
+  if (dtype == MAFAT_BF16 && S.f == 3 && S.cin >= 64) {
+    // 3x3 patch kernel (each block's input patch loaded once per 32-channel
+    // chunk and shared by the nine taps).  Shapes from a sweep over the
+    // YOLOv2 stages at 608x608 (5x5/8/2x2): 16x16-pixel blocks x 64
+    // channels with four waves of 64x64 accumulators are the fastest where
+    // tiles are large; on small tiles (the deep layers' ~20x20) 16x16 blocks
+    // mostly compute padding, and 10x10 blocks x 32 channels win, 8x8 blocks
+    // on smaller tiles still.  The pick: the largest block whose padded
+    // pixel count stays within 1.4x of the tiles' pixels.  With fewer input
+    // channels (one or two chunks) the LDS-ring kernel's higher occupancy
+    // wins instead (below).
     c.kind = K_CONV_PATCH;
-    c.wgm = 2; c.wgn = 2;
-    const int nstage = S.cin / 32;
     struct PS { int br, bc, bm, bn, wgm, wgn, ns; };
     static const PS kPatch[] = {
 #define MAFAT_PATCH(br_, bc_, bm_, bn_, wgm_, wgn_, ns_) {br_, bc_, bm_, bn_, wgm_, wgn_, ns_},
         MAFAT_PATCH_SHAPES
 #undef MAFAT_PATCH
     };
-    double best = 1e30;
-    for (const PS& r : kPatch) {
-      if (r.bn > S.cout && r.bn > 32) continue;
+    int64_t useful = 0;
+    for (const TileGeom& T : S.tiles) useful += static_cast<int64_t>(T.ch) * T.cw;
+    const int npatch = static_cast<int>(sizeof(kPatch) / sizeof(kPatch[0]));
+    for (int k = 0; k < npatch; ++k) {
+      const PS& r = kPatch[k];
       int64_t mb = 0;
       for (const TileGeom& T : S.tiles)
         mb += static_cast<int64_t>((T.ch + r.br - 1) / r.br) * ((T.cw + r.bc - 1) / r.bc);
-      const int64_t blocks = mb * ((S.cout + r.bn - 1) / r.bn);
-      const double wgs = static_cast<double>(blocks) * batch;
-      const int ppx = ((r.br + 2) * (r.bc + 2) + 15) / 16 * 16;
-      const double slot = (ppx + 9.0 * r.bn) * 64.0;
-      const int nw = r.wgm * r.wgn;
-      const double mt = r.bm / r.wgm / 16.0, nt = r.bn / r.wgn / 16.0;
-      const double loadc = slot / 27.0;
-      const double mfma = 2.0 * r.bm * r.bn * 288.0 / 4096.0;
-      const double ldsc = 9.0 * nw * (mt + nt) * 1024.0 / 128.0;
-      const double per = std::max(std::max(loadc, mfma), ldsc);
-      const double t = 2e-6 + std::ceil(wgs / 256.0) * nstage * per / 2.4e9;
-      if (t < best * 0.97) {
-        best = t;
-        c.br = r.br; c.bc = r.bc; c.bm = r.bm; c.bn = r.bn; c.wgm = r.wgm; c.wgn = r.wgn; c.depth = r.ns;
-        c.blocks = blocks;
-      }
+      c.br = r.br; c.bc = r.bc; c.bm = r.bm; c.bn = r.bn; c.wgm = r.wgm; c.wgn = r.wgn; c.depth = r.ns;
+      c.blocks = mb * ((S.cout + r.bn - 1) / r.bn);
+      if (static_cast<double>(mb) * r.br * r.bc <= 1.4 * static_cast<double>(useful)) break;
     }
   } else if (dtype == MAFAT_BF16) {
     // LDS-ring kernel.  Block shapes from a sweep over every YOLOv2 stage
@@ -228,7 +216,11 @@ WorkspaceLayout workspace_layout(const Group& G, int batch, int dtype) {
 
 namespace {
 
-int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const void* x, void* y,
+// Runs stages [s_begin, s_end) of group g.  events, if given, holds two
+// hipEvent_t per stage, indexed from s_begin: events[2k] is recorded when
+// the first kernel of stage s_begin + k starts, events[2k + 1] when its last
+// kernel ends (timestamps of the dispatches themselves).
+int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int batch, int dtype, const void* x, void* y,
                    const void* const* w, const float* const* scale, const float* const* bias,
                    void* ws, size_t ws_bytes, hipStream_t stream, void* const* events) {
   const Group& G = plan->groups[g];
@@ -262,11 +254,11 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
         return fail(MAFAT_EINVAL, "layer " + std::to_string(l) + ": weights, scale or bias not 16-byte aligned");
     }
 
-  const int ns = static_cast<int>(G.stages.size());
-  for (int s = 0; s < ns; ++s) {
+  for (int s = s_begin; s < s_end; ++s) {
     const Stage& S = G.stages[s];
-    if (events && events[s] && hipEventRecord(static_cast<hipEvent_t>(events[s]), stream) != hipSuccess)
-      return fail(MAFAT_EHIP, "hipEventRecord failed");
+    hipEvent_t ev_start = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin)]) : nullptr;
+    hipEvent_t ev_stop = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin) + 1]) : nullptr;
+    bool launched = false;
     const StageConfig cfg = choose_config(S, batch, dtype);
     int kind = cfg.kind;
     // The matrix-core kernel addresses a frame's source buffer with 32-bit
@@ -325,10 +317,25 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
       const int64_t blocks = total * A.nblk_n * batch;
       if (blocks >= (1ll << 31)) return fail(MAFAT_EUNSUPPORTED, "grid too large");
       A.total_blocks = static_cast<int32_t>(blocks);
+      const bool last_chunk = t1 >= G.ntiles;
+      const LaunchEvents lev{launched ? nullptr : ev_start, last_chunk ? ev_stop : nullptr};
       hipError_t e;
-      if (kind == K_CONV_RING) e = launch_conv_ring(S.f, S.pool, shape, A, stream);
-      else if (kind == K_CONV_PATCH) e = launch_conv_patch(S.pool, shape, A, stream);
-      else e = launch_stage(kind, dtype, S.f, S.pool, shape, A, stream);
+      if (A.total_blocks <= 0) {
+        e = hipSuccess;
+      } else if (kind == K_CONV_RING) {
+        e = launch_conv_ring(S.f, S.pool, shape, A, stream, lev);
+      } else if (kind == K_CONV_PATCH) {
+        e = launch_conv_patch(S.pool, shape, A, stream, lev);
+      } else {
+        e = launch_stage(kind, dtype, S.f, S.pool, shape, A, stream, lev);
+      }
+      if (A.total_blocks > 0) {
+        launched = true;
+      } else if (last_chunk) {  // nothing launched for the last chunk: close the interval here
+        if ((!launched && ev_start && hipEventRecord(ev_start, stream) != hipSuccess) ||
+            (ev_stop && hipEventRecord(ev_stop, stream) != hipSuccess))
+          return fail(MAFAT_EHIP, "hipEventRecord failed");
+      }
       if (e != hipSuccess)
         return fail(MAFAT_EHIP, std::string("stage launch failed: ") + hipGetErrorString(e));
 #ifdef MAFAT_TUNING
@@ -368,8 +375,6 @@ int run_group_impl(const mafat_plan* plan, int g, int batch, int dtype, const vo
 #endif
     }
   }
-  if (events && events[ns] && hipEventRecord(static_cast<hipEvent_t>(events[ns]), stream) != hipSuccess)
-    return fail(MAFAT_EHIP, "hipEventRecord failed");
   return MAFAT_OK;
 }
 
@@ -395,8 +400,24 @@ extern "C" int mafat_run_group(const mafat_plan* plan, int32_t group, int32_t ba
   if (rc != MAFAT_OK) return rc;
   if (group < 0 || group >= static_cast<int>(plan->groups.size()))
     return fail(MAFAT_EINVAL, "group index out of range");
-  return run_group_impl(plan, group, batch, dtype, x, y, w, scale, bias, workspace, ws_bytes,
+  return run_group_impl(plan, group, 0, static_cast<int>(plan->groups[group].stages.size()), batch, dtype, x, y,
+                        w, scale, bias, workspace, ws_bytes,
                         static_cast<hipStream_t>(stream), events);
+}
+
+extern "C" int mafat_run_stage(const mafat_plan* plan, int32_t group, int32_t stage, int32_t batch,
+                               int32_t dtype, const void* x, void* y, const void* const* w,
+                               const float* const* scale, const float* const* bias, void* workspace,
+                               size_t ws_bytes, void* stream) {
+  clear_error();
+  int rc = check_common(plan, batch, dtype);
+  if (rc != MAFAT_OK) return rc;
+  if (group < 0 || group >= static_cast<int>(plan->groups.size()))
+    return fail(MAFAT_EINVAL, "group index out of range");
+  if (stage < 0 || stage >= static_cast<int>(plan->groups[group].stages.size()))
+    return fail(MAFAT_EINVAL, "stage index out of range");
+  return run_group_impl(plan, group, stage, stage + 1, batch, dtype, x, y, w, scale, bias, workspace, ws_bytes,
+                        static_cast<hipStream_t>(stream), nullptr);
 }
 
 extern "C" int mafat_run_network(const mafat_plan* plan, int32_t batch, int32_t dtype,
@@ -412,7 +433,8 @@ extern "C" int mafat_run_network(const mafat_plan* plan, int32_t batch, int32_t 
   for (int g = 0; g < ng; ++g) {
     const void* gin = (g == 0) ? x : cut_bufs[g - 1];
     void* gout = (g == ng - 1) ? y : cut_bufs[g];
-    rc = run_group_impl(plan, g, batch, dtype, gin, gout, w, scale, bias, workspace, ws_bytes,
+    rc = run_group_impl(plan, g, 0, static_cast<int>(plan->groups[g].stages.size()), batch, dtype, gin, gout, w,
+                        scale, bias, workspace, ws_bytes,
                         static_cast<hipStream_t>(stream), nullptr);
     if (rc != MAFAT_OK) return rc;
   }

@@ -31,7 +31,8 @@ DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
 # Every symbol include/mafat.h declares.
 EXPORTS = ("mafat_plan_create", "mafat_plan_destroy", "mafat_plan_layer_shape", "mafat_plan_group",
            "mafat_plan_regions", "mafat_plan_macs", "mafat_plan_stages", "mafat_plan_stage_layers",
-           "mafat_workspace_size", "mafat_run_group", "mafat_run_network", "mafat_status_string",
+           "mafat_workspace_size", "mafat_run_group", "mafat_run_stage", "mafat_run_network",
+           "mafat_status_string",
            "mafat_last_error")
 
 
@@ -80,6 +81,7 @@ def lib():
         L.mafat_plan_stage_layers.argtypes = [planp, i32, i32, i32p, i32p]
         L.mafat_workspace_size.argtypes = [planp, i32, i32, ctypes.POINTER(sz)]
         L.mafat_run_group.argtypes = [planp, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp, vpp]
+        L.mafat_run_stage.argtypes = [planp, i32, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp]
         L.mafat_run_network.argtypes = [planp, i32, i32, vp, vp, vpp, vpp, vpp, vpp, vp, sz, vp]
         L.mafat_status_string.argtypes = [ctypes.c_int]
         L.mafat_status_string.restype = ctypes.c_char_p
@@ -179,11 +181,19 @@ def mafat_run_group(plan, group, batch, dtype, x, y, w, scale, bias, workspace, 
                     events=None):
     """x, y, workspace: device pointers (int); w/scale/bias: lists of device
     pointers indexed by layer (None for pools); stream: hipStream_t (int);
-    events: None or a list of n_stages+1 hipEvent_t handles."""
+    events: None or a list of 2 * n_stages hipEvent_t handles (start and end
+    of each stage's kernels; entries may be None)."""
     ev = _ptrs(events) if events is not None else None
     _check("mafat_run_group",
            lib().mafat_run_group(plan, group, batch, dtype, x, y, _ptrs(w), _ptrs(scale), _ptrs(bias),
                                  workspace, ws_bytes, stream, ev))
+
+
+def mafat_run_stage(plan, group, stage, batch, dtype, x, y, w, scale, bias, workspace, ws_bytes, stream):
+    """One stage of a group (same pointer conventions as mafat_run_group)."""
+    _check("mafat_run_stage",
+           lib().mafat_run_stage(plan, group, stage, batch, dtype, x, y, _ptrs(w), _ptrs(scale), _ptrs(bias),
+                                 workspace, ws_bytes, stream))
 
 
 def mafat_run_network(plan, batch, dtype, x, y, cut_bufs, w, scale, bias, workspace, ws_bytes, stream):
@@ -289,6 +299,11 @@ class Network:
         mafat_run_group(self.plan.handle, g, self.batch, self.code, x.data_ptr(), y.data_ptr(),
                         self._wp, self._sp, self._bp, self.ws.data_ptr(), self.ws_bytes,
                         _stream_handle(stream), events)
+
+    def run_stage(self, g, s, x, y, stream=None):
+        mafat_run_stage(self.plan.handle, g, s, self.batch, self.code, x.data_ptr(), y.data_ptr(),
+                        self._wp, self._sp, self._bp, self.ws.data_ptr(), self.ws_bytes,
+                        _stream_handle(stream))
 
     def group_io(self, g, x):
         gin = x if g == 0 else self.cuts[g - 1]

@@ -181,4 +181,11 @@ def test_run_argument_errors_before_any_launch(lib):
     # network with several groups but no cut buffers
     plan2 = M.Plan(W.TINY, (64, 64, 3), "2x2/2/2x2")
     assert L.mafat_run_network(plan2.handle, 1, 0, fake, fake * 4, None, w, w, w, fake, 1 << 30, None) == M.MAFAT_EINVAL
+    # single stage: stage index out of range, bad group, then the group checks
+    ns = plan.stages(0)
+    assert L.mafat_run_stage(plan.handle, 0, len(ns), 1, 0, fake, fake * 4, w, w, w, fake, need, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_stage(plan.handle, 0, -1, 1, 0, fake, fake * 4, w, w, w, fake, need, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_stage(plan.handle, 1, 0, 1, 0, fake, fake * 4, w, w, w, fake, need, None) == M.MAFAT_EINVAL
+    rc = L.mafat_run_stage(plan.handle, 0, 0, 1, M.MAFAT_F32, fake, fake * 4, w, w, w, fake, need - 1, None)
+    assert rc == M.MAFAT_EWORKSPACE
     assert M.lib().mafat_status_string(M.MAFAT_EWORKSPACE) == b"workspace too small"

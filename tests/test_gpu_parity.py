@@ -116,3 +116,30 @@ def test_deterministic_bitwise():
     b = net.run(x).clone()
     torch.cuda.synchronize()
     assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_run_stage_sequence_equals_run_group(dtype):
+    # mafat_run_stage for every stage in order == mafat_run_group, bit for bit
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    print(f"[parity] run_stage sequence vs run_group, YOLOv2 96x96 {dtype}", flush=True)
+    p = W.make_inputs(W.YOLOV2_16, 96, 96, 3, 1, 4, dtype)
+    plan = M.Plan(W.YOLOV2_16, (96, 96, 3), "3x3/8/2x2")
+    net = M.Network(plan, p, 1, dtype)
+    x = net.input_tensor(p["x"])
+    ref = net.run(x).clone()
+    refc = [c.clone() for c in net.cuts]
+    net.y.zero_()
+    for c in net.cuts:
+        c.zero_()
+    for g in range(plan.n_groups):
+        gin, gout = net.group_io(g, x)
+        for s in range(len(plan.stages(g))):
+            net.run_stage(g, s, gin, gout)
+    torch.cuda.synchronize()
+    assert torch.equal(net.y.view(torch.int16 if dtype == "bf16" else torch.int32),
+                       ref.view(torch.int16 if dtype == "bf16" else torch.int32))
+    for a, b in zip(net.cuts, refc):
+        assert torch.equal(a, b)
+
