@@ -223,6 +223,51 @@ def measured_traffic(workload, stage_layers):
     return None
 
 
+def config_search(args):
+    """Configuration search (Algorithm 2) against an exhaustive measurement
+    of its search space on this GPU: every candidate (cuts 16/12/8 x first
+    grid 1..5, second group 2x2) of the 608x608 bf16 batch-1 YOLOv2 stack is
+    timed; for each device-memory limit the search's pick (device memory
+    model, no bias) is compared with the fastest measured candidate whose
+    predicted memory fits.  Prints one JSON line."""
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    from paper_2107_06960_amd import workloads as W
+    torch.cuda.set_device(0)
+    layers, hwc = W.YOLOV2_16, (608, 608, 3)
+    cands = []
+    for cut in (16, 12, 8):
+        for t in (1, 2, 3, 4, 5):
+            cands.append(f"{t}x{t}/NoCut" if cut == 16 else f"{t}x{t}/{cut}/2x2")
+    params = W.make_inputs(layers, *hwc, 1, 0, "bf16")
+    meas = {}
+    for spec in cands:
+        plan = M.Plan(layers, hwc, spec)
+        net = M.Network(plan, params, 1, "bf16")
+        x = net.input_tensor(params["x"])
+        for _ in range(5):
+            net.run(x)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            net.run(x)
+        torch.cuda.synchronize()
+        meas[spec] = {"ms": (time.perf_counter() - t0) / args.steps * 1e3,
+                      "device_mib": plan.predict_mem("device", 1, "bf16") / 2 ** 20,
+                      "paper_f32_mib": plan.predict_mem("paper", 1, "f32") / 2 ** 20 + 31}
+        del net, x
+        print(json.dumps({"candidate": spec, **{k: round(v, 4) for k, v in meas[spec].items()}}), flush=True)
+    rows = []
+    for lim in (21, 24, 26, 28, 30, 40, 64, 128):
+        spec, pred, fits = M.mafat_get_config(layers, hwc, lim * 2 ** 20, model="device", batch=1, dtype="bf16")
+        ok = [c for c in cands if meas[c]["device_mib"] < lim]
+        best = min(ok, key=lambda c: meas[c]["ms"]) if ok else None
+        rows.append({"limit_mib": lim, "search": spec, "fits": fits, "search_ms": round(meas[spec]["ms"], 4),
+                     "best": best, "best_ms": round(meas[best]["ms"], 4) if best else None,
+                     "slowdown_vs_best": round(meas[spec]["ms"] / meas[best]["ms"] - 1, 4) if best else None})
+    print(json.dumps({"config_search": rows}), flush=True)
+
+
 def copy_calibration(mib, reps=5):
     """A plain device copy of a known size, for scaling the HBM byte counters."""
     import torch
@@ -245,11 +290,16 @@ def main():
     ap.add_argument("--graph", action="store_true", help="replay one step from a captured HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-untiled", action="store_true")
+    ap.add_argument("--config-search", action="store_true",
+                    help="only evaluate the configuration search against a measured sweep and exit")
     ap.add_argument("--copy-calibration", type=int, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.config_search:
+        config_search(args)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "only the one-GPU path is built: --gpus must be 1 (frames, and the "

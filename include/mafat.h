@@ -73,6 +73,7 @@ typedef enum {
 typedef enum { MAFAT_CONV = 0, MAFAT_MAXPOOL = 1 } mafat_op;
 typedef enum { MAFAT_ACT_LINEAR = 0, MAFAT_ACT_LEAKY01 = 1 } mafat_act;
 typedef enum { MAFAT_F32 = 0, MAFAT_BF16 = 1 } mafat_dtype;
+typedef enum { MAFAT_MEM_DEVICE = 0, MAFAT_MEM_PAPER = 1 } mafat_mem_model;
 
 /* One layer (section 4.1 describes a layer by width, height, filter size
  * and stride; channels, padding and activation are added).  c_out and act
@@ -191,6 +192,45 @@ int mafat_run_network(const mafat_plan* plan, int32_t batch, int32_t dtype,
                       const void* const* w, const float* const* scale,
                       const float* const* bias, void* workspace, size_t ws_bytes,
                       void* stream);
+
+/* Memory prediction for a plan (section 4.1).
+ *   model MAFAT_MEM_PAPER: the paper's predictor (Algorithm 1) on this plan's
+ *     region tables ("Grid"): the largest, over every tile of every group
+ *     and every layer of the group, of
+ *       w_out*h_out*c_in*f*f/s (im2col scratch) + w_out*h_out*c_out (output)
+ *       + 2 * w_in*h_in*c_in (input),
+ *     with the tile's input/output extents at that layer, halo included, in
+ *     elements (integer division by s), times the dtype's element size (4 or
+ *     2 bytes); batch is ignored.  The paper adds a platform constant (31 MB
+ *     on its board); the caller adds its own (see mafat_get_config).
+ *   model MAFAT_MEM_DEVICE: the device memory a run of this library needs,
+ *     all of it caller-owned: input, output and cut tensors (batch frames),
+ *     parameters (weights in dtype, float32 scale and bias) and the
+ *     workspace (mafat_workspace_size).  Every tile of a stage runs at once
+ *     on the GPU, so the workspace holds every tile's intermediates.
+ * *bytes receives the prediction.  Errors: EINVAL (null plan or pointer,
+ * batch < 1, unknown model), EUNSUPPORTED (dtype). */
+int mafat_predict_mem(const mafat_plan* plan, int32_t model, int32_t batch, int32_t dtype,
+                      int64_t* bytes);
+
+/* Configuration search (section 4.2, Algorithm 2): for each cut in cuts[]
+ * (in order; a cut <= 0 or >= n_layers means one group of all layers) and
+ * each first-group grid t in grids[] (in order; t x t tiles), the plan
+ * {cut, t x t, second_grid x second_grid} is predicted with
+ * mafat_predict_mem(model, batch, dtype); the first whose prediction plus
+ * bias_bytes is below limit_bytes is returned (*out_fits = 1).  If none
+ * fits, the last one tried is returned (*out_fits = 0) -- with the paper's
+ * lists (cuts {16, 12, 8}, grids {1..5}, second grid 2) that is its
+ * fallback 5x5/8/2x2.  Outputs: *out_cut (n_layers for one group),
+ * *out_grid1, *out_grid2 (0 for one group), *out_pred (prediction + bias;
+ * may be NULL), *out_fits (may be NULL).  Errors: EINVAL (null pointer,
+ * empty list, second_grid < 1) and the errors of mafat_plan_create for a
+ * candidate that cannot be planned. */
+int mafat_get_config(const mafat_layer* layers, int32_t n_layers, int32_t in_h, int32_t in_w,
+                     int32_t in_c, int32_t model, int32_t batch, int32_t dtype, int64_t bias_bytes,
+                     int64_t limit_bytes, const int32_t* cuts, int32_t n_cuts, const int32_t* grids,
+                     int32_t n_grids, int32_t second_grid, int32_t* out_cut, int32_t* out_grid1,
+                     int32_t* out_grid2, int64_t* out_pred, int32_t* out_fits);
 
 /* Static text of a status code. */
 const char* mafat_status_string(int status);

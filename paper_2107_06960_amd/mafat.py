@@ -26,14 +26,15 @@ MAFAT_EWORKSPACE, MAFAT_EHIP, MAFAT_ENOMEM = -4, -5, -6
 MAFAT_CONV, MAFAT_MAXPOOL = 0, 1
 MAFAT_ACT_LINEAR, MAFAT_ACT_LEAKY01 = 0, 1
 MAFAT_F32, MAFAT_BF16 = 0, 1
+MAFAT_MEM_DEVICE, MAFAT_MEM_PAPER = 0, 1
+MEM_MODELS = {"device": MAFAT_MEM_DEVICE, "paper": MAFAT_MEM_PAPER}
 DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
 
 # Every symbol include/mafat.h declares.
 EXPORTS = ("mafat_plan_create", "mafat_plan_destroy", "mafat_plan_layer_shape", "mafat_plan_group",
            "mafat_plan_regions", "mafat_plan_macs", "mafat_plan_stages", "mafat_plan_stage_layers",
            "mafat_workspace_size", "mafat_run_group", "mafat_run_stage", "mafat_run_network",
-           "mafat_status_string",
-           "mafat_last_error")
+           "mafat_predict_mem", "mafat_get_config", "mafat_status_string", "mafat_last_error")
 
 
 class mafat_layer(ctypes.Structure):
@@ -83,6 +84,10 @@ def lib():
         L.mafat_run_group.argtypes = [planp, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp, vpp]
         L.mafat_run_stage.argtypes = [planp, i32, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp]
         L.mafat_run_network.argtypes = [planp, i32, i32, vp, vp, vpp, vpp, vpp, vpp, vp, sz, vp]
+        i64p = ctypes.POINTER(i64)
+        L.mafat_predict_mem.argtypes = [planp, i32, i32, i32, i64p]
+        L.mafat_get_config.argtypes = [ctypes.POINTER(mafat_layer), i32, i32, i32, i32, i32, i32, i32, i64, i64,
+                                       i32p, i32, i32p, i32, i32, i32p, i32p, i32p, i64p, i32p]
         L.mafat_status_string.argtypes = [ctypes.c_int]
         L.mafat_status_string.restype = ctypes.c_char_p
         L.mafat_last_error.argtypes = []
@@ -202,6 +207,43 @@ def mafat_run_network(plan, batch, dtype, x, y, cut_bufs, w, scale, bias, worksp
                                    _ptrs(bias), workspace, ws_bytes, stream))
 
 
+def _layer_array(layers):
+    arr = (mafat_layer * len(layers))()
+    for k, L in enumerate(layers):
+        op = MAFAT_CONV if L["op"] == W.CONV else MAFAT_MAXPOOL
+        act = MAFAT_ACT_LEAKY01 if L.get("act") == W.LEAKY else MAFAT_ACT_LINEAR
+        arr[k] = mafat_layer(op, int(L.get("c_out", 0)), int(L["f"]), int(L["s"]), int(L["p"]), act)
+    return arr
+
+
+def mafat_predict_mem(plan, model, batch, dtype):
+    """Predicted bytes (int) of a plan handle under model 'device' or 'paper'."""
+    out = ctypes.c_int64()
+    _check("mafat_predict_mem", lib().mafat_predict_mem(plan, MEM_MODELS.get(model, model), batch,
+                                                        DTYPES.get(dtype, dtype), ctypes.byref(out)))
+    return out.value
+
+
+def mafat_get_config(layers, in_hwc, limit_bytes, model="paper", batch=1, dtype="f32", bias_bytes=0,
+                     cuts=(16, 12, 8), grids=(1, 2, 3, 4, 5), second_grid=2):
+    """Algorithm 2.  Returns (tiling spec in the paper's notation, prediction + bias, fits)."""
+    h, w, c = in_hwc
+    cc = (ctypes.c_int32 * len(cuts))(*cuts)
+    gg = (ctypes.c_int32 * len(grids))(*grids)
+    oc, o1, o2, fits = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+    pred = ctypes.c_int64()
+    _check("mafat_get_config",
+           lib().mafat_get_config(_layer_array(layers), len(layers), h, w, c, MEM_MODELS.get(model, model), batch,
+                                  DTYPES.get(dtype, dtype), int(bias_bytes), int(limit_bytes), cc, len(cuts), gg,
+                                  len(grids), second_grid, ctypes.byref(oc), ctypes.byref(o1), ctypes.byref(o2),
+                                  ctypes.byref(pred), ctypes.byref(fits)))
+    if oc.value >= len(layers):
+        spec = f"{o1.value}x{o1.value}/NoCut"
+    else:
+        spec = f"{o1.value}x{o1.value}/{oc.value}/{o2.value}x{o2.value}"
+    return spec, pred.value, bool(fits.value)
+
+
 # ------------------------------------------------------------------ convenience
 
 class Plan:
@@ -240,6 +282,9 @@ class Plan:
 
     def stages(self, g):
         return mafat_plan_stages(self.handle, g)
+
+    def predict_mem(self, model="device", batch=1, dtype="bf16"):
+        return mafat_predict_mem(self.handle, model, batch, dtype)
 
     def workspace_size(self, batch, dtype):
         return mafat_workspace_size(self.handle, batch, DTYPES.get(dtype, dtype))

@@ -1,0 +1,47 @@
+"""GPU: the device memory model of mafat_predict_mem against the device
+memory a run actually holds (torch's allocator statistics), on every
+full-size workload, the six configurations of the 608x608 sweep among them.
+
+The library allocates nothing; the caller's buffers (input, output, cut
+tensors, parameters, workspace) are all there is.  Measured: torch's
+requested-bytes statistic (the sizes asked of its allocator, before its
+rounding and block reuse), its peak over a run of the network minus its
+value before the network was built; the prediction must equal it exactly.
+(The allocator's own allocated-bytes figure, which rounds and may hand out a
+larger cached block, is printed alongside.)"""
+import pytest
+
+from paper_2107_06960_amd import workloads as W
+
+from gpu_util import require_gpu
+
+FULL = ["tiny", "yolo416_ftp3", "yolo608_5x5_8_2x2", "yolo608_4x4_12_1x1_b8"] + \
+    ["yolo608_sweep_" + t.replace("/", "_") for t in W.SWEEP6]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("name", FULL)
+def test_device_model_matches_measured_peak(name):
+    require_gpu()
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    wl = W.WORKLOADS[name]
+    print(f"[memory] {name}: {wl.h}x{wl.w}x{wl.c} {wl.tiling} batch={wl.batch} {wl.dtype}", flush=True)
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    base = torch.cuda.memory_stats().get("requested_bytes.all.current", 0)
+    base_alloc = torch.cuda.memory_allocated()
+    p = W.workload_inputs(wl)
+    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling)
+    net = M.Network(plan, p, wl.batch, wl.dtype)
+    x = net.input_tensor(p["x"])
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    net.run(x)
+    torch.cuda.synchronize()
+    used = torch.cuda.memory_stats()["requested_bytes.all.peak"] - base
+    alloc = torch.cuda.max_memory_allocated() - base_alloc
+    pred = plan.predict_mem("device", wl.batch, wl.dtype)
+    print(f"[memory] {name}: predicted {pred} B, requested {used} B (allocator blocks {alloc} B)", flush=True)
+    assert used == pred
+    del net, x

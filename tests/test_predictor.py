@@ -1,0 +1,137 @@
+"""Memory predictor (Algorithm 1) and configuration search (Algorithm 2):
+the library's C ABI against the oracle, and both against the paper.
+
+Pins to the paper (section 2, section 5, Table 1):
+  * one tile, one group (1x1/NoCut) at 608x608 float32: the prediction is
+    the Darknet memory of layer 2 that section 2 prints as 135 MB (input +
+    output + im2col scratch, 135.38 MiB), plus the second copy of the input
+    Algorithm 1 counts (2 * input);
+  * Table 1's "Algorithm" column at 256, 192, 128, 32 and 16 MB (limits in
+    MiB, bias 31 MiB, float32, 608x608) is reproduced by the search with
+    this predictor.  At 96, 80, 64 and 48 MB the paper's own search picked
+    coarser configurations than Algorithm 1 read literally does (its "Grid"
+    sizes are not given): those rows are parity unpinned, and the test
+    records the literal reading's picks so a change shows up.
+"""
+import numpy as np
+import pytest
+
+from oracle import predictor as P
+from paper_2107_06960_amd import mafat as M
+from paper_2107_06960_amd import workloads as W
+
+MiB = 1 << 20
+
+
+def _lib():
+    import os
+    if not os.path.exists(M.LIB_PATH):
+        from paper_2107_06960_amd import build
+        build.build(verbose=False)
+    return M.lib()
+
+
+@pytest.mark.parametrize("spec", ["1x1/NoCut", "2x2/NoCut", "5x5/8/2x2", "4x4/12/1x1", "3x3/4/2x2", "6x6/8/2x2"])
+def test_paper_model_matches_oracle_yolo608(spec):
+    _lib()
+    gs, r, c = W.parse_tiling(spec, 16)
+    plan = M.Plan(W.YOLOV2_16, (608, 608, 3), spec)
+    want = P.predict_mem(W.YOLOV2_16, 608, 608, 3, gs, r, c)
+    assert plan.predict_mem("paper", 1, "f32") == 4 * want
+    assert plan.predict_mem("paper", 1, "bf16") == 2 * want
+
+
+def test_paper_model_matches_oracle_random():
+    _lib()
+    rng = np.random.default_rng(21)
+    for _ in range(40):
+        layers, ch = [], int(rng.integers(1, 24))
+        for _ in range(int(rng.integers(1, 6))):
+            if rng.random() < 0.3 and layers and layers[-1]["op"] == W.CONV:
+                layers.append(W.maxpool())
+            else:
+                layers.append(W.conv(int(rng.integers(1, 40)), int(rng.choice([1, 3]))))
+        h, w = int(rng.integers(12, 70)), int(rng.integers(12, 70))
+        n = len(layers)
+        cut = int(rng.integers(1, n)) if n > 1 and rng.random() < 0.6 else None
+        gs = [0] if cut is None else [0, cut]
+        try:
+            plan = M.Plan(layers, (h, w, ch), (gs, [int(rng.integers(1, 4)) for _ in gs],
+                                               [int(rng.integers(1, 4)) for _ in gs]))
+        except M.MafatError:
+            continue  # grid finer than a group output: rejected by the planner
+        want = P.predict_mem(layers, h, w, ch, plan.group_start, plan.rows, plan.cols)
+        assert plan.predict_mem("paper", 1, "f32") == 4 * want
+
+
+def test_paper_model_one_tile_is_darknet_layer2():
+    # section 2: layer 2 of YOLOv2 at 608x608 needs 135 MB in Darknet (input
+    # 11.28 + output 22.56 + im2col scratch 101.53 MiB); Algorithm 1 counts
+    # the input twice
+    _lib()
+    plan = M.Plan(W.YOLOV2_16, (608, 608, 3), "1x1/NoCut")
+    pred = plan.predict_mem("paper", 1, "f32") / MiB
+    layer2_input = 304 * 304 * 32 * 4 / MiB
+    assert 134.5 <= pred - layer2_input <= 135.5
+
+
+TABLE1_PINNED = {256: "1x1/NoCut", 192: "1x1/NoCut", 128: "2x2/NoCut", 32: "5x5/8/2x2", 16: "5x5/8/2x2"}
+# literal reading's picks where the paper printed 2x2/12/2x2, 3x3/8/2x2, 5x5/8/2x2, 5x5/8/2x2
+TABLE1_UNPINNED = {96: "2x2/NoCut", 80: "3x3/NoCut", 64: "4x4/NoCut", 48: "5x5/12/2x2"}
+
+
+@pytest.mark.parametrize("mb", sorted(TABLE1_PINNED) + sorted(TABLE1_UNPINNED))
+def test_search_table1(mb):
+    _lib()
+    spec, pred, fits = M.mafat_get_config(W.YOLOV2_16, (608, 608, 3), mb * MiB, model="paper", dtype="f32",
+                                          bias_bytes=31 * MiB)
+    want = TABLE1_PINNED.get(mb, TABLE1_UNPINNED.get(mb))
+    assert spec == want
+    assert fits == (mb > 43)  # 5x5/8/2x2 (42.8 MiB) is the smallest prediction: below it, the fallback
+    # the oracle's search agrees
+    cut, t, g2, opred, ofits = P.get_config(W.YOLOV2_16, 608, 608, 3, mb * MiB)
+    ospec = f"{t}x{t}/NoCut" if cut == 16 else f"{t}x{t}/{cut}/{g2}x{g2}"
+    assert (ospec, opred, ofits) == (spec, pred, fits)
+
+
+def test_search_matches_oracle_over_limits():
+    _lib()
+    for mb in range(30, 260, 7):
+        for cuts in ((16, 12, 8), (8, 12, 16), (12, 4)):
+            spec, pred, fits = M.mafat_get_config(W.YOLOV2_16, (608, 608, 3), mb * MiB, model="paper",
+                                                  dtype="f32", bias_bytes=31 * MiB, cuts=cuts)
+            cut, t, g2, opred, ofits = P.get_config(W.YOLOV2_16, 608, 608, 3, mb * MiB, cuts=cuts)
+            ospec = f"{t}x{t}/NoCut" if cut == 16 else f"{t}x{t}/{cut}/{g2}x{g2}"
+            assert (spec, pred, fits) == (ospec, opred, ofits), (mb, cuts)
+
+
+def test_device_model_counts_every_buffer():
+    # the device model is the sum of the caller-owned buffers a run needs
+    _lib()
+    for name in ("yolo608_5x5_8_2x2", "yolo608_4x4_12_1x1_b8", "tiny"):
+        wl = W.WORKLOADS[name]
+        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling)
+        esz = 4 if wl.dtype == "f32" else 2
+        b = wl.batch
+        tot = b * wl.h * wl.w * wl.c * esz
+        tot += b * int(np.prod(plan.group_out_shape(plan.n_groups - 1))) * esz
+        tot += sum(b * int(np.prod(plan.group_out_shape(g))) * esz for g in range(plan.n_groups - 1))
+        for l, L in enumerate(wl.layers):
+            if L["op"] == W.CONV:
+                d = plan.shape(l)
+                tot += d[5] * L["f"] ** 2 * d[2] * esz + 8 * d[5]
+        tot += plan.workspace_size(b, wl.dtype)
+        assert plan.predict_mem("device", b, wl.dtype) == tot
+
+
+def test_predict_and_search_errors():
+    L = _lib()
+    import ctypes
+    plan = M.Plan(W.TINY, (64, 64, 3), "2x2")
+    out = ctypes.c_int64()
+    assert L.mafat_predict_mem(plan.handle, 7, 1, 0, ctypes.byref(out)) == M.MAFAT_EINVAL
+    assert L.mafat_predict_mem(plan.handle, 0, 0, 0, ctypes.byref(out)) == M.MAFAT_EINVAL
+    assert L.mafat_predict_mem(plan.handle, 0, 1, 9, ctypes.byref(out)) == M.MAFAT_EUNSUPPORTED
+    assert L.mafat_predict_mem(None, 0, 1, 0, ctypes.byref(out)) == M.MAFAT_EINVAL
+    with pytest.raises(M.MafatError):  # a grid finer than the group output cannot be planned
+        M.mafat_get_config(W.TINY, (64, 64, 3), 1, grids=(40,), cuts=(3,))
