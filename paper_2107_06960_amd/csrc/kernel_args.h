@@ -70,15 +70,15 @@ struct MfmaShape {
 
 // Instantiated patch kernel shapes: (br, bc, bm, bn, wgm, wgn, ring slots).
 #define MAFAT_PATCH_SHAPES                \
-  MAFAT_PATCH(16, 16, 256, 64, 4, 1, 2)   \
-  MAFAT_PATCH(10, 10, 128, 32, 4, 1, 4)   \
-  MAFAT_PATCH(8, 8, 64, 32, 4, 1, 4)
+  MAFAT_PATCH(16, 16, 256, 64, 8, 1, 2)   \
+  MAFAT_PATCH(12, 12, 192, 64, 4, 2, 2)   \
+  MAFAT_PATCH(10, 10, 128, 32, 8, 1, 4)   \
+  MAFAT_PATCH(8, 8, 64, 32, 4, 2, 4)
 #ifdef MAFAT_TUNING
 #define MAFAT_PATCH_TUNE_SHAPES           \
-  MAFAT_PATCH(10, 10, 128, 32, 2, 2, 4)   \
-  MAFAT_PATCH(16, 16, 256, 64, 2, 2, 2)   \
-  MAFAT_PATCH(8, 16, 128, 64, 2, 2, 3)    \
-  MAFAT_PATCH(16, 16, 256, 32, 2, 2, 3)
+  MAFAT_PATCH(16, 16, 256, 64, 4, 1, 2)   \
+  MAFAT_PATCH(12, 12, 192, 64, 4, 1, 2)   \
+  MAFAT_PATCH(10, 10, 128, 32, 4, 1, 4)
 #else
 #define MAFAT_PATCH_TUNE_SHAPES
 #endif
@@ -92,11 +92,9 @@ struct MfmaShape {
   MAFAT_RING(128, 128, 2, 2, 2, 3, 1)
 #ifdef MAFAT_TUNING
 #define MAFAT_RING_TUNE_SHAPES        \
-  MAFAT_RING(64, 64, 2, 2, 2, 6, 1)   \
-  MAFAT_RING(64, 64, 2, 2, 1, 4, 1)   \
-  MAFAT_RING(32, 64, 2, 2, 1, 6, 1)   \
-  MAFAT_RING(32, 64, 2, 2, 1, 4, 1)   \
-  MAFAT_RING(32, 64, 2, 2, 1, 3, 0)
+  MAFAT_RING(32, 32, 2, 2, 1, 3, 1)   \
+  MAFAT_RING(32, 32, 2, 2, 1, 4, 1)   \
+  MAFAT_RING(64, 64, 2, 2, 2, 4, 1)
 #else
 #define MAFAT_RING_TUNE_SHAPES
 #endif

@@ -101,17 +101,18 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
   }
   const int esz = (dtype == MAFAT_BF16) ? 2 : 4;
   const double K = static_cast<double>(S.f) * S.f * S.cin;
-  if (dtype == MAFAT_BF16 && S.f == 3 && S.cin >= 64) {
+  if (dtype == MAFAT_BF16 && S.f == 3) {
     // 3x3 patch kernel (each block's input patch loaded once per 32-channel
-    // chunk and shared by the nine taps).  Shapes from a sweep over the
-    // YOLOv2 stages at 608x608 (5x5/8/2x2): 16x16-pixel blocks x 64
-    // channels with four waves of 64x64 accumulators are the fastest where
-    // tiles are large; on small tiles (the deep layers' ~20x20) 16x16 blocks
-    // mostly compute padding, and 10x10 blocks x 32 channels win, 8x8 blocks
-    // on smaller tiles still.  The pick: the largest block whose padded
-    // pixel count stays within 1.4x of the tiles' pixels.  With fewer input
-    // channels (one or two chunks) the LDS-ring kernel's higher occupancy
-    // wins instead (below).
+    // chunk and shared by the nine taps), 8 waves per workgroup (two per
+    // SIMD: LDS reads reach ~220 bytes/clock per CU only with more than one
+    // wave per SIMD).  Block shape by a model fitted to a sweep of the
+    // YOLOv2 stages at 608x608 (5x5/8/2x2): one workgroup per CU (the ring
+    // takes most of the LDS), so a stage takes ceil(workgroups / 256)
+    // rounds of ~3 us (decode, first loads, epilogue) plus, per 32-channel
+    // chunk, ~0.18 ns per block pixel-channel (edge blocks of a tile compute
+    // their full rectangle).  Large blocks waste work on small tiles and
+    // leave CUs idle on small stages; small blocks re-load more halo and
+    // weights.
     c.kind = K_CONV_PATCH;
     struct PS { int br, bc, bm, bn, wgm, wgn, ns; };
     static const PS kPatch[] = {
@@ -119,17 +120,21 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
         MAFAT_PATCH_SHAPES
 #undef MAFAT_PATCH
     };
-    int64_t useful = 0;
-    for (const TileGeom& T : S.tiles) useful += static_cast<int64_t>(T.ch) * T.cw;
-    const int npatch = static_cast<int>(sizeof(kPatch) / sizeof(kPatch[0]));
-    for (int k = 0; k < npatch; ++k) {
-      const PS& r = kPatch[k];
+    const int chunks = S.cin / 32;
+    double best = 1e30;
+    for (const PS& r : kPatch) {
+      if (r.bn > S.cout && r.bn > 32) continue;
       int64_t mb = 0;
       for (const TileGeom& T : S.tiles)
         mb += static_cast<int64_t>((T.ch + r.br - 1) / r.br) * ((T.cw + r.bc - 1) / r.bc);
-      c.br = r.br; c.bc = r.bc; c.bm = r.bm; c.bn = r.bn; c.wgm = r.wgm; c.wgn = r.wgn; c.depth = r.ns;
-      c.blocks = mb * ((S.cout + r.bn - 1) / r.bn);
-      if (static_cast<double>(mb) * r.br * r.bc <= 1.4 * static_cast<double>(useful)) break;
+      const int64_t blocks = mb * ((S.cout + r.bn - 1) / r.bn);
+      const double rounds = std::ceil(static_cast<double>(blocks) * batch / 256.0);
+      const double t = rounds * (3e-6 + chunks * static_cast<double>(r.bm) * r.bn * 0.18e-9);
+      if (t < best * 0.98) {
+        best = t;
+        c.br = r.br; c.bc = r.bc; c.bm = r.bm; c.bn = r.bn; c.wgm = r.wgm; c.wgn = r.wgn; c.depth = r.ns;
+        c.blocks = blocks;
+      }
     }
   } else if (dtype == MAFAT_BF16) {
     // LDS-ring kernel.  Block shapes from a sweep over every YOLOv2 stage
