@@ -28,6 +28,9 @@
 // weight rows past c_out, are fetched at an offset with bit 31 set, past the
 // buffer descriptor's range: the range check returns zeros.  Loads run NS-1
 // chunks ahead; every chunk costs one explicit vmcnt wait and one barrier.
+// With NS = 1 (one slot) a chunk is loaded, awaited and computed in turn:
+// the LDS footprint halves, so two workgroups share a CU and hide each
+// other's load latency.
 //
 // Requires f = 3, c_in % 32 == 0, c_out % 16 == 0, byte offsets below 2^31
 // within a frame's source buffer and within the weights (host-checked); a
@@ -94,7 +97,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
   static_assert(MT >= 1 && NT >= 1 && MT * 16 == WM && NT * 16 == WN, "wave tile");
   static_assert(BR * BC <= BM && BM % (16 * WGM) == 0, "block rows");
   static_assert(!POOL || (BR % 2 == 0 && BC % 2 == 0), "pooled blocks cover whole windows");
-  static_assert(NS >= 2 && NS <= 6 && (NS - 2) * LPS <= 63, "ring depth");
+  static_assert(NS >= 1 && NS <= 6 && (NS - 2) * LPS <= 63, "ring depth");
   __shared__ __align__(1024) unsigned char smem[NS * SLOT + (SINK ? 1024 : 0)];
 
   KTile tl;
@@ -247,16 +250,28 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
     }
   };
 
+  if constexpr (NS == 1) {
+    // One slot (half the LDS, so two workgroups fit on a CU and hide each
+    // other's load latency): load a chunk, wait, compute, repeat.
+    for (int s = 0; s < nstage; ++s) {
+      if (s > 0) pbarrier();  // every wave is done reading the slot
+      issue(s, 0);
+      pwait_vmcnt<0>();
+      pbarrier();
+      compute(0);
+    }
+  } else {
 #pragma unroll
-  for (int p = 0; p < NS - 1; ++p)
-    if (p < nstage) issue(p, p);
-  int slot = 0;
-  for (int s = 0; s < nstage; ++s) {
-    pwait_stage<LPS, NS - 2>(nstage - 1 - s);
-    pbarrier();
-    if (s + NS - 1 < nstage) issue(s + NS - 1, slot == 0 ? NS - 1 : slot - 1);
-    compute(slot);
-    slot = (slot == NS - 1) ? 0 : slot + 1;
+    for (int p = 0; p < NS - 1; ++p)
+      if (p < nstage) issue(p, p);
+    int slot = 0;
+    for (int s = 0; s < nstage; ++s) {
+      pwait_stage<LPS, NS - 2>(nstage - 1 - s);
+      pbarrier();
+      if (s + NS - 1 < nstage) issue(s + NS - 1, slot == 0 ? NS - 1 : slot - 1);
+      compute(slot);
+      slot = (slot == NS - 1) ? 0 : slot + 1;
+    }
   }
 
   // Epilogue: folded batch-norm, activation (leaky: max(v, 0.1 v)), the

@@ -594,11 +594,13 @@ void conv_rgb_kernel(const StageArgs a) {
 //      windows of 2x2); lane l loads, for each ky, the pixel (kx = l / 16)
 //      of its pixel's (l % 16) filter window (kx slot 3 repeats kx = 2, which
 //      meets zero weights);
-//   3. the epilogue follows store_direct: without a pool the weights are
-//      the A operand (a lane ends with 4 consecutive channels of one pixel,
-//      one 8-byte store); with a fused 2x2 pool the pixels are (a lane's 4
-//      accumulator rows are one window of one channel: scale and bias, the
-//      window maximum, then the activation, which is monotone).
+//   3. epilogue: without a pool the weights are the A operand (a lane ends
+//      with 4 consecutive channels of one pixel, one 8-byte store); with a
+//      fused 2x2 pool the pixels are (a lane's 4 accumulator rows are one
+//      window of one channel: scale and bias, the window maximum, then the
+//      activation, which is monotone), and a wave takes whole rows of
+//      tiles, whose pooled output is one contiguous run: it is staged in LDS
+//      and written with 16-byte stores.
 // Requires c_out = 16 * NJ, c_in = 3, f = 3, s = 1, p = 1 (host-checked).
 template <bool POOL, int NJ>
 __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
@@ -616,6 +618,7 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
   __shared__ __align__(16) uint16_t sx[SR * RS];
   __shared__ __align__(16) uint16_t swt[COUT * 27];
   __shared__ __align__(16) float ssb[2 * COUT];  // scale, bias
+  __shared__ __align__(16) uint16_t spool[POOL ? 4 * 4 * (BC / 8) * COUT : 8];  // per-wave pooled row staging
 
   MAFAT_TRACE(0);
   KTile tl;
@@ -692,16 +695,15 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
 
   const int p = lane & 15;  // pixel of the MFMA tile whose operand this lane loads
   const int kx = min(kq, 2);
-  for (int t = wave; t < NTILE; t += 4) {
-    // tile t: rows 2 (t / TPR) .. +1, columns 8 (t % TPR) .. +7, as 4
-    // windows of 2x2: pixel p is window p >> 2, position p & 3 in it
+  // MFMAs of 16-pixel tile t: rows 2 (t / TPR) .. +1, columns 8 (t % TPR)
+  // .. +7, as 4 windows of 2x2 (pixel p is window p >> 2, position p & 3).
+  auto tile_mfma = [&](int t, f32x4 (&acc)[NJ]) {
     const int py = 2 * (t / TPR) + ((p & 3) >> 1);
     const int pxl = 8 * (t % TPR) + 2 * (p >> 2) + (p & 1);
     const u32x2* xp = reinterpret_cast<const u32x2*>(sx + py * RS + (pxl + kx) * 4);
     u32x2 xf[3];
 #pragma unroll
     for (int ky = 0; ky < 3; ++ky) xf[ky] = xp[ky * (RS / 4)];
-    f32x4 acc[NJ];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -712,22 +714,50 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
                       : __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(wa, xa, acc[j], 0, 0, 0);
       }
     }
-    if constexpr (POOL) {
-      // a lane's accumulator rows are window kq of the tile, column = channel
-      const int oy = oy0 + 2 * (t / TPR), ox = ox0 + 8 * (t % TPR) + 2 * kq;
-      const bool ok = (oy - tl.cy0) < tl.ch && (ox - tl.cx0) < tl.cw;
-      uint16_t* drow = dst + (((oy >> 1) - tl.dy0) * tl.dw + ((ox >> 1) - tl.dx0)) * COUT;
+  };
+  if constexpr (POOL) {
+    // A wave takes whole tile rows (the TPR tiles of two conv rows, i.e.
+    // 4 * TPR pooled pixels of one pooled row, contiguous in the output).
+    // A lane's accumulator rows are window kq of its tile, column = its
+    // channel: the pooled values go through this wave's LDS staging row,
+    // then leave as 16-byte stores (8 channels of one pooled pixel per lane).
+    constexpr int PPR = 4 * TPR;   // pooled pixels per tile row
+    constexpr int CPL = COUT / 8;  // 16-byte chunks per pooled pixel
+    uint16_t* lrow = spool + wave * PPR * COUT;
+    for (int tr = wave; tr < BR / 2; tr += 4) {
 #pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        float v[4];
+      for (int c = 0; c < TPR; ++c) {
+        f32x4 acc[NJ];
+        tile_mfma(tr * TPR + c, acc);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = fmaf(acc[j][r], sc[j][0], bi[j][0]);
-        float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-        m = fmaxf(m, slope * m);
-        if (ok) store1(drow + 16 * j + p, m);
+        for (int j = 0; j < NJ; ++j) {
+          float v[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) v[r] = fmaf(acc[j][r], sc[j][0], bi[j][0]);
+          float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+          m = fmaxf(m, slope * m);
+          store1(lrow + (c * 4 + kq) * COUT + 16 * j + p, m);
+        }
       }
-    } else {
+      __builtin_amdgcn_wave_barrier();  // LDS ops of a wave run in order; keep the compiler from moving them
+      const int oy = oy0 + 2 * tr;
+#pragma unroll
+      for (int e = lane; e < PPR * CPL; e += 64) {
+        const int q = e / CPL, ck = e - q * CPL;
+        const int ox = ox0 + 2 * q;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(lrow + q * COUT + ck * 8);
+        if ((oy - tl.cy0) < tl.ch && (ox - tl.cx0) < tl.cw)
+          *reinterpret_cast<u32x4*>(dst + (((oy >> 1) - tl.dy0) * tl.dw + ((ox >> 1) - tl.dx0)) * COUT + ck * 8) = v;
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  } else {
+    for (int t = wave; t < NTILE; t += 4) {
+      f32x4 acc[NJ];
+      tile_mfma(t, acc);
       // a lane's accumulator rows are channels 4 kq .. +3 of pixel p
+      const int py = 2 * (t / TPR) + ((p & 3) >> 1);
+      const int pxl = 8 * (t % TPR) + 2 * (p >> 2) + (p & 1);
       const int oy = oy0 + py, ox = ox0 + pxl;
       const bool ok = (oy - tl.cy0) < tl.ch && (ox - tl.cx0) < tl.cw;
       uint16_t* drow = dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * COUT;

@@ -88,7 +88,7 @@ StageConfig tune_override(const Stage& S, StageConfig c) {
 // re-read fewer operands, smaller ones give more workgroups.
 StageConfig choose_config(const Stage& S, int batch, int dtype) {
   StageConfig c{};
-  c.bm = 64; c.bn = 64; c.depth = 3; c.kg = 1; c.wgm = 2; c.wgn = 2;
+  c.bm = 64; c.bn = 64; c.depth = 3; c.kg = 1; c.wgm = 2; c.wgn = 2; c.br = 0; c.bc = 0;
   if (S.kind == STAGE_POOL) { c.kind = K_POOL; return c; }
   if (!mfma_ok(S, dtype)) {
     c.kind = rgb_ok(S) ? K_CONV_RGB : K_CONV_DIRECT;
@@ -124,6 +124,10 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
     double best = 1e30;
     for (const PS& r : kPatch) {
       if (r.bn > S.cout && r.bn > 32) continue;
+      // One-slot rings only for single-chunk layers (c_in = 32), where they
+      // are measured fastest (three workgroups per CU overlap their loads);
+      // the model below does not capture that, so the shape is taken as is.
+      if ((r.ns == 1) != (chunks == 1 && S.cout >= 64)) continue;
       int64_t mb = 0;
       for (const TileGeom& T : S.tiles)
         mb += static_cast<int64_t>((T.ch + r.br - 1) / r.br) * ((T.cw + r.bc - 1) / r.bc);
@@ -136,7 +140,8 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
         c.blocks = blocks;
       }
     }
-  } else if (dtype == MAFAT_BF16) {
+  }
+  if (dtype == MAFAT_BF16 && (S.f != 3 || c.kind != K_CONV_PATCH || c.br == 0)) {
     // LDS-ring kernel.  Block shapes from a sweep over every YOLOv2 stage
     // at 608x608 (tiling 5x5/8/2x2; blocks 32..128 x 32..128, ring depths
     // 2..8, one or two K groups): the K loop of a workgroup is bound by LDS
@@ -159,7 +164,7 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
     int64_t mb = 0;
     for (const TileGeom& T : S.tiles) mb += (static_cast<int64_t>(T.ch) * T.cw + c.bm - 1) / c.bm;
     c.blocks = mb * ((S.cout + c.bn - 1) / c.bn);
-  } else {
+  } else if (dtype != MAFAT_BF16) {
     c.kind = K_CONV_MFMA;
     const double clk = 2.4e9, mfma_rate = 4096.0 * clk, l2_rate = 64.0 * clk, t0 = 2e-6;
     static const int kShapes[][2] = {{128, 128}, {128, 64}, {64, 128}, {64, 64}, {64, 32}, {32, 64}};
