@@ -22,8 +22,13 @@
 // buffer_load_dwordx4 ... lds (global -> LDS, 64 lanes = 1 KiB = 16 rows of
 // 64 bytes per instruction): lane l writes row (l >> 2) of its 16-row group
 // at 16-byte position (l & 3) and fetches the row's 16-byte chunk
-// (l & 3) ^ ((row >> 1) & 3), so MFMA fragment reads of consecutive rows at
-// one K offset hit distinct LDS banks.  Patch pixels outside the image (the
+// (l & 3) ^ key(row), so that the 8 rows an MFMA fragment read serves per
+// LDS cycle (at one K offset) hit distinct banks: weight rows use
+// key = (row >> 1) & 3 (they are read 8 consecutive rows at a time); patch
+// pixel (py, px) uses key = ((px >> 1) ^ 2 py) & 3, which stays
+// conflict-free across the block-row wraps, 2x2 pool windows and tap shifts
+// of the fragments (found by enumerating the fragments of every block
+// shape).  Patch pixels outside the image (the
 // zero padding), outside the tile's source region, or past the patch, and
 // weight rows past c_out, are fetched at an offset with bit 31 set, past the
 // buffer descriptor's range: the range check returns zeros.  Loads run NS-1
@@ -64,7 +69,7 @@ __device__ __forceinline__ void pwait_stage(int rem) {
 }
 __device__ __forceinline__ void pbarrier() { asm volatile("s_barrier" ::: "memory"); }
 
-// Byte offset of 16-byte chunk q of 64-byte row `row` in a slot region.
+// Byte offset of 16-byte chunk q of 64-byte weight row `row` in a slot region.
 __device__ __forceinline__ int swz(int row, int q) { return row * 64 + ((q ^ ((row >> 1) & 3)) << 4); }
 
 // Block pixel (py, px) of GEMM row r.
@@ -153,7 +158,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
     const int py = p / PC, px = p - (p / PC) * PC;
     const int iy = by0 - 1 + py, ix = bx0 - 1 + px;
     const bool ok = g < NA && p < PR * PC && iy >= ry0 && iy < ry1 && ix >= rx0 && ix < rx1;
-    const int chunk = lpos ^ ((p >> 1) & 3);
+    const int chunk = lpos ^ (((px >> 1) ^ (py << 1)) & 3);
     a_off[k] = ok ? static_cast<unsigned>((((iy - tl.sy0) * sw + (ix - tl.sx0)) * cin) * 2 + chunk * 16)
                   : 0x80000000u;
   }
@@ -191,14 +196,21 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
   // 16-byte chunk q = l >> 4 (K elements 8q .. 8q+7 of the 32).  B: weight
   // row tap * BN + wn*WN + 16 j + (l & 15), chunk q.
   const int q = lane >> 4;
-  int p0[MT];
+  // Per fragment: byte offset of the lane's patch pixel (tap (0, 0)) and the
+  // two halves of its swizzle key for each tap column / row.
+  int pb[MT], kx3[MT][3], ky3[MT][3];
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
     int r = wm * WM + i * 16 + (lane & 15);
     r = (r < BR * BC) ? r : 0;  // padding rows: any valid pixel, result discarded
     int py, px;
     block_pixel<BC, POOL>(r, &py, &px);
-    p0[i] = py * PC + px;
+    pb[i] = (py * PC + px) * 64;
+#pragma unroll
+    for (int d = 0; d < 3; ++d) {
+      kx3[i][d] = q ^ ((px + d) >> 1);
+      ky3[i][d] = (py + d) << 1;
+    }
   }
   const int rb = wn * WN + (lane & 15);
   const int b_lane = A_BYTES + swz(rb, q);  // (tap * BN + 16 j) rows later: same swizzle
@@ -215,9 +227,11 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
   // interleaving them, so each tap's LDS latency hides behind the previous
   // tap's MFMAs.
   auto load_frags = [&](const unsigned char* sp, int t, u32x4 (&af)[MT], u32x4 (&bfr)[NT]) {
-    const int toff = (t / 3) * PC + (t % 3);
+    const int ty = t / 3, tx = t % 3;
 #pragma unroll
-    for (int i = 0; i < MT; ++i) af[i] = *reinterpret_cast<const u32x4*>(sp + swz(p0[i] + toff, q));
+    for (int i = 0; i < MT; ++i)
+      af[i] = *reinterpret_cast<const u32x4*>(sp + pb[i] + (ty * PC + tx) * 64 +
+                                              (((kx3[i][tx] ^ ky3[i][ty]) & 3) << 4));
 #pragma unroll
     for (int j = 0; j < NT; ++j)
       bfr[j] = *reinterpret_cast<const u32x4*>(sp + b_lane + (t * BN + j * 16) * 64);
