@@ -31,6 +31,9 @@ def hipcc():
 
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+          # matrix-core accumulators in ordinary VGPRs (no AGPR copies in
+          # the epilogues)
+          "-mllvm", "-amdgpu-mfma-vgpr-form",
           "-I", os.path.join(HERE, "..", "include")]
 
 

@@ -46,6 +46,20 @@
 #include "kernel_args.h"
 
 namespace mafat {
+#ifdef MAFAT_TUNING
+// Tuning builds only: phase timestamps (wall clock, 100 MHz) of three
+// workgroups (the first, the middle and the last of the grid).
+__device__ long long g_patch_trace[3][64];
+#define MAFAT_PTRACE(slot_)                                                                      \
+  do {                                                                                           \
+    if (threadIdx.x == 0 && (slot_) < 64 &&                                                      \
+        (blockIdx.x == 0 || blockIdx.x == gridDim.x / 2 || blockIdx.x == gridDim.x - 1))         \
+      g_patch_trace[blockIdx.x == 0 ? 0 : (blockIdx.x == gridDim.x - 1 ? 2 : 1)][(slot_)] =      \
+          wall_clock64();                                                                        \
+  } while (0)
+#else
+#define MAFAT_PTRACE(slot_) do {} while (0)
+#endif
 namespace {
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
@@ -105,8 +119,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
   static_assert(NS >= 1 && NS <= 6 && (NS - 2) * LPS <= 63, "ring depth");
   __shared__ __align__(1024) unsigned char smem[NS * SLOT + (SINK ? 1024 : 0)];
 
+  MAFAT_PTRACE(0);
   KTile tl;
   const BlockPos bp = decode_block(a, &tl);
+  MAFAT_PTRACE(1 + (tl.ch < -1 ? 1 : 0));
   const int tid = static_cast<int>(threadIdx.x), lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WGN, wn = wave - wm * WGN;
@@ -272,6 +288,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
       issue(s, 0);
       pwait_vmcnt<0>();
       pbarrier();
+      MAFAT_PTRACE(8 + s);
       compute(0);
     }
   } else {
@@ -282,12 +299,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
     for (int s = 0; s < nstage; ++s) {
       pwait_stage<LPS, NS - 2>(nstage - 1 - s);
       pbarrier();
+      MAFAT_PTRACE(8 + s);
       if (s + NS - 1 < nstage) issue(s + NS - 1, slot == 0 ? NS - 1 : slot - 1);
       compute(slot);
       slot = (slot == NS - 1) ? 0 : slot + 1;
     }
   }
 
+  MAFAT_PTRACE(4);
   // Epilogue: folded batch-norm, activation (leaky: max(v, 0.1 v)), the
   // fused pool, round to bf16, store the pixels inside the tile's computed
   // rectangle.
@@ -335,6 +354,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
       }
     }
   }
+  MAFAT_PTRACE(5);
 }
 
 template <bool POOL>
@@ -364,4 +384,9 @@ hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs&
   return pool ? launch_patch_p<true>(shape, args, stream, ev) : launch_patch_p<false>(shape, args, stream, ev);
 }
 
+#ifdef MAFAT_TUNING
+extern "C" int mafat_debug_patch_trace(long long* host_out) {
+  return hipMemcpyFromSymbol(host_out, HIP_SYMBOL(g_patch_trace), sizeof(g_patch_trace)) == hipSuccess ? 0 : -1;
+}
+#endif
 }  // namespace mafat

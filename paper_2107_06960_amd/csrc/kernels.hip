@@ -584,9 +584,10 @@ void conv_rgb_kernel(const StageArgs a) {
 // a BR x BC block of conv outputs (all c_out channels) of one tile:
 //   1. the (BR+2) x (BC+2) input patch is staged in LDS as 8-byte pixels
 //      (c0, c1, c2, 0), so the 4 K values of a lane's operand are one
-//      aligned 8-byte LDS read at a per-lane constant offset; the patch is
-//      fetched with coalesced 2-byte buffer loads (all of a thread's loads
-//      are issued before its first LDS write), zero outside the image and
+//      aligned 8-byte LDS read at a per-lane constant offset; a thread
+//      fetches whole pixels, each with one aligned 4-byte and one 2-byte
+//      buffer load (all of a thread's loads are issued before its first
+//      LDS write), zero outside the image and
 //      outside the tile's source region (those loads get an offset past
 //      the descriptor's range); the weights, scale and bias, the same for
 //      every workgroup, are staged with one 16-byte load per thread;
@@ -613,8 +614,6 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
   constexpr int TPR = BC / 8;                // tiles per 2 rows
   constexpr int COUT = 16 * NJ;
   constexpr int W16 = COUT * 27 * 2 / 16;    // 16-byte pieces of the weights
-  constexpr int NEL = SR * SC * 4;           // staged elements (incl. the zero 4th channel)
-  constexpr int NLD = (NEL + 255) / 256;     // staging elements per thread
   __shared__ __align__(16) uint16_t sx[SR * RS];
   __shared__ __align__(16) uint16_t swt[COUT * 27];
   __shared__ __align__(16) float ssb[2 * COUT];  // scale, bias
@@ -628,7 +627,6 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
   const int nbx = (tl.cw + BC - 1) / BC;
   const int by = bp.mb / nbx, bx = bp.mb - by * nbx;
   const int oy0 = tl.cy0 + by * BR, ox0 = tl.cx0 + bx * BC;
-  const uint16_t* src = static_cast<const uint16_t*>(a.src) + bp.frame * a.src_fstride + tl.src_off;
   uint16_t* dst = static_cast<uint16_t*>(a.dst) + bp.frame * a.dst_fstride + tl.dst_off;
   const int kq = lane >> 4;
 
@@ -642,29 +640,45 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
     const int i = tid - W16 - COUT / 4;
     reinterpret_cast<f32x4*>(ssb + COUT)[i] = reinterpret_cast<const f32x4*>(a.bias)[i];
   }
-  // Input patch: rows oy0-1 .. oy0+BR, columns ox0-1 .. ox0+BC.  Elements
+  // Input patch: rows oy0-1 .. oy0+BR, columns ox0-1 .. ox0+BC, one pixel
+  // (3 bf16, 6 bytes) per thread and step: an aligned 4-byte and a 2-byte
+  // load (which halves of the pixel they hold depends on its address
+  // modulo 4), written to LDS as one 8-byte slot (c0, c1, c2, 0).  Pixels
   // outside the image, or outside this tile's source region (only outputs
   // outside the tile's computed rectangle would read them), read 0.
   const int ylo = max(0, tl.cy0 - 1), yhi = min(a.in_h, tl.cy0 + tl.ch + 1);
   const int xlo = max(0, tl.cx0 - 1), xhi = min(a.in_w, tl.cx0 + tl.cw + 1);
+  const int64_t sb = bp.frame * a.src_fstride + tl.src_off;  // elements; the source buffer is 16-byte aligned
+  const int bpar = static_cast<int>(sb & 1);
   const __amdgpu_buffer_rsrc_t rs =
-      make_rsrc(src, static_cast<unsigned>((a.src_fstride - tl.src_off) * 2));
-  uint32_t ld[NLD];
+      make_rsrc(static_cast<const uint16_t*>(a.src) + sb, static_cast<unsigned>((a.src_fstride - tl.src_off) * 2));
+  const int p00 = (oy0 - 1 - tl.sy0) * tl.sw + (ox0 - 1 - tl.sx0);  // patch origin in the source region
+  constexpr int NPX = SR * SC;
+  constexpr int NPT = (NPX + 255) / 256;  // pixels per thread
+  uint32_t la[NPT], lb[NPT];
+  bool lodd[NPT];
 #pragma unroll
-  for (int k = 0; k < NLD; ++k) {
+  for (int k = 0; k < NPT; ++k) {
     const int e = tid + 256 * k;
-    const int r = e / (SC * 4), rem = e - r * (SC * 4);
-    const int px = rem >> 2, c = rem & 3;
+    const int r = e / SC, px = e - r * SC;
     const int iy = oy0 - 1 + r, ix = ox0 - 1 + px;
-    const bool ok = e < NEL && c < 3 && iy >= ylo && iy < yhi && ix >= xlo && ix < xhi;
-    const unsigned off = static_cast<unsigned>((((iy - tl.sy0) * tl.sw + (ix - tl.sx0)) * 3 + c) * 2);
-    ld[k] = __builtin_amdgcn_raw_buffer_load_b16(rs, static_cast<int>(ok ? off : 0x80000000u), 0, 0);
+    const bool ok = e < NPX && static_cast<unsigned>(iy - ylo) < static_cast<unsigned>(yhi - ylo) &&
+                    static_cast<unsigned>(ix - xlo) < static_cast<unsigned>(xhi - xlo);
+    const int p = p00 + r * tl.sw + px;
+    const bool odd = ((bpar + p) & 1) != 0;  // c0 at an address = 2 (mod 4): the dword holds c1, c2
+    const unsigned off = static_cast<unsigned>(p * 6);
+    const unsigned oa = odd ? off + 2u : off, ob = odd ? off : off + 4u;
+    la[k] = __builtin_amdgcn_raw_buffer_load_b32(rs, static_cast<int>(ok ? oa : 0x80000000u), 0, 0);
+    lb[k] = __builtin_amdgcn_raw_buffer_load_b16(rs, static_cast<int>(ok ? ob : 0x80000000u), 0, 0);
+    lodd[k] = odd;
   }
 #pragma unroll
-  for (int k = 0; k < NLD; ++k) {
+  for (int k = 0; k < NPT; ++k) {
     const int e = tid + 256 * k;
-    const int r = e / (SC * 4), rem = e - r * (SC * 4);
-    if (e < NEL) sx[r * RS + rem] = static_cast<uint16_t>(ld[k]);
+    const int r = e / SC, px = e - r * SC;
+    const uint32_t b = lb[k] & 0xffffu;
+    const u32x2 v = lodd[k] ? u32x2{b | (la[k] << 16), la[k] >> 16} : u32x2{la[k], b};
+    if (e < NPX) *reinterpret_cast<u32x2*>(sx + r * RS + px * 4) = v;
   }
   MAFAT_TRACE(6);
   __syncthreads();

@@ -16,6 +16,7 @@
 #ifdef MAFAT_TUNING
 extern "C" int mafat_debug_trace(long long* host_out);
 extern "C" int mafat_debug_ring_trace(long long* host_out);
+extern "C" int mafat_debug_patch_trace(long long* host_out);
 #endif
 
 namespace mafat {
@@ -349,10 +350,11 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
       if (e != hipSuccess)
         return fail(MAFAT_EHIP, std::string("stage launch failed: ") + hipGetErrorString(e));
 #ifdef MAFAT_TUNING
-      if (std::getenv("MAFAT_TRACE_DUMP") && kind == K_CONV_RING) {
+      if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH)) {
         long long tr[3][64];
         hipStreamSynchronize(stream);
-        mafat_debug_ring_trace(&tr[0][0]);
+        if (kind == K_CONV_RING) mafat_debug_ring_trace(&tr[0][0]);
+        else mafat_debug_patch_trace(&tr[0][0]);
         std::fprintf(stderr, "RTRACE stage %d-%d %dx%d kg%d ns%d grid %d\n", S.first, S.last, shape.bm, shape.bn,
                      shape.kg, shape.depth, A.total_blocks);
         for (int w = 0; w < 3; ++w) {
