@@ -50,6 +50,7 @@ namespace mafat {
 // Tuning builds only: phase timestamps (wall clock, 100 MHz) of three
 // workgroups (the first, the middle and the last of the grid).
 __device__ long long g_patch_trace[3][64];
+MAFAT_WG_TRACE_DECL(g_wg_patch)
 #define MAFAT_PTRACE(slot_)                                                                      \
   do {                                                                                           \
     if (threadIdx.x == 0 && (slot_) < 64 &&                                                      \
@@ -101,7 +102,8 @@ __device__ __forceinline__ void block_pixel(int r, int* py, int* px) {
 }
 
 template <int BR, int BC, int BM, int BN, int WGM, int WGN, int NS, bool POOL>
-__global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageArgs a) {
+__global__ __launch_bounds__(64 * WGM * WGN) __attribute__((amdgpu_waves_per_eu(NS == 1 ? 6 : 1)))
+void conv_patch_kernel(const StageArgs a) {
   constexpr int NWAVE = WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN, MT = WM / 16, NT = WN / 16;
   constexpr int PR = BR + 2, PC = BC + 2;
@@ -120,6 +122,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
   __shared__ __align__(1024) unsigned char smem[NS * SLOT + (SINK ? 1024 : 0)];
 
   MAFAT_PTRACE(0);
+  MAFAT_WG_MARK(g_wg_patch, 0);
   KTile tl;
   const BlockPos bp = decode_block(a, &tl);
   MAFAT_PTRACE(1 + (tl.ch < -1 ? 1 : 0));
@@ -355,6 +358,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void conv_patch_kernel(const StageA
     }
   }
   MAFAT_PTRACE(5);
+  MAFAT_WG_MARK(g_wg_patch, 1);
 }
 
 template <bool POOL>
@@ -385,6 +389,9 @@ hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs&
 }
 
 #ifdef MAFAT_TUNING
+extern "C" int mafat_debug_wg_patch(long long* host_out) {
+  return hipMemcpyFromSymbol(host_out, HIP_SYMBOL(g_wg_patch), sizeof(g_wg_patch)) == hipSuccess ? 0 : -1;
+}
 extern "C" int mafat_debug_patch_trace(long long* host_out) {
   return hipMemcpyFromSymbol(host_out, HIP_SYMBOL(g_patch_trace), sizeof(g_patch_trace)) == hipSuccess ? 0 : -1;
 }

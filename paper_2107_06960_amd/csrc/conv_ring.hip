@@ -53,6 +53,7 @@ namespace mafat {
 // Tuning builds only: phase timestamps (wall clock, 100 MHz) of three
 // workgroups (the first, the middle and the last of the grid).
 __device__ long long g_ring_trace[3][64];
+MAFAT_WG_TRACE_DECL(g_wg_ring)
 #define MAFAT_RTRACE(slot_)                                                                      \
   do {                                                                                           \
     if (threadIdx.x == 0 && (slot_) < 64 &&                                                      \
@@ -114,6 +115,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void conv_ring_kernel(const St
   __shared__ __align__(1024) unsigned char smem[NS * SLOT];
 
   MAFAT_RTRACE(0);
+  MAFAT_WG_MARK(g_wg_ring, 0);
   KTile tl;
   const BlockPos bp = decode_block(a, &tl);
   MAFAT_RTRACE(1 + (tl.ch < -1 ? 1 : 0));
@@ -360,6 +362,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void conv_ring_kernel(const St
     }
   }
   MAFAT_RTRACE(5);
+  MAFAT_WG_MARK(g_wg_ring, 1);
 }
 
 template <int F, bool POOL>
@@ -381,6 +384,9 @@ hipError_t launch_ring_fp(const MfmaShape& sh, const StageArgs& args, hipStream_
 }  // namespace
 
 #ifdef MAFAT_TUNING
+extern "C" int mafat_debug_wg_ring(long long* host_out) {
+  return hipMemcpyFromSymbol(host_out, HIP_SYMBOL(g_wg_ring), sizeof(g_wg_ring)) == hipSuccess ? 0 : -1;
+}
 extern "C" int mafat_debug_ring_trace(long long* host_out) {
   return hipMemcpyFromSymbol(host_out, HIP_SYMBOL(g_ring_trace), sizeof(g_ring_trace)) == hipSuccess ? 0 : -1;
 }

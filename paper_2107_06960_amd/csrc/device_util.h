@@ -8,6 +8,19 @@
 
 #include "kernel_args.h"
 
+#ifdef MAFAT_TUNING
+// Tuning builds only: start (k = 0) and end (k = 1) wall-clock stamps of
+// every workgroup (the first 8192) of the last launch of a kernel family.
+#define MAFAT_WG_TRACE_DECL(name_) __device__ long long name_[2][8192];
+#define MAFAT_WG_MARK(name_, k_)                                            \
+  do {                                                                      \
+    if (threadIdx.x == 0 && blockIdx.x < 8192) name_[(k_)][blockIdx.x] = wall_clock64(); \
+  } while (0)
+#else
+#define MAFAT_WG_TRACE_DECL(name_)
+#define MAFAT_WG_MARK(name_, k_) do {} while (0)
+#endif
+
 namespace mafat {
 namespace {
 

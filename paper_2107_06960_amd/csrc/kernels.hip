@@ -31,6 +31,7 @@ namespace mafat {
 #ifdef MAFAT_TUNING
 // Tuning builds only: phase timestamps of a few workgroups.
 __device__ long long g_trace[4][64];
+MAFAT_WG_TRACE_DECL(g_wg_rgb)
 #define MAFAT_TRACE(slot_)                                                                     \
   do {                                                                                         \
     if (threadIdx.x == 0 && (blockIdx.x == 0 || blockIdx.x == gridDim.x - 1 ||                 \
@@ -619,6 +620,7 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
   __shared__ __align__(16) float ssb[2 * COUT];  // scale, bias
   __shared__ __align__(16) uint16_t spool[POOL ? 4 * 4 * (BC / 8) * COUT : 8];  // per-wave pooled row staging
 
+  MAFAT_WG_MARK(g_wg_rgb, 0);
   MAFAT_TRACE(0);
   KTile tl;
   const BlockPos bp = decode_block(a, &tl);
@@ -787,6 +789,7 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
       }
     }
   }
+  MAFAT_WG_MARK(g_wg_rgb, 1);
   MAFAT_TRACE(3);
 }
 
@@ -884,6 +887,9 @@ hipError_t launch_dt(int kind, int f, bool pool, MfmaShape sh, const StageArgs& 
 }  // namespace
 
 #ifdef MAFAT_TUNING
+extern "C" int mafat_debug_wg_rgb(long long* host_out) {
+  return hipMemcpyFromSymbol(host_out, HIP_SYMBOL(g_wg_rgb), sizeof(g_wg_rgb)) == hipSuccess ? 0 : -1;
+}
 extern "C" int mafat_debug_trace(long long* host_out) {
   return hipMemcpyFromSymbol(host_out, HIP_SYMBOL(g_trace), sizeof(g_trace)) == hipSuccess ? 0 : -1;
 }

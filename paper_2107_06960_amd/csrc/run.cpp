@@ -9,6 +9,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <vector>
 
 #include "kernel_args.h"
 #include "mafat_internal.h"
@@ -16,6 +17,9 @@
 #ifdef MAFAT_TUNING
 extern "C" int mafat_debug_trace(long long* host_out);
 extern "C" int mafat_debug_ring_trace(long long* host_out);
+extern "C" int mafat_debug_wg_rgb(long long* host_out);
+extern "C" int mafat_debug_wg_patch(long long* host_out);
+extern "C" int mafat_debug_wg_ring(long long* host_out);
 extern "C" int mafat_debug_patch_trace(long long* host_out);
 #endif
 
@@ -135,7 +139,10 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
       const int64_t blocks = mb * ((S.cout + r.bn - 1) / r.bn);
       const double rounds = std::ceil(static_cast<double>(blocks) * batch / 256.0);
       const double t = rounds * (3e-6 + chunks * static_cast<double>(r.bm) * r.bn * 0.18e-9);
-      if (t < best * 0.98) {
+      // Within 2 % of the best, fewer blocks win (less halo and weight
+      // traffic; e.g. 12x16 over 12x12 blocks, whose GEMM rows are padded
+      // from 144 to 192).
+      if (t < best * 0.98 || (t < best * 1.02 && blocks < c.blocks)) {
         best = t;
         c.br = r.br; c.bc = r.bc; c.bm = r.bm; c.bn = r.bn; c.wgm = r.wgm; c.wgn = r.wgn; c.depth = r.ns;
         c.blocks = blocks;
@@ -350,6 +357,26 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
       if (e != hipSuccess)
         return fail(MAFAT_EHIP, std::string("stage launch failed: ") + hipGetErrorString(e));
 #ifdef MAFAT_TUNING
+      if (std::getenv("MAFAT_WG_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH || kind == K_CONV_RGB_MFMA)) {
+        static long long wt[2][8192];
+        hipStreamSynchronize(stream);
+        if (kind == K_CONV_RING) mafat_debug_wg_ring(&wt[0][0]);
+        else if (kind == K_CONV_PATCH) mafat_debug_wg_patch(&wt[0][0]);
+        else mafat_debug_wg_rgb(&wt[0][0]);
+        const int n = std::min(A.total_blocks, 8192);
+        std::vector<long long> d(n);
+        long long s0 = wt[0][0], s1 = wt[0][0], e0 = wt[1][0], e1 = wt[1][0];
+        for (int b = 0; b < n; ++b) {
+          s0 = std::min(s0, wt[0][b]); s1 = std::max(s1, wt[0][b]);
+          e0 = std::min(e0, wt[1][b]); e1 = std::max(e1, wt[1][b]);
+          d[b] = wt[1][b] - wt[0][b];
+        }
+        std::sort(d.begin(), d.end());
+        std::fprintf(stderr, "WGSPAN stage %d-%d kind %d grid %d: span %lld ns, starts %lld, first end %lld, "
+                     "dur p10 %lld p50 %lld p90 %lld max %lld ns\n", S.first, S.last, kind, A.total_blocks,
+                     (e1 - s0) * 10, (s1 - s0) * 10, (e0 - s0) * 10, d[n / 10] * 10, d[n / 2] * 10,
+                     d[(9 * n) / 10] * 10, d.back() * 10);
+      }
       if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH)) {
         long long tr[3][64];
         hipStreamSynchronize(stream);
