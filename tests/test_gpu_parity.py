@@ -60,6 +60,17 @@ def test_yolo_odd_image_batch(orc):
     _check_full(orc, W.YOLOV2_16, 71, 93, 3, "3x2/8/2x2", 2, "bf16", seed=5)
 
 
+@pytest.mark.parametrize("h,w,pool", [(96, 96, False), (96, 100, False), (96, 96, True), (96, 100, True)])
+def test_patch_block_shapes(orc, h, w, pool):
+    # one 3x3 conv, 64 -> 256 channels (bf16), on one tile: the runtime
+    # takes 192-row patch blocks here, 12x16 for 96x96 and 16x12 for
+    # 96x100 (fewer blocks), with and without the fused pool
+    layers = [dict(op=W.CONV, c_out=256, f=3, s=1, p=1, act=W.LEAKY)]
+    if pool:
+        layers.append(dict(op=W.MAXPOOL, f=2, s=2, p=0))
+    _check_full(orc, layers, h, w, 64, "1x1/NoCut", 1, "bf16", seed=21)
+
+
 def test_many_tiles_chunked_launch(orc):
     # 9x8 = 72 tiles > one launch's 64-tile argument block
     _check_full(orc, W.TINY, 64, 64, 3, "9x8", 1, "f32", seed=9)
