@@ -102,7 +102,7 @@ __device__ __forceinline__ void block_pixel(int r, int* py, int* px) {
 }
 
 template <int BR, int BC, int BM, int BN, int WGM, int WGN, int NS, bool POOL>
-__global__ __launch_bounds__(64 * WGM * WGN) __attribute__((amdgpu_waves_per_eu(NS == 1 ? 6 : 1)))
+__global__ __launch_bounds__(64 * WGM * WGN)
 void conv_patch_kernel(const StageArgs a) {
   constexpr int NWAVE = WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN, MT = WM / 16, NT = WN / 16;
