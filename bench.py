@@ -268,6 +268,56 @@ def config_search(args):
     print(json.dumps({"config_search": rows}), flush=True)
 
 
+def all_configs(args):
+    """Every workload of the build (the paper's configurations and the six
+    cut x grid runs): per-step latency (median, p10, p90 of HIP events on the
+    launch stream around each mafat_run_network call, 10 warm-up steps
+    first), frames/s at the median, executed TFLOP/s and its fraction of the
+    dtype's matrix-core peak, and peak device memory against the untiled
+    execution of the same layers.  One JSON line per workload."""
+    import numpy as np
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    from paper_2107_06960_amd import workloads as W
+    torch.cuda.set_device(0)
+    ev = HipEvents()
+    stream = torch.cuda.current_stream()
+    for name, wl in W.WORKLOADS.items():
+        params = W.workload_inputs(wl)
+        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling)
+        net = M.Network(plan, params, wl.batch, wl.dtype)
+        x = net.input_tensor(params["x"])
+        for _ in range(10):
+            net.run(x)
+        torch.cuda.synchronize()
+        n = args.steps
+        hs = ev.create(2 * n)
+        for r in range(n):
+            ev.record(hs[2 * r], stream)
+            net.run(x, stream=stream)
+            ev.record(hs[2 * r + 1], stream)
+        torch.cuda.synchronize()
+        ms = np.array([ev.ms(hs[2 * r], hs[2 * r + 1]) for r in range(n)])
+        ev.destroy(hs)
+        p10, p50, p90 = (float(np.percentile(ms, q)) for q in (10, 50, 90))
+        ex = sum(2 * plan.macs(g)[0] for g in range(plan.n_groups)) * wl.batch
+        us = sum(2 * plan.macs(g)[1] for g in range(plan.n_groups)) * wl.batch
+        del net, x
+        tp, _ = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch, wl.dtype,
+                                    params["x"])
+        up, ums = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), untiled_groups(wl.layers), params,
+                                      wl.batch, wl.dtype, params["x"])
+        print(json.dumps({
+            "workload": name, "input": f"{wl.h}x{wl.w}x{wl.c}", "batch": wl.batch, "dtype": wl.dtype,
+            "tiling": wl.tiling, "steps": n, "ms_p50": round(p50, 5), "ms_p10": round(p10, 5),
+            "ms_p90": round(p90, 5), "frames_per_s": round(wl.batch / (p50 * 1e-3), 1),
+            "gflop_executed": round(ex / 1e9, 3), "gflop_useful": round(us / 1e9, 3),
+            "tflops_executed": round(ex / (p50 * 1e-3) / 1e12, 2),
+            "frac_peak": round(ex / (p50 * 1e-3) / 1e12 / PEAK_TFLOPS[wl.dtype], 4),
+            "peak_mem_mib": round(tp / 2 ** 20, 2), "untiled_peak_mem_mib": round(up / 2 ** 20, 2),
+            "untiled_ms": round(ums, 5)}), flush=True)
+
+
 def copy_calibration(mib, reps=5):
     """A plain device copy of a known size, for scaling the HBM byte counters."""
     import torch
@@ -290,6 +340,8 @@ def main():
     ap.add_argument("--graph", action="store_true", help="replay one step from a captured HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-untiled", action="store_true")
+    ap.add_argument("--all-configs", action="store_true",
+                    help="latency quantiles, throughput and peak memory of every workload (one JSON line each)")
     ap.add_argument("--config-search", action="store_true",
                     help="only evaluate the configuration search against a measured sweep and exit")
     ap.add_argument("--copy-calibration", type=int, metavar="MIB",
@@ -300,6 +352,9 @@ def main():
         return
     if args.config_search:
         config_search(args)
+        return
+    if args.all_configs:
+        all_configs(args)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "only the one-GPU path is built: --gpus must be 1 (frames, and the "
@@ -347,6 +402,29 @@ def main():
     ms_step = el / args.steps * 1e3
     fps = wl.batch * args.steps / el
 
+    # The same step replayed from a captured HIP graph (reported beside the
+    # plain loop, which is the headline value).
+    graph_ms = None
+    if graph is None:
+        gs_ = torch.cuda.Stream()
+        gs_.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(gs_):
+            for _ in range(3):
+                net.run(x, stream=gs_)
+        torch.cuda.current_stream().wait_stream(gs_)
+        g_ = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g_):
+            net.run(x, stream=torch.cuda.current_stream())
+        for _ in range(args.warmup):
+            g_.replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            g_.replay()
+        torch.cuda.synchronize()
+        graph_ms = (time.perf_counter() - t0) / args.steps * 1e3
+        del g_
+
     # Per-stage and per-group durations: the same steps again, one run_group
     # call per group, with start/stop events recorded on the launch stream by
     # the kernel dispatches themselves (hipExtLaunchKernel: nothing is
@@ -373,9 +451,12 @@ def main():
         for g in range(ng):
             net.run_group(g, io[g][0], io[g][1], stream=stream, events=sev[r][g])
     torch.cuda.synchronize()
+    step_ev_ms = [0.0] * nsteps_ev
     for r in range(nsteps_ev):
         for g in range(ng):
-            group_ms[g] += ev.ms(gev[r][g][0], gev[r][g][1]) / nsteps_ev
+            gm = ev.ms(gev[r][g][0], gev[r][g][1])
+            group_ms[g] += gm / nsteps_ev
+            step_ev_ms[r] += gm
             hs = sev[r][g]
             for s_ in range(len(stages[g])):
                 stage_ms[g][s_] += ev.ms(hs[2 * s_], hs[2 * s_ + 1]) / nsteps_ev
@@ -432,6 +513,9 @@ def main():
         "frac_mfma_peak_executed": round(exec_flops / (ms_step * 1e-3) / 1e12 / peak, 4),
         "gflop_executed_per_step": round(exec_flops / 1e9, 3),
         "gflop_useful_per_step": round(useful_flops / 1e9, 3),
+        "graph_ms_per_step": round(graph_ms, 5) if graph_ms is not None else None,
+        "step_ms_events": {q: round(float(np.percentile(step_ev_ms, v)), 5)
+                           for q, v in (("p10", 10), ("p50", 50), ("p90", 90))},
         "group_ms": [round(v, 5) for v in group_ms],
         "group_frac_mfma_peak": [round(sum(flops[g]) * wl.batch / (group_ms[g] * 1e-3) / 1e12 / peak, 4)
                                  for g in range(ng)],

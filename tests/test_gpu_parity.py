@@ -154,3 +154,36 @@ def test_run_stage_sequence_equals_run_group(dtype):
     for a, b in zip(net.cuts, refc):
         assert torch.equal(a, b)
 
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_graph_replay_equals_eager(dtype):
+    # The network captured in a HIP graph (torch.cuda.CUDAGraph) and replayed
+    # three times, with eager runs of another input and synchronisations in
+    # between: every replay equals the eager result bit for bit.
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    p = W.make_inputs(W.YOLOV2_16, 96, 96, 3, 1, 4, dtype)
+    q = W.make_inputs(W.YOLOV2_16, 96, 96, 3, 1, 5, dtype)
+    plan = M.Plan(W.YOLOV2_16, (96, 96, 3), "3x3/8/2x2")
+    net = M.Network(plan, p, 1, dtype)
+    x = net.input_tensor(p["x"])
+    x_other = net.input_tensor(q["x"])
+    eager = net.run(x).clone()
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        net.run(x, stream=s)
+    torch.cuda.current_stream().wait_stream(s)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        net.run(x, stream=torch.cuda.current_stream())
+    for k in range(3):
+        other = net.run(x_other).clone()        # eager work between replays
+        torch.cuda.synchronize()
+        assert not torch.equal(other, eager)
+        net.y.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(net.y, eager), k
