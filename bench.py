@@ -114,13 +114,13 @@ def untiled_groups(layers):
     return starts, [1] * len(starts), [1] * len(starts)
 
 
-def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs=2):
+def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs=2, reuse=False):
     import torch
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     torch.cuda.reset_peak_memory_stats()
     base = torch.cuda.memory_allocated()
-    plan = M.Plan(layers, hwc, tiling)
+    plan = M.Plan(layers, hwc, tiling, reuse=reuse)
     net = M.Network(plan, params, batch, dtype)
     x = net.input_tensor(x_np)
     for _ in range(runs):
@@ -282,9 +282,9 @@ def all_configs(args):
     torch.cuda.set_device(0)
     ev = HipEvents()
     stream = torch.cuda.current_stream()
-    for name, wl in W.WORKLOADS.items():
+    for name, wl, reuse in [(n, w, r) for n, w in W.WORKLOADS.items() for r in (False, True)]:
         params = W.workload_inputs(wl)
-        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling)
+        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=reuse)
         net = M.Network(plan, params, wl.batch, wl.dtype)
         x = net.input_tensor(params["x"])
         for _ in range(10):
@@ -304,12 +304,12 @@ def all_configs(args):
         us = sum(2 * plan.macs(g)[1] for g in range(plan.n_groups)) * wl.batch
         del net, x
         tp, _ = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch, wl.dtype,
-                                    params["x"])
+                                    params["x"], reuse=reuse)
         up, ums = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), untiled_groups(wl.layers), params,
                                       wl.batch, wl.dtype, params["x"])
         print(json.dumps({
             "workload": name, "input": f"{wl.h}x{wl.w}x{wl.c}", "batch": wl.batch, "dtype": wl.dtype,
-            "tiling": wl.tiling, "steps": n, "ms_p50": round(p50, 5), "ms_p10": round(p10, 5),
+            "tiling": wl.tiling, "tile_reuse": reuse, "steps": n, "ms_p50": round(p50, 5), "ms_p10": round(p10, 5),
             "ms_p90": round(p90, 5), "frames_per_s": round(wl.batch / (p50 * 1e-3), 1),
             "gflop_executed": round(ex / 1e9, 3), "gflop_useful": round(us / 1e9, 3),
             "tflops_executed": round(ex / (p50 * 1e-3) / 1e12, 2),
@@ -401,6 +401,21 @@ def main():
     el = time.perf_counter() - t0
     ms_step = el / args.steps * 1e3
     fps = wl.batch * args.steps / el
+
+    # The same workload with tile reuse (each tile computes only its part of
+    # every stage output; no halo recompute), timed the same way.
+    rplan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=True)
+    rnet = M.Network(rplan, params, wl.batch, wl.dtype)
+    rx = rnet.input_tensor(params["x"])
+    for _ in range(args.warmup):
+        rnet.run(rx)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        rnet.run(rx)
+    torch.cuda.synchronize()
+    reuse_ms = (time.perf_counter() - t0) / args.steps * 1e3
+    del rnet, rx, rplan
 
     # The same step replayed from a captured HIP graph (reported beside the
     # plain loop, which is the headline value).
@@ -514,6 +529,7 @@ def main():
         "gflop_executed_per_step": round(exec_flops / 1e9, 3),
         "gflop_useful_per_step": round(useful_flops / 1e9, 3),
         "graph_ms_per_step": round(graph_ms, 5) if graph_ms is not None else None,
+        "tile_reuse_ms_per_step": round(reuse_ms, 5),
         "step_ms_events": {q: round(float(np.percentile(step_ev_ms, v)), 5)
                            for q, v in (("p10", 10), ("p50", 50), ("p90", 90))},
         "group_ms": [round(v, 5) for v in group_ms],

@@ -106,6 +106,30 @@ int mafat_plan_create(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
                       int32_t n_groups, const int32_t* grid_rows,
                       const int32_t* grid_cols, mafat_plan** out);
 
+/* Plan flags (mafat_plan_create_flags). */
+enum {
+  /* Tile reuse: the data reuse between adjacent tiles that DeepThings adds
+   * to fused tile partitioning (section 3; NEXT step of the method), taken
+   * to whole stages.  The runtime runs a group's stages one after another
+   * over all tiles, so each stage's output is partitioned into the group's
+   * grid (floor boundaries, as the group output) and every tile computes
+   * only its own part, into a full tensor of the stage output in the
+   * workspace; the next stage reads the halo from the neighbouring tiles'
+   * parts instead of recomputing it.  Results equal the untiled network's
+   * (up to accumulation order); executed MACs equal the untiled ones;
+   * the workspace holds two full stage outputs per frame instead of every
+   * tile's intermediates.  mafat_plan_regions and the paper's memory model
+   * keep describing the plain partition. */
+  MAFAT_PLAN_TILE_REUSE = 1
+};
+
+/* mafat_plan_create with flags (0 or MAFAT_PLAN_TILE_REUSE).  Errors: those
+ * of mafat_plan_create, and EINVAL for unknown flags. */
+int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
+                            int32_t in_w, int32_t in_c, const int32_t* group_start,
+                            int32_t n_groups, const int32_t* grid_rows,
+                            const int32_t* grid_cols, int32_t flags, mafat_plan** out);
+
 /* Frees a plan (NULL is ignored). */
 void mafat_plan_destroy(mafat_plan* plan);
 

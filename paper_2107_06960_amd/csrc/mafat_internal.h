@@ -53,8 +53,10 @@ struct Group {
   int rows, cols, ntiles;
   std::vector<mafat_rect> in_r, out_r;  // [tile * nlayers + (l - l0)]
   std::vector<Stage> stages;
-  int64_t scratch_elems;  // per tile per scratch buffer
+  int64_t scratch_elems;  // per tile per scratch buffer (tile reuse: per scratch buffer)
   int nbufs;              // scratch buffers (0, 1 or 2)
+  int64_t scratch_frame;  // scratch elements of one frame
+  bool reuse;             // tile reuse: every stage output computed once (full tensors)
   int64_t macs_exec, macs_untiled;
 };
 

@@ -47,8 +47,9 @@ void back_project(int a, int b, int F, int S, int P, int E, int* ia, int* ib) {
   *ib = std::min(E, (b - 1) * S - P + F);
 }
 
-int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, Group* out) {
+int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool reuse, Group* out) {
   Group G;
+  G.reuse = reuse;
   G.l0 = g0; G.l1 = g1; G.rows = rows; G.cols = cols; G.ntiles = rows * cols;
   const int nl = g1 - g0 + 1;
   const auto& dl = plan.dims[g1];
@@ -118,6 +119,53 @@ int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, Group* out
   const int ns = static_cast<int>(G.stages.size());
   G.nbufs = std::min(2, ns - 1);
   G.scratch_elems = 0;
+  if (reuse) {
+    // Tile reuse (the data reuse between adjacent tiles of DeepThings'
+    // fused tile partitioning, taken to the whole stage): the stages run one
+    // after another over all tiles, so every stage's output is partitioned
+    // into the group's grid (the same floor boundaries as the group output)
+    // and each tile computes only its own part, into a full tensor of the
+    // stage output; the next stage reads its halo from the neighbours'
+    // parts.  Nothing is computed twice.  A conv stage with a fused pool
+    // computes the conv outputs of its pool windows (twice the partition).
+    for (int s = 0; s < ns; ++s) {
+      Stage& S = G.stages[s];
+      S.src_buf = (s == 0) ? BUF_GROUP_IO : ((s - 1) % 2);
+      S.dst_buf = (s == ns - 1) ? BUF_GROUP_IO : (s % 2);
+      if (S.dst_buf != BUF_GROUP_IO)
+        G.scratch_elems = std::max<int64_t>(G.scratch_elems, static_cast<int64_t>(S.out_h) * S.out_w * S.cout);
+      for (int i = 0; i < rows; ++i)
+        for (int j = 0; j < cols; ++j) {
+          int y0, y1, x0, x1;
+          split(S.out_h, rows, i, &y0, &y1);
+          split(S.out_w, cols, j, &x0, &x1);
+          TileGeom T{};
+          const int k = S.pool ? 2 : 1;
+          T.cy0 = k * y0; T.ch = k * (y1 - y0);
+          T.cx0 = k * x0; T.cw = k * (x1 - x0);
+          T.sy0 = 0; T.sx0 = 0; T.sw = S.in_w;
+          T.src_off = (S.src_buf == BUF_GROUP_IO) ? 0 : S.src_buf;  // scaled below
+          T.dy0 = 0; T.dx0 = 0; T.dw = S.out_w;
+          T.dst_off = (S.dst_buf == BUF_GROUP_IO) ? 0 : S.dst_buf;  // scaled below
+          S.tiles.push_back(T);
+        }
+    }
+    // Scratch of one frame: [buffer][full stage output], 256-byte aligned.
+    G.scratch_elems = (G.scratch_elems + 127) / 128 * 128;
+    G.scratch_frame = static_cast<int64_t>(G.nbufs) * G.scratch_elems;
+    for (Stage& S : G.stages)
+      for (TileGeom& T : S.tiles) {
+        if (S.src_buf != BUF_GROUP_IO) T.src_off *= G.scratch_elems;
+        if (S.dst_buf != BUF_GROUP_IO) T.dst_off *= G.scratch_elems;
+      }
+    G.macs_exec = 0;  // the conv outputs computed (all of them, less the rows/columns an odd pool drops)
+    for (const Stage& S : G.stages)
+      if (S.kind == STAGE_CONV)
+        for (const TileGeom& T : S.tiles)
+          G.macs_exec += static_cast<int64_t>(T.ch) * T.cw * S.cout * S.f * S.f * S.cin;
+    *out = std::move(G);
+    return MAFAT_OK;
+  }
   for (int s = 0; s < ns; ++s) {
     Stage& S = G.stages[s];
     S.src_buf = (s == 0) ? BUF_GROUP_IO : ((s - 1) % 2);
@@ -152,6 +200,7 @@ int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, Group* out
   // Scratch buffers of one frame: [buffer][tile][scratch_elems]; every
   // tile's buffer starts on a 256-byte boundary for both dtypes.
   G.scratch_elems = (G.scratch_elems + 127) / 128 * 128;
+  G.scratch_frame = static_cast<int64_t>(G.nbufs) * G.ntiles * G.scratch_elems;
   for (Stage& S : G.stages)
     for (TileGeom& T : S.tiles) {
       if (S.src_buf != BUF_GROUP_IO) T.src_off *= G.scratch_elems;
@@ -170,9 +219,21 @@ extern "C" int mafat_plan_create(const mafat_layer* layers, int32_t n_layers, in
                                  int32_t in_w, int32_t in_c, const int32_t* group_start,
                                  int32_t n_groups, const int32_t* grid_rows,
                                  const int32_t* grid_cols, mafat_plan** out) {
+  return mafat_plan_create_flags(layers, n_layers, in_h, in_w, in_c, group_start, n_groups, grid_rows, grid_cols,
+                                 0, out);
+}
+
+extern "C" int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
+                                       int32_t in_w, int32_t in_c, const int32_t* group_start,
+                                       int32_t n_groups, const int32_t* grid_rows,
+                                       const int32_t* grid_cols, int32_t flags, mafat_plan** out) {
   clear_error();
   if (!out) { set_error("out is NULL"); return MAFAT_EINVAL; }
   *out = nullptr;
+  if (flags & ~MAFAT_PLAN_TILE_REUSE) {
+    set_error("unknown plan flags");
+    return MAFAT_EINVAL;
+  }
   if (!layers || !group_start || !grid_rows || !grid_cols || n_layers < 1 || n_groups < 1) {
     set_error("null pointer or empty layer/group list");
     return MAFAT_EINVAL;
@@ -220,7 +281,8 @@ extern "C" int mafat_plan_create(const mafat_layer* layers, int32_t n_layers, in
         return MAFAT_ESHAPE;
       }
       Group G;
-      const int rc = build_group(*plan, g0, end - 1, grid_rows[g], grid_cols[g], &G);
+      const int rc = build_group(*plan, g0, end - 1, grid_rows[g], grid_cols[g],
+                                 (flags & MAFAT_PLAN_TILE_REUSE) != 0, &G);
       if (rc != MAFAT_OK) { delete plan; return rc; }
       plan->groups.push_back(std::move(G));
     }

@@ -227,7 +227,7 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
 WorkspaceLayout workspace_layout(const Group& G, int batch, int dtype) {
   const size_t esz = (dtype == MAFAT_F32) ? 4 : 2;
   WorkspaceLayout L{};
-  L.scratch = (static_cast<size_t>(batch) * G.nbufs * G.ntiles * G.scratch_elems * esz + 255) & ~static_cast<size_t>(255);
+  L.scratch = (static_cast<size_t>(batch) * G.scratch_frame * esz + 255) & ~static_cast<size_t>(255);
   L.total = L.scratch;
   return L;
 }
@@ -255,7 +255,7 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
   const auto& dout = plan->dims[G.l1];
   const int64_t in_frame = static_cast<int64_t>(din[0]) * din[1] * din[2];
   const int64_t out_frame = static_cast<int64_t>(dout[3]) * dout[4] * dout[5];
-  const int64_t scr_frame = static_cast<int64_t>(G.nbufs) * G.ntiles * G.scratch_elems;
+  const int64_t scr_frame = G.scratch_frame;
   if (in_frame >= (1ll << 31) || out_frame >= (1ll << 31) || scr_frame >= (1ll << 31))
     return fail(MAFAT_EUNSUPPORTED, "a frame's tensor exceeds 2^31 elements");
   {

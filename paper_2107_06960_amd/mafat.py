@@ -27,11 +27,12 @@ MAFAT_CONV, MAFAT_MAXPOOL = 0, 1
 MAFAT_ACT_LINEAR, MAFAT_ACT_LEAKY01 = 0, 1
 MAFAT_F32, MAFAT_BF16 = 0, 1
 MAFAT_MEM_DEVICE, MAFAT_MEM_PAPER = 0, 1
+MAFAT_PLAN_TILE_REUSE = 1
 MEM_MODELS = {"device": MAFAT_MEM_DEVICE, "paper": MAFAT_MEM_PAPER}
 DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
 
 # Every symbol include/mafat.h declares.
-EXPORTS = ("mafat_plan_create", "mafat_plan_destroy", "mafat_plan_layer_shape", "mafat_plan_group",
+EXPORTS = ("mafat_plan_create", "mafat_plan_create_flags", "mafat_plan_destroy", "mafat_plan_layer_shape", "mafat_plan_group",
            "mafat_plan_regions", "mafat_plan_macs", "mafat_plan_stages", "mafat_plan_stage_layers",
            "mafat_workspace_size", "mafat_run_group", "mafat_run_stage", "mafat_run_network",
            "mafat_predict_mem", "mafat_get_config", "mafat_status_string", "mafat_last_error")
@@ -71,6 +72,8 @@ def lib():
         planp = ctypes.c_void_p
         L.mafat_plan_create.argtypes = [ctypes.POINTER(mafat_layer), i32, i32, i32, i32, i32p, i32,
                                         i32p, i32p, ctypes.POINTER(planp)]
+        L.mafat_plan_create_flags.argtypes = [ctypes.POINTER(mafat_layer), i32, i32, i32, i32, i32p, i32,
+                                              i32p, i32p, i32, ctypes.POINTER(planp)]
         L.mafat_plan_destroy.argtypes = [planp]
         L.mafat_plan_destroy.restype = None
         L.mafat_plan_layer_shape.argtypes = [planp, i32, i32p]
@@ -114,8 +117,9 @@ def _ptrs(vals):
 
 # ------------------------------------------------------------------ C names
 
-def mafat_plan_create(layers, in_h, in_w, in_c, group_start, grid_rows, grid_cols):
-    """Returns a plan handle (int); raises MafatError with the library's status."""
+def mafat_plan_create(layers, in_h, in_w, in_c, group_start, grid_rows, grid_cols, flags=0):
+    """Returns a plan handle (int); raises MafatError with the library's status.
+    flags: 0 or MAFAT_PLAN_TILE_REUSE (mafat_plan_create_flags)."""
     n = len(layers)
     arr = (mafat_layer * n)()
     for k, L in enumerate(layers):
@@ -126,8 +130,13 @@ def mafat_plan_create(layers, in_h, in_w, in_c, group_start, grid_rows, grid_col
     rr = (ctypes.c_int32 * len(grid_rows))(*grid_rows)
     cc = (ctypes.c_int32 * len(grid_cols))(*grid_cols)
     h = ctypes.c_void_p()
-    _check("mafat_plan_create",
-           lib().mafat_plan_create(arr, n, in_h, in_w, in_c, gs, len(group_start), rr, cc, ctypes.byref(h)))
+    if flags:
+        _check("mafat_plan_create_flags",
+               lib().mafat_plan_create_flags(arr, n, in_h, in_w, in_c, gs, len(group_start), rr, cc, flags,
+                                             ctypes.byref(h)))
+    else:
+        _check("mafat_plan_create",
+               lib().mafat_plan_create(arr, n, in_h, in_w, in_c, gs, len(group_start), rr, cc, ctypes.byref(h)))
     return h.value
 
 
@@ -250,13 +259,14 @@ class Plan:
     """A plan for a layer stack, an input shape and a tiling spec such as
     ``"5x5/8/2x2"`` (section 5.1 notation) or explicit group lists."""
 
-    def __init__(self, layers, in_hwc, tiling="1x1/NoCut"):
+    def __init__(self, layers, in_hwc, tiling="1x1/NoCut", reuse=False):
         self.layers = list(layers)
+        self.reuse = bool(reuse)
         self.h, self.w, self.c = in_hwc
         self.group_start, self.rows, self.cols = W.parse_tiling(tiling, len(layers)) \
             if isinstance(tiling, str) else tiling
         self.handle = mafat_plan_create(self.layers, self.h, self.w, self.c, self.group_start,
-                                        self.rows, self.cols)
+                                        self.rows, self.cols, MAFAT_PLAN_TILE_REUSE if self.reuse else 0)
         self.n_groups = len(self.group_start)
 
     def __del__(self):

@@ -119,6 +119,38 @@ def test_workspace_size(lib):
     assert one.workspace_size(3, "f32") == 0
 
 
+def test_tile_reuse_plan(lib):
+    # tile reuse: executed MACs equal the untiled ones (even extents) and
+    # never exceed them (odd extents: the rows/columns a pool drops are not
+    # computed); the workspace is two full stage outputs per frame
+    for tiling in ("5x5/8/2x2", "3x3/NoCut", "4x4/12/1x1"):
+        plan = M.Plan(W.YOLOV2_16, (608, 608, 3), tiling, reuse=True)
+        plain = M.Plan(W.YOLOV2_16, (608, 608, 3), tiling)
+        for g in range(plan.n_groups):
+            ex, un = plan.macs(g)
+            assert ex == un == plain.macs(g)[1]
+        assert plan.stages(0) == plain.stages(0)
+        # largest stage output that is not a group output, over all groups
+        big = 0
+        for g in range(plan.n_groups):
+            for (a, b) in plan.stages(g)[:-1]:
+                d = plan.shape(b)
+                big = max(big, d[3] * d[4] * d[5])
+        big = (big + 127) // 128 * 128
+        nst = max(len(plan.stages(g)) for g in range(plan.n_groups))
+        assert plan.workspace_size(3, "bf16") == (3 * 2 * big * 2 + 255) // 256 * 256 or nst < 3
+    odd = M.Plan(W.YOLOV2_16, (71, 93, 3), "3x2/8/2x2", reuse=True)
+    for g in range(odd.n_groups):
+        ex, un = odd.macs(g)
+        assert 0 < ex <= un
+    # unknown flags
+    arr = (M.mafat_layer * 1)(M.mafat_layer(0, 8, 3, 1, 1, 1))
+    h = ctypes.c_void_p()
+    one = (ctypes.c_int32 * 1)(1)
+    rc = M.lib().mafat_plan_create_flags(arr, 1, 16, 16, 3, (ctypes.c_int32 * 1)(0), 1, one, one, 2, ctypes.byref(h))
+    assert rc == M.MAFAT_EINVAL and not h.value
+
+
 def _create_rc(layers, h, w, c, gs, rows, cols):
     n = len(layers)
     arr = (M.mafat_layer * max(1, n))()

@@ -21,10 +21,10 @@ def _gpu():
     require_gpu()
 
 
-def _check_full(orc, layers, h, w, c, tiling, batch, dtype, seed=0):
-    print(f"[parity] {h}x{w}x{c} {tiling} batch={batch} {dtype} seed={seed}", flush=True)
+def _check_full(orc, layers, h, w, c, tiling, batch, dtype, seed=0, reuse=False):
+    print(f"[parity] {h}x{w}x{c} {tiling} batch={batch} {dtype} seed={seed} reuse={reuse}", flush=True)
     p = W.make_inputs(layers, h, w, c, batch, seed, dtype)
-    out, cuts, net, _ = run_gpu(layers, h, w, c, p, tiling, batch, dtype)
+    out, cuts, net, _ = run_gpu(layers, h, w, c, p, tiling, batch, dtype, reuse=reuse)
     ref = orc.forward_layers(layers, h, w, c, p["x"], p)
     err = normwise_err(out, ref)
     assert err <= TOL[dtype], (tiling, dtype, err)
@@ -187,3 +187,27 @@ def test_graph_replay_equals_eager(dtype):
         g.replay()
         torch.cuda.synchronize()
         assert torch.equal(net.y, eager), k
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("tiling", ["3x3/NoCut", "5x5/8/2x2", "2x3/4/3x2"])
+def test_tile_reuse(orc, dtype, tiling):
+    # tile reuse: each tile computes only its part of every stage output,
+    # reading the halo from its neighbours' parts
+    _check_full(orc, W.YOLOV2_16, 80, 80, 3, tiling, 1, dtype, seed=3, reuse=True)
+
+
+def test_tile_reuse_odd_batch(orc):
+    # odd extents (pools drop a row/column), batch 2, ragged partitions
+    _check_full(orc, W.YOLOV2_16, 71, 93, 3, "3x2/8/2x2", 2, "bf16", seed=5, reuse=True)
+    _check_full(orc, W.TINY, 64, 64, 3, "9x8", 1, "f32", seed=9, reuse=True)
+
+
+def test_tile_reuse_equals_plain_partition_f32():
+    # f32: the same sums in the same order per output element, so tile
+    # reuse and the plain partition agree to rounding of the accumulation
+    # order only (the kernels' block shapes may differ)
+    p = W.make_inputs(W.YOLOV2_16, 96, 96, 3, 1, 7, "f32")
+    a = run_gpu(W.YOLOV2_16, 96, 96, 3, p, "4x4/8/2x2", 1, "f32", want_cuts=False)
+    b = run_gpu(W.YOLOV2_16, 96, 96, 3, p, "4x4/8/2x2", 1, "f32", want_cuts=False, reuse=True)
+    assert normwise_err(b, a) <= TOL["f32"]
