@@ -211,3 +211,19 @@ def test_tile_reuse_equals_plain_partition_f32():
     a = run_gpu(W.YOLOV2_16, 96, 96, 3, p, "4x4/8/2x2", 1, "f32", want_cuts=False)
     b = run_gpu(W.YOLOV2_16, 96, 96, 3, p, "4x4/8/2x2", 1, "f32", want_cuts=False, reuse=True)
     assert normwise_err(b, a) <= TOL["f32"]
+
+
+# A VGG-style stack (3x3 convolutions in pairs and triples between pools,
+# linear last layer): another CNN than YOLOv2 for the generalisations the
+# method names as future work (more groups, non-square grids, other nets).
+VGG_LIKE = [W.conv(64), W.conv(64), W.maxpool(), W.conv(128), W.conv(128), W.maxpool(),
+            W.conv(256), W.conv(256), W.conv(256, act=W.LINEAR)]
+
+
+@pytest.mark.parametrize("reuse", [False, True])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_more_groups_and_other_networks(orc, dtype, reuse):
+    # four groups on YOLOv2 (cuts after every pool but the first)
+    _check_full(orc, W.YOLOV2_16, 80, 80, 3, "4x4/4/3x3/8/2x2/12/1x1", 1, dtype, seed=31, reuse=reuse)
+    # three groups with non-square grids on the VGG-style stack
+    _check_full(orc, VGG_LIKE, 64, 64, 3, "3x2/3/2x3/6/1x2", 1, dtype, seed=32, reuse=reuse)
