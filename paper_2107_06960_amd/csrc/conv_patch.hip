@@ -311,50 +311,66 @@ void conv_patch_kernel(const StageArgs a) {
 
   MAFAT_PTRACE(4);
   // Epilogue: folded batch-norm, activation (leaky: max(v, 0.1 v)), the
-  // fused pool, round to bf16, store the pixels inside the tile's computed
-  // rectangle.
+  // fused pool, round to bf16; the block's outputs are staged in LDS (the
+  // ring is free by now) as rows of BN channels per output pixel and leave
+  // as 16-byte stores, each pixel's BN channels one contiguous run (whole
+  // cache lines instead of 8- or 2-byte pieces from every lane).  Only the
+  // pixels inside the tile's computed rectangle are stored.
+  constexpr int NTHR = 64 * NWAVE;
+  constexpr int RSB = BN * 2 + 16;                       // LDS bytes per staged pixel row
+  constexpr int NPXO = POOL ? (BR / 2) * (BC / 2) : BR * BC;  // output pixels of the block
+  constexpr int CPB = BN / 8;                             // 16-byte chunks per pixel row
+  static_assert(NPXO * RSB <= NS * SLOT, "staged block fits in the ring");
   const float slope = act_slope(a.act);
-  const int vy = tl.cy0 + tl.ch - by0, vx = tl.cx0 + tl.cw - bx0;  // valid extent of this block
+  __syncthreads();  // every wave is done reading the ring
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
-    int oy, ox;
-    bool ok;
-    if (POOL) {
-      const int r = wm * WM + i * 16 + 4 * (lane >> 4);  // first row of this lane's window
-      int py, px;
-      block_pixel<BC, true>(r < BR * BC ? r : 0, &py, &px);
-      ok = r < BR * BC && py < vy && px < vx;
-      oy = (by0 + py) >> 1;
-      ox = (bx0 + px) >> 1;
-    } else {
-      const int r = wm * WM + i * 16 + (lane & 15);
-      int py, px;
-      block_pixel<BC, false>(r < BR * BC ? r : 0, &py, &px);
-      ok = r < BR * BC && py < vy && px < vx;
-      oy = by0 + py;
-      ox = bx0 + px;
-    }
-    uint16_t* drow = dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * cout;
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
       if (POOL) {
-        const int co = n0 + wn * WN + j * 16 + (lane & 15);
+        const int r = wm * WM + i * 16 + 4 * (lane >> 4);  // first GEMM row of this lane's window
         float v[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = fmaf(acc[j][i][r], sc[j][0], bi[j][0]);
+        for (int k = 0; k < 4; ++k) v[k] = fmaf(acc[j][i][k], sc[j][0], bi[j][0]);
         float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
         mx = fmaxf(mx, slope * mx);
-        if (ok && co < cout) store1(drow + co, mx);
+        if (r < BR * BC)
+          store1(reinterpret_cast<uint16_t*>(smem + (r >> 2) * RSB) + wn * WN + j * 16 + (lane & 15), mx);
       } else {
-        const int co = n0 + wn * WN + j * 16 + 4 * (lane >> 4);
+        const int r = wm * WM + i * 16 + (lane & 15);
         float v[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          v[r] = fmaf(acc[j][i][r], sc[j][r], bi[j][r]);
-          v[r] = fmaxf(v[r], slope * v[r]);
+        for (int k = 0; k < 4; ++k) {
+          v[k] = fmaf(acc[j][i][k], sc[j][k], bi[j][k]);
+          v[k] = fmaxf(v[k], slope * v[k]);
         }
-        if (ok && co < cout) store4<MAFAT_BF16>(drow + co, v);
+        if (r < BR * BC)
+          store4<MAFAT_BF16>(reinterpret_cast<uint16_t*>(smem + r * RSB) + wn * WN + j * 16 + 4 * (lane >> 4), v);
       }
+    }
+  }
+  __syncthreads();
+  const int vy = tl.cy0 + tl.ch - by0, vx = tl.cx0 + tl.cw - bx0;  // valid extent of this block
+  for (int e = tid; e < NPXO * CPB; e += NTHR) {
+    const int p = e / CPB, k = e - p * CPB;
+    int oy, ox;
+    bool ok;
+    if (POOL) {
+      constexpr int WC = BC / 2;
+      const int wy = p / WC, wx = p - wy * WC;
+      ok = 2 * wy < vy && 2 * wx < vx;
+      oy = (by0 + 2 * wy) >> 1;
+      ox = (bx0 + 2 * wx) >> 1;
+    } else {
+      const int py = p / BC, px = p - py * BC;
+      ok = py < vy && px < vx;
+      oy = by0 + py;
+      ox = bx0 + px;
+    }
+    const int c0 = n0 + k * 8;
+    if (ok && c0 < cout) {
+      const u32x4 v = *reinterpret_cast<const u32x4*>(smem + p * RSB + k * 16);
+      *reinterpret_cast<u32x4*>(dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * cout + c0) = v;
     }
   }
   MAFAT_PTRACE(5);
