@@ -320,45 +320,58 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void conv_ring_kernel(const St
   }
 
   // Epilogue: folded batch-norm, activation (leaky: max(v, 0.1 v)), the
-  // fused pool, round to bf16, store the tile's own output rectangle.
+  // fused pool, round to bf16; the block's outputs are staged in LDS as rows
+  // of BN channels per output pixel and leave as 16-byte stores (each
+  // pixel's BN channels one contiguous run); only the tile's own output
+  // rectangle is stored.
+  constexpr int NTHR = 64 * NWAVE;
+  constexpr int RSB = BN * 2 + 16;          // LDS bytes per staged pixel row
+  constexpr int NPXO = POOL ? BM / 4 : BM;  // output pixels of the block
+  constexpr int CPB = BN / 8;               // 16-byte chunks per pixel row
+  static_assert(NPXO * RSB <= NS * SLOT, "staged block fits in the ring");
   const float slope = act_slope(a.act);
+  __syncthreads();  // every wave is done with the ring (and the K-group exchange)
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
-    int oy, ox;
-    bool ok;
-    if (POOL) {
-      const int m = m0 + wm * WM + i * 16 + 4 * (lane >> 4);  // first row of this lane's window
-      const int pw = tl.cw >> 1, qq = m >> 2, qy = qq / pw;
-      oy = (tl.cy0 >> 1) + qy;
-      ox = (tl.cx0 >> 1) + (qq - qy * pw);
-      ok = m < M_;
-    } else {
-      const int m = m0 + wm * WM + i * 16 + (lane & 15);
-      row_pixel<false>(tl, m < M_ ? m : 0, &oy, &ox);
-      ok = m < M_;
-    }
-    uint16_t* drow = dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * cout;
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
       if (KG == 2 && (j < grp * (NT / 2) || j >= (grp + 1) * (NT / 2))) continue;
       if (POOL) {
-        const int co = n0 + wn * WN + j * 16 + (lane & 15);
+        const int rl = wm * WM + i * 16 + 4 * (lane >> 4);  // first block row of this lane's window
         float v[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) v[r] = fmaf(acc[j][i][r], sc[j][0], bi[j][0]);
         float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
         mx = fmaxf(mx, slope * mx);
-        if (ok && co < cout) store1(drow + co, mx);
+        store1(reinterpret_cast<uint16_t*>(smem + (rl >> 2) * RSB) + wn * WN + j * 16 + (lane & 15), mx);
       } else {
-        const int co = n0 + wn * WN + j * 16 + 4 * (lane >> 4);
+        const int rl = wm * WM + i * 16 + (lane & 15);
         float v[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           v[r] = fmaf(acc[j][i][r], sc[j][r], bi[j][r]);
           v[r] = fmaxf(v[r], slope * v[r]);
         }
-        if (ok && co < cout) store4<MAFAT_BF16>(drow + co, v);
+        store4<MAFAT_BF16>(reinterpret_cast<uint16_t*>(smem + rl * RSB) + wn * WN + j * 16 + 4 * (lane >> 4), v);
       }
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < NPXO * CPB; e += NTHR) {
+    const int p = e / CPB, k = e - p * CPB;
+    const int m = m0 + (POOL ? 4 * p : p);
+    const int c0 = n0 + k * 8;
+    if (m < M_ && c0 < cout) {
+      int oy, ox;
+      if (POOL) {
+        const int pw = tl.cw >> 1, qq = m >> 2, qy = qq / pw;
+        oy = (tl.cy0 >> 1) + qy;
+        ox = (tl.cx0 >> 1) + (qq - qy * pw);
+      } else {
+        row_pixel<false>(tl, m, &oy, &ox);
+      }
+      const u32x4 v = *reinterpret_cast<const u32x4*>(smem + p * RSB + k * 16);
+      *reinterpret_cast<u32x4*>(dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * cout + c0) = v;
     }
   }
   MAFAT_RTRACE(5);
