@@ -123,24 +123,57 @@ void conv_patch_kernel(const StageArgs a) {
 
   MAFAT_PTRACE(0);
   MAFAT_WG_MARK(g_wg_patch, 0);
-  KTile tl;
-  const BlockPos bp = decode_block(a, &tl);
-  MAFAT_PTRACE(1 + (tl.ch < -1 ? 1 : 0));
   const int tid = static_cast<int>(threadIdx.x), lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lrow = lane >> 2, lpos = lane & 3;
+  const int cin = a.cin, cout = a.cout;
+  const int K = 9 * cin;
+  const __amdgpu_buffer_rsrc_t rsb = make_rsrc(a.w, static_cast<unsigned>(cout * K * 2));
+  // Weight loads: instruction g of a chunk's weight part fills weight rows
+  // [16 g, 16 g + 16) of the slot (row = tap * BN + n); g past NB fills the
+  // sink.  Chunk c adds 64 c bytes.
+  unsigned b_off[NBW];
+  auto issue_b = [&](int c, int slot) {
+    unsigned char* sl = smem + slot * SLOT;
+    const unsigned coff = static_cast<unsigned>(c * 64);
+#pragma unroll
+    for (int k = 0; k < NBW; ++k) {
+      const int g = k * NWAVE + wave;
+      unsigned char* d = (g < NB) ? sl + A_BYTES + g * 1024 : smem + NS * SLOT;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, (lds_ptr_t)d, 16,
+                                               static_cast<int>(b_off[k] + coff), 0, 0, 0);
+    }
+  };
+  // The weight rows depend only on the channel block: their first chunk is
+  // issued while the tile table is still on its way.
+  auto early = [&](int nb) {
+    const int n0e = nb * BN;
+#pragma unroll
+    for (int k = 0; k < NBW; ++k) {
+      const int g = k * NWAVE + wave;
+      const int row = 16 * g + lrow;           // weight row within the slot
+      const int t = row / BN, n = row - t * BN;
+      const int co = n0e + n;
+      const int chunk = lpos ^ ((row >> 1) & 3);
+      b_off[k] = (g < NB && co < cout) ? static_cast<unsigned>((co * K + t * cin) * 2 + chunk * 16)
+                                       : 0x80000000u;
+    }
+    issue_b(0, 0);
+  };
+  KTile tl;
+  const BlockPos bp = decode_block(a, &tl, early);
+  MAFAT_PTRACE(1 + (tl.ch < -1 ? 1 : 0));
   const int wm = wave / WGN, wn = wave - wm * WGN;
   const int nbx = (tl.cw + BC - 1) / BC;
   const int bby = bp.mb / nbx, bbx = bp.mb - bby * nbx;
   const int by0 = tl.cy0 + bby * BR, bx0 = tl.cx0 + bbx * BC;  // block origin (conv outputs)
   const int n0 = bp.nb * BN;
-  const int cin = a.cin, cout = a.cout, sw = tl.sw;
+  const int sw = tl.sw;
   const int64_t sbase = bp.frame * a.src_fstride + tl.src_off;
   uint16_t* dst = static_cast<uint16_t*>(a.dst) + bp.frame * a.dst_fstride + tl.dst_off;
-  const int K = 9 * cin;
   const int nstage = cin >> 5;
   const __amdgpu_buffer_rsrc_t rsa = make_rsrc(static_cast<const uint16_t*>(a.src) + sbase,
                                                static_cast<unsigned>((a.src_fstride - tl.src_off) * 2));
-  const __amdgpu_buffer_rsrc_t rsb = make_rsrc(a.w, static_cast<unsigned>(cout * K * 2));
 
   // Scale and bias of this lane's output channels.
   float sc[NT][4], bi[NT][4];
@@ -161,15 +194,14 @@ void conv_patch_kernel(const StageArgs a) {
     }
   }
 
-  // This lane's loads (chunk 0; chunk c adds 64 c bytes).  Instruction g of
-  // a chunk: g < NA fills patch rows [16 g, 16 g + 16), else weight rows
-  // [16 (g - NA), +16) (row = tap * BN + n); g past NA + NB fills the sink.
-  const int lrow = lane >> 2, lpos = lane & 3;
+  // This lane's patch loads (chunk 0; chunk c adds 64 c bytes): instruction
+  // g of a chunk's patch part fills patch rows [16 g, 16 g + 16); g past NA
+  // fills the sink.
   // Source region of the tile: the conv outputs [cy0, cy0 + ch) read rows
   // [cy0 - 1, cy0 + ch] (columns likewise), clipped to the image.
   const int ry0 = max(tl.cy0 - 1, 0), ry1 = min(tl.cy0 + tl.ch + 1, a.in_h);
   const int rx0 = max(tl.cx0 - 1, 0), rx1 = min(tl.cx0 + tl.cw + 1, a.in_w);
-  unsigned a_off[NAW], b_off[NBW];
+  unsigned a_off[NAW];
 #pragma unroll
   for (int k = 0; k < NAW; ++k) {
     const int g = k * NWAVE + wave;
@@ -181,17 +213,7 @@ void conv_patch_kernel(const StageArgs a) {
     a_off[k] = ok ? static_cast<unsigned>((((iy - tl.sy0) * sw + (ix - tl.sx0)) * cin) * 2 + chunk * 16)
                   : 0x80000000u;
   }
-#pragma unroll
-  for (int k = 0; k < NBW; ++k) {
-    const int g = k * NWAVE + wave;
-    const int row = 16 * g + lrow;           // weight row within the slot
-    const int t = row / BN, n = row - t * BN;
-    const int co = n0 + n;
-    const int chunk = lpos ^ ((row >> 1) & 3);
-    b_off[k] = (g < NB && co < cout) ? static_cast<unsigned>((co * K + t * cin) * 2 + chunk * 16)
-                                     : 0x80000000u;
-  }
-  auto issue = [&](int c, int slot) {
+  auto issue_a = [&](int c, int slot) {
     unsigned char* sl = smem + slot * SLOT;
     const unsigned coff = static_cast<unsigned>(c * 64);
 #pragma unroll
@@ -201,13 +223,11 @@ void conv_patch_kernel(const StageArgs a) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, (lds_ptr_t)d, 16,
                                                static_cast<int>(a_off[k] + coff), 0, 0, 0);
     }
-#pragma unroll
-    for (int k = 0; k < NBW; ++k) {
-      const int g = k * NWAVE + wave;
-      unsigned char* d = (g < NB) ? sl + A_BYTES + g * 1024 : smem + NS * SLOT;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, (lds_ptr_t)d, 16,
-                                               static_cast<int>(b_off[k] + coff), 0, 0, 0);
-    }
+  };
+  // A chunk's loads (chunk 0's weight part was issued during the decode).
+  auto issue = [&](int c, int slot) {
+    issue_a(c, slot);
+    if (c > 0) issue_b(c, slot);
   };
 
   // Fragment reads.  A: lane l supplies GEMM row wm*WM + 16 i + (l & 15),

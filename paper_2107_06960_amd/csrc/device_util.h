@@ -79,7 +79,15 @@ struct BlockPos {
 // dynamic index into the argument block would be a chain of dependent
 // scalar loads).  The tile is then found with a ballot over the block
 // prefix and its fields are taken with readlane.
-__device__ __forceinline__ BlockPos decode_block(const StageArgs& a, KTile* tile) {
+//
+// `early(nb)` runs once the channel block is known (it needs only the scalar
+// header) and before the tile table is used: a kernel issues its first
+// weight loads there, so their latency overlaps the table's.
+struct NoEarly {
+  __device__ void operator()(int) const {}
+};
+template <typename Early = NoEarly>
+__device__ __forceinline__ BlockPos decode_block(const StageArgs& a, KTile* tile, Early early = Early{}) {
   static_assert(kMaxTilesPerLaunch == 64 && sizeof(KTile) == 28, "one tile per lane of a wave");
   const int lane = static_cast<int>(threadIdx.x) & 63;
   // (C-style cast: converts from the constant address space.)
@@ -104,6 +112,7 @@ __device__ __forceinline__ BlockPos decode_block(const StageArgs& a, KTile* tile
     mg = blk / a.nblk_n;
     p.nb = blk - mg * a.nblk_n;
   }
+  early(p.nb);
   // Tiles whose first block is at or before mg, not counting tile 0.
   const int t = __popcll(__builtin_amdgcn_ballot_w64(lane >= 1 && lane < a.ntiles && pre <= mg));
   p.tile = t;
