@@ -116,25 +116,85 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void conv_ring_kernel(const St
 
   MAFAT_RTRACE(0);
   MAFAT_WG_MARK(g_wg_ring, 0);
-  KTile tl;
-  const BlockPos bp = decode_block(a, &tl);
-  MAFAT_RTRACE(1 + (tl.ch < -1 ? 1 : 0));
   const int tid = static_cast<int>(threadIdx.x), lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int grp = wave / (WGM * WGN), wq = wave - grp * (WGM * WGN);
-  const int wm = wq / WGN, wn = wq - wm * WGN;
-  const int M = tl.ch * tl.cw;
-  const int m0 = bp.mb * BM, n0 = bp.nb * BN;
-  const int cin = a.cin, cout = a.cout, sw = tl.sw;
-  const int64_t sbase = bp.frame * a.src_fstride + tl.src_off;
-  uint16_t* dst = static_cast<uint16_t*>(a.dst) + bp.frame * a.dst_fstride + tl.dst_off;
+  const int cin = a.cin, cout = a.cout;
   const int K = F * F * cin;
   const int cblocks = cin >> 5;            // 32-channel sub-chunks per tap
   const int nsub = F * F * cblocks;
   const int nstage = (nsub + 1) >> 1;
+  const __amdgpu_buffer_rsrc_t rsb = make_rsrc(a.w, static_cast<unsigned>(cout * K * 2));
+  // This lane's loads: row (lane >> 3) of 8-row group (k * NWAVE + wave) of
+  // the A rows (k < APW) and of the B rows (k < BPW); global 16-byte chunk
+  // cg of the 128-byte stage row = piece pc of sub-chunk hh.
+  const int lrow = lane >> 3;
+  const int cg = (lane & 7) ^ lrow;
+  const int hh = cg >> 2, pc = cg & 3;
+
+  // Load cursor (wave-uniform) over the 64-byte sub-chunks of K: an outer
+  // and an inner index, inner fastest.  KORD 0: outer = filter tap, inner =
+  // channel block; KORD 1: outer = channel block, inner = tap, so the f*f
+  // taps of one channel block follow each other and their shifted re-reads
+  // of the same input pixels hit the L1 cache.  A padded last sub-chunk
+  // (past the end of K) reads zero A rows and re-reads valid weights.
+  constexpr int TAPS = F * F;
+  const int ilim = KORD ? TAPS : cblocks, olim = KORD ? cblocks : TAPS;
+  // Offsets of the stage whose first sub-chunk is at cursor (o0, i0), for
+  // this lane's half hh: the tap's mask bit (31: an invalid sub-chunk), the
+  // A offset (source row width swv) and the B offset; and the next cursor.
+  struct SubOff { unsigned tap, aoff, boff; int on, in; };
+  auto sub_offsets = [&](int o0, int i0, int swv) {
+    const int w0 = (ilim - 2 - i0) >> 31;  // -1: the next sub-chunk starts a new outer index
+    const int o1 = o0 - w0, i1 = (i0 + 1) & ~w0;
+    const int w1 = (ilim - 2 - i1) >> 31;
+    const bool v0 = o0 < olim, v1 = o1 < olim;
+    const int tap0 = v0 ? (KORD ? i0 : o0) : 0, cb0 = v0 ? (KORD ? o0 : i0) : 0;
+    const int tap1 = v1 ? (KORD ? i1 : o1) : 0, cb1 = v1 ? (KORD ? o1 : i1) : 0;
+    const int ky0 = tap0 / F, kx0 = tap0 - ky0 * F;
+    const int ky1 = tap1 / F, kx1 = tap1 - ky1 * F;
+    const int ao0 = (((ky0 - P) * swv + (kx0 - P)) * cin + cb0 * 32) * 2;
+    const int ao1 = (((ky1 - P) * swv + (kx1 - P)) * cin + cb1 * 32) * 2;
+    const int bo0 = (tap0 * cin + cb0 * 32) * 2;
+    const int bo1 = (tap1 * cin + cb1 * 32) * 2;
+    SubOff r;
+    r.tap = static_cast<unsigned>(hh ? (v1 ? tap1 : 31) : (v0 ? tap0 : 31));
+    r.aoff = static_cast<unsigned>(hh ? ao1 : ao0);
+    r.boff = static_cast<unsigned>(hh ? bo1 : bo0);
+    r.on = o1 - w1;
+    r.in = (i1 + 1) & ~w1;
+    return r;
+  };
+  unsigned b_off[BPW];
+  auto issue_b = [&](int slot, unsigned boff) {
+    unsigned char* sbase_l = smem + slot * SLOT;
+#pragma unroll
+    for (int k = 0; k < BPW; ++k)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rsb, (lds_ptr_t)(sbase_l + (BM + 8 * (k * NWAVE + wave)) * ROWB), 16,
+          static_cast<int>(b_off[k] + boff), 0, 0, 0);
+  };
+  // The weight rows depend only on the channel block: the first stage's are
+  // issued while the tile table is still on its way.
+  auto early = [&](int nb) {
+#pragma unroll
+    for (int k = 0; k < BPW; ++k) {
+      const int co = nb * BN + 8 * (k * NWAVE + wave) + lrow;
+      b_off[k] = co < cout ? static_cast<unsigned>((co * K + pc * 8) * 2) : 0x80000000u;
+    }
+    issue_b(0, sub_offsets(0, 0, 0).boff);
+  };
+  KTile tl;
+  const BlockPos bp = decode_block(a, &tl, early);
+  MAFAT_RTRACE(1 + (tl.ch < -1 ? 1 : 0));
+  const int grp = wave / (WGM * WGN), wq = wave - grp * (WGM * WGN);
+  const int wm = wq / WGN, wn = wq - wm * WGN;
+  const int M = tl.ch * tl.cw;
+  const int m0 = bp.mb * BM, n0 = bp.nb * BN;
+  const int sw = tl.sw;
+  const int64_t sbase = bp.frame * a.src_fstride + tl.src_off;
+  uint16_t* dst = static_cast<uint16_t*>(a.dst) + bp.frame * a.dst_fstride + tl.dst_off;
   const __amdgpu_buffer_rsrc_t rsa = make_rsrc(static_cast<const uint16_t*>(a.src) + sbase,
                                                static_cast<unsigned>((a.src_fstride - tl.src_off) * 2));
-  const __amdgpu_buffer_rsrc_t rsb = make_rsrc(a.w, static_cast<unsigned>(cout * K * 2));
 
   // Scale and bias of this lane's output channels (issued first, so their
   // latency overlaps the main loop).
@@ -156,13 +216,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void conv_ring_kernel(const St
     }
   }
 
-  // This lane's loads: row (lane >> 3) of 8-row group (k * NWAVE + wave) of
-  // the A rows (k < APW) and of the B rows (k < BPW); global 16-byte chunk
-  // cg of the 128-byte stage row = piece pc of sub-chunk hh.
-  const int lrow = lane >> 3;
-  const int cg = (lane & 7) ^ lrow;
-  const int hh = cg >> 2, pc = cg & 3;
-  unsigned a_off[APW], a_inv[APW], b_off[BPW];
+  unsigned a_off[APW], a_inv[APW];
 #pragma unroll
   for (int k = 0; k < APW; ++k) {
     const int m = m0 + 8 * (k * NWAVE + wave) + lrow;
@@ -179,55 +233,25 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void conv_ring_kernel(const St
     }
     a_inv[k] = (m < M) ? inv : ~0u;
   }
-#pragma unroll
-  for (int k = 0; k < BPW; ++k) {
-    const int co = n0 + 8 * (k * NWAVE + wave) + lrow;
-    b_off[k] = co < cout ? static_cast<unsigned>((co * K + pc * 8) * 2) : 0x80000000u;
-  }
 
-  // Load cursor (wave-uniform) over the 64-byte sub-chunks of K: an outer
-  // and an inner index, inner fastest.  KORD 0: outer = filter tap, inner =
-  // channel block; KORD 1: outer = channel block, inner = tap, so the f*f
-  // taps of one channel block follow each other and their shifted re-reads
-  // of the same input pixels hit the L1 cache.  A padded last sub-chunk
-  // (past the end of K) reads zero A rows and re-reads valid weights.
-  constexpr int TAPS = F * F;
-  const int ilim = KORD ? TAPS : cblocks, olim = KORD ? cblocks : TAPS;
+  // A stage's loads at the cursor (the first stage's weights were issued
+  // during the decode).
   int lc_o = 0, lc_i = 0;
-  auto issue = [&](int slot) {
+  auto issue = [&](int slot, bool skip_b) {
     const int o0 = __builtin_amdgcn_readfirstlane(lc_o);
     const int i0 = __builtin_amdgcn_readfirstlane(lc_i);
-    const int w0 = (ilim - 2 - i0) >> 31;  // -1: the next sub-chunk starts a new outer index
-    const int o1 = o0 - w0, i1 = (i0 + 1) & ~w0;
-    const int w1 = (ilim - 2 - i1) >> 31;
-    const bool v0 = o0 < olim, v1 = o1 < olim;
-    const int tap0 = v0 ? (KORD ? i0 : o0) : 0, cb0 = v0 ? (KORD ? o0 : i0) : 0;
-    const int tap1 = v1 ? (KORD ? i1 : o1) : 0, cb1 = v1 ? (KORD ? o1 : i1) : 0;
-    const int ky0 = tap0 / F, kx0 = tap0 - ky0 * F;
-    const int ky1 = tap1 / F, kx1 = tap1 - ky1 * F;
-    const int ao0 = (((ky0 - P) * sw + (kx0 - P)) * cin + cb0 * 32) * 2;
-    const int ao1 = (((ky1 - P) * sw + (kx1 - P)) * cin + cb1 * 32) * 2;
-    const int bo0 = (tap0 * cin + cb0 * 32) * 2;
-    const int bo1 = (tap1 * cin + cb1 * 32) * 2;
-    // mask bit of the tap (bit 31 is set in every row's mask: invalid sub-chunk)
-    const unsigned tap = static_cast<unsigned>(hh ? (v1 ? tap1 : 31) : (v0 ? tap0 : 31));
-    const unsigned aoff = static_cast<unsigned>(hh ? ao1 : ao0);
-    const unsigned boff = static_cast<unsigned>(hh ? bo1 : bo0);
+    const SubOff so = sub_offsets(o0, i0, sw);
     unsigned char* sbase_l = smem + slot * SLOT;
 #pragma unroll
     for (int k = 0; k < APW; ++k) {
-      const unsigned bad = (a_inv[k] >> tap) & 1u;
+      const unsigned bad = (a_inv[k] >> so.tap) & 1u;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
           rsa, (lds_ptr_t)(sbase_l + (8 * (k * NWAVE + wave)) * ROWB), 16,
-          static_cast<int>((a_off[k] + aoff) | (bad << 31)), 0, 0, 0);
+          static_cast<int>((a_off[k] + so.aoff) | (bad << 31)), 0, 0, 0);
     }
-#pragma unroll
-    for (int k = 0; k < BPW; ++k)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          rsb, (lds_ptr_t)(sbase_l + (BM + 8 * (k * NWAVE + wave)) * ROWB), 16,
-          static_cast<int>(b_off[k] + boff), 0, 0, 0);
-    lc_o = o1 - w1;
-    lc_i = (i1 + 1) & ~w1;
+    if (!skip_b) issue_b(slot, so.boff);
+    lc_o = so.on;
+    lc_i = so.in;
   };
 
   // Fragment reads: lane l supplies rows (l & 15) of a 16-row fragment at K
@@ -272,13 +296,13 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void conv_ring_kernel(const St
   // Prologue: stages 0 .. NS-2 in flight.
 #pragma unroll
   for (int p = 0; p < NS - 1; ++p)
-    if (p < nstage) issue(p);
+    if (p < nstage) issue(p, p == 0);
   int slot = 0;
   for (int s = 0; s < nstage; ++s) {
     wait_stage<LPS, NS - 2>(nstage - 1 - s);
     wg_barrier();
     MAFAT_RTRACE(8 + s);
-    if (s + NS - 1 < nstage) issue(slot == 0 ? NS - 1 : slot - 1);
+    if (s + NS - 1 < nstage) issue(slot == 0 ? NS - 1 : slot - 1, false);
     compute(slot);
     slot = (slot == NS - 1) ? 0 : slot + 1;
   }
