@@ -622,9 +622,18 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
 
   MAFAT_WG_MARK(g_wg_rgb, 0);
   MAFAT_TRACE(0);
+  const int tid = static_cast<int>(threadIdx.x), lane = tid & 63, wave = tid >> 6;
+  // Weights, scale, bias (the same for every block; 16 bytes per thread):
+  // fetched before the tile table is decoded, written to LDS after the
+  // input patch's loads are issued.
+  const u32x4* psrc = (tid < W16)              ? reinterpret_cast<const u32x4*>(a.w) + tid
+                      : (tid < W16 + COUT / 4) ? reinterpret_cast<const u32x4*>(a.scale) + (tid - W16)
+                      : (tid < W16 + COUT / 2) ? reinterpret_cast<const u32x4*>(a.bias) + (tid - W16 - COUT / 4)
+                                               : nullptr;
+  u32x4 pv = u32x4{0u, 0u, 0u, 0u};
+  if (psrc) pv = *psrc;
   KTile tl;
   const BlockPos bp = decode_block(a, &tl);
-  const int tid = static_cast<int>(threadIdx.x), lane = tid & 63, wave = tid >> 6;
   MAFAT_TRACE(4 + (tl.ch > 30000 ? 1 : 0));
   const int nbx = (tl.cw + BC - 1) / BC;
   const int by = bp.mb / nbx, bx = bp.mb - by * nbx;
@@ -632,16 +641,6 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
   uint16_t* dst = static_cast<uint16_t*>(a.dst) + bp.frame * a.dst_fstride + tl.dst_off;
   const int kq = lane >> 4;
 
-  // Weights, scale, bias -> LDS (16 bytes per thread).
-  if (tid < W16) {
-    reinterpret_cast<u32x4*>(swt)[tid] = reinterpret_cast<const u32x4*>(a.w)[tid];
-  } else if (tid < W16 + COUT / 4) {
-    const int i = tid - W16;
-    reinterpret_cast<f32x4*>(ssb)[i] = reinterpret_cast<const f32x4*>(a.scale)[i];
-  } else if (tid < W16 + COUT / 2) {
-    const int i = tid - W16 - COUT / 4;
-    reinterpret_cast<f32x4*>(ssb + COUT)[i] = reinterpret_cast<const f32x4*>(a.bias)[i];
-  }
   // Input patch: rows oy0-1 .. oy0+BR, columns ox0-1 .. ox0+BC, one pixel
   // (3 bf16, 6 bytes) per thread and step: an aligned 4-byte and a 2-byte
   // load (which halves of the pixel they hold depends on its address
@@ -674,6 +673,8 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
     lb[k] = __builtin_amdgcn_raw_buffer_load_b16(rs, static_cast<int>(ok ? ob : 0x80000000u), 0, 0);
     lodd[k] = odd;
   }
+  if (tid < W16) reinterpret_cast<u32x4*>(swt)[tid] = pv;
+  else if (tid < W16 + COUT / 2) reinterpret_cast<u32x4*>(ssb)[tid - W16] = pv;  // scale, then bias
 #pragma unroll
   for (int k = 0; k < NPT; ++k) {
     const int e = tid + 256 * k;
