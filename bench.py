@@ -340,6 +340,8 @@ def main():
     ap.add_argument("--graph", action="store_true", help="replay one step from a captured HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-untiled", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the tile-reuse and HIP-graph timings (for profiler runs: only the plain steps)")
     ap.add_argument("--all-configs", action="store_true",
                     help="latency quantiles, throughput and peak memory of every workload (one JSON line each)")
     ap.add_argument("--config-search", action="store_true",
@@ -402,25 +404,27 @@ def main():
     ms_step = el / args.steps * 1e3
     fps = wl.batch * args.steps / el
 
-    # The same workload with tile reuse (each tile computes only its part of
-    # every stage output; no halo recompute), timed the same way.
-    rplan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=True)
-    rnet = M.Network(rplan, params, wl.batch, wl.dtype)
-    rx = rnet.input_tensor(params["x"])
-    for _ in range(args.warmup):
-        rnet.run(rx)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        rnet.run(rx)
-    torch.cuda.synchronize()
-    reuse_ms = (time.perf_counter() - t0) / args.steps * 1e3
-    del rnet, rx, rplan
+    reuse_ms = None
+    if not args.no_extras:
+        # The same workload with tile reuse (each tile computes only its part of
+        # every stage output; no halo recompute), timed the same way.
+        rplan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=True)
+        rnet = M.Network(rplan, params, wl.batch, wl.dtype)
+        rx = rnet.input_tensor(params["x"])
+        for _ in range(args.warmup):
+            rnet.run(rx)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            rnet.run(rx)
+        torch.cuda.synchronize()
+        reuse_ms = (time.perf_counter() - t0) / args.steps * 1e3
+        del rnet, rx, rplan
 
     # The same step replayed from a captured HIP graph (reported beside the
     # plain loop, which is the headline value).
     graph_ms = None
-    if graph is None:
+    if graph is None and not args.no_extras:
         gs_ = torch.cuda.Stream()
         gs_.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(gs_):
@@ -529,7 +533,7 @@ def main():
         "gflop_executed_per_step": round(exec_flops / 1e9, 3),
         "gflop_useful_per_step": round(useful_flops / 1e9, 3),
         "graph_ms_per_step": round(graph_ms, 5) if graph_ms is not None else None,
-        "tile_reuse_ms_per_step": round(reuse_ms, 5),
+        "tile_reuse_ms_per_step": round(reuse_ms, 5) if reuse_ms is not None else None,
         "step_ms_events": {q: round(float(np.percentile(step_ev_ms, v)), 5)
                            for q, v in (("p10", 10), ("p50", 50), ("p90", 90))},
         "group_ms": [round(v, 5) for v in group_ms],
