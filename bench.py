@@ -114,15 +114,17 @@ def untiled_groups(layers):
     return starts, [1] * len(starts), [1] * len(starts)
 
 
-def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs=2, reuse=False):
+def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs=2, reuse=False, packed=False):
     import torch
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     torch.cuda.reset_peak_memory_stats()
     base = torch.cuda.memory_allocated()
-    plan = M.Plan(layers, hwc, tiling, reuse=reuse)
+    plan = M.Plan(layers, hwc, tiling, reuse=reuse, packed_weights=packed)
     net = M.Network(plan, params, batch, dtype)
     x = net.input_tensor(x_np)
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()   # after the weights are packed
     for _ in range(runs):
         net.run(x)
     torch.cuda.synchronize()
@@ -284,7 +286,7 @@ def all_configs(args):
     stream = torch.cuda.current_stream()
     for name, wl, reuse in [(n, w, r) for n, w in W.WORKLOADS.items() for r in (False, True)]:
         params = W.workload_inputs(wl)
-        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=reuse)
+        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=reuse, packed_weights=True)
         net = M.Network(plan, params, wl.batch, wl.dtype)
         x = net.input_tensor(params["x"])
         for _ in range(10):
@@ -304,12 +306,13 @@ def all_configs(args):
         us = sum(2 * plan.macs(g)[1] for g in range(plan.n_groups)) * wl.batch
         del net, x
         tp, _ = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch, wl.dtype,
-                                    params["x"], reuse=reuse)
+                                    params["x"], reuse=reuse, packed=True)
         up, ums = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), untiled_groups(wl.layers), params,
                                       wl.batch, wl.dtype, params["x"])
         print(json.dumps({
             "workload": name, "input": f"{wl.h}x{wl.w}x{wl.c}", "batch": wl.batch, "dtype": wl.dtype,
-            "tiling": wl.tiling, "tile_reuse": reuse, "steps": n, "ms_p50": round(p50, 5), "ms_p10": round(p10, 5),
+            "tiling": wl.tiling, "tile_reuse": reuse, "weights": "packed" if wl.dtype == "bf16" else "KRSC",
+            "steps": n, "ms_p50": round(p50, 5), "ms_p10": round(p10, 5),
             "ms_p90": round(p90, 5), "frames_per_s": round(wl.batch / (p50 * 1e-3), 1),
             "gflop_executed": round(ex / 1e9, 3), "gflop_useful": round(us / 1e9, 3),
             "tflops_executed": round(ex / (p50 * 1e-3) / 1e12, 2),
@@ -374,7 +377,10 @@ def main():
     torch.cuda.set_device(0)
     wl = W.WORKLOADS[args.workload]
     params = W.workload_inputs(wl)
-    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling)
+    # The library's fast path: weights packed once for the patch kernels
+    # (MAFAT_PLAN_PACKED_WEIGHTS, mafat_pack_weights at load, outside the
+    # timed steps); the same steps with KRSC weights are reported beside.
+    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, packed_weights=True)
     net = M.Network(plan, params, wl.batch, wl.dtype)
     x = net.input_tensor(params["x"])
     stream = torch.cuda.current_stream()
@@ -404,22 +410,25 @@ def main():
     ms_step = el / args.steps * 1e3
     fps = wl.batch * args.steps / el
 
-    reuse_ms = None
-    if not args.no_extras:
-        # The same workload with tile reuse (each tile computes only its part of
-        # every stage output; no halo recompute), timed the same way.
-        rplan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=True)
-        rnet = M.Network(rplan, params, wl.batch, wl.dtype)
-        rx = rnet.input_tensor(params["x"])
+    def time_variant(**kw):
+        vplan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, **kw)
+        vnet = M.Network(vplan, params, wl.batch, wl.dtype)
+        vx = vnet.input_tensor(params["x"])
         for _ in range(args.warmup):
-            rnet.run(rx)
+            vnet.run(vx)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(args.steps):
-            rnet.run(rx)
+            vnet.run(vx)
         torch.cuda.synchronize()
-        reuse_ms = (time.perf_counter() - t0) / args.steps * 1e3
-        del rnet, rx, rplan
+        return (time.perf_counter() - t0) / args.steps * 1e3
+
+    reuse_ms = krsc_ms = None
+    if not args.no_extras:
+        # The same workload with tile reuse (each tile computes only its part
+        # of every stage output; no halo recompute), and with KRSC weights.
+        reuse_ms = time_variant(reuse=True, packed_weights=True)
+        krsc_ms = time_variant()
 
     # The same step replayed from a captured HIP graph (reported beside the
     # plain loop, which is the headline value).
@@ -526,7 +535,7 @@ def main():
         "data": "synthetic (seeded U[0,1) input, He-normal weights, folded-BN scale/bias)",
         "config": {"workload": wl.name, "network": "YOLOv2 layers 0-15" if len(wl.layers) == 16 else wl.note,
                    "input": f"{wl.h}x{wl.w}x{wl.c}", "batch": wl.batch, "tiling": wl.tiling,
-                   "accumulate": "f32", "graph": bool(args.graph)},
+                   "accumulate": "f32", "graph": bool(args.graph), "weights": "packed for the patch kernels"},
         "tflops_executed": round(exec_flops / (ms_step * 1e-3) / 1e12, 2),
         "tflops_useful": round(useful_flops / (ms_step * 1e-3) / 1e12, 2),
         "frac_mfma_peak_executed": round(exec_flops / (ms_step * 1e-3) / 1e12 / peak, 4),
@@ -534,6 +543,7 @@ def main():
         "gflop_useful_per_step": round(useful_flops / 1e9, 3),
         "graph_ms_per_step": round(graph_ms, 5) if graph_ms is not None else None,
         "tile_reuse_ms_per_step": round(reuse_ms, 5) if reuse_ms is not None else None,
+        "krsc_weights_ms_per_step": round(krsc_ms, 5) if krsc_ms is not None else None,
         "step_ms_events": {q: round(float(np.percentile(step_ev_ms, v)), 5)
                            for q, v in (("p10", 10), ("p50", 50), ("p90", 90))},
         "group_ms": [round(v, 5) for v in group_ms],
@@ -546,10 +556,10 @@ def main():
     if not args.no_untiled:
         del net, x
         tp, tms = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch,
-                                      wl.dtype, params["x"])
+                                      wl.dtype, params["x"], packed=True)
         ug = untiled_groups(wl.layers)
         up, ums = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), ug, params, wl.batch,
-                                      wl.dtype, params["x"])
+                                      wl.dtype, params["x"], packed=True)
         res["peak_mem_mib"] = round(tp / 2 ** 20, 2)
         res["untiled_peak_mem_mib"] = round(up / 2 ** 20, 2)
         res["untiled_ms_per_step"] = round(ums, 5)

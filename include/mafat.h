@@ -120,15 +120,40 @@ enum {
    * the workspace holds two full stage outputs per frame instead of every
    * tile's intermediates.  mafat_plan_regions and the paper's memory model
    * keep describing the plain partition. */
-  MAFAT_PLAN_TILE_REUSE = 1
+  MAFAT_PLAN_TILE_REUSE = 1,
+  /* Packed weights: for every conv layer whose mafat_packed_weights_size is
+   * nonzero (bf16 3x3 layers run by the patch kernel), the w[layer] passed
+   * to the run functions is that layer's weights repacked by
+   * mafat_pack_weights: per block of output channels and 32-channel chunk,
+   * the nine taps' rows one contiguous run, so the kernel's weight loads
+   * read whole cache lines.  The other layers keep KRSC.  Every batch runs
+   * the stage configurations chosen for one frame (the packing follows
+   * their output-channel blocks). */
+  MAFAT_PLAN_PACKED_WEIGHTS = 2
 };
 
-/* mafat_plan_create with flags (0 or MAFAT_PLAN_TILE_REUSE).  Errors: those
- * of mafat_plan_create, and EINVAL for unknown flags. */
+/* mafat_plan_create with flags (MAFAT_PLAN_TILE_REUSE and/or
+ * MAFAT_PLAN_PACKED_WEIGHTS, or 0).  Errors: those of mafat_plan_create, and
+ * EINVAL for unknown flags. */
 int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
                             int32_t in_w, int32_t in_c, const int32_t* group_start,
                             int32_t n_groups, const int32_t* grid_rows,
                             const int32_t* grid_cols, int32_t flags, mafat_plan** out);
+
+/* Bytes of the packed weights of conv layer `layer` in `dtype` (device
+ * buffer, 16-byte aligned, caller-owned); 0 when the layer's weights are
+ * passed as KRSC (plan without MAFAT_PLAN_PACKED_WEIGHTS, f32, 1x1 or
+ * first-layer convolutions, pools).  Errors: EINVAL, EUNSUPPORTED (dtype). */
+int mafat_packed_weights_size(const mafat_plan* plan, int32_t layer, int32_t dtype, size_t* bytes);
+
+/* Enqueues on `stream` the repack of conv layer `layer`'s KRSC weights
+ * (w_krsc, device, c_out x 3 x 3 x c_in in `dtype`) into w_packed (device,
+ * mafat_packed_weights_size bytes); both 16-byte aligned, not overlapping.
+ * Done once per set of weights; the packed buffer then serves every run of
+ * plans with the same layers, grid and flags.  Errors: EINVAL (no packing
+ * for this layer, null or misaligned pointer), EUNSUPPORTED, EHIP. */
+int mafat_pack_weights(const mafat_plan* plan, int32_t layer, int32_t dtype, const void* w_krsc,
+                       void* w_packed, void* stream);
 
 /* Frees a plan (NULL is ignored). */
 void mafat_plan_destroy(mafat_plan* plan);

@@ -128,14 +128,21 @@ void conv_patch_kernel(const StageArgs a) {
   const int lrow = lane >> 2, lpos = lane & 3;
   const int cin = a.cin, cout = a.cout;
   const int K = 9 * cin;
-  const __amdgpu_buffer_rsrc_t rsb = make_rsrc(a.w, static_cast<unsigned>(cout * K * 2));
+  // Weights: KRSC, or packed per channel block and chunk ([cout/BN][cin/32]
+  // [9][BN][32], rows past c_out zero), where a chunk's BN x 9 rows are one
+  // contiguous run (whole lines for the 16-row load instructions).
+  const int nchunk = cin >> 5;
+  const bool wpk = a.w_packed != 0;
+  const __amdgpu_buffer_rsrc_t rsb =
+      make_rsrc(a.w, static_cast<unsigned>(wpk ? a.nblk_n * nchunk * 9 * BN * 64 : cout * K * 2));
+  const unsigned bstride = wpk ? static_cast<unsigned>(9 * BN * 64) : 64u;  // bytes from one chunk to the next
   // Weight loads: instruction g of a chunk's weight part fills weight rows
   // [16 g, 16 g + 16) of the slot (row = tap * BN + n); g past NB fills the
   // sink.  Chunk c adds 64 c bytes.
   unsigned b_off[NBW];
   auto issue_b = [&](int c, int slot) {
     unsigned char* sl = smem + slot * SLOT;
-    const unsigned coff = static_cast<unsigned>(c * 64);
+    const unsigned coff = static_cast<unsigned>(c) * bstride;
 #pragma unroll
     for (int k = 0; k < NBW; ++k) {
       const int g = k * NWAVE + wave;
@@ -155,8 +162,11 @@ void conv_patch_kernel(const StageArgs a) {
       const int t = row / BN, n = row - t * BN;
       const int co = n0e + n;
       const int chunk = lpos ^ ((row >> 1) & 3);
-      b_off[k] = (g < NB && co < cout) ? static_cast<unsigned>((co * K + t * cin) * 2 + chunk * 16)
-                                       : 0x80000000u;
+      if (wpk)
+        b_off[k] = (g < NB) ? static_cast<unsigned>(((nb * nchunk) * 9 * BN + row) * 64 + chunk * 16) : 0x80000000u;
+      else
+        b_off[k] = (g < NB && co < cout) ? static_cast<unsigned>((co * K + t * cin) * 2 + chunk * 16)
+                                         : 0x80000000u;
     }
     issue_b(0, 0);
   };

@@ -36,6 +36,7 @@ struct StageArgs {
   int32_t total_blocks; // batch * mblk_total * nblk_n
   int32_t chan_major;   // 1: blocks ordered channel-block-major (each XCD gets a slice of
                         //    the weights); 0: pixel-block-major (a slice of the pixels)
+  int32_t w_packed;     // patch kernel: w is packed [cout/BN][cin/32][9][BN][32] (else KRSC)
   int32_t mblk_prefix[kMaxTilesPerLaunch + 1];
   KTile tiles[kMaxTilesPerLaunch];
 };
@@ -122,6 +123,10 @@ hipError_t launch_conv_ring(int f, bool pool, const MfmaShape& shape, const Stag
 // Launch one bf16 3x3 patch-kernel stage chunk (conv_patch.hip).
 hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs& args, hipStream_t stream,
                              LaunchEvents ev);
+
+// Repack one layer's KRSC bf16 weights into the patch kernel's packed layout.
+hipError_t launch_pack_weights(const uint16_t* src, uint16_t* dst, int cout, int cin, int bn, int nblk,
+                               hipStream_t stream);
 
 // Pixel-axis block size of each kernel family.
 int block_units(int kind, MfmaShape shape);

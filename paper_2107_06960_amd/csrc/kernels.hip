@@ -902,6 +902,39 @@ int block_units(int kind, MfmaShape shape) {
   return 64;
 }
 
+namespace {
+// Weight repack for the patch kernel: one 16-byte piece (8 channels) per
+// thread, [cout/BN][cin/32][9][BN][32] from KRSC [cout][3][3][cin]; rows
+// past c_out are zero.
+__global__ __launch_bounds__(256) void pack_weights_kernel(const uint16_t* src, uint16_t* dst, int cout, int cin,
+                                                           int bn, int nblk) {
+  const int nchunk = cin >> 5;
+  const int64_t total = static_cast<int64_t>(nblk) * nchunk * 9 * bn * 4;
+  const int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (e >= total) return;
+  const int q = static_cast<int>(e & 3);                // 8-channel piece of the 32
+  int64_t r = e >> 2;
+  const int n = static_cast<int>(r % bn); r /= bn;      // row of the channel block
+  const int t = static_cast<int>(r % 9); r /= 9;        // tap
+  const int c = static_cast<int>(r % nchunk); r /= nchunk;  // 32-channel chunk
+  const int b = static_cast<int>(r);                    // channel block
+  const int co = b * bn + n;
+  u32x4 v = u32x4{0u, 0u, 0u, 0u};
+  if (co < cout) v = *reinterpret_cast<const u32x4*>(src + (static_cast<int64_t>(co) * 9 + t) * cin + c * 32 + q * 8);
+  *reinterpret_cast<u32x4*>(dst + e * 8) = v;
+}
+
+}  // namespace
+
+hipError_t launch_pack_weights(const uint16_t* src, uint16_t* dst, int cout, int cin, int bn, int nblk,
+                               hipStream_t stream) {
+  const int64_t total = static_cast<int64_t>(nblk) * (cin >> 5) * 9 * bn * 4;
+  if (total <= 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>((total + 255) / 256));
+  hipLaunchKernelGGL(pack_weights_kernel, grid, dim3(256), 0, stream, src, dst, cout, cin, bn, nblk);
+  return hipGetLastError();
+}
+
 hipError_t launch_stage(int kind, int dtype, int f, bool pool, MfmaShape shape,
                         const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
   if (args.total_blocks <= 0) return hipSuccess;

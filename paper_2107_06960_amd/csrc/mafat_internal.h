@@ -67,6 +67,7 @@ struct mafat_plan {
   std::vector<mafat_layer> layers;
   std::vector<std::array<int, 6>> dims;  // in_h, in_w, in_c, out_h, out_w, out_c
   std::vector<mafat::Group> groups;
+  bool packed_weights = false;  // MAFAT_PLAN_PACKED_WEIGHTS
 };
 
 namespace mafat {
@@ -84,6 +85,17 @@ struct StageConfig {
   int64_t blocks;    // output blocks per frame (pixel blocks x channel blocks)
 };
 StageConfig choose_config(const Stage& S, int batch, int dtype);
+
+// The configuration a stage runs with in a plan (choose_config with the
+// batch the plan's weight layout fixes, and the generic kernel for frames
+// too large for 32-bit offsets).
+StageConfig stage_config(const mafat_plan& P, const Group& G, const Stage& S, int batch, int dtype);
+
+// Packed weights of a conv layer (run by the bf16 3x3 patch kernel in a
+// plan with packed weights): [channel block][32-channel chunk][tap][BN
+// rows][32 channels], rows past c_out zero.  Returns false (and bn = 0)
+// for a layer whose weights stay KRSC.
+bool packed_layout(const mafat_plan& P, int layer, int dtype, int* bn, int* nblk, int* nchunk);
 
 // Workspace layout for one group: the ping-pong scratch buffers of every
 // tile of every frame, 256-byte aligned.  Sizes in bytes.

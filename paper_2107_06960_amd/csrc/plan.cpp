@@ -230,7 +230,7 @@ extern "C" int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_laye
   clear_error();
   if (!out) { set_error("out is NULL"); return MAFAT_EINVAL; }
   *out = nullptr;
-  if (flags & ~MAFAT_PLAN_TILE_REUSE) {
+  if (flags & ~(MAFAT_PLAN_TILE_REUSE | MAFAT_PLAN_PACKED_WEIGHTS)) {
     set_error("unknown plan flags");
     return MAFAT_EINVAL;
   }
@@ -246,6 +246,7 @@ extern "C" int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_laye
   if (!plan) return MAFAT_ENOMEM;
   try {
     plan->n = n_layers; plan->in_h = in_h; plan->in_w = in_w; plan->in_c = in_c;
+    plan->packed_weights = (flags & MAFAT_PLAN_PACKED_WEIGHTS) != 0;
     plan->layers.assign(layers, layers + n_layers);
     int h = in_h, w = in_w, c = in_c;
     for (int l = 0; l < n_layers; ++l) {

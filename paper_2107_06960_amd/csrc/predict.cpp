@@ -69,11 +69,15 @@ int64_t device_bytes(const mafat_plan& P, int batch, int dtype) {
     const auto& d = P.dims[P.groups[g].l1];
     total += static_cast<int64_t>(batch) * d[3] * d[4] * d[5] * esz;
   }
-  for (int l = 0; l < P.n; ++l) {  // parameters
+  for (int l = 0; l < P.n; ++l) {  // parameters (packed weights where the plan packs them)
     const mafat_layer& L = P.layers[l];
     if (L.op != MAFAT_CONV) continue;
     const auto& d = P.dims[l];
-    total += static_cast<int64_t>(d[5]) * L.f * L.f * d[2] * esz + 2 * 4 * static_cast<int64_t>(d[5]);
+    int bn, nblk, nchunk;
+    const int64_t w = packed_layout(P, l, dtype, &bn, &nblk, &nchunk)
+                          ? static_cast<int64_t>(nblk) * nchunk * 9 * bn * 32 * esz
+                          : static_cast<int64_t>(d[5]) * L.f * L.f * d[2] * esz;
+    total += w + 2 * 4 * static_cast<int64_t>(d[5]);
   }
   size_t ws = 0;
   mafat_workspace_size(&P, batch, dtype, &ws);

@@ -225,6 +225,38 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
   return tune_override(S, c);
 }
 
+StageConfig stage_config(const mafat_plan& P, const Group& G, const Stage& S, int batch, int dtype) {
+  // A plan with packed weights fixes the layout for every batch: its
+  // stages take the configuration chosen for one frame.
+  StageConfig c = choose_config(S, P.packed_weights ? 1 : batch, dtype);
+  // The matrix-core kernels address a frame's source buffer with 32-bit
+  // byte offsets; the generic kernel covers larger frames.
+  const int64_t esz = (dtype == MAFAT_F32) ? 4 : 2;
+  const auto& din = P.dims[G.l0];
+  const int64_t src_frame = (S.src_buf == BUF_GROUP_IO) ? static_cast<int64_t>(din[0]) * din[1] * din[2]
+                                                        : G.scratch_frame;
+  if ((c.kind == K_CONV_MFMA || c.kind == K_CONV_RING || c.kind == K_CONV_PATCH) &&
+      src_frame * esz >= (1ll << 31))
+    c.kind = K_CONV_DIRECT;
+  return c;
+}
+
+bool packed_layout(const mafat_plan& P, int layer, int dtype, int* bn, int* nblk, int* nchunk) {
+  *bn = *nblk = *nchunk = 0;
+  if (!P.packed_weights || dtype != MAFAT_BF16) return false;
+  for (const Group& G : P.groups)
+    for (const Stage& S : G.stages)
+      if (S.kind == STAGE_CONV && S.first == layer) {
+        const StageConfig c = stage_config(P, G, S, 1, dtype);
+        if (c.kind != K_CONV_PATCH) return false;
+        *bn = c.bn;
+        *nblk = (S.cout + c.bn - 1) / c.bn;
+        *nchunk = S.cin / 32;
+        return true;
+      }
+  return false;
+}
+
 WorkspaceLayout workspace_layout(const Group& G, int batch, int dtype) {
   const size_t esz = (dtype == MAFAT_F32) ? 4 : 2;
   WorkspaceLayout L{};
@@ -278,14 +310,8 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
     hipEvent_t ev_start = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin)]) : nullptr;
     hipEvent_t ev_stop = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin) + 1]) : nullptr;
     bool launched = false;
-    const StageConfig cfg = choose_config(S, batch, dtype);
-    int kind = cfg.kind;
-    // The matrix-core kernel addresses a frame's source buffer with 32-bit
-    // byte offsets; the generic kernel covers larger frames.
-    const int64_t src_frame_elems = (S.src_buf == BUF_GROUP_IO) ? in_frame : scr_frame;
-    if ((kind == K_CONV_MFMA || kind == K_CONV_RING || kind == K_CONV_PATCH) &&
-        src_frame_elems * static_cast<int64_t>(esz) >= (1ll << 31))
-      kind = K_CONV_DIRECT;
+    const StageConfig cfg = stage_config(*plan, G, S, batch, dtype);
+    const int kind = cfg.kind;
     const bool matrix = (kind == K_CONV_MFMA || kind == K_CONV_RING || kind == K_CONV_PATCH);
     const MfmaShape shape{cfg.bm, cfg.bn, cfg.depth, cfg.kg, cfg.wgm, cfg.wgn, cfg.kord, cfg.br, cfg.bc};
     const int bu = (kind == K_CONV_RGB) ? 256 / (S.cout / 8) : block_units(kind, shape);
@@ -305,6 +331,7 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
     A.act = S.act;
     A.nblk_n = matrix ? (S.cout + shape.bn - 1) / shape.bn : 1;
     A.chan_major = matrix ? cfg.chan_major : 0;
+    A.w_packed = (plan->packed_weights && kind == K_CONV_PATCH) ? 1 : 0;
     for (int t0 = 0; t0 < G.ntiles; t0 += kMaxTilesPerLaunch) {
       const int t1 = std::min(G.ntiles, t0 + kMaxTilesPerLaunch);
       A.ntiles = t1 - t0;
@@ -493,3 +520,37 @@ extern "C" int mafat_debug_config(const mafat_plan* plan, int32_t g, int32_t s, 
   return 0;
 }
 #endif
+
+extern "C" int mafat_packed_weights_size(const mafat_plan* plan, int32_t layer, int32_t dtype, size_t* bytes) {
+  clear_error();
+  if (!plan || !bytes || layer < 0 || layer >= plan->n) {
+    set_error("plan and bytes must be non-NULL and the layer in range");
+    return MAFAT_EINVAL;
+  }
+  if (dtype != MAFAT_F32 && dtype != MAFAT_BF16) {
+    set_error("dtype must be F32 or BF16");
+    return MAFAT_EUNSUPPORTED;
+  }
+  int bn, nblk, nchunk;
+  *bytes = packed_layout(*plan, layer, dtype, &bn, &nblk, &nchunk)
+               ? static_cast<size_t>(nblk) * nchunk * 9 * bn * 32 * 2
+               : 0;
+  return MAFAT_OK;
+}
+
+extern "C" int mafat_pack_weights(const mafat_plan* plan, int32_t layer, int32_t dtype, const void* w_krsc,
+                                  void* w_packed, void* stream) {
+  size_t bytes = 0;
+  int rc = mafat_packed_weights_size(plan, layer, dtype, &bytes);
+  if (rc != MAFAT_OK) return rc;
+  if (bytes == 0) return fail(MAFAT_EINVAL, "layer " + std::to_string(layer) + " takes KRSC weights (no packing)");
+  if (!w_krsc || !w_packed || !aligned16(w_krsc) || !aligned16(w_packed))
+    return fail(MAFAT_EINVAL, "weights must be non-NULL and 16-byte aligned");
+  int bn, nblk, nchunk;
+  packed_layout(*plan, layer, dtype, &bn, &nblk, &nchunk);
+  const auto& d = plan->dims[layer];
+  const hipError_t e = launch_pack_weights(static_cast<const uint16_t*>(w_krsc), static_cast<uint16_t*>(w_packed),
+                                           d[5], d[2], bn, nblk, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(MAFAT_EHIP, std::string("pack launch failed: ") + hipGetErrorString(e));
+  return MAFAT_OK;
+}

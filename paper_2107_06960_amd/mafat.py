@@ -27,12 +27,13 @@ MAFAT_CONV, MAFAT_MAXPOOL = 0, 1
 MAFAT_ACT_LINEAR, MAFAT_ACT_LEAKY01 = 0, 1
 MAFAT_F32, MAFAT_BF16 = 0, 1
 MAFAT_MEM_DEVICE, MAFAT_MEM_PAPER = 0, 1
-MAFAT_PLAN_TILE_REUSE = 1
+MAFAT_PLAN_TILE_REUSE, MAFAT_PLAN_PACKED_WEIGHTS = 1, 2
 MEM_MODELS = {"device": MAFAT_MEM_DEVICE, "paper": MAFAT_MEM_PAPER}
 DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
 
 # Every symbol include/mafat.h declares.
-EXPORTS = ("mafat_plan_create", "mafat_plan_create_flags", "mafat_plan_destroy", "mafat_plan_layer_shape", "mafat_plan_group",
+EXPORTS = ("mafat_plan_create", "mafat_plan_create_flags", "mafat_plan_destroy",
+           "mafat_packed_weights_size", "mafat_pack_weights", "mafat_plan_layer_shape", "mafat_plan_group",
            "mafat_plan_regions", "mafat_plan_macs", "mafat_plan_stages", "mafat_plan_stage_layers",
            "mafat_workspace_size", "mafat_run_group", "mafat_run_stage", "mafat_run_network",
            "mafat_predict_mem", "mafat_get_config", "mafat_status_string", "mafat_last_error")
@@ -75,6 +76,8 @@ def lib():
         L.mafat_plan_create_flags.argtypes = [ctypes.POINTER(mafat_layer), i32, i32, i32, i32, i32p, i32,
                                               i32p, i32p, i32, ctypes.POINTER(planp)]
         L.mafat_plan_destroy.argtypes = [planp]
+        L.mafat_packed_weights_size.argtypes = [planp, i32, i32, ctypes.POINTER(sz)]
+        L.mafat_pack_weights.argtypes = [planp, i32, i32, vp, vp, vp]
         L.mafat_plan_destroy.restype = None
         L.mafat_plan_layer_shape.argtypes = [planp, i32, i32p]
         L.mafat_plan_group.argtypes = [planp, i32, i32p, i32p, i32p]
@@ -142,6 +145,19 @@ def mafat_plan_create(layers, in_h, in_w, in_c, group_start, grid_rows, grid_col
 
 def mafat_plan_destroy(plan):
     lib().mafat_plan_destroy(plan)
+
+
+def mafat_packed_weights_size(plan, layer, dtype):
+    v = ctypes.c_size_t()
+    _check("mafat_packed_weights_size",
+           lib().mafat_packed_weights_size(plan, layer, DTYPES.get(dtype, dtype), ctypes.byref(v)))
+    return v.value
+
+
+def mafat_pack_weights(plan, layer, dtype, w_krsc_ptr, w_packed_ptr, stream=None):
+    _check("mafat_pack_weights",
+           lib().mafat_pack_weights(plan, layer, DTYPES.get(dtype, dtype), w_krsc_ptr, w_packed_ptr,
+                                    _stream_handle(stream)))
 
 
 def mafat_plan_layer_shape(plan, layer):
@@ -259,14 +275,17 @@ class Plan:
     """A plan for a layer stack, an input shape and a tiling spec such as
     ``"5x5/8/2x2"`` (section 5.1 notation) or explicit group lists."""
 
-    def __init__(self, layers, in_hwc, tiling="1x1/NoCut", reuse=False):
+    def __init__(self, layers, in_hwc, tiling="1x1/NoCut", reuse=False, packed_weights=False):
         self.layers = list(layers)
         self.reuse = bool(reuse)
+        self.packed_weights = bool(packed_weights)
         self.h, self.w, self.c = in_hwc
         self.group_start, self.rows, self.cols = W.parse_tiling(tiling, len(layers)) \
             if isinstance(tiling, str) else tiling
         self.handle = mafat_plan_create(self.layers, self.h, self.w, self.c, self.group_start,
-                                        self.rows, self.cols, MAFAT_PLAN_TILE_REUSE if self.reuse else 0)
+                                        self.rows, self.cols,
+                                        (MAFAT_PLAN_TILE_REUSE if self.reuse else 0) |
+                                        (MAFAT_PLAN_PACKED_WEIGHTS if self.packed_weights else 0))
         self.n_groups = len(self.group_start)
 
     def __del__(self):
@@ -326,7 +345,15 @@ class Network:
             if L["op"] != W.CONV:
                 self.w.append(None); self.scale.append(None); self.bias.append(None)
                 continue
-            self.w.append(torch.from_numpy(np.ascontiguousarray(params["w"][k])).to(device=device, dtype=tdt))
+            w = torch.from_numpy(np.ascontiguousarray(params["w"][k])).to(device=device, dtype=tdt)
+            nbytes = mafat_packed_weights_size(plan.handle, k, dtype)
+            if nbytes:  # the plan takes this layer's weights packed (mafat_pack_weights)
+                wp = torch.empty(nbytes // w.element_size(), dtype=tdt, device=device)
+                mafat_pack_weights(plan.handle, k, dtype, w.data_ptr(), wp.data_ptr())
+                torch.cuda.synchronize()
+                del w
+                w = wp
+            self.w.append(w)
             self.scale.append(torch.from_numpy(np.ascontiguousarray(params["scale"][k])).to(device))
             self.bias.append(torch.from_numpy(np.ascontiguousarray(params["bias"][k])).to(device))
         self.cuts = [torch.empty((batch,) + plan.group_out_shape(g), dtype=tdt, device=device)

@@ -147,8 +147,36 @@ def test_tile_reuse_plan(lib):
     arr = (M.mafat_layer * 1)(M.mafat_layer(0, 8, 3, 1, 1, 1))
     h = ctypes.c_void_p()
     one = (ctypes.c_int32 * 1)(1)
-    rc = M.lib().mafat_plan_create_flags(arr, 1, 16, 16, 3, (ctypes.c_int32 * 1)(0), 1, one, one, 2, ctypes.byref(h))
+    rc = M.lib().mafat_plan_create_flags(arr, 1, 16, 16, 3, (ctypes.c_int32 * 1)(0), 1, one, one, 4, ctypes.byref(h))
     assert rc == M.MAFAT_EINVAL and not h.value
+
+
+def test_packed_weights_plan(lib):
+    # packed weights: only bf16 3x3 layers run by the patch kernel are
+    # packed (same bytes as KRSC when c_out is a multiple of the block);
+    # plans without the flag pack nothing; packing a KRSC layer is EINVAL
+    plain = M.Plan(W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2")
+    packed = M.Plan(W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2", packed_weights=True)
+    for l, L in enumerate(W.YOLOV2_16):
+        assert M.mafat_packed_weights_size(plain.handle, l, "bf16") == 0
+        assert M.mafat_packed_weights_size(packed.handle, l, "f32") == 0
+        n = M.mafat_packed_weights_size(packed.handle, l, "bf16")
+        if L["op"] == W.CONV and L["f"] == 3 and l > 0:
+            d = packed.shape(l)
+            assert n == d[5] * 9 * d[2] * 2, l
+        else:
+            assert n == 0, l
+    assert packed.predict_mem("device", 1, "bf16") == plain.predict_mem("device", 1, "bf16")
+    # first layer: KRSC, rejected before anything is enqueued
+    assert M.lib().mafat_pack_weights(packed.handle, 0, M.MAFAT_BF16, 16, 16, None) == M.MAFAT_EINVAL
+    assert M.lib().mafat_pack_weights(packed.handle, 8, M.MAFAT_BF16, None, 16, None) == M.MAFAT_EINVAL
+    with pytest.raises(M.MafatError):
+        M.mafat_packed_weights_size(packed.handle, 99, "bf16")
+    arr = (M.mafat_layer * 1)(M.mafat_layer(0, 8, 3, 1, 1, 1))
+    h = ctypes.c_void_p()
+    one = (ctypes.c_int32 * 1)(1)
+    assert M.lib().mafat_plan_create_flags(arr, 1, 16, 16, 3, (ctypes.c_int32 * 1)(0), 1, one, one, 4,
+                                           ctypes.byref(h)) == M.MAFAT_EINVAL
 
 
 def _create_rc(layers, h, w, c, gs, rows, cols):

@@ -20,21 +20,21 @@ FULL = ["tiny", "yolo416_ftp3", "yolo608_5x5_8_2x2", "yolo608_4x4_12_1x1_b8"] + 
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("reuse", [False, True])
+@pytest.mark.parametrize("reuse,packed", [(False, False), (True, False), (False, True)])
 @pytest.mark.parametrize("name", FULL)
-def test_device_model_matches_measured_peak(name, reuse):
+def test_device_model_matches_measured_peak(name, reuse, packed):
     require_gpu()
     import torch
     from paper_2107_06960_amd import mafat as M
     wl = W.WORKLOADS[name]
-    print(f"[memory] {name}: {wl.h}x{wl.w}x{wl.c} {wl.tiling} batch={wl.batch} {wl.dtype} reuse={reuse}",
+    print(f"[memory] {name}: {wl.h}x{wl.w}x{wl.c} {wl.tiling} batch={wl.batch} {wl.dtype} reuse={reuse} packed={packed}",
           flush=True)
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     base = torch.cuda.memory_stats().get("requested_bytes.all.current", 0)
     base_alloc = torch.cuda.memory_allocated()
     p = W.workload_inputs(wl)
-    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=reuse)
+    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=reuse, packed_weights=packed)
     net = M.Network(plan, p, wl.batch, wl.dtype)
     x = net.input_tensor(p["x"])
     torch.cuda.synchronize()

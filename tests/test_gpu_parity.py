@@ -227,3 +227,64 @@ def test_more_groups_and_other_networks(orc, dtype, reuse):
     _check_full(orc, W.YOLOV2_16, 80, 80, 3, "4x4/4/3x3/8/2x2/12/1x1", 1, dtype, seed=31, reuse=reuse)
     # three groups with non-square grids on the VGG-style stack
     _check_full(orc, VGG_LIKE, 64, 64, 3, "3x2/3/2x3/6/1x2", 1, dtype, seed=32, reuse=reuse)
+
+
+def test_pack_weights_kernel_layout():
+    # the repack kernel against the layout written out with torch ops:
+    # [cout/BN][cin/32][9][BN][32], rows past c_out zero
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    layers = [W.conv(96), W.conv(48)]   # c_out not a multiple of the block: zero rows
+    plan = M.Plan(layers, (40, 40, 64), "1x1", packed_weights=True)
+    g = torch.Generator().manual_seed(3)
+    for l in range(2):
+        d = plan.shape(l)
+        cout, cin = d[5], d[2]
+        n = M.mafat_packed_weights_size(plan.handle, l, "bf16")
+        assert n > 0
+        w = torch.randn(cout, 3, 3, cin, generator=g).to(torch.bfloat16).cuda()
+        out = torch.full((n // 2,), float("nan"), dtype=torch.bfloat16, device="cuda")
+        M.mafat_pack_weights(plan.handle, l, "bf16", w.data_ptr(), out.data_ptr())
+        torch.cuda.synchronize()
+        nst = cin // 32
+        blocks = n // 2 // (nst * 9 * 32)       # nblk * BN (the block size is the runtime's choice)
+        matched = False
+        for bn in (16, 32, 64, 128, 256):
+            if blocks % bn or (cout + bn - 1) // bn * bn != blocks:
+                continue
+            ref = torch.zeros(blocks, 3, 3, cin, dtype=torch.bfloat16, device="cuda")
+            ref[:cout] = w
+            ref = ref.view(blocks // bn, bn, 9, nst, 32).permute(0, 3, 2, 1, 4).contiguous().view(-1)
+            matched = matched or torch.equal(out, ref)
+        assert matched, l
+
+
+@pytest.mark.parametrize("reuse", [False, True])
+def test_packed_weights_bit_identical(reuse):
+    # the same stage configurations read the same weights from the packed
+    # layout: the output is bit for bit that of KRSC weights (batch 1)
+    import torch
+    p = W.make_inputs(W.YOLOV2_16, 128, 128, 3, 1, 8, "bf16")
+    from paper_2107_06960_amd import mafat as M
+    outs = []
+    for packed in (False, True):
+        plan = M.Plan(W.YOLOV2_16, (128, 128, 3), "5x5/8/2x2", reuse=reuse, packed_weights=packed)
+        net = M.Network(plan, p, 1, "bf16")
+        outs.append(net.run(net.input_tensor(p["x"])).clone())
+        torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1])
+
+
+def test_packed_weights_parity(orc):
+    # batch 2 (stage configurations of one frame), odd extents, with reuse
+    from paper_2107_06960_amd import mafat as M
+    layers, h, w, c = W.YOLOV2_16, 71, 93, 3
+    p = W.make_inputs(layers, h, w, c, 2, 5, "bf16")
+    plan = M.Plan(layers, (h, w, c), "3x2/8/2x2", reuse=True, packed_weights=True)
+    net = M.Network(plan, p, 2, "bf16")
+    y = net.run(net.input_tensor(p["x"]))
+    import torch
+    torch.cuda.synchronize()
+    out = y.float().cpu().numpy().astype(np.float64)
+    ref = orc.forward_layers(layers, h, w, c, p["x"], p)
+    assert normwise_err(out, ref) <= TOL["bf16"]
