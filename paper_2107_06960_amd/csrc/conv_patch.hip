@@ -25,17 +25,25 @@
 // (l & 3) ^ key(row), so that the 8 rows an MFMA fragment read serves per
 // LDS cycle (at one K offset) hit distinct banks: weight rows use
 // key = (row >> 1) & 3 (they are read 8 consecutive rows at a time); patch
-// pixel (py, px) uses key = ((px >> 1) ^ 2 py) & 3, which stays
-// conflict-free across the block-row wraps, 2x2 pool windows and tap shifts
-// of the fragments (found by enumerating the fragments of every block
-// shape).  Patch pixels outside the image (the
+// pixel (py, px) uses key = ((px >> 1) ^ 2 py) & 3.  (Measured bank-conflict
+// cycles: none for 16x16 blocks without a pool, 12-30 % of the LDS cycles
+// for the other shapes; a model of 8-lane phases over 32 banks predicts
+// none, so the hardware's grouping differs from it.)  Patch pixels outside
+// the image (the
 // zero padding), outside the tile's source region, or past the patch, and
 // weight rows past c_out, are fetched at an offset with bit 31 set, past the
 // buffer descriptor's range: the range check returns zeros.  Loads run NS-1
 // chunks ahead; every chunk costs one explicit vmcnt wait and one barrier.
 // With NS = 1 (one slot) a chunk is loaded, awaited and computed in turn:
 // the LDS footprint halves, so two workgroups share a CU and hide each
-// other's load latency.
+// other's load latency.  The first chunk's weight rows are issued while the
+// tile table is still being decoded (they depend only on the channel
+// block).  Weights come as KRSC, or packed per channel block and chunk
+// ([c_out/BN][c_in/32][9][BN][32]) so that a chunk's rows are one run.
+//
+// Epilogue: scale, bias, activation and the fused pool in registers, the
+// block's outputs staged in LDS as rows of BN channels, then written as
+// 16-byte chunks (each output pixel's BN channels contiguous).
 //
 // Requires f = 3, c_in % 32 == 0, c_out % 16 == 0, byte offsets below 2^31
 // within a frame's source buffer and within the weights (host-checked); a

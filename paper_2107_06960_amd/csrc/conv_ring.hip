@@ -35,11 +35,12 @@
 // group g multiplies the 64-byte half g of every stage, and the two partial
 // sums meet through LDS at the end (each group then stores half of the
 // channel tiles).
-// Epilogue: as the other matrix-core kernel (see store_tile): without a
-// pool the weights are the MFMA's A operand, so a lane holds 4 consecutive
-// channels of one pixel (one 8-byte store); with a fused pool the pixels
+// Epilogue: without a pool the weights are the MFMA's A operand, so a lane
+// holds 4 consecutive channels of one pixel; with a fused pool the pixels
 // are, quad-ordered, so a lane's 4 accumulator rows are one 2x2 window,
-// reduced in the lane.
+// reduced in the lane.  The block's outputs are staged in LDS as rows of BN
+// channels and leave as 16-byte stores.  The first stage's weight rows are
+// issued while the tile table is being decoded.
 //
 // Requires c_in % 32 == 0, c_out % 16 == 0, byte offsets below 2^31 within
 // a frame's source buffer and within the weights (checked by the host).
