@@ -109,7 +109,11 @@ __device__ __forceinline__ void block_pixel(int r, int* py, int* px) {
   }
 }
 
-template <int BR, int BC, int BM, int BN, int WGM, int WGN, int NS, bool POOL>
+// N2 > 0: a 1x1 convolution with N2 outputs of this stage's output (all BN
+// = c_out channels in the block) follows in the same workgroup: the block's
+// activated bf16 outputs stay in LDS and are the A operand of a second GEMM
+// with its weights (a.w2, [N2][BN]), whose result is the stage's output.
+template <int BR, int BC, int BM, int BN, int WGM, int WGN, int NS, bool POOL, int N2 = 0>
 __global__ __launch_bounds__(64 * WGM * WGN)
 void conv_patch_kernel(const StageArgs a) {
   constexpr int NWAVE = WGM * WGN;
@@ -127,7 +131,43 @@ void conv_patch_kernel(const StageArgs a) {
   static_assert(BR * BC <= BM && BM % (16 * WGM) == 0, "block rows");
   static_assert(!POOL || (BR % 2 == 0 && BC % 2 == 0), "pooled blocks cover whole windows");
   static_assert(NS >= 1 && NS <= 6 && (NS - 2) * LPS <= 63, "ring depth");
-  __shared__ __align__(1024) unsigned char smem[NS * SLOT + (SINK ? 1024 : 0)];
+  // Fused 1x1 weights (N2 > 0): their own LDS region past the ring.
+  constexpr int W2D = NS * SLOT + (SINK ? 1024 : 0);
+  __shared__ __align__(1024) unsigned char smem[W2D + (N2 > 0 ? N2 * BN * 2 : 0)];
+  static_assert(N2 == 0 || (!POOL && BM == BR * BC && N2 % 16 == 0 && BN % 32 == 0),
+                "fused 1x1: no pool, no padding rows");
+  // Fused 1x1: its weights ([N2][BN] bf16) go straight to LDS now (rows of
+  // BN = 128 channels, 16-byte piece q of row r at slot q ^ (r & 15), so
+  // the 16 rows of a fragment read fall in different banks); its scale and
+  // bias are fetched into registers.  The second GEMM's waves: WC2 along
+  // its channels (CT2 16-channel tiles each) times WP2 along the block's
+  // pixels (PG2 16-pixel groups).
+  constexpr int WC2 = 2, WP2 = WGM * WGN / WC2;
+  constexpr int CT2 = N2 > 0 ? N2 / 16 / WC2 : 1, PG2 = BM / 16 / WP2;
+  static_assert(N2 == 0 || (N2 % (16 * WC2) == 0 && (BM / 16) % WP2 == 0 && BN == 128 &&
+                            (N2 * BN * 2) % (1024 * WGM * WGN) == 0), "second GEMM");
+  float sc2[CT2][4], bi2[CT2][4];
+  if constexpr (N2 > 0) {
+    const int w0 = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+    const int l0 = static_cast<int>(threadIdx.x) & 63;
+    const __amdgpu_buffer_rsrc_t rs2 = make_rsrc(a.w2, static_cast<unsigned>(N2 * BN * 2));
+#pragma unroll
+    for (int k = 0; k < N2 * BN * 2 / (1024 * WGM * WGN); ++k) {
+      const int e = (k * WGM * WGN + w0) * 64 + l0;  // LDS slot of this lane's piece
+      const int r = e >> 4, q = (e & 15) ^ (r & 15);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs2, (lds_ptr_t)(smem + W2D + (k * WGM * WGN + w0) * 1024), 16,
+                                               (r * 16 + q) * 16, 0, 0, 0);
+    }
+    const int wc = w0 % WC2;
+#pragma unroll
+    for (int j = 0; j < CT2; ++j) {
+      const int c2 = (wc * CT2 + j) * 16 + 4 * (l0 >> 4);
+      const f32x4 s4 = *reinterpret_cast<const f32x4*>(a.scale2 + c2);
+      const f32x4 b4 = *reinterpret_cast<const f32x4*>(a.bias2 + c2);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) { sc2[j][r] = s4[r]; bi2[j][r] = b4[r]; }
+    }
+  }
 
   MAFAT_PTRACE(0);
   MAFAT_WG_MARK(g_wg_patch, 0);
@@ -387,8 +427,69 @@ void conv_patch_kernel(const StageArgs a) {
       }
     }
   }
-  __syncthreads();
   const int vy = tl.cy0 + tl.ch - by0, vx = tl.cx0 + tl.cw - bx0;  // valid extent of this block
+  if constexpr (N2 > 0) {
+    // Second GEMM, in LDS: out[p][c2] = sum_c act(stage)[p][c] w2[c2][c];
+    // the results replace the staged rows once every wave has read them.
+    MAFAT_PTRACE(16);
+    __syncthreads();  // the staged rows are complete (the weights arrived before the first chunk)
+    MAFAT_PTRACE(17);
+    const int wp = wave / WC2, wc = wave - (wave / WC2) * WC2;
+    f32x4 acc2[PG2][CT2];
+#pragma unroll
+    for (int i = 0; i < PG2; ++i)
+#pragma unroll
+      for (int j = 0; j < CT2; ++j) acc2[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int ra = ((wp * PG2) * 16 + (lane & 15)) * RSB + 16 * (lane >> 4);
+    const int rb2 = W2D + ((wc * CT2) * 16 + (lane & 15)) * (BN * 2);
+#pragma unroll
+    for (int k0 = 0; k0 < BN; k0 += 32) {
+      u32x4 av[PG2], bv[CT2];
+#pragma unroll
+      for (int i = 0; i < PG2; ++i) av[i] = *reinterpret_cast<const u32x4*>(smem + ra + i * 16 * RSB + k0 * 2);
+#pragma unroll
+      for (int j = 0; j < CT2; ++j)
+        bv[j] = *reinterpret_cast<const u32x4*>(smem + rb2 + j * 16 * (BN * 2) +
+                                                (((k0 >> 3) + (lane >> 4)) ^ (lane & 15)) * 16);
+#pragma unroll
+      for (int i = 0; i < PG2; ++i)
+#pragma unroll
+        for (int j = 0; j < CT2; ++j) mma<MAFAT_BF16>(acc2[i][j], bv[j], av[i]);
+    }
+    MAFAT_PTRACE(18);
+    __syncthreads();  // every wave is done reading the staged rows
+    // a lane's results: channels 16 j' + 4 (lane >> 4) .. + 3 of pixel
+    // 16 i' + (lane & 15) (i', j' the global group and tile)
+    const float slope2 = act_slope(a.act2);
+#pragma unroll
+    for (int i = 0; i < PG2; ++i)
+#pragma unroll
+      for (int j = 0; j < CT2; ++j) {
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          v[r] = fmaf(acc2[i][j][r], sc2[j][r], bi2[j][r]);
+          v[r] = fmaxf(v[r], slope2 * v[r]);
+        }
+        store4<MAFAT_BF16>(reinterpret_cast<uint16_t*>(smem + ((wp * PG2 + i) * 16 + (lane & 15)) * RSB) +
+                               (wc * CT2 + j) * 16 + 4 * (lane >> 4), v);
+      }
+    __syncthreads();
+    MAFAT_PTRACE(19);
+    constexpr int CPB2 = N2 / 8;
+    for (int e = tid; e < NPXO * CPB2; e += NTHR) {
+      const int p = e / CPB2, k = e - p * CPB2;
+      const int py = p / BC, px = p - py * BC;
+      if (py < vy && px < vx) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(smem + p * RSB + k * 16);
+        *reinterpret_cast<u32x4*>(dst + ((by0 + py - tl.dy0) * tl.dw + (bx0 + px - tl.dx0)) * N2 + k * 8) = v;
+      }
+    }
+    MAFAT_PTRACE(5);
+    MAFAT_WG_MARK(g_wg_patch, 1);
+    return;
+  }
+  __syncthreads();
   for (int e = tid; e < NPXO * CPB; e += NTHR) {
     const int p = e / CPB, k = e - p * CPB;
     int oy, ox;
@@ -435,6 +536,15 @@ hipError_t launch_patch_p(const MfmaShape& sh, const StageArgs& args, hipStream_
 }
 
 }  // namespace
+
+hipError_t launch_conv_patch_fused(const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
+  if (args.total_blocks <= 0) return hipSuccess;
+  if (args.cout != 128 || args.cout2 != 64) return hipErrorInvalidValue;
+  hipExtLaunchKernelGGL((conv_patch_kernel<8, 16, 128, 128, 4, 2, 1, false, 64>),
+                        dim3(static_cast<unsigned>(args.total_blocks)), dim3(512), 0, stream, ev.start, ev.stop, 0,
+                        args);
+  return hipGetLastError();
+}
 
 hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs& args, hipStream_t stream,
                              LaunchEvents ev) {

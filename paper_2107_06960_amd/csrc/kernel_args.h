@@ -37,6 +37,12 @@ struct StageArgs {
   int32_t chan_major;   // 1: blocks ordered channel-block-major (each XCD gets a slice of
                         //    the weights); 0: pixel-block-major (a slice of the pixels)
   int32_t w_packed;     // patch kernel: w is packed [cout/BN][cin/32][9][BN][32] (else KRSC)
+  // Fused second layer (a 1x1 convolution of this stage's output, computed
+  // in the same workgroup): weights [cout2][cin = cout], its scale and bias.
+  const void* w2;
+  const float* scale2;
+  const float* bias2;
+  int32_t cout2, act2;
   int32_t mblk_prefix[kMaxTilesPerLaunch + 1];
   KTile tiles[kMaxTilesPerLaunch];
 };
@@ -78,7 +84,8 @@ struct MfmaShape {
   MAFAT_PATCH(10, 10, 128, 32, 8, 1, 2)   \
   MAFAT_PATCH(8, 8, 64, 32, 4, 2, 2)      \
   MAFAT_PATCH(8, 16, 128, 64, 8, 1, 1)    \
-  MAFAT_PATCH(12, 16, 192, 64, 4, 2, 1)
+  MAFAT_PATCH(12, 16, 192, 64, 4, 2, 1)   \
+  MAFAT_PATCH(8, 16, 128, 128, 4, 2, 1)
 #ifdef MAFAT_TUNING
 #define MAFAT_PATCH_TUNE_SHAPES           \
   MAFAT_PATCH(16, 12, 192, 64, 4, 2, 1)   \
@@ -123,6 +130,12 @@ hipError_t launch_conv_ring(int f, bool pool, const MfmaShape& shape, const Stag
 // Launch one bf16 3x3 patch-kernel stage chunk (conv_patch.hip).
 hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs& args, hipStream_t stream,
                              LaunchEvents ev);
+
+// Launch a bf16 3x3 stage with 128 output channels fused with the 1x1
+// stage (64 outputs) that follows it (conv_patch.hip): 8x16 blocks of all
+// 128 channels; args.w2 / scale2 / bias2 / cout2 / act2 describe the 1x1
+// layer, the destination fields the 1x1 stage's output.
+hipError_t launch_conv_patch_fused(const StageArgs& args, hipStream_t stream, LaunchEvents ev);
 
 // Repack one layer's KRSC bf16 weights into the patch kernel's packed layout.
 hipError_t launch_pack_weights(const uint16_t* src, uint16_t* dst, int cout, int cin, int bn, int nblk,

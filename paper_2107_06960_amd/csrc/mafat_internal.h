@@ -83,6 +83,8 @@ struct StageConfig {
   int wgm, wgn;      // wave arrangement (see MfmaShape)
   int chan_major;    // block order (see StageArgs::chan_major)
   int64_t blocks;    // output blocks per frame (pixel blocks x channel blocks)
+  int fuse;          // 1: runs fused with the next (1x1) stage when both are launched
+                     //    together; -1: the second stage of such a pair; 0: neither
 };
 StageConfig choose_config(const Stage& S, int batch, int dtype);
 

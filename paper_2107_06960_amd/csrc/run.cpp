@@ -128,7 +128,7 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
     const int chunks = S.cin / 32;
     double best = 1e30;
     for (const PS& r : kPatch) {
-      if (r.bn > S.cout && r.bn > 32) continue;
+      if ((r.bn > S.cout && r.bn > 32) || r.bn == 128) continue;  // 128: the fused pair's shape
       // One-slot rings only for single-chunk layers (c_in = 32), where they
       // are measured fastest (several workgroups per CU overlap their loads);
       // among them the model below picks (12x16 blocks on YOLOv2's layer 2
@@ -225,10 +225,54 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
   return tune_override(S, c);
 }
 
+namespace {
+
+// A bf16 3x3 stage with 128 outputs (c_in a multiple of 32, no pool)
+// followed by a 1x1 stage 128 -> 64 (no pool) that computes the same
+// rectangles (YOLOv2's layers 4 and 5): the pair runs as one kernel, the
+// 1x1 GEMM taking the 3x3 block's outputs from LDS (one output pass and
+// one kernel boundary less).
+bool fused_pair(const mafat_plan& P, const Group& G, int s, int dtype) {
+  if (dtype != MAFAT_BF16 || s < 0 || s + 1 >= static_cast<int>(G.stages.size())) return false;
+  const Stage& A = G.stages[s];
+  const Stage& B = G.stages[s + 1];
+  if (A.kind != STAGE_CONV || B.kind != STAGE_CONV) return false;
+  if (A.f != 3 || A.p != 1 || A.pool || A.cin % 32 != 0 || A.cout != 128) return false;
+  if (B.f != 1 || B.p != 0 || B.pool || B.cin != 128 || B.cout != 64) return false;
+  if (!mfma_ok(A, dtype) || A.tiles.size() != B.tiles.size()) return false;
+  for (size_t t = 0; t < A.tiles.size(); ++t) {
+    const TileGeom& a = A.tiles[t];
+    const TileGeom& b = B.tiles[t];
+    if (a.cy0 != b.cy0 || a.cx0 != b.cx0 || a.ch != b.ch || a.cw != b.cw) return false;
+  }
+  // 32-bit byte offsets within a frame's source buffer
+  const auto& din = P.dims[G.l0];
+  const int64_t src_frame = (A.src_buf == BUF_GROUP_IO) ? static_cast<int64_t>(din[0]) * din[1] * din[2]
+                                                        : G.scratch_frame;
+  return src_frame * 2 < (1ll << 31);
+}
+
+}  // namespace
+
 StageConfig stage_config(const mafat_plan& P, const Group& G, const Stage& S, int batch, int dtype) {
+  const int si = static_cast<int>(&S - G.stages.data());
+  if (fused_pair(P, G, si, dtype)) {
+    // 8x16 blocks of all 128 channels, one ring slot (the weights of a
+    // 32-channel chunk take 72 KiB): on YOLOv2's layer 4 at 608x608 with
+    // 5x5 tiles one workgroup per CU, in one round.
+    StageConfig c{};
+    c.kind = K_CONV_PATCH;
+    c.br = 8; c.bc = 16; c.bm = 128; c.bn = 128; c.wgm = 4; c.wgn = 2; c.depth = 1; c.kg = 1; c.kord = 1;
+    int64_t mb = 0;
+    for (const TileGeom& T : S.tiles) mb += static_cast<int64_t>((T.ch + 7) / 8) * ((T.cw + 15) / 16);
+    c.blocks = mb;
+    c.fuse = 1;
+    return c;
+  }
   // A plan with packed weights fixes the layout for every batch: its
   // stages take the configuration chosen for one frame.
   StageConfig c = choose_config(S, P.packed_weights ? 1 : batch, dtype);
+  if (fused_pair(P, G, si - 1, dtype)) c.fuse = -1;
   // The matrix-core kernels address a frame's source buffer with 32-bit
   // byte offsets; the generic kernel covers larger frames.
   const int64_t esz = (dtype == MAFAT_F32) ? 4 : 2;
@@ -305,26 +349,51 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         return fail(MAFAT_EINVAL, "layer " + std::to_string(l) + ": weights, scale or bias not 16-byte aligned");
     }
 
+  // A fused pair never writes the buffer it reads: inside a group its
+  // input and output would be the same ping-pong scratch buffer (stages
+  // s - 1 and s + 1), which other workgroups may still be reading, so the
+  // pair writes stage s's buffer instead and the later stages of this call
+  // run with the two scratch buffers swapped.
+  bool swapped = false;
+  const int64_t bstride = G.reuse ? G.scratch_elems : static_cast<int64_t>(G.ntiles) * G.scratch_elems;
+  auto eff = [&](int buf) { return (swapped && buf >= 0) ? 1 - buf : buf; };
   for (int s = s_begin; s < s_end; ++s) {
     const Stage& S = G.stages[s];
     hipEvent_t ev_start = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin)]) : nullptr;
     hipEvent_t ev_stop = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin) + 1]) : nullptr;
     bool launched = false;
     const StageConfig cfg = stage_config(*plan, G, S, batch, dtype);
+    // Both stages of a fused pair in this call: one kernel for the two
+    // (the second stage's interval is recorded empty, after it).
+    const bool fuse = cfg.fuse == 1 && s + 1 < s_end;
+    const Stage* S2 = fuse ? &G.stages[s + 1] : nullptr;
     const int kind = cfg.kind;
     const bool matrix = (kind == K_CONV_MFMA || kind == K_CONV_RING || kind == K_CONV_PATCH);
     const MfmaShape shape{cfg.bm, cfg.bn, cfg.depth, cfg.kg, cfg.wgm, cfg.wgn, cfg.kord, cfg.br, cfg.bc};
     const int bu = (kind == K_CONV_RGB) ? 256 / (S.cout / 8) : block_units(kind, shape);
     StageArgs A;
     std::memset(&A, 0, sizeof(A));
-    A.src = (S.src_buf == BUF_GROUP_IO) ? x : ws;
-    A.dst = (S.dst_buf == BUF_GROUP_IO) ? y : ws;
-    A.src_fstride = (S.src_buf == BUF_GROUP_IO) ? in_frame : scr_frame;
-    A.dst_fstride = (S.dst_buf == BUF_GROUP_IO) ? out_frame : scr_frame;
+    const Stage& SD = fuse ? *S2 : S;  // the stage whose output this launch writes
+    const int src_b = eff(S.src_buf);
+    int dst_b = eff(SD.dst_buf);
+    if (fuse && dst_b >= 0 && dst_b == src_b) dst_b = eff(S.dst_buf);
+    const int64_t src_shift = (S.src_buf >= 0) ? (src_b - S.src_buf) * bstride : 0;
+    const int64_t dst_shift = (SD.dst_buf >= 0) ? (dst_b - SD.dst_buf) * bstride : 0;
+    A.src = (src_b == BUF_GROUP_IO) ? x : ws;
+    A.dst = (dst_b == BUF_GROUP_IO) ? y : ws;
+    A.src_fstride = (src_b == BUF_GROUP_IO) ? in_frame : scr_frame;
+    A.dst_fstride = (dst_b == BUF_GROUP_IO) ? out_frame : scr_frame;
     if (S.kind == STAGE_CONV) {
       A.w = w[S.first];
       A.scale = scale[S.first];
       A.bias = bias[S.first];
+    }
+    if (fuse) {
+      A.w2 = w[S2->first];
+      A.scale2 = scale[S2->first];
+      A.bias2 = bias[S2->first];
+      A.cout2 = S2->cout;
+      A.act2 = S2->act;
     }
     A.in_h = S.in_h; A.in_w = S.in_w;
     A.cin = S.cin; A.cout = S.cout;
@@ -344,10 +413,11 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         k.ch = static_cast<int16_t>(T.ch);   k.cw = static_cast<int16_t>(T.cw);
         k.sy0 = static_cast<int16_t>(T.sy0); k.sx0 = static_cast<int16_t>(T.sx0);
         k.sw = static_cast<int16_t>(T.sw);
-        k.dy0 = static_cast<int16_t>(T.dy0); k.dx0 = static_cast<int16_t>(T.dx0);
-        k.dw = static_cast<int16_t>(T.dw);
-        k.src_off = static_cast<int32_t>(T.src_off);
-        k.dst_off = static_cast<int32_t>(T.dst_off);
+        const TileGeom& TD = SD.tiles[t];
+        k.dy0 = static_cast<int16_t>(TD.dy0); k.dx0 = static_cast<int16_t>(TD.dx0);
+        k.dw = static_cast<int16_t>(TD.dw);
+        k.src_off = static_cast<int32_t>(T.src_off + src_shift);
+        k.dst_off = static_cast<int32_t>(TD.dst_off + dst_shift);
         int64_t units = static_cast<int64_t>(T.ch) * T.cw;
         if ((kind == K_CONV_DIRECT || kind == K_CONV_RGB) && S.pool) units /= 4;
         if (kind == K_CONV_RGB_MFMA)  // 2-D blocks of conv outputs
@@ -370,6 +440,8 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         e = hipSuccess;
       } else if (kind == K_CONV_RING) {
         e = launch_conv_ring(S.f, S.pool, shape, A, stream, lev);
+      } else if (fuse) {
+        e = launch_conv_patch_fused(A, stream, lev);
       } else if (kind == K_CONV_PATCH) {
         e = launch_conv_patch(S.pool, shape, A, stream, lev);
       } else {
@@ -440,6 +512,15 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         std::fprintf(stderr, "  start spread wg-last minus wg0: %lld ns\n", (tr[1][0] - tr[0][0]) * 10);
       }
 #endif
+    }
+    if (dst_b != eff(SD.dst_buf)) swapped = !swapped;
+    if (fuse) {
+      ++s;
+      if (events) {
+        for (int k = 0; k < 2; ++k)
+          if (hipEventRecord(static_cast<hipEvent_t>(events[2 * (s - s_begin) + k]), stream) != hipSuccess)
+            return fail(MAFAT_EHIP, "hipEventRecord failed");
+      }
     }
   }
   return MAFAT_OK;

@@ -288,3 +288,64 @@ def test_packed_weights_parity(orc):
     out = y.float().cpu().numpy().astype(np.float64)
     ref = orc.forward_layers(layers, h, w, c, p["x"], p)
     assert normwise_err(out, ref) <= TOL["bf16"]
+
+
+# A 3x3 conv with 128 outputs followed by a 1x1 conv 128 -> 64 (YOLOv2's
+# layers 4-5): the runtime runs the pair as one kernel in bf16.
+FUSED_PAIR = [W.conv(128), W.conv(64, 1)]
+
+
+@pytest.mark.parametrize("reuse,packed,act2", [(False, False, W.LEAKY), (True, False, W.LEAKY),
+                                                (False, True, W.LINEAR), (True, True, W.LEAKY)])
+def test_fused_pair_parity(orc, reuse, packed, act2):
+    # ragged extents (blocks of 16x16 past the tile edges), 2x3 tiles, batch 2
+    from paper_2107_06960_amd import mafat as M
+    import torch
+    layers = [W.conv(128), W.conv(64, 1, act2)]
+    h, w, c = 45, 61, 64
+    print(f"[parity] fused pair {h}x{w}x{c} reuse={reuse} packed={packed} act2={act2}", flush=True)
+    p = W.make_inputs(layers, h, w, c, 2, 21, "bf16")
+    plan = M.Plan(layers, (h, w, c), "2x3/NoCut", reuse=reuse, packed_weights=packed)
+    net = M.Network(plan, p, 2, "bf16")
+    net.y.fill_(float("nan"))
+    y = net.run(net.input_tensor(p["x"]))
+    torch.cuda.synchronize()
+    out = y.float().cpu().numpy().astype(np.float64)
+    ref = orc.forward_layers(layers, h, w, c, p["x"], p)
+    err = normwise_err(out, ref)
+    assert err <= TOL["bf16"], err
+
+
+# The pair inside a group (scratch buffers on both sides), several rounds
+# of workgroups: the fused kernel must not write the buffer it reads.
+FUSED_MID = [W.conv(64), W.conv(128), W.conv(64, 1), W.conv(32)]
+
+
+@pytest.mark.parametrize("layers,h,w,c,batch,tiling,reuse", [
+    (FUSED_PAIR, 50, 39, 64, 1, "3x2/NoCut", False),
+    (FUSED_MID, 120, 136, 32, 6, "2x2/NoCut", False),
+    (FUSED_MID, 120, 136, 32, 6, "2x2/NoCut", True),
+])
+def test_fused_pair_equals_separate_stages(orc, layers, h, w, c, batch, tiling, reuse):
+    # the fused kernel == its two stages run one by one (the 3x3 stage's
+    # bf16 outputs through memory, then the 1x1 kernel), bit for bit: the
+    # same roundings and the same accumulation order over the 128 channels
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    print(f"[parity] fused pair vs separate stages {h}x{w}x{c} batch={batch} {tiling} reuse={reuse}", flush=True)
+    p = W.make_inputs(layers, h, w, c, batch, 22, "bf16")
+    plan = M.Plan(layers, (h, w, c), tiling, reuse=reuse)
+    net = M.Network(plan, p, batch, "bf16")
+    x = net.input_tensor(p["x"])
+    ref = net.run(x).clone()
+    net.y.zero_()
+    gin, gout = net.group_io(0, x)
+    for s in range(len(plan.stages(0))):
+        net.run_stage(0, s, gin, gout)
+    torch.cuda.synchronize()
+    d = (net.y.float() - ref.float()).abs().max().item()
+    assert torch.equal(net.y.view(torch.int16), ref.view(torch.int16)), d
+    out = ref.float().cpu().numpy().astype(np.float64)
+    for f in (0, batch - 1):
+        e = normwise_err(out[f], orc.forward_layers(layers, h, w, c, p["x"][f:f + 1], p)[0])
+        assert e <= TOL["bf16"], (f, e)
