@@ -131,9 +131,15 @@ void conv_patch_kernel(const StageArgs a) {
   static_assert(BR * BC <= BM && BM % (16 * WGM) == 0, "block rows");
   static_assert(!POOL || (BR % 2 == 0 && BC % 2 == 0), "pooled blocks cover whole windows");
   static_assert(NS >= 1 && NS <= 6 && (NS - 2) * LPS <= 63, "ring depth");
-  // Fused 1x1 weights (N2 > 0): their own LDS region past the ring.
+  // Fused variant (N2 > 0): the 1x1 weights in their own LDS region past
+  // the ring, then a second region Y for the second chunk's patch and the
+  // weights of its first YT taps (instruction k of a chunk's weight part is
+  // tap k here), loaded while the first chunk is computed.
   constexpr int W2D = NS * SLOT + (SINK ? 1024 : 0);
-  __shared__ __align__(1024) unsigned char smem[W2D + (N2 > 0 ? N2 * BN * 2 : 0)];
+  constexpr int YT = 5;
+  constexpr int YOFF = W2D + N2 * BN * 2;
+  static_assert(N2 == 0 || (NS == 1 && NBW == 9 && NB == 9 * NWAVE), "fused variant: one slot, a tap per instruction");
+  __shared__ __align__(1024) unsigned char smem[YOFF + (N2 > 0 ? A_BYTES + YT * BN * 64 : 0)];
   static_assert(N2 == 0 || (!POOL && BM == BR * BC && N2 % 16 == 0 && BN % 32 == 0),
                 "fused 1x1: no pool, no padding rows");
   // Fused 1x1: its weights ([N2][BN] bf16) go straight to LDS now (rows of
@@ -361,7 +367,85 @@ void conv_patch_kernel(const StageArgs a) {
     }
   };
 
-  if constexpr (NS == 1) {
+  if constexpr (N2 > 0) {
+    if (nstage == 2) {
+      // Two chunks, the second one's loads overlapped with compute: its
+      // patch and first YT taps go to Y at once, its last taps to the
+      // slot once the first chunk is done with it.
+      auto frags2 = [&](const unsigned char* spa, const unsigned char* spb, int t, u32x4 (&af)[MT],
+                        u32x4 (&bfr)[NT]) {
+        const int ty = t / 3, tx = t % 3;
+#pragma unroll
+        for (int i = 0; i < MT; ++i)
+          af[i] = *reinterpret_cast<const u32x4*>(spa + pb[i] + (ty * PC + tx) * 64 +
+                                                  (((kx3[i][tx] ^ ky3[i][ty]) & 3) << 4));
+#pragma unroll
+        for (int j = 0; j < NT; ++j)
+          bfr[j] = *reinterpret_cast<const u32x4*>(spb + b_lane + (t * BN + j * 16) * 64);
+      };
+      auto taps = [&](const unsigned char* spa, const unsigned char* spb, auto t0c, auto t1c) {
+        constexpr int T0 = decltype(t0c)::value, T1 = decltype(t1c)::value;
+        u32x4 af0[MT], bf0[NT], af1[MT], bf1[NT];
+        frags2(spa, spb, T0, af0, bf0);
+#pragma unroll
+        for (int t = T0; t < T1; t += 2) {
+          if (t + 1 < T1) frags2(spa, spb, t + 1, af1, bf1);
+          __builtin_amdgcn_sched_barrier(0);
+          mfmas(af0, bf0);
+          __builtin_amdgcn_sched_barrier(0);
+          if (t + 1 < T1) {
+            if (t + 2 < T1) frags2(spa, spb, t + 2, af0, bf0);
+            __builtin_amdgcn_sched_barrier(0);
+            mfmas(af1, bf1);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+      };
+      auto issue_b_taps = [&](unsigned char* sl, auto k0c, auto k1c) {
+#pragma unroll
+        for (int k = decltype(k0c)::value; k < decltype(k1c)::value; ++k)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, (lds_ptr_t)(sl + A_BYTES + (k * NWAVE + wave) * 1024), 16,
+                                                   static_cast<int>(b_off[k] + bstride), 0, 0, 0);
+      };
+      unsigned char* const Y = smem + YOFF;
+      using I0 = std::integral_constant<int, 0>;
+      using IY = std::integral_constant<int, YT>;
+      using I9 = std::integral_constant<int, 9>;
+      issue_a(0, 0);                     // chunk 0's weights are on their way already
+      {                                  // chunk 1: patch and taps [0, YT) to Y
+        const unsigned coff = 64u;
+#pragma unroll
+        for (int k = 0; k < NAW; ++k) {
+          const int g = k * NWAVE + wave;
+          unsigned char* d = (g < NA) ? Y + g * 1024 : smem + NS * SLOT;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, (lds_ptr_t)d, 16, static_cast<int>(a_off[k] + coff), 0, 0, 0);
+        }
+        issue_b_taps(Y, I0{}, IY{});
+      }
+      pwait_vmcnt<NAW + YT>();           // chunk 0 is in
+      pbarrier();
+      MAFAT_PTRACE(8);
+      taps(smem, smem, I0{}, I9{});
+      pbarrier();                        // every wave is done with the slot
+      issue_b_taps(smem, IY{}, I9{});    // chunk 1, taps [YT, 9), to the slot
+      pwait_vmcnt<9 - YT>();             // chunk 1's patch and first taps are in
+      pbarrier();
+      MAFAT_PTRACE(9);
+      taps(Y, Y, I0{}, IY{});
+      pwait_vmcnt<0>();
+      pbarrier();
+      MAFAT_PTRACE(10);
+      taps(Y, smem, IY{}, I9{});
+    } else {
+      for (int s = 0; s < nstage; ++s) {
+        if (s > 0) pbarrier();
+        issue(s, 0);
+        pwait_vmcnt<0>();
+        pbarrier();
+        compute(0);
+      }
+    }
+  } else if constexpr (NS == 1) {
     // One slot (half the LDS, so two workgroups fit on a CU and hide each
     // other's load latency): load a chunk, wait, compute, repeat.
     for (int s = 0; s < nstage; ++s) {
