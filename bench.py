@@ -86,10 +86,11 @@ def stage_flops(plan, g):
     return out
 
 
-def stage_bytes(plan, g, esz):
-    """Algorithmic HBM bytes of every stage of group g for one frame: each
-    tile's input region (halo included) read once, the weights (and scale,
-    bias) once, each tile's output rectangle written once."""
+def stage_io_bytes(plan, g, esz):
+    """Algorithmic HBM bytes of every stage of group g for one frame, as
+    (read, written, weights): each tile's input region (halo included) read
+    once, each tile's output rectangle written once, the weights (and
+    scale, bias) once."""
     first, nl, nt = plan.group(g)
     R = plan.regions(g)
     out = []
@@ -100,8 +101,15 @@ def stage_bytes(plan, g, esz):
         wr = sum(int(R[t, kb, 5] - R[t, kb, 4]) * int(R[t, kb, 7] - R[t, kb, 6]) for t in range(nt)) * db[5] * esz
         L = plan.layers[a]
         w = (da[5] * L["f"] * L["f"] * da[2] * esz + 8 * da[5]) if L["op"] == "conv" else 0
-        out.append(rd + wr + w)
+        out.append((rd, wr, w))
     return out
+
+
+def launch_bytes(io, launch):
+    """Algorithmic bytes of one kernel launch running the stages `launch`
+    (a fused pair keeps its intermediate on chip): the first stage's input,
+    the last stage's output, every stage's weights."""
+    return io[launch[0]][0] + io[launch[-1]][1] + sum(io[s][2] for s in launch)
 
 
 def untiled_groups(layers):
@@ -493,20 +501,21 @@ def main():
 
     flops = [stage_flops(plan, g) for g in range(ng)]
     esz = 2 if wl.dtype == "bf16" else 4
-    sbytes = [stage_bytes(plan, g, esz) for g in range(ng)]
+    sio = [stage_io_bytes(plan, g, esz) for g in range(ng)]
     exec_flops = sum(2 * plan.macs(g)[0] for g in range(ng)) * wl.batch
     useful_flops = sum(2 * plan.macs(g)[1] for g in range(ng)) * wl.batch
     peak = PEAK_TFLOPS[wl.dtype]
-    per_stage = []
+    per_stage = []  # one entry per kernel launch (a fused pair of stages is one)
     for g in range(ng):
-        for s, (a, b) in enumerate(stages[g]):
-            f = flops[g][s] * wl.batch
-            t = stage_ms[g][s]
+        for ln in plan.launches(g, wl.batch, wl.dtype):
+            a, b = stages[g][ln[0]][0], stages[g][ln[-1]][1]
+            f = sum(flops[g][s] for s in ln) * wl.batch
+            t = stage_ms[g][ln[0]]  # a fused pair's kernel: the first stage's events
             # the 3-channel first layer runs on the vector ALUs in fp32 (on
             # the matrix cores in bf16), the rest on the matrix cores
             vec = plan.layers[a]["op"] == "conv" and plan.shape(a)[2] == 3 and wl.dtype == "f32"
             pk, bound = (PEAK_VALU_TFLOPS, "alu") if vec else (peak, "mfma")
-            nb = sbytes[g][s] * wl.batch
+            nb = launch_bytes(sio[g], ln) * wl.batch
             per_stage.append({"group": g, "layers": [a, b], "ms": round(t, 5),
                               "gflop": round(f / 1e9, 4), "bound": bound, "peak_tflops": pk,
                               "tflops": round(f / (t * 1e-3) / 1e12, 2) if t > 0 else None,

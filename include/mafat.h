@@ -191,6 +191,18 @@ int mafat_plan_stages(const mafat_plan* plan, int32_t group, int32_t* n_stages);
 int mafat_plan_stage_layers(const mafat_plan* plan, int32_t group, int32_t stage,
                             int32_t* first_layer, int32_t* last_layer);
 
+/* *fused = 1 if mafat_run_group / mafat_run_network run stage `stage` of
+ * group g together with stage + 1 in one kernel for this batch and dtype,
+ * else 0.  This is the case for a bfloat16 3x3 convolution with 128
+ * outputs and no pool whose next stage is a 1x1 convolution 128 -> 64 over
+ * the same rectangles (YOLOv2's layers 4-5): the 1x1 GEMM runs on the 3x3
+ * outputs held in LDS, so the intermediate never goes to memory (the layer
+ * fusion inside a tile of the paper's fused tile partitioning, Sec. 3,
+ * taken down to a workgroup's block).  mafat_run_stage always runs one
+ * stage.  Errors: EINVAL (NULL, index out of range), EUNSUPPORTED (dtype). */
+int mafat_plan_stage_fused(const mafat_plan* plan, int32_t group, int32_t stage, int32_t batch,
+                           int32_t dtype, int32_t* fused);
+
 /* Bytes of device workspace mafat_run_group / mafat_run_network need for
  * `batch` frames in `dtype` (0 if none).  It holds the tiles' intermediate
  * activations between stages; the largest group decides.  Errors: EINVAL. */
@@ -211,7 +223,9 @@ int mafat_workspace_size(const mafat_plan* plan, int32_t batch, int32_t dtype,
  *              the first kernel of stage s starts and events[2s+1] when its
  *              last kernel ends (timestamps of the kernel dispatches
  *              themselves, so timing adds nothing between kernels); entries
- *              may be NULL
+ *              may be NULL.  For a fused pair (mafat_plan_stage_fused) the
+ *              first stage's events enclose the pair's kernel; the second
+ *              stage's two events are recorded after it and time nothing
  * x and y must not overlap.  Errors: EINVAL, EUNSUPPORTED (dtype),
  * EWORKSPACE, EHIP. */
 int mafat_run_group(const mafat_plan* plan, int32_t group, int32_t batch, int32_t dtype,

@@ -517,9 +517,10 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
     if (fuse) {
       ++s;
       if (events) {
-        for (int k = 0; k < 2; ++k)
-          if (hipEventRecord(static_cast<hipEvent_t>(events[2 * (s - s_begin) + k]), stream) != hipSuccess)
-            return fail(MAFAT_EHIP, "hipEventRecord failed");
+        for (int k = 0; k < 2; ++k) {
+          hipEvent_t e2 = static_cast<hipEvent_t>(events[2 * (s - s_begin) + k]);
+          if (e2 && hipEventRecord(e2, stream) != hipSuccess) return fail(MAFAT_EHIP, "hipEventRecord failed");
+        }
       }
     }
   }
@@ -586,6 +587,27 @@ extern "C" int mafat_run_network(const mafat_plan* plan, int32_t batch, int32_t 
                         static_cast<hipStream_t>(stream), nullptr);
     if (rc != MAFAT_OK) return rc;
   }
+  return MAFAT_OK;
+}
+
+extern "C" int mafat_plan_stage_fused(const mafat_plan* plan, int32_t group, int32_t stage, int32_t batch,
+                                      int32_t dtype, int32_t* fused) {
+  clear_error();
+  if (!plan || !fused || group < 0 || group >= static_cast<int>(plan->groups.size()) || batch < 1) {
+    set_error("plan and fused must be non-NULL, the group in range and batch >= 1");
+    return MAFAT_EINVAL;
+  }
+  const Group& G = plan->groups[group];
+  if (stage < 0 || stage >= static_cast<int>(G.stages.size())) {
+    set_error("stage out of range");
+    return MAFAT_EINVAL;
+  }
+  if (dtype != MAFAT_F32 && dtype != MAFAT_BF16) {
+    set_error("dtype must be F32 or BF16");
+    return MAFAT_EUNSUPPORTED;
+  }
+  *fused = (stage + 1 < static_cast<int>(G.stages.size()) &&
+            stage_config(*plan, G, G.stages[stage], batch, dtype).fuse == 1) ? 1 : 0;
   return MAFAT_OK;
 }
 

@@ -35,6 +35,7 @@ DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
 EXPORTS = ("mafat_plan_create", "mafat_plan_create_flags", "mafat_plan_destroy",
            "mafat_packed_weights_size", "mafat_pack_weights", "mafat_plan_layer_shape", "mafat_plan_group",
            "mafat_plan_regions", "mafat_plan_macs", "mafat_plan_stages", "mafat_plan_stage_layers",
+           "mafat_plan_stage_fused",
            "mafat_workspace_size", "mafat_run_group", "mafat_run_stage", "mafat_run_network",
            "mafat_predict_mem", "mafat_get_config", "mafat_status_string", "mafat_last_error")
 
@@ -86,6 +87,7 @@ def lib():
         L.mafat_plan_macs.argtypes = [planp, i32, ctypes.POINTER(i64), ctypes.POINTER(i64)]
         L.mafat_plan_stages.argtypes = [planp, i32, i32p]
         L.mafat_plan_stage_layers.argtypes = [planp, i32, i32, i32p, i32p]
+        L.mafat_plan_stage_fused.argtypes = [planp, i32, i32, i32, i32, i32p]
         L.mafat_workspace_size.argtypes = [planp, i32, i32, ctypes.POINTER(sz)]
         L.mafat_run_group.argtypes = [planp, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp, vpp]
         L.mafat_run_stage.argtypes = [planp, i32, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp]
@@ -201,6 +203,13 @@ def mafat_plan_stages(plan, group):
     return out
 
 
+def mafat_plan_stage_fused(plan, group, stage, batch, dtype):
+    f = ctypes.c_int32()
+    _check("mafat_plan_stage_fused", lib().mafat_plan_stage_fused(plan, group, stage, batch, DTYPES.get(dtype, dtype),
+                                                                  ctypes.byref(f)))
+    return bool(f.value)
+
+
 def mafat_workspace_size(plan, batch, dtype):
     n = ctypes.c_size_t()
     _check("mafat_workspace_size", lib().mafat_workspace_size(plan, batch, dtype, ctypes.byref(n)))
@@ -311,6 +320,19 @@ class Plan:
 
     def stages(self, g):
         return mafat_plan_stages(self.handle, g)
+
+    def stage_fused(self, g, s, batch=1, dtype="bf16"):
+        return mafat_plan_stage_fused(self.handle, g, s, batch, dtype)
+
+    def launches(self, g, batch=1, dtype="bf16"):
+        """The kernel launches of mafat_run_group for group g: lists of stage
+        indices (a fused pair is one launch)."""
+        st, out, s = self.stages(g), [], 0
+        while s < len(st):
+            n = 2 if self.stage_fused(g, s, batch, dtype) else 1
+            out.append(list(range(s, s + n)))
+            s += n
+        return out
 
     def predict_mem(self, model="device", batch=1, dtype="bf16"):
         return mafat_predict_mem(self.handle, model, batch, dtype)

@@ -109,6 +109,31 @@ def test_stages_fuse_conv_and_following_pool(lib):
     assert plan.stages(1)[0] == (3, 3)
 
 
+def test_fused_pair_detection(lib):
+    # bf16: layer 4 (3x3, 64 -> 128) runs with layer 5 (1x1, 128 -> 64) in
+    # one kernel, whatever the batch or plan flags; f32 and other shapes not
+    for flags in ({}, {"reuse": True}, {"packed_weights": True}):
+        plan = M.Plan(W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2", **flags)
+        for batch in (1, 8):
+            got = [plan.stage_fused(0, s, batch, "bf16") for s in range(len(plan.stages(0)))]
+            assert got == [False, False, True, False, False], (flags, batch, got)
+            assert plan.launches(0, batch, "bf16") == [[0], [1], [2, 3], [4]]
+            assert not any(plan.stage_fused(1, s, batch, "bf16") for s in range(len(plan.stages(1))))
+        assert not any(plan.stage_fused(0, s, 1, "f32") for s in range(len(plan.stages(0))))
+    # a cut between layers 4 and 5 separates them
+    plan = M.Plan(W.YOLOV2_16, (608, 608, 3), "3x3/5/2x2")
+    assert plan.stages(0)[-1] == (4, 4) and not plan.stage_fused(0, len(plan.stages(0)) - 1, 1, "bf16")
+    # other channel counts, a pool after the 3x3, or a 3x3 second layer: no
+    for layers in ([W.conv(96), W.conv(64, 1)], [W.conv(128), W.conv(32, 1)],
+                   [W.conv(128), W.maxpool(), W.conv(64, 1)], [W.conv(128), W.conv(64)]):
+        plan = M.Plan(layers, (32, 32, 64), "2x2/NoCut")
+        assert not plan.stage_fused(0, 0, 1, "bf16"), layers
+    plan = M.Plan([W.conv(128), W.conv(64, 1, W.LINEAR)], (32, 32, 64), "2x2/NoCut")
+    assert plan.stage_fused(0, 0, 1, "bf16") and not plan.stage_fused(0, 1, 1, "bf16")
+    with pytest.raises(M.MafatError):
+        plan.stage_fused(0, 2, 1, "bf16")
+
+
 def test_workspace_size(lib):
     plan = M.Plan(W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2")
     b1 = plan.workspace_size(1, "bf16")

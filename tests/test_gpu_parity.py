@@ -349,3 +349,42 @@ def test_fused_pair_equals_separate_stages(orc, layers, h, w, c, batch, tiling, 
     for f in (0, batch - 1):
         e = normwise_err(out[f], orc.forward_layers(layers, h, w, c, p["x"][f:f + 1], p)[0])
         assert e <= TOL["bf16"], (f, e)
+
+
+@pytest.mark.parametrize("which", ["all", "ends"])
+def test_run_group_events(which):
+    # per-stage events (all entries) and group events (first and last only,
+    # the rest NULL) around a group with a fused pair: the run succeeds, the
+    # output is unchanged, the intervals are ordered
+    import sys
+    import os
+    import torch
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    from bench import HipEvents
+    from paper_2107_06960_amd import mafat as M
+    print(f"[parity] run_group events={which}", flush=True)
+    p = W.make_inputs(W.YOLOV2_16, 96, 96, 3, 1, 9, "bf16")
+    plan = M.Plan(W.YOLOV2_16, (96, 96, 3), "3x3/8/2x2", packed_weights=True)
+    assert plan.launches(0) == [[0], [1], [2, 3], [4]]
+    net = M.Network(plan, p, 1, "bf16")
+    x = net.input_tensor(p["x"])
+    ref = net.run(x).clone()
+    ev = HipEvents()
+    n = len(plan.stages(0))
+    evs = ev.create(2 * n)
+    lst = list(evs) if which == "all" else [evs[0]] + [None] * (2 * n - 2) + [evs[-1]]
+    gin, gout = net.group_io(0, x)
+    net.run_group(0, gin, gout, events=lst)
+    for g in range(1, plan.n_groups):
+        a, b = net.group_io(g, x)
+        net.run_group(g, a, b)
+    torch.cuda.synchronize()
+    assert torch.equal(net.y, ref)
+    assert ev.ms(evs[0], evs[-1]) > 0
+    if which == "all":
+        for s in range(n):
+            assert ev.ms(evs[2 * s], evs[2 * s + 1]) >= 0
+            if s + 1 < n:
+                assert ev.ms(evs[2 * s + 1], evs[2 * s + 2]) >= 0
+        assert ev.ms(evs[4], evs[5]) > 0  # the fused pair's kernel
+    ev.destroy(evs)
