@@ -122,13 +122,14 @@ def untiled_groups(layers):
     return starts, [1] * len(starts), [1] * len(starts)
 
 
-def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs=2, reuse=False, packed=False):
+def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs=2, reuse=False, packed=False,
+                        tile_batch=0):
     import torch
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     torch.cuda.reset_peak_memory_stats()
     base = torch.cuda.memory_allocated()
-    plan = M.Plan(layers, hwc, tiling, reuse=reuse, packed_weights=packed)
+    plan = M.Plan(layers, hwc, tiling, reuse=reuse, packed_weights=packed, tile_batch=tile_batch)
     net = M.Network(plan, params, batch, dtype)
     x = net.input_tensor(x_np)
     torch.cuda.synchronize()
@@ -572,6 +573,13 @@ def main():
         res["peak_mem_mib"] = round(tp / 2 ** 20, 2)
         res["untiled_peak_mem_mib"] = round(up / 2 ** 20, 2)
         res["untiled_ms_per_step"] = round(ums, 5)
+        if not args.no_extras:
+            # The paper's execution order: one tile at a time through its
+            # group (mafat_plan_set_tile_batch(plan, 1)): less workspace,
+            # many more launches.
+            sp, sms = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch,
+                                          wl.dtype, params["x"], packed=True, tile_batch=1)
+            res["tiles_in_sequence"] = {"peak_mem_mib": round(sp / 2 ** 20, 2), "ms_per_step": round(sms, 5)}
 
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, params, sum(plan.macs(g)[0] for g in range(ng)))

@@ -140,6 +140,21 @@ int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_layers, int32_t
                             int32_t n_groups, const int32_t* grid_rows,
                             const int32_t* grid_cols, int32_t flags, mafat_plan** out);
 
+/* Tile batches: run at most `tiles` tiles of a group at a time (0: all
+ * tiles at once, the default).  mafat_run_group / mafat_run_network then
+ * take the group's tiles in row-major batches of `tiles`, each batch through
+ * all of the group's stages before the next, and the workspace holds one
+ * batch's intermediates instead of every tile's.  With tiles = 1 this is
+ * the paper's execution order (tiles one after another, Sec. 4), whose peak
+ * memory falls with finer grids; on the GPU a batch must still fill the
+ * device to run fast.  Results are bit-identical to the default.  Call
+ * before sizing the workspace; mafat_run_stage then fails (EUNSUPPORTED)
+ * for groups split into several batches, and the per-stage events of
+ * mafat_run_group enclose the stage's first to last launch (other stages'
+ * launches in between).  Errors: EINVAL (NULL, tiles < 0), EUNSUPPORTED
+ * (a plan with MAFAT_PLAN_TILE_REUSE and 0 < tiles < a group's tile count). */
+int mafat_plan_set_tile_batch(mafat_plan* plan, int32_t tiles);
+
 /* Bytes of the packed weights of conv layer `layer` in `dtype` (device
  * buffer, 16-byte aligned, caller-owned); 0 when the layer's weights are
  * passed as KRSC (plan without MAFAT_PLAN_PACKED_WEIGHTS, f32, 1x1 or

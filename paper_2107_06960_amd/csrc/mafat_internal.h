@@ -57,6 +57,8 @@ struct Group {
   int nbufs;              // scratch buffers (0, 1 or 2)
   int64_t scratch_frame;  // scratch elements of one frame
   bool reuse;             // tile reuse: every stage output computed once (full tensors)
+  int tile_batch;         // tiles run through the stages together (ntiles unless
+                          // mafat_plan_set_tile_batch set fewer); scratch per batch
   int64_t macs_exec, macs_untiled;
 };
 

@@ -153,6 +153,7 @@ int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool reuse
     // Scratch of one frame: [buffer][full stage output], 256-byte aligned.
     G.scratch_elems = (G.scratch_elems + 127) / 128 * 128;
     G.scratch_frame = static_cast<int64_t>(G.nbufs) * G.scratch_elems;
+    G.tile_batch = G.ntiles;
     for (Stage& S : G.stages)
       for (TileGeom& T : S.tiles) {
         if (S.src_buf != BUF_GROUP_IO) T.src_off *= G.scratch_elems;
@@ -201,6 +202,7 @@ int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool reuse
   // tile's buffer starts on a 256-byte boundary for both dtypes.
   G.scratch_elems = (G.scratch_elems + 127) / 128 * 128;
   G.scratch_frame = static_cast<int64_t>(G.nbufs) * G.ntiles * G.scratch_elems;
+  G.tile_batch = G.ntiles;
   for (Stage& S : G.stages)
     for (TileGeom& T : S.tiles) {
       if (S.src_buf != BUF_GROUP_IO) T.src_off *= G.scratch_elems;
@@ -208,6 +210,21 @@ int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool reuse
     }
   *out = std::move(G);
   return MAFAT_OK;
+}
+
+// Tile batches of K tiles (fused tile partitioning without tile reuse):
+// tile t's intermediates live in slot t mod K of each scratch buffer, so
+// the workspace holds K tiles ([buffer][slot][scratch_elems] per frame).
+void set_tile_batch(Group& G, int K) {
+  G.tile_batch = K;
+  G.scratch_frame = static_cast<int64_t>(G.nbufs) * K * G.scratch_elems;
+  for (Stage& S : G.stages)
+    for (int t = 0; t < G.ntiles; ++t) {
+      TileGeom& T = S.tiles[static_cast<size_t>(t)];
+      const int64_t slot = t % K;
+      if (S.src_buf != BUF_GROUP_IO) T.src_off = (S.src_buf * static_cast<int64_t>(K) + slot) * G.scratch_elems;
+      if (S.dst_buf != BUF_GROUP_IO) T.dst_off = (S.dst_buf * static_cast<int64_t>(K) + slot) * G.scratch_elems;
+    }
 }
 
 }  // namespace
@@ -350,6 +367,22 @@ extern "C" int mafat_plan_stage_layers(const mafat_plan* plan, int32_t group, in
   if (stage < 0 || stage >= static_cast<int>(G.stages.size())) return MAFAT_EINVAL;
   if (first_layer) *first_layer = G.stages[stage].first;
   if (last_layer) *last_layer = G.stages[stage].last;
+  return MAFAT_OK;
+}
+
+extern "C" int mafat_plan_set_tile_batch(mafat_plan* plan, int32_t tiles) {
+  clear_error();
+  if (!plan || tiles < 0) {
+    set_error("plan must be non-NULL and tiles >= 0");
+    return MAFAT_EINVAL;
+  }
+  for (const Group& G : plan->groups)
+    if (G.reuse && tiles > 0 && tiles < G.ntiles) {
+      set_error("tile reuse needs every tile of a stage before the next stage: no tile batches");
+      return MAFAT_EUNSUPPORTED;
+    }
+  for (Group& G : plan->groups)
+    if (!G.reuse) set_tile_batch(G, (tiles == 0) ? G.ntiles : std::min<int>(tiles, G.ntiles));
   return MAFAT_OK;
 }
 

@@ -349,177 +349,186 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         return fail(MAFAT_EINVAL, "layer " + std::to_string(l) + ": weights, scale or bias not 16-byte aligned");
     }
 
-  // A fused pair never writes the buffer it reads: inside a group its
-  // input and output would be the same ping-pong scratch buffer (stages
-  // s - 1 and s + 1), which other workgroups may still be reading, so the
-  // pair writes stage s's buffer instead and the later stages of this call
-  // run with the two scratch buffers swapped.
-  bool swapped = false;
-  const int64_t bstride = G.reuse ? G.scratch_elems : static_cast<int64_t>(G.ntiles) * G.scratch_elems;
-  auto eff = [&](int buf) { return (swapped && buf >= 0) ? 1 - buf : buf; };
-  for (int s = s_begin; s < s_end; ++s) {
-    const Stage& S = G.stages[s];
-    hipEvent_t ev_start = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin)]) : nullptr;
-    hipEvent_t ev_stop = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin) + 1]) : nullptr;
-    bool launched = false;
-    const StageConfig cfg = stage_config(*plan, G, S, batch, dtype);
-    // Both stages of a fused pair in this call: one kernel for the two
-    // (the second stage's interval is recorded empty, after it).
-    const bool fuse = cfg.fuse == 1 && s + 1 < s_end;
-    const Stage* S2 = fuse ? &G.stages[s + 1] : nullptr;
-    const int kind = cfg.kind;
-    const bool matrix = (kind == K_CONV_MFMA || kind == K_CONV_RING || kind == K_CONV_PATCH);
-    const MfmaShape shape{cfg.bm, cfg.bn, cfg.depth, cfg.kg, cfg.wgm, cfg.wgn, cfg.kord, cfg.br, cfg.bc};
-    const int bu = (kind == K_CONV_RGB) ? 256 / (S.cout / 8) : block_units(kind, shape);
-    StageArgs A;
-    std::memset(&A, 0, sizeof(A));
-    const Stage& SD = fuse ? *S2 : S;  // the stage whose output this launch writes
-    const int src_b = eff(S.src_buf);
-    int dst_b = eff(SD.dst_buf);
-    if (fuse && dst_b >= 0 && dst_b == src_b) dst_b = eff(S.dst_buf);
-    const int64_t src_shift = (S.src_buf >= 0) ? (src_b - S.src_buf) * bstride : 0;
-    const int64_t dst_shift = (SD.dst_buf >= 0) ? (dst_b - SD.dst_buf) * bstride : 0;
-    A.src = (src_b == BUF_GROUP_IO) ? x : ws;
-    A.dst = (dst_b == BUF_GROUP_IO) ? y : ws;
-    A.src_fstride = (src_b == BUF_GROUP_IO) ? in_frame : scr_frame;
-    A.dst_fstride = (dst_b == BUF_GROUP_IO) ? out_frame : scr_frame;
-    if (S.kind == STAGE_CONV) {
-      A.w = w[S.first];
-      A.scale = scale[S.first];
-      A.bias = bias[S.first];
-    }
-    if (fuse) {
-      A.w2 = w[S2->first];
-      A.scale2 = scale[S2->first];
-      A.bias2 = bias[S2->first];
-      A.cout2 = S2->cout;
-      A.act2 = S2->act;
-    }
-    A.in_h = S.in_h; A.in_w = S.in_w;
-    A.cin = S.cin; A.cout = S.cout;
-    A.act = S.act;
-    A.nblk_n = matrix ? (S.cout + shape.bn - 1) / shape.bn : 1;
-    A.chan_major = matrix ? cfg.chan_major : 0;
-    A.w_packed = (plan->packed_weights && kind == K_CONV_PATCH) ? 1 : 0;
-    for (int t0 = 0; t0 < G.ntiles; t0 += kMaxTilesPerLaunch) {
-      const int t1 = std::min(G.ntiles, t0 + kMaxTilesPerLaunch);
-      A.ntiles = t1 - t0;
-      int64_t total = 0;
-      A.mblk_prefix[0] = 0;
-      for (int t = t0; t < t1; ++t) {
-        const TileGeom& T = S.tiles[t];
-        KTile& k = A.tiles[t - t0];
-        k.cy0 = static_cast<int16_t>(T.cy0); k.cx0 = static_cast<int16_t>(T.cx0);
-        k.ch = static_cast<int16_t>(T.ch);   k.cw = static_cast<int16_t>(T.cw);
-        k.sy0 = static_cast<int16_t>(T.sy0); k.sx0 = static_cast<int16_t>(T.sx0);
-        k.sw = static_cast<int16_t>(T.sw);
-        const TileGeom& TD = SD.tiles[t];
-        k.dy0 = static_cast<int16_t>(TD.dy0); k.dx0 = static_cast<int16_t>(TD.dx0);
-        k.dw = static_cast<int16_t>(TD.dw);
-        k.src_off = static_cast<int32_t>(T.src_off + src_shift);
-        k.dst_off = static_cast<int32_t>(TD.dst_off + dst_shift);
-        int64_t units = static_cast<int64_t>(T.ch) * T.cw;
-        if ((kind == K_CONV_DIRECT || kind == K_CONV_RGB) && S.pool) units /= 4;
-        if (kind == K_CONV_RGB_MFMA)  // 2-D blocks of conv outputs
-          total += static_cast<int64_t>((T.ch + kRgbBlockRows - 1) / kRgbBlockRows) *
-                   ((T.cw + kRgbBlockCols - 1) / kRgbBlockCols);
-        else if (kind == K_CONV_PATCH)
-          total += static_cast<int64_t>((T.ch + shape.br - 1) / shape.br) * ((T.cw + shape.bc - 1) / shape.bc);
-        else
-          total += (units + bu - 1) / bu;
-        A.mblk_prefix[t - t0 + 1] = static_cast<int32_t>(total);
+  // Tile batches (mafat_plan_set_tile_batch): tiles [b0, b0 + K) go through
+  // all stages, then the next K tiles; the workspace holds K tiles.
+  const int K = G.tile_batch;
+  const int64_t bstride = G.reuse ? G.scratch_elems : static_cast<int64_t>(K) * G.scratch_elems;
+  std::vector<char> started(static_cast<size_t>(s_end - s_begin), 0);  // start event recorded
+  for (int b0 = 0; b0 < G.ntiles; b0 += K) {
+    const int b1 = std::min(G.ntiles, b0 + K);
+    const bool last_batch = b1 >= G.ntiles;
+    // A fused pair never writes the buffer it reads: inside a group its
+    // input and output would be the same ping-pong scratch buffer (stages
+    // s - 1 and s + 1), which other workgroups may still be reading, so the
+    // pair writes stage s's buffer instead and the later stages of this
+    // batch run with the two scratch buffers swapped.
+    bool swapped = false;
+    auto eff = [&](int buf) { return (swapped && buf >= 0) ? 1 - buf : buf; };
+    for (int s = s_begin; s < s_end; ++s) {
+      const Stage& S = G.stages[s];
+      hipEvent_t ev_start = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin)]) : nullptr;
+      hipEvent_t ev_stop = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin) + 1]) : nullptr;
+      bool launched = started[static_cast<size_t>(s - s_begin)] != 0;
+      const StageConfig cfg = stage_config(*plan, G, S, batch, dtype);
+      // Both stages of a fused pair in this call: one kernel for the two
+      // (the second stage's interval is recorded empty, after it).
+      const bool fuse = cfg.fuse == 1 && s + 1 < s_end;
+      const Stage* S2 = fuse ? &G.stages[s + 1] : nullptr;
+      const int kind = cfg.kind;
+      const bool matrix = (kind == K_CONV_MFMA || kind == K_CONV_RING || kind == K_CONV_PATCH);
+      const MfmaShape shape{cfg.bm, cfg.bn, cfg.depth, cfg.kg, cfg.wgm, cfg.wgn, cfg.kord, cfg.br, cfg.bc};
+      const int bu = (kind == K_CONV_RGB) ? 256 / (S.cout / 8) : block_units(kind, shape);
+      StageArgs A;
+      std::memset(&A, 0, sizeof(A));
+      const Stage& SD = fuse ? *S2 : S;  // the stage whose output this launch writes
+      const int src_b = eff(S.src_buf);
+      int dst_b = eff(SD.dst_buf);
+      if (fuse && dst_b >= 0 && dst_b == src_b) dst_b = eff(S.dst_buf);
+      const int64_t src_shift = (S.src_buf >= 0) ? (src_b - S.src_buf) * bstride : 0;
+      const int64_t dst_shift = (SD.dst_buf >= 0) ? (dst_b - SD.dst_buf) * bstride : 0;
+      A.src = (src_b == BUF_GROUP_IO) ? x : ws;
+      A.dst = (dst_b == BUF_GROUP_IO) ? y : ws;
+      A.src_fstride = (src_b == BUF_GROUP_IO) ? in_frame : scr_frame;
+      A.dst_fstride = (dst_b == BUF_GROUP_IO) ? out_frame : scr_frame;
+      if (S.kind == STAGE_CONV) {
+        A.w = w[S.first];
+        A.scale = scale[S.first];
+        A.bias = bias[S.first];
       }
-      A.mblk_total = static_cast<int32_t>(total);
-      const int64_t blocks = total * A.nblk_n * batch;
-      if (blocks >= (1ll << 31)) return fail(MAFAT_EUNSUPPORTED, "grid too large");
-      A.total_blocks = static_cast<int32_t>(blocks);
-      const bool last_chunk = t1 >= G.ntiles;
-      const LaunchEvents lev{launched ? nullptr : ev_start, last_chunk ? ev_stop : nullptr};
-      hipError_t e;
-      if (A.total_blocks <= 0) {
-        e = hipSuccess;
-      } else if (kind == K_CONV_RING) {
-        e = launch_conv_ring(S.f, S.pool, shape, A, stream, lev);
-      } else if (fuse) {
-        e = launch_conv_patch_fused(A, stream, lev);
-      } else if (kind == K_CONV_PATCH) {
-        e = launch_conv_patch(S.pool, shape, A, stream, lev);
-      } else {
-        e = launch_stage(kind, dtype, S.f, S.pool, shape, A, stream, lev);
+      if (fuse) {
+        A.w2 = w[S2->first];
+        A.scale2 = scale[S2->first];
+        A.bias2 = bias[S2->first];
+        A.cout2 = S2->cout;
+        A.act2 = S2->act;
       }
-      if (A.total_blocks > 0) {
-        launched = true;
-      } else if (last_chunk) {  // nothing launched for the last chunk: close the interval here
-        if ((!launched && ev_start && hipEventRecord(ev_start, stream) != hipSuccess) ||
-            (ev_stop && hipEventRecord(ev_stop, stream) != hipSuccess))
-          return fail(MAFAT_EHIP, "hipEventRecord failed");
-      }
-      if (e != hipSuccess)
-        return fail(MAFAT_EHIP, std::string("stage launch failed: ") + hipGetErrorString(e));
+      A.in_h = S.in_h; A.in_w = S.in_w;
+      A.cin = S.cin; A.cout = S.cout;
+      A.act = S.act;
+      A.nblk_n = matrix ? (S.cout + shape.bn - 1) / shape.bn : 1;
+      A.chan_major = matrix ? cfg.chan_major : 0;
+      A.w_packed = (plan->packed_weights && kind == K_CONV_PATCH) ? 1 : 0;
+      for (int t0 = b0; t0 < b1; t0 += kMaxTilesPerLaunch) {
+        const int t1 = std::min(b1, t0 + kMaxTilesPerLaunch);
+        A.ntiles = t1 - t0;
+        int64_t total = 0;
+        A.mblk_prefix[0] = 0;
+        for (int t = t0; t < t1; ++t) {
+          const TileGeom& T = S.tiles[t];
+          KTile& k = A.tiles[t - t0];
+          k.cy0 = static_cast<int16_t>(T.cy0); k.cx0 = static_cast<int16_t>(T.cx0);
+          k.ch = static_cast<int16_t>(T.ch);   k.cw = static_cast<int16_t>(T.cw);
+          k.sy0 = static_cast<int16_t>(T.sy0); k.sx0 = static_cast<int16_t>(T.sx0);
+          k.sw = static_cast<int16_t>(T.sw);
+          const TileGeom& TD = SD.tiles[t];
+          k.dy0 = static_cast<int16_t>(TD.dy0); k.dx0 = static_cast<int16_t>(TD.dx0);
+          k.dw = static_cast<int16_t>(TD.dw);
+          k.src_off = static_cast<int32_t>(T.src_off + src_shift);
+          k.dst_off = static_cast<int32_t>(TD.dst_off + dst_shift);
+          int64_t units = static_cast<int64_t>(T.ch) * T.cw;
+          if ((kind == K_CONV_DIRECT || kind == K_CONV_RGB) && S.pool) units /= 4;
+          if (kind == K_CONV_RGB_MFMA)  // 2-D blocks of conv outputs
+            total += static_cast<int64_t>((T.ch + kRgbBlockRows - 1) / kRgbBlockRows) *
+                     ((T.cw + kRgbBlockCols - 1) / kRgbBlockCols);
+          else if (kind == K_CONV_PATCH)
+            total += static_cast<int64_t>((T.ch + shape.br - 1) / shape.br) * ((T.cw + shape.bc - 1) / shape.bc);
+          else
+            total += (units + bu - 1) / bu;
+          A.mblk_prefix[t - t0 + 1] = static_cast<int32_t>(total);
+        }
+        A.mblk_total = static_cast<int32_t>(total);
+        const int64_t blocks = total * A.nblk_n * batch;
+        if (blocks >= (1ll << 31)) return fail(MAFAT_EUNSUPPORTED, "grid too large");
+        A.total_blocks = static_cast<int32_t>(blocks);
+        const bool last_chunk = last_batch && t1 >= b1;
+        const LaunchEvents lev{launched ? nullptr : ev_start, last_chunk ? ev_stop : nullptr};
+        hipError_t e;
+        if (A.total_blocks <= 0) {
+          e = hipSuccess;
+        } else if (kind == K_CONV_RING) {
+          e = launch_conv_ring(S.f, S.pool, shape, A, stream, lev);
+        } else if (fuse) {
+          e = launch_conv_patch_fused(A, stream, lev);
+        } else if (kind == K_CONV_PATCH) {
+          e = launch_conv_patch(S.pool, shape, A, stream, lev);
+        } else {
+          e = launch_stage(kind, dtype, S.f, S.pool, shape, A, stream, lev);
+        }
+        if (A.total_blocks > 0) {
+          launched = true;
+        } else if (last_chunk) {  // nothing launched for the last chunk: close the interval here
+          if ((!launched && ev_start && hipEventRecord(ev_start, stream) != hipSuccess) ||
+              (ev_stop && hipEventRecord(ev_stop, stream) != hipSuccess))
+            return fail(MAFAT_EHIP, "hipEventRecord failed");
+        }
+        if (e != hipSuccess)
+          return fail(MAFAT_EHIP, std::string("stage launch failed: ") + hipGetErrorString(e));
 #ifdef MAFAT_TUNING
-      if (std::getenv("MAFAT_WG_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH || kind == K_CONV_RGB_MFMA)) {
-        static long long wt[2][8192];
-        hipStreamSynchronize(stream);
-        if (kind == K_CONV_RING) mafat_debug_wg_ring(&wt[0][0]);
-        else if (kind == K_CONV_PATCH) mafat_debug_wg_patch(&wt[0][0]);
-        else mafat_debug_wg_rgb(&wt[0][0]);
-        const int n = std::min(A.total_blocks, 8192);
-        std::vector<long long> d(n);
-        long long s0 = wt[0][0], s1 = wt[0][0], e0 = wt[1][0], e1 = wt[1][0];
-        for (int b = 0; b < n; ++b) {
-          s0 = std::min(s0, wt[0][b]); s1 = std::max(s1, wt[0][b]);
-          e0 = std::min(e0, wt[1][b]); e1 = std::max(e1, wt[1][b]);
-          d[b] = wt[1][b] - wt[0][b];
+        if (std::getenv("MAFAT_WG_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH || kind == K_CONV_RGB_MFMA)) {
+          static long long wt[2][8192];
+          hipStreamSynchronize(stream);
+          if (kind == K_CONV_RING) mafat_debug_wg_ring(&wt[0][0]);
+          else if (kind == K_CONV_PATCH) mafat_debug_wg_patch(&wt[0][0]);
+          else mafat_debug_wg_rgb(&wt[0][0]);
+          const int n = std::min(A.total_blocks, 8192);
+          std::vector<long long> d(n);
+          long long s0 = wt[0][0], s1 = wt[0][0], e0 = wt[1][0], e1 = wt[1][0];
+          for (int b = 0; b < n; ++b) {
+            s0 = std::min(s0, wt[0][b]); s1 = std::max(s1, wt[0][b]);
+            e0 = std::min(e0, wt[1][b]); e1 = std::max(e1, wt[1][b]);
+            d[b] = wt[1][b] - wt[0][b];
+          }
+          std::sort(d.begin(), d.end());
+          std::fprintf(stderr, "WGSPAN stage %d-%d kind %d grid %d: span %lld ns, starts %lld, first end %lld, "
+                       "dur p10 %lld p50 %lld p90 %lld max %lld ns\n", S.first, S.last, kind, A.total_blocks,
+                       (e1 - s0) * 10, (s1 - s0) * 10, (e0 - s0) * 10, d[n / 10] * 10, d[n / 2] * 10,
+                       d[(9 * n) / 10] * 10, d.back() * 10);
         }
-        std::sort(d.begin(), d.end());
-        std::fprintf(stderr, "WGSPAN stage %d-%d kind %d grid %d: span %lld ns, starts %lld, first end %lld, "
-                     "dur p10 %lld p50 %lld p90 %lld max %lld ns\n", S.first, S.last, kind, A.total_blocks,
-                     (e1 - s0) * 10, (s1 - s0) * 10, (e0 - s0) * 10, d[n / 10] * 10, d[n / 2] * 10,
-                     d[(9 * n) / 10] * 10, d.back() * 10);
-      }
-      if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH)) {
-        long long tr[3][64];
-        hipStreamSynchronize(stream);
-        if (kind == K_CONV_RING) mafat_debug_ring_trace(&tr[0][0]);
-        else mafat_debug_patch_trace(&tr[0][0]);
-        std::fprintf(stderr, "RTRACE stage %d-%d %dx%d kg%d ns%d grid %d\n", S.first, S.last, shape.bm, shape.bn,
-                     shape.kg, shape.depth, A.total_blocks);
-        for (int w = 0; w < 3; ++w) {
-          std::fprintf(stderr, "  wg%d decode +%lld loopend +%lld end +%lld iters:", w, (tr[w][1] - tr[w][0]) * 10,
-                       (tr[w][4] - tr[w][0]) * 10, (tr[w][5] - tr[w][0]) * 10);
-          for (int k = 8; k < 44; ++k) std::fprintf(stderr, " %lld", (tr[w][k] - tr[w][0]) * 10);
-          std::fprintf(stderr, "\n");
+        if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH)) {
+          long long tr[3][64];
+          hipStreamSynchronize(stream);
+          if (kind == K_CONV_RING) mafat_debug_ring_trace(&tr[0][0]);
+          else mafat_debug_patch_trace(&tr[0][0]);
+          std::fprintf(stderr, "RTRACE stage %d-%d %dx%d kg%d ns%d grid %d\n", S.first, S.last, shape.bm, shape.bn,
+                       shape.kg, shape.depth, A.total_blocks);
+          for (int w = 0; w < 3; ++w) {
+            std::fprintf(stderr, "  wg%d decode +%lld loopend +%lld end +%lld iters:", w, (tr[w][1] - tr[w][0]) * 10,
+                         (tr[w][4] - tr[w][0]) * 10, (tr[w][5] - tr[w][0]) * 10);
+            for (int k = 8; k < 44; ++k) std::fprintf(stderr, " %lld", (tr[w][k] - tr[w][0]) * 10);
+            std::fprintf(stderr, "\n");
+          }
+          std::fprintf(stderr, "  start spread: mid-first %lld last-first %lld ns\n", (tr[1][0] - tr[0][0]) * 10,
+                       (tr[2][0] - tr[0][0]) * 10);
         }
-        std::fprintf(stderr, "  start spread: mid-first %lld last-first %lld ns\n", (tr[1][0] - tr[0][0]) * 10,
-                     (tr[2][0] - tr[0][0]) * 10);
-      }
-      if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_MFMA || kind == K_CONV_RGB_MFMA)) {
-        long long tr[4][64];
-        hipStreamSynchronize(stream);
-        mafat_debug_trace(&tr[0][0]);
-        std::fprintf(stderr, "TRACE stage %d-%d tile %dx%d depth %d grid %d\n", S.first, S.last,
-                     shape.bm, shape.bn, shape.depth, A.total_blocks);
-        for (int w = 0; w < 3; ++w) {
-          std::fprintf(stderr, "  wg%d decoded +%lld addr +%lld issued +%lld lstored +%lld barrier +%lld loop +%lld end +%lld steps:", w,
-                       (tr[w][4] - tr[w][0]) * 10, (tr[w][5] - tr[w][0]) * 10, (tr[w][6] - tr[w][0]) * 10,
-                       (tr[w][7] - tr[w][0]) * 10, (tr[w][1] - tr[w][0]) * 10, (tr[w][2] - tr[w][0]) * 10,
-                       (tr[w][3] - tr[w][0]) * 10);
-          for (int k = 8; k < 20; ++k) std::fprintf(stderr, " %lld", (tr[w][k] - tr[w][0]) * 10);
-          std::fprintf(stderr, " | remap +%lld divs +%lld prefix +%lld", (tr[w][60] - tr[w][0]) * 10,
-                       (tr[w][61] - tr[w][0]) * 10, (tr[w][62] - tr[w][0]) * 10);
-          std::fprintf(stderr, "\n");
+        if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_MFMA || kind == K_CONV_RGB_MFMA)) {
+          long long tr[4][64];
+          hipStreamSynchronize(stream);
+          mafat_debug_trace(&tr[0][0]);
+          std::fprintf(stderr, "TRACE stage %d-%d tile %dx%d depth %d grid %d\n", S.first, S.last,
+                       shape.bm, shape.bn, shape.depth, A.total_blocks);
+          for (int w = 0; w < 3; ++w) {
+            std::fprintf(stderr, "  wg%d decoded +%lld addr +%lld issued +%lld lstored +%lld barrier +%lld loop +%lld end +%lld steps:", w,
+                         (tr[w][4] - tr[w][0]) * 10, (tr[w][5] - tr[w][0]) * 10, (tr[w][6] - tr[w][0]) * 10,
+                         (tr[w][7] - tr[w][0]) * 10, (tr[w][1] - tr[w][0]) * 10, (tr[w][2] - tr[w][0]) * 10,
+                         (tr[w][3] - tr[w][0]) * 10);
+            for (int k = 8; k < 20; ++k) std::fprintf(stderr, " %lld", (tr[w][k] - tr[w][0]) * 10);
+            std::fprintf(stderr, " | remap +%lld divs +%lld prefix +%lld", (tr[w][60] - tr[w][0]) * 10,
+                         (tr[w][61] - tr[w][0]) * 10, (tr[w][62] - tr[w][0]) * 10);
+            std::fprintf(stderr, "\n");
+          }
+          std::fprintf(stderr, "  start spread wg-last minus wg0: %lld ns\n", (tr[1][0] - tr[0][0]) * 10);
         }
-        std::fprintf(stderr, "  start spread wg-last minus wg0: %lld ns\n", (tr[1][0] - tr[0][0]) * 10);
-      }
 #endif
-    }
-    if (dst_b != eff(SD.dst_buf)) swapped = !swapped;
-    if (fuse) {
-      ++s;
-      if (events) {
-        for (int k = 0; k < 2; ++k) {
-          hipEvent_t e2 = static_cast<hipEvent_t>(events[2 * (s - s_begin) + k]);
-          if (e2 && hipEventRecord(e2, stream) != hipSuccess) return fail(MAFAT_EHIP, "hipEventRecord failed");
+      }
+      started[static_cast<size_t>(s - s_begin)] = launched ? 1 : 0;
+      if (dst_b != eff(SD.dst_buf)) swapped = !swapped;
+      if (fuse) {
+        ++s;
+        if (events) {
+          for (int k = 0; k < 2; ++k) {
+            hipEvent_t e2 = static_cast<hipEvent_t>(events[2 * (s - s_begin) + k]);
+            if (e2 && hipEventRecord(e2, stream) != hipSuccess) return fail(MAFAT_EHIP, "hipEventRecord failed");
+          }
         }
       }
     }
@@ -565,6 +574,8 @@ extern "C" int mafat_run_stage(const mafat_plan* plan, int32_t group, int32_t st
     return fail(MAFAT_EINVAL, "group index out of range");
   if (stage < 0 || stage >= static_cast<int>(plan->groups[group].stages.size()))
     return fail(MAFAT_EINVAL, "stage index out of range");
+  if (plan->groups[group].tile_batch < plan->groups[group].ntiles)
+    return fail(MAFAT_EUNSUPPORTED, "the group runs in tile batches: its stages cannot run one at a time");
   return run_group_impl(plan, group, stage, stage + 1, batch, dtype, x, y, w, scale, bias, workspace, ws_bytes,
                         static_cast<hipStream_t>(stream), nullptr);
 }

@@ -35,7 +35,7 @@ DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
 EXPORTS = ("mafat_plan_create", "mafat_plan_create_flags", "mafat_plan_destroy",
            "mafat_packed_weights_size", "mafat_pack_weights", "mafat_plan_layer_shape", "mafat_plan_group",
            "mafat_plan_regions", "mafat_plan_macs", "mafat_plan_stages", "mafat_plan_stage_layers",
-           "mafat_plan_stage_fused",
+           "mafat_plan_stage_fused", "mafat_plan_set_tile_batch",
            "mafat_workspace_size", "mafat_run_group", "mafat_run_stage", "mafat_run_network",
            "mafat_predict_mem", "mafat_get_config", "mafat_status_string", "mafat_last_error")
 
@@ -88,6 +88,7 @@ def lib():
         L.mafat_plan_stages.argtypes = [planp, i32, i32p]
         L.mafat_plan_stage_layers.argtypes = [planp, i32, i32, i32p, i32p]
         L.mafat_plan_stage_fused.argtypes = [planp, i32, i32, i32, i32, i32p]
+        L.mafat_plan_set_tile_batch.argtypes = [planp, i32]
         L.mafat_workspace_size.argtypes = [planp, i32, i32, ctypes.POINTER(sz)]
         L.mafat_run_group.argtypes = [planp, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp, vpp]
         L.mafat_run_stage.argtypes = [planp, i32, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp]
@@ -203,6 +204,10 @@ def mafat_plan_stages(plan, group):
     return out
 
 
+def mafat_plan_set_tile_batch(plan, tiles):
+    _check("mafat_plan_set_tile_batch", lib().mafat_plan_set_tile_batch(plan, tiles))
+
+
 def mafat_plan_stage_fused(plan, group, stage, batch, dtype):
     f = ctypes.c_int32()
     _check("mafat_plan_stage_fused", lib().mafat_plan_stage_fused(plan, group, stage, batch, DTYPES.get(dtype, dtype),
@@ -284,10 +289,11 @@ class Plan:
     """A plan for a layer stack, an input shape and a tiling spec such as
     ``"5x5/8/2x2"`` (section 5.1 notation) or explicit group lists."""
 
-    def __init__(self, layers, in_hwc, tiling="1x1/NoCut", reuse=False, packed_weights=False):
+    def __init__(self, layers, in_hwc, tiling="1x1/NoCut", reuse=False, packed_weights=False, tile_batch=0):
         self.layers = list(layers)
         self.reuse = bool(reuse)
         self.packed_weights = bool(packed_weights)
+        self.tile_batch = int(tile_batch)
         self.h, self.w, self.c = in_hwc
         self.group_start, self.rows, self.cols = W.parse_tiling(tiling, len(layers)) \
             if isinstance(tiling, str) else tiling
@@ -296,6 +302,8 @@ class Plan:
                                         (MAFAT_PLAN_TILE_REUSE if self.reuse else 0) |
                                         (MAFAT_PLAN_PACKED_WEIGHTS if self.packed_weights else 0))
         self.n_groups = len(self.group_start)
+        if self.tile_batch:
+            mafat_plan_set_tile_batch(self.handle, self.tile_batch)
 
     def __del__(self):
         h = getattr(self, "handle", None)

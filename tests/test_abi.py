@@ -134,6 +134,38 @@ def test_fused_pair_detection(lib):
         plan.stage_fused(0, 2, 1, "bf16")
 
 
+def test_tile_batch(lib):
+    # tiles in batches of K: the workspace holds K tiles' intermediates per
+    # scratch buffer; with one tile at a time finer grids need less memory
+    # (the paper's trend), with all tiles at once more
+    layers, hwc = W.YOLOV2_16, (608, 608, 3)
+    full = M.Plan(layers, hwc, "5x5/NoCut")
+    one = M.Plan(layers, hwc, "5x5/NoCut", tile_batch=1)
+    seven = M.Plan(layers, hwc, "5x5/NoCut", tile_batch=7)
+    big = M.Plan(layers, hwc, "5x5/NoCut", tile_batch=99)   # >= the tile count: all at once
+    ws = {k: p.workspace_size(1, "bf16") for k, p in (("full", full), ("one", one), ("seven", seven), ("big", big))}
+    assert ws["big"] == ws["full"]
+    assert ws["one"] < ws["seven"] < ws["full"]
+    per_tile = ws["one"] // 256 * 256
+    assert abs(ws["seven"] - 7 * ws["one"]) <= 7 * 256 and abs(ws["full"] - 25 * ws["one"]) <= 25 * 256, (ws, per_tile)
+    dev = lambda t, k: M.Plan(layers, hwc, t, tile_batch=k).predict_mem("device", 1, "bf16")
+    seq = [dev(t, 1) for t in ("1x1/NoCut", "2x2/NoCut", "3x3/NoCut", "5x5/NoCut")]
+    assert seq == sorted(seq, reverse=True) and seq[-1] < seq[0], seq
+    par = [dev(t, 0) for t in ("1x1/NoCut", "3x3/NoCut", "5x5/NoCut")]
+    assert par == sorted(par), par
+    # the stage layout is unchanged; errors
+    assert one.stages(0) == full.stages(0)
+    with pytest.raises(M.MafatError) as e:
+        M.Plan(layers, hwc, "5x5/NoCut", reuse=True, tile_batch=3)
+    assert e.value.rc == M.MAFAT_EUNSUPPORTED
+    M.Plan(layers, hwc, "5x5/NoCut", reuse=True, tile_batch=25)   # every tile at once: allowed
+    assert M.lib().mafat_plan_set_tile_batch(full.handle, -1) == M.MAFAT_EINVAL
+    assert M.lib().mafat_plan_set_tile_batch(None, 1) == M.MAFAT_EINVAL
+    # back to all tiles at once
+    assert M.lib().mafat_plan_set_tile_batch(one.handle, 0) == 0
+    assert one.workspace_size(1, "bf16") == ws["full"]
+
+
 def test_workspace_size(lib):
     plan = M.Plan(W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2")
     b1 = plan.workspace_size(1, "bf16")
@@ -274,3 +306,8 @@ def test_run_argument_errors_before_any_launch(lib):
     rc = L.mafat_run_stage(plan.handle, 0, 0, 1, M.MAFAT_F32, fake, fake * 4, w, w, w, fake, need - 1, None)
     assert rc == M.MAFAT_EWORKSPACE
     assert M.lib().mafat_status_string(M.MAFAT_EWORKSPACE) == b"workspace too small"
+    # a group split into tile batches cannot run one stage at a time
+    plan3 = M.Plan(W.TINY, (64, 64, 3), "2x2", tile_batch=1)
+    need3 = plan3.workspace_size(1, "f32")
+    rc = L.mafat_run_stage(plan3.handle, 0, 0, 1, M.MAFAT_F32, fake, fake * 4, w, w, w, fake, need3, None)
+    assert rc == M.MAFAT_EUNSUPPORTED

@@ -388,3 +388,44 @@ def test_run_group_events(which):
                 assert ev.ms(evs[2 * s + 1], evs[2 * s + 2]) >= 0
         assert ev.ms(evs[4], evs[5]) > 0  # the fused pair's kernel
     ev.destroy(evs)
+
+
+@pytest.mark.parametrize("dtype,tiling,k", [("bf16", "5x5/8/2x2", 1), ("bf16", "5x5/8/2x2", 3),
+                                             ("bf16", "5x5/8/2x2", 7), ("f32", "3x3/NoCut", 2),
+                                             ("f32", "5x5/8/2x2", 4)])
+def test_tile_batch_bit_identical(dtype, tiling, k):
+    # tiles in batches of k (each batch through all stages, the workspace
+    # holding k tiles) == every tile at once, bit for bit, cut tensors too;
+    # bf16 runs the fused layers 4-5 inside every batch
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    print(f"[parity] tile batch {k}: YOLOv2 96x96 {tiling} {dtype} batch=2", flush=True)
+    p = W.make_inputs(W.YOLOV2_16, 96, 96, 3, 2, 12, dtype)
+    res = []
+    for tb in (0, k):
+        plan = M.Plan(W.YOLOV2_16, (96, 96, 3), tiling, packed_weights=(dtype == "bf16"), tile_batch=tb)
+        net = M.Network(plan, p, 2, dtype)
+        net.y.fill_(float("nan"))
+        y = net.run(net.input_tensor(p["x"])).clone()
+        torch.cuda.synchronize()
+        res.append((y, [c.clone() for c in net.cuts], plan.workspace_size(2, dtype)))
+    assert res[1][2] < res[0][2]
+    assert torch.equal(res[0][0], res[1][0])
+    for a, b in zip(res[0][1], res[1][1]):
+        assert torch.equal(a, b)
+
+
+def test_tile_batch_parity(orc):
+    # one tile at a time, odd extents, batch 2, against the oracle
+    from paper_2107_06960_amd import mafat as M
+    import torch
+    layers, h, w, c = W.YOLOV2_16, 71, 93, 3
+    print(f"[parity] tile batch 1: YOLOv2 {h}x{w} 3x2/8/2x2 bf16 batch=2", flush=True)
+    p = W.make_inputs(layers, h, w, c, 2, 13, "bf16")
+    plan = M.Plan(layers, (h, w, c), "3x2/8/2x2", packed_weights=True, tile_batch=1)
+    net = M.Network(plan, p, 2, "bf16")
+    y = net.run(net.input_tensor(p["x"]))
+    torch.cuda.synchronize()
+    out = y.float().cpu().numpy().astype(np.float64)
+    ref = orc.forward_layers(layers, h, w, c, p["x"], p)
+    assert normwise_err(out, ref) <= TOL["bf16"]
