@@ -281,7 +281,8 @@ def config_search(args):
 
 def all_configs(args):
     """Every workload of the build (the paper's configurations and the six
-    cut x grid runs): per-step latency (median, p10, p90 of HIP events on the
+    cut x grid runs), each with every tile at once, with tile reuse, and one
+    tile at a time (the paper's order): per-step latency (median, p10, p90 of HIP events on the
     launch stream around each mafat_run_network call, 10 warm-up steps
     first), frames/s at the median, executed TFLOP/s and its fraction of the
     dtype's matrix-core peak, and peak device memory against the untiled
@@ -293,9 +294,10 @@ def all_configs(args):
     torch.cuda.set_device(0)
     ev = HipEvents()
     stream = torch.cuda.current_stream()
-    for name, wl, reuse in [(n, w, r) for n, w in W.WORKLOADS.items() for r in (False, True)]:
+    variants = ((False, 0), (True, 0), (False, 1))  # (tile reuse, tile batch: 0 all tiles at once)
+    for name, wl, reuse, tb in [(n, w, r, k) for n, w in W.WORKLOADS.items() for r, k in variants]:
         params = W.workload_inputs(wl)
-        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=reuse, packed_weights=True)
+        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=reuse, packed_weights=True, tile_batch=tb)
         net = M.Network(plan, params, wl.batch, wl.dtype)
         x = net.input_tensor(params["x"])
         for _ in range(10):
@@ -315,12 +317,13 @@ def all_configs(args):
         us = sum(2 * plan.macs(g)[1] for g in range(plan.n_groups)) * wl.batch
         del net, x
         tp, _ = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch, wl.dtype,
-                                    params["x"], reuse=reuse, packed=True)
+                                    params["x"], reuse=reuse, packed=True, tile_batch=tb)
         up, ums = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), untiled_groups(wl.layers), params,
                                       wl.batch, wl.dtype, params["x"])
         print(json.dumps({
             "workload": name, "input": f"{wl.h}x{wl.w}x{wl.c}", "batch": wl.batch, "dtype": wl.dtype,
-            "tiling": wl.tiling, "tile_reuse": reuse, "weights": "packed" if wl.dtype == "bf16" else "KRSC",
+            "tiling": wl.tiling, "tile_reuse": reuse, "tile_batch": tb or "all",
+            "weights": "packed" if wl.dtype == "bf16" else "KRSC",
             "steps": n, "ms_p50": round(p50, 5), "ms_p10": round(p10, 5),
             "ms_p90": round(p90, 5), "frames_per_s": round(wl.batch / (p50 * 1e-3), 1),
             "gflop_executed": round(ex / 1e9, 3), "gflop_useful": round(us / 1e9, 3),
