@@ -73,7 +73,7 @@ typedef enum {
 typedef enum { MAFAT_CONV = 0, MAFAT_MAXPOOL = 1 } mafat_op;
 typedef enum { MAFAT_ACT_LINEAR = 0, MAFAT_ACT_LEAKY01 = 1 } mafat_act;
 typedef enum { MAFAT_F32 = 0, MAFAT_BF16 = 1 } mafat_dtype;
-typedef enum { MAFAT_MEM_DEVICE = 0, MAFAT_MEM_PAPER = 1 } mafat_mem_model;
+typedef enum { MAFAT_MEM_DEVICE = 0, MAFAT_MEM_PAPER = 1, MAFAT_MEM_DEVICE_SEQ = 2 } mafat_mem_model;
 
 /* One layer (section 4.1 describes a layer by width, height, filter size
  * and stride; channels, padding and activation are added).  c_out and act
@@ -284,8 +284,15 @@ int mafat_run_network(const mafat_plan* plan, int32_t batch, int32_t dtype,
  *   model MAFAT_MEM_DEVICE: the device memory a run of this library needs,
  *     all of it caller-owned: input, output and cut tensors (batch frames),
  *     parameters (weights in dtype, float32 scale and bias) and the
- *     workspace (mafat_workspace_size).  Every tile of a stage runs at once
- *     on the GPU, so the workspace holds every tile's intermediates.
+ *     workspace (mafat_workspace_size).  By default every tile of a stage
+ *     runs at once on the GPU, so the workspace holds every tile's
+ *     intermediates; with a tile batch (mafat_plan_set_tile_batch) it holds
+ *     one batch's.
+ *   model MAFAT_MEM_DEVICE_SEQ: the device memory of the same plan run one
+ *     tile at a time (tile batch 1, the paper's execution order), whatever
+ *     the plan's tile batch; for groups with tile reuse, their workspace as
+ *     MAFAT_MEM_DEVICE.  With mafat_get_config this is the paper's search
+ *     under a device-memory limit.
  * *bytes receives the prediction.  Errors: EINVAL (null plan or pointer,
  * batch < 1, unknown model), EUNSUPPORTED (dtype). */
 int mafat_predict_mem(const mafat_plan* plan, int32_t model, int32_t batch, int32_t dtype,

@@ -18,7 +18,9 @@
 //                    parameters (weights in the run dtype, float32 scale and
 //                    bias) and the workspace.  On the GPU every tile of a
 //                    stage runs at once, so the working set is all tiles'
-//                    intermediates (the workspace), not the largest tile's.
+//                    intermediates (the workspace), not the largest tile's;
+//                    with a tile batch K, K tiles' intermediates.
+//   MAFAT_MEM_DEVICE_SEQ the same with one tile at a time (tile batch 1).
 //
 // mafat_get_config: the configuration search of the paper (section 4.2,
 // Algorithm 2): cuts are tried in the given order (a cut >= n_layers means
@@ -59,7 +61,7 @@ int64_t paper_group_max(const mafat_plan& P, const Group& G) {
   return best;
 }
 
-int64_t device_bytes(const mafat_plan& P, int batch, int dtype) {
+int64_t device_bytes(const mafat_plan& P, int batch, int dtype, bool one_tile) {
   const int64_t esz = (dtype == MAFAT_F32) ? 4 : 2;
   const auto& d0 = P.dims.front();
   const auto& dn = P.dims.back();
@@ -80,7 +82,14 @@ int64_t device_bytes(const mafat_plan& P, int batch, int dtype) {
     total += w + 2 * 4 * static_cast<int64_t>(d[5]);
   }
   size_t ws = 0;
-  mafat_workspace_size(&P, batch, dtype, &ws);
+  if (!one_tile) {
+    mafat_workspace_size(&P, batch, dtype, &ws);
+  } else {  // the workspace of tile batch 1: one tile slot per scratch buffer
+    for (const Group& G : P.groups) {
+      const int64_t frame = G.reuse ? G.scratch_frame : static_cast<int64_t>(G.nbufs) * G.scratch_elems;
+      ws = std::max(ws, (static_cast<size_t>(batch) * frame * esz + 255) & ~static_cast<size_t>(255));
+    }
+  }
   return total + static_cast<int64_t>(ws);
 }
 
@@ -91,7 +100,7 @@ int predict(const mafat_plan* plan, int model, int batch, int dtype, int64_t* by
     *bytes = best * ((dtype == MAFAT_F32) ? 4 : 2);
     return MAFAT_OK;
   }
-  *bytes = device_bytes(*plan, batch, dtype);
+  *bytes = device_bytes(*plan, batch, dtype, model == MAFAT_MEM_DEVICE_SEQ);
   return MAFAT_OK;
 }
 
@@ -108,7 +117,7 @@ extern "C" int mafat_predict_mem(const mafat_plan* plan, int32_t model, int32_t 
     set_error("dtype must be F32 or BF16");
     return MAFAT_EUNSUPPORTED;
   }
-  if (model != MAFAT_MEM_PAPER && model != MAFAT_MEM_DEVICE) {
+  if (model != MAFAT_MEM_PAPER && model != MAFAT_MEM_DEVICE && model != MAFAT_MEM_DEVICE_SEQ) {
     set_error("unknown memory model");
     return MAFAT_EINVAL;
   }

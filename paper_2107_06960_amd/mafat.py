@@ -26,9 +26,9 @@ MAFAT_EWORKSPACE, MAFAT_EHIP, MAFAT_ENOMEM = -4, -5, -6
 MAFAT_CONV, MAFAT_MAXPOOL = 0, 1
 MAFAT_ACT_LINEAR, MAFAT_ACT_LEAKY01 = 0, 1
 MAFAT_F32, MAFAT_BF16 = 0, 1
-MAFAT_MEM_DEVICE, MAFAT_MEM_PAPER = 0, 1
+MAFAT_MEM_DEVICE, MAFAT_MEM_PAPER, MAFAT_MEM_DEVICE_SEQ = 0, 1, 2
 MAFAT_PLAN_TILE_REUSE, MAFAT_PLAN_PACKED_WEIGHTS = 1, 2
-MEM_MODELS = {"device": MAFAT_MEM_DEVICE, "paper": MAFAT_MEM_PAPER}
+MEM_MODELS = {"device": MAFAT_MEM_DEVICE, "paper": MAFAT_MEM_PAPER, "device_seq": MAFAT_MEM_DEVICE_SEQ}
 DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
 
 # Every symbol include/mafat.h declares.

@@ -49,3 +49,33 @@ def test_device_model_matches_measured_peak(name, reuse, packed, tile_batch):
     print(f"[memory] {name}: predicted {pred} B, requested {used} B (allocator blocks {alloc} B)", flush=True)
     assert used == pred
     del net, x
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("mib", [12, 16, 24])
+def test_search_under_device_limit_runs_within_it(mib):
+    # Algorithm 2 with the sequential device model picks a configuration;
+    # run one tile at a time, it holds exactly the predicted bytes, which
+    # are below the limit
+    require_gpu()
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    spec, pred, fits = M.mafat_get_config(W.YOLOV2_16, (608, 608, 3), mib << 20, model="device_seq",
+                                          dtype="bf16")
+    print(f"[memory] search under {mib} MiB: {spec}, predicted {pred} B", flush=True)
+    assert fits
+    wl = W.WORKLOADS["yolo608_5x5_8_2x2"]
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    base = torch.cuda.memory_stats().get("requested_bytes.all.current", 0)
+    p = W.workload_inputs(wl)
+    plan = M.Plan(W.YOLOV2_16, (608, 608, 3), spec, tile_batch=1)
+    net = M.Network(plan, p, 1, "bf16")
+    x = net.input_tensor(p["x"])
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    net.run(x)
+    torch.cuda.synchronize()
+    used = torch.cuda.memory_stats()["requested_bytes.all.peak"] - base
+    assert used == pred < (mib << 20)
+    del net, x

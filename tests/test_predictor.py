@@ -125,6 +125,43 @@ def test_device_model_counts_every_buffer():
         assert plan.predict_mem("device", b, wl.dtype) == tot
 
 
+def test_device_seq_model_is_tile_batch_one():
+    # the sequential device model of a plan == the device model of the same
+    # plan run with tile batch 1, whatever the plan's own batch; finer grids
+    # need less under it (the paper's trend), more under the default model
+    _lib()
+    for spec in ("1x1/NoCut", "3x3/NoCut", "5x5/8/2x2", "4x4/12/1x1", "6x6/12/2x2"):
+        for batch in (1, 4):
+            for tb in (0, 3):
+                plan = M.Plan(W.YOLOV2_16, (608, 608, 3), spec, tile_batch=tb)
+                one = M.Plan(W.YOLOV2_16, (608, 608, 3), spec, tile_batch=1)
+                assert plan.predict_mem("device_seq", batch, "bf16") == one.predict_mem("device", batch, "bf16")
+    seq = [M.Plan(W.YOLOV2_16, (608, 608, 3), f"{t}x{t}/8/2x2").predict_mem("device_seq", 1, "bf16")
+           for t in (1, 2, 3, 4, 5)]
+    assert seq == sorted(seq, reverse=True) and seq[0] > seq[-1], seq
+
+
+@pytest.mark.parametrize("mib", [12, 14, 16, 20, 24])
+def test_search_device_seq(mib):
+    # Algorithm 2 under a device-memory limit with tiles run one at a time:
+    # the first configuration (cuts 16, 12, 8; grids 1..5) whose sequential
+    # device prediction is below the limit, checked by brute force here
+    _lib()
+    spec, pred, fits = M.mafat_get_config(W.YOLOV2_16, (608, 608, 3), mib * MiB, model="device_seq",
+                                          dtype="bf16")
+    want = None
+    for cut in (16, 12, 8):
+        for t in (1, 2, 3, 4, 5):
+            sp = f"{t}x{t}/NoCut" if cut >= 16 else f"{t}x{t}/{cut}/2x2"
+            p_ = M.Plan(W.YOLOV2_16, (608, 608, 3), sp).predict_mem("device_seq", 1, "bf16")
+            if want is None and p_ < mib * MiB:
+                want = (sp, p_)
+    if want is None:
+        assert not fits and spec == "5x5/8/2x2"
+    else:
+        assert fits and (spec, pred) == want
+
+
 def test_predict_and_search_errors():
     L = _lib()
     import ctypes
