@@ -328,16 +328,18 @@ void conv_patch_kernel(const StageArgs a) {
   // read from LDS (into the other register set) before the MFMAs of tap t
   // are issued, and a scheduling barrier keeps the compiler from
   // interleaving them, so each tap's LDS latency hides behind the previous
-  // tap's MFMAs.
-  auto load_frags = [&](const unsigned char* sp, int t, u32x4 (&af)[MT], u32x4 (&bfr)[NT]) {
+  // tap's MFMAs.  A chunk's patch is read at spa, its weight rows at spb
+  // (the same slot, except in the fused variant's split second chunk).
+  auto load_frags = [&](const unsigned char* spa, const unsigned char* spb, int t, u32x4 (&af)[MT],
+                        u32x4 (&bfr)[NT]) {
     const int ty = t / 3, tx = t % 3;
 #pragma unroll
     for (int i = 0; i < MT; ++i)
-      af[i] = *reinterpret_cast<const u32x4*>(sp + pb[i] + (ty * PC + tx) * 64 +
+      af[i] = *reinterpret_cast<const u32x4*>(spa + pb[i] + (ty * PC + tx) * 64 +
                                               (((kx3[i][tx] ^ ky3[i][ty]) & 3) << 4));
 #pragma unroll
     for (int j = 0; j < NT; ++j)
-      bfr[j] = *reinterpret_cast<const u32x4*>(sp + b_lane + (t * BN + j * 16) * 64);
+      bfr[j] = *reinterpret_cast<const u32x4*>(spb + b_lane + (t * BN + j * 16) * 64);
   };
   auto mfmas = [&](const u32x4 (&af)[MT], const u32x4 (&bfr)[NT]) {
 #pragma unroll
@@ -348,23 +350,30 @@ void conv_patch_kernel(const StageArgs a) {
         else mma<MAFAT_BF16>(acc[j][i], bfr[j], af[i]);
       }
   };
-  auto compute = [&](int slot) {
-    const unsigned char* sp = smem + slot * SLOT;
+  // Taps [T0, T1) of one chunk (T0, T1 as std::integral_constant).
+  auto taps = [&](const unsigned char* spa, const unsigned char* spb, auto t0c, auto t1c) {
+    constexpr int T0 = decltype(t0c)::value, T1 = decltype(t1c)::value;
     u32x4 af0[MT], bf0[NT], af1[MT], bf1[NT];
-    load_frags(sp, 0, af0, bf0);
+    load_frags(spa, spb, T0, af0, bf0);
 #pragma unroll
-    for (int t = 0; t < 9; t += 2) {
-      if (t + 1 < 9) load_frags(sp, t + 1, af1, bf1);
+    for (int t = T0; t < T1; t += 2) {
+      if (t + 1 < T1) load_frags(spa, spb, t + 1, af1, bf1);
       __builtin_amdgcn_sched_barrier(0);
       mfmas(af0, bf0);
       __builtin_amdgcn_sched_barrier(0);
-      if (t + 1 < 9) {
-        if (t + 2 < 9) load_frags(sp, t + 2, af0, bf0);
+      if (t + 1 < T1) {
+        if (t + 2 < T1) load_frags(spa, spb, t + 2, af0, bf0);
         __builtin_amdgcn_sched_barrier(0);
         mfmas(af1, bf1);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I9 = std::integral_constant<int, 9>;
+  auto compute = [&](int slot) {
+    const unsigned char* sp = smem + slot * SLOT;
+    taps(sp, sp, I0{}, I9{});
   };
 
   if constexpr (N2 > 0) {
@@ -372,35 +381,6 @@ void conv_patch_kernel(const StageArgs a) {
       // Two chunks, the second one's loads overlapped with compute: its
       // patch and first YT taps go to Y at once, its last taps to the
       // slot once the first chunk is done with it.
-      auto frags2 = [&](const unsigned char* spa, const unsigned char* spb, int t, u32x4 (&af)[MT],
-                        u32x4 (&bfr)[NT]) {
-        const int ty = t / 3, tx = t % 3;
-#pragma unroll
-        for (int i = 0; i < MT; ++i)
-          af[i] = *reinterpret_cast<const u32x4*>(spa + pb[i] + (ty * PC + tx) * 64 +
-                                                  (((kx3[i][tx] ^ ky3[i][ty]) & 3) << 4));
-#pragma unroll
-        for (int j = 0; j < NT; ++j)
-          bfr[j] = *reinterpret_cast<const u32x4*>(spb + b_lane + (t * BN + j * 16) * 64);
-      };
-      auto taps = [&](const unsigned char* spa, const unsigned char* spb, auto t0c, auto t1c) {
-        constexpr int T0 = decltype(t0c)::value, T1 = decltype(t1c)::value;
-        u32x4 af0[MT], bf0[NT], af1[MT], bf1[NT];
-        frags2(spa, spb, T0, af0, bf0);
-#pragma unroll
-        for (int t = T0; t < T1; t += 2) {
-          if (t + 1 < T1) frags2(spa, spb, t + 1, af1, bf1);
-          __builtin_amdgcn_sched_barrier(0);
-          mfmas(af0, bf0);
-          __builtin_amdgcn_sched_barrier(0);
-          if (t + 1 < T1) {
-            if (t + 2 < T1) frags2(spa, spb, t + 2, af0, bf0);
-            __builtin_amdgcn_sched_barrier(0);
-            mfmas(af1, bf1);
-            __builtin_amdgcn_sched_barrier(0);
-          }
-        }
-      };
       auto issue_b_taps = [&](unsigned char* sl, auto k0c, auto k1c) {
 #pragma unroll
         for (int k = decltype(k0c)::value; k < decltype(k1c)::value; ++k)
@@ -408,9 +388,7 @@ void conv_patch_kernel(const StageArgs a) {
                                                    static_cast<int>(b_off[k] + bstride), 0, 0, 0);
       };
       unsigned char* const Y = smem + YOFF;
-      using I0 = std::integral_constant<int, 0>;
       using IY = std::integral_constant<int, YT>;
-      using I9 = std::integral_constant<int, 9>;
       issue_a(0, 0);                     // chunk 0's weights are on their way already
       {                                  // chunk 1: patch and taps [0, YT) to Y
         const unsigned coff = 64u;
