@@ -82,3 +82,24 @@ def test_fullsize_sampled(orc, name):
                 assert err <= TOL[wl.dtype], (name, nl, f, (y0, y1, x0, x1), err)
     print(f"[fullsize] {name}: worst normwise error {worst:.3g}", flush=True)
 
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("k", [1, 5])
+def test_fullsize_tile_batch_bit_identical(k):
+    # the benchmark workload at full size, tiles in batches of k (one tile,
+    # one grid row of the first group) == every tile at once, bit for bit
+    require_gpu()
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    wl = W.WORKLOADS["yolo608_5x5_8_2x2"]
+    print(f"[fullsize] {wl.name} tile batch {k} vs all tiles", flush=True)
+    p = W.workload_inputs(wl)
+    outs = []
+    for tb in (0, k):
+        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, packed_weights=True, tile_batch=tb)
+        net = M.Network(plan, p, wl.batch, wl.dtype)
+        outs.append(net.run(net.input_tensor(p["x"])).clone())
+        torch.cuda.synchronize()
+        del net
+    assert torch.equal(outs[0], outs[1])
