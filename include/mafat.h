@@ -254,8 +254,11 @@ int mafat_run_group(const mafat_plan* plan, int32_t group, int32_t batch, int32_
  * group output y (last stage) or the workspace.  Calling it for stages 0 ..
  * n_stages-1 in order on one stream with the same workspace computes what
  * mafat_run_group computes; one stage alone can be launched repeatedly
- * (e.g. to time its kernel).  Same arguments, conventions and errors as
- * mafat_run_group, plus EINVAL for a stage index out of range. */
+ * (e.g. to time its kernel).  It always runs one stage alone (a fused
+ * pair's stages as two kernels, see mafat_plan_stage_fused).  Same
+ * arguments, conventions and errors as mafat_run_group, plus EINVAL for a
+ * stage index out of range and EUNSUPPORTED for a group that runs in
+ * several tile batches (mafat_plan_set_tile_batch). */
 int mafat_run_stage(const mafat_plan* plan, int32_t group, int32_t stage, int32_t batch,
                     int32_t dtype, const void* x, void* y, const void* const* w,
                     const float* const* scale, const float* const* bias, void* workspace,
