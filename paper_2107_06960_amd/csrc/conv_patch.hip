@@ -45,6 +45,12 @@
 // block's outputs staged in LDS as rows of BN channels, then written as
 // 16-byte chunks (each output pixel's BN channels contiguous).
 //
+// Fused variant (template argument N2 > 0, BN = c_out = 128, no pool): the
+// staged block is the A operand of a following 1x1 convolution with N2
+// outputs, run from LDS in the same workgroup, so the 3x3 layer's output
+// never goes to memory; with two input chunks the second one's patch and
+// first taps load into a second LDS region while the first is computed.
+//
 // Requires f = 3, c_in % 32 == 0, c_out % 16 == 0, byte offsets below 2^31
 // within a frame's source buffer and within the weights (host-checked); a
 // fused pool needs even block sizes and even tile origins and extents.

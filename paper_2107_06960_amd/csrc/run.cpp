@@ -311,10 +311,14 @@ WorkspaceLayout workspace_layout(const Group& G, int batch, int dtype) {
 
 namespace {
 
-// Runs stages [s_begin, s_end) of group g.  events, if given, holds two
-// hipEvent_t per stage, indexed from s_begin: events[2k] is recorded when
-// the first kernel of stage s_begin + k starts, events[2k + 1] when its last
-// kernel ends (timestamps of the dispatches themselves).
+// Runs stages [s_begin, s_end) of group g: per tile batch (all tiles
+// unless the plan sets fewer), every stage in order, a stage as one launch
+// per 64 tiles; a fused pair whose two stages are both in the range as one
+// kernel.  events, if given, holds two hipEvent_t per stage, indexed from
+// s_begin: events[2k] is recorded when the first kernel of stage
+// s_begin + k starts, events[2k + 1] when its last kernel ends (timestamps
+// of the dispatches themselves); a fused pair's second stage gets two plain
+// records after the pair's kernel.
 int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int batch, int dtype, const void* x, void* y,
                    const void* const* w, const float* const* scale, const float* const* bias,
                    void* ws, size_t ws_bytes, hipStream_t stream, void* const* events) {
