@@ -81,7 +81,7 @@ struct MfmaShape {
   MAFAT_PATCH(12, 12, 192, 64, 4, 2, 2)   \
   MAFAT_PATCH(12, 16, 192, 64, 4, 2, 2)   \
   MAFAT_PATCH(16, 12, 192, 64, 4, 2, 2)   \
-  MAFAT_PATCH(10, 10, 128, 32, 8, 1, 2)   \
+  MAFAT_PATCH(10, 10, 128, 32, 4, 1, 2)   \
   MAFAT_PATCH(8, 8, 64, 32, 4, 2, 2)      \
   MAFAT_PATCH(8, 16, 128, 64, 8, 1, 1)    \
   MAFAT_PATCH(12, 16, 192, 64, 4, 2, 1)   \
