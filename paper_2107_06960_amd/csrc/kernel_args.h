@@ -60,7 +60,7 @@ enum KernelKind {
 
 // Conv outputs (rows x columns) per workgroup of the matrix-core first-layer
 // kernel.
-constexpr int kRgbBlockRows = 32, kRgbBlockCols = 32;
+constexpr int kRgbBlockRows = 16, kRgbBlockCols = 32;
 
 // Block shape of the MFMA kernel: output pixels x output channels, the
 // depth of its load pipeline (3 to 6 stages of 128 bytes of K in flight) and
