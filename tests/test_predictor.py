@@ -141,7 +141,7 @@ def test_device_seq_model_is_tile_batch_one():
     assert seq == sorted(seq, reverse=True) and seq[0] > seq[-1], seq
 
 
-@pytest.mark.parametrize("mib", [12, 14, 16, 20, 24])
+@pytest.mark.parametrize("mib", [8, 12, 14, 16, 20, 24])
 def test_search_device_seq(mib):
     # Algorithm 2 under a device-memory limit with tiles run one at a time:
     # the first configuration (cuts 16, 12, 8; grids 1..5) whose sequential
