@@ -112,6 +112,15 @@ def launch_bytes(io, launch):
     return io[launch[0]][0] + io[launch[-1]][1] + sum(io[s][2] for s in launch)
 
 
+def bench_network(M, wl, params):
+    """The plan and device network bench.py times for workload wl: its
+    tiling, batch and dtype, bf16 3x3 weights packed once for the patch
+    kernels (MAFAT_PLAN_PACKED_WEIGHTS).  The full-size parity tests build
+    their network with this same function."""
+    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, packed_weights=True)
+    return plan, M.Network(plan, params, wl.batch, wl.dtype)
+
+
 def untiled_groups(layers):
     """Every stage its own group on a 1x1 grid: the untiled layer-by-layer
     execution with the same kernels (a conv and its following pool fused)."""
@@ -122,14 +131,14 @@ def untiled_groups(layers):
     return starts, [1] * len(starts), [1] * len(starts)
 
 
-def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs=2, reuse=False, packed=False,
+def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs=2, part=False, packed=False,
                         tile_batch=0):
     import torch
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     torch.cuda.reset_peak_memory_stats()
     base = torch.cuda.memory_allocated()
-    plan = M.Plan(layers, hwc, tiling, reuse=reuse, packed_weights=packed, tile_batch=tile_batch)
+    plan = M.Plan(layers, hwc, tiling, stage_partition=part, packed_weights=packed, tile_batch=tile_batch)
     net = M.Network(plan, params, batch, dtype)
     x = net.input_tensor(x_np)
     torch.cuda.synchronize()
@@ -148,13 +157,50 @@ def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs
     return peak, ms
 
 
-def cpu_baseline(wl, params, exec_macs_per_frame, min_s=10.0, max_s=30.0):
-    """Oracle rate (MAC/s) on one core, on 2x2-pixel output rectangles of
-    frame 0 (each computed from its whole receptive-field cone through layers
-    0-15), extrapolated to a frame by the configuration's executed MACs."""
+def host_cpu():
+    """CPU model, logical CPU count and the CPUs this process may run on."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except AttributeError:
+        usable = os.cpu_count()
+    return {"cpu_model": model, "nproc": os.cpu_count(), "usable_cpus": usable}
+
+
+def cpu_baseline(wl, params, exec_macs_per_frame, min_wall_s=1.5, cone_s=(5.0, 10.0)):
+    """The oracle timed on the host cores (baseline only).
+
+    value: frames/s of the oracle's own fused-tile forward (forward_tiled,
+    the workload's tiling, float64) on frame 0, with the layer loops split
+    over all usable host cores (at most 16, a one-GPU machine's CPU share),
+    repeated until at least min_wall_s of wall time.  single_thread: the
+    oracle on one thread on 2x2-pixel output rectangles of frame 0 (each
+    through its whole receptive field, untiled), its MAC rate scaled to the
+    configuration's executed MACs per frame."""
     import numpy as np
     from oracle import oracle as O
+    info = host_cpu()
+    threads = max(1, min(16, info["usable_cpus"] or 1))
     layers = wl.layers
+    gs, rows, cols = wl.groups()
+    O.set_threads(threads)
+    frames, t0 = 0, time.perf_counter()
+    while True:
+        O.forward_tiled(layers, wl.h, wl.w, wl.c, params["x"][:1], params, gs, rows, cols)
+        frames += 1
+        if time.perf_counter() - t0 >= min_wall_s:
+            break
+    tiled_s = (time.perf_counter() - t0) / frames
+
+    O.set_threads(1)
     dims = O.shapes(layers, wl.h, wl.w, wl.c)
     oh, ow = int(dims[-1, 3]), int(dims[-1, 4])
     gr, gc = oh // 2, ow // 2
@@ -164,7 +210,7 @@ def cpu_baseline(wl, params, exec_macs_per_frame, min_s=10.0, max_s=30.0):
     order = first + [t for t in range(0, gr * gc, 7) if t not in first]
     x0 = params["x"][0]
     macs = 0
-    t0 = time.perf_counter()
+    t1 = time.perf_counter()
     used = []
     for t in order:
         y0, y1, x0_, x1 = (int(v) for v in R[t, -1, 4:])
@@ -174,16 +220,22 @@ def cpu_baseline(wl, params, exec_macs_per_frame, min_s=10.0, max_s=30.0):
                 a = int(R[t, l, 5] - R[t, l, 4]) * int(R[t, l, 7] - R[t, l, 6])
                 macs += a * int(dims[l, 5]) * L["f"] ** 2 * int(dims[l, 2])
         used.append(t)
-        el = time.perf_counter() - t0
-        if el >= min_s or el + el / len(used) > max_s:
+        el = time.perf_counter() - t1
+        if el >= cone_s[0] or el + el / len(used) > cone_s[1]:
             break
-    el = time.perf_counter() - t0
+    el = time.perf_counter() - t1
     rate = macs / el
-    return {"value": rate / exec_macs_per_frame, "unit": "frames/s", "cores": 1, "kind": "oracle",
-            "sample": (f"{len(used)} output rects of 2x2 px of frame 0, each through its full receptive "
-                       f"field of layers 0-15 ({macs / 1e9:.2f} GMAC in {el:.1f} s, float64, one thread); "
-                       f"frames/s = MAC rate / executed MAC per frame of {wl.tiling}"),
-            "gmac_per_s": rate / 1e9}
+    return {"value": round(1.0 / tiled_s, 4), "unit": "frames/s", "cores": threads,
+            "kind": "oracle",
+            "sample": (f"{frames} frame(s) (frame 0) of the oracle's fused-tile forward with tiling {wl.tiling}, "
+                       f"float64, layer loops on {threads} threads: {tiled_s:.2f} s per frame, "
+                       f"{exec_macs_per_frame / tiled_s / 1e9:.2f} GMAC/s"),
+            **info,
+            "single_thread": {"value": round(rate / exec_macs_per_frame, 5), "unit": "frames/s", "cores": 1,
+                              "sample": (f"{len(used)} output rects of 2x2 px of frame 0, each through its full "
+                                         f"receptive field of layers 0-15 ({macs / 1e9:.2f} GMAC in {el:.1f} s, "
+                                         f"float64, untiled); frames/s = MAC rate / executed MAC per frame"),
+                              "gmac_per_s": round(rate / 1e9, 4)}}
 
 
 def csrc_digest():
@@ -281,7 +333,7 @@ def config_search(args):
 
 def all_configs(args):
     """Every workload of the build (the paper's configurations and the six
-    cut x grid runs), each with every tile at once, with tile reuse, and one
+    cut x grid runs), each with every tile at once, with the stage partition, and one
     tile at a time (the paper's order): per-step latency (median, p10, p90 of HIP events on the
     launch stream around each mafat_run_network call, 10 warm-up steps
     first), frames/s at the median, executed TFLOP/s and its fraction of the
@@ -294,10 +346,10 @@ def all_configs(args):
     torch.cuda.set_device(0)
     ev = HipEvents()
     stream = torch.cuda.current_stream()
-    variants = ((False, 0), (True, 0), (False, 1))  # (tile reuse, tile batch: 0 all tiles at once)
-    for name, wl, reuse, tb in [(n, w, r, k) for n, w in W.WORKLOADS.items() for r, k in variants]:
+    variants = ((False, 0), (True, 0), (False, 1))  # (stage partition, tile batch: 0 all tiles at once)
+    for name, wl, part, tb in [(n, w, r, k) for n, w in W.WORKLOADS.items() for r, k in variants]:
         params = W.workload_inputs(wl)
-        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=reuse, packed_weights=True, tile_batch=tb)
+        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, stage_partition=part, packed_weights=True, tile_batch=tb)
         net = M.Network(plan, params, wl.batch, wl.dtype)
         x = net.input_tensor(params["x"])
         for _ in range(10):
@@ -317,12 +369,12 @@ def all_configs(args):
         us = sum(2 * plan.macs(g)[1] for g in range(plan.n_groups)) * wl.batch
         del net, x
         tp, _ = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch, wl.dtype,
-                                    params["x"], reuse=reuse, packed=True, tile_batch=tb)
+                                    params["x"], part=part, packed=True, tile_batch=tb)
         up, ums = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), untiled_groups(wl.layers), params,
                                       wl.batch, wl.dtype, params["x"])
         print(json.dumps({
             "workload": name, "input": f"{wl.h}x{wl.w}x{wl.c}", "batch": wl.batch, "dtype": wl.dtype,
-            "tiling": wl.tiling, "tile_reuse": reuse, "tile_batch": tb or "all",
+            "tiling": wl.tiling, "stage_partition": part, "tile_batch": tb or "all",
             "weights": "packed" if wl.dtype == "bf16" else "KRSC",
             "steps": n, "ms_p50": round(p50, 5), "ms_p10": round(p10, 5),
             "ms_p90": round(p90, 5), "frames_per_s": round(wl.batch / (p50 * 1e-3), 1),
@@ -356,7 +408,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-untiled", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
-                    help="skip the tile-reuse and HIP-graph timings (for profiler runs: only the plain steps)")
+                    help="skip the stage-partition and HIP-graph timings (for profiler runs: only the plain steps)")
     ap.add_argument("--all-configs", action="store_true",
                     help="latency quantiles, throughput and peak memory of every workload (one JSON line each)")
     ap.add_argument("--config-search", action="store_true",
@@ -392,8 +444,7 @@ def main():
     # The library's fast path: weights packed once for the patch kernels
     # (MAFAT_PLAN_PACKED_WEIGHTS, mafat_pack_weights at load, outside the
     # timed steps); the same steps with KRSC weights are reported beside.
-    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, packed_weights=True)
-    net = M.Network(plan, params, wl.batch, wl.dtype)
+    plan, net = bench_network(M, wl, params)
     x = net.input_tensor(params["x"])
     stream = torch.cuda.current_stream()
 
@@ -422,8 +473,10 @@ def main():
     ms_step = el / args.steps * 1e3
     fps = wl.batch * args.steps / el
 
-    def time_variant(**kw):
-        vplan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, **kw)
+    def time_variant(tiling=None, **kw):
+        # the headline's loop (warm-up steps, then host time over the timed
+        # steps between two synchronisations) on another plan
+        vplan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling if tiling is None else tiling, **kw)
         vnet = M.Network(vplan, params, wl.batch, wl.dtype)
         vx = vnet.input_tensor(params["x"])
         for _ in range(args.warmup):
@@ -435,11 +488,16 @@ def main():
         torch.cuda.synchronize()
         return (time.perf_counter() - t0) / args.steps * 1e3
 
-    reuse_ms = krsc_ms = None
+    partition_ms = krsc_ms = untiled_ms = None
+    if not args.no_untiled:
+        # The untiled layer-by-layer execution (every stage its own group on
+        # a 1x1 grid, same kernels, packed weights), timed exactly like the
+        # headline.
+        untiled_ms = time_variant(tiling=untiled_groups(wl.layers), packed_weights=True)
     if not args.no_extras:
-        # The same workload with tile reuse (each tile computes only its part
+        # The same workload with the stage partition (each tile computes only its part
         # of every stage output; no halo recompute), and with KRSC weights.
-        reuse_ms = time_variant(reuse=True, packed_weights=True)
+        partition_ms = time_variant(stage_partition=True, packed_weights=True)
         krsc_ms = time_variant()
 
     # The same step replayed from a captured HIP graph (reported beside the
@@ -515,27 +573,41 @@ def main():
             a, b = stages[g][ln[0]][0], stages[g][ln[-1]][1]
             f = sum(flops[g][s] for s in ln) * wl.batch
             t = stage_ms[g][ln[0]]  # a fused pair's kernel: the first stage's events
-            # the 3-channel first layer runs on the vector ALUs in fp32 (on
-            # the matrix cores in bf16), the rest on the matrix cores
-            vec = plan.layers[a]["op"] == "conv" and plan.shape(a)[2] == 3 and wl.dtype == "f32"
-            pk, bound = (PEAK_VALU_TFLOPS, "alu") if vec else (peak, "mfma")
+            # The 3-channel first layer (and a launch that starts with it)
+            # moves many bytes per flop: in bf16 it is bound by HBM (its
+            # matrix-core work, K = 27, is tiny), in fp32 by the vector ALUs;
+            # the other launches by the matrix cores.
+            first = plan.layers[a]["op"] == "conv" and plan.shape(a)[2] == 3
             nb = launch_bytes(sio[g], ln) * wl.batch
-            per_stage.append({"group": g, "layers": [a, b], "ms": round(t, 5),
-                              "gflop": round(f / 1e9, 4), "bound": bound, "peak_tflops": pk,
-                              "tflops": round(f / (t * 1e-3) / 1e12, 2) if t > 0 else None,
-                              "frac": round(f / (t * 1e-3) / 1e12 / pk, 4) if t > 0 else None,
-                              "hbm_mb": round(nb / 1e6, 3),
-                              "gbs": round(nb / (t * 1e-3) / 1e9, 1) if t > 0 else None,
-                              "hbm_frac": round(nb / (t * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) if t > 0 else None})
+            if first and wl.dtype == "f32":
+                pk, bound = PEAK_VALU_TFLOPS, "alu"
+            elif first:
+                pk, bound = PEAK_HBM_GBS, "hbm"
+            else:
+                pk, bound = peak, "mfma"
+            row = {"group": g, "layers": [a, b], "ms": round(t, 5), "gflop": round(f / 1e9, 4), "bound": bound,
+                   "tflops": round(f / (t * 1e-3) / 1e12, 2) if t > 0 else None,
+                   "frac_mfma": round(f / (t * 1e-3) / 1e12 / peak, 4) if t > 0 else None,
+                   "hbm_mb": round(nb / 1e6, 3),
+                   "gbs": round(nb / (t * 1e-3) / 1e9, 1) if t > 0 else None,
+                   "hbm_frac": round(nb / (t * 1e-3) / 1e9 / PEAK_HBM_GBS, 4) if t > 0 else None}
+            row["frac"] = row["hbm_frac"] if bound == "hbm" else (
+                round(f / (t * 1e-3) / 1e12 / pk, 4) if t > 0 else None)
+            per_stage.append(row)
     dom = max(per_stage, key=lambda r: r["ms"])
     dom_f = dom["gflop"] * 1e9
-    roof = {"bound": dom["bound"], "achieved": round(dom_f / (dom["ms"] * 1e-3) / 1e12, 2),
-            "peak": dom["peak_tflops"], "unit": "TFLOP/s",
-            "frac": round(dom_f / (dom["ms"] * 1e-3) / 1e12 / dom["peak_tflops"], 4), "traffic": None,
-            "kernel": f"stage layers {dom['layers'][0]}-{dom['layers'][1]} (group {dom['group']})",
-            "per_launch_gflop": dom["gflop"], "avg_ms": dom["ms"],
-            "timing": "kernel start/stop HIP events of the dispatch (hipExtLaunchKernel) on the launch stream, "
-                      "averaged over the event-timed steps of the whole network"}
+    if dom["bound"] == "hbm":
+        roof = {"bound": "hbm", "achieved": dom["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": dom["hbm_frac"], "traffic": None}
+    else:
+        pk = PEAK_VALU_TFLOPS if dom["bound"] == "alu" else peak
+        roof = {"bound": dom["bound"], "achieved": round(dom_f / (dom["ms"] * 1e-3) / 1e12, 2), "peak": pk,
+                "unit": "TFLOP/s", "frac": round(dom_f / (dom["ms"] * 1e-3) / 1e12 / pk, 4), "traffic": None}
+    roof.update({
+        "kernel": f"stage layers {dom['layers'][0]}-{dom['layers'][1]} (group {dom['group']})",
+        "per_launch_gflop": dom["gflop"], "per_launch_hbm_mb": dom["hbm_mb"], "avg_ms": dom["ms"],
+        "timing": "kernel start/stop HIP events of the dispatch (hipExtLaunchKernel) on the launch stream, "
+                  "averaged over the event-timed steps of the whole network"})
     tr = measured_traffic(wl.name, dom["layers"])
     if tr is not None:
         roof["traffic"] = tr["bytes"]
@@ -555,7 +627,7 @@ def main():
         "gflop_executed_per_step": round(exec_flops / 1e9, 3),
         "gflop_useful_per_step": round(useful_flops / 1e9, 3),
         "graph_ms_per_step": round(graph_ms, 5) if graph_ms is not None else None,
-        "tile_reuse_ms_per_step": round(reuse_ms, 5) if reuse_ms is not None else None,
+        "stage_partition_ms_per_step": round(partition_ms, 5) if partition_ms is not None else None,
         "krsc_weights_ms_per_step": round(krsc_ms, 5) if krsc_ms is not None else None,
         "step_ms_events": {q: round(float(np.percentile(step_ev_ms, v)), 5)
                            for q, v in (("p10", 10), ("p50", 50), ("p90", 90))},
@@ -565,17 +637,26 @@ def main():
         "per_stage": per_stage,
         "roofline": roof,
     }
+    shallow = [r for r in per_stage if r["bound"] == "hbm"]
+    if shallow:
+        # the one bandwidth-bound launch (the 3-channel first layer with its
+        # pool, or the fused launch that starts with it): achieved HBM rate
+        # of its algorithmic bytes against the 8 TB/s peak
+        r0 = shallow[0]
+        res["first_layer_hbm"] = {"layers": r0["layers"], "achieved_gbs": r0["gbs"], "peak_gbs": PEAK_HBM_GBS,
+                                  "frac": r0["hbm_frac"], "algorithmic_mb": r0["hbm_mb"], "ms": r0["ms"]}
 
     if not args.no_untiled:
         del net, x
-        tp, tms = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch,
-                                      wl.dtype, params["x"], packed=True)
+        tp, _ = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch,
+                                    wl.dtype, params["x"], packed=True)
         ug = untiled_groups(wl.layers)
-        up, ums = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), ug, params, wl.batch,
-                                      wl.dtype, params["x"], packed=True)
+        up, _ = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), ug, params, wl.batch,
+                                    wl.dtype, params["x"], packed=True)
         res["peak_mem_mib"] = round(tp / 2 ** 20, 2)
         res["untiled_peak_mem_mib"] = round(up / 2 ** 20, 2)
-        res["untiled_ms_per_step"] = round(ums, 5)
+        res["untiled_ms_per_step"] = round(untiled_ms, 5)
+        res["tiled_over_untiled_time"] = round(ms_step / untiled_ms, 4)
         if not args.no_extras:
             # The paper's execution order: one tile at a time through its
             # group (mafat_plan_set_tile_batch(plan, 1)): less workspace,

@@ -32,7 +32,8 @@
  *
  * Ownership and threading
  *   - A plan is created and destroyed by the library, read-only after
- *     creation, and may be shared between threads.
+ *     creation (except mafat_plan_set_tile_batch, which must not run while
+ *     other threads use the plan), and may be shared between threads.
  *   - Every device buffer (input, output, cut tensors, weights, scale, bias,
  *     workspace) is owned by the caller.  The library never allocates or
  *     frees device memory and never synchronises a stream; run functions only
@@ -108,19 +109,20 @@ int mafat_plan_create(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
 
 /* Plan flags (mafat_plan_create_flags). */
 enum {
-  /* Tile reuse: the data reuse between adjacent tiles that DeepThings adds
-   * to fused tile partitioning (section 3; NEXT step of the method), taken
-   * to whole stages.  The runtime runs a group's stages one after another
-   * over all tiles, so each stage's output is partitioned into the group's
-   * grid (floor boundaries, as the group output) and every tile computes
-   * only its own part, into a full tensor of the stage output in the
-   * workspace; the next stage reads the halo from the neighbouring tiles'
-   * parts instead of recomputing it.  Results equal the untiled network's
-   * (up to accumulation order); executed MACs equal the untiled ones;
-   * the workspace holds two full stage outputs per frame instead of every
-   * tile's intermediates.  mafat_plan_regions and the paper's memory model
-   * keep describing the plain partition. */
-  MAFAT_PLAN_TILE_REUSE = 1,
+  /* Stage partition: the data-reuse variant of fused tile partitioning
+   * (section 3: neighbouring tiles share the overlap they would otherwise
+   * both compute), taken to whole stages.  Every stage of a group runs over
+   * all tiles before the next one starts; each stage's output is split into
+   * the group's grid (floor boundaries, as the group output) and every tile
+   * computes only its own part, into a whole-tensor copy of the stage output
+   * in the workspace, from which the next stage reads its halo.  Nothing is
+   * computed twice, but nothing is fused per tile either: this is the
+   * untiled layer-by-layer execution with each layer's work split into the
+   * group's tiles.  Results equal the untiled network's (up to accumulation
+   * order); executed MACs equal the untiled ones; the workspace holds two
+   * whole stage outputs per frame.  mafat_plan_regions and the paper's
+   * memory model keep describing the plain (recomputing) partition. */
+  MAFAT_PLAN_STAGE_PARTITION = 1,
   /* Packed weights: for every conv layer whose mafat_packed_weights_size is
    * nonzero (bf16 3x3 layers run by the patch kernel), the w[layer] passed
    * to the run functions is that layer's weights repacked by
@@ -128,20 +130,22 @@ enum {
    * the nine taps' rows one contiguous run, so the kernel's weight loads
    * read whole cache lines.  The other layers keep KRSC.  Every batch runs
    * the stage configurations chosen for one frame (the packing follows
-   * their output-channel blocks). */
+   * their output-channel blocks).  A layout of this library, not of the
+   * paper. */
   MAFAT_PLAN_PACKED_WEIGHTS = 2
 };
 
-/* mafat_plan_create with flags (MAFAT_PLAN_TILE_REUSE and/or
- * MAFAT_PLAN_PACKED_WEIGHTS, or 0).  Errors: those of mafat_plan_create, and
- * EINVAL for unknown flags. */
+/* mafat_plan_create (sections 4 and 4.1) with flags
+ * (MAFAT_PLAN_STAGE_PARTITION and/or MAFAT_PLAN_PACKED_WEIGHTS, or 0).
+ * Errors: those of mafat_plan_create, and EINVAL for unknown flags. */
 int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
                             int32_t in_w, int32_t in_c, const int32_t* group_start,
                             int32_t n_groups, const int32_t* grid_rows,
                             const int32_t* grid_cols, int32_t flags, mafat_plan** out);
 
-/* Tile batches: run at most `tiles` tiles of a group at a time (0: all
- * tiles at once, the default).  mafat_run_group / mafat_run_network then
+/* Tile batches (the order of section 4, where the tiles of a group are
+ * processed one after another): run at most `tiles` tiles of a group at a
+ * time (0: all tiles at once, the default).  mafat_run_group / mafat_run_network then
  * take the group's tiles in row-major batches of `tiles`, each batch through
  * all of the group's stages before the next, and the workspace holds one
  * batch's intermediates instead of every tile's.  With tiles = 1 this is
@@ -150,12 +154,17 @@ int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_layers, int32_t
  * device to run fast.  Results are bit-identical to the default.  Call
  * before sizing the workspace; mafat_run_stage then fails (EUNSUPPORTED)
  * for groups split into several batches, and the per-stage events of
- * mafat_run_group enclose the stage's first to last launch (other stages'
+ * mafat_run_group_timed enclose the stage's first to last launch (other stages'
  * launches in between).  Errors: EINVAL (NULL, tiles < 0), EUNSUPPORTED
- * (a plan with MAFAT_PLAN_TILE_REUSE and 0 < tiles < a group's tile count). */
+ * (a plan with MAFAT_PLAN_STAGE_PARTITION and 0 < tiles < a group's tile
+ * count).  Not thread-safe: it rewrites the plan's per-tile workspace
+ * offsets, so no other thread may use the plan (run it, size its workspace)
+ * during the call; the plan is read-only again afterwards. */
 int mafat_plan_set_tile_batch(mafat_plan* plan, int32_t tiles);
 
-/* Bytes of the packed weights of conv layer `layer` in `dtype` (device
+/* Weight layout of this library's 3x3 kernels (no counterpart in the paper,
+ * whose layers hold their weights as the framework stores them).
+ * Bytes of the packed weights of conv layer `layer` in `dtype` (device
  * buffer, 16-byte aligned, caller-owned); 0 when the layer's weights are
  * passed as KRSC (plan without MAFAT_PLAN_PACKED_WEIGHTS, f32, 1x1 or
  * first-layer convolutions, pools).  Errors: EINVAL, EUNSUPPORTED (dtype). */
@@ -170,19 +179,31 @@ int mafat_packed_weights_size(const mafat_plan* plan, int32_t layer, int32_t dty
 int mafat_pack_weights(const mafat_plan* plan, int32_t layer, int32_t dtype, const void* w_krsc,
                        void* w_packed, void* stream);
 
-/* Frees a plan (NULL is ignored). */
+/* Frees a plan made by mafat_plan_create (NULL is ignored). */
 void mafat_plan_destroy(mafat_plan* plan);
 
-/* dims[6] = in_h, in_w, in_c, out_h, out_w, out_c of layer `layer`.
+/* Shape inference (section 4.1 describes each layer by its width, height,
+ * filter and stride; out = floor((in + 2p - f) / s) + 1):
+ * dims[6] = in_h, in_w, in_c, out_h, out_w, out_c of layer `layer`.
  * Errors: EINVAL. */
 int mafat_plan_layer_shape(const mafat_plan* plan, int32_t layer, int32_t dims[6]);
 
-/* Group g's first layer, number of layers and number of tiles.
+/* Layer groups and their grids (section 4: a group covers the layers up to
+ * a cut and has its own N x M tile grid):
+ * group g's first layer, number of layers and number of tiles.
  * Any output pointer may be NULL.  Errors: EINVAL. */
 int mafat_plan_group(const mafat_plan* plan, int32_t group, int32_t* first_layer,
                      int32_t* n_layers, int32_t* n_tiles);
 
-/* Region table of group g, [tile][layer - first_layer] (tiles row-major):
+/* Number of tiles (grid rows x columns) of group g's output partition
+ * (section 4: the group output is split into an N x M grid of tiles).
+ * Errors: EINVAL (NULL plan or pointer, group out of range). */
+int mafat_plan_num_tiles(const mafat_plan* plan, int32_t group, int32_t* n_tiles);
+
+/* Per-tile regions (section 4.1, the "Grid"/traversal function giving each
+ * tile's extent at every layer with its overlap; computed here as the exact
+ * receptive-field interval, clipped to the tensor).
+ * Region table of group g, [tile][layer - first_layer] (tiles row-major):
  * in_rects = the region of the layer's input the tile reads (halo included,
  * clipped to the tensor); out_rects = the region of the layer's output the
  * tile computes.  Within a tile, in_rects[k] == out_rects[k-1].  The last
@@ -192,21 +213,29 @@ int mafat_plan_group(const mafat_plan* plan, int32_t group, int32_t* first_layer
 int mafat_plan_regions(const mafat_plan* plan, int32_t group, mafat_rect* in_rects,
                        mafat_rect* out_rects, int64_t capacity);
 
-/* Multiply-accumulates of group g per frame: executed (every tile's
+/* Work accounting (section 4: overlapping regions are computed by every
+ * tile that needs them, so finer grids and deeper groups execute more).
+ * Multiply-accumulates of group g per frame: executed (every tile's
  * convolution outputs, halo recompute included, times c_in*f*f) and untiled
  * (the same layers on whole tensors).  Either pointer may be NULL. */
 int mafat_plan_macs(const mafat_plan* plan, int32_t group, int64_t* executed,
                     int64_t* untiled);
 
-/* Number of kernel stages group g runs and, for stage s, its first and last
+/* Execution stages of this library (a tile's layers run in order, section
+ * 4; a convolution and the max-pool after it run as one stage).
+ * Number of kernel stages group g runs and, for stage s, its first and last
  * layer (a convolution directly followed by a 2x2 max-pool in the same group
  * is one stage; every other layer is a stage of its own).  Used for
- * per-stage timing with the events argument of mafat_run_group. */
+ * per-stage timing with the events argument of mafat_run_group_timed.
+ * Errors: EINVAL. */
 int mafat_plan_stages(const mafat_plan* plan, int32_t group, int32_t* n_stages);
 int mafat_plan_stage_layers(const mafat_plan* plan, int32_t group, int32_t stage,
                             int32_t* first_layer, int32_t* last_layer);
 
-/* *fused = 1 if mafat_run_group / mafat_run_network run stage `stage` of
+/* Layer fusion inside a tile (section 3: a tile's sub-convolutions are fused
+ * across the layers of its group and run as one unit), taken down to a
+ * workgroup's block of pixels.
+ * *fused = 1 if mafat_run_group / mafat_run_network run stage `stage` of
  * group g together with stage + 1 in one kernel for this batch and dtype,
  * else 0.  This is the case for a bfloat16 3x3 convolution with 128
  * outputs and no pool whose next stage is a 1x1 convolution 128 -> 64 over
@@ -218,13 +247,18 @@ int mafat_plan_stage_layers(const mafat_plan* plan, int32_t group, int32_t stage
 int mafat_plan_stage_fused(const mafat_plan* plan, int32_t group, int32_t stage, int32_t batch,
                            int32_t dtype, int32_t* fused);
 
-/* Bytes of device workspace mafat_run_group / mafat_run_network need for
+/* Working memory of a group's tiles (section 4: a tile's intermediate
+ * results exist only while the tile is processed; section 4.1 sizes them).
+ * Bytes of device workspace mafat_run_group / mafat_run_network need for
  * `batch` frames in `dtype` (0 if none).  It holds the tiles' intermediate
  * activations between stages; the largest group decides.  Errors: EINVAL. */
 int mafat_workspace_size(const mafat_plan* plan, int32_t batch, int32_t dtype,
                          size_t* bytes);
 
-/* Runs group g on `batch` frames.
+/* Fused tile execution of one layer group (sections 3 and 4: every tile of
+ * the group's grid is pushed through all of the group's layers from its own
+ * input region, and the tile outputs are merged into the group output).
+ * Runs group g on `batch` frames.
  *   x          device, the group input: batch x H x W x C of the group's first
  *              layer input (the network input for g = 0, else the previous
  *              group's output)
@@ -234,22 +268,31 @@ int mafat_workspace_size(const mafat_plan* plan, int32_t batch, int32_t dtype,
  *              entries); entries of max-pool layers are ignored
  *   workspace  device, 256-byte aligned, at least mafat_workspace_size bytes
  *   stream     hipStream_t (NULL: the default stream)
- *   events     NULL, or 2 * n_stages hipEvent_t: events[2s] is recorded when
- *              the first kernel of stage s starts and events[2s+1] when its
- *              last kernel ends (timestamps of the kernel dispatches
- *              themselves, so timing adds nothing between kernels); entries
- *              may be NULL.  For a fused pair (mafat_plan_stage_fused) the
- *              first stage's events enclose the pair's kernel; the second
- *              stage's two events are recorded after it and time nothing
  * x and y must not overlap.  Errors: EINVAL, EUNSUPPORTED (dtype),
  * EWORKSPACE, EHIP. */
 int mafat_run_group(const mafat_plan* plan, int32_t group, int32_t batch, int32_t dtype,
                     const void* x, void* y, const void* const* w,
                     const float* const* scale, const float* const* bias,
-                    void* workspace, size_t ws_bytes, void* stream,
-                    void* const* events);
+                    void* workspace, size_t ws_bytes, void* stream);
 
-/* Runs only stage `stage` of group g (see mafat_plan_stages): the stage
+/* mafat_run_group (sections 3 and 4) with per-stage timestamps, for
+ * measurement.  events: 2 * n_stages hipEvent_t (host array): events[2s] is
+ * recorded when the first kernel of stage s starts and events[2s+1] when
+ * its last kernel ends (timestamps of the kernel dispatches themselves, so
+ * timing adds nothing between kernels); entries may be NULL.  For a fused
+ * pair (mafat_plan_stage_fused) the first stage's events enclose the pair's
+ * kernel; the second stage's two events are recorded after it and time
+ * nothing.  Errors: those of mafat_run_group, and EINVAL for a NULL events
+ * array. */
+int mafat_run_group_timed(const mafat_plan* plan, int32_t group, int32_t batch, int32_t dtype,
+                          const void* x, void* y, const void* const* w,
+                          const float* const* scale, const float* const* bias,
+                          void* workspace, size_t ws_bytes, void* stream,
+                          void* const* events);
+
+/* One stage of a group's fused tile execution (sections 3 and 4), for
+ * per-stage measurement.
+ * Runs only stage `stage` of group g (see mafat_plan_stages): the stage
  * reads the group input x (first stage) or the workspace, and writes the
  * group output y (last stage) or the workspace.  Calling it for stages 0 ..
  * n_stages-1 in order on one stream with the same workspace computes what
@@ -264,7 +307,10 @@ int mafat_run_stage(const mafat_plan* plan, int32_t group, int32_t stage, int32_
                     const float* const* scale, const float* const* bias, void* workspace,
                     size_t ws_bytes, void* stream);
 
-/* Runs every group in order on one stream: group 0 reads x, group g writes
+/* The whole network under a MAFAT configuration (section 4: group 1's tile
+ * outputs are merged into the cut tensor, which group 2 re-tiles with its
+ * own grid).
+ * Runs every group in order on one stream: group 0 reads x, group g writes
  * cut_bufs[g] (n_groups-1 caller-owned tensors, each the shape of its group's
  * output) and group g+1 reads it; the last group writes y.  Same argument
  * conventions and errors as mafat_run_group. */
@@ -293,7 +339,7 @@ int mafat_run_network(const mafat_plan* plan, int32_t batch, int32_t dtype,
  *     one batch's.
  *   model MAFAT_MEM_DEVICE_SEQ: the device memory of the same plan run one
  *     tile at a time (tile batch 1, the paper's execution order), whatever
- *     the plan's tile batch; for groups with tile reuse, their workspace as
+ *     the plan's tile batch; for groups with the stage partition, their workspace as
  *     MAFAT_MEM_DEVICE.  With mafat_get_config this is the paper's search
  *     under a device-memory limit.
  * *bytes receives the prediction.  Errors: EINVAL (null plan or pointer,
@@ -320,10 +366,12 @@ int mafat_get_config(const mafat_layer* layers, int32_t n_layers, int32_t in_h, 
                      int32_t n_grids, int32_t second_grid, int32_t* out_cut, int32_t* out_grid1,
                      int32_t* out_grid2, int64_t* out_pred, int32_t* out_fits);
 
-/* Static text of a status code. */
+/* Error reporting of this library (no counterpart in the paper).
+ * Static text of a status code. */
 const char* mafat_status_string(int status);
 
-/* Thread-local detail of the last failing call on this thread ("" if none). */
+/* Error reporting of this library (no counterpart in the paper).
+ * Thread-local detail of the last failing call on this thread ("" if none). */
 const char* mafat_last_error(void);
 
 #ifdef __cplusplus

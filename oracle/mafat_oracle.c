@@ -34,6 +34,7 @@
 #include "mafat_oracle.h"
 
 #include <math.h>
+#include <pthread.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -146,14 +147,14 @@ static double pool_pixel(const view_t* in, const orc_layer* L, int y, int x,
   return round_bf16 ? orc_round_bf16(m) : m;
 }
 
-/* Computes layer l on the output rectangle [oy0,oy1) x [ox0,ox1) into the
- * dense buffer out (rect-local NHWC). */
-static void layer_rect(const view_t* in, const orc_layer* L, int out_c,
+/* Rows [ya, yb) of layer l's output rectangle [oy0,oy1) x [ox0,ox1), into
+ * the dense buffer out (rect-local NHWC). */
+static void layer_rows(const view_t* in, const orc_layer* L, int out_c,
                        const double* wt, const double* scale, const double* bias,
-                       int round_bf16, int oy0, int oy1, int ox0, int ox1,
+                       int round_bf16, int oy0, int ya, int yb, int ox0, int ox1,
                        double* out) {
   const int ow = ox1 - ox0;
-  for (int y = oy0; y < oy1; ++y)
+  for (int y = ya; y < yb; ++y)
     for (int x = ox0; x < ox1; ++x) {
       double* o = out + ((size_t)(y - oy0) * ow + (x - ox0)) * out_c;
       for (int ch = 0; ch < out_c; ++ch)
@@ -161,6 +162,67 @@ static void layer_rect(const view_t* in, const orc_layer* L, int out_c,
                     ? conv_pixel(in, L, wt, scale[ch], bias[ch], y, x, ch, round_bf16)
                     : pool_pixel(in, L, y, x, ch, round_bf16);
     }
+}
+
+/* Worker threads for layer_rect (orc_set_threads): the output rows of a
+ * layer are split into contiguous bands, one per thread.  Every output
+ * element is still computed by conv_pixel / pool_pixel alone, in the same
+ * summation order, so the result does not depend on the thread count. */
+static int g_threads = 1;
+
+int orc_set_threads(int n) {
+  if (n < 1) return ORC_EINVAL;
+  g_threads = n > 256 ? 256 : n;
+  return ORC_OK;
+}
+
+typedef struct {
+  view_t in;  /* private copy: its err points at this band's flag */
+  const orc_layer* L;
+  int out_c;
+  const double *wt, *scale, *bias;
+  int round_bf16, oy0, ya, yb, ox0, ox1;
+  double* out;
+  int err;
+} band_t;
+
+static void* band_run(void* arg) {
+  band_t* b = (band_t*)arg;
+  layer_rows(&b->in, b->L, b->out_c, b->wt, b->scale, b->bias, b->round_bf16, b->oy0, b->ya, b->yb,
+             b->ox0, b->ox1, b->out);
+  return NULL;
+}
+
+/* Computes layer l on the output rectangle [oy0,oy1) x [ox0,ox1) into the
+ * dense buffer out (rect-local NHWC). */
+static void layer_rect(const view_t* in, const orc_layer* L, int out_c,
+                       const double* wt, const double* scale, const double* bias,
+                       int round_bf16, int oy0, int oy1, int ox0, int ox1,
+                       double* out) {
+  int nt = g_threads < oy1 - oy0 ? g_threads : oy1 - oy0;
+  if (nt <= 1) {
+    layer_rows(in, L, out_c, wt, scale, bias, round_bf16, oy0, oy0, oy1, ox0, ox1, out);
+    return;
+  }
+  band_t bands[256];
+  pthread_t tid[256];
+  int started[256];
+  for (int k = 0; k < nt; ++k) {
+    band_t* b = &bands[k];
+    b->in = *in;
+    b->err = 0;
+    b->in.err = &b->err;
+    b->L = L; b->out_c = out_c; b->wt = wt; b->scale = scale; b->bias = bias;
+    b->round_bf16 = round_bf16; b->oy0 = oy0; b->ox0 = ox0; b->ox1 = ox1; b->out = out;
+    b->ya = oy0 + (int)((int64_t)(oy1 - oy0) * k / nt);
+    b->yb = oy0 + (int)((int64_t)(oy1 - oy0) * (k + 1) / nt);
+    started[k] = pthread_create(&tid[k], NULL, band_run, b) == 0;
+    if (!started[k]) band_run(b); /* no thread: run the band here */
+  }
+  for (int k = 0; k < nt; ++k) {
+    if (started[k]) pthread_join(tid[k], NULL);
+    if (bands[k].err) *in->err = bands[k].err;
+  }
 }
 
 /* ------------------------------------------------------------------ */

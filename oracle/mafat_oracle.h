@@ -101,6 +101,12 @@ int orc_forward_rect(const orc_layer* layers, int n, int h, int w, int c,
 /* bfloat16 round-to-nearest-even of a value (via float32), as a double. */
 double orc_round_bf16(double v);
 
+/* Number of threads the layer loops use (default 1): each layer's output
+ * rows are split into contiguous bands, every element still computed alone
+ * in its fixed summation order, so results do not depend on it.  Errors:
+ * ORC_EINVAL for n < 1 (n is capped at 256). */
+int orc_set_threads(int n);
+
 #ifdef __cplusplus
 }
 #endif

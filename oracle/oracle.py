@@ -43,7 +43,7 @@ def build(force: bool = False) -> str:
             os.path.getmtime(_SRC), os.path.getmtime(os.path.join(_HERE, "mafat_oracle.h"))):
         tmp = _LIB + f".tmp{os.getpid()}"
         subprocess.check_call(["gcc", "-std=c99", "-O2", "-ffp-contract=off", "-fno-fast-math",
-                               "-Wall", "-Wextra", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"])
+                               "-Wall", "-Wextra", "-fPIC", "-shared", "-pthread", _SRC, "-o", tmp, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -64,6 +64,7 @@ def lib():
         L.orc_regions_bruteforce.argtypes = [lp, i, i, i, i, ip, i, ip, ip, ip]
         L.orc_forward_tiled.argtypes = [lp, i, i, i, i, i, ip, i, ip, ip, dp, dpp, dpp, dpp, i, dp, dpp]
         L.orc_forward_rect.argtypes = [lp, i, i, i, i, dp, dpp, dpp, dpp, i, i, i, i, i, dp]
+        L.orc_set_threads.argtypes = [i]
         L.orc_round_bf16.argtypes = [ctypes.c_double]
         L.orc_round_bf16.restype = ctypes.c_double
         _lib = L
@@ -196,6 +197,11 @@ def forward_rect(layers, h, w, c, x1, params, oy0, oy1, ox0, ox1, round_bf16=Fal
     _check(lib().orc_forward_rect(_layers(layers), n, h, w, c, xp, wp, sp, bp, int(round_bf16),
                                   oy0, oy1, ox0, ox1, y.ctypes.data_as(ctypes.POINTER(ctypes.c_double))))
     return y
+
+
+def set_threads(n: int) -> None:
+    """Threads of the layer loops (output-row bands; results unchanged)."""
+    _check(lib().orc_set_threads(int(n)))
 
 
 def round_bf16(v: float) -> float:

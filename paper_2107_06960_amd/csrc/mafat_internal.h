@@ -53,10 +53,10 @@ struct Group {
   int rows, cols, ntiles;
   std::vector<mafat_rect> in_r, out_r;  // [tile * nlayers + (l - l0)]
   std::vector<Stage> stages;
-  int64_t scratch_elems;  // per tile per scratch buffer (tile reuse: per scratch buffer)
+  int64_t scratch_elems;  // per tile per scratch buffer (stage partition: per scratch buffer)
   int nbufs;              // scratch buffers (0, 1 or 2)
   int64_t scratch_frame;  // scratch elements of one frame
-  bool reuse;             // tile reuse: every stage output computed once (full tensors)
+  bool partition;         // stage partition: every stage output computed once (full tensors)
   int tile_batch;         // tiles run through the stages together (ntiles unless
                           // mafat_plan_set_tile_batch set fewer); scratch per batch
   int64_t macs_exec, macs_untiled;

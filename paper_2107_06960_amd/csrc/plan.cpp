@@ -47,9 +47,9 @@ void back_project(int a, int b, int F, int S, int P, int E, int* ia, int* ib) {
   *ib = std::min(E, (b - 1) * S - P + F);
 }
 
-int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool reuse, Group* out) {
+int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool partition, Group* out) {
   Group G;
-  G.reuse = reuse;
+  G.partition = partition;
   G.l0 = g0; G.l1 = g1; G.rows = rows; G.cols = cols; G.ntiles = rows * cols;
   const int nl = g1 - g0 + 1;
   const auto& dl = plan.dims[g1];
@@ -119,7 +119,7 @@ int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool reuse
   const int ns = static_cast<int>(G.stages.size());
   G.nbufs = std::min(2, ns - 1);
   G.scratch_elems = 0;
-  if (reuse) {
+  if (partition) {
     // Tile reuse (the data reuse between adjacent tiles of DeepThings'
     // fused tile partitioning, taken to the whole stage): the stages run one
     // after another over all tiles, so every stage's output is partitioned
@@ -212,7 +212,7 @@ int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool reuse
   return MAFAT_OK;
 }
 
-// Tile batches of K tiles (fused tile partitioning without tile reuse):
+// Tile batches of K tiles (fused tile partitioning without the stage partition):
 // tile t's intermediates live in slot t mod K of each scratch buffer, so
 // the workspace holds K tiles ([buffer][slot][scratch_elems] per frame).
 void set_tile_batch(Group& G, int K) {
@@ -247,7 +247,7 @@ extern "C" int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_laye
   clear_error();
   if (!out) { set_error("out is NULL"); return MAFAT_EINVAL; }
   *out = nullptr;
-  if (flags & ~(MAFAT_PLAN_TILE_REUSE | MAFAT_PLAN_PACKED_WEIGHTS)) {
+  if (flags & ~(MAFAT_PLAN_STAGE_PARTITION | MAFAT_PLAN_PACKED_WEIGHTS)) {
     set_error("unknown plan flags");
     return MAFAT_EINVAL;
   }
@@ -300,7 +300,7 @@ extern "C" int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_laye
       }
       Group G;
       const int rc = build_group(*plan, g0, end - 1, grid_rows[g], grid_cols[g],
-                                 (flags & MAFAT_PLAN_TILE_REUSE) != 0, &G);
+                                 (flags & MAFAT_PLAN_STAGE_PARTITION) != 0, &G);
       if (rc != MAFAT_OK) { delete plan; return rc; }
       plan->groups.push_back(std::move(G));
     }
@@ -328,6 +328,16 @@ extern "C" int mafat_plan_group(const mafat_plan* plan, int32_t group, int32_t* 
   if (first_layer) *first_layer = G.l0;
   if (n_layers) *n_layers = G.l1 - G.l0 + 1;
   if (n_tiles) *n_tiles = G.ntiles;
+  return MAFAT_OK;
+}
+
+extern "C" int mafat_plan_num_tiles(const mafat_plan* plan, int32_t group, int32_t* n_tiles) {
+  clear_error();
+  if (!plan || !n_tiles || group < 0 || group >= static_cast<int>(plan->groups.size())) {
+    set_error("plan and n_tiles must be non-NULL and the group in range");
+    return MAFAT_EINVAL;
+  }
+  *n_tiles = plan->groups[group].ntiles;
   return MAFAT_OK;
 }
 
@@ -377,12 +387,12 @@ extern "C" int mafat_plan_set_tile_batch(mafat_plan* plan, int32_t tiles) {
     return MAFAT_EINVAL;
   }
   for (const Group& G : plan->groups)
-    if (G.reuse && tiles > 0 && tiles < G.ntiles) {
-      set_error("tile reuse needs every tile of a stage before the next stage: no tile batches");
+    if (G.partition && tiles > 0 && tiles < G.ntiles) {
+      set_error("the stage partition needs every tile of a stage before the next stage: no tile batches");
       return MAFAT_EUNSUPPORTED;
     }
   for (Group& G : plan->groups)
-    if (!G.reuse) set_tile_batch(G, (tiles == 0) ? G.ntiles : std::min<int>(tiles, G.ntiles));
+    if (!G.partition) set_tile_batch(G, (tiles == 0) ? G.ntiles : std::min<int>(tiles, G.ntiles));
   return MAFAT_OK;
 }
 

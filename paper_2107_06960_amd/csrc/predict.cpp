@@ -86,7 +86,7 @@ int64_t device_bytes(const mafat_plan& P, int batch, int dtype, bool one_tile) {
     mafat_workspace_size(&P, batch, dtype, &ws);
   } else {  // the workspace of tile batch 1: one tile slot per scratch buffer
     for (const Group& G : P.groups) {
-      const int64_t frame = G.reuse ? G.scratch_frame : static_cast<int64_t>(G.nbufs) * G.scratch_elems;
+      const int64_t frame = G.partition ? G.scratch_frame : static_cast<int64_t>(G.nbufs) * G.scratch_elems;
       ws = std::max(ws, (static_cast<size_t>(batch) * frame * esz + 255) & ~static_cast<size_t>(255));
     }
   }

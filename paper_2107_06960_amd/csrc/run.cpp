@@ -356,7 +356,7 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
   // Tile batches (mafat_plan_set_tile_batch): tiles [b0, b0 + K) go through
   // all stages, then the next K tiles; the workspace holds K tiles.
   const int K = G.tile_batch;
-  const int64_t bstride = G.reuse ? G.scratch_elems : static_cast<int64_t>(K) * G.scratch_elems;
+  const int64_t bstride = G.partition ? G.scratch_elems : static_cast<int64_t>(K) * G.scratch_elems;
   std::vector<char> started(static_cast<size_t>(s_end - s_begin), 0);  // start event recorded
   for (int b0 = 0; b0 < G.ntiles; b0 += K) {
     const int b1 = std::min(G.ntiles, b0 + K);
@@ -552,19 +552,37 @@ int check_common(const mafat_plan* plan, int batch, int dtype) {
 
 using namespace mafat;
 
-extern "C" int mafat_run_group(const mafat_plan* plan, int32_t group, int32_t batch, int32_t dtype,
-                               const void* x, void* y, const void* const* w,
-                               const float* const* scale, const float* const* bias,
-                               void* workspace, size_t ws_bytes, void* stream,
-                               void* const* events) {
-  clear_error();
+namespace mafat {
+namespace {
+int run_group_checked(const mafat_plan* plan, int group, int batch, int dtype, const void* x, void* y,
+                      const void* const* w, const float* const* scale, const float* const* bias, void* workspace,
+                      size_t ws_bytes, void* stream, void* const* events) {
   int rc = check_common(plan, batch, dtype);
   if (rc != MAFAT_OK) return rc;
   if (group < 0 || group >= static_cast<int>(plan->groups.size()))
     return fail(MAFAT_EINVAL, "group index out of range");
   return run_group_impl(plan, group, 0, static_cast<int>(plan->groups[group].stages.size()), batch, dtype, x, y,
-                        w, scale, bias, workspace, ws_bytes,
-                        static_cast<hipStream_t>(stream), events);
+                        w, scale, bias, workspace, ws_bytes, static_cast<hipStream_t>(stream), events);
+}
+}  // namespace
+}  // namespace mafat
+
+extern "C" int mafat_run_group(const mafat_plan* plan, int32_t group, int32_t batch, int32_t dtype,
+                               const void* x, void* y, const void* const* w,
+                               const float* const* scale, const float* const* bias,
+                               void* workspace, size_t ws_bytes, void* stream) {
+  clear_error();
+  return run_group_checked(plan, group, batch, dtype, x, y, w, scale, bias, workspace, ws_bytes, stream, nullptr);
+}
+
+extern "C" int mafat_run_group_timed(const mafat_plan* plan, int32_t group, int32_t batch, int32_t dtype,
+                                     const void* x, void* y, const void* const* w,
+                                     const float* const* scale, const float* const* bias,
+                                     void* workspace, size_t ws_bytes, void* stream,
+                                     void* const* events) {
+  clear_error();
+  if (!events) return fail(MAFAT_EINVAL, "events is NULL (use mafat_run_group to run without timestamps)");
+  return run_group_checked(plan, group, batch, dtype, x, y, w, scale, bias, workspace, ws_bytes, stream, events);
 }
 
 extern "C" int mafat_run_stage(const mafat_plan* plan, int32_t group, int32_t stage, int32_t batch,

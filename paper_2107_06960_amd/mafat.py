@@ -27,16 +27,16 @@ MAFAT_CONV, MAFAT_MAXPOOL = 0, 1
 MAFAT_ACT_LINEAR, MAFAT_ACT_LEAKY01 = 0, 1
 MAFAT_F32, MAFAT_BF16 = 0, 1
 MAFAT_MEM_DEVICE, MAFAT_MEM_PAPER, MAFAT_MEM_DEVICE_SEQ = 0, 1, 2
-MAFAT_PLAN_TILE_REUSE, MAFAT_PLAN_PACKED_WEIGHTS = 1, 2
+MAFAT_PLAN_STAGE_PARTITION, MAFAT_PLAN_PACKED_WEIGHTS = 1, 2
 MEM_MODELS = {"device": MAFAT_MEM_DEVICE, "paper": MAFAT_MEM_PAPER, "device_seq": MAFAT_MEM_DEVICE_SEQ}
 DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
 
 # Every symbol include/mafat.h declares.
 EXPORTS = ("mafat_plan_create", "mafat_plan_create_flags", "mafat_plan_destroy",
            "mafat_packed_weights_size", "mafat_pack_weights", "mafat_plan_layer_shape", "mafat_plan_group",
-           "mafat_plan_regions", "mafat_plan_macs", "mafat_plan_stages", "mafat_plan_stage_layers",
+           "mafat_plan_num_tiles", "mafat_plan_regions", "mafat_plan_macs", "mafat_plan_stages", "mafat_plan_stage_layers",
            "mafat_plan_stage_fused", "mafat_plan_set_tile_batch",
-           "mafat_workspace_size", "mafat_run_group", "mafat_run_stage", "mafat_run_network",
+           "mafat_workspace_size", "mafat_run_group", "mafat_run_group_timed", "mafat_run_stage", "mafat_run_network",
            "mafat_predict_mem", "mafat_get_config", "mafat_status_string", "mafat_last_error")
 
 
@@ -82,6 +82,7 @@ def lib():
         L.mafat_plan_destroy.restype = None
         L.mafat_plan_layer_shape.argtypes = [planp, i32, i32p]
         L.mafat_plan_group.argtypes = [planp, i32, i32p, i32p, i32p]
+        L.mafat_plan_num_tiles.argtypes = [planp, i32, i32p]
         L.mafat_plan_regions.argtypes = [planp, i32, ctypes.POINTER(mafat_rect),
                                          ctypes.POINTER(mafat_rect), i64]
         L.mafat_plan_macs.argtypes = [planp, i32, ctypes.POINTER(i64), ctypes.POINTER(i64)]
@@ -90,7 +91,8 @@ def lib():
         L.mafat_plan_stage_fused.argtypes = [planp, i32, i32, i32, i32, i32p]
         L.mafat_plan_set_tile_batch.argtypes = [planp, i32]
         L.mafat_workspace_size.argtypes = [planp, i32, i32, ctypes.POINTER(sz)]
-        L.mafat_run_group.argtypes = [planp, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp, vpp]
+        L.mafat_run_group.argtypes = [planp, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp]
+        L.mafat_run_group_timed.argtypes = [planp, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp, vpp]
         L.mafat_run_stage.argtypes = [planp, i32, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp]
         L.mafat_run_network.argtypes = [planp, i32, i32, vp, vp, vpp, vpp, vpp, vpp, vp, sz, vp]
         i64p = ctypes.POINTER(i64)
@@ -125,7 +127,8 @@ def _ptrs(vals):
 
 def mafat_plan_create(layers, in_h, in_w, in_c, group_start, grid_rows, grid_cols, flags=0):
     """Returns a plan handle (int); raises MafatError with the library's status.
-    flags: 0 or MAFAT_PLAN_TILE_REUSE (mafat_plan_create_flags)."""
+    flags: 0, or MAFAT_PLAN_STAGE_PARTITION and/or MAFAT_PLAN_PACKED_WEIGHTS
+    (mafat_plan_create_flags)."""
     n = len(layers)
     arr = (mafat_layer * n)()
     for k, L in enumerate(layers):
@@ -176,6 +179,12 @@ def mafat_plan_group(plan, group):
     return a.value, b.value, c.value
 
 
+def mafat_plan_num_tiles(plan, group):
+    n = ctypes.c_int32()
+    _check("mafat_plan_num_tiles", lib().mafat_plan_num_tiles(plan, group, ctypes.byref(n)))
+    return n.value
+
+
 def mafat_plan_regions(plan, group):
     """int32 array (tiles, layers_in_group, 8): in y0,y1,x0,x1 then out y0,y1,x0,x1."""
     _, nl, nt = mafat_plan_group(plan, group)
@@ -221,16 +230,21 @@ def mafat_workspace_size(plan, batch, dtype):
     return n.value
 
 
-def mafat_run_group(plan, group, batch, dtype, x, y, w, scale, bias, workspace, ws_bytes, stream,
-                    events=None):
+def mafat_run_group(plan, group, batch, dtype, x, y, w, scale, bias, workspace, ws_bytes, stream):
     """x, y, workspace: device pointers (int); w/scale/bias: lists of device
-    pointers indexed by layer (None for pools); stream: hipStream_t (int);
-    events: None or a list of 2 * n_stages hipEvent_t handles (start and end
-    of each stage's kernels; entries may be None)."""
-    ev = _ptrs(events) if events is not None else None
+    pointers indexed by layer (None for pools); stream: hipStream_t (int)."""
     _check("mafat_run_group",
            lib().mafat_run_group(plan, group, batch, dtype, x, y, _ptrs(w), _ptrs(scale), _ptrs(bias),
-                                 workspace, ws_bytes, stream, ev))
+                                 workspace, ws_bytes, stream))
+
+
+def mafat_run_group_timed(plan, group, batch, dtype, x, y, w, scale, bias, workspace, ws_bytes, stream,
+                          events):
+    """mafat_run_group plus events: a list of 2 * n_stages hipEvent_t
+    handles (start and end of each stage's kernels; entries may be None)."""
+    _check("mafat_run_group_timed",
+           lib().mafat_run_group_timed(plan, group, batch, dtype, x, y, _ptrs(w), _ptrs(scale), _ptrs(bias),
+                                       workspace, ws_bytes, stream, _ptrs(events)))
 
 
 def mafat_run_stage(plan, group, stage, batch, dtype, x, y, w, scale, bias, workspace, ws_bytes, stream):
@@ -289,9 +303,10 @@ class Plan:
     """A plan for a layer stack, an input shape and a tiling spec such as
     ``"5x5/8/2x2"`` (section 5.1 notation) or explicit group lists."""
 
-    def __init__(self, layers, in_hwc, tiling="1x1/NoCut", reuse=False, packed_weights=False, tile_batch=0):
+    def __init__(self, layers, in_hwc, tiling="1x1/NoCut", stage_partition=False, packed_weights=False,
+                 tile_batch=0):
         self.layers = list(layers)
-        self.reuse = bool(reuse)
+        self.stage_partition = bool(stage_partition)
         self.packed_weights = bool(packed_weights)
         self.tile_batch = int(tile_batch)
         self.h, self.w, self.c = in_hwc
@@ -299,7 +314,7 @@ class Plan:
             if isinstance(tiling, str) else tiling
         self.handle = mafat_plan_create(self.layers, self.h, self.w, self.c, self.group_start,
                                         self.rows, self.cols,
-                                        (MAFAT_PLAN_TILE_REUSE if self.reuse else 0) |
+                                        (MAFAT_PLAN_STAGE_PARTITION if self.stage_partition else 0) |
                                         (MAFAT_PLAN_PACKED_WEIGHTS if self.packed_weights else 0))
         self.n_groups = len(self.group_start)
         if self.tile_batch:
@@ -319,6 +334,9 @@ class Plan:
 
     def group(self, g):
         return mafat_plan_group(self.handle, g)
+
+    def num_tiles(self, g):
+        return mafat_plan_num_tiles(self.handle, g)
 
     def regions(self, g):
         return mafat_plan_regions(self.handle, g)
@@ -408,9 +426,12 @@ class Network:
         return self.y
 
     def run_group(self, g, x, y, stream=None, events=None):
-        mafat_run_group(self.plan.handle, g, self.batch, self.code, x.data_ptr(), y.data_ptr(),
-                        self._wp, self._sp, self._bp, self.ws.data_ptr(), self.ws_bytes,
-                        _stream_handle(stream), events)
+        args = (self.plan.handle, g, self.batch, self.code, x.data_ptr(), y.data_ptr(),
+                self._wp, self._sp, self._bp, self.ws.data_ptr(), self.ws_bytes, _stream_handle(stream))
+        if events is None:
+            mafat_run_group(*args)
+        else:
+            mafat_run_group_timed(*args, events)
 
     def run_stage(self, g, s, x, y, stream=None):
         mafat_run_stage(self.plan.handle, g, s, self.batch, self.code, x.data_ptr(), y.data_ptr(),

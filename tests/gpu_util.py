@@ -12,12 +12,12 @@ def require_gpu():
         pytest.skip("no GPU")
 
 
-def run_gpu(layers, h, w, c, params, tiling, batch, dtype, x=None, want_cuts=True, sentinel=True, reuse=False):
+def run_gpu(layers, h, w, c, params, tiling, batch, dtype, x=None, want_cuts=True, sentinel=True, part=False):
     """Runs the library (mafat_run_network) and returns float64 numpy output
     (and the cut tensors)."""
     import torch
     from paper_2107_06960_amd import mafat as M
-    plan = M.Plan(layers, (h, w, c), tiling, reuse=reuse)
+    plan = M.Plan(layers, (h, w, c), tiling, stage_partition=part)
     net = M.Network(plan, params, batch, dtype)
     xt = net.input_tensor(params["x"] if x is None else x)
     if sentinel:

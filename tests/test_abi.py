@@ -60,6 +60,7 @@ def test_plan_regions_and_macs_match_oracle(lib, orc, name):
     for g in range(len(gs)):
         assert np.array_equal(plan.regions(g), R[g])
         assert plan.macs(g) == macs[g]
+        assert plan.num_tiles(g) == R[g].shape[0] == r[g] * c[g]
     dims = orc.shapes(wl.layers, wl.h, wl.w, wl.c)
     for l in range(len(wl.layers)):
         assert plan.shape(l) == tuple(dims[l])
@@ -112,7 +113,7 @@ def test_stages_fuse_conv_and_following_pool(lib):
 def test_fused_pair_detection(lib):
     # bf16: layer 4 (3x3, 64 -> 128) runs with layer 5 (1x1, 128 -> 64) in
     # one kernel, whatever the batch or plan flags; f32 and other shapes not
-    for flags in ({}, {"reuse": True}, {"packed_weights": True}):
+    for flags in ({}, {"stage_partition": True}, {"packed_weights": True}):
         plan = M.Plan(W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2", **flags)
         for batch in (1, 8):
             got = [plan.stage_fused(0, s, batch, "bf16") for s in range(len(plan.stages(0)))]
@@ -156,9 +157,9 @@ def test_tile_batch(lib):
     # the stage layout is unchanged; errors
     assert one.stages(0) == full.stages(0)
     with pytest.raises(M.MafatError) as e:
-        M.Plan(layers, hwc, "5x5/NoCut", reuse=True, tile_batch=3)
+        M.Plan(layers, hwc, "5x5/NoCut", stage_partition=True, tile_batch=3)
     assert e.value.rc == M.MAFAT_EUNSUPPORTED
-    M.Plan(layers, hwc, "5x5/NoCut", reuse=True, tile_batch=25)   # every tile at once: allowed
+    M.Plan(layers, hwc, "5x5/NoCut", stage_partition=True, tile_batch=25)   # every tile at once: allowed
     assert M.lib().mafat_plan_set_tile_batch(full.handle, -1) == M.MAFAT_EINVAL
     assert M.lib().mafat_plan_set_tile_batch(None, 1) == M.MAFAT_EINVAL
     # back to all tiles at once
@@ -176,12 +177,12 @@ def test_workspace_size(lib):
     assert one.workspace_size(3, "f32") == 0
 
 
-def test_tile_reuse_plan(lib):
-    # tile reuse: executed MACs equal the untiled ones (even extents) and
+def test_stage_partition_plan(lib):
+    # stage partition: executed MACs equal the untiled ones (even extents) and
     # never exceed them (odd extents: the rows/columns a pool drops are not
     # computed); the workspace is two full stage outputs per frame
     for tiling in ("5x5/8/2x2", "3x3/NoCut", "4x4/12/1x1"):
-        plan = M.Plan(W.YOLOV2_16, (608, 608, 3), tiling, reuse=True)
+        plan = M.Plan(W.YOLOV2_16, (608, 608, 3), tiling, stage_partition=True)
         plain = M.Plan(W.YOLOV2_16, (608, 608, 3), tiling)
         for g in range(plan.n_groups):
             ex, un = plan.macs(g)
@@ -196,7 +197,7 @@ def test_tile_reuse_plan(lib):
         big = (big + 127) // 128 * 128
         nst = max(len(plan.stages(g)) for g in range(plan.n_groups))
         assert plan.workspace_size(3, "bf16") == (3 * 2 * big * 2 + 255) // 256 * 256 or nst < 3
-    odd = M.Plan(W.YOLOV2_16, (71, 93, 3), "3x2/8/2x2", reuse=True)
+    odd = M.Plan(W.YOLOV2_16, (71, 93, 3), "3x2/8/2x2", stage_partition=True)
     for g in range(odd.n_groups):
         ex, un = odd.macs(g)
         assert 0 < ex <= un
@@ -261,6 +262,7 @@ def test_plan_create_error_codes(lib):
     assert _create_rc([(0, 8, 3, 1, 1, 7)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED  # activation
     assert _create_rc([(9, 8, 3, 1, 1, 1)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EINVAL        # op
     assert _create_rc([conv3, pool], 16, 16, 3, [0], [9], [1]) == M.MAFAT_ESHAPE               # grid > out
+    assert b"grid 9x1" in M.lib().mafat_last_error()
     assert _create_rc([conv3, pool], 16, 16, 3, [1], [1], [1]) == M.MAFAT_ESHAPE               # start != 0
     assert _create_rc([conv3, pool], 16, 16, 3, [0, 0], [1, 1], [1, 1]) == M.MAFAT_ESHAPE      # not increasing
     assert _create_rc([conv3, pool], 16, 16, 3, [0, 2], [1, 1], [1, 1]) == M.MAFAT_ESHAPE      # start >= n
@@ -269,7 +271,17 @@ def test_plan_create_error_codes(lib):
     assert _create_rc([conv3], 40000, 4, 3, [0], [1], [1]) == M.MAFAT_ESHAPE                   # > 32767
     assert _create_rc([], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EINVAL
     assert M.lib().mafat_plan_create(None, 1, 1, 1, 1, None, 1, None, None, None) == M.MAFAT_EINVAL
-    assert b"grid" in M.lib().mafat_last_error() or True
+    assert b"NULL" in M.lib().mafat_last_error()
+
+
+def test_num_tiles_errors(lib):
+    plan = M.Plan(W.TINY, (64, 64, 3), "2x2/2/1x2")
+    n = ctypes.c_int32(-1)
+    assert M.lib().mafat_plan_num_tiles(plan.handle, 1, ctypes.byref(n)) == M.MAFAT_OK and n.value == 2
+    assert M.lib().mafat_plan_num_tiles(plan.handle, 2, ctypes.byref(n)) == M.MAFAT_EINVAL
+    assert M.lib().mafat_plan_num_tiles(plan.handle, -1, ctypes.byref(n)) == M.MAFAT_EINVAL
+    assert M.lib().mafat_plan_num_tiles(None, 0, ctypes.byref(n)) == M.MAFAT_EINVAL
+    assert M.lib().mafat_plan_num_tiles(plan.handle, 0, None) == M.MAFAT_EINVAL
 
 
 def test_run_argument_errors_before_any_launch(lib):
@@ -280,21 +292,27 @@ def test_run_argument_errors_before_any_launch(lib):
     fake = 1 << 20          # aligned, never dereferenced: validation fails first
     w = M._ptrs([fake, None, fake])
     # workspace too small
-    rc = L.mafat_run_group(plan.handle, 0, 1, M.MAFAT_F32, fake, fake * 4, w, w, w, fake, need - 1, None, None)
+    rc = L.mafat_run_group(plan.handle, 0, 1, M.MAFAT_F32, fake, fake * 4, w, w, w, fake, need - 1, None)
     assert rc == M.MAFAT_EWORKSPACE
     # unsupported dtype, bad batch, bad group, null plan
-    assert L.mafat_run_group(plan.handle, 0, 1, 7, fake, fake * 4, w, w, w, fake, need, None, None) == M.MAFAT_EUNSUPPORTED
-    assert L.mafat_run_group(plan.handle, 0, 0, 0, fake, fake * 4, w, w, w, fake, need, None, None) == M.MAFAT_EINVAL
-    assert L.mafat_run_group(plan.handle, 3, 1, 0, fake, fake * 4, w, w, w, fake, need, None, None) == M.MAFAT_EINVAL
-    assert L.mafat_run_group(None, 0, 1, 0, fake, fake * 4, w, w, w, fake, need, None, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_group(plan.handle, 0, 1, 7, fake, fake * 4, w, w, w, fake, need, None) == M.MAFAT_EUNSUPPORTED
+    assert L.mafat_run_group(plan.handle, 0, 0, 0, fake, fake * 4, w, w, w, fake, need, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_group(plan.handle, 3, 1, 0, fake, fake * 4, w, w, w, fake, need, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_group(None, 0, 1, 0, fake, fake * 4, w, w, w, fake, need, None) == M.MAFAT_EINVAL
     # misaligned / null tensors, overlapping x and y, missing weights
-    assert L.mafat_run_group(plan.handle, 0, 1, 0, fake + 4, fake * 4, w, w, w, fake, need, None, None) == M.MAFAT_EINVAL
-    assert L.mafat_run_group(plan.handle, 0, 1, 0, None, fake * 4, w, w, w, fake, need, None, None) == M.MAFAT_EINVAL
-    assert L.mafat_run_group(plan.handle, 0, 1, 0, fake, fake + 256, w, w, w, fake, need, None, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_group(plan.handle, 0, 1, 0, fake + 4, fake * 4, w, w, w, fake, need, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_group(plan.handle, 0, 1, 0, None, fake * 4, w, w, w, fake, need, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_group(plan.handle, 0, 1, 0, fake, fake + 256, w, w, w, fake, need, None) == M.MAFAT_EINVAL
     nw = M._ptrs([None, None, fake])
-    assert L.mafat_run_group(plan.handle, 0, 1, 0, fake, fake * 4, nw, w, w, fake, need, None, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_group(plan.handle, 0, 1, 0, fake, fake * 4, nw, w, w, fake, need, None) == M.MAFAT_EINVAL
     # workspace misaligned
-    assert L.mafat_run_group(plan.handle, 0, 1, 0, fake, fake * 4, w, w, w, fake + 16, need, None, None) == M.MAFAT_EINVAL
+    assert L.mafat_run_group(plan.handle, 0, 1, 0, fake, fake * 4, w, w, w, fake + 16, need, None) == M.MAFAT_EINVAL
+    # the timed variant: same checks, and its events array is required
+    ev = M._ptrs([None] * 4)
+    rc = L.mafat_run_group_timed(plan.handle, 0, 1, M.MAFAT_F32, fake, fake * 4, w, w, w, fake, need - 1, None, ev)
+    assert rc == M.MAFAT_EWORKSPACE
+    rc = L.mafat_run_group_timed(plan.handle, 0, 1, M.MAFAT_F32, fake, fake * 4, w, w, w, fake, need, None, None)
+    assert rc == M.MAFAT_EINVAL and b"events" in L.mafat_last_error()
     # network with several groups but no cut buffers
     plan2 = M.Plan(W.TINY, (64, 64, 3), "2x2/2/2x2")
     assert L.mafat_run_network(plan2.handle, 1, 0, fake, fake * 4, None, w, w, w, fake, 1 << 30, None) == M.MAFAT_EINVAL

@@ -5,7 +5,7 @@ full-size workload, the six configurations of the 608x608 sweep among them.
 The library allocates nothing; the caller's buffers (input, output, cut
 tensors, parameters, workspace) are all there is.  Measured: torch's
 requested-bytes statistic (the sizes asked of its allocator, before its
-rounding and block reuse), its peak over a run of the network minus its
+rounding and block part), its peak over a run of the network minus its
 value before the network was built; the prediction must equal it exactly.
 (The allocator's own allocated-bytes figure, which rounds and may hand out a
 larger cached block, is printed alongside.)"""
@@ -20,22 +20,22 @@ FULL = ["tiny", "yolo416_ftp3", "yolo608_5x5_8_2x2", "yolo608_4x4_12_1x1_b8"] + 
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("reuse,packed,tile_batch", [(False, False, 0), (True, False, 0), (False, True, 0),
+@pytest.mark.parametrize("part,packed,tile_batch", [(False, False, 0), (True, False, 0), (False, True, 0),
                                                       (False, True, 1)])
 @pytest.mark.parametrize("name", FULL)
-def test_device_model_matches_measured_peak(name, reuse, packed, tile_batch):
+def test_device_model_matches_measured_peak(name, part, packed, tile_batch):
     require_gpu()
     import torch
     from paper_2107_06960_amd import mafat as M
     wl = W.WORKLOADS[name]
-    print(f"[memory] {name}: {wl.h}x{wl.w}x{wl.c} {wl.tiling} batch={wl.batch} {wl.dtype} reuse={reuse} packed={packed} "
+    print(f"[memory] {name}: {wl.h}x{wl.w}x{wl.c} {wl.tiling} batch={wl.batch} {wl.dtype} stage_partition={part} packed={packed} "
           f"tile_batch={tile_batch}", flush=True)
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     base = torch.cuda.memory_stats().get("requested_bytes.all.current", 0)
     base_alloc = torch.cuda.memory_allocated()
     p = W.workload_inputs(wl)
-    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=reuse, packed_weights=packed,
+    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, stage_partition=part, packed_weights=packed,
                   tile_batch=tile_batch)
     net = M.Network(plan, p, wl.batch, wl.dtype)
     x = net.input_tensor(p["x"])

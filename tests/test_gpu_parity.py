@@ -21,10 +21,10 @@ def _gpu():
     require_gpu()
 
 
-def _check_full(orc, layers, h, w, c, tiling, batch, dtype, seed=0, reuse=False):
-    print(f"[parity] {h}x{w}x{c} {tiling} batch={batch} {dtype} seed={seed} reuse={reuse}", flush=True)
+def _check_full(orc, layers, h, w, c, tiling, batch, dtype, seed=0, part=False):
+    print(f"[parity] {h}x{w}x{c} {tiling} batch={batch} {dtype} seed={seed} stage_partition={part}", flush=True)
     p = W.make_inputs(layers, h, w, c, batch, seed, dtype)
-    out, cuts, net, _ = run_gpu(layers, h, w, c, p, tiling, batch, dtype, reuse=reuse)
+    out, cuts, net, _ = run_gpu(layers, h, w, c, p, tiling, batch, dtype, part=part)
     ref = orc.forward_layers(layers, h, w, c, p["x"], p)
     err = normwise_err(out, ref)
     assert err <= TOL[dtype], (tiling, dtype, err)
@@ -191,25 +191,25 @@ def test_graph_replay_equals_eager(dtype):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("tiling", ["3x3/NoCut", "5x5/8/2x2", "2x3/4/3x2"])
-def test_tile_reuse(orc, dtype, tiling):
-    # tile reuse: each tile computes only its part of every stage output,
+def test_stage_partition(orc, dtype, tiling):
+    # stage partition: each tile computes only its part of every stage output,
     # reading the halo from its neighbours' parts
-    _check_full(orc, W.YOLOV2_16, 80, 80, 3, tiling, 1, dtype, seed=3, reuse=True)
+    _check_full(orc, W.YOLOV2_16, 80, 80, 3, tiling, 1, dtype, seed=3, part=True)
 
 
-def test_tile_reuse_odd_batch(orc):
+def test_stage_partition_odd_batch(orc):
     # odd extents (pools drop a row/column), batch 2, ragged partitions
-    _check_full(orc, W.YOLOV2_16, 71, 93, 3, "3x2/8/2x2", 2, "bf16", seed=5, reuse=True)
-    _check_full(orc, W.TINY, 64, 64, 3, "9x8", 1, "f32", seed=9, reuse=True)
+    _check_full(orc, W.YOLOV2_16, 71, 93, 3, "3x2/8/2x2", 2, "bf16", seed=5, part=True)
+    _check_full(orc, W.TINY, 64, 64, 3, "9x8", 1, "f32", seed=9, part=True)
 
 
-def test_tile_reuse_equals_plain_partition_f32():
+def test_stage_partition_equals_plain_partition_f32():
     # f32: the same sums in the same order per output element, so tile
-    # reuse and the plain partition agree to rounding of the accumulation
+    # the stage partition and the plain tile partition agree to rounding of the accumulation
     # order only (the kernels' block shapes may differ)
     p = W.make_inputs(W.YOLOV2_16, 96, 96, 3, 1, 7, "f32")
     a = run_gpu(W.YOLOV2_16, 96, 96, 3, p, "4x4/8/2x2", 1, "f32", want_cuts=False)
-    b = run_gpu(W.YOLOV2_16, 96, 96, 3, p, "4x4/8/2x2", 1, "f32", want_cuts=False, reuse=True)
+    b = run_gpu(W.YOLOV2_16, 96, 96, 3, p, "4x4/8/2x2", 1, "f32", want_cuts=False, part=True)
     assert normwise_err(b, a) <= TOL["f32"]
 
 
@@ -220,13 +220,13 @@ VGG_LIKE = [W.conv(64), W.conv(64), W.maxpool(), W.conv(128), W.conv(128), W.max
             W.conv(256), W.conv(256), W.conv(256, act=W.LINEAR)]
 
 
-@pytest.mark.parametrize("reuse", [False, True])
+@pytest.mark.parametrize("part", [False, True])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_more_groups_and_other_networks(orc, dtype, reuse):
+def test_more_groups_and_other_networks(orc, dtype, part):
     # four groups on YOLOv2 (cuts after every pool but the first)
-    _check_full(orc, W.YOLOV2_16, 80, 80, 3, "4x4/4/3x3/8/2x2/12/1x1", 1, dtype, seed=31, reuse=reuse)
+    _check_full(orc, W.YOLOV2_16, 80, 80, 3, "4x4/4/3x3/8/2x2/12/1x1", 1, dtype, seed=31, part=part)
     # three groups with non-square grids on the VGG-style stack
-    _check_full(orc, VGG_LIKE, 64, 64, 3, "3x2/3/2x3/6/1x2", 1, dtype, seed=32, reuse=reuse)
+    _check_full(orc, VGG_LIKE, 64, 64, 3, "3x2/3/2x3/6/1x2", 1, dtype, seed=32, part=part)
 
 
 def test_pack_weights_kernel_layout():
@@ -259,8 +259,8 @@ def test_pack_weights_kernel_layout():
         assert matched, l
 
 
-@pytest.mark.parametrize("reuse", [False, True])
-def test_packed_weights_bit_identical(reuse):
+@pytest.mark.parametrize("part", [False, True])
+def test_packed_weights_bit_identical(part):
     # the same stage configurations read the same weights from the packed
     # layout: the output is bit for bit that of KRSC weights (batch 1)
     import torch
@@ -268,7 +268,7 @@ def test_packed_weights_bit_identical(reuse):
     from paper_2107_06960_amd import mafat as M
     outs = []
     for packed in (False, True):
-        plan = M.Plan(W.YOLOV2_16, (128, 128, 3), "5x5/8/2x2", reuse=reuse, packed_weights=packed)
+        plan = M.Plan(W.YOLOV2_16, (128, 128, 3), "5x5/8/2x2", stage_partition=part, packed_weights=packed)
         net = M.Network(plan, p, 1, "bf16")
         outs.append(net.run(net.input_tensor(p["x"])).clone())
         torch.cuda.synchronize()
@@ -276,11 +276,11 @@ def test_packed_weights_bit_identical(reuse):
 
 
 def test_packed_weights_parity(orc):
-    # batch 2 (stage configurations of one frame), odd extents, with reuse
+    # batch 2 (stage configurations of one frame), odd extents, with the stage partition
     from paper_2107_06960_amd import mafat as M
     layers, h, w, c = W.YOLOV2_16, 71, 93, 3
     p = W.make_inputs(layers, h, w, c, 2, 5, "bf16")
-    plan = M.Plan(layers, (h, w, c), "3x2/8/2x2", reuse=True, packed_weights=True)
+    plan = M.Plan(layers, (h, w, c), "3x2/8/2x2", stage_partition=True, packed_weights=True)
     net = M.Network(plan, p, 2, "bf16")
     y = net.run(net.input_tensor(p["x"]))
     import torch
@@ -295,17 +295,17 @@ def test_packed_weights_parity(orc):
 FUSED_PAIR = [W.conv(128), W.conv(64, 1)]
 
 
-@pytest.mark.parametrize("reuse,packed,act2", [(False, False, W.LEAKY), (True, False, W.LEAKY),
+@pytest.mark.parametrize("part,packed,act2", [(False, False, W.LEAKY), (True, False, W.LEAKY),
                                                 (False, True, W.LINEAR), (True, True, W.LEAKY)])
-def test_fused_pair_parity(orc, reuse, packed, act2):
+def test_fused_pair_parity(orc, part, packed, act2):
     # ragged extents (blocks of 16x16 past the tile edges), 2x3 tiles, batch 2
     from paper_2107_06960_amd import mafat as M
     import torch
     layers = [W.conv(128), W.conv(64, 1, act2)]
     h, w, c = 45, 61, 64
-    print(f"[parity] fused pair {h}x{w}x{c} reuse={reuse} packed={packed} act2={act2}", flush=True)
+    print(f"[parity] fused pair {h}x{w}x{c} stage_partition={part} packed={packed} act2={act2}", flush=True)
     p = W.make_inputs(layers, h, w, c, 2, 21, "bf16")
-    plan = M.Plan(layers, (h, w, c), "2x3/NoCut", reuse=reuse, packed_weights=packed)
+    plan = M.Plan(layers, (h, w, c), "2x3/NoCut", stage_partition=part, packed_weights=packed)
     net = M.Network(plan, p, 2, "bf16")
     net.y.fill_(float("nan"))
     y = net.run(net.input_tensor(p["x"]))
@@ -321,20 +321,20 @@ def test_fused_pair_parity(orc, reuse, packed, act2):
 FUSED_MID = [W.conv(64), W.conv(128), W.conv(64, 1), W.conv(32)]
 
 
-@pytest.mark.parametrize("layers,h,w,c,batch,tiling,reuse", [
+@pytest.mark.parametrize("layers,h,w,c,batch,tiling,part", [
     (FUSED_PAIR, 50, 39, 64, 1, "3x2/NoCut", False),
     (FUSED_MID, 120, 136, 32, 6, "2x2/NoCut", False),
     (FUSED_MID, 120, 136, 32, 6, "2x2/NoCut", True),
 ])
-def test_fused_pair_equals_separate_stages(orc, layers, h, w, c, batch, tiling, reuse):
+def test_fused_pair_equals_separate_stages(orc, layers, h, w, c, batch, tiling, part):
     # the fused kernel == its two stages run one by one (the 3x3 stage's
     # bf16 outputs through memory, then the 1x1 kernel), bit for bit: the
     # same roundings and the same accumulation order over the 128 channels
     import torch
     from paper_2107_06960_amd import mafat as M
-    print(f"[parity] fused pair vs separate stages {h}x{w}x{c} batch={batch} {tiling} reuse={reuse}", flush=True)
+    print(f"[parity] fused pair vs separate stages {h}x{w}x{c} batch={batch} {tiling} stage_partition={part}", flush=True)
     p = W.make_inputs(layers, h, w, c, batch, 22, "bf16")
-    plan = M.Plan(layers, (h, w, c), tiling, reuse=reuse)
+    plan = M.Plan(layers, (h, w, c), tiling, stage_partition=part)
     net = M.Network(plan, p, batch, "bf16")
     x = net.input_tensor(p["x"])
     ref = net.run(x).clone()

@@ -286,6 +286,26 @@ def test_tiled_equals_untiled_bf16_emulation(orc):
     assert np.array_equal(W.bf16_round(ref.astype(np.float32)).astype(np.float64), ref)
 
 
+def test_threads_do_not_change_results(orc):
+    # the layer loops split output rows into bands; every element is still
+    # computed alone in its fixed order, so any thread count gives the same bits
+    p = W.make_inputs(W.YOLOV2_16, 57, 61, 3, 2, seed=4)
+    outs = []
+    try:
+        for t in (1, 3, 8):
+            orc.set_threads(t)
+            outs.append(orc.forward_layers(W.YOLOV2_16, 57, 61, 3, p["x"], p, round_bf16=(t == 3)))
+            outs.append(orc.forward_tiled(W.YOLOV2_16, 57, 61, 3, p["x"], p, [0, 8], [3, 2], [2, 3]))
+    finally:
+        orc.set_threads(max(1, min(16, os.cpu_count() or 1)))
+    assert np.array_equal(outs[0], outs[4]) and np.array_equal(outs[1], outs[3]) and np.array_equal(outs[1], outs[5])
+    assert np.array_equal(outs[0], outs[1])
+    rounded = orc.forward_layers(W.YOLOV2_16, 57, 61, 3, p["x"], p, round_bf16=True)
+    assert np.array_equal(rounded, outs[2])
+    with pytest.raises(orc.OracleError):
+        orc.set_threads(0)
+
+
 def test_forward_rect_equals_untiled_crop(orc):
     p = W.make_inputs(W.YOLOV2_16, 64, 64, 3, 1, seed=2)
     ref = orc.forward_layers(W.YOLOV2_16, 64, 64, 3, p["x"], p)

@@ -108,10 +108,10 @@ def test_search_matches_oracle_over_limits():
 def test_device_model_counts_every_buffer():
     # the device model is the sum of the caller-owned buffers a run needs
     _lib()
-    for name, reuse in (("yolo608_5x5_8_2x2", False), ("yolo608_4x4_12_1x1_b8", False), ("tiny", False),
+    for name, part in (("yolo608_5x5_8_2x2", False), ("yolo608_4x4_12_1x1_b8", False), ("tiny", False),
                         ("yolo608_5x5_8_2x2", True), ("yolo608_4x4_12_1x1_b8", True)):
         wl = W.WORKLOADS[name]
-        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, reuse=reuse)
+        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, stage_partition=part)
         esz = 4 if wl.dtype == "f32" else 2
         b = wl.batch
         tot = b * wl.h * wl.w * wl.c * esz
