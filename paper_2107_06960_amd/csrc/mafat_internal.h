@@ -108,6 +108,12 @@ struct WorkspaceLayout {
 };
 WorkspaceLayout workspace_layout(const Group& G, int batch, int dtype);
 
+// Every group of a plan in order (mafat_run_network without clearing the
+// error state), on the given workspace; stream is a hipStream_t.
+int run_network_impl(const mafat_plan* plan, int batch, int dtype, const void* x, void* y,
+                     void* const* cut_bufs, const void* const* w, const float* const* scale,
+                     const float* const* bias, void* workspace, size_t ws_bytes, void* stream);
+
 // Thread-local error detail (mafat_last_error).
 void set_error(const std::string& msg);
 void clear_error();

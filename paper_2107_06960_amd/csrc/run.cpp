@@ -602,12 +602,9 @@ extern "C" int mafat_run_stage(const mafat_plan* plan, int32_t group, int32_t st
                         static_cast<hipStream_t>(stream), nullptr);
 }
 
-extern "C" int mafat_run_network(const mafat_plan* plan, int32_t batch, int32_t dtype,
-                                 const void* x, void* y, void* const* cut_bufs,
-                                 const void* const* w, const float* const* scale,
-                                 const float* const* bias, void* workspace, size_t ws_bytes,
-                                 void* stream) {
-  clear_error();
+int mafat::run_network_impl(const mafat_plan* plan, int batch, int dtype, const void* x, void* y,
+                            void* const* cut_bufs, const void* const* w, const float* const* scale,
+                            const float* const* bias, void* workspace, size_t ws_bytes, void* stream) {
   int rc = check_common(plan, batch, dtype);
   if (rc != MAFAT_OK) return rc;
   const int ng = static_cast<int>(plan->groups.size());
@@ -621,6 +618,15 @@ extern "C" int mafat_run_network(const mafat_plan* plan, int32_t batch, int32_t 
     if (rc != MAFAT_OK) return rc;
   }
   return MAFAT_OK;
+}
+
+extern "C" int mafat_run_network(const mafat_plan* plan, int32_t batch, int32_t dtype,
+                                 const void* x, void* y, void* const* cut_bufs,
+                                 const void* const* w, const float* const* scale,
+                                 const float* const* bias, void* workspace, size_t ws_bytes,
+                                 void* stream) {
+  clear_error();
+  return run_network_impl(plan, batch, dtype, x, y, cut_bufs, w, scale, bias, workspace, ws_bytes, stream);
 }
 
 extern "C" int mafat_plan_stage_fused(const mafat_plan* plan, int32_t group, int32_t stage, int32_t batch,

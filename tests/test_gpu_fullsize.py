@@ -16,7 +16,17 @@ oracle the same rounded values):
   - elementwise error |gpu - ref| / max(|ref|, 1e-3 max|ref|) within
     ELEM_TOL (logged);
   - bf16: against the oracle with every layer output rounded to bf16 as the
-    kernels round it (oracle round_bf16 mode), normwise within BF16_EMU_TOL.
+    kernels round it (oracle round_bf16 mode), normwise within BF16_EMU_TOL,
+    and at least BF16_SAME[n] of the elements after layer n-1 bit-identical
+    to it.
+
+The bf16 figures against the rounding oracle are regression guards set from
+the measured values (608x608, seed 0: normwise 3.0e-3 / 4.1e-3 / 5.4e-3 /
+7.1e-3 and 100 / 98.9 / 76.8 / 37.8 % identical after layers 3 / 7 / 11 /
+15), not derived bounds: a layer output differs from the rounding oracle only
+where the fp32 sum, accumulated in another order, rounds to the other
+neighbouring bf16 value, and such one-ulp differences feed every later layer
+that reads the element, so the identical share falls with depth.
 """
 import numpy as np
 import pytest
@@ -33,8 +43,10 @@ FULL = ["yolo416_ftp3", "yolo608_5x5_8_2x2", "yolo608_4x4_12_1x1_b8"] + \
 # zero (leaky outputs cross zero) from dividing by nothing.
 ELEM_FLOOR = 1e-3
 ELEM_TOL = {"f32": 1e-2, "bf16": 8.0}
-# Normwise error against the oracle that rounds every layer output to bf16.
-BF16_EMU_TOL = 2e-2
+# Normwise error against the oracle that rounds every layer output to bf16,
+# and the share of elements identical to it, by the number of layers run.
+BF16_EMU_TOL = 1.2e-2
+BF16_SAME = {4: 0.999, 8: 0.97, 12: 0.6, 16: 0.25}
 
 _REF = {}
 
@@ -101,6 +113,7 @@ def test_fullsize_whole_tensors(orc, name):
             same = float(np.mean(g == emu[b]))
             msg += f" | vs bf16-rounding oracle: normwise {e2:.3e}, bit-identical {100 * same:.1f} %"
             assert e2 <= BF16_EMU_TOL, (name, b, e2)
+            assert same >= BF16_SAME[b], (name, b, same)
         print(msg, flush=True)
         assert nerr <= TOL[wl.dtype], (name, b, nerr)
         assert eerr <= ELEM_TOL[wl.dtype], (name, b, eerr)
