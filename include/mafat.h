@@ -320,6 +320,25 @@ int mafat_run_network(const mafat_plan* plan, int32_t batch, int32_t dtype,
                       const float* const* bias, void* workspace, size_t ws_bytes,
                       void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * mafat_run_network without a workspace argument.  The workspace is a
+ * static device array of MAFAT_STATIC_WORKSPACE_MIB MiB that every GPU the
+ * library runs on holds until the process ends; the call allocates nothing
+ * (no hipMalloc, no allocating library routine).  The caller still owns x,
+ * y, the cut tensors and the parameters (same conventions as
+ * mafat_run_network).  The stream (NULL: the default stream) must belong to
+ * the current device.  All calls on one GPU share its array: calls that
+ * overlap in time on one GPU (several streams or threads) race.  Errors:
+ * those of mafat_run_network, EWORKSPACE when mafat_workspace_size(plan,
+ * batch, dtype) exceeds the array, EINVAL for a stream of another device,
+ * EHIP if the array's device address cannot be obtained. */
+#define MAFAT_STATIC_WORKSPACE_MIB 32
+int mafat_run_network_static(const mafat_plan* plan, int32_t batch, int32_t dtype,
+                             const void* x, void* y, void* const* cut_bufs,
+                             const void* const* w, const float* const* scale,
+                             const float* const* bias, void* stream);
+
 /* Memory prediction for a plan (section 4.1).
  *   model MAFAT_MEM_PAPER: the paper's predictor (Algorithm 1) on this plan's
  *     region tables ("Grid"): the largest, over every tile of every group

@@ -28,6 +28,7 @@ MAFAT_ACT_LINEAR, MAFAT_ACT_LEAKY01 = 0, 1
 MAFAT_F32, MAFAT_BF16 = 0, 1
 MAFAT_MEM_DEVICE, MAFAT_MEM_PAPER, MAFAT_MEM_DEVICE_SEQ = 0, 1, 2
 MAFAT_PLAN_STAGE_PARTITION, MAFAT_PLAN_PACKED_WEIGHTS = 1, 2
+MAFAT_STATIC_WORKSPACE_MIB = 32   # include/mafat.h: size of the static workspace of mafat_run_network_static
 MEM_MODELS = {"device": MAFAT_MEM_DEVICE, "paper": MAFAT_MEM_PAPER, "device_seq": MAFAT_MEM_DEVICE_SEQ}
 DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
 
@@ -37,6 +38,7 @@ EXPORTS = ("mafat_plan_create", "mafat_plan_create_flags", "mafat_plan_destroy",
            "mafat_plan_num_tiles", "mafat_plan_regions", "mafat_plan_macs", "mafat_plan_stages", "mafat_plan_stage_layers",
            "mafat_plan_stage_fused", "mafat_plan_set_tile_batch",
            "mafat_workspace_size", "mafat_run_group", "mafat_run_group_timed", "mafat_run_stage", "mafat_run_network",
+           "mafat_run_network_static",
            "mafat_predict_mem", "mafat_get_config", "mafat_status_string", "mafat_last_error")
 
 
@@ -95,6 +97,7 @@ def lib():
         L.mafat_run_group_timed.argtypes = [planp, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp, vpp]
         L.mafat_run_stage.argtypes = [planp, i32, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp]
         L.mafat_run_network.argtypes = [planp, i32, i32, vp, vp, vpp, vpp, vpp, vpp, vp, sz, vp]
+        L.mafat_run_network_static.argtypes = [planp, i32, i32, vp, vp, vpp, vpp, vpp, vpp, vp]
         i64p = ctypes.POINTER(i64)
         L.mafat_predict_mem.argtypes = [planp, i32, i32, i32, i64p]
         L.mafat_get_config.argtypes = [ctypes.POINTER(mafat_layer), i32, i32, i32, i32, i32, i32, i32, i64, i64,
@@ -258,6 +261,14 @@ def mafat_run_network(plan, batch, dtype, x, y, cut_bufs, w, scale, bias, worksp
     _check("mafat_run_network",
            lib().mafat_run_network(plan, batch, dtype, x, y, _ptrs(cut_bufs), _ptrs(w), _ptrs(scale),
                                    _ptrs(bias), workspace, ws_bytes, stream))
+
+
+def mafat_run_network_static(plan, batch, dtype, x, y, cut_bufs, w, scale, bias, stream):
+    """mafat_run_network with the library's static workspace (no workspace
+    argument; allocates nothing)."""
+    _check("mafat_run_network_static",
+           lib().mafat_run_network_static(plan, batch, dtype, x, y, _ptrs(cut_bufs), _ptrs(w), _ptrs(scale),
+                                          _ptrs(bias), stream))
 
 
 def _layer_array(layers):
