@@ -573,15 +573,18 @@ def main():
             a, b = stages[g][ln[0]][0], stages[g][ln[-1]][1]
             f = sum(flops[g][s] for s in ln) * wl.batch
             t = stage_ms[g][ln[0]]  # a fused pair's kernel: the first stage's events
-            # The 3-channel first layer (and a launch that starts with it)
-            # moves many bytes per flop: in bf16 it is bound by HBM (its
-            # matrix-core work, K = 27, is tiny), in fp32 by the vector ALUs;
-            # the other launches by the matrix cores.
-            first = plan.layers[a]["op"] == "conv" and plan.shape(a)[2] == 3
+            # Which roofline binds a launch: HBM when its algorithmic
+            # intensity (flops per algorithmic byte) is below the ridge
+            # point of the matrix-core peak over 8 TB/s (312 flop/byte in
+            # bf16, 19.7 in fp32: the stand-alone first layer, K = 27, and
+            # the 1x1 layers), else the matrix cores; the fp32 3-channel
+            # first layer runs on the vector ALUs.
+            first_alone = plan.layers[a]["op"] == "conv" and plan.shape(a)[2] == 3 and b <= a + 1
             nb = launch_bytes(sio[g], ln) * wl.batch
-            if first and wl.dtype == "f32":
+            ridge = peak * 1e12 / (PEAK_HBM_GBS * 1e9)
+            if first_alone and wl.dtype == "f32":
                 pk, bound = PEAK_VALU_TFLOPS, "alu"
-            elif first:
+            elif nb > 0 and f / nb < ridge:
                 pk, bound = PEAK_HBM_GBS, "hbm"
             else:
                 pk, bound = peak, "mfma"
@@ -637,14 +640,18 @@ def main():
         "per_stage": per_stage,
         "roofline": roof,
     }
-    shallow = [r for r in per_stage if r["bound"] == "hbm"]
-    if shallow:
-        # the one bandwidth-bound launch (the 3-channel first layer with its
-        # pool, or the fused launch that starts with it): achieved HBM rate
-        # of its algorithmic bytes against the 8 TB/s peak
-        r0 = shallow[0]
-        res["first_layer_hbm"] = {"layers": r0["layers"], "achieved_gbs": r0["gbs"], "peak_gbs": PEAK_HBM_GBS,
-                                  "frac": r0["hbm_frac"], "algorithmic_mb": r0["hbm_mb"], "ms": r0["ms"]}
+    # The launch that runs layer 0 (the 3-channel first layer, alone or with
+    # the stage after it): its achieved HBM rate of algorithmic bytes against
+    # 8 TB/s, and the shallow group's (group 0: tile input regions with halo,
+    # weights once, group output once, over the group's time).
+    r0 = per_stage[0]
+    res["first_layer_launch"] = {"layers": r0["layers"], "bound": r0["bound"], "ms": r0["ms"],
+                                 "achieved_gbs": r0["gbs"], "hbm_frac": r0["hbm_frac"],
+                                 "frac_mfma": r0["frac_mfma"], "algorithmic_mb": r0["hbm_mb"]}
+    g0_bytes = launch_bytes(sio[0], list(range(len(stages[0])))) * wl.batch
+    res["shallow_group_hbm"] = {"algorithmic_mb": round(g0_bytes / 1e6, 3), "ms": round(group_ms[0], 5),
+                                "achieved_gbs": round(g0_bytes / (group_ms[0] * 1e-3) / 1e9, 1),
+                                "frac": round(g0_bytes / (group_ms[0] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4)}
 
     if not args.no_untiled:
         del net, x

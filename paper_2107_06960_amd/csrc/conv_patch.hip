@@ -51,6 +51,19 @@
 // never goes to memory; with two input chunks the second one's patch and
 // first taps load into a second LDS region while the first is computed.
 //
+// First-layer variant (template argument PRE, one input chunk of 32
+// channels, fused pool): the block's input patch is not loaded from memory
+// but computed in the workgroup from the group input, by the 3-channel 3x3
+// first layer and its 2x2/2 max-pool (the layer pair before this stage):
+// the (2 PR + 2) x (2 PC + 2) pixel input patch is staged in LDS as 8-byte
+// pixels, every 2x2 window of first-layer outputs is one 16x16x16 MFMA row
+// quad (K = 27 as 3 filter rows x 4 column slots x 4 channel slots, as in
+// the stand-alone first-layer kernel, so the values are bit-identical to
+// it), and the pooled, activated, bf16-rounded values are written straight
+// into the patch rows of the slot in the patch layout (zero outside the
+// first layer's output, the zero padding of this stage).  The first layer's
+// output never goes to memory.
+//
 // Requires f = 3, c_in % 32 == 0, c_out % 16 == 0, byte offsets below 2^31
 // within a frame's source buffer and within the weights (host-checked); a
 // fused pool needs even block sizes and even tile origins and extents.
@@ -119,7 +132,7 @@ __device__ __forceinline__ void block_pixel(int r, int* py, int* px) {
 // = c_out channels in the block) follows in the same workgroup: the block's
 // activated bf16 outputs stay in LDS and are the A operand of a second GEMM
 // with its weights (a.w2, [N2][BN]), whose result is the stage's output.
-template <int BR, int BC, int BM, int BN, int WGM, int WGN, int NS, bool POOL, int N2 = 0>
+template <int BR, int BC, int BM, int BN, int WGM, int WGN, int NS, bool POOL, int N2 = 0, bool PRE = false>
 __global__ __launch_bounds__(64 * WGM * WGN)
 void conv_patch_kernel(const StageArgs a) {
   constexpr int NWAVE = WGM * WGN;
@@ -145,7 +158,18 @@ void conv_patch_kernel(const StageArgs a) {
   constexpr int YT = 5;
   constexpr int YOFF = W2D + N2 * BN * 2;
   static_assert(N2 == 0 || (NS == 1 && NBW == 9 && NB == 9 * NWAVE), "fused variant: one slot, a tap per instruction");
-  __shared__ __align__(1024) unsigned char smem[YOFF + (N2 > 0 ? A_BYTES + YT * BN * 64 : 0)];
+  // First-layer variant (PRE): past the ring, the input patch (IR x IC
+  // pixels of 8 bytes, rows IRS bytes apart), then the first layer's
+  // weights (32 x 27 bf16) and its scale and bias (32 floats each).
+  constexpr int IR = 2 * PR + 2, IC = 2 * PC + 2, IRS = IC * 8 + 16;
+  constexpr int C0 = 32;                               // first-layer outputs = this stage's c_in
+  constexpr int XOFF = W2D;                            // input patch
+  constexpr int W0OFF = XOFF + IR * IRS;               // first-layer weights
+  constexpr int SB0OFF = W0OFF + (C0 * 27 * 2 + 15) / 16 * 16;  // scale, bias
+  constexpr int PRE_END = SB0OFF + 2 * C0 * 4;
+  static_assert(!PRE || (NS == 1 && N2 == 0 && POOL), "first-layer variant: one slot, a fused pool");
+  constexpr int SMEM = PRE ? PRE_END : YOFF + (N2 > 0 ? A_BYTES + YT * BN * 64 : 0);
+  __shared__ __align__(1024) unsigned char smem[SMEM];
   static_assert(N2 == 0 || (!POOL && BM == BR * BC && N2 % 16 == 0 && BN % 32 == 0),
                 "fused 1x1: no pool, no padding rows");
   // Fused 1x1: its weights ([N2][BN] bf16) go straight to LDS now (rows of
@@ -179,6 +203,21 @@ void conv_patch_kernel(const StageArgs a) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) { sc2[j][r] = s4[r]; bi2[j][r] = b4[r]; }
     }
+  }
+
+  // First-layer variant: its weights, scale and bias (the same for every
+  // workgroup, one 16-byte piece per thread) are fetched before the tile
+  // table is decoded and written to LDS with the input patch.
+  constexpr int W0P = C0 * 27 * 2 / 16;  // 16-byte pieces of the first layer's weights
+  static_assert(!PRE || (W0P + C0 / 2 <= 64 * WGM * WGN), "one piece per thread");
+  u32x4 pre_v = u32x4{0u, 0u, 0u, 0u};
+  if constexpr (PRE) {
+    const int t0 = static_cast<int>(threadIdx.x);
+    const u32x4* ps = (t0 < W0P)              ? reinterpret_cast<const u32x4*>(a.w0) + t0
+                      : (t0 < W0P + C0 / 4)   ? reinterpret_cast<const u32x4*>(a.scale0) + (t0 - W0P)
+                      : (t0 < W0P + C0 / 2)   ? reinterpret_cast<const u32x4*>(a.bias0) + (t0 - W0P - C0 / 4)
+                                              : nullptr;
+    if (ps) pre_v = *ps;
   }
 
   MAFAT_PTRACE(0);
@@ -382,7 +421,119 @@ void conv_patch_kernel(const StageArgs a) {
     taps(sp, sp, I0{}, I9{});
   };
 
-  if constexpr (N2 > 0) {
+  if constexpr (PRE) {
+    // The block's input patch = the pooled first-layer outputs at patch
+    // pixels (py, px) <-> first-layer output (by0 - 1 + py, bx0 - 1 + px),
+    // i.e. first-layer conv outputs 2 (by0 - 1) + [0, 2 PR) (rows; columns
+    // likewise), i.e. group-input pixels starting one row/column earlier.
+    const int gy0 = 2 * (by0 - 1) - 1, gx0 = 2 * (bx0 - 1) - 1;  // input patch origin
+    // Group-input rows and columns this tile's first-layer outputs read:
+    // its pooled region [cy0 - 1, cy0 + ch + 1) of this stage's input
+    // (clipped to it), doubled, widened by the 3x3 window, clipped to the
+    // image.  Pixels outside read as zero, like the stand-alone kernel's.
+    const int ylo = max(0, 2 * ry0 - 1), yhi = min(a.in_h0, 2 * ry1 + 1);
+    const int xlo = max(0, 2 * rx0 - 1), xhi = min(a.in_w0, 2 * rx1 + 1);
+    const int64_t sb0 = bp.frame * a.src_fstride + tl.src_off;  // elements (3 per pixel)
+    const int bpar = static_cast<int>(sb0 & 1);
+    const __amdgpu_buffer_rsrc_t rs0 = make_rsrc(static_cast<const uint16_t*>(a.src) + sb0,
+                                                 static_cast<unsigned>((a.src_fstride - tl.src_off) * 2));
+    constexpr int NPX0 = IR * IC;
+    constexpr int NTH = 64 * NWAVE;
+    constexpr int NPT0 = (NPX0 + NTH - 1) / NTH;
+    uint32_t la[NPT0], lb[NPT0];
+    bool lodd[NPT0];
+#pragma unroll
+    for (int k = 0; k < NPT0; ++k) {  // one pixel (6 bytes): an aligned 4-byte and a 2-byte load
+      const int e = tid + NTH * k;
+      const int r = e / IC, c = e - r * IC;
+      const int iy = gy0 + r, ix = gx0 + c;
+      const bool ok = e < NPX0 && iy >= ylo && iy < yhi && ix >= xlo && ix < xhi;
+      const int pp = (iy - tl.sy0) * tl.sw + (ix - tl.sx0);
+      const bool odd = ((bpar + pp) & 1) != 0;  // c0 at an address = 2 (mod 4): the dword holds c1, c2
+      const unsigned off = static_cast<unsigned>(pp * 6);
+      la[k] = __builtin_amdgcn_raw_buffer_load_b32(rs0, static_cast<int>(ok ? (odd ? off + 2u : off) : 0x80000000u),
+                                                   0, 0);
+      lb[k] = __builtin_amdgcn_raw_buffer_load_b16(rs0, static_cast<int>(ok ? (odd ? off : off + 4u) : 0x80000000u),
+                                                   0, 0);
+      lodd[k] = odd;
+    }
+    if (tid < W0P)
+      *reinterpret_cast<u32x4*>(smem + W0OFF + tid * 16) = pre_v;
+    else if (tid < W0P + C0 / 2)  // scale (C0 floats), then bias
+      *reinterpret_cast<u32x4*>(smem + SB0OFF + (tid - W0P) * 16) = pre_v;
+    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+    for (int k = 0; k < NPT0; ++k) {
+      const int e = tid + NTH * k;
+      const int r = e / IC, c = e - r * IC;
+      const uint32_t b16 = lb[k] & 0xffffu;
+      const u32x2 v = lodd[k] ? u32x2{b16 | (la[k] << 16), la[k] >> 16} : u32x2{la[k], b16};
+      if (e < NPX0) *reinterpret_cast<u32x2*>(smem + XOFF + r * IRS + c * 8) = v;
+    }
+    __syncthreads();
+    MAFAT_PTRACE(6);
+
+    // First layer on the matrix cores: 16x16x16 MFMAs, A = 16 first-layer
+    // outputs (4 pool windows = 4 patch pixels, window-major), B = 16
+    // channels, K = (kx slot, channel slot) for one filter row.  Lane l
+    // supplies output pixel l & 15 at kx slot l >> 4 (slot 3: zero weights).
+    typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+    const int kq = lane >> 4, kx = min(kq, 2), pl = lane & 15;
+    const uint16_t* sw0 = reinterpret_cast<const uint16_t*>(smem + W0OFF);
+    const float* ssb0 = reinterpret_cast<const float*>(smem + SB0OFF);
+    u32x2 wf[C0 / 16][3];
+    float sc0[C0 / 16], bi0[C0 / 16];
+#pragma unroll
+    for (int j = 0; j < C0 / 16; ++j) {
+#pragma unroll
+      for (int ky = 0; ky < 3; ++ky) {
+        const int wr = (16 * j + pl) * 27 + ky * 9 + 3 * kx;
+        const uint32_t w0 = sw0[wr], w1 = sw0[wr + 1], w2 = sw0[wr + 2];
+        wf[j][ky] = kq < 3 ? u32x2{w0 | (w1 << 16), w2} : u32x2{0u, 0u};
+      }
+      sc0[j] = ssb0[16 * j + pl];
+      bi0[j] = ssb0[C0 + 16 * j + pl];
+    }
+    const float slope0 = act_slope(a.act0);
+    constexpr int NQ = PR * PC;            // patch pixels
+    constexpr int NG = (NQ + 3) / 4;       // MFMA row tiles (4 patch pixels each)
+    for (int t = wave; t < NG; t += NWAVE) {
+      int q = 4 * t + (pl >> 2);           // this lane's operand row: patch pixel q, window position pl & 3
+      q = q < NQ ? q : 0;
+      const int qy = q / PC, qx = q - (q / PC) * PC;
+      const unsigned char* xp = smem + XOFF + (2 * qy + ((pl & 3) >> 1)) * IRS + (2 * qx + (pl & 1) + kx) * 8;
+      u32x2 xf[3];
+#pragma unroll
+      for (int ky = 0; ky < 3; ++ky) xf[ky] = *reinterpret_cast<const u32x2*>(xp + ky * IRS);
+      // accumulator rows 4 kq .. 4 kq + 3 of this lane: the window of patch pixel 4 t + kq
+      const int qo = 4 * t + kq;
+      const int oy = qo / PC, ox = qo - (qo / PC) * PC;
+      const int gy = by0 - 1 + oy, gx = bx0 - 1 + ox;  // its position in this stage's input
+      const bool inside = gy >= 0 && gy < a.in_h && gx >= 0 && gx < a.in_w;
+      const int key = ((ox >> 1) ^ (oy << 1)) & 3;
+#pragma unroll
+      for (int j = 0; j < C0 / 16; ++j) {
+        f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ky = 0; ky < 3; ++ky)
+          acc0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, xf[ky]),
+                                                          __builtin_bit_cast(bf16x4, wf[j][ky]), acc0, 0, 0, 0);
+        float v[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) v[r] = fmaf(acc0[r], sc0[j], bi0[j]);
+        float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+        m = fmaxf(m, slope0 * m);
+        const int ch = 16 * j + pl;
+        if (qo < NQ)
+          store1(reinterpret_cast<uint16_t*>(smem + qo * 64 + ((((ch >> 3) ^ key) & 3) << 4)) + (ch & 7),
+                 inside ? m : 0.f);
+      }
+    }
+    pwait_vmcnt<0>();  // this stage's weights (issued during the decode)
+    pbarrier();        // the patch is complete
+    MAFAT_PTRACE(8);
+    compute(0);
+  } else if constexpr (N2 > 0) {
     if (nstage == 2) {
       // Two chunks, the second one's loads overlapped with compute: its
       // patch and first YT taps go to Y at once, its last taps to the
@@ -609,6 +760,15 @@ hipError_t launch_conv_patch_fused(const StageArgs& args, hipStream_t stream, La
   if (args.total_blocks <= 0) return hipSuccess;
   if (args.cout != 128 || args.cout2 != 64) return hipErrorInvalidValue;
   hipExtLaunchKernelGGL((conv_patch_kernel<8, 16, 128, 128, 4, 2, 1, false, 64>),
+                        dim3(static_cast<unsigned>(args.total_blocks)), dim3(512), 0, stream, ev.start, ev.stop, 0,
+                        args);
+  return hipGetLastError();
+}
+
+hipError_t launch_conv_patch_first(const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
+  if (args.total_blocks <= 0) return hipSuccess;
+  if (args.cin != 32 || args.cout != 64 || args.nblk_n != 1) return hipErrorInvalidValue;
+  hipExtLaunchKernelGGL((conv_patch_kernel<12, 16, 192, 64, 4, 2, 1, true, 0, true>),
                         dim3(static_cast<unsigned>(args.total_blocks)), dim3(512), 0, stream, ev.start, ev.stop, 0,
                         args);
   return hipGetLastError();

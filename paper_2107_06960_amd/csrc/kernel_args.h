@@ -43,6 +43,14 @@ struct StageArgs {
   const float* scale2;
   const float* bias2;
   int32_t cout2, act2;
+  // Fused first layer (a 3-channel 3x3 convolution with a 2x2/2 max-pool
+  // that produces this stage's input in the same workgroup): its weights
+  // [cout0 = cin][3][3][3], scale, bias, activation and its input extent
+  // (the group input, read through src / the tile source fields).
+  const void* w0;
+  const float* scale0;
+  const float* bias0;
+  int32_t act0, in_h0, in_w0;
   int32_t mblk_prefix[kMaxTilesPerLaunch + 1];
   KTile tiles[kMaxTilesPerLaunch];
 };
@@ -136,6 +144,15 @@ hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs&
 // 128 channels; args.w2 / scale2 / bias2 / cout2 / act2 describe the 1x1
 // layer, the destination fields the 1x1 stage's output.
 hipError_t launch_conv_patch_fused(const StageArgs& args, hipStream_t stream, LaunchEvents ev);
+
+// Launch a bf16 3-channel first layer with its 2x2/2 pool fused with the
+// 3x3 stage (32 -> 64 channels, fused pool) that follows it
+// (conv_patch.hip): each workgroup computes the first layer's pooled output
+// over its block's input patch into LDS, then the 3x3 stage from there.
+// args describe the 3x3 stage (tiles: its computed rectangles and output;
+// the source fields: the group input), w0 / scale0 / bias0 / act0 / in_h0 /
+// in_w0 the first layer.
+hipError_t launch_conv_patch_first(const StageArgs& args, hipStream_t stream, LaunchEvents ev);
 
 // Repack one layer's KRSC bf16 weights into the patch kernel's packed layout.
 hipError_t launch_pack_weights(const uint16_t* src, uint16_t* dst, int cout, int cin, int bn, int nblk,

@@ -252,10 +252,58 @@ bool fused_pair(const mafat_plan& P, const Group& G, int s, int dtype) {
   return src_frame * 2 < (1ll << 31);
 }
 
+// The group's first stage is a bf16 3-channel 3x3 convolution (32 outputs)
+// with a 2x2/2 pool, and the next stage a 3x3 convolution 32 -> 64 with a
+// 2x2/2 pool (YOLOv2's layers 0-3): the pair runs as one kernel, each
+// workgroup computing the first layer's pooled outputs over its block's
+// input patch in LDS (the first layer's output never goes to memory).
+bool fused_first(const mafat_plan& P, const Group& G, int s, int dtype) {
+  if (dtype != MAFAT_BF16 || s != 0 || s + 1 >= static_cast<int>(G.stages.size())) return false;
+  const Stage& A = G.stages[s];
+  const Stage& B = G.stages[s + 1];
+  if (A.kind != STAGE_CONV || B.kind != STAGE_CONV || A.src_buf != BUF_GROUP_IO) return false;
+  if (A.f != 3 || A.p != 1 || !A.pool || A.cin != 3 || A.cout != 32) return false;
+  if (B.f != 3 || B.p != 1 || !B.pool || B.cin != 32 || B.cout != 64) return false;
+  if (!mfma_ok(B, dtype) || A.tiles.size() != B.tiles.size()) return false;
+  // pooled blocks need even tile origins and extents (as for any fused pool)
+  for (const TileGeom& T : B.tiles)
+    if ((T.cy0 | T.cx0 | T.ch | T.cw) & 1) return false;
+  const auto& din = P.dims[G.l0];
+  return static_cast<int64_t>(din[0]) * din[1] * din[2] * 2 < (1ll << 31);
+}
+
+StageConfig first_pair_config(const Stage& B) {
+  // 12x16 blocks of the 3x3 stage's conv outputs, all 64 channels, 4x2
+  // waves of 48x32, one ring slot (the shape the stand-alone stage takes
+  // on YOLOv2's layers 2-3 at 608x608)
+  StageConfig c{};
+  c.kind = K_CONV_PATCH;
+  c.br = 12; c.bc = 16; c.bm = 192; c.bn = 64; c.wgm = 4; c.wgn = 2; c.depth = 1; c.kg = 1; c.kord = 1;
+  int64_t mb = 0;
+  for (const TileGeom& T : B.tiles) mb += static_cast<int64_t>((T.ch + 11) / 12) * ((T.cw + 15) / 16);
+  c.blocks = mb;
+  c.chan_major = 0;
+  return c;
+}
+
 }  // namespace
 
 StageConfig stage_config(const mafat_plan& P, const Group& G, const Stage& S, int batch, int dtype) {
   const int si = static_cast<int>(&S - G.stages.data());
+  if (fused_first(P, G, si, dtype)) {
+    // its own configuration (the first-layer kernel) when it runs alone;
+    // run together with the next stage, the launch takes the pair's shape
+    StageConfig c = choose_config(S, P.packed_weights ? 1 : batch, dtype);
+    c.fuse = 2;
+    return c;
+  }
+  if (fused_first(P, G, si - 1, dtype)) {
+    // run alone (mafat_run_stage) it takes the fused kernel's block shape,
+    // so its packed weights serve both
+    StageConfig c = first_pair_config(S);
+    c.fuse = -2;
+    return c;
+  }
   if (fused_pair(P, G, si, dtype)) {
     // 8x16 blocks of all 128 channels, one ring slot (the weights of a
     // 32-channel chunk take 72 KiB): on YOLOv2's layer 4 at 608x608 with
@@ -373,11 +421,16 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
       hipEvent_t ev_start = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin)]) : nullptr;
       hipEvent_t ev_stop = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin) + 1]) : nullptr;
       bool launched = started[static_cast<size_t>(s - s_begin)] != 0;
-      const StageConfig cfg = stage_config(*plan, G, S, batch, dtype);
+      const StageConfig scfg = stage_config(*plan, G, S, batch, dtype);
       // Both stages of a fused pair in this call: one kernel for the two
-      // (the second stage's interval is recorded empty, after it).
-      const bool fuse = cfg.fuse == 1 && s + 1 < s_end;
+      // (the second stage's interval is recorded empty, after it).  A
+      // first-layer pair (fuse 2) computes the second stage's blocks, its
+      // first stage inside them, in the pair's own block shape.
+      const bool fuse = scfg.fuse > 0 && s + 1 < s_end;
+      const bool first = fuse && scfg.fuse == 2;
       const Stage* S2 = fuse ? &G.stages[s + 1] : nullptr;
+      const StageConfig cfg = first ? first_pair_config(*S2) : scfg;
+      const Stage& SC = first ? *S2 : S;  // the convolution whose GEMM the launch computes
       const int kind = cfg.kind;
       const bool matrix = (kind == K_CONV_MFMA || kind == K_CONV_RING || kind == K_CONV_PATCH);
       const MfmaShape shape{cfg.bm, cfg.bn, cfg.depth, cfg.kg, cfg.wgm, cfg.wgn, cfg.kord, cfg.br, cfg.bc};
@@ -394,22 +447,28 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
       A.dst = (dst_b == BUF_GROUP_IO) ? y : ws;
       A.src_fstride = (src_b == BUF_GROUP_IO) ? in_frame : scr_frame;
       A.dst_fstride = (dst_b == BUF_GROUP_IO) ? out_frame : scr_frame;
-      if (S.kind == STAGE_CONV) {
-        A.w = w[S.first];
-        A.scale = scale[S.first];
-        A.bias = bias[S.first];
+      if (SC.kind == STAGE_CONV) {
+        A.w = w[SC.first];
+        A.scale = scale[SC.first];
+        A.bias = bias[SC.first];
       }
-      if (fuse) {
+      if (first) {
+        A.w0 = w[S.first];
+        A.scale0 = scale[S.first];
+        A.bias0 = bias[S.first];
+        A.act0 = S.act;
+        A.in_h0 = S.in_h; A.in_w0 = S.in_w;
+      } else if (fuse) {
         A.w2 = w[S2->first];
         A.scale2 = scale[S2->first];
         A.bias2 = bias[S2->first];
         A.cout2 = S2->cout;
         A.act2 = S2->act;
       }
-      A.in_h = S.in_h; A.in_w = S.in_w;
-      A.cin = S.cin; A.cout = S.cout;
-      A.act = S.act;
-      A.nblk_n = matrix ? (S.cout + shape.bn - 1) / shape.bn : 1;
+      A.in_h = SC.in_h; A.in_w = SC.in_w;
+      A.cin = SC.cin; A.cout = SC.cout;
+      A.act = SC.act;
+      A.nblk_n = matrix ? (SC.cout + shape.bn - 1) / shape.bn : 1;
       A.chan_major = matrix ? cfg.chan_major : 0;
       A.w_packed = (plan->packed_weights && kind == K_CONV_PATCH) ? 1 : 0;
       for (int t0 = b0; t0 < b1; t0 += kMaxTilesPerLaunch) {
@@ -419,9 +478,10 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         A.mblk_prefix[0] = 0;
         for (int t = t0; t < t1; ++t) {
           const TileGeom& T = S.tiles[t];
+          const TileGeom& TC = SC.tiles[t];  // computed rectangle
           KTile& k = A.tiles[t - t0];
-          k.cy0 = static_cast<int16_t>(T.cy0); k.cx0 = static_cast<int16_t>(T.cx0);
-          k.ch = static_cast<int16_t>(T.ch);   k.cw = static_cast<int16_t>(T.cw);
+          k.cy0 = static_cast<int16_t>(TC.cy0); k.cx0 = static_cast<int16_t>(TC.cx0);
+          k.ch = static_cast<int16_t>(TC.ch);   k.cw = static_cast<int16_t>(TC.cw);
           k.sy0 = static_cast<int16_t>(T.sy0); k.sx0 = static_cast<int16_t>(T.sx0);
           k.sw = static_cast<int16_t>(T.sw);
           const TileGeom& TD = SD.tiles[t];
@@ -429,13 +489,13 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
           k.dw = static_cast<int16_t>(TD.dw);
           k.src_off = static_cast<int32_t>(T.src_off + src_shift);
           k.dst_off = static_cast<int32_t>(TD.dst_off + dst_shift);
-          int64_t units = static_cast<int64_t>(T.ch) * T.cw;
+          int64_t units = static_cast<int64_t>(TC.ch) * TC.cw;
           if ((kind == K_CONV_DIRECT || kind == K_CONV_RGB) && S.pool) units /= 4;
           if (kind == K_CONV_RGB_MFMA)  // 2-D blocks of conv outputs
-            total += static_cast<int64_t>((T.ch + kRgbBlockRows - 1) / kRgbBlockRows) *
-                     ((T.cw + kRgbBlockCols - 1) / kRgbBlockCols);
+            total += static_cast<int64_t>((TC.ch + kRgbBlockRows - 1) / kRgbBlockRows) *
+                     ((TC.cw + kRgbBlockCols - 1) / kRgbBlockCols);
           else if (kind == K_CONV_PATCH)
-            total += static_cast<int64_t>((T.ch + shape.br - 1) / shape.br) * ((T.cw + shape.bc - 1) / shape.bc);
+            total += static_cast<int64_t>((TC.ch + shape.br - 1) / shape.br) * ((TC.cw + shape.bc - 1) / shape.bc);
           else
             total += (units + bu - 1) / bu;
           A.mblk_prefix[t - t0 + 1] = static_cast<int32_t>(total);
@@ -451,6 +511,8 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
           e = hipSuccess;
         } else if (kind == K_CONV_RING) {
           e = launch_conv_ring(S.f, S.pool, shape, A, stream, lev);
+        } else if (first) {
+          e = launch_conv_patch_first(A, stream, lev);
         } else if (fuse) {
           e = launch_conv_patch_fused(A, stream, lev);
         } else if (kind == K_CONV_PATCH) {
@@ -496,8 +558,9 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
           std::fprintf(stderr, "RTRACE stage %d-%d %dx%d kg%d ns%d grid %d\n", S.first, S.last, shape.bm, shape.bn,
                        shape.kg, shape.depth, A.total_blocks);
           for (int w = 0; w < 3; ++w) {
-            std::fprintf(stderr, "  wg%d decode +%lld loopend +%lld end +%lld iters:", w, (tr[w][1] - tr[w][0]) * 10,
-                         (tr[w][4] - tr[w][0]) * 10, (tr[w][5] - tr[w][0]) * 10);
+            std::fprintf(stderr, "  wg%d decode +%lld staged +%lld loopend +%lld end +%lld iters:", w,
+                         (tr[w][1] - tr[w][0]) * 10, (tr[w][6] - tr[w][0]) * 10, (tr[w][4] - tr[w][0]) * 10,
+                         (tr[w][5] - tr[w][0]) * 10);
             for (int k = 8; k < 44; ++k) std::fprintf(stderr, " %lld", (tr[w][k] - tr[w][0]) * 10);
             std::fprintf(stderr, "\n");
           }
@@ -646,7 +709,7 @@ extern "C" int mafat_plan_stage_fused(const mafat_plan* plan, int32_t group, int
     return MAFAT_EUNSUPPORTED;
   }
   *fused = (stage + 1 < static_cast<int>(G.stages.size()) &&
-            stage_config(*plan, G, G.stages[stage], batch, dtype).fuse == 1) ? 1 : 0;
+            stage_config(*plan, G, G.stages[stage], batch, dtype).fuse > 0) ? 1 : 0;
   return MAFAT_OK;
 }
 

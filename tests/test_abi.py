@@ -111,14 +111,16 @@ def test_stages_fuse_conv_and_following_pool(lib):
 
 
 def test_fused_pair_detection(lib):
-    # bf16: layer 4 (3x3, 64 -> 128) runs with layer 5 (1x1, 128 -> 64) in
-    # one kernel, whatever the batch or plan flags; f32 and other shapes not
+    # bf16: layers 0-1 (3 -> 32, pool) run inside layers 2-3 (3x3 32 -> 64,
+    # pool), and layer 4 (3x3, 64 -> 128) with layer 5 (1x1, 128 -> 64), in
+    # one kernel each, whatever the batch or plan flags; f32 and other shapes
+    # not
     for flags in ({}, {"stage_partition": True}, {"packed_weights": True}):
         plan = M.Plan(W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2", **flags)
         for batch in (1, 8):
             got = [plan.stage_fused(0, s, batch, "bf16") for s in range(len(plan.stages(0)))]
-            assert got == [False, False, True, False, False], (flags, batch, got)
-            assert plan.launches(0, batch, "bf16") == [[0], [1], [2, 3], [4]]
+            assert got == [True, False, True, False, False], (flags, batch, got)
+            assert plan.launches(0, batch, "bf16") == [[0, 1], [2, 3], [4]]
             assert not any(plan.stage_fused(1, s, batch, "bf16") for s in range(len(plan.stages(1))))
         assert not any(plan.stage_fused(0, s, 1, "f32") for s in range(len(plan.stages(0))))
     # a cut between layers 4 and 5 separates them
@@ -131,6 +133,16 @@ def test_fused_pair_detection(lib):
         assert not plan.stage_fused(0, 0, 1, "bf16"), layers
     plan = M.Plan([W.conv(128), W.conv(64, 1, W.LINEAR)], (32, 32, 64), "2x2/NoCut")
     assert plan.stage_fused(0, 0, 1, "bf16") and not plan.stage_fused(0, 1, 1, "bf16")
+    # the first-layer pair needs the group's first stage to be the 3-channel
+    # layer with a pool and the next a 3x3 32 -> 64 with a pool, in one group
+    assert not M.Plan(W.YOLOV2_16, (96, 96, 3), "3x3/2/2x2").stage_fused(0, 0, 1, "bf16")   # cut between
+    assert M.Plan(W.YOLOV2_16, (96, 96, 3), "3x3/4/2x2").stage_fused(0, 0, 1, "bf16")
+    for layers in ([W.conv(16), W.maxpool(), W.conv(64), W.maxpool()],      # 16 first-layer outputs
+                   [W.conv(32), W.conv(64), W.maxpool()],                   # no pool after the first
+                   [W.conv(32), W.maxpool(), W.conv(64)],                   # no pool after the second
+                   [W.conv(32), W.maxpool(), W.conv(128), W.maxpool()],     # 128 outputs
+                   [W.conv(32), W.maxpool(), W.conv(64, 1), W.maxpool()]):  # 1x1 second
+        assert not M.Plan(layers, (64, 64, 3), "2x2/NoCut").stage_fused(0, 0, 1, "bf16"), layers
     with pytest.raises(M.MafatError):
         plan.stage_fused(0, 2, 1, "bf16")
 

@@ -27,7 +27,7 @@ def test_launch_bytes_of_fused_pair():
     plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, packed_weights=True)
     io = bench.stage_io_bytes(plan, 0, 2)
     launches = plan.launches(0, 1, "bf16")
-    assert launches == [[0], [1], [2, 3], [4]]
+    assert launches == [[0, 1], [2, 3], [4]]
     fused = bench.launch_bytes(io, [2, 3])
     assert fused == io[2][0] + io[3][1] + io[2][2] + io[3][2]
     assert fused < bench.launch_bytes(io, [2]) + bench.launch_bytes(io, [3])

@@ -351,10 +351,52 @@ def test_fused_pair_equals_separate_stages(orc, layers, h, w, c, batch, tiling, 
         assert e <= TOL["bf16"], (f, e)
 
 
+FIRST_PAIR = [W.conv(32), W.maxpool(), W.conv(64), W.maxpool(), W.conv(32, 1)]
+
+
+@pytest.mark.parametrize("h,w,batch,tiling,part,packed", [
+    (96, 96, 1, "3x3/NoCut", False, True),
+    (71, 93, 3, "2x3/NoCut", False, False),
+    (130, 66, 2, "4x2/4/1x1", False, True),
+    (71, 93, 2, "3x2/NoCut", True, True),
+    (40, 48, 1, "1x1/NoCut", False, True),
+])
+def test_first_layer_pair_equals_separate_stages(orc, h, w, batch, tiling, part, packed):
+    # the 3-channel first layer + pool computed inside the 3x3 stage's
+    # workgroups (its output never leaves LDS) == the two stages run one by
+    # one through memory, bit for bit (same MFMA sequences and roundings);
+    # and the oracle
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    print(f"[parity] first-layer pair vs separate stages {h}x{w}x3 batch={batch} {tiling} "
+          f"stage_partition={part} packed={packed}", flush=True)
+    p = W.make_inputs(FIRST_PAIR, h, w, 3, batch, 23, "bf16")
+    plan = M.Plan(FIRST_PAIR, (h, w, 3), tiling, stage_partition=part, packed_weights=packed)
+    assert plan.stage_fused(0, 0, batch, "bf16")
+    net = M.Network(plan, p, batch, "bf16")
+    x = net.input_tensor(p["x"])
+    net.y.fill_(float("nan"))
+    ref = net.run(x).clone()
+    refc = [c.clone() for c in net.cuts]
+    assert not torch.isnan(ref).any()
+    net.y.zero_()
+    for g in range(plan.n_groups):
+        gin, gout = net.group_io(g, x)
+        for s in range(len(plan.stages(g))):
+            net.run_stage(g, s, gin, gout)
+    torch.cuda.synchronize()
+    assert torch.equal(net.y.view(torch.int16), ref.view(torch.int16))
+    for a, b in zip(net.cuts, refc):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    out = ref.float().cpu().numpy().astype(np.float64)
+    e = normwise_err(out, orc.forward_layers(FIRST_PAIR, h, w, 3, p["x"], p))
+    assert e <= TOL["bf16"], e
+
+
 @pytest.mark.parametrize("which", ["all", "ends"])
 def test_run_group_events(which):
     # per-stage events (all entries) and group events (first and last only,
-    # the rest NULL) around a group with a fused pair: the run succeeds, the
+    # the rest NULL) around a group with two fused pairs: the run succeeds, the
     # output is unchanged, the intervals are ordered
     import sys
     import os
@@ -365,7 +407,7 @@ def test_run_group_events(which):
     print(f"[parity] run_group events={which}", flush=True)
     p = W.make_inputs(W.YOLOV2_16, 96, 96, 3, 1, 9, "bf16")
     plan = M.Plan(W.YOLOV2_16, (96, 96, 3), "3x3/8/2x2", packed_weights=True)
-    assert plan.launches(0) == [[0], [1], [2, 3], [4]]
+    assert plan.launches(0) == [[0, 1], [2, 3], [4]]
     net = M.Network(plan, p, 1, "bf16")
     x = net.input_tensor(p["x"])
     ref = net.run(x).clone()
@@ -386,7 +428,8 @@ def test_run_group_events(which):
             assert ev.ms(evs[2 * s], evs[2 * s + 1]) >= 0
             if s + 1 < n:
                 assert ev.ms(evs[2 * s + 1], evs[2 * s + 2]) >= 0
-        assert ev.ms(evs[4], evs[5]) > 0  # the fused pair's kernel
+        assert ev.ms(evs[0], evs[1]) > 0  # the first-layer pair's kernel (layers 0-3)
+        assert ev.ms(evs[4], evs[5]) > 0  # the fused pair's kernel (layers 4-5)
     ev.destroy(evs)
 
 
