@@ -72,6 +72,10 @@
 #include "device_util.h"
 #include "kernel_args.h"
 
+#ifndef MAFAT_PRE_WAVES
+#define MAFAT_PRE_WAVES 1
+#endif
+
 namespace mafat {
 #ifdef MAFAT_TUNING
 // Tuning builds only: phase timestamps (wall clock, 100 MHz) of three
@@ -133,7 +137,7 @@ __device__ __forceinline__ void block_pixel(int r, int* py, int* px) {
 // activated bf16 outputs stay in LDS and are the A operand of a second GEMM
 // with its weights (a.w2, [N2][BN]), whose result is the stage's output.
 template <int BR, int BC, int BM, int BN, int WGM, int WGN, int NS, bool POOL, int N2 = 0, bool PRE = false>
-__global__ __launch_bounds__(64 * WGM * WGN)
+__global__ __launch_bounds__(64 * WGM * WGN) __attribute__((amdgpu_waves_per_eu(PRE ? MAFAT_PRE_WAVES : 1)))
 void conv_patch_kernel(const StageArgs a) {
   constexpr int NWAVE = WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN, MT = WM / 16, NT = WN / 16;
@@ -158,17 +162,24 @@ void conv_patch_kernel(const StageArgs a) {
   constexpr int YT = 5;
   constexpr int YOFF = W2D + N2 * BN * 2;
   static_assert(N2 == 0 || (NS == 1 && NBW == 9 && NB == 9 * NWAVE), "fused variant: one slot, a tap per instruction");
-  // First-layer variant (PRE): past the ring, the input patch (IR x IC
-  // pixels of 8 bytes, rows IRS bytes apart), then the first layer's
-  // weights (32 x 27 bf16) and its scale and bias (32 floats each).
+  // First-layer variant (PRE): one slot and nothing past it.  The weight
+  // rows of taps 0-4 load during the tile decode; while the first layer
+  // runs, the space of taps 5-8 holds the input patch (IR x IC pixels of 8
+  // bytes, rows IRS bytes apart), the first layer's weights (32 x 27 bf16),
+  // its scale and bias (32 floats each) and a table of the patch pixels
+  // (see below); taps 5-8 load there once the first layer is done, while
+  // taps 0-4 are computed.  52 KiB: three workgroups per CU.
   constexpr int IR = 2 * PR + 2, IC = 2 * PC + 2, IRS = IC * 8 + 16;
   constexpr int C0 = 32;                               // first-layer outputs = this stage's c_in
-  constexpr int XOFF = W2D;                            // input patch
+  constexpr int G5 = 5 * BN / 16;                      // weight load instructions of taps 0-4
+  constexpr int XOFF = A_BYTES + 5 * BN * 64;          // input patch (where taps 5-8 go later)
   constexpr int W0OFF = XOFF + IR * IRS;               // first-layer weights
   constexpr int SB0OFF = W0OFF + (C0 * 27 * 2 + 15) / 16 * 16;  // scale, bias
-  constexpr int PRE_END = SB0OFF + 2 * C0 * 4;
-  static_assert(!PRE || (NS == 1 && N2 == 0 && POOL), "first-layer variant: one slot, a fused pool");
-  constexpr int SMEM = PRE ? PRE_END : YOFF + (N2 > 0 ? A_BYTES + YT * BN * 64 : 0);
+  constexpr int QTOFF = SB0OFF + 2 * C0 * 4;           // patch pixel table
+  constexpr int PRE_END = QTOFF + PR * PC * 4;
+  static_assert(!PRE || (NS == 1 && N2 == 0 && POOL && PRE_END <= SLOT && (5 * BN) % 16 == 0),
+                "first-layer variant: one slot, a fused pool, its staging inside the slot");
+  constexpr int SMEM = PRE ? SLOT : YOFF + (N2 > 0 ? A_BYTES + YT * BN * 64 : 0);
   __shared__ __align__(1024) unsigned char smem[SMEM];
   static_assert(N2 == 0 || (!POOL && BM == BR * BC && N2 % 16 == 0 && BN % 32 == 0),
                 "fused 1x1: no pool, no padding rows");
@@ -267,7 +278,17 @@ void conv_patch_kernel(const StageArgs a) {
         b_off[k] = (g < NB && co < cout) ? static_cast<unsigned>((co * K + t * cin) * 2 + chunk * 16)
                                          : 0x80000000u;
     }
-    issue_b(0, 0);
+    if constexpr (PRE) {  // taps 0-4 only (their rows: instructions g < G5)
+#pragma unroll
+      for (int k = 0; k < NBW; ++k) {
+        const int g = k * NWAVE + wave;
+        if (g < G5)
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, (lds_ptr_t)(smem + A_BYTES + g * 1024), 16,
+                                                   static_cast<int>(b_off[k]), 0, 0, 0);
+      }
+    } else {
+      issue_b(0, 0);
+    }
   };
   KTile tl;
   const BlockPos bp = decode_block(a, &tl, early);
@@ -457,6 +478,21 @@ void conv_patch_kernel(const StageArgs a) {
                                                    0, 0);
       lodd[k] = odd;
     }
+    // Patch pixel table, entry q = (qy, qx): bits 0-15 the LDS offset of its
+    // first-layer window (input patch row 2 qy, column 2 qx), bits 16-24 q,
+    // bits 25-26 its swizzle key ((qx >> 1) ^ 2 qy) & 3, bit 27 set if it
+    // lies inside this stage's input (else it is zero padding).
+    constexpr int NQ = PR * PC;            // patch pixels
+    static_assert(XOFF + 2 * (PR - 1) * IRS + 2 * (PC - 1) * 8 < 65536 && NQ <= 512, "table fields");
+    static_assert(NQ <= 64 * NWAVE, "one table entry per thread");
+    if (tid < NQ) {
+      const int qy = tid / PC, qx = tid - (tid / PC) * PC;
+      const int gy = by0 - 1 + qy, gx = bx0 - 1 + qx;
+      const bool inside = gy >= 0 && gy < a.in_h && gx >= 0 && gx < a.in_w;
+      const unsigned e = static_cast<unsigned>(XOFF + 2 * qy * IRS + 2 * qx * 8) | (static_cast<unsigned>(tid) << 16) |
+                         (static_cast<unsigned>(((qx >> 1) ^ (qy << 1)) & 3) << 25) | (inside ? (1u << 27) : 0u);
+      *reinterpret_cast<unsigned*>(smem + QTOFF + tid * 4) = e;
+    }
     if (tid < W0P)
       *reinterpret_cast<u32x4*>(smem + W0OFF + tid * 16) = pre_v;
     else if (tid < W0P + C0 / 2)  // scale (C0 floats), then bias
@@ -481,8 +517,10 @@ void conv_patch_kernel(const StageArgs a) {
     const int kq = lane >> 4, kx = min(kq, 2), pl = lane & 15;
     const uint16_t* sw0 = reinterpret_cast<const uint16_t*>(smem + W0OFF);
     const float* ssb0 = reinterpret_cast<const float*>(smem + SB0OFF);
+    const unsigned* qtab = reinterpret_cast<const unsigned*>(smem + QTOFF);
     u32x2 wf[C0 / 16][3];
     float sc0[C0 / 16], bi0[C0 / 16];
+    bool neg = false;
 #pragma unroll
     for (int j = 0; j < C0 / 16; ++j) {
 #pragma unroll
@@ -493,46 +531,81 @@ void conv_patch_kernel(const StageArgs a) {
       }
       sc0[j] = ssb0[16 * j + pl];
       bi0[j] = ssb0[C0 + 16 * j + pl];
+      neg = neg || !(sc0[j] >= 0.f);
     }
+    // With a non-negative scale, v -> fma(v, s, b) is non-decreasing, so the
+    // window maximum may be taken before the scale (the same value: rounding
+    // keeps the order); otherwise (some scale of the wave negative or NaN)
+    // every element is scaled first.
     const float slope0 = act_slope(a.act0);
-    constexpr int NQ = PR * PC;            // patch pixels
+    const int lx = ((pl & 3) >> 1) * IRS + ((pl & 1) + kx) * 8;  // this lane's place in a window
     constexpr int NG = (NQ + 3) / 4;       // MFMA row tiles (4 patch pixels each)
-    for (int t = wave; t < NG; t += NWAVE) {
-      int q = 4 * t + (pl >> 2);           // this lane's operand row: patch pixel q, window position pl & 3
-      q = q < NQ ? q : 0;
-      const int qy = q / PC, qx = q - (q / PC) * PC;
-      const unsigned char* xp = smem + XOFF + (2 * qy + ((pl & 3) >> 1)) * IRS + (2 * qx + (pl & 1) + kx) * 8;
-      u32x2 xf[3];
+    constexpr int NIT = (NG + NWAVE - 1) / NWAVE;  // tiles per wave (the last one may run past NG)
+    constexpr int DUMMY = QTOFF + (NQ * 4 + 255) / 256 * 256;  // stores of tiles past NG land here
+    static_assert(DUMMY + 64 * 2 <= SLOT, "dummy store area");
+    // A fixed trip count, unrolled and free of branches, so that the
+    // compiler can issue the next tiles' table and patch reads while the
+    // current tile's MFMAs run; the sign test of the scales is hoisted out.
+    auto first_layer = [&](auto negc) {
+      constexpr bool NEG = decltype(negc)::value;
 #pragma unroll
-      for (int ky = 0; ky < 3; ++ky) xf[ky] = *reinterpret_cast<const u32x2*>(xp + ky * IRS);
-      // accumulator rows 4 kq .. 4 kq + 3 of this lane: the window of patch pixel 4 t + kq
-      const int qo = 4 * t + kq;
-      const int oy = qo / PC, ox = qo - (qo / PC) * PC;
-      const int gy = by0 - 1 + oy, gx = bx0 - 1 + ox;  // its position in this stage's input
-      const bool inside = gy >= 0 && gy < a.in_h && gx >= 0 && gx < a.in_w;
-      const int key = ((ox >> 1) ^ (oy << 1)) & 3;
+      for (int it = 0; it < NIT; ++it) {
+        const int t = wave + NWAVE * it;
+        const int q = 4 * t + (pl >> 2);   // this lane's operand row: patch pixel q, window position pl & 3
+        const unsigned eq = qtab[q < NQ ? q : 0];
+        const int qo = 4 * t + kq;         // this lane's results: the window of patch pixel qo
+        const bool valid = qo < NQ;        // false only in tiles past NG
+        const unsigned eo = qtab[valid ? qo : 0];
+        const unsigned char* xp = smem + (eq & 0xffffu) + lx;
+        u32x2 xf[3];
 #pragma unroll
-      for (int j = 0; j < C0 / 16; ++j) {
-        f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int ky = 0; ky < 3; ++ky) xf[ky] = *reinterpret_cast<const u32x2*>(xp + ky * IRS);
+        const bool inside = (eo >> 27) & 1u;
+        const unsigned key = (eo >> 25) & 3u;
+        const unsigned srow = ((eo >> 16) & 0x1ffu) * 64 + (pl & 7) * 2;
 #pragma unroll
-        for (int ky = 0; ky < 3; ++ky)
-          acc0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, xf[ky]),
-                                                          __builtin_bit_cast(bf16x4, wf[j][ky]), acc0, 0, 0, 0);
-        float v[4];
+        for (int j = 0; j < C0 / 16; ++j) {
+          f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int r = 0; r < 4; ++r) v[r] = fmaf(acc0[r], sc0[j], bi0[j]);
-        float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-        m = fmaxf(m, slope0 * m);
-        const int ch = 16 * j + pl;
-        if (qo < NQ)
-          store1(reinterpret_cast<uint16_t*>(smem + qo * 64 + ((((ch >> 3) ^ key) & 3) << 4)) + (ch & 7),
-                 inside ? m : 0.f);
+          for (int ky = 0; ky < 3; ++ky)
+            acc0 = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(bf16x4, xf[ky]),
+                                                            __builtin_bit_cast(bf16x4, wf[j][ky]), acc0, 0, 0, 0);
+          float m;
+          if constexpr (!NEG) {
+            m = fmaf(fmaxf(fmaxf(acc0[0], acc0[1]), fmaxf(acc0[2], acc0[3])), sc0[j], bi0[j]);
+          } else {
+            float v[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) v[r] = fmaf(acc0[r], sc0[j], bi0[j]);
+            m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+          }
+          m = fmaxf(m, slope0 * m);
+          const unsigned addr = valid ? srow + ((((2 * j + (pl >> 3)) ^ key) & 3u) << 4)
+                                      : static_cast<unsigned>(DUMMY + 2 * pl);
+          store1(reinterpret_cast<uint16_t*>(smem + addr), inside ? m : 0.f);
+        }
       }
+    };
+    if (__builtin_amdgcn_ballot_w64(neg) != 0)
+      first_layer(std::true_type{});
+    else
+      first_layer(std::false_type{});
+    MAFAT_PTRACE(7);
+    pbarrier();  // every wave is done with the input patch: taps 5-8 load over it
+#pragma unroll
+    for (int k = 0; k < NBW; ++k) {
+      const int g = k * NWAVE + wave;
+      if (g >= G5 && g < NB)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, (lds_ptr_t)(smem + A_BYTES + g * 1024), 16,
+                                                 static_cast<int>(b_off[k]), 0, 0, 0);
     }
-    pwait_vmcnt<0>();  // this stage's weights (issued during the decode)
-    pbarrier();        // the patch is complete
     MAFAT_PTRACE(8);
-    compute(0);
+    using I5 = std::integral_constant<int, 5>;
+    taps(smem, smem, I0{}, I5{});  // taps 0-4 (their rows were in before the first layer started)
+    pwait_vmcnt<0>();
+    pbarrier();
+    MAFAT_PTRACE(9);
+    taps(smem, smem, I5{}, I9{});
   } else if constexpr (N2 > 0) {
     if (nstage == 2) {
       // Two chunks, the second one's loads overlapped with compute: its
@@ -765,13 +838,20 @@ hipError_t launch_conv_patch_fused(const StageArgs& args, hipStream_t stream, La
   return hipGetLastError();
 }
 
-hipError_t launch_conv_patch_first(const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
+hipError_t launch_conv_patch_first(const MfmaShape& sh, const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
   if (args.total_blocks <= 0) return hipSuccess;
   if (args.cin != 32 || args.cout != 64 || args.nblk_n != 1) return hipErrorInvalidValue;
-  hipExtLaunchKernelGGL((conv_patch_kernel<12, 16, 192, 64, 4, 2, 1, true, 0, true>),
-                        dim3(static_cast<unsigned>(args.total_blocks)), dim3(512), 0, stream, ev.start, ev.stop, 0,
-                        args);
-  return hipGetLastError();
+#define MAFAT_FIRST(br_, bc_, bm_, wgm_, wgn_)                                                            \
+  if (sh.br == (br_) && sh.bc == (bc_) && sh.bm == (bm_) && sh.bn == 64 && sh.wgm == (wgm_) &&            \
+      sh.wgn == (wgn_)) {                                                                                 \
+    hipExtLaunchKernelGGL((conv_patch_kernel<br_, bc_, bm_, 64, wgm_, wgn_, 1, true, 0, true>),           \
+                          dim3(static_cast<unsigned>(args.total_blocks)), dim3(64 * (wgm_) * (wgn_)), 0,  \
+                          stream, ev.start, ev.stop, 0, args);                                            \
+    return hipGetLastError();                                                                             \
+  }
+  MAFAT_FIRST_SHAPES
+#undef MAFAT_FIRST
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_conv_patch(bool pool, const MfmaShape& shape, const StageArgs& args, hipStream_t stream,

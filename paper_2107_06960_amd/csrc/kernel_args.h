@@ -93,6 +93,7 @@ struct MfmaShape {
   MAFAT_PATCH(8, 8, 64, 32, 4, 2, 2)      \
   MAFAT_PATCH(8, 16, 128, 64, 8, 1, 1)    \
   MAFAT_PATCH(12, 16, 192, 64, 4, 2, 1)   \
+  MAFAT_PATCH(14, 18, 256, 64, 4, 2, 1)   \
   MAFAT_PATCH(8, 16, 128, 128, 4, 2, 1)
 #ifdef MAFAT_TUNING
 #define MAFAT_PATCH_TUNE_SHAPES           \
@@ -152,7 +153,14 @@ hipError_t launch_conv_patch_fused(const StageArgs& args, hipStream_t stream, La
 // args describe the 3x3 stage (tiles: its computed rectangles and output;
 // the source fields: the group input), w0 / scale0 / bias0 / act0 / in_h0 /
 // in_w0 the first layer.
-hipError_t launch_conv_patch_first(const StageArgs& args, hipStream_t stream, LaunchEvents ev);
+hipError_t launch_conv_patch_first(const MfmaShape& shape, const StageArgs& args, hipStream_t stream,
+                                   LaunchEvents ev);
+
+// Instantiated block shapes of the first-layer pair: (br, bc, bm, wgm, wgn),
+// 64 channels, one ring slot.
+#define MAFAT_FIRST_SHAPES           \
+  MAFAT_FIRST(12, 16, 192, 4, 2)     \
+  MAFAT_FIRST(14, 18, 256, 4, 2)
 
 // Repack one layer's KRSC bf16 weights into the patch kernel's packed layout.
 hipError_t launch_pack_weights(const uint16_t* src, uint16_t* dst, int cout, int cin, int bn, int nblk,

@@ -128,7 +128,9 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
     const int chunks = S.cin / 32;
     double best = 1e30;
     for (const PS& r : kPatch) {
-      if ((r.bn > S.cout && r.bn > 32) || r.bn == 128) continue;  // 128: the fused pair's shape
+      // 128 channels: the fused layer 4-5 pair's shape; 14x18: a first-layer
+      // pair's shape (its second stage alone takes it too)
+      if ((r.bn > S.cout && r.bn > 32) || r.bn == 128 || r.br == 14) continue;
       // One-slot rings only for single-chunk layers (c_in = 32), where they
       // are measured fastest (several workgroups per CU overlap their loads);
       // among them the model below picks (12x16 blocks on YOLOv2's layer 2
@@ -272,17 +274,31 @@ bool fused_first(const mafat_plan& P, const Group& G, int s, int dtype) {
   return static_cast<int64_t>(din[0]) * din[1] * din[2] * 2 < (1ll << 31);
 }
 
-StageConfig first_pair_config(const Stage& B) {
-  // 12x16 blocks of the 3x3 stage's conv outputs, all 64 channels, 4x2
-  // waves of 48x32, one ring slot (the shape the stand-alone stage takes
-  // on YOLOv2's layers 2-3 at 608x608)
+StageConfig first_pair_config(const Stage& B, int batch) {
+  // Blocks of the 3x3 stage's conv outputs, all 64 channels, 4x2 waves, one
+  // ring slot: 12x16 (48x32 per wave) or 14x18 (64x32 per wave, 256 GEMM
+  // rows for 252 outputs).  Two workgroups fit a CU (LDS), so a launch takes
+  // ceil(blocks / 512) rounds; a workgroup costs a fixed ~2.5 us (decode,
+  // input and weight latency, epilogue) plus ~0.027 us per GEMM row
+  // (per-workgroup timestamps at 608x608, 5x5 tiles, where 14x18 blocks
+  // make 500 workgroups, one round, and 12x16 blocks 720, two).
+  struct FS { int br, bc, bm; };
+  static const FS kShapes[] = {{12, 16, 192}, {14, 18, 256}};
   StageConfig c{};
   c.kind = K_CONV_PATCH;
-  c.br = 12; c.bc = 16; c.bm = 192; c.bn = 64; c.wgm = 4; c.wgn = 2; c.depth = 1; c.kg = 1; c.kord = 1;
-  int64_t mb = 0;
-  for (const TileGeom& T : B.tiles) mb += static_cast<int64_t>((T.ch + 11) / 12) * ((T.cw + 15) / 16);
-  c.blocks = mb;
-  c.chan_major = 0;
+  c.bn = 64; c.wgm = 4; c.wgn = 2; c.depth = 1; c.kg = 1; c.kord = 1; c.chan_major = 0;
+  double best = 1e30;
+  for (const FS& f : kShapes) {
+    int64_t mb = 0;
+    for (const TileGeom& T : B.tiles)
+      mb += static_cast<int64_t>((T.ch + f.br - 1) / f.br) * ((T.cw + f.bc - 1) / f.bc);
+    const double rounds = std::ceil(static_cast<double>(mb) * batch / 512.0);
+    const double t = rounds * (2.5 + 0.027 * f.bm);
+    if (t < best) {
+      best = t;
+      c.br = f.br; c.bc = f.bc; c.bm = f.bm; c.blocks = mb;
+    }
+  }
   return c;
 }
 
@@ -300,7 +316,7 @@ StageConfig stage_config(const mafat_plan& P, const Group& G, const Stage& S, in
   if (fused_first(P, G, si - 1, dtype)) {
     // run alone (mafat_run_stage) it takes the fused kernel's block shape,
     // so its packed weights serve both
-    StageConfig c = first_pair_config(S);
+    StageConfig c = first_pair_config(S, P.packed_weights ? 1 : batch);
     c.fuse = -2;
     return c;
   }
@@ -429,7 +445,7 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
       const bool fuse = scfg.fuse > 0 && s + 1 < s_end;
       const bool first = fuse && scfg.fuse == 2;
       const Stage* S2 = fuse ? &G.stages[s + 1] : nullptr;
-      const StageConfig cfg = first ? first_pair_config(*S2) : scfg;
+      const StageConfig cfg = first ? first_pair_config(*S2, batch) : scfg;
       const Stage& SC = first ? *S2 : S;  // the convolution whose GEMM the launch computes
       const int kind = cfg.kind;
       const bool matrix = (kind == K_CONV_MFMA || kind == K_CONV_RING || kind == K_CONV_PATCH);
@@ -512,7 +528,7 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         } else if (kind == K_CONV_RING) {
           e = launch_conv_ring(S.f, S.pool, shape, A, stream, lev);
         } else if (first) {
-          e = launch_conv_patch_first(A, stream, lev);
+          e = launch_conv_patch_first(shape, A, stream, lev);
         } else if (fuse) {
           e = launch_conv_patch_fused(A, stream, lev);
         } else if (kind == K_CONV_PATCH) {
@@ -558,6 +574,8 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
           std::fprintf(stderr, "RTRACE stage %d-%d %dx%d kg%d ns%d grid %d\n", S.first, S.last, shape.bm, shape.bn,
                        shape.kg, shape.depth, A.total_blocks);
           for (int w = 0; w < 3; ++w) {
+            std::fprintf(stderr, "  wg%d slots 6-9: %lld %lld %lld %lld\n", w, (tr[w][6] - tr[w][0]) * 10,
+                         (tr[w][7] - tr[w][0]) * 10, (tr[w][8] - tr[w][0]) * 10, (tr[w][9] - tr[w][0]) * 10);
             std::fprintf(stderr, "  wg%d decode +%lld staged +%lld loopend +%lld end +%lld iters:", w,
                          (tr[w][1] - tr[w][0]) * 10, (tr[w][6] - tr[w][0]) * 10, (tr[w][4] - tr[w][0]) * 10,
                          (tr[w][5] - tr[w][0]) * 10);

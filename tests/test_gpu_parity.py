@@ -360,6 +360,8 @@ FIRST_PAIR = [W.conv(32), W.maxpool(), W.conv(64), W.maxpool(), W.conv(32, 1)]
     (130, 66, 2, "4x2/4/1x1", False, True),
     (71, 93, 2, "3x2/NoCut", True, True),
     (40, 48, 1, "1x1/NoCut", False, True),
+    (608, 608, 1, "5x5/4/2x2", False, True),    # the 14x18 blocks (one round of workgroups)
+    (600, 584, 2, "5x5/NoCut", False, False),
 ])
 def test_first_layer_pair_equals_separate_stages(orc, h, w, batch, tiling, part, packed):
     # the 3-channel first layer + pool computed inside the 3x3 stage's
