@@ -28,6 +28,7 @@ struct StageArgs {
   int64_t src_fstride;  // elements between frames
   int64_t dst_fstride;
   int32_t in_h, in_w;   // extent of the stage input tensor (zero padding outside)
+  int32_t f, s, p;      // filter, stride, padding of the stage's first layer (generic kernels)
   int32_t cin, cout;
   int32_t act;
   int32_t ntiles;
@@ -97,6 +98,8 @@ struct MfmaShape {
   MAFAT_PATCH(8, 16, 128, 128, 4, 2, 1)
 #ifdef MAFAT_TUNING
 #define MAFAT_PATCH_TUNE_SHAPES           \
+  MAFAT_PATCH(10, 10, 128, 32, 4, 1, 3)   \
+  MAFAT_PATCH(10, 10, 128, 32, 4, 1, 4)   \
   MAFAT_PATCH(16, 12, 192, 64, 4, 2, 1)   \
   MAFAT_PATCH(16, 16, 256, 64, 8, 1, 1)   \
   MAFAT_PATCH(8, 16, 128, 64, 4, 1, 1)    \
@@ -114,6 +117,8 @@ struct MfmaShape {
   MAFAT_RING(128, 128, 2, 2, 2, 3, 1)
 #ifdef MAFAT_TUNING
 #define MAFAT_RING_TUNE_SHAPES        \
+  MAFAT_RING(32, 64, 2, 2, 1, 6, 1)   \
+  MAFAT_RING(32, 64, 2, 2, 1, 8, 1)   \
   MAFAT_RING(32, 32, 2, 2, 1, 3, 1)   \
   MAFAT_RING(32, 32, 2, 2, 1, 4, 1)   \
   MAFAT_RING(64, 64, 2, 2, 2, 4, 1)

@@ -374,11 +374,15 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma_kernel(const StageArgs a) 
 
 // Direct convolution on the vector ALUs, one thread per output pixel (or per
 // 2x2 pool window), all output channels in chunks of 8.  Weights are read
-// with wave-uniform addresses (scalar cache).
+// with wave-uniform addresses (scalar cache).  F > 0: an f = F "same"
+// convolution (stride 1, padding (F - 1) / 2); F = 0: any filter, stride and
+// padding, taken from the stage arguments (a.f, a.s, a.p).
 template <int DT, int F, bool POOL>
 __global__ __launch_bounds__(256) void conv_direct_kernel(const StageArgs a) {
   using T = typename Elt<DT>::T;
-  constexpr int P = (F - 1) / 2;
+  const int f = F > 0 ? F : a.f;
+  const int st = F > 0 ? 1 : a.s;
+  const int pd = F > 0 ? (F - 1) / 2 : a.p;
   constexpr int NP = POOL ? 4 : 1;
   constexpr int CO = 8;
   KTile tl;
@@ -389,7 +393,7 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const StageArgs a) {
   int oy[NP], ox[NP];
 #pragma unroll
   for (int p = 0; p < NP; ++p) row_pixel<POOL>(tl, POOL ? 4 * u + p : u, &oy[p], &ox[p]);
-  const int cin = a.cin, cout = a.cout, K = F * F * cin;
+  const int cin = a.cin, cout = a.cout, K = f * f * cin;
   const T* src = static_cast<const T*>(a.src) + bp.frame * a.src_fstride + tl.src_off;
   T* dst = static_cast<T*>(a.dst) + bp.frame * a.dst_fstride + tl.dst_off;
   const T* wgt = static_cast<const T*>(a.w);
@@ -401,20 +405,18 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const StageArgs a) {
     for (int p = 0; p < NP; ++p)
 #pragma unroll
       for (int j = 0; j < CO; ++j) acc[p][j] = 0.f;
-#pragma unroll
-    for (int ky = 0; ky < F; ++ky)
-#pragma unroll
-      for (int kx = 0; kx < F; ++kx) {
+    for (int ky = 0; ky < f; ++ky)
+      for (int kx = 0; kx < f; ++kx) {
         const T* px[NP];
         bool ok[NP];
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
-          const int iy = oy[p] + ky - P, ix = ox[p] + kx - P;
+          const int iy = oy[p] * st + ky - pd, ix = ox[p] * st + kx - pd;
           ok[p] = static_cast<unsigned>(iy) < static_cast<unsigned>(a.in_h) &&
                   static_cast<unsigned>(ix) < static_cast<unsigned>(a.in_w);
           px[p] = ok[p] ? src + ((iy - tl.sy0) * tl.sw + (ix - tl.sx0)) * cin : src;
         }
-        const T* wt = wgt + static_cast<int64_t>(co0) * K + (ky * F + kx) * cin;
+        const T* wt = wgt + static_cast<int64_t>(co0) * K + (ky * f + kx) * cin;
         for (int ci = 0; ci < cin; ++ci) {
           float xv[NP];
 #pragma unroll
@@ -795,8 +797,11 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
 }
 
 
-// Lone 2x2/2 max-pool: 64 output pixels per block, 4 threads per pixel
-// striding over channels.  The computed rectangle is in pool-output
+// A max-pool stage (one that does not follow a convolution, or any other
+// window than 2x2/2): 64 output pixels per block, 4 threads per pixel
+// striding over channels.  Output (y, x) takes the maximum over the in-image
+// elements of rows y*s - p .. y*s - p + f - 1 (columns likewise; padding is
+// not part of the window).  The computed rectangle is in pool-output
 // coordinates.
 template <int DT>
 __global__ __launch_bounds__(256) void pool_kernel(const StageArgs a) {
@@ -810,12 +815,13 @@ __global__ __launch_bounds__(256) void pool_kernel(const StageArgs a) {
   const int c_in = a.cin;
   const T* src = static_cast<const T*>(a.src) + bp.frame * a.src_fstride + tl.src_off;
   T* dst = static_cast<T*>(a.dst) + bp.frame * a.dst_fstride + tl.dst_off;
-  const T* p00 = src + ((2 * oy - tl.sy0) * tl.sw + (2 * ox - tl.sx0)) * c_in;
-  const T* p10 = p00 + tl.sw * c_in;
+  const int y0 = max(oy * a.s - a.p, 0), y1 = min(oy * a.s - a.p + a.f, a.in_h);
+  const int x0 = max(ox * a.s - a.p, 0), x1 = min(ox * a.s - a.p + a.f, a.in_w);
   T* o = dst + ((oy - tl.dy0) * tl.dw + (ox - tl.dx0)) * c_in;
   for (int c = static_cast<int>(threadIdx.x) & 3; c < c_in; c += 4) {
-    const float m = fmaxf(fmaxf(to_f(p00[c]), to_f(p00[c + c_in])),
-                          fmaxf(to_f(p10[c]), to_f(p10[c + c_in])));
+    float m = -INFINITY;
+    for (int iy = y0; iy < y1; ++iy)
+      for (int ix = x0; ix < x1; ++ix) m = fmaxf(m, to_f(src[((iy - tl.sy0) * tl.sw + (ix - tl.sx0)) * c_in + c]));
     put(o + c, m);
   }
 }
@@ -859,8 +865,8 @@ hipError_t launch_conv(int kind, MfmaShape sh, const StageArgs& args, hipStream_
     return hipGetLastError();
   }
   // bf16 matrix-core stages run the LDS-ring kernel (conv_ring.hip); this
-  // register-staged kernel serves float32.
-  if constexpr (DT != MAFAT_F32) return hipErrorInvalidValue;
+  // register-staged kernel serves float32 ("same" 1x1 and 3x3 only).
+  if constexpr (DT != MAFAT_F32 || F == 0) return hipErrorInvalidValue;
   else switch (sh.depth) {
     case 3: return launch_mfma<DT, F, POOL, 3>(sh, args, stream, ev);
     case 4: return launch_mfma<DT, F, POOL, 4>(sh, args, stream, ev);
@@ -882,6 +888,9 @@ hipError_t launch_dt(int kind, int f, bool pool, MfmaShape sh, const StageArgs& 
                           : launch_conv<DT, 3, false>(kind, sh, args, stream, ev);
   if (f == 1) return pool ? launch_conv<DT, 1, true>(kind, sh, args, stream, ev)
                           : launch_conv<DT, 1, false>(kind, sh, args, stream, ev);
+  if (f == 0 && kind == K_CONV_DIRECT)  // any filter, stride and padding (stage arguments)
+    return pool ? launch_conv<DT, 0, true>(kind, sh, args, stream, ev)
+                : launch_conv<DT, 0, false>(kind, sh, args, stream, ev);
   return hipErrorInvalidValue;
 }
 

@@ -18,6 +18,10 @@ constexpr int kMaxTilesPerLaunch = 64;
 // Largest tensor extent the 16-bit tile descriptors can address.
 constexpr int kMaxExtent = 32767;
 
+// Largest filter and stride of a layer (the generic kernels loop over the
+// window at run time).
+constexpr int kMaxFilter = 11, kMaxStride = 4;
+
 enum StageKind { STAGE_CONV = 0, STAGE_POOL = 1 };
 
 // Where a stage reads from / writes to.
@@ -43,7 +47,7 @@ struct Stage {
   bool pool;         // conv stage with a fused 2x2/2 max-pool
   int in_h, in_w, cin;     // input tensor of the first layer
   int out_h, out_w, cout;  // output tensor of the last layer
-  int f, p, act;           // conv parameters (conv stages)
+  int f, s, p, act;        // filter, stride, padding (conv or pool), activation (conv)
   int src_buf, dst_buf;    // BufKind
   std::vector<TileGeom> tiles;
 };

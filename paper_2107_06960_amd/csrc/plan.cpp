@@ -18,21 +18,23 @@ void clear_error() { g_last_error.clear(); }
 namespace {
 
 bool layer_supported(const mafat_layer& L, std::string* why) {
+  // Any square filter up to kMaxFilter, stride up to kMaxStride, padding
+  // below the filter size (zero padding for a convolution; a max-pool takes
+  // the maximum over the in-image elements of its window).
+  if (L.op != MAFAT_CONV && L.op != MAFAT_MAXPOOL) { *why = "unknown layer op"; return false; }
+  if (L.f < 1 || L.f > kMaxFilter) { *why = "filter must be 1.." + std::to_string(kMaxFilter); return false; }
+  if (L.s < 1 || L.s > kMaxStride) { *why = "stride must be 1.." + std::to_string(kMaxStride); return false; }
+  if (L.p < 0 || L.p >= L.f) { *why = "padding must be 0..f-1"; return false; }
   if (L.op == MAFAT_CONV) {
-    if (L.f != 1 && L.f != 3) { *why = "convolution filter must be 1 or 3"; return false; }
-    if (L.s != 1) { *why = "convolution stride must be 1"; return false; }
-    if (L.p != (L.f - 1) / 2) { *why = "convolution padding must be (f-1)/2"; return false; }
     if (L.c_out < 1) { *why = "convolution c_out must be positive"; return false; }
     if (L.act != MAFAT_ACT_LINEAR && L.act != MAFAT_ACT_LEAKY01) { *why = "unknown activation"; return false; }
-    return true;
   }
-  if (L.op == MAFAT_MAXPOOL) {
-    if (L.f != 2 || L.s != 2 || L.p != 0) { *why = "max-pool must be 2x2, stride 2, no padding"; return false; }
-    return true;
-  }
-  *why = "unknown layer op";
-  return false;
+  return true;
 }
+
+// A 2x2, stride 2, unpadded max-pool: the one a convolution stage takes
+// into its epilogue.
+bool pool_2x2(const mafat_layer& L) { return L.op == MAFAT_MAXPOOL && L.f == 2 && L.s == 2 && L.p == 0; }
 
 // Tile i of N over the extent [0, E): [floor(iE/N), floor((i+1)E/N)).
 void split(int E, int N, int i, int* a, int* b) {
@@ -100,14 +102,14 @@ int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool parti
     S.first = l;
     if (L.op == MAFAT_CONV) {
       S.kind = STAGE_CONV;
-      S.pool = (l + 1 <= g1 && plan.layers[l + 1].op == MAFAT_MAXPOOL);
+      S.pool = (l + 1 <= g1 && pool_2x2(plan.layers[l + 1]));
       S.last = S.pool ? l + 1 : l;
-      S.f = L.f; S.p = L.p; S.act = L.act;
+      S.f = L.f; S.s = L.s; S.p = L.p; S.act = L.act;
     } else {
       S.kind = STAGE_POOL;
       S.pool = false;
       S.last = l;
-      S.f = L.f; S.p = 0; S.act = MAFAT_ACT_LINEAR;
+      S.f = L.f; S.s = L.s; S.p = L.p; S.act = MAFAT_ACT_LINEAR;
     }
     const auto& din = plan.dims[S.first];
     const auto& dout = plan.dims[S.last];

@@ -37,16 +37,23 @@ int fail(int status, const std::string& msg) {
 // input channels), output channels in multiples of 16, and its weights
 // addressable with 32-bit byte offsets (the source buffer is checked per
 // launch).
+// The matrix-core and first-layer kernels take "same" convolutions only:
+// f = 1 or 3, stride 1, padding (f - 1) / 2.  Every other convolution (and
+// channel count) runs on the generic kernel.
+bool same_conv(const Stage& S) {
+  return S.kind == STAGE_CONV && (S.f == 1 || S.f == 3) && S.s == 1 && S.p == (S.f - 1) / 2;
+}
+
 bool mfma_ok(const Stage& S, int dtype) {
   const int kc = (dtype == MAFAT_BF16) ? 32 : 16;
   const int64_t esz = (dtype == MAFAT_BF16) ? 2 : 4;
-  return S.kind == STAGE_CONV && S.cin % kc == 0 && S.cout % 16 == 0 &&
+  return same_conv(S) && S.cin % kc == 0 && S.cout % 16 == 0 &&
          static_cast<int64_t>(S.cout) * S.f * S.f * S.cin * esz < (1ll << 31);
 }
 
 // The vector first-layer kernel: 3 input channels, 3x3, 8/16/32/64 outputs.
 bool rgb_ok(const Stage& S) {
-  return S.kind == STAGE_CONV && S.cin == 3 && S.f == 3 &&
+  return same_conv(S) && S.cin == 3 && S.f == 3 &&
          (S.cout == 8 || S.cout == 16 || S.cout == 32 || S.cout == 64);
 }
 
@@ -239,8 +246,8 @@ bool fused_pair(const mafat_plan& P, const Group& G, int s, int dtype) {
   const Stage& A = G.stages[s];
   const Stage& B = G.stages[s + 1];
   if (A.kind != STAGE_CONV || B.kind != STAGE_CONV) return false;
-  if (A.f != 3 || A.p != 1 || A.pool || A.cin % 32 != 0 || A.cout != 128) return false;
-  if (B.f != 1 || B.p != 0 || B.pool || B.cin != 128 || B.cout != 64) return false;
+  if (!same_conv(A) || A.f != 3 || A.pool || A.cin % 32 != 0 || A.cout != 128) return false;
+  if (!same_conv(B) || B.f != 1 || B.pool || B.cin != 128 || B.cout != 64) return false;
   if (!mfma_ok(A, dtype) || A.tiles.size() != B.tiles.size()) return false;
   for (size_t t = 0; t < A.tiles.size(); ++t) {
     const TileGeom& a = A.tiles[t];
@@ -264,8 +271,8 @@ bool fused_first(const mafat_plan& P, const Group& G, int s, int dtype) {
   const Stage& A = G.stages[s];
   const Stage& B = G.stages[s + 1];
   if (A.kind != STAGE_CONV || B.kind != STAGE_CONV || A.src_buf != BUF_GROUP_IO) return false;
-  if (A.f != 3 || A.p != 1 || !A.pool || A.cin != 3 || A.cout != 32) return false;
-  if (B.f != 3 || B.p != 1 || !B.pool || B.cin != 32 || B.cout != 64) return false;
+  if (!same_conv(A) || A.f != 3 || !A.pool || A.cin != 3 || A.cout != 32) return false;
+  if (!same_conv(B) || B.f != 3 || !B.pool || B.cin != 32 || B.cout != 64) return false;
   if (!mfma_ok(B, dtype) || A.tiles.size() != B.tiles.size()) return false;
   // pooled blocks need even tile origins and extents (as for any fused pool)
   for (const TileGeom& T : B.tiles)
@@ -482,6 +489,7 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         A.act2 = S2->act;
       }
       A.in_h = SC.in_h; A.in_w = SC.in_w;
+      A.f = SC.f; A.s = SC.s; A.p = SC.p;
       A.cin = SC.cin; A.cout = SC.cout;
       A.act = SC.act;
       A.nblk_n = matrix ? (SC.cout + shape.bn - 1) / shape.bn : 1;
@@ -534,7 +542,7 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         } else if (kind == K_CONV_PATCH) {
           e = launch_conv_patch(S.pool, shape, A, stream, lev);
         } else {
-          e = launch_stage(kind, dtype, S.f, S.pool, shape, A, stream, lev);
+          e = launch_stage(kind, dtype, same_conv(S) ? S.f : 0, S.pool, shape, A, stream, lev);
         }
         if (A.total_blocks > 0) {
           launched = true;

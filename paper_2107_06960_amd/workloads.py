@@ -37,13 +37,15 @@ CONV, MAXPOOL = "conv", "max"
 LINEAR, LEAKY = "linear", "leaky"
 
 
-def conv(c_out: int, f: int = 3, act: str = LEAKY) -> dict:
-    """A stride-1 'same' convolution (pad (f-1)/2) with scale/bias + act."""
-    return {"op": CONV, "c_out": c_out, "f": f, "s": 1, "p": (f - 1) // 2, "act": act}
+def conv(c_out: int, f: int = 3, act: str = LEAKY, s: int = 1, p: int = None) -> dict:
+    """A convolution with scale/bias + act; by default stride 1 and 'same'
+    padding (f-1)/2."""
+    return {"op": CONV, "c_out": c_out, "f": f, "s": s, "p": (f - 1) // 2 if p is None else p, "act": act}
 
 
-def maxpool(f: int = 2, s: int = 2) -> dict:
-    return {"op": MAXPOOL, "c_out": 0, "f": f, "s": s, "p": 0, "act": LINEAR}
+def maxpool(f: int = 2, s: int = 2, p: int = 0) -> dict:
+    """A max-pool over the in-image elements of each f x f window."""
+    return {"op": MAXPOOL, "c_out": 0, "f": f, "s": s, "p": p, "act": LINEAR}
 
 
 # YOLOv2 layers 0-15.
@@ -55,6 +57,13 @@ YOLOV2_16 = [
 ]
 
 TINY = [conv(16), maxpool(), conv(32)]
+
+# Other layer kinds (the generalisation to other CNNs the paper names as
+# future work, section 6): a ResNet-style stem (7x7 stride-2 convolution,
+# 3x3 stride-2 padded max-pool) followed by 3x3 convolutions, a strided 3x3
+# downsampling convolution, a 3x3 stride-1 max-pool and a 5x5 convolution.
+OTHER_CNN = [conv(32, 7, s=2, p=3), maxpool(3, 2, 1), conv(32), conv(64, 3, s=2, p=1),
+             maxpool(3, 1, 1), conv(64, 5), conv(32, 1), maxpool(), conv(64)]
 
 
 def parse_tiling(spec: str, n_layers: int):

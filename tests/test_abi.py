@@ -67,12 +67,24 @@ def test_plan_regions_and_macs_match_oracle(lib, orc, name):
 
 
 def _random_supported(rng):
+    # "same" 1x1 / 3x3 convolutions and 2x2/2 pools, and now and then any
+    # filter, stride <= filter (so that receptive fields stay rectangles) and
+    # padding < filter, for convolutions and max-pools
     layers, c = [], int(rng.integers(1, 40))
     for _ in range(int(rng.integers(1, 7))):
-        if rng.random() < 0.35:
+        u = rng.random()
+        if u < 0.25:
             layers.append(W.maxpool())
-        else:
+        elif u < 0.6:
             layers.append(W.conv(int(rng.integers(1, 70)), int(rng.choice([1, 3]))))
+        else:
+            f = int(rng.integers(1, 8))
+            s = int(rng.integers(1, min(f, 3) + 1))
+            p = int(rng.integers(0, f))
+            if rng.random() < 0.5:
+                layers.append(W.maxpool(f, s, p))
+            else:
+                layers.append(W.conv(int(rng.integers(1, 40)), f, s=s, p=p))
     return layers, c
 
 
@@ -99,6 +111,23 @@ def test_plan_regions_random_match_bruteforce(lib, orc):
         for g in range(ng):
             assert np.array_equal(plan.regions(g), B[g]), (layers, h, w, c, gs, rows, cols)
         done += 1
+
+
+def test_other_cnn_regions_and_stages(lib, orc):
+    # strided and padded convolutions and pools (a ResNet-style stem, a 3x3
+    # stride-1 pool, a 5x5 convolution): regions equal the oracle's brute
+    # force; only 2x2/2 pools join the convolution before them in a stage
+    layers = W.OTHER_CNN
+    for tiling in ("3x3/NoCut", "2x3/4/2x2", "4x4/2/3x2/6/1x2"):
+        gs, r, c = W.parse_tiling(tiling, len(layers))
+        plan = M.Plan(layers, (224, 200, 3), tiling)
+        B = orc.regions_bruteforce(layers, 224, 200, 3, gs, r, c)
+        for g in range(len(gs)):
+            assert np.array_equal(plan.regions(g), B[g]), tiling
+    plan = M.Plan(layers, (224, 200, 3), "1x1/NoCut")
+    assert plan.stages(0) == [(0, 0), (1, 1), (2, 2), (3, 3), (4, 4), (5, 5), (6, 7), (8, 8)]
+    dims = orc.shapes(layers, 224, 200, 3)
+    assert [plan.shape(l) for l in range(len(layers))] == [tuple(d) for d in dims]
 
 
 def test_stages_fuse_conv_and_following_pool(lib):
@@ -268,9 +297,13 @@ def test_plan_create_error_codes(lib):
     pool = (1, 0, 2, 2, 0, 0)
     ok = _create_rc([conv3, pool], 16, 16, 3, [0], [2], [2])
     assert ok == M.MAFAT_OK
-    assert _create_rc([(0, 8, 5, 1, 2, 1)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED  # 5x5
-    assert _create_rc([(0, 8, 3, 2, 1, 1)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED  # stride 2
-    assert _create_rc([(1, 0, 3, 2, 0, 0)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED  # 3x3 pool
+    assert _create_rc([(0, 8, 5, 1, 2, 1)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_OK            # 5x5
+    assert _create_rc([(0, 8, 3, 2, 1, 1)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_OK            # stride 2
+    assert _create_rc([(1, 0, 3, 2, 1, 0)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_OK            # 3x3 pool
+    assert _create_rc([(0, 8, 13, 1, 6, 1)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED  # 13x13
+    assert _create_rc([(0, 8, 3, 5, 1, 1)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED   # stride 5
+    assert _create_rc([(1, 0, 3, 2, 3, 0)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED   # padding 3 >= f
+    assert _create_rc([(0, 8, 3, 1, -1, 1)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED  # padding < 0
     assert _create_rc([(0, 8, 3, 1, 1, 7)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EUNSUPPORTED  # activation
     assert _create_rc([(9, 8, 3, 1, 1, 1)], 16, 16, 3, [0], [1], [1]) == M.MAFAT_EINVAL        # op
     assert _create_rc([conv3, pool], 16, 16, 3, [0], [9], [1]) == M.MAFAT_ESHAPE               # grid > out

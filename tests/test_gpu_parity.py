@@ -229,6 +229,16 @@ def test_more_groups_and_other_networks(orc, dtype, part):
     _check_full(orc, VGG_LIKE, 64, 64, 3, "3x2/3/2x3/6/1x2", 1, dtype, seed=32, part=part)
 
 
+@pytest.mark.parametrize("tiling,batch", [("3x3/NoCut", 1), ("2x3/4/2x2", 2), ("4x4/2/3x2/6/1x2", 1)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_strided_and_padded_layers(orc, dtype, tiling, batch):
+    # a ResNet-style stem (7x7 stride-2 convolution, 3x3 stride-2 padded
+    # max-pool), a stride-2 3x3 convolution, a 3x3 stride-1 max-pool, a 5x5
+    # convolution: the generic kernels, tiled, against the oracle
+    _check_full(orc, W.OTHER_CNN, 224, 200, 3, tiling, batch, dtype, seed=41)
+    _check_full(orc, W.OTHER_CNN, 97, 131, 3, tiling, 1, dtype, seed=42, part=True)
+
+
 def test_pack_weights_kernel_layout():
     # the repack kernel against the layout written out with torch ops:
     # [cout/BN][cin/32][9][BN][32], rows past c_out zero
