@@ -26,9 +26,13 @@
  *   - dtype MAFAT_F32: float32 activations and weights, float32 accumulate.
  *     dtype MAFAT_BF16: bfloat16 activations and weights, float32 accumulate;
  *     every layer output is rounded to bfloat16 (nearest, ties to even).
- *   - Supported layers: convolution with f in {1, 3}, s = 1, p = (f-1)/2;
- *     max-pool with f = 2, s = 2, p = 0 (odd extents drop the last row or
- *     column).  Tensor extents must be at most 32767.
+ *   - Supported layers: convolution and max-pool with a square filter
+ *     1 <= f <= 11, stride 1 <= s <= 4 and padding 0 <= p < f; output extent
+ *     floor((in + 2p - f) / s) + 1.  A max-pool takes the maximum over the
+ *     in-image elements of its window.  3x3 and 1x1 "same" convolutions
+ *     (s = 1, p = (f-1)/2) run on the matrix cores, a 2x2/2 max-pool after
+ *     a convolution in its epilogue; other layers on generic vector-ALU
+ *     kernels.  Tensor extents must be at most 32767.
  *
  * Ownership and threading
  *   - A plan is created and destroyed by the library, read-only after
