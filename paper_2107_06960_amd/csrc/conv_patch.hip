@@ -478,21 +478,33 @@ void conv_patch_kernel(const StageArgs a) {
                                                    0, 0);
       lodd[k] = odd;
     }
-    // Patch pixel table, entry q = (qy, qx): bits 0-15 the LDS offset of its
-    // first-layer window (input patch row 2 qy, column 2 qx), bits 16-24 q,
-    // bits 25-26 its swizzle key ((qx >> 1) ^ 2 qy) & 3, bit 27 set if it
-    // lies inside this stage's input (else it is zero padding).
+    // Patch pixel table, one entry per MFMA row of the first-layer loop
+    // (tiles of 4 patch pixels, NIT per wave): entry q = (qy, qx), bits
+    // 0-15 the LDS offset of its first-layer window (input patch row 2 qy,
+    // column 2 qx), bits 16-31 where its pooled values go: the patch row
+    // (64 q) with its swizzle key ((qx >> 1) ^ 2 qy) & 3 in bits 4-5, or,
+    // for a pixel outside this stage's input (zero padding) or past the
+    // patch, a dummy row (the patch is zeroed first, so padding reads 0).
     constexpr int NQ = PR * PC;            // patch pixels
-    static_assert(XOFF + 2 * (PR - 1) * IRS + 2 * (PC - 1) * 8 < 65536 && NQ <= 512, "table fields");
-    static_assert(NQ <= 64 * NWAVE, "one table entry per thread");
-    if (tid < NQ) {
+    constexpr int NG = (NQ + 3) / 4;       // MFMA row tiles (4 patch pixels each)
+    constexpr int NIT = (NG + NWAVE - 1) / NWAVE;  // tiles per wave (the last one may run past NG)
+    constexpr int NQT = NIT * NWAVE * 4;   // table entries
+    constexpr int DUMMY = (QTOFF + NQT * 4 + 63) / 64 * 64;  // a 64-byte dummy patch row
+    static_assert(XOFF + 2 * (PR - 1) * IRS + 2 * (PC - 1) * 8 < 65536 && DUMMY + 64 <= SLOT && DUMMY < 65536,
+                  "table fields and dummy row");
+    static_assert(NQT <= 64 * NWAVE, "one table entry per thread");
+    if (tid < NQT) {
       const int qy = tid / PC, qx = tid - (tid / PC) * PC;
       const int gy = by0 - 1 + qy, gx = bx0 - 1 + qx;
-      const bool inside = gy >= 0 && gy < a.in_h && gx >= 0 && gx < a.in_w;
-      const unsigned e = static_cast<unsigned>(XOFF + 2 * qy * IRS + 2 * qx * 8) | (static_cast<unsigned>(tid) << 16) |
-                         (static_cast<unsigned>(((qx >> 1) ^ (qy << 1)) & 3) << 25) | (inside ? (1u << 27) : 0u);
+      const bool store = tid < NQ && gy >= 0 && gy < a.in_h && gx >= 0 && gx < a.in_w;
+      const unsigned row = store ? static_cast<unsigned>(tid * 64 + ((((qx >> 1) ^ (qy << 1)) & 3) << 4))
+                                 : static_cast<unsigned>(DUMMY);
+      const unsigned e = static_cast<unsigned>(XOFF + 2 * min(qy, PR - 1) * IRS + 2 * qx * 8) | (row << 16);
       *reinterpret_cast<unsigned*>(smem + QTOFF + tid * 4) = e;
     }
+    // zero the patch (padding pixels keep it)
+    for (int k = tid; k < A_BYTES / 16; k += 64 * NWAVE)
+      *reinterpret_cast<u32x4*>(smem + k * 16) = u32x4{0u, 0u, 0u, 0u};
     if (tid < W0P)
       *reinterpret_cast<u32x4*>(smem + W0OFF + tid * 16) = pre_v;
     else if (tid < W0P + C0 / 2)  // scale (C0 floats), then bias
@@ -539,10 +551,9 @@ void conv_patch_kernel(const StageArgs a) {
     // every element is scaled first.
     const float slope0 = act_slope(a.act0);
     const int lx = ((pl & 3) >> 1) * IRS + ((pl & 1) + kx) * 8;  // this lane's place in a window
-    constexpr int NG = (NQ + 3) / 4;       // MFMA row tiles (4 patch pixels each)
-    constexpr int NIT = (NG + NWAVE - 1) / NWAVE;  // tiles per wave (the last one may run past NG)
-    constexpr int DUMMY = QTOFF + (NQ * 4 + 255) / 256 * 256;  // stores of tiles past NG land here
-    static_assert(DUMMY + 64 * 2 <= SLOT, "dummy store area");
+    // this lane's part of a pooled value's store address: chunk (c >> 3) of
+    // channel c = 16 j + pl at bits 4-5 (XOR the pixel's key), c & 7 below
+    const unsigned sx = static_cast<unsigned>((pl >> 3) << 4), so = static_cast<unsigned>((pl & 7) * 2);
     // A fixed trip count, unrolled and free of branches, so that the
     // compiler can issue the next tiles' table and patch reads while the
     // current tile's MFMAs run; the sign test of the scales is hoisted out.
@@ -551,18 +562,13 @@ void conv_patch_kernel(const StageArgs a) {
 #pragma unroll
       for (int it = 0; it < NIT; ++it) {
         const int t = wave + NWAVE * it;
-        const int q = 4 * t + (pl >> 2);   // this lane's operand row: patch pixel q, window position pl & 3
-        const unsigned eq = qtab[q < NQ ? q : 0];
-        const int qo = 4 * t + kq;         // this lane's results: the window of patch pixel qo
-        const bool valid = qo < NQ;        // false only in tiles past NG
-        const unsigned eo = qtab[valid ? qo : 0];
+        const unsigned eq = qtab[4 * t + (pl >> 2)];  // operand row: patch pixel 4 t + (pl >> 2), window position pl & 3
+        const unsigned eo = qtab[4 * t + kq];         // results: the window of patch pixel 4 t + kq
         const unsigned char* xp = smem + (eq & 0xffffu) + lx;
         u32x2 xf[3];
 #pragma unroll
         for (int ky = 0; ky < 3; ++ky) xf[ky] = *reinterpret_cast<const u32x2*>(xp + ky * IRS);
-        const bool inside = (eo >> 27) & 1u;
-        const unsigned key = (eo >> 25) & 3u;
-        const unsigned srow = ((eo >> 16) & 0x1ffu) * 64 + (pl & 7) * 2;
+        const unsigned a0 = ((eo >> 16) ^ sx) + so;  // channel tile j = 0; j = 1 is chunk ^ 2
 #pragma unroll
         for (int j = 0; j < C0 / 16; ++j) {
           f32x4 acc0 = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -580,9 +586,7 @@ void conv_patch_kernel(const StageArgs a) {
             m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
           }
           m = fmaxf(m, slope0 * m);
-          const unsigned addr = valid ? srow + ((((2 * j + (pl >> 3)) ^ key) & 3u) << 4)
-                                      : static_cast<unsigned>(DUMMY + 2 * pl);
-          store1(reinterpret_cast<uint16_t*>(smem + addr), inside ? m : 0.f);
+          store1(reinterpret_cast<uint16_t*>(smem + (a0 ^ static_cast<unsigned>(32 * j))), m);
         }
       }
     };
