@@ -133,11 +133,16 @@ def untiled_groups(layers):
 
 def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs=2, part=False, packed=False,
                         tile_batch=0):
+    """Peak device memory of a run: torch's requested-bytes statistic (the
+    sizes of the buffers the caller allocates: input, output, cut tensors,
+    parameters, workspace; the library allocates nothing), its peak during
+    the runs minus its value before the network was built.  (The
+    allocator's own figure adds its block rounding.)  Returns (bytes, ms)."""
     import torch
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     torch.cuda.reset_peak_memory_stats()
-    base = torch.cuda.memory_allocated()
+    base = torch.cuda.memory_stats().get("requested_bytes.all.current", 0)
     plan = M.Plan(layers, hwc, tiling, stage_partition=part, packed_weights=packed, tile_batch=tile_batch)
     net = M.Network(plan, params, batch, dtype)
     x = net.input_tensor(x_np)
@@ -146,7 +151,7 @@ def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs
     for _ in range(runs):
         net.run(x)
     torch.cuda.synchronize()
-    peak = torch.cuda.max_memory_allocated() - base
+    peak = torch.cuda.memory_stats()["requested_bytes.all.peak"] - base
     t0 = time.perf_counter()
     n = 20
     for _ in range(n):
@@ -288,46 +293,73 @@ def measured_traffic(workload, stage_layers):
 
 def config_search(args):
     """Configuration search (Algorithm 2) against an exhaustive measurement
-    of its search space on this GPU: every candidate (cuts 16/12/8 x first
-    grid 1..5, second group 2x2) of the 608x608 bf16 batch-1 YOLOv2 stack is
-    timed; for each device-memory limit the search's pick (device memory
-    model, no bias) is compared with the fastest measured candidate whose
-    predicted memory fits.  Prints one JSON line."""
+    of its search space on this GPU, YOLOv2 layers 0-15 at 608x608, bf16,
+    batch 1.  Candidates: the paper's cuts (16 = no cut, 12, 8) x first-group
+    grids 1x1..5x5, second group 2x2, each run with every tile of a stage at
+    once (tile batch 'all') and with one tile at a time (tile batch 1, the
+    paper's execution order); every candidate is timed like the headline
+    (packed weights, warm-up, then host time over the steps) and its peak
+    device memory measured (torch's requested bytes).  For each
+    device-memory limit the search takes Algorithm 2 under the device model
+    of every tile at once, and if no candidate fits, under the model of one
+    tile at a time; it is compared with the fastest candidate whose measured
+    peak fits, as is the fastest measured candidate whose predicted memory
+    fits (the predictor with measured latencies).
+    Prints one JSON line per candidate and one summary line."""
     import torch
     from paper_2107_06960_amd import mafat as M
     from paper_2107_06960_amd import workloads as W
     torch.cuda.set_device(0)
     layers, hwc = W.YOLOV2_16, (608, 608, 3)
+    params = W.make_inputs(layers, *hwc, 1, 0, "bf16")
     cands = []
     for cut in (16, 12, 8):
         for t in (1, 2, 3, 4, 5):
-            cands.append(f"{t}x{t}/NoCut" if cut == 16 else f"{t}x{t}/{cut}/2x2")
-    params = W.make_inputs(layers, *hwc, 1, 0, "bf16")
+            spec = f"{t}x{t}/NoCut" if cut == 16 else f"{t}x{t}/{cut}/2x2"
+            for tb in (0, 1):
+                cands.append((spec, tb))
     meas = {}
-    for spec in cands:
-        plan = M.Plan(layers, hwc, spec)
+    for spec, tb in cands:
+        peak, _ = measure_peak_memory(M, layers, hwc, spec, params, 1, "bf16", params["x"], packed=True,
+                                      tile_batch=tb)
+        plan = M.Plan(layers, hwc, spec, packed_weights=True, tile_batch=tb)
         net = M.Network(plan, params, 1, "bf16")
         x = net.input_tensor(params["x"])
-        for _ in range(5):
+        for _ in range(args.warmup):
             net.run(x)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(args.steps):
             net.run(x)
         torch.cuda.synchronize()
-        meas[spec] = {"ms": (time.perf_counter() - t0) / args.steps * 1e3,
-                      "device_mib": plan.predict_mem("device", 1, "bf16") / 2 ** 20,
-                      "paper_f32_mib": plan.predict_mem("paper", 1, "f32") / 2 ** 20 + 31}
+        model = "device" if tb == 0 else "device_seq"
+        meas[(spec, tb)] = {"ms": (time.perf_counter() - t0) / args.steps * 1e3,
+                            "peak_mib": peak / 2 ** 20,
+                            "predicted_mib": plan.predict_mem(model, 1, "bf16") / 2 ** 20}
         del net, x
-        print(json.dumps({"candidate": spec, **{k: round(v, 4) for k, v in meas[spec].items()}}), flush=True)
+        print(json.dumps({"candidate": spec, "tile_batch": tb or "all",
+                          **{k: round(v, 4) for k, v in meas[(spec, tb)].items()}}), flush=True)
     rows = []
-    for lim in (21, 24, 26, 28, 30, 40, 64, 128):
+    for lim in (12, 13, 14, 16, 18, 20, 22, 24, 26, 28, 30, 34, 40):
         spec, pred, fits = M.mafat_get_config(layers, hwc, lim * 2 ** 20, model="device", batch=1, dtype="bf16")
-        ok = [c for c in cands if meas[c]["device_mib"] < lim]
+        tb = 0
+        if not fits:
+            spec, pred, fits = M.mafat_get_config(layers, hwc, lim * 2 ** 20, model="device_seq", batch=1,
+                                                  dtype="bf16")
+            tb = 1
+        ok = [c for c in cands if meas[c]["peak_mib"] <= lim]
         best = min(ok, key=lambda c: meas[c]["ms"]) if ok else None
-        rows.append({"limit_mib": lim, "search": spec, "fits": fits, "search_ms": round(meas[spec]["ms"], 4),
-                     "best": best, "best_ms": round(meas[best]["ms"], 4) if best else None,
-                     "slowdown_vs_best": round(meas[spec]["ms"] / meas[best]["ms"] - 1, 4) if best else None})
+        okp = [c for c in cands if meas[c]["predicted_mib"] < lim]
+        pm = min(okp, key=lambda c: meas[c]["ms"]) if okp else None
+        pick = meas[(spec, tb)]
+        rows.append({"limit_mib": lim, "search": spec, "search_tile_batch": tb or "all", "search_fits": fits,
+                     "search_ms": round(pick["ms"], 4), "search_peak_mib": round(pick["peak_mib"], 2),
+                     "best": best[0] if best else None, "best_tile_batch": (best[1] or "all") if best else None,
+                     "best_ms": round(meas[best]["ms"], 4) if best else None,
+                     "slowdown_vs_best": round(pick["ms"] / meas[best]["ms"] - 1, 4) if best else None,
+                     "predicted_measured": pm[0] if pm else None,
+                     "predicted_measured_tile_batch": (pm[1] or "all") if pm else None,
+                     "predicted_measured_ms": round(meas[pm]["ms"], 4) if pm else None})
     print(json.dumps({"config_search": rows}), flush=True)
 
 
