@@ -291,6 +291,28 @@ def measured_traffic(workload, stage_layers):
     return None
 
 
+def profiled_launch(workload, layers):
+    """Average duration (ms) of the launch running layers [a, b] under
+    rocprofv3's kernel trace, from the committed summary
+    profiles/stage_kernels_<workload>.md ('launch A-B: avg_us=...' lines
+    below a 'csrc_sha256:' line); None when it was taken on other kernel
+    sources or has no such line."""
+    path = os.path.join(ROOT, "profiles", f"stage_kernels_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    sha, want = None, f"launch {layers[0]}-{layers[1]}:"
+    with open(path) as fh:
+        for line in fh:
+            line = line.strip()
+            if line.startswith("csrc_sha256:"):
+                sha = line.split(":", 1)[1].strip()
+            elif line.startswith(want) and sha == csrc_digest():
+                for f in line[len(want):].split("#")[0].split():
+                    if f.startswith("avg_us="):
+                        return {"avg_ms": float(f[7:]) / 1e3, "source": os.path.relpath(path, ROOT)}
+    return None
+
+
 def config_search(args):
     """Configuration search (Algorithm 2) against an exhaustive measurement
     of its search space on this GPU, YOLOv2 layers 0-15 at 608x608, bf16,
@@ -643,6 +665,14 @@ def main():
         "per_launch_gflop": dom["gflop"], "per_launch_hbm_mb": dom["hbm_mb"], "avg_ms": dom["ms"],
         "timing": "kernel start/stop HIP events of the dispatch (hipExtLaunchKernel) on the launch stream, "
                   "averaged over the event-timed steps of the whole network"})
+    prof = profiled_launch(wl.name, dom["layers"])
+    if prof is not None:
+        # the same launch under rocprofv3's kernel trace (profiler overhead
+        # included), and the fraction it gives
+        roof["rocprof_avg_ms"] = round(prof["avg_ms"], 5)
+        roof["rocprof_frac"] = round(dom_f / (prof["avg_ms"] * 1e-3) / 1e12 / roof["peak"], 4) \
+            if roof["unit"] == "TFLOP/s" else None
+        roof["rocprof_source"] = prof["source"]
     tr = measured_traffic(wl.name, dom["layers"])
     if tr is not None:
         roof["traffic"] = tr["bytes"]

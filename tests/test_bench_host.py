@@ -46,3 +46,13 @@ def test_traffic_summary_matches_sources_or_is_ignored():
         assert tr["fetch_bytes"] > 0 and tr["write_bytes"] > 0
         assert tr["bytes"] == tr["fetch_bytes"] + tr["write_bytes"]
     assert bench.measured_traffic("no_such_workload", [8, 8]) is None
+
+
+def test_profiled_launch_matches_sources_or_is_ignored():
+    # the committed per-launch rocprofv3 averages are used only for the
+    # kernel sources they were taken on
+    p = bench.profiled_launch("yolo608_5x5_8_2x2", [0, 3])
+    if p is not None:
+        assert 0 < p["avg_ms"] < 1.0 and p["source"].startswith("profiles/")
+    assert bench.profiled_launch("no_such_workload", [0, 3]) is None
+    assert bench.profiled_launch("yolo608_5x5_8_2x2", [99, 99]) is None
