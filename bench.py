@@ -391,8 +391,9 @@ def all_configs(args):
     tile at a time (the paper's order): per-step latency (median, p10, p90 of HIP events on the
     launch stream around each mafat_run_network call, 10 warm-up steps
     first), frames/s at the median, executed TFLOP/s and its fraction of the
-    dtype's matrix-core peak, and peak device memory against the untiled
-    execution of the same layers.  One JSON line per workload."""
+    dtype's matrix-core peak, and peak device memory and median latency
+    (timed the same way) of the untiled execution of the same layers.  One
+    JSON line per workload and variant."""
     import numpy as np
     import torch
     from paper_2107_06960_amd import mafat as M
@@ -400,12 +401,9 @@ def all_configs(args):
     torch.cuda.set_device(0)
     ev = HipEvents()
     stream = torch.cuda.current_stream()
-    variants = ((False, 0), (True, 0), (False, 1))  # (stage partition, tile batch: 0 all tiles at once)
-    for name, wl, part, tb in [(n, w, r, k) for n, w in W.WORKLOADS.items() for r, k in variants]:
-        params = W.workload_inputs(wl)
-        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, stage_partition=part, packed_weights=True, tile_batch=tb)
-        net = M.Network(plan, params, wl.batch, wl.dtype)
-        x = net.input_tensor(params["x"])
+
+    def event_ms(net, x):
+        # 10 warm-up steps, then one start/stop event pair per step
         for _ in range(10):
             net.run(x)
         torch.cuda.synchronize()
@@ -418,19 +416,36 @@ def all_configs(args):
         torch.cuda.synchronize()
         ms = np.array([ev.ms(hs[2 * r], hs[2 * r + 1]) for r in range(n)])
         ev.destroy(hs)
-        p10, p50, p90 = (float(np.percentile(ms, q)) for q in (10, 50, 90))
+        return tuple(float(np.percentile(ms, q)) for q in (10, 50, 90))
+
+    variants = ((False, 0), (True, 0), (False, 1))  # (stage partition, tile batch: 0 all tiles at once)
+    untiled = {}
+    for name, wl, part, tb in [(n, w, r, k) for n, w in W.WORKLOADS.items() for r, k in variants]:
+        params = W.workload_inputs(wl)
+        plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, stage_partition=part, packed_weights=True, tile_batch=tb)
+        net = M.Network(plan, params, wl.batch, wl.dtype)
+        x = net.input_tensor(params["x"])
+        p10, p50, p90 = event_ms(net, x)
         ex = sum(2 * plan.macs(g)[0] for g in range(plan.n_groups)) * wl.batch
         us = sum(2 * plan.macs(g)[1] for g in range(plan.n_groups)) * wl.batch
         del net, x
         tp, _ = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch, wl.dtype,
                                     params["x"], part=part, packed=True, tile_batch=tb)
-        up, ums = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), untiled_groups(wl.layers), params,
-                                      wl.batch, wl.dtype, params["x"])
+        if name not in untiled:
+            up, _ = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), untiled_groups(wl.layers), params,
+                                        wl.batch, wl.dtype, params["x"], packed=True)
+            # the untiled execution timed the same way (events, median)
+            uplan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), untiled_groups(wl.layers), packed_weights=True)
+            unet = M.Network(uplan, params, wl.batch, wl.dtype)
+            ux = unet.input_tensor(params["x"])
+            untiled[name] = (up, event_ms(unet, ux)[1])
+            del unet, ux
+        up, ums = untiled[name]
         print(json.dumps({
             "workload": name, "input": f"{wl.h}x{wl.w}x{wl.c}", "batch": wl.batch, "dtype": wl.dtype,
             "tiling": wl.tiling, "stage_partition": part, "tile_batch": tb or "all",
             "weights": "packed" if wl.dtype == "bf16" else "KRSC",
-            "steps": n, "ms_p50": round(p50, 5), "ms_p10": round(p10, 5),
+            "steps": args.steps, "ms_p50": round(p50, 5), "ms_p10": round(p10, 5),
             "ms_p90": round(p90, 5), "frames_per_s": round(wl.batch / (p50 * 1e-3), 1),
             "gflop_executed": round(ex / 1e9, 3), "gflop_useful": round(us / 1e9, 3),
             "tflops_executed": round(ex / (p50 * 1e-3) / 1e12, 2),
