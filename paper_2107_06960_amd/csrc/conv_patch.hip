@@ -12,9 +12,9 @@
 // taps' MFMAs from LDS, the A operand of tap (ky, kx) being the patch
 // shifted by (ky, kx).
 //
-// GEMM view per chunk and tap: M = the block's pixels (row r <-> pixel
-// (r / BC, r % BC), or with a fused pool every 4 consecutive rows one 2x2
-// window), N = BN output channels, K = 32 channels:
+// GEMM view per chunk and tap: M = the block's pixels, window-major (every
+// 4 consecutive rows one 2x2 window, which a fused pool reduces in the
+// lane), N = BN output channels, K = 32 channels:
 // one v_mfma_f32_16x16x32_bf16 per 16x16 accumulator tile.
 //
 // Data movement: a ring of NS slots in LDS, slot = [patch pixels x 64 B]
@@ -23,9 +23,8 @@
 // 64 bytes per instruction): lane l writes row (l >> 2) of its 16-row group
 // at 16-byte position (l & 3) and fetches the row's 16-byte chunk
 // (l & 3) ^ key(row), so that the rows an MFMA fragment read serves per
-// LDS cycle hit distinct banks: weight rows use key = (row >> 1) & 3; patch
-// pixels the key of key_x / key_y below.  Patch pixels outside
-// the image (the
+// LDS cycle hit distinct banks: weight rows use key = (row >> 1) & 3, patch
+// pixels the key of patch_key below.  Patch pixels outside the image (the
 // zero padding), outside the tile's source region, or past the patch, and
 // weight rows past c_out, are fetched at an offset with bit 31 set, past the
 // buffer descriptor's range: the range check returns zeros.  Loads run NS-1
@@ -61,8 +60,9 @@
 // output never goes to memory.
 //
 // Requires f = 3, c_in % 32 == 0, c_out % 16 == 0, byte offsets below 2^31
-// within a frame's source buffer and within the weights (host-checked); a
-// fused pool needs even block sizes and even tile origins and extents.
+// within a frame's source buffer and within the weights (host-checked);
+// even block sizes (compile-time); a fused pool needs even tile origins and
+// extents.
 #include <hip/hip_runtime.h>
 
 #include "device_util.h"
@@ -114,39 +114,29 @@ __device__ __forceinline__ void pbarrier() { asm volatile("s_barrier" ::: "memor
 // Byte offset of 16-byte chunk q of 64-byte weight row `row` in a slot region.
 __device__ __forceinline__ int swz(int row, int q) { return row * 64 + ((q ^ ((row >> 1) & 3)) << 4); }
 
-// Swizzle key of patch pixel (py, px): 16-byte position p of the pixel's
-// 64-byte LDS row holds K chunk p ^ key, key = key_x(px) ^ key_y(py).
-// A 16-byte LDS read is served 16 lanes per cycle from 64 banks, the lanes
-// of one cycle being one half of the wave with one parity of lane bits 2-4
-// (calibrated with the hardware's bank-conflict counter); an MFMA fragment
-// read (row l & 15, K chunk l >> 4) is conflict-free when the 16 (patch row
-// mod 4, chunk ^ key) pairs of each such lane set differ.  With pixel-major
-// GEMM rows (16 pixels of one block row per fragment) key_x = (px >> 1) & 3,
-// key_y = 2 py does that for 8x16, 12x16 and 16x16 blocks; with window-major
-// rows (a fused pool: 4 windows of two rows per fragment) key_x = 0 and
-// key_y = py & 3 bit-reversed does it for 12x16 and 16x16 blocks.
-template <bool WIN>
-__device__ __forceinline__ int key_x(int px) {
-  return WIN ? 0 : (px >> 1) & 3;
-}
-template <bool WIN>
-__device__ __forceinline__ int key_y(int py) {
-  return WIN ? (((py & 1) << 1) | ((py >> 1) & 1)) : (py << 1) & 3;
+// GEMM rows of a block are window-major: every 4 consecutive rows are one
+// 2x2 window of the block (block sizes are even), windows row by row.  With
+// a fused pool a lane's 4 accumulator rows are then one pool window.
+template <int BC>
+__device__ __forceinline__ void block_pixel(int r, int* py, int* px) {
+  constexpr int WC = BC / 2;  // windows per block row
+  const int q = r >> 2, s = r & 3, wy = q / WC;
+  *py = 2 * wy + (s >> 1);
+  *px = 2 * (q - wy * WC) + (s & 1);
 }
 
-// Block pixel (py, px) of GEMM row r.
-template <int BC, bool POOL>
-__device__ __forceinline__ void block_pixel(int r, int* py, int* px) {
-  if (POOL) {
-    constexpr int WC = BC / 2;  // windows per block row
-    const int q = r >> 2, s = r & 3, wy = q / WC;
-    *py = 2 * wy + (s >> 1);
-    *px = 2 * (q - wy * WC) + (s & 1);
-  } else {
-    *py = r / BC;
-    *px = r - (r / BC) * BC;
-  }
-}
+// Swizzle key of patch pixel (py, px): 16-byte position p of the pixel's
+// 64-byte LDS row holds K chunk p ^ key.  A 16-byte LDS read is served 16
+// lanes per cycle from 64 banks, the lanes of one cycle being one half of
+// the wave with one parity of lane bits 2-4 (calibrated with the hardware's
+// bank-conflict counter); an MFMA fragment read (row l & 15, K chunk l >> 4)
+// is conflict-free when the 16 (patch row mod 4, chunk ^ key) pairs of each
+// such lane set differ.  With window-major GEMM rows, key = py & 3
+// bit-reversed makes every tap's fragment reads conflict-free for blocks
+// 8 or 16 pixels wide and leaves 0.75-1.3 extra cycles per 4-cycle read for
+// 10-, 12- and 18-wide ones (pixel-major rows with the best key of that form:
+// 0 for 16-wide blocks, 2.7-3.6 for the others).
+__device__ __forceinline__ int patch_key(int py) { return ((py & 1) << 1) | ((py >> 1) & 1); }
 
 // N2 > 0: a 1x1 convolution with N2 outputs of this stage's output (all BN
 // = c_out channels in the block) follows in the same workgroup: the block's
@@ -168,7 +158,7 @@ void conv_patch_kernel(const StageArgs a) {
   constexpr int LPS = NAW + NBW;  // loads per thread per chunk
   static_assert(MT >= 1 && NT >= 1 && MT * 16 == WM && NT * 16 == WN, "wave tile");
   static_assert(BR * BC <= BM && BM % (16 * WGM) == 0, "block rows");
-  static_assert(!POOL || (BR % 2 == 0 && BC % 2 == 0), "pooled blocks cover whole windows");
+  static_assert(BR % 2 == 0 && BC % 2 == 0, "blocks cover whole 2x2 windows (window-major GEMM rows)");
   static_assert(NS >= 1 && NS <= 6 && (NS - 2) * LPS <= 63, "ring depth");
   // Fused variant (N2 > 0): the 1x1 weights in their own LDS region past
   // the ring, then a second region Y for the second chunk's patch and the
@@ -355,7 +345,7 @@ void conv_patch_kernel(const StageArgs a) {
     const int py = p / PC, px = p - (p / PC) * PC;
     const int iy = by0 - 1 + py, ix = bx0 - 1 + px;
     const bool ok = g < NA && p < PR * PC && iy >= ry0 && iy < ry1 && ix >= rx0 && ix < rx1;
-    const int chunk = lpos ^ ((key_x<POOL>(px) ^ key_y<POOL>(py)) & 3);
+    const int chunk = lpos ^ patch_key(py);
     a_off[k] = ok ? static_cast<unsigned>((((iy - tl.sy0) * sw + (ix - tl.sx0)) * cin) * 2 + chunk * 16)
                   : 0x80000000u;
   }
@@ -381,21 +371,20 @@ void conv_patch_kernel(const StageArgs a) {
   // 16-byte chunk q = l >> 4 (K elements 8q .. 8q+7 of the 32).  B: weight
   // row tap * BN + wn*WN + 16 j + (l & 15), chunk q.
   const int q = lane >> 4;
-  // Per fragment: byte offset of the lane's patch pixel (tap (0, 0)) and the
-  // two halves of its swizzle key for each tap column / row.
-  int pb[MT], kx3[MT][3], ky3[MT][3];
+  // Per fragment: byte offset of the lane's patch pixel (tap (0, 0)) and its
+  // K chunk XOR the swizzle key for each tap row.  A padding row (past the
+  // block's pixels; its result is discarded) reads the pixel of row r ^ 12,
+  // a row served in the same LDS cycle (a broadcast, no conflict), or pixel 0.
+  int pb[MT], kq3[MT][3];
 #pragma unroll
   for (int i = 0; i < MT; ++i) {
     int r = wm * WM + i * 16 + (lane & 15);
-    r = (r < BR * BC) ? r : 0;  // padding rows: any valid pixel, result discarded
+    r = (r < BR * BC) ? r : (((r ^ 12) < BR * BC) ? (r ^ 12) : 0);
     int py, px;
-    block_pixel<BC, POOL>(r, &py, &px);
+    block_pixel<BC>(r, &py, &px);
     pb[i] = (py * PC + px) * 64;
 #pragma unroll
-    for (int d = 0; d < 3; ++d) {
-      kx3[i][d] = q ^ key_x<POOL>(px + d);
-      ky3[i][d] = key_y<POOL>(py + d);
-    }
+    for (int d = 0; d < 3; ++d) kq3[i][d] = q ^ patch_key(py + d);
   }
   const int rb = wn * WN + (lane & 15);
   const int b_lane = A_BYTES + swz(rb, q);  // (tap * BN + 16 j) rows later: same swizzle
@@ -418,7 +407,7 @@ void conv_patch_kernel(const StageArgs a) {
 #pragma unroll
     for (int i = 0; i < MT; ++i)
       af[i] = *reinterpret_cast<const u32x4*>(spa + pb[i] + (ty * PC + tx) * 64 +
-                                              (((kx3[i][tx] ^ ky3[i][ty]) & 3) << 4));
+                                              ((kq3[i][ty] & 3) << 4));
 #pragma unroll
     for (int j = 0; j < NT; ++j)
       bfr[j] = *reinterpret_cast<const u32x4*>(spb + b_lane + (t * BN + j * 16) * 64);
@@ -513,7 +502,7 @@ void conv_patch_kernel(const StageArgs a) {
       const int qy = tid / PC, qx = tid - (tid / PC) * PC;
       const int gy = by0 - 1 + qy, gx = bx0 - 1 + qx;
       const bool store = tid < NQ && gy >= 0 && gy < a.in_h && gx >= 0 && gx < a.in_w;
-      const unsigned row = store ? static_cast<unsigned>(tid * 64 + (((key_x<true>(qx) ^ key_y<true>(qy)) & 3) << 4))
+      const unsigned row = store ? static_cast<unsigned>(tid * 64 + (patch_key(qy) << 4))
                                  : static_cast<unsigned>(DUMMY);
       const unsigned e = static_cast<unsigned>(XOFF + 2 * min(qy, PR - 1) * IRS + 2 * qx * 8) | (row << 16);
       *reinterpret_cast<unsigned*>(smem + QTOFF + tid * 4) = e;
@@ -728,6 +717,8 @@ void conv_patch_kernel(const StageArgs a) {
           store1(reinterpret_cast<uint16_t*>(smem + (r >> 2) * RSB) + wn * WN + j * 16 + (lane & 15), mx);
       } else {
         const int r = wm * WM + i * 16 + (lane & 15);
+        int py, px;
+        block_pixel<BC>(r, &py, &px);  // staged at the pixel's row-major index
         float v[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -735,7 +726,9 @@ void conv_patch_kernel(const StageArgs a) {
           v[k] = fmaxf(v[k], slope * v[k]);
         }
         if (r < BR * BC)
-          store4<MAFAT_BF16>(reinterpret_cast<uint16_t*>(smem + r * RSB) + wn * WN + j * 16 + 4 * (lane >> 4), v);
+          store4<MAFAT_BF16>(reinterpret_cast<uint16_t*>(smem + (py * BC + px) * RSB) + wn * WN + j * 16 +
+                                 4 * (lane >> 4),
+                             v);
       }
     }
   }
