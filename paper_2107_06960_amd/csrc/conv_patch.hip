@@ -130,8 +130,8 @@ __device__ __forceinline__ void block_pixel(int r, int* py, int* px) {
 // lanes per cycle from 64 banks, the lanes of one cycle being one half of
 // the wave with one parity of lane bits 2-4 (calibrated with the hardware's
 // bank-conflict counter); an MFMA fragment read (row l & 15, K chunk l >> 4)
-// is conflict-free when the 16 (patch row mod 4, chunk ^ key) pairs of each
-// such lane set differ.  With window-major GEMM rows, key = py & 3
+// is conflict-free when the 16 (pixel's LDS row index mod 4, chunk ^ key)
+// pairs of each such lane set differ.  With window-major GEMM rows, key = py & 3
 // bit-reversed makes every tap's fragment reads conflict-free for blocks
 // 8 or 16 pixels wide and leaves 0.75-1.3 extra cycles per 4-cycle read for
 // 10-, 12- and 18-wide ones (pixel-major rows with the best key of that form:
