@@ -239,6 +239,60 @@ def test_strided_and_padded_layers(orc, dtype, tiling, batch):
     _check_full(orc, W.OTHER_CNN, 97, 131, 3, tiling, 1, dtype, seed=42, part=True)
 
 
+# The largest filter and stride the plan takes (11, 4), a 9x9 stride-3
+# convolution, padded 3x3 / 5x5 pools and a 1x1 stride-4 convolution.
+WIDE_STRIDES = [W.conv(32, 11, s=4, p=2), W.maxpool(3, 2, 0), W.conv(48, 5), W.maxpool(5, 1, 2),
+                W.conv(16, 9, s=3, p=4), W.conv(16, 1, s=4, p=0)]
+
+
+@pytest.mark.parametrize("tiling", ["3x3/NoCut", "2x3/2/2x1", "5x4/4/3x3"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_largest_filters_and_strides(orc, dtype, tiling):
+    # 227x227 -> 56x56 -> 27x27 -> 27x27 -> 27x27 -> 9x9 -> 3x3
+    _check_full(orc, WIDE_STRIDES, 227, 227, 3, tiling, 1, dtype, seed=51)
+    # 203x251 -> 50x62 -> 24x30 -> ... -> 8x10 -> 2x3, stage partition
+    _check_full(orc, WIDE_STRIDES, 203, 251, 3, "2x2/2/2x3", 1, dtype, seed=52, part=True)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_single_pixel_tiles(orc, dtype):
+    # every tile one output pixel: 20x20 = 400 tiles in group 1 (7 launches
+    # per stage) and 10x10 in group 2; ragged 1xN and Nx1 grids
+    layers = [W.conv(32), W.maxpool(), W.conv(32), W.maxpool(), W.conv(32, 1)]
+    _check_full(orc, layers, 40, 40, 32, "20x20/2/10x10", 1, dtype, seed=61)
+    _check_full(orc, layers, 40, 42, 32, "1x21/2/10x1", 2, dtype, seed=62)
+
+
+@pytest.mark.parametrize("dtype,hwc", [("bf16", (4096, 4096, 64)), ("f32", (2048, 2048, 128))])
+def test_two_gib_frame_runs_the_generic_kernel(orc, dtype, hwc):
+    # An input frame of 2^31 bytes: past the matrix-core kernels' 32-bit
+    # byte offsets, so the runtime takes the generic kernel; every output
+    # element is checked for being written, sampled rectangles (corners,
+    # edges, tile seams, interior) against the oracle.
+    h, w, c = hwc
+    layers = [W.conv(16)]
+    print(f"[parity] {h}x{w}x{c} {dtype}: 2^31-byte frame, generic kernel", flush=True)
+    # parameters by the usual recipe; the input (10^9 elements) seeded
+    # U[0, 1) in steps of 1/256, exact in bf16 (no rounding pass needed)
+    p = W.make_inputs(layers, 8, 8, c, 1, 71, dtype)
+    rng = np.random.default_rng(71)
+    p["x"] = rng.integers(0, 256, size=(1, h, w, c), dtype=np.uint8).astype(np.float32) / np.float32(256)
+    out, _, net, _ = run_gpu(layers, h, w, c, p, "2x2", 1, dtype)
+    del net
+    assert not np.isnan(out).any()
+    x = p["x"][0]
+    rects = [(0, 2, 0, 2), (h - 2, h, w - 2, w), (0, 2, w // 2 - 1, w // 2 + 1), (h // 2 - 1, h // 2 + 1, 0, 2),
+             (h // 2 - 1, h // 2 + 1, w // 2 - 1, w // 2 + 1), (1234, 1240, 777, 781), (h - 5, h, 3, 9)]
+    for (y0, y1, x0, x1) in rects:
+        # the oracle on the input rows/columns these outputs read (a 3x3
+        # "same" convolution: one more on each side, clipped to the image)
+        a0, a1, b0, b1 = max(0, y0 - 1), min(h, y1 + 1), max(0, x0 - 1), min(w, x1 + 1)
+        sub = orc.forward_layers(layers, a1 - a0, b1 - b0, c, x[None, a0:a1, b0:b1], p)[0]
+        ref = sub[y0 - a0:y1 - a0, x0 - b0:x1 - b0]
+        err = normwise_err(out[0, y0:y1, x0:x1], ref)
+        assert err <= TOL[dtype], ((y0, y1, x0, x1), err)
+
+
 def test_pack_weights_kernel_layout():
     # the repack kernel against the layout written out with torch ops:
     # [cout/BN][cin/32][9][BN][32], rows past c_out zero
