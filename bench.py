@@ -17,6 +17,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import dataclasses
 import json
 import os
 import sys
@@ -473,6 +474,9 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="yolo608_5x5_8_2x2")
+    ap.add_argument("--batch", type=int, default=0,
+                    help="frames per step (default: the workload's own batch); the committed "
+                         "profiles cover the workload's own batch only")
     ap.add_argument("--graph", action="store_true", help="replay one step from a captured HIP graph")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-untiled", action="store_true")
@@ -509,6 +513,9 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
     wl = W.WORKLOADS[args.workload]
+    own_batch = args.batch in (0, wl.batch)
+    if not own_batch:
+        wl = dataclasses.replace(wl, batch=args.batch)
     params = W.workload_inputs(wl)
     # The library's fast path: weights packed once for the patch kernels
     # (MAFAT_PLAN_PACKED_WEIGHTS, mafat_pack_weights at load, outside the
@@ -680,7 +687,9 @@ def main():
         "per_launch_gflop": dom["gflop"], "per_launch_hbm_mb": dom["hbm_mb"], "avg_ms": dom["ms"],
         "timing": "kernel start/stop HIP events of the dispatch (hipExtLaunchKernel) on the launch stream, "
                   "averaged over the event-timed steps of the whole network"})
-    prof = profiled_launch(wl.name, dom["layers"])
+    # rocprofv3 figures of the committed profiles (taken at the workload's
+    # own batch)
+    prof = profiled_launch(wl.name, dom["layers"]) if own_batch else None
     if prof is not None:
         # the same launch under rocprofv3's kernel trace (profiler overhead
         # included), and the fraction it gives
@@ -688,7 +697,7 @@ def main():
         roof["rocprof_frac"] = round(dom_f / (prof["avg_ms"] * 1e-3) / 1e12 / roof["peak"], 4) \
             if roof["unit"] == "TFLOP/s" else None
         roof["rocprof_source"] = prof["source"]
-    tr = measured_traffic(wl.name, dom["layers"])
+    tr = measured_traffic(wl.name, dom["layers"]) if own_batch else None
     if tr is not None:
         roof["traffic"] = tr["bytes"]
         roof["traffic_detail"] = tr
