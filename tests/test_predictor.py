@@ -9,9 +9,11 @@ Pins to the paper (section 2, section 5, Table 1):
   * Table 1's "Algorithm" column at 256, 192, 128, 32 and 16 MB (limits in
     MiB, bias 31 MiB, float32, 608x608) is reproduced by the search with
     this predictor.  At 96, 80, 64 and 48 MB the paper's own search picked
-    coarser configurations than Algorithm 1 read literally does (its "Grid"
-    sizes are not given): those rows are parity unpinned, and the test
-    records the literal reading's picks so a change shows up.
+    other configurations than Algorithm 1 read literally does (its "Grid"
+    sizes are not given): those rows are parity unpinned; for them the test
+    checks only that the library's search equals the oracle's (an
+    independent implementation of the same reading) and prints the paper's
+    configuration beside the pick.
 """
 import numpy as np
 import pytest
@@ -75,23 +77,28 @@ def test_paper_model_one_tile_is_darknet_layer2():
     assert 134.5 <= pred - layer2_input <= 135.5
 
 
-TABLE1_PINNED = {256: "1x1/NoCut", 192: "1x1/NoCut", 128: "2x2/NoCut", 32: "5x5/8/2x2", 16: "5x5/8/2x2"}
-# literal reading's picks where the paper printed 2x2/12/2x2, 3x3/8/2x2, 5x5/8/2x2, 5x5/8/2x2
-TABLE1_UNPINNED = {96: "2x2/NoCut", 80: "3x3/NoCut", 64: "4x4/NoCut", 48: "5x5/12/2x2"}
+# Table 1, "Algorithm" column: the configuration the paper's search picked
+# per memory limit (MB).
+TABLE1 = {256: "1x1/NoCut", 192: "1x1/NoCut", 128: "2x2/NoCut", 96: "2x2/12/2x2", 80: "3x3/8/2x2",
+          64: "5x5/8/2x2", 48: "5x5/8/2x2", 32: "5x5/8/2x2", 16: "5x5/8/2x2"}
+# rows the literal reading of Algorithms 1 and 2 reproduces
+TABLE1_PINNED = (256, 192, 128, 32, 16)
 
 
-@pytest.mark.parametrize("mb", sorted(TABLE1_PINNED) + sorted(TABLE1_UNPINNED))
+@pytest.mark.parametrize("mb", sorted(TABLE1))
 def test_search_table1(mb):
     _lib()
     spec, pred, fits = M.mafat_get_config(W.YOLOV2_16, (608, 608, 3), mb * MiB, model="paper", dtype="f32",
                                           bias_bytes=31 * MiB)
-    want = TABLE1_PINNED.get(mb, TABLE1_UNPINNED.get(mb))
-    assert spec == want
     assert fits == (mb > 43)  # 5x5/8/2x2 (42.8 MiB) is the smallest prediction: below it, the fallback
     # the oracle's search agrees
     cut, t, g2, opred, ofits = P.get_config(W.YOLOV2_16, 608, 608, 3, mb * MiB)
     ospec = f"{t}x{t}/NoCut" if cut == 16 else f"{t}x{t}/{cut}/{g2}x{g2}"
     assert (ospec, opred, ofits) == (spec, pred, fits)
+    if mb in TABLE1_PINNED:
+        assert spec == TABLE1[mb]
+    else:
+        print(f"Table 1 at {mb} MB: paper {TABLE1[mb]}, literal reading {spec} (parity unpinned)")
 
 
 def test_search_matches_oracle_over_limits():
