@@ -272,8 +272,10 @@ int mafat_workspace_size(const mafat_plan* plan, int32_t batch, int32_t dtype,
  *              entries); entries of max-pool layers are ignored
  *   workspace  device, 256-byte aligned, at least mafat_workspace_size bytes
  *   stream     hipStream_t (NULL: the default stream)
- * x and y must not overlap.  Errors: EINVAL, EUNSUPPORTED (dtype),
- * EWORKSPACE, EHIP. */
+ * x and y must not overlap.  Errors: EINVAL, EUNSUPPORTED (dtype, or a
+ * frame's group input, output or workspace share holding 2^31 elements or
+ * more), EWORKSPACE, EHIP.  Frames of 2^31 bytes or more (but fewer
+ * elements) run on the generic kernels. */
 int mafat_run_group(const mafat_plan* plan, int32_t group, int32_t batch, int32_t dtype,
                     const void* x, void* y, const void* const* w,
                     const float* const* scale, const float* const* bias,
