@@ -264,11 +264,11 @@ def test_single_pixel_tiles(orc, dtype):
 
 
 @pytest.mark.parametrize("dtype,hwc", [("bf16", (4096, 4096, 64)), ("f32", (2048, 2048, 128))])
-def test_two_gib_frame_runs_the_generic_kernel(orc, dtype, hwc):
+def test_two_gib_input_frame(orc, dtype, hwc):
     # An input frame of 2^31 bytes: past the matrix-core kernels' 32-bit
-    # byte offsets, so the runtime takes the generic kernel; every output
-    # element is checked for being written, sampled rectangles (corners,
-    # edges, tile seams, interior) against the oracle.
+    # byte offsets (the runtime routes such stages to the generic kernel);
+    # every output element is checked for being written, sampled
+    # rectangles (corners, edges, tile seams, interior) against the oracle.
     h, w, c = hwc
     layers = [W.conv(16)]
     print(f"[parity] {h}x{w}x{c} {dtype}: 2^31-byte frame, generic kernel", flush=True)
