@@ -241,15 +241,39 @@ int mafat_plan_stage_layers(const mafat_plan* plan, int32_t group, int32_t stage
  * workgroup's block of pixels.
  * *fused = 1 if mafat_run_group / mafat_run_network run stage `stage` of
  * group g together with stage + 1 in one kernel for this batch and dtype,
- * else 0.  This is the case for a bfloat16 3x3 convolution with 128
+ * else 0.  Two pairs qualify (bfloat16): a 3x3 convolution with 128
  * outputs and no pool whose next stage is a 1x1 convolution 128 -> 64 over
- * the same rectangles (YOLOv2's layers 4-5): the 1x1 GEMM runs on the 3x3
- * outputs held in LDS, so the intermediate never goes to memory (the layer
- * fusion inside a tile of the paper's fused tile partitioning, Sec. 3,
- * taken down to a workgroup's block).  mafat_run_stage always runs one
- * stage.  Errors: EINVAL (NULL, index out of range), EUNSUPPORTED (dtype). */
+ * the same rectangles (YOLOv2's layers 4-5: the 1x1 GEMM runs on the 3x3
+ * outputs held in LDS), and a group's first stage when it is a 3-channel
+ * 3x3 convolution with 32 outputs and a 2x2/2 pool followed by a 3x3
+ * convolution 32 -> 64 with a 2x2/2 pool (YOLOv2's layers 0-3: each
+ * workgroup computes the first layer's pooled output for its own input
+ * patch in LDS).  In both the intermediate never goes to memory.
+ * mafat_run_stage always runs one stage.  Errors: EINVAL (NULL, index out
+ * of range), EUNSUPPORTED (dtype). */
 int mafat_plan_stage_fused(const mafat_plan* plan, int32_t group, int32_t stage, int32_t batch,
                            int32_t dtype, int32_t* fused);
+
+/* Kernel families a stage can run on (mafat_plan_stage_kernel). */
+typedef enum {
+  MAFAT_KERNEL_PATCH = 0,        /* bf16 3x3 on the matrix cores, the input patch shared by the taps */
+  MAFAT_KERNEL_PATCH_FIRST = 1,  /* the same with the 3-channel first layer and its pool computed inside */
+  MAFAT_KERNEL_PATCH_1X1 = 2,    /* the same with the following 1x1 convolution computed inside */
+  MAFAT_KERNEL_RING = 3,         /* bf16 implicit GEMM through an LDS ring (1x1 convolutions) */
+  MAFAT_KERNEL_MFMA_F32 = 4,     /* float32 3x3 / 1x1 on the matrix cores */
+  MAFAT_KERNEL_FIRST_LAYER = 5,  /* a 3-channel 3x3 first layer run alone */
+  MAFAT_KERNEL_GENERIC = 6,      /* vector-ALU convolution: any supported layer and size */
+  MAFAT_KERNEL_POOL = 7          /* a max-pool that does not follow a convolution */
+} mafat_kernel;
+
+/* The per-tile layer execution of a group (sections 3 and 4) as launched on
+ * this GPU, for tests and tools: *kernel = the mafat_kernel family that
+ * runs stage `stage` of group g in mafat_run_group / mafat_run_network for
+ * this batch and dtype (both stages of a fused pair report the pair's
+ * kernel).  Errors: EINVAL (NULL, index out of range, batch < 1),
+ * EUNSUPPORTED (dtype). */
+int mafat_plan_stage_kernel(const mafat_plan* plan, int32_t group, int32_t stage, int32_t batch,
+                            int32_t dtype, int32_t* kernel);
 
 /* Working memory of a group's tiles (section 4: a tile's intermediate
  * results exist only while the tile is processed; section 4.1 sizes them).

@@ -739,6 +739,43 @@ extern "C" int mafat_plan_stage_fused(const mafat_plan* plan, int32_t group, int
   return MAFAT_OK;
 }
 
+extern "C" int mafat_plan_stage_kernel(const mafat_plan* plan, int32_t group, int32_t stage, int32_t batch,
+                                       int32_t dtype, int32_t* kernel) {
+  clear_error();
+  if (!plan || !kernel || group < 0 || group >= static_cast<int>(plan->groups.size()) || batch < 1) {
+    set_error("plan and kernel must be non-NULL, the group in range and batch >= 1");
+    return MAFAT_EINVAL;
+  }
+  const Group& G = plan->groups[group];
+  if (stage < 0 || stage >= static_cast<int>(G.stages.size())) {
+    set_error("stage out of range");
+    return MAFAT_EINVAL;
+  }
+  if (dtype != MAFAT_F32 && dtype != MAFAT_BF16) {
+    set_error("dtype must be F32 or BF16");
+    return MAFAT_EUNSUPPORTED;
+  }
+  // the choice run_group_impl makes (both stages of a fused pair run in
+  // the pair's kernel)
+  const StageConfig c = stage_config(*plan, G, G.stages[stage], batch, dtype);
+  if (c.fuse == 2 || c.fuse == -2) {
+    *kernel = MAFAT_KERNEL_PATCH_FIRST;
+  } else if (c.fuse == 1 || c.fuse == -1) {
+    *kernel = MAFAT_KERNEL_PATCH_1X1;
+  } else {
+    switch (c.kind) {
+      case K_CONV_PATCH: *kernel = MAFAT_KERNEL_PATCH; break;
+      case K_CONV_RING: *kernel = MAFAT_KERNEL_RING; break;
+      case K_CONV_MFMA: *kernel = MAFAT_KERNEL_MFMA_F32; break;
+      case K_CONV_RGB:
+      case K_CONV_RGB_MFMA: *kernel = MAFAT_KERNEL_FIRST_LAYER; break;
+      case K_POOL: *kernel = MAFAT_KERNEL_POOL; break;
+      default: *kernel = MAFAT_KERNEL_GENERIC; break;
+    }
+  }
+  return MAFAT_OK;
+}
+
 #ifdef MAFAT_TUNING
 // Tuning builds only: the configuration the runtime picks for stage s of
 // group g: kind, bm, bn, depth, kg, kord, br, bc.

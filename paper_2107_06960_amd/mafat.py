@@ -36,7 +36,7 @@ DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
 EXPORTS = ("mafat_plan_create", "mafat_plan_create_flags", "mafat_plan_destroy",
            "mafat_packed_weights_size", "mafat_pack_weights", "mafat_plan_layer_shape", "mafat_plan_group",
            "mafat_plan_num_tiles", "mafat_plan_regions", "mafat_plan_macs", "mafat_plan_stages", "mafat_plan_stage_layers",
-           "mafat_plan_stage_fused", "mafat_plan_set_tile_batch",
+           "mafat_plan_stage_fused", "mafat_plan_stage_kernel", "mafat_plan_set_tile_batch",
            "mafat_workspace_size", "mafat_run_group", "mafat_run_group_timed", "mafat_run_stage", "mafat_run_network",
            "mafat_run_network_static",
            "mafat_predict_mem", "mafat_get_config", "mafat_status_string", "mafat_last_error")
@@ -91,6 +91,7 @@ def lib():
         L.mafat_plan_stages.argtypes = [planp, i32, i32p]
         L.mafat_plan_stage_layers.argtypes = [planp, i32, i32, i32p, i32p]
         L.mafat_plan_stage_fused.argtypes = [planp, i32, i32, i32, i32, i32p]
+        L.mafat_plan_stage_kernel.argtypes = [planp, i32, i32, i32, i32, i32p]
         L.mafat_plan_set_tile_batch.argtypes = [planp, i32]
         L.mafat_workspace_size.argtypes = [planp, i32, i32, ctypes.POINTER(sz)]
         L.mafat_run_group.argtypes = [planp, i32, i32, i32, vp, vp, vpp, vpp, vpp, vp, sz, vp]
@@ -227,6 +228,18 @@ def mafat_plan_stage_fused(plan, group, stage, batch, dtype):
     return bool(f.value)
 
 
+# mafat_kernel values, by name
+KERNELS = ("patch", "patch_first", "patch_1x1", "ring", "mfma_f32", "first_layer", "generic", "pool")
+
+
+def mafat_plan_stage_kernel(plan, group, stage, batch, dtype):
+    """The kernel family (a KERNELS name) that runs a stage in mafat_run_group."""
+    out = ctypes.c_int32()
+    _check("mafat_plan_stage_kernel", lib().mafat_plan_stage_kernel(plan, group, stage, batch, DTYPES.get(dtype, dtype),
+                                                                    ctypes.byref(out)))
+    return KERNELS[out.value]
+
+
 def mafat_workspace_size(plan, batch, dtype):
     n = ctypes.c_size_t()
     _check("mafat_workspace_size", lib().mafat_workspace_size(plan, batch, dtype, ctypes.byref(n)))
@@ -360,6 +373,9 @@ class Plan:
 
     def stage_fused(self, g, s, batch=1, dtype="bf16"):
         return mafat_plan_stage_fused(self.handle, g, s, batch, dtype)
+
+    def stage_kernel(self, g, s, batch=1, dtype="bf16"):
+        return mafat_plan_stage_kernel(self.handle, g, s, batch, dtype)
 
     def launches(self, g, batch=1, dtype="bf16"):
         """The kernel launches of mafat_run_group for group g: lists of stage

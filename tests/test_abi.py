@@ -139,6 +139,47 @@ def test_stages_fuse_conv_and_following_pool(lib):
     assert plan.stages(1)[0] == (3, 3)
 
 
+def _kernels(plan, batch, dtype):
+    return [[plan.stage_kernel(g, s, batch, dtype) for s in range(len(plan.stages(g)))]
+            for g in range(plan.n_groups)]
+
+
+def test_stage_kernels(lib):
+    # which kernel family runs each stage (host-side routing, no GPU)
+    import bench
+    wl = W.WORKLOADS["yolo608_5x5_8_2x2"]
+    for part in (False, True):
+        plan = M.Plan(wl.layers, (608, 608, 3), wl.tiling, stage_partition=part, packed_weights=True)
+        assert _kernels(plan, 1, "bf16") == [
+            ["patch_first", "patch_first", "patch_1x1", "patch_1x1", "patch"],
+            ["patch", "ring", "patch", "patch", "ring", "patch", "ring"]]
+    # float32: the first layer alone, every other stage on the fp32 matrix cores
+    plan = M.Plan(W.YOLOV2_16, (416, 416, 3), "3x3/NoCut")
+    assert _kernels(plan, 1, "f32") == [["first_layer"] + ["mfma_f32"] * 11]
+    # every stage its own group: no fused pairs
+    plan = M.Plan(W.YOLOV2_16, (608, 608, 3), bench.untiled_groups(W.YOLOV2_16), packed_weights=True)
+    assert [k[0] for k in _kernels(plan, 1, "bf16")] == \
+        ["first_layer", "patch", "patch", "ring", "patch", "patch", "ring", "patch", "patch", "ring", "patch", "ring"]
+    # an input frame of 2^31 bytes leaves the matrix-core kernels' 32-bit
+    # byte offsets: the generic kernel; one column less stays on them
+    for dtype, big, small in (("bf16", (4096, 4096, 64), (4096, 4095, 64)),
+                              ("f32", (2048, 2048, 128), (2048, 2047, 128))):
+        assert _kernels(M.Plan([W.conv(16)], big, "2x2"), 1, dtype) == [["generic"]]
+        assert _kernels(M.Plan([W.conv(16)], small, "2x2"), 1, dtype) == [["patch" if dtype == "bf16" else "mfma_f32"]]
+    # strided, large-filter and padded-pool layers: generic kernels and lone
+    # pools; "same" 3x3 / 1x1 layers among them stay on the matrix cores
+    plan = M.Plan(W.OTHER_CNN, (224, 200, 3), "3x3/NoCut")
+    assert _kernels(plan, 1, "bf16") == [["generic", "pool", "patch", "generic", "pool", "generic", "ring", "patch"]]
+    # errors
+    h = plan.handle
+    out = ctypes.c_int32()
+    assert lib.mafat_plan_stage_kernel(h, 1, 0, 1, M.MAFAT_BF16, ctypes.byref(out)) == M.MAFAT_EINVAL
+    assert lib.mafat_plan_stage_kernel(h, 0, 8, 1, M.MAFAT_BF16, ctypes.byref(out)) == M.MAFAT_EINVAL
+    assert lib.mafat_plan_stage_kernel(h, 0, 0, 0, M.MAFAT_BF16, ctypes.byref(out)) == M.MAFAT_EINVAL
+    assert lib.mafat_plan_stage_kernel(h, 0, 0, 1, 7, ctypes.byref(out)) == M.MAFAT_EUNSUPPORTED
+    assert lib.mafat_plan_stage_kernel(h, 0, 0, 1, M.MAFAT_BF16, None) == M.MAFAT_EINVAL
+
+
 def test_fused_pair_detection(lib):
     # bf16: layers 0-1 (3 -> 32, pool) run inside layers 2-3 (3x3 32 -> 64,
     # pool), and layer 4 (3x3, 64 -> 128) with layer 5 (1x1, 128 -> 64), in

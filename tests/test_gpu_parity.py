@@ -266,12 +266,14 @@ def test_single_pixel_tiles(orc, dtype):
 @pytest.mark.parametrize("dtype,hwc", [("bf16", (4096, 4096, 64)), ("f32", (2048, 2048, 128))])
 def test_two_gib_input_frame(orc, dtype, hwc):
     # An input frame of 2^31 bytes: past the matrix-core kernels' 32-bit
-    # byte offsets (the runtime routes such stages to the generic kernel);
+    # byte offsets, so the runtime routes the stage to the generic kernel;
     # every output element is checked for being written, sampled
     # rectangles (corners, edges, tile seams, interior) against the oracle.
+    from paper_2107_06960_amd import mafat as M
     h, w, c = hwc
     layers = [W.conv(16)]
     print(f"[parity] {h}x{w}x{c} {dtype}: 2^31-byte frame, generic kernel", flush=True)
+    assert M.Plan(layers, hwc, "2x2").stage_kernel(0, 0, 1, dtype) == "generic"
     # parameters by the usual recipe; the input (10^9 elements) seeded
     # U[0, 1) in steps of 1/256, exact in bf16 (no rounding pass needed)
     p = W.make_inputs(layers, 8, 8, c, 1, 71, dtype)
