@@ -186,7 +186,7 @@ def cpu_baseline(wl, params, exec_macs_per_frame, min_wall_s=1.5, cone_s=(5.0, 1
 
     value: frames/s of the oracle's own fused-tile forward (forward_tiled,
     the workload's tiling, float64) on frame 0, with the layer loops split
-    over all usable host cores (at most 16, a one-GPU machine's CPU share),
+    over all usable host cores (at most 16 threads),
     repeated until at least min_wall_s of wall time.  single_thread: the
     oracle on one thread on 2x2-pixel output rectangles of frame 0 (each
     through its whole receptive field, untiled), its MAC rate scaled to the

@@ -17,7 +17,7 @@ def pytest_configure(config):
 def orc():
     from oracle import oracle
     oracle.lib()
-    # all host cores (at most 16, the CPU share of a one-GPU machine): the
+    # all host cores (at most 16 threads): the
     # layer loops split output rows into bands, results are unchanged
     oracle.set_threads(max(1, min(16, os.cpu_count() or 1)))
     return oracle
