@@ -21,7 +21,13 @@
  *
  * Readings where the paper is silent (each also listed in the design notes):
  *   - partition of an extent E into N parts: part i is [floor(iE/N),
- *     floor((i+1)E/N));
+ *     floor((i+1)E/N)), unless the caller gives the boundaries (variable
+ *     tiling, which section 6 proposes as future work: end tiles of another
+ *     size than the inner ones, so that the tiles' tasks vary less);
+ *   - balanced boundaries (orc_balanced_bounds): along one axis a tile's
+ *     task is the extent of its input region at the group's first layer;
+ *     the boundaries minimise the largest task extent, then the sum of the
+ *     squared task extents, then come first in lexicographic order;
  *   - padding: convolutions pad only outside the image (never at a tile
  *     border); a tile computes its halo itself (no data reuse);
  *   - every convolution is followed by scale/bias and its activation; a
@@ -294,6 +300,37 @@ static void split(int E, int N, int i, int* a, int* b) {
   *b = (int)(((long long)(i + 1) * E) / N);
 }
 
+/* Part i of N of [0, E): [bounds[i], bounds[i+1]) when the caller gave
+ * boundaries, else the even split. */
+static void span(int E, int N, int i, const int* bounds, int* a, int* b) {
+  if (bounds) { *a = bounds[i]; *b = bounds[i + 1]; }
+  else split(E, N, i, a, b);
+}
+
+/* Boundaries of N parts of [0, E): 0 = b[0] < b[1] < ... < b[N] = E. */
+static int bounds_ok(const int* b, int N, int E) {
+  if (b[0] != 0 || b[N] != E) return 0;
+  for (int i = 0; i < N; ++i)
+    if (b[i + 1] <= b[i]) return 0;
+  return 1;
+}
+
+/* Checks the per-group boundary lists (concatenated over groups, rows+1 /
+ * cols+1 entries per group; NULL = even splits) against the group output
+ * extents. */
+static int all_bounds_ok(const int* dims, int n, const int* gs, int ng, const int* rows,
+                         const int* cols, const int* rb, const int* cb) {
+  for (int g = 0; g < ng; ++g) {
+    int g1 = ((g + 1 < ng) ? gs[g + 1] : n) - 1;
+    const int* dl = dims + 6 * g1;
+    if (rb && !bounds_ok(rb, rows[g], dl[3])) return 0;
+    if (cb && !bounds_ok(cb, cols[g], dl[4])) return 0;
+    if (rb) rb += rows[g] + 1;
+    if (cb) cb += cols[g] + 1;
+  }
+  return 1;
+}
+
 /* Input interval of a layer (filter F, stride S, pad P) that the output
  * interval [a, b) reads, clipped to the input extent [0, E). */
 static void back_project(int a, int b, int F, int S, int P, int E, int* ia, int* ib) {
@@ -304,12 +341,25 @@ static void back_project(int a, int b, int F, int S, int P, int E, int* ia, int*
 int orc_regions(const orc_layer* layers, int n, int h, int w, int c,
                 const int* group_start, int n_groups, const int* grid_rows,
                 const int* grid_cols, int* out) {
+  return orc_regions_bounds(layers, n, h, w, c, group_start, n_groups, grid_rows, grid_cols,
+                            NULL, NULL, out);
+}
+
+int orc_regions_bounds(const orc_layer* layers, int n, int h, int w, int c,
+                       const int* group_start, int n_groups, const int* grid_rows,
+                       const int* grid_cols, const int* row_bounds, const int* col_bounds,
+                       int* out) {
   if (!out || !groups_ok(n, group_start, n_groups, grid_rows, grid_cols)) return ORC_EINVAL;
   int* dims = (int*)malloc(sizeof(int) * 6 * (size_t)n);
   if (!dims) return ORC_ENOMEM;
   int rc = orc_shapes(layers, n, h, w, c, dims);
   if (rc) { free(dims); return rc; }
+  if (!all_bounds_ok(dims, n, group_start, n_groups, grid_rows, grid_cols, row_bounds, col_bounds)) {
+    free(dims);
+    return ORC_EINVAL;
+  }
   int* o = out;
+  const int *rb = row_bounds, *cb = col_bounds;
   for (int g = 0; g < n_groups; ++g) {
     int g0 = group_start[g], g1 = ((g + 1 < n_groups) ? group_start[g + 1] : n) - 1;
     int R = grid_rows[g], Cc = grid_cols[g], nl = g1 - g0 + 1;
@@ -318,8 +368,8 @@ int orc_regions(const orc_layer* layers, int n, int h, int w, int c,
     for (int i = 0; i < R; ++i)
       for (int j = 0; j < Cc; ++j) {
         int oy0, oy1, ox0, ox1;
-        split(dl[3], R, i, &oy0, &oy1);
-        split(dl[4], Cc, j, &ox0, &ox1);
+        span(dl[3], R, i, rb, &oy0, &oy1);
+        span(dl[4], Cc, j, cb, &ox0, &ox1);
         for (int l = g1; l >= g0; --l) {
           const orc_layer* L = &layers[l];
           const int* d = dims + 6 * l;
@@ -333,6 +383,8 @@ int orc_regions(const orc_layer* layers, int n, int h, int w, int c,
         }
         o += nl * 8;
       }
+    if (rb) rb += R + 1;
+    if (cb) cb += Cc + 1;
   }
   free(dims);
   return ORC_OK;
@@ -357,12 +409,25 @@ static int mask_rect(const unsigned char* m, int H, int W, int* r) {
 int orc_regions_bruteforce(const orc_layer* layers, int n, int h, int w, int c,
                            const int* group_start, int n_groups,
                            const int* grid_rows, const int* grid_cols, int* out) {
+  return orc_regions_bruteforce_bounds(layers, n, h, w, c, group_start, n_groups, grid_rows,
+                                       grid_cols, NULL, NULL, out);
+}
+
+int orc_regions_bruteforce_bounds(const orc_layer* layers, int n, int h, int w, int c,
+                                  const int* group_start, int n_groups,
+                                  const int* grid_rows, const int* grid_cols,
+                                  const int* row_bounds, const int* col_bounds, int* out) {
   if (!out || !groups_ok(n, group_start, n_groups, grid_rows, grid_cols)) return ORC_EINVAL;
   int* dims = (int*)malloc(sizeof(int) * 6 * (size_t)n);
   if (!dims) return ORC_ENOMEM;
   int rc = orc_shapes(layers, n, h, w, c, dims);
   if (rc) { free(dims); return rc; }
+  if (!all_bounds_ok(dims, n, group_start, n_groups, grid_rows, grid_cols, row_bounds, col_bounds)) {
+    free(dims);
+    return ORC_EINVAL;
+  }
   int* o = out;
+  const int *rb = row_bounds, *cb = col_bounds;
   for (int g = 0; g < n_groups && rc == 0; ++g) {
     int g0 = group_start[g], g1 = ((g + 1 < n_groups) ? group_start[g + 1] : n) - 1;
     int R = grid_rows[g], Cc = grid_cols[g], nl = g1 - g0 + 1;
@@ -374,8 +439,8 @@ int orc_regions_bruteforce(const orc_layer* layers, int n, int h, int w, int c,
         int oh = dl[3], ow = dl[4];
         unsigned char* cur = (unsigned char*)calloc((size_t)oh * ow, 1);
         int a, b, p, q;
-        split(oh, R, i, &a, &b);
-        split(ow, Cc, j, &p, &q);
+        span(oh, R, i, rb, &a, &b);
+        span(ow, Cc, j, cb, &p, &q);
         for (int y = a; y < b; ++y)
           for (int x = p; x < q; ++x) cur[(size_t)y * ow + x] = 1;
         for (int l = g1; l >= g0 && rc == 0; --l) {
@@ -400,6 +465,8 @@ int orc_regions_bruteforce(const orc_layer* layers, int n, int h, int w, int c,
         free(cur);
         o += nl * 8;
       }
+    if (rb) rb += R + 1;
+    if (cb) cb += Cc + 1;
   }
   free(dims);
   return rc;
@@ -455,6 +522,17 @@ int orc_forward_tiled(const orc_layer* layers, int n, int h, int w, int c,
                       const double* x, const double* const* wt,
                       const double* const* scale, const double* const* bias,
                       int round_bf16, double* y, double* const* cut_out) {
+  return orc_forward_tiled_bounds(layers, n, h, w, c, batch, group_start, n_groups, grid_rows,
+                                  grid_cols, NULL, NULL, x, wt, scale, bias, round_bf16, y, cut_out);
+}
+
+int orc_forward_tiled_bounds(const orc_layer* layers, int n, int h, int w, int c,
+                             int batch, const int* group_start, int n_groups,
+                             const int* grid_rows, const int* grid_cols,
+                             const int* row_bounds, const int* col_bounds,
+                             const double* x, const double* const* wt,
+                             const double* const* scale, const double* const* bias,
+                             int round_bf16, double* y, double* const* cut_out) {
   if (batch < 1 || !x || !y) return ORC_EINVAL;
   int nreg = orc_regions_size(n, group_start, n_groups, grid_rows, grid_cols);
   if (nreg < 0) return nreg;
@@ -462,7 +540,9 @@ int orc_forward_tiled(const orc_layer* layers, int n, int h, int w, int c,
   int* regs = (int*)malloc(sizeof(int) * (size_t)nreg);
   if (!dims || !regs) { free(dims); free(regs); return ORC_ENOMEM; }
   int rc = orc_shapes(layers, n, h, w, c, dims);
-  if (!rc) rc = orc_regions(layers, n, h, w, c, group_start, n_groups, grid_rows, grid_cols, regs);
+  if (!rc)
+    rc = orc_regions_bounds(layers, n, h, w, c, group_start, n_groups, grid_rows, grid_cols,
+                            row_bounds, col_bounds, regs);
   for (int l = 0; l < n && !rc; ++l)
     if (layers[l].op == ORC_CONV && (!wt || !wt[l] || !scale || !scale[l] || !bias || !bias[l])) rc = ORC_EINVAL;
   const double* gin = x;
@@ -542,5 +622,68 @@ int orc_forward_rect(const orc_layer* layers, int n, int h, int w, int c,
   free(full);
   free(dims);
   free(regs);
+  return rc;
+}
+
+/* ------------------------------------------------------------------ */
+/* variable tiling: balanced boundaries                                 */
+/* ------------------------------------------------------------------ */
+
+/* Extent, at the input of layer g0, of the input region that the output
+ * interval [a, b) of layer g1 reads along one axis (axis 0: rows, 1:
+ * columns), by back-projecting the interval layer by layer. */
+static int task_extent(const orc_layer* layers, const int* dims, int g0, int g1, int axis,
+                       int a, int b) {
+  for (int l = g1; l >= g0; --l) {
+    const orc_layer* L = &layers[l];
+    int ia, ib;
+    back_project(a, b, L->f, L->s, L->p, dims[6 * l + axis], &ia, &ib);
+    a = ia;
+    b = ib;
+  }
+  return b - a;
+}
+
+int orc_balanced_bounds(const orc_layer* layers, int n, int h, int w, int c, int g0, int g1,
+                        int axis, int parts, int* bounds) {
+  if (!bounds || g0 < 0 || g1 < g0 || g1 >= n || (axis != 0 && axis != 1) || parts < 1)
+    return ORC_EINVAL;
+  int* dims = (int*)malloc(sizeof(int) * 6 * (size_t)n);
+  if (!dims) return ORC_ENOMEM;
+  int rc = orc_shapes(layers, n, h, w, c, dims);
+  const int E = rc ? 0 : dims[6 * g1 + 3 + axis];
+  if (!rc && parts > E) rc = ORC_EINVAL;
+  /* every choice of the parts-1 inner boundaries out of 1 .. E-1 */
+  double combos = 1.0;
+  for (int k = 0; k < parts - 1 && !rc; ++k) combos = combos * (double)(E - 1 - k) / (double)(k + 1);
+  if (!rc && combos > 2.0e8) rc = ORC_EINVAL;  /* brute force only: small cases */
+  int* cur = (int*)malloc(sizeof(int) * (size_t)(parts + 1));
+  if (!rc && !cur) rc = ORC_ENOMEM;
+  if (!rc) {
+    long long best_max = -1, best_sq = 0;
+    for (int k = 0; k <= parts; ++k) cur[k] = (k == parts) ? E : k;  /* first in lexicographic order */
+    for (;;) {
+      long long mx = 0, sq = 0;
+      for (int k = 0; k < parts; ++k) {
+        long long t = task_extent(layers, dims, g0, g1, axis, cur[k], cur[k + 1]);
+        if (t > mx) mx = t;
+        sq += t * t;
+      }
+      /* strictly better only: the first optimum in lexicographic order stays */
+      if (best_max < 0 || mx < best_max || (mx == best_max && sq < best_sq)) {
+        best_max = mx;
+        best_sq = sq;
+        memcpy(bounds, cur, sizeof(int) * (size_t)(parts + 1));
+      }
+      /* next combination: the last inner boundary that can still move */
+      int k = parts - 1;
+      while (k >= 1 && cur[k] == E - (parts - k)) --k;
+      if (k < 1) break;
+      ++cur[k];
+      for (int j = k + 1; j < parts; ++j) cur[j] = cur[j - 1] + 1;
+    }
+  }
+  free(cur);
+  free(dims);
   return rc;
 }

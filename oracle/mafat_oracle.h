@@ -68,12 +68,29 @@ int orc_regions(const orc_layer* layers, int n, int h, int w, int c,
                 const int* group_start, int n_groups, const int* grid_rows,
                 const int* grid_cols, int* out);
 
+/* orc_regions with each group's tile boundaries given (variable tiling,
+ * proposed in section 6): row_bounds holds, concatenated over groups,
+ * grid_rows[g] + 1 increasing row boundaries of group g's output (0 first,
+ * the output height last; tile row i covers [b[i], b[i+1])), col_bounds
+ * the same for columns.  Either may be NULL for even splits.  ORC_EINVAL
+ * for boundaries that are not strictly increasing from 0 to the extent. */
+int orc_regions_bounds(const orc_layer* layers, int n, int h, int w, int c,
+                       const int* group_start, int n_groups, const int* grid_rows,
+                       const int* grid_cols, const int* row_bounds, const int* col_bounds,
+                       int* out);
+
 /* The same table, built by enumerating every contributing input element of
  * every output element of each tile (receptive fields), layer by layer.
  * Returns ORC_ENOTRECT if a receptive field is not a full rectangle. */
 int orc_regions_bruteforce(const orc_layer* layers, int n, int h, int w, int c,
                            const int* group_start, int n_groups,
                            const int* grid_rows, const int* grid_cols, int* out);
+
+/* orc_regions_bruteforce with given tile boundaries (as orc_regions_bounds). */
+int orc_regions_bruteforce_bounds(const orc_layer* layers, int n, int h, int w, int c,
+                                  const int* group_start, int n_groups,
+                                  const int* grid_rows, const int* grid_cols,
+                                  const int* row_bounds, const int* col_bounds, int* out);
 
 /* FTP execution (sections 3-4): every group is split into its own output tile
  * grid, every tile is pushed through all layers of the group using only its
@@ -88,6 +105,27 @@ int orc_forward_tiled(const orc_layer* layers, int n, int h, int w, int c,
                       const double* x, const double* const* wt,
                       const double* const* scale, const double* const* bias,
                       int round_bf16, double* y, double* const* cut_out);
+
+/* orc_forward_tiled with given tile boundaries (as orc_regions_bounds). */
+int orc_forward_tiled_bounds(const orc_layer* layers, int n, int h, int w, int c,
+                             int batch, const int* group_start, int n_groups,
+                             const int* grid_rows, const int* grid_cols,
+                             const int* row_bounds, const int* col_bounds,
+                             const double* x, const double* const* wt,
+                             const double* const* scale, const double* const* bias,
+                             int round_bf16, double* y, double* const* cut_out);
+
+/* Balanced boundaries of `parts` tiles along one axis (0: rows, 1: columns)
+ * of the output of layer group [g0, g1] (variable tiling, section 6: end
+ * tiles sized differently from inner ones so that task sizes vary less).
+ * A tile's task along the axis is the extent of the input region of layer
+ * g0 that its output interval reads.  By brute force over every choice of
+ * boundaries: the smallest largest task extent, then the smallest sum of
+ * squared task extents, then the first boundary list in lexicographic
+ * order.  bounds receives parts + 1 values (0 ... extent).  ORC_EINVAL for
+ * parts outside 1 .. extent or more than 2e8 choices. */
+int orc_balanced_bounds(const orc_layer* layers, int n, int h, int w, int c, int g0, int g1,
+                        int axis, int parts, int* bounds);
 
 /* Output of the whole stack [0, n) on one output rectangle of one frame,
  * computed from that rectangle's receptive field only (a one-tile FTP).

@@ -64,6 +64,11 @@ def lib():
         L.orc_regions_bruteforce.argtypes = [lp, i, i, i, i, ip, i, ip, ip, ip]
         L.orc_forward_tiled.argtypes = [lp, i, i, i, i, i, ip, i, ip, ip, dp, dpp, dpp, dpp, i, dp, dpp]
         L.orc_forward_rect.argtypes = [lp, i, i, i, i, dp, dpp, dpp, dpp, i, i, i, i, i, dp]
+        L.orc_regions_bounds.argtypes = [lp, i, i, i, i, ip, i, ip, ip, ip, ip, ip]
+        L.orc_regions_bruteforce_bounds.argtypes = [lp, i, i, i, i, ip, i, ip, ip, ip, ip, ip]
+        L.orc_forward_tiled_bounds.argtypes = [lp, i, i, i, i, i, ip, i, ip, ip, ip, ip, dp, dpp, dpp,
+                                               dpp, i, dp, dpp]
+        L.orc_balanced_bounds.argtypes = [lp, i, i, i, i, i, i, i, i, ip]
         L.orc_set_threads.argtypes = [i]
         L.orc_round_bf16.argtypes = [ctypes.c_double]
         L.orc_round_bf16.restype = ctypes.c_double
@@ -127,7 +132,17 @@ def forward_layers(layers, h, w, c, x, params, l0=0, l1=None, round_bf16=False):
     return y
 
 
-def _region_call(fn, layers, h, w, c, group_start, rows, cols):
+def _bounds(bounds):
+    """Per-group boundary lists (None: even splits for every group) as one
+    concatenated int array and its pointer (NULL for None)."""
+    if bounds is None:
+        return None, None
+    flat = np.ascontiguousarray(np.concatenate([np.asarray(b, dtype=np.int32) for b in bounds]))
+    return flat, flat.ctypes.data_as(ctypes.POINTER(ctypes.c_int))
+
+
+def _region_call(fn, layers, h, w, c, group_start, rows, cols, with_bounds=False, row_bounds=None,
+                 col_bounds=None):
     n = len(layers)
     gs, gsp = _ints(group_start)
     r, rp = _ints(rows)
@@ -136,8 +151,13 @@ def _region_call(fn, layers, h, w, c, group_start, rows, cols):
     if size < 0:
         raise OracleError(size)
     out = np.zeros(size, dtype=np.int32)
-    _check(fn(_layers(layers), n, h, w, c, gsp, len(gs), rp, cp,
-              out.ctypes.data_as(ctypes.POINTER(ctypes.c_int))))
+    outp = out.ctypes.data_as(ctypes.POINTER(ctypes.c_int))
+    if with_bounds:
+        rb, rbp = _bounds(row_bounds)
+        cb, cbp = _bounds(col_bounds)
+        _check(fn(_layers(layers), n, h, w, c, gsp, len(gs), rp, cp, rbp, cbp, outp))
+    else:
+        _check(fn(_layers(layers), n, h, w, c, gsp, len(gs), rp, cp, outp))
     res, off = [], 0
     for g in range(len(gs)):
         end = gs[g + 1] if g + 1 < len(gs) else n
@@ -147,18 +167,35 @@ def _region_call(fn, layers, h, w, c, group_start, rows, cols):
     return res
 
 
-def regions(layers, h, w, c, group_start, rows, cols):
+def regions(layers, h, w, c, group_start, rows, cols, row_bounds=None, col_bounds=None):
     """List over groups of int arrays (tiles, layers_in_group, 8):
-    in y0,y1,x0,x1 then out y0,y1,x0,x1 (half-open)."""
-    return _region_call(lib().orc_regions, layers, h, w, c, group_start, rows, cols)
+    in y0,y1,x0,x1 then out y0,y1,x0,x1 (half-open).  row_bounds /
+    col_bounds: per-group boundary lists (rows+1 / cols+1 values each), or
+    None for even splits."""
+    if row_bounds is None and col_bounds is None:
+        return _region_call(lib().orc_regions, layers, h, w, c, group_start, rows, cols)
+    return _region_call(lib().orc_regions_bounds, layers, h, w, c, group_start, rows, cols, True,
+                        row_bounds, col_bounds)
 
 
-def regions_bruteforce(layers, h, w, c, group_start, rows, cols):
-    return _region_call(lib().orc_regions_bruteforce, layers, h, w, c, group_start, rows, cols)
+def regions_bruteforce(layers, h, w, c, group_start, rows, cols, row_bounds=None, col_bounds=None):
+    if row_bounds is None and col_bounds is None:
+        return _region_call(lib().orc_regions_bruteforce, layers, h, w, c, group_start, rows, cols)
+    return _region_call(lib().orc_regions_bruteforce_bounds, layers, h, w, c, group_start, rows, cols,
+                        True, row_bounds, col_bounds)
+
+
+def balanced_bounds(layers, h, w, c, g0, g1, axis, parts):
+    """Balanced tile boundaries along one axis (0 rows, 1 columns) of group
+    [g0, g1], by brute force (see orc_balanced_bounds)."""
+    out = np.zeros(parts + 1, dtype=np.int32)
+    _check(lib().orc_balanced_bounds(_layers(layers), len(layers), h, w, c, g0, g1, axis, parts,
+                                     out.ctypes.data_as(ctypes.POINTER(ctypes.c_int))))
+    return out
 
 
 def forward_tiled(layers, h, w, c, x, params, group_start, rows, cols, round_bf16=False,
-                  want_cuts=False):
+                  want_cuts=False, row_bounds=None, col_bounds=None):
     n = len(layers)
     dims = shapes(layers, h, w, c)
     x, xp = _dbl(x)
@@ -179,9 +216,11 @@ def forward_tiled(layers, h, w, c, x, params, group_start, rows, cols, round_bf1
     kw, wp = _ptr_list(params["w"])
     ks, sp = _ptr_list(params["scale"])
     kb, bp = _ptr_list(params["bias"])
-    _check(lib().orc_forward_tiled(_layers(layers), n, h, w, c, batch, gsp, len(gs), rp, cp, xp,
-                                   wp, sp, bp, int(round_bf16),
-                                   y.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), cut_pp))
+    rb, rbp = _bounds(row_bounds)
+    cb, cbp = _bounds(col_bounds)
+    _check(lib().orc_forward_tiled_bounds(_layers(layers), n, h, w, c, batch, gsp, len(gs), rp, cp,
+                                          rbp, cbp, xp, wp, sp, bp, int(round_bf16),
+                                          y.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), cut_pp))
     return (y, cuts) if want_cuts else y
 
 
