@@ -133,7 +133,7 @@ def untiled_groups(layers):
 
 
 def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs=2, part=False, packed=False,
-                        tile_batch=0):
+                        tile_batch=0, bounds=None):
     """Peak device memory of a run: torch's requested-bytes statistic (the
     sizes of the buffers the caller allocates: input, output, cut tensors,
     parameters, workspace; the library allocates nothing), its peak during
@@ -144,7 +144,8 @@ def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs
     torch.cuda.empty_cache()
     torch.cuda.reset_peak_memory_stats()
     base = torch.cuda.memory_stats().get("requested_bytes.all.current", 0)
-    plan = M.Plan(layers, hwc, tiling, stage_partition=part, packed_weights=packed, tile_batch=tile_batch)
+    plan = M.Plan(layers, hwc, tiling, stage_partition=part, packed_weights=packed, tile_batch=tile_batch,
+                  bounds=bounds)
     net = M.Network(plan, params, batch, dtype)
     x = net.input_tensor(x_np)
     torch.cuda.synchronize()
@@ -386,6 +387,71 @@ def config_search(args):
     print(json.dumps({"config_search": rows}), flush=True)
 
 
+def variable_tiling(args):
+    """Variable tiling (each group's balanced tile boundaries,
+    mafat_balanced_bounds) against the even split, YOLOv2 layers 0-15,
+    608x608x3, bf16, batch 1, on the paper's candidates (cuts 16 = no cut,
+    12, 8; first-group grids 2x2..5x5; second group 2x2), each with every
+    tile of a stage at once and with one tile at a time (the paper's order):
+    the largest tile input region of each group, predicted memory (the
+    paper's model and the device model of the tile batch), measured peak
+    device memory and host time per frame (packed weights, warm-up, then
+    the steps).  One JSON line per candidate, then, per device-memory limit,
+    the first candidate in Algorithm 2's order whose one-tile-at-a-time
+    prediction fits, with even and with balanced boundaries."""
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    from paper_2107_06960_amd import workloads as W
+    torch.cuda.set_device(0)
+    layers, hwc = W.YOLOV2_16, (608, 608, 3)
+    params = W.make_inputs(layers, *hwc, 1, 0, "bf16")
+    order, meas = [], {}
+    for cut in (16, 12, 8):
+        for t in (2, 3, 4, 5):
+            spec = f"{t}x{t}/NoCut" if cut == 16 else f"{t}x{t}/{cut}/2x2"
+            order.append(spec)
+            for bounds in (None, "balanced"):
+                for tb in (0, 1):
+                    peak, _ = measure_peak_memory(M, layers, hwc, spec, params, 1, "bf16", params["x"],
+                                                  packed=True, tile_batch=tb, bounds=bounds)
+                    plan = M.Plan(layers, hwc, spec, packed_weights=True, tile_batch=tb, bounds=bounds)
+                    net = M.Network(plan, params, 1, "bf16")
+                    x = net.input_tensor(params["x"])
+                    for _ in range(args.warmup):
+                        net.run(x)
+                    torch.cuda.synchronize()
+                    t0 = time.perf_counter()
+                    for _ in range(args.steps):
+                        net.run(x)
+                    torch.cuda.synchronize()
+                    ms = (time.perf_counter() - t0) / args.steps * 1e3
+                    del net, x
+                    largest = []
+                    for g in range(plan.n_groups):
+                        R = plan.regions(g)
+                        largest.append(int(((R[:, 0, 1] - R[:, 0, 0]) * (R[:, 0, 3] - R[:, 0, 2])).max()))
+                    rec = {"candidate": spec, "bounds": bounds or "even", "tile_batch": tb or "all",
+                           "row_bounds": plan.bounds[0] if plan.bounds else None,
+                           "largest_input_region_px": largest,
+                           "predicted_paper_mib": round(plan.predict_mem("paper", 1, "bf16") / 2 ** 20, 3),
+                           "predicted_mib": round(plan.predict_mem("device" if tb == 0 else "device_seq", 1,
+                                                                   "bf16") / 2 ** 20, 3),
+                           "peak_mib": round(peak / 2 ** 20, 3), "ms": round(ms, 4)}
+                    meas[(spec, bounds, tb)] = rec
+                    print(json.dumps(rec), flush=True)
+    rows = []
+    for lim in (11, 11.5, 12, 12.5, 13, 14):
+        row = {"limit_mib": lim}
+        for bounds in (None, "balanced"):
+            pick = next((c for c in order if meas[(c, bounds, 1)]["predicted_mib"] < lim), None)
+            key = bounds or "even"
+            row[key] = pick
+            row[key + "_ms"] = meas[(pick, bounds, 1)]["ms"] if pick else None
+            row[key + "_peak_mib"] = meas[(pick, bounds, 1)]["peak_mib"] if pick else None
+        rows.append(row)
+    print(json.dumps({"variable_tiling_search": rows}), flush=True)
+
+
 def all_configs(args):
     """Every workload of the build (the paper's configurations and the six
     cut x grid runs), each with every tile at once, with the stage partition, and one
@@ -486,6 +552,8 @@ def main():
                     help="latency quantiles, throughput and peak memory of every workload (one JSON line each)")
     ap.add_argument("--config-search", action="store_true",
                     help="only evaluate the configuration search against a measured sweep and exit")
+    ap.add_argument("--variable-tiling", action="store_true",
+                    help="only compare balanced (variable) tile boundaries with the even split and exit")
     ap.add_argument("--copy-calibration", type=int, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -494,6 +562,9 @@ def main():
         return
     if args.config_search:
         config_search(args)
+        return
+    if args.variable_tiling:
+        variable_tiling(args)
         return
     if args.all_configs:
         all_configs(args)
@@ -564,7 +635,7 @@ def main():
         torch.cuda.synchronize()
         return (time.perf_counter() - t0) / args.steps * 1e3
 
-    partition_ms = krsc_ms = untiled_ms = None
+    partition_ms = krsc_ms = untiled_ms = balanced_ms = None
     if not args.no_untiled:
         # The untiled layer-by-layer execution (every stage its own group on
         # a 1x1 grid, same kernels, packed weights), timed exactly like the
@@ -575,6 +646,8 @@ def main():
         # of every stage output; no halo recompute), and with KRSC weights.
         partition_ms = time_variant(stage_partition=True, packed_weights=True)
         krsc_ms = time_variant()
+        # Variable tiling: each group's balanced tile boundaries.
+        balanced_ms = time_variant(packed_weights=True, bounds="balanced")
 
     # The same step replayed from a captured HIP graph (reported beside the
     # plain loop, which is the headline value).
@@ -718,6 +791,7 @@ def main():
         "graph_ms_per_step": round(graph_ms, 5) if graph_ms is not None else None,
         "stage_partition_ms_per_step": round(partition_ms, 5) if partition_ms is not None else None,
         "krsc_weights_ms_per_step": round(krsc_ms, 5) if krsc_ms is not None else None,
+        "balanced_bounds_ms_per_step": round(balanced_ms, 5) if balanced_ms is not None else None,
         "step_ms_events": {q: round(float(np.percentile(step_ev_ms, v)), 5)
                            for q, v in (("p10", 10), ("p50", 50), ("p90", 90))},
         "group_ms": [round(v, 5) for v in group_ms],

@@ -147,6 +147,45 @@ int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_layers, int32_t
                             int32_t n_groups, const int32_t* grid_rows,
                             const int32_t* grid_cols, int32_t flags, mafat_plan** out);
 
+/* mafat_plan_create_flags with each group's tile boundaries given: variable
+ * tiling, which section 6 proposes as future work (end tiles sized unlike
+ * the inner ones, so that the tiles' tasks vary less and the largest
+ * footprint falls).
+ *   row_bounds  concatenated over groups, grid_rows[g] + 1 row boundaries
+ *               of group g's output: 0 = b[0] < b[1] < ... < b[rows] = the
+ *               output height; tile row i covers rows [b[i], b[i+1])
+ *   col_bounds  the same for columns (grid_cols[g] + 1 per group)
+ * Either may be NULL: the floor split of mafat_plan_create on that axis for
+ * every group.  Host arrays, read during the call only.  Everything else
+ * (regions, stages, kernels, workspace, predictor) follows the given tiles.
+ * Errors: those of mafat_plan_create_flags; ESHAPE (boundaries not strictly
+ * increasing from 0 to the group output extent); EUNSUPPORTED (boundaries
+ * with MAFAT_PLAN_STAGE_PARTITION, which splits every stage evenly). */
+int mafat_plan_create_bounds(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
+                             int32_t in_w, int32_t in_c, const int32_t* group_start,
+                             int32_t n_groups, const int32_t* grid_rows,
+                             const int32_t* grid_cols, const int32_t* row_bounds,
+                             const int32_t* col_bounds, int32_t flags, mafat_plan** out);
+
+/* Balanced tile boundaries for variable tiling (section 6) of the group of
+ * layers [first_layer, last_layer] of the stack (shapes inferred from the
+ * in_h x in_w x in_c input): `rows` parts of the group output's height into
+ * row_bounds[rows + 1], `cols` parts of its width into col_bounds[cols + 1]
+ * (either pointer may be NULL to skip that axis).  Along an axis a tile's
+ * task extent is the extent of the input region of first_layer that its
+ * output interval reads (back-projected through the group, clipped to the
+ * tensor, as mafat_plan_regions).  The boundaries minimise the largest task
+ * extent, then the sum of the squared task extents, and are the first such
+ * list in lexicographic order (exact: bisection on the largest extent, then
+ * a dynamic programme).  Pass them to mafat_plan_create_bounds.
+ * Errors: EINVAL (null layers, layer range outside the stack), the shape
+ * errors of mafat_plan_create, ESHAPE (parts outside 1 .. extent),
+ * EUNSUPPORTED (a search too large to run). */
+int mafat_balanced_bounds(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
+                          int32_t in_w, int32_t in_c, int32_t first_layer,
+                          int32_t last_layer, int32_t rows, int32_t cols,
+                          int32_t* row_bounds, int32_t* col_bounds);
+
 /* Tile batches (the order of section 4, where the tiles of a group are
  * processed one after another): run at most `tiles` tiles of a group at a
  * time (0: all tiles at once, the default).  mafat_run_group / mafat_run_network then
@@ -414,6 +453,20 @@ int mafat_get_config(const mafat_layer* layers, int32_t n_layers, int32_t in_h, 
                      int64_t limit_bytes, const int32_t* cuts, int32_t n_cuts, const int32_t* grids,
                      int32_t n_grids, int32_t second_grid, int32_t* out_cut, int32_t* out_grid1,
                      int32_t* out_grid2, int64_t* out_pred, int32_t* out_fits);
+
+/* mafat_get_config with variable tiling (section 6): the same search, with
+ * every candidate's groups split at their mafat_balanced_bounds boundaries
+ * instead of evenly (square grids, rows and columns balanced alike).  The
+ * chosen configuration is planned with mafat_balanced_bounds and
+ * mafat_plan_create_bounds.  Same arguments, outputs and errors as
+ * mafat_get_config, plus those of mafat_balanced_bounds and ENOMEM. */
+int mafat_get_config_balanced(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
+                              int32_t in_w, int32_t in_c, int32_t model, int32_t batch,
+                              int32_t dtype, int64_t bias_bytes, int64_t limit_bytes,
+                              const int32_t* cuts, int32_t n_cuts, const int32_t* grids,
+                              int32_t n_grids, int32_t second_grid, int32_t* out_cut,
+                              int32_t* out_grid1, int32_t* out_grid2, int64_t* out_pred,
+                              int32_t* out_fits);
 
 /* Error reporting of this library (no counterpart in the paper).
  * Static text of a status code. */

@@ -4,6 +4,8 @@
 // workspace sizing and multiply-accumulate accounting.  Pure integer host
 // code; no HIP calls.
 #include <algorithm>
+#include <climits>
+#include <cstdint>
 #include <cstring>
 #include <new>
 
@@ -49,7 +51,18 @@ void back_project(int a, int b, int F, int S, int P, int E, int* ia, int* ib) {
   *ib = std::min(E, (b - 1) * S - P + F);
 }
 
-int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool partition, Group* out) {
+// Boundaries b[0..N] of N parts of [0, E): 0 = b[0] < ... < b[N] = E.
+bool bounds_valid(const int32_t* b, int N, int E) {
+  if (b[0] != 0 || b[N] != E) return false;
+  for (int i = 0; i < N; ++i)
+    if (b[i + 1] <= b[i]) return false;
+  return true;
+}
+
+// rb / cb: the group output's row / column boundaries (rows + 1 / cols + 1
+// values), or NULL for the even floor split.
+int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool partition,
+                const int32_t* rb, const int32_t* cb, Group* out) {
   Group G;
   G.partition = partition;
   G.l0 = g0; G.l1 = g1; G.rows = rows; G.cols = cols; G.ntiles = rows * cols;
@@ -60,14 +73,19 @@ int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool parti
               " does not fit the group output " + std::to_string(dl[3]) + "x" + std::to_string(dl[4]));
     return MAFAT_ESHAPE;
   }
+  if ((rb && !bounds_valid(rb, rows, dl[3])) || (cb && !bounds_valid(cb, cols, dl[4]))) {
+    set_error("tile boundaries of a group must rise strictly from 0 to its output extent (" +
+              std::to_string(dl[3]) + " rows, " + std::to_string(dl[4]) + " columns)");
+    return MAFAT_ESHAPE;
+  }
   G.in_r.resize(static_cast<size_t>(G.ntiles) * nl);
   G.out_r.resize(static_cast<size_t>(G.ntiles) * nl);
   for (int i = 0; i < rows; ++i)
     for (int j = 0; j < cols; ++j) {
       const int t = i * cols + j;
       mafat_rect o;
-      split(dl[3], rows, i, &o.y0, &o.y1);
-      split(dl[4], cols, j, &o.x0, &o.x1);
+      if (rb) { o.y0 = rb[i]; o.y1 = rb[i + 1]; } else split(dl[3], rows, i, &o.y0, &o.y1);
+      if (cb) { o.x0 = cb[j]; o.x1 = cb[j + 1]; } else split(dl[4], cols, j, &o.x0, &o.x1);
       for (int l = g1; l >= g0; --l) {
         const mafat_layer& L = plan.layers[l];
         const auto& d = plan.dims[l];
@@ -246,12 +264,25 @@ extern "C" int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_laye
                                        int32_t in_w, int32_t in_c, const int32_t* group_start,
                                        int32_t n_groups, const int32_t* grid_rows,
                                        const int32_t* grid_cols, int32_t flags, mafat_plan** out) {
+  return mafat_plan_create_bounds(layers, n_layers, in_h, in_w, in_c, group_start, n_groups, grid_rows,
+                                  grid_cols, nullptr, nullptr, flags, out);
+}
+
+extern "C" int mafat_plan_create_bounds(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
+                                        int32_t in_w, int32_t in_c, const int32_t* group_start,
+                                        int32_t n_groups, const int32_t* grid_rows,
+                                        const int32_t* grid_cols, const int32_t* row_bounds,
+                                        const int32_t* col_bounds, int32_t flags, mafat_plan** out) {
   clear_error();
   if (!out) { set_error("out is NULL"); return MAFAT_EINVAL; }
   *out = nullptr;
   if (flags & ~(MAFAT_PLAN_STAGE_PARTITION | MAFAT_PLAN_PACKED_WEIGHTS)) {
     set_error("unknown plan flags");
     return MAFAT_EINVAL;
+  }
+  if ((flags & MAFAT_PLAN_STAGE_PARTITION) && (row_bounds || col_bounds)) {
+    set_error("the stage partition splits every stage evenly: no tile boundaries with it");
+    return MAFAT_EUNSUPPORTED;
   }
   if (!layers || !group_start || !grid_rows || !grid_cols || n_layers < 1 || n_groups < 1) {
     set_error("null pointer or empty layer/group list");
@@ -292,6 +323,7 @@ extern "C" int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_laye
       delete plan;
       return MAFAT_ESHAPE;
     }
+    const int32_t *rb = row_bounds, *cb = col_bounds;
     for (int g = 0; g < n_groups; ++g) {
       const int g0 = group_start[g];
       const int end = (g + 1 < n_groups) ? group_start[g + 1] : n_layers;
@@ -302,8 +334,10 @@ extern "C" int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_laye
       }
       Group G;
       const int rc = build_group(*plan, g0, end - 1, grid_rows[g], grid_cols[g],
-                                 (flags & MAFAT_PLAN_STAGE_PARTITION) != 0, &G);
+                                 (flags & MAFAT_PLAN_STAGE_PARTITION) != 0, rb, cb, &G);
       if (rc != MAFAT_OK) { delete plan; return rc; }
+      if (rb) rb += grid_rows[g] + 1;
+      if (cb) cb += grid_cols[g] + 1;
       plan->groups.push_back(std::move(G));
     }
   } catch (const std::bad_alloc&) {
@@ -313,6 +347,168 @@ extern "C" int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_laye
   }
   *out = plan;
   return MAFAT_OK;
+}
+
+namespace mafat {
+namespace {
+
+// Balanced boundaries of N parts along one axis (0: rows, 1: columns) of
+// the output of layers [g0, g1] (variable tiling).  A part's task extent is
+// the extent of the input region of layer g0 that its output interval
+// reads; the result minimises the largest task extent, then the sum of the
+// squared task extents, and is the first such boundary list in
+// lexicographic order.
+//
+// Back-projection maps an interval's start and end independently, so the
+// task extent of [a, b) is END[b] - START[a], non-increasing in a and
+// non-decreasing in b.  Hence (1) the smallest feasible largest extent T is
+// found by bisection, a T being feasible when the greedy left-to-right
+// cover (each part as long as T allows) needs at most N parts -- any cover
+// with fewer parts refines into exactly N, sub-intervals never costing more;
+// (2) boundary k of any cover with extents <= T lies in a window: at most the
+// greedy reach of k parts from the left, at least the greedy reach of N - k
+// parts from the right; a dynamic programme over the windows minimises the
+// sum of squares, and the reconstruction takes the smallest boundary at each
+// step.
+int balanced_axis(const mafat_plan& P, int g0, int g1, int axis, int N, int32_t* out) {
+  const int E = P.dims[g1][3 + axis];
+  if (N < 1 || N > E) {
+    set_error("parts " + std::to_string(N) + " outside 1.." + std::to_string(E));
+    return MAFAT_ESHAPE;
+  }
+  std::vector<int64_t> st(static_cast<size_t>(E) + 1), en(static_cast<size_t>(E) + 1);
+  for (int v = 0; v <= E; ++v) {
+    int64_t a = v, b = v;
+    for (int l = g1; l >= g0; --l) {
+      const mafat_layer& L = P.layers[l];
+      const int64_t Ein = P.dims[l][axis];
+      a = std::max<int64_t>(0, a * L.s - L.p);
+      b = std::min<int64_t>(Ein, (b - 1) * L.s - L.p + L.f);
+    }
+    st[v] = a;
+    en[v] = b;
+  }
+  auto cost = [&](int a, int b) { return en[b] - st[a]; };
+  // Greedy reach from the left after k parts (capped at E) and from the
+  // right after j parts, for a bound T; -1 / E + 1 when a part cannot
+  // advance.
+  auto reach_left = [&](int64_t T, std::vector<int>* r) {
+    r->assign(static_cast<size_t>(N) + 1, E);
+    int pos = 0, b = 1;
+    (*r)[0] = 0;
+    for (int k = 1; k <= N; ++k) {
+      if (pos >= E) { (*r)[k] = E; continue; }
+      if (b <= pos) b = pos + 1;
+      if (cost(pos, b) > T) { for (int j = k; j <= N; ++j) (*r)[j] = -1; return; }
+      while (b < E && cost(pos, b + 1) <= T) ++b;
+      pos = b;
+      (*r)[k] = pos;
+    }
+  };
+  auto reach_right = [&](int64_t T, std::vector<int>* q) {
+    q->assign(static_cast<size_t>(N) + 1, 0);
+    int pos = E, a = E - 1;
+    (*q)[0] = E;
+    for (int j = 1; j <= N; ++j) {
+      if (pos <= 0) { (*q)[j] = 0; continue; }
+      if (a >= pos) a = pos - 1;
+      if (cost(a, pos) > T) { for (int i = j; i <= N; ++i) (*q)[i] = E + 1; return; }
+      while (a > 0 && cost(a - 1, pos) <= T) --a;
+      pos = a;
+      (*q)[j] = pos;
+    }
+  };
+  std::vector<int> r, q;
+  int64_t lo = 1, hi = cost(0, E);
+  while (lo < hi) {
+    const int64_t mid = lo + (hi - lo) / 2;
+    reach_left(mid, &r);
+    if (r[N] == E) hi = mid; else lo = mid + 1;
+  }
+  const int64_t T = lo;
+  reach_left(T, &r);
+  reach_right(T, &q);
+  std::vector<int> wlo(static_cast<size_t>(N) + 1), whi(static_cast<size_t>(N) + 1);
+  double work = 0;
+  for (int k = 0; k <= N; ++k) {
+    wlo[k] = std::max(k, q[N - k]);
+    whi[k] = std::min(r[k], E - (N - k));
+    if (wlo[k] > whi[k]) {
+      set_error("internal: empty boundary window");
+      return MAFAT_EINVAL;
+    }
+    if (k > 0) work += static_cast<double>(whi[k] - wlo[k] + 1) * (whi[k - 1] - wlo[k - 1] + 1);
+  }
+  if (work > 4.0e9) {
+    set_error("balanced boundaries: search too large");
+    return MAFAT_EUNSUPPORTED;
+  }
+  // s[k][b - wlo[k]]: least sum of squares covering [b, E) with N - k parts.
+  constexpr int64_t INF = INT64_MAX;
+  std::vector<std::vector<int64_t>> sfx(static_cast<size_t>(N) + 1);
+  for (int k = N; k >= 0; --k) {
+    sfx[k].assign(static_cast<size_t>(whi[k] - wlo[k] + 1), INF);
+    for (int b = wlo[k]; b <= whi[k]; ++b) {
+      if (k == N) { sfx[k][b - wlo[k]] = (b == E) ? 0 : INF; continue; }
+      int64_t best = INF;
+      for (int c = std::max(b + 1, wlo[k + 1]); c <= whi[k + 1]; ++c) {
+        const int64_t t = cost(b, c);
+        if (t > T) break;  // non-decreasing in c
+        const int64_t rest = sfx[k + 1][c - wlo[k + 1]];
+        if (rest != INF) best = std::min(best, t * t + rest);
+      }
+      sfx[k][b - wlo[k]] = best;
+    }
+  }
+  if (sfx[0][0] == INF) {
+    set_error("internal: no balanced cover");
+    return MAFAT_EINVAL;
+  }
+  out[0] = 0;
+  for (int k = 1; k <= N; ++k) {
+    const int b = out[k - 1];
+    const int64_t need = sfx[k - 1][b - wlo[k - 1]];
+    int pick = -1;
+    for (int c = std::max(b + 1, wlo[k]); c <= whi[k]; ++c) {
+      const int64_t t = cost(b, c);
+      if (t > T) break;
+      const int64_t rest = sfx[k][c - wlo[k]];
+      if (rest != INF && t * t + rest == need) { pick = c; break; }
+    }
+    if (pick < 0) {
+      set_error("internal: balanced reconstruction failed");
+      return MAFAT_EINVAL;
+    }
+    out[k] = pick;
+  }
+  return MAFAT_OK;
+}
+
+}  // namespace
+}  // namespace mafat
+
+extern "C" int mafat_balanced_bounds(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
+                                     int32_t in_w, int32_t in_c, int32_t first_layer,
+                                     int32_t last_layer, int32_t rows, int32_t cols,
+                                     int32_t* row_bounds, int32_t* col_bounds) {
+  clear_error();
+  if (!layers || n_layers < 1 || first_layer < 0 || last_layer < first_layer || last_layer >= n_layers) {
+    set_error("null layer list or layer range outside the stack");
+    return MAFAT_EINVAL;
+  }
+  const int32_t start = 0, one = 1;
+  mafat_plan* plan = nullptr;
+  int rc = mafat_plan_create(layers, n_layers, in_h, in_w, in_c, &start, 1, &one, &one, &plan);
+  if (rc != MAFAT_OK) return rc;  // shape inference errors, with their message
+  try {
+    if (row_bounds) rc = balanced_axis(*plan, first_layer, last_layer, 0, rows, row_bounds);
+    if (rc == MAFAT_OK && col_bounds) rc = balanced_axis(*plan, first_layer, last_layer, 1, cols, col_bounds);
+  } catch (const std::bad_alloc&) {
+    set_error("host allocation failed");
+    rc = MAFAT_ENOMEM;
+  }
+  mafat_plan_destroy(plan);
+  return rc;
 }
 
 extern "C" void mafat_plan_destroy(mafat_plan* plan) { delete plan; }

@@ -124,11 +124,16 @@ extern "C" int mafat_predict_mem(const mafat_plan* plan, int32_t model, int32_t 
   return predict(plan, model, batch, dtype, bytes);
 }
 
-extern "C" int mafat_get_config(const mafat_layer* layers, int32_t n_layers, int32_t in_h, int32_t in_w,
-                                int32_t in_c, int32_t model, int32_t batch, int32_t dtype, int64_t bias_bytes,
-                                int64_t limit_bytes, const int32_t* cuts, int32_t n_cuts, const int32_t* grids,
-                                int32_t n_grids, int32_t second_grid, int32_t* out_cut, int32_t* out_grid1,
-                                int32_t* out_grid2, int64_t* out_pred, int32_t* out_fits) {
+namespace {
+
+// Algorithm 2 over the candidates; with `balanced` every candidate's groups
+// take their balanced tile boundaries (mafat_balanced_bounds) instead of the
+// even split.
+int get_config(const mafat_layer* layers, int32_t n_layers, int32_t in_h, int32_t in_w, int32_t in_c,
+               int32_t model, int32_t batch, int32_t dtype, int64_t bias_bytes, int64_t limit_bytes,
+               const int32_t* cuts, int32_t n_cuts, const int32_t* grids, int32_t n_grids, int32_t second_grid,
+               bool balanced, int32_t* out_cut, int32_t* out_grid1, int32_t* out_grid2, int64_t* out_pred,
+               int32_t* out_fits) {
   clear_error();
   if (!layers || !cuts || !grids || n_cuts < 1 || n_grids < 1 || second_grid < 1 || !out_cut || !out_grid1 ||
       !out_grid2) {
@@ -145,7 +150,25 @@ extern "C" int mafat_get_config(const mafat_layer* layers, int32_t n_layers, int
       const int32_t starts[2] = {0, cut};
       const int32_t rows[2] = {t, second_grid};
       mafat_plan* plan = nullptr;
-      int rc = mafat_plan_create(layers, n_layers, in_h, in_w, in_c, starts, split ? 2 : 1, rows, rows, &plan);
+      int rc = MAFAT_OK;
+      if (balanced) {
+        // boundaries of each group: rows, then columns (square grids)
+        std::vector<int32_t> rb, cb;
+        const int ng = split ? 2 : 1;
+        for (int g = 0; g < ng && rc == MAFAT_OK; ++g) {
+          const int g0 = starts[g], g1 = (g + 1 < ng ? starts[g + 1] : n_layers) - 1;
+          std::vector<int32_t> r(static_cast<size_t>(rows[g]) + 1), c(static_cast<size_t>(rows[g]) + 1);
+          rc = mafat_balanced_bounds(layers, n_layers, in_h, in_w, in_c, g0, g1, rows[g], rows[g], r.data(),
+                                     c.data());
+          rb.insert(rb.end(), r.begin(), r.end());
+          cb.insert(cb.end(), c.begin(), c.end());
+        }
+        if (rc == MAFAT_OK)
+          rc = mafat_plan_create_bounds(layers, n_layers, in_h, in_w, in_c, starts, ng, rows, rows, rb.data(),
+                                        cb.data(), 0, &plan);
+      } else {
+        rc = mafat_plan_create(layers, n_layers, in_h, in_w, in_c, starts, split ? 2 : 1, rows, rows, &plan);
+      }
       if (rc != MAFAT_OK) return rc;  // mafat_last_error() names the problem
       int64_t pred = 0;
       rc = mafat_predict_mem(plan, model, batch, dtype, &pred);
@@ -167,4 +190,31 @@ extern "C" int mafat_get_config(const mafat_layer* layers, int32_t n_layers, int
   if (out_pred) *out_pred = last_pred + bias_bytes;
   if (out_fits) *out_fits = 0;
   return MAFAT_OK;
+}
+
+}  // namespace
+
+extern "C" int mafat_get_config(const mafat_layer* layers, int32_t n_layers, int32_t in_h, int32_t in_w,
+                                int32_t in_c, int32_t model, int32_t batch, int32_t dtype, int64_t bias_bytes,
+                                int64_t limit_bytes, const int32_t* cuts, int32_t n_cuts, const int32_t* grids,
+                                int32_t n_grids, int32_t second_grid, int32_t* out_cut, int32_t* out_grid1,
+                                int32_t* out_grid2, int64_t* out_pred, int32_t* out_fits) {
+  return get_config(layers, n_layers, in_h, in_w, in_c, model, batch, dtype, bias_bytes, limit_bytes, cuts, n_cuts,
+                    grids, n_grids, second_grid, false, out_cut, out_grid1, out_grid2, out_pred, out_fits);
+}
+
+extern "C" int mafat_get_config_balanced(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
+                                         int32_t in_w, int32_t in_c, int32_t model, int32_t batch,
+                                         int32_t dtype, int64_t bias_bytes, int64_t limit_bytes,
+                                         const int32_t* cuts, int32_t n_cuts, const int32_t* grids,
+                                         int32_t n_grids, int32_t second_grid, int32_t* out_cut,
+                                         int32_t* out_grid1, int32_t* out_grid2, int64_t* out_pred,
+                                         int32_t* out_fits) {
+  try {
+    return get_config(layers, n_layers, in_h, in_w, in_c, model, batch, dtype, bias_bytes, limit_bytes, cuts,
+                      n_cuts, grids, n_grids, second_grid, true, out_cut, out_grid1, out_grid2, out_pred, out_fits);
+  } catch (const std::bad_alloc&) {
+    set_error("host allocation failed");
+    return MAFAT_ENOMEM;
+  }
 }

@@ -33,13 +33,15 @@ MEM_MODELS = {"device": MAFAT_MEM_DEVICE, "paper": MAFAT_MEM_PAPER, "device_seq"
 DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
 
 # Every symbol include/mafat.h declares.
-EXPORTS = ("mafat_plan_create", "mafat_plan_create_flags", "mafat_plan_destroy",
+EXPORTS = ("mafat_plan_create", "mafat_plan_create_flags", "mafat_plan_create_bounds",
+           "mafat_balanced_bounds", "mafat_plan_destroy",
            "mafat_packed_weights_size", "mafat_pack_weights", "mafat_plan_layer_shape", "mafat_plan_group",
            "mafat_plan_num_tiles", "mafat_plan_regions", "mafat_plan_macs", "mafat_plan_stages", "mafat_plan_stage_layers",
            "mafat_plan_stage_fused", "mafat_plan_stage_kernel", "mafat_plan_set_tile_batch",
            "mafat_workspace_size", "mafat_run_group", "mafat_run_group_timed", "mafat_run_stage", "mafat_run_network",
            "mafat_run_network_static",
-           "mafat_predict_mem", "mafat_get_config", "mafat_status_string", "mafat_last_error")
+           "mafat_predict_mem", "mafat_get_config", "mafat_get_config_balanced", "mafat_status_string",
+           "mafat_last_error")
 
 
 class mafat_layer(ctypes.Structure):
@@ -78,6 +80,10 @@ def lib():
                                         i32p, i32p, ctypes.POINTER(planp)]
         L.mafat_plan_create_flags.argtypes = [ctypes.POINTER(mafat_layer), i32, i32, i32, i32, i32p, i32,
                                               i32p, i32p, i32, ctypes.POINTER(planp)]
+        L.mafat_plan_create_bounds.argtypes = [ctypes.POINTER(mafat_layer), i32, i32, i32, i32, i32p, i32,
+                                               i32p, i32p, i32p, i32p, i32, ctypes.POINTER(planp)]
+        L.mafat_balanced_bounds.argtypes = [ctypes.POINTER(mafat_layer), i32, i32, i32, i32, i32, i32, i32, i32,
+                                            i32p, i32p]
         L.mafat_plan_destroy.argtypes = [planp]
         L.mafat_packed_weights_size.argtypes = [planp, i32, i32, ctypes.POINTER(sz)]
         L.mafat_pack_weights.argtypes = [planp, i32, i32, vp, vp, vp]
@@ -103,6 +109,7 @@ def lib():
         L.mafat_predict_mem.argtypes = [planp, i32, i32, i32, i64p]
         L.mafat_get_config.argtypes = [ctypes.POINTER(mafat_layer), i32, i32, i32, i32, i32, i32, i32, i64, i64,
                                        i32p, i32, i32p, i32, i32, i32p, i32p, i32p, i64p, i32p]
+        L.mafat_get_config_balanced.argtypes = L.mafat_get_config.argtypes
         L.mafat_status_string.argtypes = [ctypes.c_int]
         L.mafat_status_string.restype = ctypes.c_char_p
         L.mafat_last_error.argtypes = []
@@ -129,21 +136,41 @@ def _ptrs(vals):
 
 # ------------------------------------------------------------------ C names
 
-def mafat_plan_create(layers, in_h, in_w, in_c, group_start, grid_rows, grid_cols, flags=0):
-    """Returns a plan handle (int); raises MafatError with the library's status.
-    flags: 0, or MAFAT_PLAN_STAGE_PARTITION and/or MAFAT_PLAN_PACKED_WEIGHTS
-    (mafat_plan_create_flags)."""
-    n = len(layers)
-    arr = (mafat_layer * n)()
+def _layer_array(layers):
+    arr = (mafat_layer * len(layers))()
     for k, L in enumerate(layers):
         op = MAFAT_CONV if L["op"] == W.CONV else MAFAT_MAXPOOL
         act = MAFAT_ACT_LEAKY01 if L.get("act") == W.LEAKY else MAFAT_ACT_LINEAR
         arr[k] = mafat_layer(op, int(L.get("c_out", 0)), int(L["f"]), int(L["s"]), int(L["p"]), act)
+    return arr
+
+
+def _flat_bounds(bounds):
+    """Per-group boundary lists -> one concatenated int32 array (None -> NULL)."""
+    if bounds is None:
+        return None
+    flat = [int(v) for b in bounds for v in b]
+    return (ctypes.c_int32 * len(flat))(*flat)
+
+
+def mafat_plan_create(layers, in_h, in_w, in_c, group_start, grid_rows, grid_cols, flags=0,
+                      row_bounds=None, col_bounds=None):
+    """Returns a plan handle (int); raises MafatError with the library's status.
+    flags: 0, or MAFAT_PLAN_STAGE_PARTITION and/or MAFAT_PLAN_PACKED_WEIGHTS
+    (mafat_plan_create_flags).  row_bounds / col_bounds: per-group lists of
+    rows+1 / cols+1 tile boundaries (mafat_plan_create_bounds), or None."""
+    n = len(layers)
+    arr = _layer_array(layers)
     gs = (ctypes.c_int32 * len(group_start))(*group_start)
     rr = (ctypes.c_int32 * len(grid_rows))(*grid_rows)
     cc = (ctypes.c_int32 * len(grid_cols))(*grid_cols)
     h = ctypes.c_void_p()
-    if flags:
+    if row_bounds is not None or col_bounds is not None:
+        _check("mafat_plan_create_bounds",
+               lib().mafat_plan_create_bounds(arr, n, in_h, in_w, in_c, gs, len(group_start), rr, cc,
+                                              _flat_bounds(row_bounds), _flat_bounds(col_bounds), flags,
+                                              ctypes.byref(h)))
+    elif flags:
         _check("mafat_plan_create_flags",
                lib().mafat_plan_create_flags(arr, n, in_h, in_w, in_c, gs, len(group_start), rr, cc, flags,
                                              ctypes.byref(h)))
@@ -151,6 +178,17 @@ def mafat_plan_create(layers, in_h, in_w, in_c, group_start, grid_rows, grid_col
         _check("mafat_plan_create",
                lib().mafat_plan_create(arr, n, in_h, in_w, in_c, gs, len(group_start), rr, cc, ctypes.byref(h)))
     return h.value
+
+
+def mafat_balanced_bounds(layers, in_h, in_w, in_c, first_layer, last_layer, rows, cols):
+    """(row_bounds, col_bounds): balanced tile boundaries of the group
+    [first_layer, last_layer] (lists of rows+1 and cols+1 ints)."""
+    rb = (ctypes.c_int32 * (rows + 1))()
+    cb = (ctypes.c_int32 * (cols + 1))()
+    _check("mafat_balanced_bounds",
+           lib().mafat_balanced_bounds(_layer_array(layers), len(layers), in_h, in_w, in_c, first_layer,
+                                       last_layer, rows, cols, rb, cb))
+    return list(rb), list(cb)
 
 
 def mafat_plan_destroy(plan):
@@ -302,18 +340,21 @@ def mafat_predict_mem(plan, model, batch, dtype):
 
 
 def mafat_get_config(layers, in_hwc, limit_bytes, model="paper", batch=1, dtype="f32", bias_bytes=0,
-                     cuts=(16, 12, 8), grids=(1, 2, 3, 4, 5), second_grid=2):
-    """Algorithm 2.  Returns (tiling spec in the paper's notation, prediction + bias, fits)."""
+                     cuts=(16, 12, 8), grids=(1, 2, 3, 4, 5), second_grid=2, balanced=False):
+    """Algorithm 2 (balanced=True: mafat_get_config_balanced, every
+    candidate with balanced tile boundaries).  Returns (tiling spec in the
+    paper's notation, prediction + bias, fits)."""
     h, w, c = in_hwc
     cc = (ctypes.c_int32 * len(cuts))(*cuts)
     gg = (ctypes.c_int32 * len(grids))(*grids)
     oc, o1, o2, fits = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     pred = ctypes.c_int64()
-    _check("mafat_get_config",
-           lib().mafat_get_config(_layer_array(layers), len(layers), h, w, c, MEM_MODELS.get(model, model), batch,
-                                  DTYPES.get(dtype, dtype), int(bias_bytes), int(limit_bytes), cc, len(cuts), gg,
-                                  len(grids), second_grid, ctypes.byref(oc), ctypes.byref(o1), ctypes.byref(o2),
-                                  ctypes.byref(pred), ctypes.byref(fits)))
+    name = "mafat_get_config_balanced" if balanced else "mafat_get_config"
+    _check(name,
+           getattr(lib(), name)(_layer_array(layers), len(layers), h, w, c, MEM_MODELS.get(model, model), batch,
+                                DTYPES.get(dtype, dtype), int(bias_bytes), int(limit_bytes), cc, len(cuts), gg,
+                                len(grids), second_grid, ctypes.byref(oc), ctypes.byref(o1), ctypes.byref(o2),
+                                ctypes.byref(pred), ctypes.byref(fits)))
     if oc.value >= len(layers):
         spec = f"{o1.value}x{o1.value}/NoCut"
     else:
@@ -328,7 +369,10 @@ class Plan:
     ``"5x5/8/2x2"`` (section 5.1 notation) or explicit group lists."""
 
     def __init__(self, layers, in_hwc, tiling="1x1/NoCut", stage_partition=False, packed_weights=False,
-                 tile_batch=0):
+                 tile_batch=0, bounds=None):
+        """bounds: None (even tile boundaries), "balanced" (each group's
+        mafat_balanced_bounds) or a pair (row_bounds, col_bounds) of
+        per-group boundary lists (mafat_plan_create_bounds)."""
         self.layers = list(layers)
         self.stage_partition = bool(stage_partition)
         self.packed_weights = bool(packed_weights)
@@ -336,10 +380,21 @@ class Plan:
         self.h, self.w, self.c = in_hwc
         self.group_start, self.rows, self.cols = W.parse_tiling(tiling, len(layers)) \
             if isinstance(tiling, str) else tiling
+        if isinstance(bounds, str):
+            if bounds != "balanced":
+                raise ValueError(f"bounds: None, 'balanced' or (row_bounds, col_bounds), not {bounds!r}")
+            per = [mafat_balanced_bounds(self.layers, self.h, self.w, self.c, g0,
+                                         (self.group_start[g + 1] if g + 1 < len(self.group_start)
+                                          else len(self.layers)) - 1, self.rows[g], self.cols[g])
+                   for g, g0 in enumerate(self.group_start)]
+            bounds = ([p[0] for p in per], [p[1] for p in per])
+        self.bounds = bounds
+        rb, cb = bounds if bounds is not None else (None, None)
         self.handle = mafat_plan_create(self.layers, self.h, self.w, self.c, self.group_start,
                                         self.rows, self.cols,
                                         (MAFAT_PLAN_STAGE_PARTITION if self.stage_partition else 0) |
-                                        (MAFAT_PLAN_PACKED_WEIGHTS if self.packed_weights else 0))
+                                        (MAFAT_PLAN_PACKED_WEIGHTS if self.packed_weights else 0),
+                                        row_bounds=rb, col_bounds=cb)
         self.n_groups = len(self.group_start)
         if self.tile_batch:
             mafat_plan_set_tile_batch(self.handle, self.tile_batch)

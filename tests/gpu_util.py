@@ -12,12 +12,14 @@ def require_gpu():
         pytest.skip("no GPU")
 
 
-def run_gpu(layers, h, w, c, params, tiling, batch, dtype, x=None, want_cuts=True, sentinel=True, part=False):
+def run_gpu(layers, h, w, c, params, tiling, batch, dtype, x=None, want_cuts=True, sentinel=True, part=False,
+            bounds=None):
     """Runs the library (mafat_run_network) and returns float64 numpy output
-    (and the cut tensors)."""
+    (and the cut tensors).  bounds: tile boundaries of the plan (Plan's
+    `bounds`: None, "balanced" or per-group lists)."""
     import torch
     from paper_2107_06960_amd import mafat as M
-    plan = M.Plan(layers, (h, w, c), tiling, stage_partition=part)
+    plan = M.Plan(layers, (h, w, c), tiling, stage_partition=part, bounds=bounds)
     net = M.Network(plan, params, batch, dtype)
     xt = net.input_tensor(params["x"] if x is None else x)
     if sentinel:

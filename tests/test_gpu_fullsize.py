@@ -102,6 +102,10 @@ def test_fullsize_whole_tensors(orc, name):
     got = {c: net.cuts[k].float().cpu().numpy().astype(np.float64)[frames] for k, c in enumerate(cuts)}
     got[len(wl.layers)] = net.y.float().cpu().numpy().astype(np.float64)[frames]
     del net, x
+    _check_against_oracle(orc, name, wl, p, frames, cuts, got)
+
+
+def _check_against_oracle(orc, name, wl, p, frames, cuts, got):
     ref = _reference(orc, wl, p, frames, cuts, False)
     emu = _reference(orc, wl, p, frames, cuts, True) if wl.dtype == "bf16" else None
     for b, g in got.items():
@@ -121,6 +125,36 @@ def test_fullsize_whole_tensors(orc, name):
         print(msg, flush=True)
         assert nerr <= TOL[wl.dtype], (name, b, nerr)
         assert eerr <= ELEM_TOL[wl.dtype], (name, b, eerr)
+
+
+@pytest.mark.gpu
+def test_fullsize_balanced_bounds(orc):
+    # the benchmark workload with variable tiling (each group's balanced
+    # boundaries, mafat_balanced_bounds), in the benchmark's launch
+    # configuration otherwise; the same whole-tensor checks (fused tile
+    # partitioning is exact for any partition, so the untiled oracle is the
+    # reference; it is shared with the test above when both run)
+    require_gpu()
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    name = "yolo608_5x5_8_2x2"
+    wl = W.WORKLOADS[name]
+    p = W.workload_inputs(wl)
+    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, packed_weights=True, bounds="balanced")
+    print(f"[fullsize] {name} balanced bounds rows {plan.bounds[0]} cols {plan.bounds[1]}", flush=True)
+    net = M.Network(plan, p, wl.batch, wl.dtype)
+    x = net.input_tensor(p["x"])
+    net.y.fill_(float("nan"))
+    for t in net.cuts:
+        t.fill_(float("nan"))
+    net.run(x)
+    torch.cuda.synchronize()
+    gs, _, _ = W.parse_tiling(wl.tiling, len(wl.layers))
+    cuts = gs[1:]
+    got = {c: net.cuts[k].float().cpu().numpy().astype(np.float64)[[0]] for k, c in enumerate(cuts)}
+    got[len(wl.layers)] = net.y.float().cpu().numpy().astype(np.float64)[[0]]
+    del net, x
+    _check_against_oracle(orc, name + " (balanced bounds)", wl, p, [0], cuts, got)
 
 
 @pytest.mark.gpu

@@ -8,6 +8,13 @@ forward bit for bit (fused tile partitioning is exact for any partition);
 the brute-force balanced boundaries against closed forms (stacks without a
 halo; YOLOv2's first group, whose task extents are derived by hand below)
 and against properties any optimum has.
+
+Library (CPU, through the C ABI): mafat_balanced_bounds equals the oracle's
+brute force; plans made with mafat_plan_create_bounds have the oracle's
+regions; the error codes.
+
+GPU: the library with balanced and with random boundaries against the
+oracle's tiled forward with the same boundaries, f32 and bf16.
 """
 import itertools
 
@@ -15,6 +22,8 @@ import numpy as np
 import pytest
 
 from paper_2107_06960_amd import workloads as W
+
+from gpu_util import TOL, normwise_err, require_gpu, run_gpu
 
 
 def _random_bounds(rng, E, N):
@@ -204,3 +213,170 @@ def test_balanced_properties_random(orc):
             tm = _task_extents(orc, sym, E, E, 2, 0, 3, 0, mir)
             assert (max(tb), sum(v * v for v in tb)) == (max(tm), sum(v * v for v in tm))
             assert bal <= mir   # the first in lexicographic order
+
+
+# ------------------------------------------------------------------ library (host)
+
+@pytest.fixture(scope="module")
+def M():
+    import os
+    from paper_2107_06960_amd import mafat
+    if not os.path.exists(mafat.LIB_PATH):
+        from paper_2107_06960_amd import build
+        build.build(verbose=False)
+    mafat.lib()
+    return mafat
+
+
+def test_library_balanced_bounds_match_oracle(M, orc):
+    for g0, g1 in ((0, 7), (0, 11), (0, 15), (8, 15), (12, 15)):
+        for N in (1, 2, 3, 4, 5):
+            rb, cb = M.mafat_balanced_bounds(W.YOLOV2_16, 608, 608, 3, g0, g1, N, N)
+            assert rb == list(orc.balanced_bounds(W.YOLOV2_16, 608, 608, 3, g0, g1, 0, N)), (g0, g1, N)
+            assert cb == list(orc.balanced_bounds(W.YOLOV2_16, 608, 608, 3, g0, g1, 1, N)), (g0, g1, N)
+    rng = np.random.default_rng(909)
+    done = 0
+    while done < 300:
+        layers, h, w, _, _, _, _, _ = _random_case(orc, rng, max_extent=40)
+        n = len(layers)
+        g0 = int(rng.integers(0, n))
+        dims = orc.shapes(layers, h, w, 2)
+        R = int(rng.integers(1, min(int(dims[-1, 3]), 5) + 1))
+        C = int(rng.integers(1, min(int(dims[-1, 4]), 5) + 1))
+        rb, cb = M.mafat_balanced_bounds(layers, h, w, 2, g0, n - 1, R, C)
+        assert rb == list(orc.balanced_bounds(layers, h, w, 2, g0, n - 1, 0, R)), (layers, h, w, g0, R)
+        assert cb == list(orc.balanced_bounds(layers, h, w, 2, g0, n - 1, 1, C)), (layers, h, w, g0, C)
+        done += 1
+
+
+def test_library_bounds_plan_regions_match_oracle(M, orc):
+    rng = np.random.default_rng(1010)
+    for _ in range(150):
+        layers, h, w, gs, rows, cols, rb, cb = _random_case(orc, rng, max_extent=40)
+        plan = M.Plan(layers, (h, w, 2), (gs, rows, cols), bounds=(rb, cb))
+        B = orc.regions_bruteforce(layers, h, w, 2, gs, rows, cols, rb, cb)
+        for g in range(len(gs)):
+            assert np.array_equal(plan.regions(g), B[g]), (layers, h, w, gs, rows, cols, rb, cb)
+    # only rows given: columns split evenly
+    gs, r, c = W.parse_tiling("5x5/8/2x2", 16)
+    rows_only = M.Plan(W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2", bounds=([[0, 16, 30, 45, 60, 76], [0, 19, 38]], None))
+    want = orc.regions(W.YOLOV2_16, 608, 608, 3, gs, r, c, [[0, 16, 30, 45, 60, 76], [0, 19, 38]], None)
+    for g in range(2):
+        assert np.array_equal(rows_only.regions(g), want[g])
+
+
+def test_library_balanced_plan(M, orc):
+    # Plan(bounds="balanced") takes each group's mafat_balanced_bounds; the
+    # largest tile input region is never larger than the even split's
+    for spec in ("3x3/NoCut", "5x5/8/2x2", "4x4/12/2x2", "3x3/8/2x2"):
+        even = M.Plan(W.YOLOV2_16, (608, 608, 3), spec)
+        bal = M.Plan(W.YOLOV2_16, (608, 608, 3), spec, bounds="balanced")
+        gs, r, c = W.parse_tiling(spec, 16)
+        for g in range(len(gs)):
+            g1 = (gs[g + 1] if g + 1 < len(gs) else 16) - 1
+            rb, cb = M.mafat_balanced_bounds(W.YOLOV2_16, 608, 608, 3, gs[g], g1, r[g], c[g])
+            assert bal.bounds[0][g] == rb and bal.bounds[1][g] == cb
+            Rb, Re = bal.regions(g), even.regions(g)
+            area = lambda R: (R[:, 0, 1] - R[:, 0, 0]) * (R[:, 0, 3] - R[:, 0, 2])
+            assert area(Rb).max() <= area(Re).max(), spec
+
+
+def test_library_bounds_errors(M):
+    L = W.YOLOV2_16
+    gs, r, c = W.parse_tiling("3x3/8/2x2", 16)
+    bad_rows = (
+        [[0, 30, 30, 76], [0, 19, 38]],   # not strictly increasing
+        [[0, 30, 50, 75], [0, 19, 38]],   # does not end at the extent
+        [[1, 30, 50, 76], [0, 19, 38]],   # does not start at 0
+    )
+    for rb in bad_rows:
+        with pytest.raises(M.MafatError) as e:
+            M.mafat_plan_create(L, 608, 608, 3, gs, r, c, 0, row_bounds=rb, col_bounds=None)
+        assert e.value.rc == M.MAFAT_ESHAPE
+    with pytest.raises(M.MafatError) as e:
+        M.mafat_plan_create(L, 608, 608, 3, gs, r, c, M.MAFAT_PLAN_STAGE_PARTITION,
+                            row_bounds=[[0, 26, 50, 76], [0, 19, 38]], col_bounds=None)
+    assert e.value.rc == M.MAFAT_EUNSUPPORTED
+    with pytest.raises(M.MafatError) as e:
+        M.mafat_balanced_bounds(L, 608, 608, 3, 0, 7, 77, 1)   # more parts than rows
+    assert e.value.rc == M.MAFAT_ESHAPE
+    with pytest.raises(M.MafatError) as e:
+        M.mafat_balanced_bounds(L, 608, 608, 3, 8, 7, 2, 2)    # empty layer range
+    assert e.value.rc == M.MAFAT_EINVAL
+    with pytest.raises(ValueError):
+        M.Plan(L, (608, 608, 3), "3x3/8/2x2", bounds="uneven")
+
+
+# ------------------------------------------------------------------ GPU parity
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("kind", ["balanced", "random"])
+def test_gpu_variable_tiling_parity(orc, dtype, kind):
+    require_gpu()
+    rng = np.random.default_rng(1111)
+    h = w = 160
+    layers = W.YOLOV2_16
+    spec = "5x5/8/3x3"
+    gs, r, c = W.parse_tiling(spec, 16)
+    if kind == "balanced":
+        bounds = "balanced"
+    else:
+        dims = orc.shapes(layers, h, w, 3)
+        rb, cb = [], []
+        for g in range(len(gs)):
+            last = (gs[g + 1] if g + 1 < len(gs) else 16) - 1
+            rb.append(_random_bounds(rng, int(dims[last, 3]), r[g]))
+            cb.append(_random_bounds(rng, int(dims[last, 4]), c[g]))
+        bounds = (rb, cb)
+    print(f"[variable tiling] {h}x{w}x3 {spec} {kind} {dtype}", flush=True)
+    p = W.make_inputs(layers, h, w, 3, 2, seed=31, dtype=dtype)
+    out, cuts, net, _ = run_gpu(layers, h, w, 3, p, spec, 2, dtype, bounds=bounds)
+    rb, cb = net.plan.bounds
+    print(f"[variable tiling] row bounds {rb} col bounds {cb}", flush=True)
+    ref, rcuts = orc.forward_tiled(layers, h, w, 3, p["x"], p, gs, r, c, want_cuts=True,
+                                   row_bounds=rb, col_bounds=cb)
+    assert not np.isnan(out).any()
+    err = normwise_err(out, ref)
+    cerr = normwise_err(cuts[0], rcuts[0])
+    print(f"[variable tiling] normwise output {err:.3e} cut {cerr:.3e}", flush=True)
+    assert err <= TOL[dtype] and cerr <= TOL[dtype]
+
+
+# ------------------------------------------------------------------ predictor and search
+
+def test_paper_model_with_bounds_matches_oracle(M):
+    from oracle import predictor as P
+    rng = np.random.default_rng(1212)
+    for spec in ("3x3/NoCut", "5x5/NoCut", "4x4/12/2x2", "5x5/8/2x2"):
+        gs, r, c = W.parse_tiling(spec, 16)
+        bal = M.Plan(W.YOLOV2_16, (608, 608, 3), spec, bounds="balanced")
+        rb, cb = bal.bounds
+        assert bal.predict_mem("paper", 1, "f32") == 4 * P.predict_mem(W.YOLOV2_16, 608, 608, 3, gs, r, c, rb, cb)
+        heights = [bal.group_out_shape(g)[0] for g in range(len(gs))]
+        rrb = [_random_bounds(rng, e, k) for e, k in zip(heights, r)]
+        rnd = M.Plan(W.YOLOV2_16, (608, 608, 3), spec, bounds=(rrb, None))
+        assert rnd.predict_mem("paper", 1, "bf16") == \
+            2 * P.predict_mem(W.YOLOV2_16, 608, 608, 3, gs, r, c, rrb, None)
+
+
+@pytest.mark.parametrize("mb", [40, 45, 50, 55, 64])
+def test_balanced_search_matches_oracle(M, mb):
+    # Algorithm 2 with every candidate balanced (the paper's model, float32,
+    # bias 31 MiB, 608x608): the library's search equals the oracle's; at
+    # these limits the balanced search stops no later in Algorithm 2's order
+    # than the even one (its predictions are lower on the deep groups)
+    from oracle import predictor as P
+    MiB = 1 << 20
+    spec, pred, fits = M.mafat_get_config(W.YOLOV2_16, (608, 608, 3), mb * MiB, model="paper", dtype="f32",
+                                          bias_bytes=31 * MiB, balanced=True)
+    cut, t, g2, opred, ofits = P.get_config(W.YOLOV2_16, 608, 608, 3, mb * MiB, balanced_tiles=True)
+    ospec = f"{t}x{t}/NoCut" if cut == 16 else f"{t}x{t}/{cut}/{g2}x{g2}"
+    assert (ospec, opred, ofits) == (spec, pred, fits)
+    even, epred, efits = M.mafat_get_config(W.YOLOV2_16, (608, 608, 3), mb * MiB, model="paper", dtype="f32",
+                                            bias_bytes=31 * MiB)
+    print(f"{mb} MiB: even tiles {even} ({epred / MiB:.2f} MiB), balanced {spec} ({pred / MiB:.2f} MiB)")
+    assert fits or not efits
+    order = [f"{t}x{t}/NoCut" for t in range(1, 6)] + [f"{t}x{t}/{c}/2x2" for c in (12, 8) for t in range(1, 6)]
+    if fits and efits:
+        assert order.index(spec) <= order.index(even)
