@@ -4,7 +4,9 @@ leaky activations, 16-96 channels), random input extents, 1-3 groups with
 random grids, f32 or bf16, packed or KRSC weights, the stage partition,
 tile batches and batch 1-2 -- each run of the HIP library compared with the
 oracle's untiled forward (normwise, the tolerance of each dtype), with the
-output filled with NaN first so an element no kernel writes fails."""
+output filled with NaN first so an element no kernel writes fails.  A second
+set draws the same kind of configurations with variable tiling: random or
+balanced tile boundaries per group (without the stage partition)."""
 import numpy as np
 import pytest
 
@@ -15,9 +17,22 @@ from gpu_util import TOL, normwise_err, require_gpu
 pytestmark = pytest.mark.gpu
 
 
-def _case(seed, orc):
+def _bounds(brng, dims, ends, rows, cols):
+    """Random or balanced boundaries for every group (None: balanced)."""
+    if brng.random() < 0.3:
+        return None
+    rb, cb = [], []
+    for e, r, c in zip(ends, rows, cols):
+        for E, N, out in ((int(dims[e - 1, 3]), r, rb), (int(dims[e - 1, 4]), c, cb)):
+            inner = sorted(int(v) for v in brng.choice(np.arange(1, E), N - 1, replace=False)) if N > 1 else []
+            out.append([0] + inner + [E])
+    return rb, cb
+
+
+def _case(seed, orc, variable=False):
     from paper_2107_06960_amd import mafat as M
     rng = np.random.default_rng(1000 + seed)
+    brng = np.random.default_rng(5000 + seed)
     for _ in range(100):  # draw until the plan is valid
         c0 = int(rng.choice([3, 16, 32, 64]))
         layers = []
@@ -46,24 +61,28 @@ def _case(seed, orc):
         packed = bool(rng.random() < 0.5)
         tb = 0 if part else int(rng.choice([0, 0, 1, 3]))
         batch = int(rng.choice([1, 2]))
+        bounds = None
+        if variable:
+            if part:
+                continue
+            bounds = _bounds(brng, dims, ends, rows, cols) or "balanced"
         try:
             plan = M.Plan(layers, (h, w, c0), (starts, rows, cols), stage_partition=part, packed_weights=packed,
-                          tile_batch=tb)
+                          tile_batch=tb, bounds=bounds)
         except M.MafatError:
             continue
-        return plan, layers, (h, w, c0), dtype, batch, (starts, rows, cols, part, packed, tb)
+        return plan, layers, (h, w, c0), dtype, batch, (starts, rows, cols, part, packed, tb, plan.bounds)
     raise AssertionError("no valid configuration drawn")
 
 
-@pytest.mark.parametrize("seed", range(32))
-def test_random_configuration(orc, seed):
+def _run(orc, seed, variable):
     require_gpu()
     import torch
     from paper_2107_06960_amd import mafat as M
-    plan, layers, (h, w, c0), dtype, batch, desc = _case(seed, orc)
-    print(f"[random {seed}] {h}x{w}x{c0} {dtype} batch={batch} layers="
+    plan, layers, (h, w, c0), dtype, batch, desc = _case(seed, orc, variable)
+    print(f"[random {seed}{' variable tiling' if variable else ''}] {h}x{w}x{c0} {dtype} batch={batch} layers="
           f"{[(L['op'], L.get('c_out'), L['f'], L['s'], L['p']) for L in layers]} "
-          f"groups/rows/cols/partition/packed/tile_batch={desc}", flush=True)
+          f"groups/rows/cols/partition/packed/tile_batch/bounds={desc}", flush=True)
     p = W.make_inputs(layers, h, w, c0, batch, 2000 + seed, dtype)
     net = M.Network(plan, p, batch, dtype)
     x = net.input_tensor(p["x"])
@@ -74,3 +93,13 @@ def test_random_configuration(orc, seed):
     assert not np.isnan(out).any()
     err = normwise_err(out, ref)
     assert err <= TOL[dtype], (seed, err)
+
+
+@pytest.mark.parametrize("seed", range(32))
+def test_random_configuration(orc, seed):
+    _run(orc, seed, False)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_configuration_variable_tiling(orc, seed):
+    _run(orc, 100 + seed, True)
