@@ -320,8 +320,10 @@ def config_search(args):
     of its search space on this GPU, YOLOv2 layers 0-15 at 608x608, bf16,
     batch 1.  Candidates: the paper's cuts (16 = no cut, 12, 8) x first-group
     grids 1x1..5x5, second group 2x2, each run with every tile of a stage at
-    once (tile batch 'all') and with one tile at a time (tile batch 1, the
-    paper's execution order); every candidate is timed like the headline
+    once (tile batch 'all'), with one tile at a time (tile batch 1, the
+    paper's execution order) and, for grids of 3x3 and more, one grid row of
+    the first group at a time (tile batch t: a memory/time point between the
+    two); every candidate is timed like the headline
     (packed weights, warm-up, then host time over the steps) and its peak
     device memory measured (torch's requested bytes).  For each
     device-memory limit the search takes Algorithm 2 under the device model
@@ -340,7 +342,7 @@ def config_search(args):
     for cut in (16, 12, 8):
         for t in (1, 2, 3, 4, 5):
             spec = f"{t}x{t}/NoCut" if cut == 16 else f"{t}x{t}/{cut}/2x2"
-            for tb in (0, 1):
+            for tb in (0, 1) + ((t,) if t >= 3 else ()):
                 cands.append((spec, tb))
     meas = {}
     for spec, tb in cands:
@@ -356,7 +358,8 @@ def config_search(args):
         for _ in range(args.steps):
             net.run(x)
         torch.cuda.synchronize()
-        model = "device" if tb == 0 else "device_seq"
+        # the device model follows the plan's tile batch; device_seq is one tile at a time
+        model = "device_seq" if tb == 1 else "device"
         meas[(spec, tb)] = {"ms": (time.perf_counter() - t0) / args.steps * 1e3,
                             "peak_mib": peak / 2 ** 20,
                             "predicted_mib": plan.predict_mem(model, 1, "bf16") / 2 ** 20}
