@@ -455,6 +455,93 @@ def variable_tiling(args):
     print(json.dumps({"variable_tiling_search": rows}), flush=True)
 
 
+def phase_trace(args):
+    """Per-launch phase timing of the benchmark workload from the trace
+    build of the library (libmafat_trace.so: `python -m
+    paper_2107_06960_amd.build --trace`), which stamps the wall clock (100
+    MHz) at the start and end of every workgroup and at the phase
+    boundaries of the first, middle and last workgroup of each launch.
+    After warm-up steps, each group runs once with the stamps dumped.  One
+    JSON line per launch: the spread of workgroup starts, the span from the
+    first start to the last end, workgroup durations (p10/p50/p90/max), and
+    for the three stamped workgroups the decode, the phase marks (kernel
+    specific, in ns from the workgroup's start) and the end."""
+    import re
+    import tempfile
+    import torch
+    from paper_2107_06960_amd import build as B
+    from paper_2107_06960_amd import mafat as M
+    from paper_2107_06960_amd import workloads as W
+    if not os.path.exists(B.TRACE_LIB):
+        print(json.dumps({"error": f"{B.TRACE_LIB} is missing: python -m paper_2107_06960_amd.build --trace"}))
+        sys.exit(1)
+    M.LIB_PATH = B.TRACE_LIB
+    torch.cuda.set_device(0)
+    wl = W.WORKLOADS[args.workload]
+    params = W.workload_inputs(wl)
+    plan, net = bench_network(M, wl, params)
+    x = net.input_tensor(params["x"])
+    for _ in range(max(args.warmup, 5)):
+        net.run(x)
+    torch.cuda.synchronize()
+    # the runtime prints the stamps on the C stderr: send file descriptor 2
+    # to a file while the groups run
+    sys.stderr.flush()
+    saved = os.dup(2)
+    with tempfile.TemporaryFile(mode="w+") as tf:
+        os.dup2(tf.fileno(), 2)
+        try:
+            os.environ["MAFAT_WG_DUMP"] = "1"
+            os.environ["MAFAT_TRACE_DUMP"] = "1"
+            for g in range(plan.n_groups):
+                gin, gout = net.group_io(g, x)
+                net.run_group(g, gin, gout)
+                torch.cuda.synchronize()
+        finally:
+            os.environ.pop("MAFAT_WG_DUMP", None)
+            os.environ.pop("MAFAT_TRACE_DUMP", None)
+            os.dup2(saved, 2)
+            os.close(saved)
+        tf.seek(0)
+        text = tf.read()
+    launches, cur = [], None
+    for line in text.splitlines():
+        m = re.match(r"WGSPAN stage (\d+)-(\d+) kind (\d+) grid (\d+): span (\d+) ns, starts (\d+), first end (\d+), "
+                     r"dur p10 (\d+) p50 (\d+) p90 (\d+) max (\d+) ns", line)
+        if m:
+            v = [int(t) for t in m.groups()]
+            cur = {"first_stage_layers": [v[0], v[1]], "workgroups": v[3], "span_ns": v[4], "start_spread_ns": v[5],
+                   "first_end_ns": v[6], "wg_ns": {"p10": v[7], "p50": v[8], "p90": v[9], "max": v[10]},
+                   "stamped": []}
+            launches.append(cur)
+            continue
+        m = re.match(r"\s+wg(\d) decode \+(-?\d+) staged \+(-?\d+) loopend \+(-?\d+) end \+(-?\d+) iters:(.*)", line)
+        if m and cur is not None:
+            end = int(m.group(5))
+            marks = [int(t) for t in m.group(6).split()]
+            rec = {"decode_ns": int(m.group(2)), "loop_end_ns": int(m.group(4)), "end_ns": end,
+                   "chunk_marks_ns": [t for t in marks if 0 < t <= end]}
+            if 0 < int(m.group(3)) <= end:
+                rec["staged_ns"] = int(m.group(3))
+            cur["stamped"].append(rec)
+            continue
+        m = re.match(r"\s+wg(\d) slots 6-9: (-?\d+) (-?\d+) (-?\d+) (-?\d+)", line)
+        if m and cur is not None:
+            cur.setdefault("slots_6_9_ns", []).append([int(t) for t in m.groups()[1:]])
+    kernels = []  # (group, first stage) of every launch, in order
+    for g in range(plan.n_groups):
+        s, ns = 0, len(plan.stages(g))
+        while s < ns:
+            kernels.append((g, s))
+            s += 2 if plan.stage_fused(g, s, wl.batch, wl.dtype) else 1
+    for k, rec in enumerate(launches):
+        rec["workload"] = wl.name
+        if k < len(kernels):
+            g, s = kernels[k]
+            rec["kernel"] = plan.stage_kernel(g, s, wl.batch, wl.dtype)
+        print(json.dumps(rec), flush=True)
+
+
 def all_configs(args):
     """Every workload of the build (the paper's configurations and the six
     cut x grid runs), each with every tile at once, with the stage partition, and one
@@ -555,6 +642,8 @@ def main():
                     help="latency quantiles, throughput and peak memory of every workload (one JSON line each)")
     ap.add_argument("--config-search", action="store_true",
                     help="only evaluate the configuration search against a measured sweep and exit")
+    ap.add_argument("--phase-trace", action="store_true",
+                    help="only print per-launch phase timing from the trace build of the library and exit")
     ap.add_argument("--variable-tiling", action="store_true",
                     help="only compare balanced (variable) tile boundaries with the even split and exit")
     ap.add_argument("--copy-calibration", type=int, metavar="MIB",
@@ -568,6 +657,9 @@ def main():
         return
     if args.variable_tiling:
         variable_tiling(args)
+        return
+    if args.phase_trace:
+        phase_trace(args)
         return
     if args.all_configs:
         all_configs(args)

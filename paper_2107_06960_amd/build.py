@@ -1,10 +1,14 @@
 """Builds libmafat.so (the HIP library) in-tree for gfx950.
 
-    python -m paper_2107_06960_amd.build
+    python -m paper_2107_06960_amd.build            # libmafat.so
+    python -m paper_2107_06960_amd.build --trace    # libmafat_trace.so
 
 Every source under csrc/ is compiled with hipcc for gfx950 and linked into
 paper_2107_06960_amd/libmafat.so.  Packed fp32 instructions are disabled
-for all device code.
+for all device code.  The trace variant (MAFAT_TUNING) adds wall-clock
+stamps per workgroup and per kernel phase, printed by the runtime when
+MAFAT_WG_DUMP / MAFAT_TRACE_DUMP are set (bench.py --phase-trace); it is a
+measurement build, never the product library.
 """
 from __future__ import annotations
 
@@ -37,9 +41,12 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
           "-I", os.path.join(HERE, "..", "include")]
 
 
-def _compile(src):
-    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [hipcc()] + COMMON + ["-x", "hip", "-c", src, "-o", obj]
+TRACE_LIB = os.path.join(HERE, "libmafat_trace.so")
+
+
+def _compile(src, build_dir=BUILD, extra=()):
+    obj = os.path.join(build_dir, os.path.basename(src) + ".o")
+    cmd = [hipcc()] + COMMON + list(extra) + ["-x", "hip", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
@@ -47,24 +54,27 @@ def _compile(src):
     return obj, warn.strip()
 
 
-def build(verbose: bool = True) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose: bool = True, trace: bool = False) -> str:
+    build_dir = os.path.join(BUILD, "trace") if trace else BUILD
+    lib = TRACE_LIB if trace else LIB
+    extra = ("-DMAFAT_TUNING",) if trace else ()
+    os.makedirs(build_dir, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.cpp")) + glob.glob(os.path.join(CSRC, "*.hip")))
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        results = list(ex.map(_compile, srcs))
+        results = list(ex.map(lambda src: _compile(src, build_dir, extra), srcs))
     for obj, warn in results:
         if warn and verbose:
             print(warn, file=sys.stderr)
-    tmp = LIB + f".tmp{os.getpid()}"
+    tmp = lib + f".tmp{os.getpid()}"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + [o for o, _ in results]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
     if verbose:
-        print(f"built {LIB}")
-    return LIB
+        print(f"built {lib}")
+    return lib
 
 
 if __name__ == "__main__":
-    build()
+    build(trace="--trace" in sys.argv[1:])
