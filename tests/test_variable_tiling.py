@@ -380,3 +380,28 @@ def test_balanced_search_matches_oracle(M, mb):
     order = [f"{t}x{t}/NoCut" for t in range(1, 6)] + [f"{t}x{t}/{c}/2x2" for c in (12, 8) for t in range(1, 6)]
     if fits and efits:
         assert order.index(spec) <= order.index(even)
+
+
+def test_library_balanced_bounds_large_extents(M):
+    # the largest extents the plan takes: the windowed search stays exact
+    # (a halo-free stack: the most even split, shorter parts first) and quick
+    import time
+    t0 = time.perf_counter()
+    for E, N in ((32767, 64), (32767, 7), (32767, 1), (30000, 30000 // 2)):
+        rb, _ = M.mafat_balanced_bounds([W.conv(2, 1)], E, 2, 1, 0, 0, N, 1)
+        q, r = divmod(E, N)
+        assert [rb[i + 1] - rb[i] for i in range(N)] == [q] * (N - r) + [q + 1] * r
+    # a stack with halos at a large extent: never worse than the even split
+    layers = [W.conv(2, 3), W.maxpool(), W.conv(2, 5), W.conv(2, 3, s=2, p=1)]
+    h = 32000
+    plan = M.Plan(layers, (h, 8, 1), "1x1/NoCut")
+    E = plan.group_out_shape(0)[0]
+    rb, _ = M.mafat_balanced_bounds(layers, h, 8, 1, 0, 3, 17, 1)
+    even = [i * E // 17 for i in range(18)]
+
+    def largest_task(bounds):
+        R = M.Plan(layers, (h, 8, 1), ([0], [17], [1]), bounds=([bounds], None)).regions(0)
+        return int((R[:, 0, 1] - R[:, 0, 0]).max())
+
+    assert largest_task(rb) <= largest_task(even)
+    assert time.perf_counter() - t0 < 30
