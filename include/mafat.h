@@ -281,9 +281,9 @@ int mafat_plan_stage_layers(const mafat_plan* plan, int32_t group, int32_t stage
  * *fused = 1 if mafat_run_group / mafat_run_network run stage `stage` of
  * group g together with stage + 1 in one kernel for this batch and dtype,
  * else 0.  Two pairs qualify (bfloat16): a 3x3 convolution with 128
- * outputs and no pool whose next stage is a 1x1 convolution 128 -> 64 over
- * the same rectangles (YOLOv2's layers 4-5: the 1x1 GEMM runs on the 3x3
- * outputs held in LDS), and a group's first stage when it is a 3-channel
+ * outputs and no pool whose next stage is a 1x1 convolution 128 -> 64 or
+ * 128 -> 32 over the same rectangles (YOLOv2's layers 4-5: the 1x1 GEMM
+ * runs on the 3x3 outputs held in LDS), and a group's first stage when it is a 3-channel
  * 3x3 convolution with 32 outputs and a 2x2/2 pool followed by a 3x3
  * convolution 32 -> 64 with a 2x2/2 pool (YOLOv2's layers 0-3: each
  * workgroup computes the first layer's pooled output for its own input

@@ -40,10 +40,10 @@
 // block's outputs staged in LDS as rows of BN channels, then written as
 // 16-byte chunks (each output pixel's BN channels contiguous).
 //
-// Fused variant (template argument N2 > 0, BN = c_out = 128, no pool): the
-// staged block is the A operand of a following 1x1 convolution with N2
-// outputs, run from LDS in the same workgroup, so the 3x3 layer's output
-// never goes to memory; with two input chunks the second one's patch and
+// Fused variant (template argument N2 = 32 or 64, BN = c_out = 128, no
+// pool): the staged block is the A operand of a following 1x1 convolution
+// with N2 outputs, run from LDS in the same workgroup, so the 3x3 layer's
+// output never goes to memory; with two input chunks the second one's patch and
 // first taps load into a second LDS region while the first is computed.
 //
 // First-layer variant (template argument PRE, one input chunk of 32
@@ -844,10 +844,14 @@ hipError_t launch_patch_p(const MfmaShape& sh, const StageArgs& args, hipStream_
 
 hipError_t launch_conv_patch_fused(const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
   if (args.total_blocks <= 0) return hipSuccess;
-  if (args.cout != 128 || args.cout2 != 64) return hipErrorInvalidValue;
-  hipExtLaunchKernelGGL((conv_patch_kernel<8, 16, 128, 128, 4, 2, 1, false, 64>),
-                        dim3(static_cast<unsigned>(args.total_blocks)), dim3(512), 0, stream, ev.start, ev.stop, 0,
-                        args);
+  if (args.cout != 128 || (args.cout2 != 64 && args.cout2 != 32)) return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(args.total_blocks));
+  if (args.cout2 == 64)
+    hipExtLaunchKernelGGL((conv_patch_kernel<8, 16, 128, 128, 4, 2, 1, false, 64>), grid, dim3(512), 0, stream,
+                          ev.start, ev.stop, 0, args);
+  else
+    hipExtLaunchKernelGGL((conv_patch_kernel<8, 16, 128, 128, 4, 2, 1, false, 32>), grid, dim3(512), 0, stream,
+                          ev.start, ev.stop, 0, args);
   return hipGetLastError();
 }
 

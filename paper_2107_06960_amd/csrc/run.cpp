@@ -237,8 +237,8 @@ StageConfig choose_config(const Stage& S, int batch, int dtype) {
 namespace {
 
 // A bf16 3x3 stage with 128 outputs (c_in a multiple of 32, no pool)
-// followed by a 1x1 stage 128 -> 64 (no pool) that computes the same
-// rectangles (YOLOv2's layers 4 and 5): the pair runs as one kernel, the
+// followed by a 1x1 stage 128 -> 64 or 128 -> 32 (no pool) that computes the
+// same rectangles (YOLOv2's layers 4 and 5 are the first kind): the pair runs as one kernel, the
 // 1x1 GEMM taking the 3x3 block's outputs from LDS (one output pass and
 // one kernel boundary less).
 bool fused_pair(const mafat_plan& P, const Group& G, int s, int dtype) {
@@ -247,7 +247,7 @@ bool fused_pair(const mafat_plan& P, const Group& G, int s, int dtype) {
   const Stage& B = G.stages[s + 1];
   if (A.kind != STAGE_CONV || B.kind != STAGE_CONV) return false;
   if (!same_conv(A) || A.f != 3 || A.pool || A.cin % 32 != 0 || A.cout != 128) return false;
-  if (!same_conv(B) || B.f != 1 || B.pool || B.cin != 128 || B.cout != 64) return false;
+  if (!same_conv(B) || B.f != 1 || B.pool || B.cin != 128 || (B.cout != 64 && B.cout != 32)) return false;
   if (!mfma_ok(A, dtype) || A.tiles.size() != B.tiles.size()) return false;
   for (size_t t = 0; t < A.tiles.size(); ++t) {
     const TileGeom& a = A.tiles[t];

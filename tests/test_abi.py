@@ -197,10 +197,13 @@ def test_fused_pair_detection(lib):
     plan = M.Plan(W.YOLOV2_16, (608, 608, 3), "3x3/5/2x2")
     assert plan.stages(0)[-1] == (4, 4) and not plan.stage_fused(0, len(plan.stages(0)) - 1, 1, "bf16")
     # other channel counts, a pool after the 3x3, or a 3x3 second layer: no
-    for layers in ([W.conv(96), W.conv(64, 1)], [W.conv(128), W.conv(32, 1)],
+    for layers in ([W.conv(96), W.conv(64, 1)], [W.conv(128), W.conv(48, 1)], [W.conv(128), W.conv(128, 1)],
                    [W.conv(128), W.maxpool(), W.conv(64, 1)], [W.conv(128), W.conv(64)]):
         plan = M.Plan(layers, (32, 32, 64), "2x2/NoCut")
         assert not plan.stage_fused(0, 0, 1, "bf16"), layers
+    # the 1x1 may have 32 outputs as well
+    plan = M.Plan([W.conv(128), W.conv(32, 1)], (32, 32, 64), "2x2/NoCut")
+    assert plan.stage_fused(0, 0, 1, "bf16") and plan.stage_kernel(0, 0, 1, "bf16") == "patch_1x1"
     plan = M.Plan([W.conv(128), W.conv(64, 1, W.LINEAR)], (32, 32, 64), "2x2/NoCut")
     assert plan.stage_fused(0, 0, 1, "bf16") and not plan.stage_fused(0, 1, 1, "bf16")
     # the first-layer pair needs the group's first stage to be the 3-channel

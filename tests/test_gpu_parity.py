@@ -361,15 +361,17 @@ def test_packed_weights_parity(orc):
 FUSED_PAIR = [W.conv(128), W.conv(64, 1)]
 
 
-@pytest.mark.parametrize("part,packed,act2", [(False, False, W.LEAKY), (True, False, W.LEAKY),
-                                                (False, True, W.LINEAR), (True, True, W.LEAKY)])
-def test_fused_pair_parity(orc, part, packed, act2):
+@pytest.mark.parametrize("part,packed,act2,n2", [(False, False, W.LEAKY, 64), (True, False, W.LEAKY, 64),
+                                                   (False, True, W.LINEAR, 64), (True, True, W.LEAKY, 64),
+                                                   (False, True, W.LEAKY, 32), (True, False, W.LINEAR, 32)])
+def test_fused_pair_parity(orc, part, packed, act2, n2):
     # ragged extents (blocks of 16x16 past the tile edges), 2x3 tiles, batch 2
     from paper_2107_06960_amd import mafat as M
     import torch
-    layers = [W.conv(128), W.conv(64, 1, act2)]
+    layers = [W.conv(128), W.conv(n2, 1, act2)]
     h, w, c = 45, 61, 64
-    print(f"[parity] fused pair {h}x{w}x{c} stage_partition={part} packed={packed} act2={act2}", flush=True)
+    print(f"[parity] fused pair {h}x{w}x{c} 1x1 outputs {n2} stage_partition={part} packed={packed} act2={act2}",
+          flush=True)
     p = W.make_inputs(layers, h, w, c, 2, 21, "bf16")
     plan = M.Plan(layers, (h, w, c), "2x3/NoCut", stage_partition=part, packed_weights=packed)
     net = M.Network(plan, p, 2, "bf16")
@@ -389,6 +391,7 @@ FUSED_MID = [W.conv(64), W.conv(128), W.conv(64, 1), W.conv(32)]
 
 @pytest.mark.parametrize("layers,h,w,c,batch,tiling,part", [
     (FUSED_PAIR, 50, 39, 64, 1, "3x2/NoCut", False),
+    ([W.conv(128), W.conv(32, 1)], 50, 39, 32, 2, "2x2/NoCut", False),
     (FUSED_MID, 120, 136, 32, 6, "2x2/NoCut", False),
     (FUSED_MID, 120, 136, 32, 6, "2x2/NoCut", True),
 ])
