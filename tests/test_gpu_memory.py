@@ -79,3 +79,64 @@ def test_search_under_device_limit_runs_within_it(mib):
     used = torch.cuda.memory_stats()["requested_bytes.all.peak"] - base
     assert used == pred < (mib << 20)
     del net, x
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("mib", [11, 12])
+def test_balanced_search_under_device_limit_runs_within_it(mib):
+    # variable tiling: the search with balanced boundaries
+    # (mafat_get_config_balanced, the sequential device model) fits at
+    # 11 MiB, where no evenly tiled candidate does, and the plan it names,
+    # run one tile at a time with its balanced boundaries, holds exactly the
+    # predicted bytes
+    require_gpu()
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    spec, pred, fits = M.mafat_get_config(W.YOLOV2_16, (608, 608, 3), mib << 20, model="device_seq",
+                                          dtype="bf16", balanced=True)
+    _, _, even_fits = M.mafat_get_config(W.YOLOV2_16, (608, 608, 3), mib << 20, model="device_seq", dtype="bf16")
+    print(f"[memory] balanced search under {mib} MiB: {spec}, predicted {pred} B (even tiles fit: {even_fits})",
+          flush=True)
+    assert fits
+    if mib == 11:
+        assert not even_fits
+    wl = W.WORKLOADS["yolo608_5x5_8_2x2"]
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    base = torch.cuda.memory_stats().get("requested_bytes.all.current", 0)
+    p = W.workload_inputs(wl)
+    plan = M.Plan(W.YOLOV2_16, (608, 608, 3), spec, tile_batch=1, bounds="balanced")
+    net = M.Network(plan, p, 1, "bf16")
+    x = net.input_tensor(p["x"])
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    net.run(x)
+    torch.cuda.synchronize()
+    used = torch.cuda.memory_stats()["requested_bytes.all.peak"] - base
+    assert used == pred < (mib << 20)
+    del net, x
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("spec", ["3x3/NoCut", "5x5/12/2x2", "5x5/8/2x2"])
+@pytest.mark.parametrize("tile_batch", [0, 1])
+def test_device_model_matches_measured_peak_balanced(spec, tile_batch):
+    require_gpu()
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    wl = W.WORKLOADS["yolo608_5x5_8_2x2"]
+    print(f"[memory] balanced {spec} tile_batch={tile_batch}", flush=True)
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    base = torch.cuda.memory_stats().get("requested_bytes.all.current", 0)
+    p = W.workload_inputs(wl)
+    plan = M.Plan(W.YOLOV2_16, (608, 608, 3), spec, packed_weights=True, tile_batch=tile_batch, bounds="balanced")
+    net = M.Network(plan, p, 1, "bf16")
+    x = net.input_tensor(p["x"])
+    torch.cuda.synchronize()
+    torch.cuda.reset_peak_memory_stats()
+    net.run(x)
+    torch.cuda.synchronize()
+    used = torch.cuda.memory_stats()["requested_bytes.all.peak"] - base
+    assert used == plan.predict_mem("device", 1, "bf16")
+    del net, x
