@@ -322,15 +322,6 @@ def mafat_run_network_static(plan, batch, dtype, x, y, cut_bufs, w, scale, bias,
                                           _ptrs(bias), stream))
 
 
-def _layer_array(layers):
-    arr = (mafat_layer * len(layers))()
-    for k, L in enumerate(layers):
-        op = MAFAT_CONV if L["op"] == W.CONV else MAFAT_MAXPOOL
-        act = MAFAT_ACT_LEAKY01 if L.get("act") == W.LEAKY else MAFAT_ACT_LINEAR
-        arr[k] = mafat_layer(op, int(L.get("c_out", 0)), int(L["f"]), int(L["s"]), int(L["p"]), act)
-    return arr
-
-
 def mafat_predict_mem(plan, model, batch, dtype):
     """Predicted bytes (int) of a plan handle under model 'device' or 'paper'."""
     out = ctypes.c_int64()
