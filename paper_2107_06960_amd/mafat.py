@@ -515,3 +515,23 @@ class Network:
         gin = x if g == 0 else self.cuts[g - 1]
         gout = self.y if g == self.plan.n_groups - 1 else self.cuts[g]
         return gin, gout
+
+
+def run_network(plan, x, params, out=None, stream=None):
+    """One call: the plan's network on the device tensor x (NHWC, batch
+    frames, bfloat16 or float32 -- the run dtype), with the parameters
+    `params` (per-layer host arrays w / scale / bias, as
+    workloads.make_inputs draws them) uploaded for this call
+    (mafat_run_network on caller-owned torch buffers).  Returns the output,
+    or writes it into `out` and returns that.  For repeated runs keep a
+    Network, which uploads the parameters once."""
+    import torch
+    if x.dtype not in (torch.bfloat16, torch.float32):
+        raise ValueError("x must be bfloat16 or float32")
+    dtype = "bf16" if x.dtype == torch.bfloat16 else "f32"
+    net = Network(plan, params, x.shape[0], dtype, device=x.device)
+    y = net.run(x.contiguous(), stream=stream)
+    if out is None:
+        return y
+    out.copy_(y)
+    return out

@@ -543,3 +543,26 @@ def test_tile_batch_parity(orc):
     out = y.float().cpu().numpy().astype(np.float64)
     ref = orc.forward_layers(layers, h, w, c, p["x"], p)
     assert normwise_err(out, ref) <= TOL["bf16"]
+
+
+def test_run_network_one_call(orc):
+    # the one-call form (uploads the parameters, runs, returns the output)
+    # == a Network's run, bit for bit, with and without `out`
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    layers, (h, w, c) = W.YOLOV2_16, (96, 96, 3)
+    print(f"[parity] run_network one call {h}x{w}x{c} 3x3/8/2x2 bf16 batch 2", flush=True)
+    p = W.make_inputs(layers, h, w, c, 2, 41, "bf16")
+    plan = M.Plan(layers, (h, w, c), "3x3/8/2x2")
+    net = M.Network(plan, p, 2, "bf16")
+    x = net.input_tensor(p["x"])
+    ref = net.run(x).clone()
+    y = M.run_network(plan, x, p)
+    out = torch.empty_like(ref)
+    y2 = M.run_network(plan, x, p, out=out)
+    torch.cuda.synchronize()
+    assert y2 is out
+    assert torch.equal(y.view(torch.int16), ref.view(torch.int16))
+    assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
+    e = normwise_err(ref.float().cpu().numpy().astype(np.float64), orc.forward_layers(layers, h, w, c, p["x"], p))
+    assert e <= TOL["bf16"], e
