@@ -136,12 +136,35 @@ enum {
    * the stage configurations chosen for one frame (the packing follows
    * their output-channel blocks).  A layout of this library, not of the
    * paper. */
-  MAFAT_PLAN_PACKED_WEIGHTS = 2
+  MAFAT_PLAN_PACKED_WEIGHTS = 2,
+  /* Row reuse: the data reuse of section 3 (a tile takes the overlap that
+   * tiles run before it already computed, instead of computing it again)
+   * with the tiles run one grid row after another, each row through all
+   * stages of the group before the next (the tiles of a row together).
+   * Each stage's output is split into computed parts: the group output
+   * along the group's tile boundaries, and every earlier stage output along
+   * the back-projected ends of the next stage's parts, so that a tile row
+   * computes exactly the rows below its predecessors that its own next
+   * stage reads, and nothing twice.  Per stage output the workspace holds
+   * a band: the rows a tile row computes plus the rows above them that its
+   * next stage reads (taken over from the previous row's band by a copy on
+   * the stream), the full width, two such bands per stage output
+   * alternating between rows.  Stage outputs that a fused kernel keeps on
+   * chip get no band.  Results equal the untiled network's (up to
+   * accumulation order); executed MACs equal the untiled ones;
+   * mafat_plan_set_tile_batch and mafat_run_stage do not apply
+   * (EUNSUPPORTED).  Combines with
+   * MAFAT_PLAN_PACKED_WEIGHTS and with given tile boundaries, not with
+   * MAFAT_PLAN_STAGE_PARTITION.  mafat_plan_regions and the paper's memory
+   * model keep describing the plain (recomputing) partition. */
+  MAFAT_PLAN_ROW_REUSE = 4
 };
 
 /* mafat_plan_create (sections 4 and 4.1) with flags
- * (MAFAT_PLAN_STAGE_PARTITION and/or MAFAT_PLAN_PACKED_WEIGHTS, or 0).
- * Errors: those of mafat_plan_create, and EINVAL for unknown flags. */
+ * (MAFAT_PLAN_STAGE_PARTITION or MAFAT_PLAN_ROW_REUSE, and/or
+ * MAFAT_PLAN_PACKED_WEIGHTS, or 0).
+ * Errors: those of mafat_plan_create, EINVAL for unknown flags and
+ * EUNSUPPORTED for MAFAT_PLAN_STAGE_PARTITION with MAFAT_PLAN_ROW_REUSE. */
 int mafat_plan_create_flags(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
                             int32_t in_w, int32_t in_c, const int32_t* group_start,
                             int32_t n_groups, const int32_t* grid_rows,
@@ -200,7 +223,7 @@ int mafat_balanced_bounds(const mafat_layer* layers, int32_t n_layers, int32_t i
  * mafat_run_group_timed enclose the stage's first to last launch (other stages'
  * launches in between).  Errors: EINVAL (NULL, tiles < 0), EUNSUPPORTED
  * (a plan with MAFAT_PLAN_STAGE_PARTITION and 0 < tiles < a group's tile
- * count).  Not thread-safe: it rewrites the plan's per-tile workspace
+ * count; a plan with MAFAT_PLAN_ROW_REUSE).  Not thread-safe: it rewrites the plan's per-tile workspace
  * offsets, so no other thread may use the plan (run it, size its workspace)
  * during the call; the plan is read-only again afterwards. */
 int mafat_plan_set_tile_batch(mafat_plan* plan, int32_t tiles);
@@ -370,7 +393,8 @@ int mafat_run_group_timed(const mafat_plan* plan, int32_t group, int32_t batch, 
  * pair's stages as two kernels, see mafat_plan_stage_fused).  Same
  * arguments, conventions and errors as mafat_run_group, plus EINVAL for a
  * stage index out of range and EUNSUPPORTED for a group that runs in
- * several tile batches (mafat_plan_set_tile_batch). */
+ * several tile batches (mafat_plan_set_tile_batch) and for a plan with
+ * MAFAT_PLAN_ROW_REUSE. */
 int mafat_run_stage(const mafat_plan* plan, int32_t group, int32_t stage, int32_t batch,
                     int32_t dtype, const void* x, void* y, const void* const* w,
                     const float* const* scale, const float* const* bias, void* workspace,
@@ -424,11 +448,11 @@ int mafat_run_network_static(const mafat_plan* plan, int32_t batch, int32_t dtyp
  *     workspace (mafat_workspace_size).  By default every tile of a stage
  *     runs at once on the GPU, so the workspace holds every tile's
  *     intermediates; with a tile batch (mafat_plan_set_tile_batch) it holds
- *     one batch's.
+ *     one batch's, with row reuse the stage outputs' row bands.
  *   model MAFAT_MEM_DEVICE_SEQ: the device memory of the same plan run one
  *     tile at a time (tile batch 1, the paper's execution order), whatever
- *     the plan's tile batch; for groups with the stage partition, their workspace as
- *     MAFAT_MEM_DEVICE.  With mafat_get_config this is the paper's search
+ *     the plan's tile batch; for groups with the stage partition or row
+ *     reuse, their workspace as MAFAT_MEM_DEVICE.  With mafat_get_config this is the paper's search
  *     under a device-memory limit.
  * *bytes receives the prediction.  Errors: EINVAL (null plan or pointer,
  * batch < 1, unknown model), EUNSUPPORTED (dtype). */

@@ -580,6 +580,167 @@ int orc_forward_tiled_bounds(const orc_layer* layers, int n, int h, int w, int c
   return rc;
 }
 
+/* Row reuse (the data reuse of section 3 -- a tile takes the overlap that
+ * tiles run before it computed -- with a group's tiles run one grid row after
+ * another).  Row boundaries of every layer output of group [g0, g1]:
+ * rb[(l - g0) * (rows + 1) + i].  The group output's are the tile rows'; each
+ * earlier layer's output is cut where the rows that the next layer's parts
+ * read end, so that a tile row computes the rows its own next layer reads
+ * beyond those of earlier tile rows. */
+static void reuse_rows(const orc_layer* layers, const int* dims, int g0, int g1, int rows,
+                       const int* bounds, int* rb) {
+  int* last = rb + (size_t)(g1 - g0) * (rows + 1);
+  for (int i = 0; i < rows; ++i) {
+    int a, b;
+    span(dims[6 * g1 + 3], rows, i, bounds, &a, &b);
+    last[i] = a;
+  }
+  last[rows] = dims[6 * g1 + 3];
+  for (int l = g1 - 1; l >= g0; --l) {
+    const orc_layer* N = &layers[l + 1];
+    const int* nxt = rb + (size_t)(l + 1 - g0) * (rows + 1);
+    int* cur = rb + (size_t)(l - g0) * (rows + 1);
+    cur[0] = 0;
+    for (int i = 1; i <= rows; ++i) {
+      int a, b;
+      back_project(0, nxt[i], N->f, N->s, N->p, dims[6 * (l + 1)], &a, &b);
+      cur[i] = nxt[i] > 0 ? b : 0;
+    }
+  }
+}
+
+/* First row of tile row i's band of layer l's output (l < g1): the first
+ * row that the next layer's part of tile row i reads, or the row's own first
+ * computed row if that is lower. */
+static int reuse_band_lo(const orc_layer* layers, const int* dims, int g0, int l, int rows,
+                         const int* rb, int i) {
+  const orc_layer* N = &layers[l + 1];
+  const int* nxt = rb + (size_t)(l + 1 - g0) * (rows + 1);
+  const int* cur = rb + (size_t)(l - g0) * (rows + 1);
+  int a, b;
+  back_project(nxt[i], nxt[i] + 1, N->f, N->s, N->p, dims[6 * (l + 1)], &a, &b);
+  return imin(a, cur[i]);
+}
+
+int orc_forward_row_reuse(const orc_layer* layers, int n, int h, int w, int c,
+                          int batch, const int* group_start, int n_groups,
+                          const int* grid_rows, const int* row_bounds,
+                          const double* x, const double* const* wt,
+                          const double* const* scale, const double* const* bias,
+                          int round_bf16, double* y, double* const* cut_out, int* band_rows) {
+  if (batch < 1 || (!x) != (!y) || n < 1 || n_groups < 1 || !group_start || !grid_rows) return ORC_EINVAL;
+  int* dims = (int*)malloc(sizeof(int) * 6 * (size_t)n);
+  if (!dims) return ORC_ENOMEM;
+  int rc = orc_shapes(layers, n, h, w, c, dims);
+  if (!rc && group_start[0] != 0) rc = ORC_EINVAL;
+  for (int g = 0; g < n_groups && !rc; ++g) {
+    int g1 = ((g + 1 < n_groups) ? group_start[g + 1] : n) - 1;
+    if (g1 < group_start[g] || g1 >= n || grid_rows[g] < 1 || grid_rows[g] > dims[6 * g1 + 3]) rc = ORC_EINVAL;
+  }
+  if (!rc && row_bounds) {
+    const int* rbp = row_bounds;
+    for (int g = 0; g < n_groups && !rc; ++g) {
+      int g1 = ((g + 1 < n_groups) ? group_start[g + 1] : n) - 1;
+      if (!bounds_ok(rbp, grid_rows[g], dims[6 * g1 + 3])) rc = ORC_EINVAL;
+      rbp += grid_rows[g] + 1;
+    }
+  }
+  for (int l = 0; l < n && !rc && x; ++l)
+    if (layers[l].op == ORC_CONV && (!wt || !wt[l] || !scale || !scale[l] || !bias || !bias[l])) rc = ORC_EINVAL;
+  if (band_rows)
+    for (int l = 0; l < n; ++l) band_rows[l] = 0;
+  const double* gin = x;
+  double* owned = NULL;
+  const int* rbp = row_bounds;
+  for (int g = 0; g < n_groups && !rc; ++g) {
+    const int g0 = group_start[g], g1 = ((g + 1 < n_groups) ? group_start[g + 1] : n) - 1;
+    const int rows = grid_rows[g], nl = g1 - g0 + 1;
+    int* rb = (int*)malloc(sizeof(int) * (size_t)nl * (rows + 1));
+    if (!rb) { rc = ORC_ENOMEM; break; }
+    reuse_rows(layers, dims, g0, g1, rows, rbp, rb);
+    if (rbp) rbp += rows + 1;
+    for (int l = g0; l < g1 && band_rows; ++l)
+      for (int i = 0; i < rows; ++i) {
+        int hi = rb[(size_t)(l - g0) * (rows + 1) + i + 1];
+        int lo = reuse_band_lo(layers, dims, g0, l, rows, rb, i);
+        if (hi - lo > band_rows[l]) band_rows[l] = hi - lo;
+      }
+    if (!x) { free(rb); continue; }  /* geometry only */
+    const int* din = dims + 6 * g0;
+    const int* dout = dims + 6 * g1;
+    size_t in_elems = (size_t)din[0] * din[1] * din[2];
+    size_t out_elems = (size_t)dout[3] * dout[4] * dout[5];
+    double* gout;
+    double* fresh = NULL;
+    if (g == n_groups - 1) gout = y;
+    else if (cut_out && cut_out[g]) gout = cut_out[g];
+    else gout = NULL;
+    if (!gout) {
+      fresh = (double*)malloc(sizeof(double) * out_elems * (size_t)batch);
+      if (!fresh) { free(rb); rc = ORC_ENOMEM; break; }
+      gout = fresh;
+    }
+    double** band = (double**)calloc((size_t)nl, sizeof(double*));
+    int* blo = (int*)calloc((size_t)nl, sizeof(int));
+    if (!band || !blo) rc = ORC_ENOMEM;
+    for (int b = 0; b < batch && !rc; ++b) {
+      for (int i = 0; i < rows && !rc; ++i) {
+        for (int l = g0; l <= g1 && !rc; ++l) {
+          const int* d = dims + 6 * l;
+          const int* r = rb + (size_t)(l - g0) * (rows + 1);
+          int err = 0;
+          /* the input: the group input, or the band of layer l - 1 that
+           * tile row i just completed */
+          view_t in;
+          if (l == g0) {
+            view_t v = {gin + (size_t)b * in_elems, 0, 0, d[0], d[1], d[2], d[1] * d[2], d[0], d[1], &err};
+            in = v;
+          } else {
+            const int* rp = rb + (size_t)(l - 1 - g0) * (rows + 1);
+            view_t v = {band[l - 1 - g0], blo[l - 1 - g0], 0, rp[i + 1] - blo[l - 1 - g0], d[1], d[2],
+                        d[1] * d[2], d[0], d[1], &err};
+            in = v;
+          }
+          const size_t row_elems = (size_t)d[4] * d[5];
+          if (l == g1) {  /* straight into the group output */
+            layer_rect(&in, &layers[l], d[5], wt ? wt[l] : NULL, scale ? scale[l] : NULL,
+                       bias ? bias[l] : NULL, round_bf16, r[i], r[i + 1], 0, d[4],
+                       gout + (size_t)b * out_elems + (size_t)r[i] * row_elems);
+          } else {  /* a new band: rows taken over from the old one, then its own */
+            int lo = reuse_band_lo(layers, dims, g0, l, rows, rb, i);
+            size_t nrows = (size_t)(r[i + 1] - lo);
+            double* nb = (double*)malloc(sizeof(double) * (nrows ? nrows : 1) * row_elems);
+            if (!nb) { rc = ORC_ENOMEM; break; }
+            if (r[i] > lo) {
+              /* those rows lie in the previous row's band, [blo, r[i]) */
+              if (!band[l - g0] || lo < blo[l - g0]) { free(nb); rc = ORC_EREGION; break; }
+              memcpy(nb, band[l - g0] + (size_t)(lo - blo[l - g0]) * row_elems,
+                     sizeof(double) * (size_t)(r[i] - lo) * row_elems);
+            }
+            layer_rect(&in, &layers[l], d[5], wt ? wt[l] : NULL, scale ? scale[l] : NULL,
+                       bias ? bias[l] : NULL, round_bf16, r[i], r[i + 1], 0, d[4],
+                       nb + (size_t)(r[i] - lo) * row_elems);
+            free(band[l - g0]);
+            band[l - g0] = nb;
+            blo[l - g0] = lo;
+          }
+          if (err) rc = err;
+        }
+      }
+      for (int k = 0; k < nl && band; ++k) { free(band[k]); band[k] = NULL; }
+    }
+    free(band);
+    free(blo);
+    free(rb);
+    free(owned);
+    owned = fresh;
+    gin = gout;
+  }
+  free(owned);
+  free(dims);
+  return rc;
+}
+
 int orc_forward_rect(const orc_layer* layers, int n, int h, int w, int c,
                      const double* x, const double* const* wt,
                      const double* const* scale, const double* const* bias,

@@ -115,6 +115,28 @@ int orc_forward_tiled_bounds(const orc_layer* layers, int n, int h, int w, int c
                              const double* const* scale, const double* const* bias,
                              int round_bf16, double* y, double* const* cut_out);
 
+/* Row reuse, the data reuse between tiles of section 3 (a tile takes the
+ * overlap that tiles run before it already computed instead of computing it
+ * again) with every group's tiles run one grid row after another, each row
+ * through all layers of the group.  The group output is cut into the tile
+ * rows (row_bounds as in orc_regions_bounds, NULL: even split); every earlier
+ * layer output of the group is cut where the rows that the next layer's parts
+ * read end, so a tile row computes the rows that its next layer reads
+ * beyond those of the rows before it, and no row twice.  A tile row keeps
+ * each layer's output in a band of full-width rows: its own rows and the
+ * rows above them that its next layer reads, taken over from the previous
+ * row's band; a read outside the band is ORC_EREGION.  Columns are not cut
+ * (the tiles of a row compute the same values together).  y and cut_out as
+ * orc_forward_tiled.  band_rows (n values, may be NULL) receives, per layer,
+ * the most rows any of its bands holds (0 for a group's last layer).  With x
+ * and y both NULL only band_rows is computed. */
+int orc_forward_row_reuse(const orc_layer* layers, int n, int h, int w, int c,
+                          int batch, const int* group_start, int n_groups,
+                          const int* grid_rows, const int* row_bounds,
+                          const double* x, const double* const* wt,
+                          const double* const* scale, const double* const* bias,
+                          int round_bf16, double* y, double* const* cut_out, int* band_rows);
+
 /* Balanced boundaries of `parts` tiles along one axis (0: rows, 1: columns)
  * of the output of layer group [g0, g1] (variable tiling, section 6: end
  * tiles sized differently from inner ones so that task sizes vary less).

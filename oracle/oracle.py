@@ -69,6 +69,8 @@ def lib():
         L.orc_forward_tiled_bounds.argtypes = [lp, i, i, i, i, i, ip, i, ip, ip, ip, ip, dp, dpp, dpp,
                                                dpp, i, dp, dpp]
         L.orc_balanced_bounds.argtypes = [lp, i, i, i, i, i, i, i, i, ip]
+        L.orc_forward_row_reuse.argtypes = [lp, i, i, i, i, i, ip, i, ip, ip, dp, dpp, dpp, dpp, i, dp, dpp,
+                                            ip]
         L.orc_set_threads.argtypes = [i]
         L.orc_round_bf16.argtypes = [ctypes.c_double]
         L.orc_round_bf16.restype = ctypes.c_double
@@ -222,6 +224,50 @@ def forward_tiled(layers, h, w, c, x, params, group_start, rows, cols, round_bf1
                                           rbp, cbp, xp, wp, sp, bp, int(round_bf16),
                                           y.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), cut_pp))
     return (y, cuts) if want_cuts else y
+
+
+def forward_row_reuse(layers, h, w, c, x, params, group_start, rows, round_bf16=False, want_cuts=False,
+                      row_bounds=None):
+    """Row reuse (orc_forward_row_reuse): every group's tile rows in order,
+    each layer output computed once into row bands.  Returns y (and the cut
+    tensors with want_cuts)."""
+    n = len(layers)
+    dims = shapes(layers, h, w, c)
+    x, xp = _dbl(x)
+    batch = x.shape[0]
+    y = np.zeros((batch, dims[-1, 3], dims[-1, 4], dims[-1, 5]), dtype=np.float64)
+    gs, gsp = _ints(group_start)
+    r, rp = _ints(rows)
+    cuts = []
+    cut_pp = None
+    if want_cuts and len(gs) > 1:
+        cut_pp = (ctypes.POINTER(ctypes.c_double) * (len(gs) - 1))()
+        for g in range(len(gs) - 1):
+            last = gs[g + 1] - 1
+            a = np.zeros((batch, dims[last, 3], dims[last, 4], dims[last, 5]), dtype=np.float64)
+            cuts.append(a)
+            cut_pp[g] = a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+    kw, wp = _ptr_list(params["w"])
+    ks, sp = _ptr_list(params["scale"])
+    kb, bp = _ptr_list(params["bias"])
+    rb, rbp = _bounds(row_bounds)
+    _check(lib().orc_forward_row_reuse(_layers(layers), n, h, w, c, batch, gsp, len(gs), rp, rbp, xp, wp, sp,
+                                       bp, int(round_bf16), y.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                       cut_pp, None))
+    return (y, cuts) if want_cuts else y
+
+
+def row_reuse_band_rows(layers, h, w, c, group_start, rows, row_bounds=None):
+    """Per layer, the most rows any of its row-reuse bands holds (0 for a
+    group's last layer): the geometry of orc_forward_row_reuse alone."""
+    n = len(layers)
+    gs, gsp = _ints(group_start)
+    r, rp = _ints(rows)
+    rb, rbp = _bounds(row_bounds)
+    out = np.zeros(n, dtype=np.int32)
+    _check(lib().orc_forward_row_reuse(_layers(layers), n, h, w, c, 1, gsp, len(gs), rp, rbp, None, None, None,
+                                       None, 0, None, None, out.ctypes.data_as(ctypes.POINTER(ctypes.c_int))))
+    return out
 
 
 def forward_rect(layers, h, w, c, x1, params, oy0, oy1, ox0, ox1, round_bf16=False):

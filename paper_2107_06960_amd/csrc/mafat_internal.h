@@ -50,6 +50,14 @@ struct Stage {
   int f, s, p, act;        // filter, stride, padding (conv or pool), activation (conv)
   int src_buf, dst_buf;    // BufKind
   std::vector<TileGeom> tiles;
+  // Row reuse (an output that is not the group's): per tile row i, the
+  // first row of its output band (band_lo[i]) and the rows it computes,
+  // [row_b[i], row_b[i + 1]) of the stage output; band_rows = the largest
+  // band, row_b[i + 1] - band_lo[i]; band_copies = 1 when every row's
+  // take-over from its predecessor can move within one band buffer (source
+  // and destination rows apart), else 2 (rows alternate between two).
+  std::vector<int> band_lo, row_b;
+  int band_rows = 0, band_copies = 0;
 };
 
 struct Group {
@@ -61,6 +69,7 @@ struct Group {
   int nbufs;              // scratch buffers (0, 1 or 2)
   int64_t scratch_frame;  // scratch elements of one frame
   bool partition;         // stage partition: every stage output computed once (full tensors)
+  bool reuse = false;     // row reuse: tile rows in order, stage outputs in row bands
   int tile_batch;         // tiles run through the stages together (ntiles unless
                           // mafat_plan_set_tile_batch set fewer); scratch per batch
   int64_t macs_exec, macs_untiled;
@@ -110,7 +119,18 @@ bool packed_layout(const mafat_plan& P, int layer, int dtype, int* bn, int* nblk
 struct WorkspaceLayout {
   size_t scratch, total;
 };
-WorkspaceLayout workspace_layout(const Group& G, int batch, int dtype);
+WorkspaceLayout workspace_layout(const mafat_plan& P, const Group& G, int batch, int dtype);
+
+// Row reuse: the band buffers of one frame for a dtype.  Tile row i writes
+// stage s's output into the band at base[s][i % 2] (elements from the
+// frame's scratch start, 256-byte aligned; the two are one buffer when
+// band_copies is 1), or there is none (base -1: the group output, or kept
+// on chip by a fused kernel).
+struct BandLayout {
+  std::vector<std::array<int64_t, 2>> base;
+  int64_t frame;  // elements of one frame's bands
+};
+BandLayout band_layout(const mafat_plan& P, const Group& G, int dtype);
 
 // Every group of a plan in order (mafat_run_network without clearing the
 // error state), on the given workspace; stream is a hipStream_t.

@@ -51,6 +51,24 @@ void back_project(int a, int b, int F, int S, int P, int E, int* ia, int* ib) {
   *ib = std::min(E, (b - 1) * S - P + F);
 }
 
+// Where the input rows (axis 0) or columns (axis 1) that outputs ending at
+// b (starting at a) read end (start), through layers [lf, ll] of a stack:
+// back_project's two ends, taken apart.
+int end_through(const mafat_plan& P, int lf, int ll, int axis, int b) {
+  for (int l = ll; l >= lf && b > 0; --l) {
+    const mafat_layer& L = P.layers[l];
+    b = std::min(P.dims[l][axis], (b - 1) * L.s - L.p + L.f);
+  }
+  return std::max(b, 0);
+}
+int start_through(const mafat_plan& P, int lf, int ll, int axis, int a) {
+  for (int l = ll; l >= lf; --l) {
+    const mafat_layer& L = P.layers[l];
+    a = std::max(0, a * L.s - L.p);
+  }
+  return a;
+}
+
 // Boundaries b[0..N] of N parts of [0, E): 0 = b[0] < ... < b[N] = E.
 bool bounds_valid(const int32_t* b, int N, int E) {
   if (b[0] != 0 || b[N] != E) return false;
@@ -61,10 +79,11 @@ bool bounds_valid(const int32_t* b, int N, int E) {
 
 // rb / cb: the group output's row / column boundaries (rows + 1 / cols + 1
 // values), or NULL for the even floor split.
-int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool partition,
+int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool partition, bool reuse,
                 const int32_t* rb, const int32_t* cb, Group* out) {
   Group G;
   G.partition = partition;
+  G.reuse = reuse;
   G.l0 = g0; G.l1 = g1; G.rows = rows; G.cols = cols; G.ntiles = rows * cols;
   const int nl = g1 - g0 + 1;
   const auto& dl = plan.dims[g1];
@@ -139,6 +158,84 @@ int build_group(mafat_plan& plan, int g0, int g1, int rows, int cols, bool parti
   const int ns = static_cast<int>(G.stages.size());
   G.nbufs = std::min(2, ns - 1);
   G.scratch_elems = 0;
+  if (reuse) {
+    // Row reuse (data reuse between tiles run in order): tile rows one after
+    // another.  The group output's parts are the tiles; every earlier stage
+    // output is cut at the ends of what the next stage's parts read (the
+    // back-projected ends of its boundaries), so tile row i computes, at
+    // every stage, the rows below row i - 1's that its own next stage reads
+    // and no row twice.  Columns are cut the same way (the tiles of a row
+    // run together, so any cut would do).  A stage output that is not the
+    // group's lives in a band of full-width rows: [band_lo[i], row_b[i+1])
+    // for tile row i, band_lo[i] being the first row its next stage reads
+    // (or its own first computed row, if lower); the rows above its own come
+    // from row i - 1's band, moved up in the same buffer or, where the rows
+    // they leave and the rows they go to would overlap, from the other of
+    // two buffers the rows alternate between.
+    std::vector<std::vector<int>> rbs(ns), cbs(ns);
+    rbs[ns - 1].resize(rows + 1);
+    cbs[ns - 1].resize(cols + 1);
+    for (int i = 0; i <= rows; ++i) {
+      int a, b;
+      split(dl[3], rows, std::min(i, rows - 1), &a, &b);
+      rbs[ns - 1][i] = rb ? rb[i] : (i < rows ? a : dl[3]);
+    }
+    for (int j = 0; j <= cols; ++j) {
+      int a, b;
+      split(dl[4], cols, std::min(j, cols - 1), &a, &b);
+      cbs[ns - 1][j] = cb ? cb[j] : (j < cols ? a : dl[4]);
+    }
+    for (int s = ns - 2; s >= 0; --s) {
+      const Stage& N = G.stages[s + 1];
+      rbs[s].assign(rows + 1, 0);
+      cbs[s].assign(cols + 1, 0);
+      for (int i = 1; i <= rows; ++i) rbs[s][i] = end_through(plan, N.first, N.last, 0, rbs[s + 1][i]);
+      for (int j = 1; j <= cols; ++j) cbs[s][j] = end_through(plan, N.first, N.last, 1, cbs[s + 1][j]);
+      Stage& S = G.stages[s];
+      S.row_b = rbs[s];
+      S.band_lo.assign(rows, 0);
+      S.band_rows = 0;
+      S.band_copies = 1;
+      for (int i = 0; i < rows; ++i) {
+        S.band_lo[i] = std::min(start_through(plan, N.first, N.last, 0, rbs[s + 1][i]), rbs[s][i]);
+        S.band_rows = std::max(S.band_rows, rbs[s][i + 1] - S.band_lo[i]);
+        // the rows taken over, [band_lo[i], row_b[i]), move from band
+        // position band_lo[i] - band_lo[i-1] to position 0
+        if (i > 0 && rbs[s][i] - S.band_lo[i] > S.band_lo[i] - S.band_lo[i - 1]) S.band_copies = 2;
+      }
+    }
+    int64_t frame = 0;  // the bands of every stage output (an upper bound of any dtype's)
+    for (int s = 0; s < ns; ++s) {
+      Stage& S = G.stages[s];
+      S.src_buf = (s == 0) ? BUF_GROUP_IO : BUF_SCRATCH0;
+      S.dst_buf = (s == ns - 1) ? BUF_GROUP_IO : BUF_SCRATCH0;
+      if (s < ns - 1)
+        frame += S.band_copies * ((static_cast<int64_t>(S.band_rows) * S.out_w * S.cout + 127) / 128 * 128);
+      const int k = S.pool ? 2 : 1;
+      for (int i = 0; i < rows; ++i)
+        for (int j = 0; j < cols; ++j) {
+          TileGeom T{};
+          T.cy0 = k * rbs[s][i]; T.ch = k * (rbs[s][i + 1] - rbs[s][i]);
+          T.cx0 = k * cbs[s][j]; T.cw = k * (cbs[s][j + 1] - cbs[s][j]);
+          T.sy0 = (s == 0) ? 0 : G.stages[s - 1].band_lo[i];
+          T.sx0 = 0; T.sw = S.in_w;
+          T.dy0 = (s == ns - 1) ? 0 : S.band_lo[i];
+          T.dx0 = 0; T.dw = S.out_w;
+          T.src_off = T.dst_off = 0;  // band bases: per dtype, at run time
+          S.tiles.push_back(T);
+        }
+    }
+    G.nbufs = 0;
+    G.scratch_frame = frame;
+    G.tile_batch = cols;
+    G.macs_exec = 0;
+    for (const Stage& S : G.stages)
+      if (S.kind == STAGE_CONV)
+        for (const TileGeom& T : S.tiles)
+          G.macs_exec += static_cast<int64_t>(T.ch) * T.cw * S.cout * S.f * S.f * S.cin;
+    *out = std::move(G);
+    return MAFAT_OK;
+  }
   if (partition) {
     // Tile reuse (the data reuse between adjacent tiles of DeepThings'
     // fused tile partitioning, taken to the whole stage): the stages run one
@@ -276,9 +373,13 @@ extern "C" int mafat_plan_create_bounds(const mafat_layer* layers, int32_t n_lay
   clear_error();
   if (!out) { set_error("out is NULL"); return MAFAT_EINVAL; }
   *out = nullptr;
-  if (flags & ~(MAFAT_PLAN_STAGE_PARTITION | MAFAT_PLAN_PACKED_WEIGHTS)) {
+  if (flags & ~(MAFAT_PLAN_STAGE_PARTITION | MAFAT_PLAN_PACKED_WEIGHTS | MAFAT_PLAN_ROW_REUSE)) {
     set_error("unknown plan flags");
     return MAFAT_EINVAL;
+  }
+  if ((flags & MAFAT_PLAN_STAGE_PARTITION) && (flags & MAFAT_PLAN_ROW_REUSE)) {
+    set_error("the stage partition and row reuse are two different executions: choose one");
+    return MAFAT_EUNSUPPORTED;
   }
   if ((flags & MAFAT_PLAN_STAGE_PARTITION) && (row_bounds || col_bounds)) {
     set_error("the stage partition splits every stage evenly: no tile boundaries with it");
@@ -334,7 +435,8 @@ extern "C" int mafat_plan_create_bounds(const mafat_layer* layers, int32_t n_lay
       }
       Group G;
       const int rc = build_group(*plan, g0, end - 1, grid_rows[g], grid_cols[g],
-                                 (flags & MAFAT_PLAN_STAGE_PARTITION) != 0, rb, cb, &G);
+                                 (flags & MAFAT_PLAN_STAGE_PARTITION) != 0, (flags & MAFAT_PLAN_ROW_REUSE) != 0,
+                                 rb, cb, &G);
       if (rc != MAFAT_OK) { delete plan; return rc; }
       if (rb) rb += grid_rows[g] + 1;
       if (cb) cb += grid_cols[g] + 1;
@@ -585,6 +687,11 @@ extern "C" int mafat_plan_set_tile_batch(mafat_plan* plan, int32_t tiles) {
     return MAFAT_EINVAL;
   }
   for (const Group& G : plan->groups)
+    if (G.reuse) {
+      set_error("row reuse runs one tile row at a time: no other tile batches");
+      return MAFAT_EUNSUPPORTED;
+    }
+  for (const Group& G : plan->groups)
     if (G.partition && tiles > 0 && tiles < G.ntiles) {
       set_error("the stage partition needs every tile of a stage before the next stage: no tile batches");
       return MAFAT_EUNSUPPORTED;
@@ -599,7 +706,7 @@ extern "C" int mafat_workspace_size(const mafat_plan* plan, int32_t batch, int32
   if (!plan || !bytes || batch < 1) return MAFAT_EINVAL;
   if (dtype != MAFAT_F32 && dtype != MAFAT_BF16) return MAFAT_EUNSUPPORTED;
   size_t best = 0;
-  for (const Group& G : plan->groups) best = std::max(best, workspace_layout(G, batch, dtype).total);
+  for (const Group& G : plan->groups) best = std::max(best, workspace_layout(*plan, G, batch, dtype).total);
   *bytes = best;
   return MAFAT_OK;
 }

@@ -19,8 +19,10 @@
 //                    bias) and the workspace.  On the GPU every tile of a
 //                    stage runs at once, so the working set is all tiles'
 //                    intermediates (the workspace), not the largest tile's;
-//                    with a tile batch K, K tiles' intermediates.
-//   MAFAT_MEM_DEVICE_SEQ the same with one tile at a time (tile batch 1).
+//                    with a tile batch K, K tiles' intermediates; with row
+//                    reuse, the row bands of the stage outputs.
+//   MAFAT_MEM_DEVICE_SEQ the same with one tile at a time (tile batch 1;
+//                    row reuse as it is).
 //
 // mafat_get_config: the configuration search of the paper (section 4.2,
 // Algorithm 2): cuts are tried in the given order (a cut >= n_layers means
@@ -86,6 +88,10 @@ int64_t device_bytes(const mafat_plan& P, int batch, int dtype, bool one_tile) {
     mafat_workspace_size(&P, batch, dtype, &ws);
   } else {  // the workspace of tile batch 1: one tile slot per scratch buffer
     for (const Group& G : P.groups) {
+      if (G.reuse) {  // its tile rows run one after another already
+        ws = std::max(ws, workspace_layout(P, G, batch, dtype).total);
+        continue;
+      }
       const int64_t frame = G.partition ? G.scratch_frame : static_cast<int64_t>(G.nbufs) * G.scratch_elems;
       ws = std::max(ws, (static_cast<size_t>(batch) * frame * esz + 255) & ~static_cast<size_t>(255));
     }

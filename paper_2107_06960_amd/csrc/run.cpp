@@ -372,10 +372,28 @@ bool packed_layout(const mafat_plan& P, int layer, int dtype, int* bn, int* nblk
   return false;
 }
 
-WorkspaceLayout workspace_layout(const Group& G, int batch, int dtype) {
+BandLayout band_layout(const mafat_plan& P, const Group& G, int dtype) {
+  BandLayout B;
+  const int ns = static_cast<int>(G.stages.size());
+  B.base.assign(static_cast<size_t>(ns), {-1, -1});
+  B.frame = 0;
+  for (int s = 0; s + 1 < ns; ++s) {
+    const Stage& S = G.stages[s];
+    // A stage run fused with the next one keeps its output on chip (a
+    // row-reuse group always runs whole, so its fused pairs always fuse).
+    if (stage_config(P, G, S, 1, dtype).fuse > 0) continue;
+    const int64_t band = (static_cast<int64_t>(S.band_rows) * S.out_w * S.cout + 127) / 128 * 128;
+    B.base[static_cast<size_t>(s)] = {B.frame, B.frame + (S.band_copies - 1) * band};
+    B.frame += S.band_copies * band;
+  }
+  return B;
+}
+
+WorkspaceLayout workspace_layout(const mafat_plan& P, const Group& G, int batch, int dtype) {
   const size_t esz = (dtype == MAFAT_F32) ? 4 : 2;
+  const int64_t frame = G.reuse ? band_layout(P, G, dtype).frame : G.scratch_frame;
   WorkspaceLayout L{};
-  L.scratch = (static_cast<size_t>(batch) * G.scratch_frame * esz + 255) & ~static_cast<size_t>(255);
+  L.scratch = (static_cast<size_t>(batch) * frame * esz + 255) & ~static_cast<size_t>(255);
   L.total = L.scratch;
   return L;
 }
@@ -407,7 +425,9 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
   const auto& dout = plan->dims[G.l1];
   const int64_t in_frame = static_cast<int64_t>(din[0]) * din[1] * din[2];
   const int64_t out_frame = static_cast<int64_t>(dout[3]) * dout[4] * dout[5];
-  const int64_t scr_frame = G.scratch_frame;
+  BandLayout bands;
+  if (G.reuse) bands = band_layout(*plan, G, dtype);
+  const int64_t scr_frame = G.reuse ? bands.frame : G.scratch_frame;
   if (in_frame >= (1ll << 31) || out_frame >= (1ll << 31) || scr_frame >= (1ll << 31))
     return fail(MAFAT_EUNSUPPORTED, "a frame's tensor exceeds 2^31 elements");
   {
@@ -432,6 +452,28 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
   for (int b0 = 0; b0 < G.ntiles; b0 += K) {
     const int b1 = std::min(G.ntiles, b0 + K);
     const bool last_batch = b1 >= G.ntiles;
+    // Row reuse: batch = tile row i (K = the grid's columns).  Each band
+    // this row writes into first takes over, from row i - 1's band, the
+    // rows above row i's own that the next stage reads (within one buffer
+    // the two row ranges do not overlap).
+    const int row = b0 / std::max(K, 1);
+    if (G.reuse && row > 0) {
+      for (int s = 0; s + 1 < static_cast<int>(G.stages.size()); ++s) {
+        const Stage& S = G.stages[s];
+        if (bands.base[static_cast<size_t>(s)][0] < 0) continue;
+        const int lo = S.band_lo[static_cast<size_t>(row)], prev_lo = S.band_lo[static_cast<size_t>(row - 1)];
+        const int n_rows = S.row_b[static_cast<size_t>(row)] - lo;
+        if (n_rows <= 0) continue;
+        const int64_t row_elems = static_cast<int64_t>(S.out_w) * S.cout;
+        char* base = static_cast<char*>(ws);
+        const char* from = base + (bands.base[static_cast<size_t>(s)][(row - 1) & 1] + (lo - prev_lo) * row_elems) * esz;
+        char* to = base + bands.base[static_cast<size_t>(s)][row & 1] * esz;
+        const size_t pitch = static_cast<size_t>(scr_frame) * esz;
+        const hipError_t e = hipMemcpy2DAsync(to, pitch, from, pitch, static_cast<size_t>(n_rows * row_elems) * esz,
+                                              static_cast<size_t>(batch), hipMemcpyDeviceToDevice, stream);
+        if (e != hipSuccess) return fail(MAFAT_EHIP, std::string("band copy failed: ") + hipGetErrorString(e));
+      }
+    }
     // A fused pair never writes the buffer it reads: inside a group its
     // input and output would be the same ping-pong scratch buffer (stages
     // s - 1 and s + 1), which other workgroups may still be reading, so the
@@ -511,8 +553,18 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
           const TileGeom& TD = SD.tiles[t];
           k.dy0 = static_cast<int16_t>(TD.dy0); k.dx0 = static_cast<int16_t>(TD.dx0);
           k.dw = static_cast<int16_t>(TD.dw);
-          k.src_off = static_cast<int32_t>(T.src_off + src_shift);
-          k.dst_off = static_cast<int32_t>(TD.dst_off + dst_shift);
+          if (G.reuse) {  // this row's bands (the fused pair's output is its second stage's)
+            const int sd = static_cast<int>(&SD - G.stages.data());
+            const int64_t sb = (s == 0) ? 0 : bands.base[static_cast<size_t>(s - 1)][row & 1];
+            const int64_t db = (sd + 1 == static_cast<int>(G.stages.size()))
+                                   ? 0 : bands.base[static_cast<size_t>(sd)][row & 1];
+            if (sb < 0 || db < 0) return fail(MAFAT_EINVAL, "internal: a stage output kept on chip is read");
+            k.src_off = static_cast<int32_t>(sb);
+            k.dst_off = static_cast<int32_t>(db);
+          } else {
+            k.src_off = static_cast<int32_t>(T.src_off + src_shift);
+            k.dst_off = static_cast<int32_t>(TD.dst_off + dst_shift);
+          }
           int64_t units = static_cast<int64_t>(TC.ch) * TC.cw;
           if ((kind == K_CONV_DIRECT || kind == K_CONV_RGB) && S.pool) units /= 4;
           if (kind == K_CONV_RGB_MFMA)  // 2-D blocks of conv outputs
@@ -685,8 +737,8 @@ extern "C" int mafat_run_stage(const mafat_plan* plan, int32_t group, int32_t st
     return fail(MAFAT_EINVAL, "group index out of range");
   if (stage < 0 || stage >= static_cast<int>(plan->groups[group].stages.size()))
     return fail(MAFAT_EINVAL, "stage index out of range");
-  if (plan->groups[group].tile_batch < plan->groups[group].ntiles)
-    return fail(MAFAT_EUNSUPPORTED, "the group runs in tile batches: its stages cannot run one at a time");
+  if (plan->groups[group].tile_batch < plan->groups[group].ntiles || plan->groups[group].reuse)
+    return fail(MAFAT_EUNSUPPORTED, "the group runs in tile batches or rows: its stages cannot run one at a time");
   return run_group_impl(plan, group, stage, stage + 1, batch, dtype, x, y, w, scale, bias, workspace, ws_bytes,
                         static_cast<hipStream_t>(stream), nullptr);
 }

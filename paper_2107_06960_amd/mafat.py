@@ -27,7 +27,7 @@ MAFAT_CONV, MAFAT_MAXPOOL = 0, 1
 MAFAT_ACT_LINEAR, MAFAT_ACT_LEAKY01 = 0, 1
 MAFAT_F32, MAFAT_BF16 = 0, 1
 MAFAT_MEM_DEVICE, MAFAT_MEM_PAPER, MAFAT_MEM_DEVICE_SEQ = 0, 1, 2
-MAFAT_PLAN_STAGE_PARTITION, MAFAT_PLAN_PACKED_WEIGHTS = 1, 2
+MAFAT_PLAN_STAGE_PARTITION, MAFAT_PLAN_PACKED_WEIGHTS, MAFAT_PLAN_ROW_REUSE = 1, 2, 4
 MAFAT_STATIC_WORKSPACE_MIB = 32   # include/mafat.h: size of the static workspace of mafat_run_network_static
 MEM_MODELS = {"device": MAFAT_MEM_DEVICE, "paper": MAFAT_MEM_PAPER, "device_seq": MAFAT_MEM_DEVICE_SEQ}
 DTYPES = {"f32": MAFAT_F32, "bf16": MAFAT_BF16}
@@ -156,8 +156,8 @@ def _flat_bounds(bounds):
 def mafat_plan_create(layers, in_h, in_w, in_c, group_start, grid_rows, grid_cols, flags=0,
                       row_bounds=None, col_bounds=None):
     """Returns a plan handle (int); raises MafatError with the library's status.
-    flags: 0, or MAFAT_PLAN_STAGE_PARTITION and/or MAFAT_PLAN_PACKED_WEIGHTS
-    (mafat_plan_create_flags).  row_bounds / col_bounds: per-group lists of
+    flags: 0, or MAFAT_PLAN_STAGE_PARTITION or MAFAT_PLAN_ROW_REUSE, and/or
+    MAFAT_PLAN_PACKED_WEIGHTS (mafat_plan_create_flags).  row_bounds / col_bounds: per-group lists of
     rows+1 / cols+1 tile boundaries (mafat_plan_create_bounds), or None."""
     n = len(layers)
     arr = _layer_array(layers)
@@ -360,12 +360,15 @@ class Plan:
     ``"5x5/8/2x2"`` (section 5.1 notation) or explicit group lists."""
 
     def __init__(self, layers, in_hwc, tiling="1x1/NoCut", stage_partition=False, packed_weights=False,
-                 tile_batch=0, bounds=None):
+                 tile_batch=0, bounds=None, row_reuse=False):
         """bounds: None (even tile boundaries), "balanced" (each group's
         mafat_balanced_bounds) or a pair (row_bounds, col_bounds) of
-        per-group boundary lists (mafat_plan_create_bounds)."""
+        per-group boundary lists (mafat_plan_create_bounds).  row_reuse:
+        MAFAT_PLAN_ROW_REUSE (tile rows in order, each stage output computed
+        once into row bands)."""
         self.layers = list(layers)
         self.stage_partition = bool(stage_partition)
+        self.row_reuse = bool(row_reuse)
         self.packed_weights = bool(packed_weights)
         self.tile_batch = int(tile_batch)
         self.h, self.w, self.c = in_hwc
@@ -384,7 +387,8 @@ class Plan:
         self.handle = mafat_plan_create(self.layers, self.h, self.w, self.c, self.group_start,
                                         self.rows, self.cols,
                                         (MAFAT_PLAN_STAGE_PARTITION if self.stage_partition else 0) |
-                                        (MAFAT_PLAN_PACKED_WEIGHTS if self.packed_weights else 0),
+                                        (MAFAT_PLAN_PACKED_WEIGHTS if self.packed_weights else 0) |
+                                        (MAFAT_PLAN_ROW_REUSE if self.row_reuse else 0),
                                         row_bounds=rb, col_bounds=cb)
         self.n_groups = len(self.group_start)
         if self.tile_batch:

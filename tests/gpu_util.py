@@ -13,13 +13,15 @@ def require_gpu():
 
 
 def run_gpu(layers, h, w, c, params, tiling, batch, dtype, x=None, want_cuts=True, sentinel=True, part=False,
-            bounds=None):
+            bounds=None, reuse=False, packed=False):
     """Runs the library (mafat_run_network) and returns float64 numpy output
     (and the cut tensors).  bounds: tile boundaries of the plan (Plan's
-    `bounds`: None, "balanced" or per-group lists)."""
+    `bounds`: None, "balanced" or per-group lists); reuse: row reuse;
+    packed: packed weights."""
     import torch
     from paper_2107_06960_amd import mafat as M
-    plan = M.Plan(layers, (h, w, c), tiling, stage_partition=part, bounds=bounds)
+    plan = M.Plan(layers, (h, w, c), tiling, stage_partition=part, bounds=bounds, row_reuse=reuse,
+                  packed_weights=packed)
     net = M.Network(plan, params, batch, dtype)
     xt = net.input_tensor(params["x"] if x is None else x)
     if sentinel:
