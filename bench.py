@@ -133,7 +133,7 @@ def untiled_groups(layers):
 
 
 def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs=2, part=False, packed=False,
-                        tile_batch=0, bounds=None):
+                        tile_batch=0, bounds=None, reuse=False):
     """Peak device memory of a run: torch's requested-bytes statistic (the
     sizes of the buffers the caller allocates: input, output, cut tensors,
     parameters, workspace; the library allocates nothing), its peak during
@@ -145,7 +145,7 @@ def measure_peak_memory(M, layers, hwc, tiling, params, batch, dtype, x_np, runs
     torch.cuda.reset_peak_memory_stats()
     base = torch.cuda.memory_stats().get("requested_bytes.all.current", 0)
     plan = M.Plan(layers, hwc, tiling, stage_partition=part, packed_weights=packed, tile_batch=tile_batch,
-                  bounds=bounds)
+                  bounds=bounds, row_reuse=reuse)
     net = M.Network(plan, params, batch, dtype)
     x = net.input_tensor(x_np)
     torch.cuda.synchronize()
@@ -455,6 +455,64 @@ def variable_tiling(args):
     print(json.dumps({"variable_tiling_search": rows}), flush=True)
 
 
+def row_reuse(args):
+    """Row reuse (tile rows in order, every stage output computed once into
+    row bands) against the plain partition (every tile of a stage at once,
+    halos recomputed) and against one tile at a time (the paper's order),
+    YOLOv2 layers 0-15, 608x608x3, bf16, batch 1, packed weights, on the
+    paper's candidates (cuts 16 = no cut, 12, 8; first-group grids 2x2..5x5
+    and 8x8; second group 2x2): predicted and measured peak device memory,
+    host time per frame (warm-up, then the steps) and executed GFLOP.  One
+    JSON line per candidate and execution, then, per device-memory limit,
+    the first candidate in Algorithm 2's order whose prediction fits, for
+    one tile at a time and for row reuse."""
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    from paper_2107_06960_amd import workloads as W
+    torch.cuda.set_device(0)
+    layers, hwc = W.YOLOV2_16, (608, 608, 3)
+    params = W.make_inputs(layers, *hwc, 1, 0, "bf16")
+    kinds = {"all_tiles": {}, "one_tile": {"tile_batch": 1}, "row_reuse": {"reuse": True}}
+    order, meas = [], {}
+    for cut in (16, 12, 8):
+        for t in (2, 3, 4, 5, 8):
+            spec = f"{t}x{t}/NoCut" if cut == 16 else f"{t}x{t}/{cut}/2x2"
+            order.append(spec)
+            for kind, kw in kinds.items():
+                peak, _ = measure_peak_memory(M, layers, hwc, spec, params, 1, "bf16", params["x"], packed=True, **kw)
+                plan = M.Plan(layers, hwc, spec, packed_weights=True, tile_batch=kw.get("tile_batch", 0),
+                              row_reuse=kw.get("reuse", False))
+                net = M.Network(plan, params, 1, "bf16")
+                x = net.input_tensor(params["x"])
+                for _ in range(args.warmup):
+                    net.run(x)
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                for _ in range(args.steps):
+                    net.run(x)
+                torch.cuda.synchronize()
+                ms = (time.perf_counter() - t0) / args.steps * 1e3
+                del net, x
+                gflop = 2 * sum(plan.macs(g)[0] for g in range(plan.n_groups)) / 1e9
+                rec = {"candidate": spec, "execution": kind,
+                       "predicted_mib": round(plan.predict_mem("device", 1, "bf16") / 2 ** 20, 3),
+                       "peak_mib": round(peak / 2 ** 20, 3),
+                       "workspace_mib": round(plan.workspace_size(1, "bf16") / 2 ** 20, 3),
+                       "gflop_executed": round(gflop, 3), "ms": round(ms, 4)}
+                meas[(spec, kind)] = rec
+                print(json.dumps(rec), flush=True)
+    rows = []
+    for lim in (11, 11.5, 12, 13, 14, 16, 20):
+        row = {"limit_mib": lim}
+        for kind in ("one_tile", "row_reuse"):
+            pick = next((c for c in order if meas[(c, kind)]["predicted_mib"] < lim), None)
+            row[kind] = pick
+            row[kind + "_ms"] = meas[(pick, kind)]["ms"] if pick else None
+            row[kind + "_peak_mib"] = meas[(pick, kind)]["peak_mib"] if pick else None
+        rows.append(row)
+    print(json.dumps({"row_reuse_search": rows}), flush=True)
+
+
 def phase_trace(args):
     """Per-launch phase timing of the benchmark workload from the trace
     build of the library (libmafat_trace.so: `python -m
@@ -646,6 +704,8 @@ def main():
                     help="only print per-launch phase timing from the trace build of the library and exit")
     ap.add_argument("--variable-tiling", action="store_true",
                     help="only compare balanced (variable) tile boundaries with the even split and exit")
+    ap.add_argument("--row-reuse", action="store_true",
+                    help="only compare row reuse with all tiles at once and one tile at a time and exit")
     ap.add_argument("--copy-calibration", type=int, metavar="MIB",
                     help="only run a plain device copy of MIB MiB (counter calibration) and exit")
     args = ap.parse_args()
@@ -657,6 +717,9 @@ def main():
         return
     if args.variable_tiling:
         variable_tiling(args)
+        return
+    if args.row_reuse:
+        row_reuse(args)
         return
     if args.phase_trace:
         phase_trace(args)
@@ -730,7 +793,7 @@ def main():
         torch.cuda.synchronize()
         return (time.perf_counter() - t0) / args.steps * 1e3
 
-    partition_ms = krsc_ms = untiled_ms = balanced_ms = None
+    partition_ms = krsc_ms = untiled_ms = balanced_ms = reuse_ms = None
     if not args.no_untiled:
         # The untiled layer-by-layer execution (every stage its own group on
         # a 1x1 grid, same kernels, packed weights), timed exactly like the
@@ -743,6 +806,8 @@ def main():
         krsc_ms = time_variant()
         # Variable tiling: each group's balanced tile boundaries.
         balanced_ms = time_variant(packed_weights=True, bounds="balanced")
+        # Row reuse: tile rows in order, every stage output computed once.
+        reuse_ms = time_variant(packed_weights=True, row_reuse=True)
 
     # The same step replayed from a captured HIP graph (reported beside the
     # plain loop, which is the headline value).
@@ -887,6 +952,7 @@ def main():
         "stage_partition_ms_per_step": round(partition_ms, 5) if partition_ms is not None else None,
         "krsc_weights_ms_per_step": round(krsc_ms, 5) if krsc_ms is not None else None,
         "balanced_bounds_ms_per_step": round(balanced_ms, 5) if balanced_ms is not None else None,
+        "row_reuse_ms_per_step": round(reuse_ms, 5) if reuse_ms is not None else None,
         "step_ms_events": {q: round(float(np.percentile(step_ev_ms, v)), 5)
                            for q, v in (("p10", 10), ("p50", 50), ("p90", 90))},
         "group_ms": [round(v, 5) for v in group_ms],

@@ -171,6 +171,18 @@ hipError_t launch_conv_patch_first(const MfmaShape& shape, const StageArgs& args
 hipError_t launch_pack_weights(const uint16_t* src, uint16_t* dst, int cout, int cin, int bn, int nblk,
                                hipStream_t stream);
 
+// Row reuse: the rows a tile row takes over from its predecessor's bands,
+// every band at once.  Copy k moves bytes[k] bytes from byte offset src[k]
+// to dst[k] of each frame's scratch (frames fstride bytes apart); no two
+// copies' ranges overlap.
+constexpr int kMaxBandCopies = 16;
+struct BandCopyArgs {
+  int64_t src[kMaxBandCopies], dst[kMaxBandCopies], bytes[kMaxBandCopies];
+  int64_t fstride;
+  int32_t ncopy;
+};
+hipError_t launch_band_copy(void* scratch, const BandCopyArgs& args, int batch, hipStream_t stream);
+
 // Pixel-axis block size of each kernel family.
 int block_units(int kind, MfmaShape shape);
 

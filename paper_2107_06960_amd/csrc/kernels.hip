@@ -944,6 +944,47 @@ hipError_t launch_pack_weights(const uint16_t* src, uint16_t* dst, int cout, int
   return hipGetLastError();
 }
 
+namespace {
+// Band take-over copies: unit-sized pieces (16 bytes when every offset and
+// length allows it, else 2) of all copies one after another; y = frame.
+template <typename U>
+__global__ __launch_bounds__(256) void band_copy_kernel(unsigned char* scratch, const BandCopyArgs a) {
+  unsigned char* frame = scratch + static_cast<int64_t>(blockIdx.y) * a.fstride;
+  int64_t total = 0;
+  for (int k = 0; k < a.ncopy; ++k) total += a.bytes[k] / static_cast<int64_t>(sizeof(U));
+  for (int64_t u = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; u < total;
+       u += static_cast<int64_t>(gridDim.x) * 256) {
+    int64_t r = u;
+    int k = 0;
+    while (r >= a.bytes[k] / static_cast<int64_t>(sizeof(U))) {
+      r -= a.bytes[k] / static_cast<int64_t>(sizeof(U));
+      ++k;
+    }
+    const U v = *reinterpret_cast<const U*>(frame + a.src[k] + r * static_cast<int64_t>(sizeof(U)));
+    *reinterpret_cast<U*>(frame + a.dst[k] + r * static_cast<int64_t>(sizeof(U))) = v;
+  }
+}
+}  // namespace
+
+hipError_t launch_band_copy(void* scratch, const BandCopyArgs& args, int batch, hipStream_t stream) {
+  if (args.ncopy <= 0 || batch <= 0) return hipSuccess;
+  bool wide = (args.fstride % 16) == 0;
+  int64_t total = 0;
+  for (int k = 0; k < args.ncopy; ++k) {
+    wide = wide && (args.src[k] % 16) == 0 && (args.dst[k] % 16) == 0 && (args.bytes[k] % 16) == 0;
+    total += args.bytes[k];
+  }
+  const int64_t units = total / (wide ? 16 : 2);
+  if (units <= 0) return hipSuccess;
+  const dim3 grid(static_cast<unsigned>(std::min<int64_t>((units + 255) / 256, 1024)), static_cast<unsigned>(batch));
+  if (wide)
+    hipLaunchKernelGGL(band_copy_kernel<u32x4>, grid, dim3(256), 0, stream, static_cast<unsigned char*>(scratch), args);
+  else
+    hipLaunchKernelGGL(band_copy_kernel<uint16_t>, grid, dim3(256), 0, stream, static_cast<unsigned char*>(scratch),
+                       args);
+  return hipGetLastError();
+}
+
 hipError_t launch_stage(int kind, int dtype, int f, bool pool, MfmaShape shape,
                         const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
   if (args.total_blocks <= 0) return hipSuccess;

@@ -458,6 +458,9 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
     // the two row ranges do not overlap).
     const int row = b0 / std::max(K, 1);
     if (G.reuse && row > 0) {
+      BandCopyArgs C;
+      std::memset(&C, 0, sizeof(C));
+      C.fstride = scr_frame * static_cast<int64_t>(esz);
       for (int s = 0; s + 1 < static_cast<int>(G.stages.size()); ++s) {
         const Stage& S = G.stages[s];
         if (bands.base[static_cast<size_t>(s)][0] < 0) continue;
@@ -465,12 +468,17 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         const int n_rows = S.row_b[static_cast<size_t>(row)] - lo;
         if (n_rows <= 0) continue;
         const int64_t row_elems = static_cast<int64_t>(S.out_w) * S.cout;
-        char* base = static_cast<char*>(ws);
-        const char* from = base + (bands.base[static_cast<size_t>(s)][(row - 1) & 1] + (lo - prev_lo) * row_elems) * esz;
-        char* to = base + bands.base[static_cast<size_t>(s)][row & 1] * esz;
-        const size_t pitch = static_cast<size_t>(scr_frame) * esz;
-        const hipError_t e = hipMemcpy2DAsync(to, pitch, from, pitch, static_cast<size_t>(n_rows * row_elems) * esz,
-                                              static_cast<size_t>(batch), hipMemcpyDeviceToDevice, stream);
+        C.src[C.ncopy] = (bands.base[static_cast<size_t>(s)][(row - 1) & 1] + (lo - prev_lo) * row_elems) * esz;
+        C.dst[C.ncopy] = bands.base[static_cast<size_t>(s)][row & 1] * static_cast<int64_t>(esz);
+        C.bytes[C.ncopy] = n_rows * row_elems * static_cast<int64_t>(esz);
+        if (++C.ncopy == kMaxBandCopies) {
+          const hipError_t e = launch_band_copy(ws, C, batch, stream);
+          if (e != hipSuccess) return fail(MAFAT_EHIP, std::string("band copy failed: ") + hipGetErrorString(e));
+          C.ncopy = 0;
+        }
+      }
+      if (C.ncopy > 0) {
+        const hipError_t e = launch_band_copy(ws, C, batch, stream);
         if (e != hipSuccess) return fail(MAFAT_EHIP, std::string("band copy failed: ") + hipGetErrorString(e));
       }
     }

@@ -290,7 +290,7 @@ def test_stage_partition_plan(lib):
     arr = (M.mafat_layer * 1)(M.mafat_layer(0, 8, 3, 1, 1, 1))
     h = ctypes.c_void_p()
     one = (ctypes.c_int32 * 1)(1)
-    rc = M.lib().mafat_plan_create_flags(arr, 1, 16, 16, 3, (ctypes.c_int32 * 1)(0), 1, one, one, 4, ctypes.byref(h))
+    rc = M.lib().mafat_plan_create_flags(arr, 1, 16, 16, 3, (ctypes.c_int32 * 1)(0), 1, one, one, 8, ctypes.byref(h))
     assert rc == M.MAFAT_EINVAL and not h.value
 
 
@@ -318,7 +318,7 @@ def test_packed_weights_plan(lib):
     arr = (M.mafat_layer * 1)(M.mafat_layer(0, 8, 3, 1, 1, 1))
     h = ctypes.c_void_p()
     one = (ctypes.c_int32 * 1)(1)
-    assert M.lib().mafat_plan_create_flags(arr, 1, 16, 16, 3, (ctypes.c_int32 * 1)(0), 1, one, one, 4,
+    assert M.lib().mafat_plan_create_flags(arr, 1, 16, 16, 3, (ctypes.c_int32 * 1)(0), 1, one, one, 8,
                                            ctypes.byref(h)) == M.MAFAT_EINVAL
 
 

@@ -128,6 +128,35 @@ def _check_against_oracle(orc, name, wl, p, frames, cuts, got):
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("name", ["yolo608_5x5_8_2x2", "yolo416_ftp3", "yolo608_4x4_12_1x1_b8"])
+def test_fullsize_row_reuse(orc, name):
+    # the workloads with row reuse (tile rows in order, every stage output
+    # computed once into row bands), weights laid out as the benchmark's;
+    # the same whole-tensor checks against the untiled oracle
+    require_gpu()
+    import torch
+    from paper_2107_06960_amd import mafat as M
+    wl = W.WORKLOADS[name]
+    p = W.workload_inputs(wl)
+    plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, packed_weights=(wl.dtype == "bf16"), row_reuse=True)
+    print(f"[fullsize] {name} row reuse, workspace {plan.workspace_size(wl.batch, wl.dtype)} B", flush=True)
+    net = M.Network(plan, p, wl.batch, wl.dtype)
+    x = net.input_tensor(p["x"])
+    net.y.fill_(float("nan"))
+    for t in net.cuts:
+        t.fill_(float("nan"))
+    net.run(x)
+    torch.cuda.synchronize()
+    gs, _, _ = W.parse_tiling(wl.tiling, len(wl.layers))
+    cuts = gs[1:]
+    frames = [0] if wl.batch == 1 else [0, wl.batch - 1]
+    got = {c: net.cuts[k].float().cpu().numpy().astype(np.float64)[frames] for k, c in enumerate(cuts)}
+    got[len(wl.layers)] = net.y.float().cpu().numpy().astype(np.float64)[frames]
+    del net, x
+    _check_against_oracle(orc, name + " (row reuse)", wl, p, frames, cuts, got)
+
+
+@pytest.mark.gpu
 def test_fullsize_balanced_bounds(orc):
     # the benchmark workload with variable tiling (each group's balanced
     # boundaries, mafat_balanced_bounds), in the benchmark's launch

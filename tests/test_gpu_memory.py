@@ -20,23 +20,24 @@ FULL = ["tiny", "yolo416_ftp3", "yolo608_5x5_8_2x2", "yolo608_4x4_12_1x1_b8"] + 
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("part,packed,tile_batch", [(False, False, 0), (True, False, 0), (False, True, 0),
-                                                      (False, True, 1)])
+@pytest.mark.parametrize("part,packed,tile_batch,reuse", [(False, False, 0, False), (True, False, 0, False),
+                                                            (False, True, 0, False), (False, True, 1, False),
+                                                            (False, False, 0, True), (False, True, 0, True)])
 @pytest.mark.parametrize("name", FULL)
-def test_device_model_matches_measured_peak(name, part, packed, tile_batch):
+def test_device_model_matches_measured_peak(name, part, packed, tile_batch, reuse):
     require_gpu()
     import torch
     from paper_2107_06960_amd import mafat as M
     wl = W.WORKLOADS[name]
     print(f"[memory] {name}: {wl.h}x{wl.w}x{wl.c} {wl.tiling} batch={wl.batch} {wl.dtype} stage_partition={part} packed={packed} "
-          f"tile_batch={tile_batch}", flush=True)
+          f"tile_batch={tile_batch} row_reuse={reuse}", flush=True)
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     base = torch.cuda.memory_stats().get("requested_bytes.all.current", 0)
     base_alloc = torch.cuda.memory_allocated()
     p = W.workload_inputs(wl)
     plan = M.Plan(wl.layers, (wl.h, wl.w, wl.c), wl.tiling, stage_partition=part, packed_weights=packed,
-                  tile_batch=tile_batch)
+                  tile_batch=tile_batch, row_reuse=reuse)
     net = M.Network(plan, p, wl.batch, wl.dtype)
     x = net.input_tensor(p["x"])
     torch.cuda.synchronize()
