@@ -6,7 +6,9 @@ tile batches and batch 1-2 -- each run of the HIP library compared with the
 oracle's untiled forward (normwise, the tolerance of each dtype), with the
 output filled with NaN first so an element no kernel writes fails.  A second
 set draws the same kind of configurations with variable tiling: random or
-balanced tile boundaries per group (without the stage partition)."""
+balanced tile boundaries per group (without the stage partition); a third
+with row reuse (tile rows in order, every stage output computed once into
+row bands), with even or random row boundaries."""
 import numpy as np
 import pytest
 
@@ -29,7 +31,7 @@ def _bounds(brng, dims, ends, rows, cols):
     return rb, cb
 
 
-def _case(seed, orc, variable=False):
+def _case(seed, orc, variable=False, reuse=False):
     from paper_2107_06960_amd import mafat as M
     rng = np.random.default_rng(1000 + seed)
     brng = np.random.default_rng(5000 + seed)
@@ -62,27 +64,30 @@ def _case(seed, orc, variable=False):
         tb = 0 if part else int(rng.choice([0, 0, 1, 3]))
         batch = int(rng.choice([1, 2]))
         bounds = None
-        if variable:
+        if variable or reuse:
             if part:
                 continue
-            bounds = _bounds(brng, dims, ends, rows, cols) or "balanced"
+            bounds = _bounds(brng, dims, ends, rows, cols) or ("balanced" if variable else None)
+        if reuse:
+            tb = 0
         try:
             plan = M.Plan(layers, (h, w, c0), (starts, rows, cols), stage_partition=part, packed_weights=packed,
-                          tile_batch=tb, bounds=bounds)
+                          tile_batch=tb, bounds=bounds, row_reuse=reuse)
         except M.MafatError:
             continue
-        return plan, layers, (h, w, c0), dtype, batch, (starts, rows, cols, part, packed, tb, plan.bounds)
+        return plan, layers, (h, w, c0), dtype, batch, (starts, rows, cols, part, packed, tb, plan.bounds, reuse)
     raise AssertionError("no valid configuration drawn")
 
 
-def _run(orc, seed, variable):
+def _run(orc, seed, variable, reuse=False):
     require_gpu()
     import torch
     from paper_2107_06960_amd import mafat as M
-    plan, layers, (h, w, c0), dtype, batch, desc = _case(seed, orc, variable)
-    print(f"[random {seed}{' variable tiling' if variable else ''}] {h}x{w}x{c0} {dtype} batch={batch} layers="
+    plan, layers, (h, w, c0), dtype, batch, desc = _case(seed, orc, variable, reuse)
+    kind = " variable tiling" if variable else (" row reuse" if reuse else "")
+    print(f"[random {seed}{kind}] {h}x{w}x{c0} {dtype} batch={batch} layers="
           f"{[(L['op'], L.get('c_out'), L['f'], L['s'], L['p']) for L in layers]} "
-          f"groups/rows/cols/partition/packed/tile_batch/bounds={desc}", flush=True)
+          f"groups/rows/cols/partition/packed/tile_batch/bounds/reuse={desc}", flush=True)
     p = W.make_inputs(layers, h, w, c0, batch, 2000 + seed, dtype)
     net = M.Network(plan, p, batch, dtype)
     x = net.input_tensor(p["x"])
@@ -103,3 +108,8 @@ def test_random_configuration(orc, seed):
 @pytest.mark.parametrize("seed", range(16))
 def test_random_configuration_variable_tiling(orc, seed):
     _run(orc, 100 + seed, True)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_configuration_row_reuse(orc, seed):
+    _run(orc, 200 + seed, False, reuse=True)

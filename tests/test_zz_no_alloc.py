@@ -29,16 +29,18 @@ def _static_run(plan, net, x):
 def test_static_workspace_equals_caller_workspace():
     require_gpu()
     import torch
-    cases = [  # the benchmark workload, then a smaller input, then another network and dtype
-        (W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2", 1, "bf16", 0),
-        (W.YOLOV2_16, (200, 168, 3), "3x2/8/2x2", 2, "bf16", 1),
-        (W.TINY, (64, 64, 3), "2x2", 1, "f32", 2),
+    cases = [  # the benchmark workload, then a smaller input, then another network and dtype,
+               # then row reuse (its band take-over copies run on the static array too)
+        (W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2", 1, "bf16", 0, False),
+        (W.YOLOV2_16, (200, 168, 3), "3x2/8/2x2", 2, "bf16", 1, False),
+        (W.TINY, (64, 64, 3), "2x2", 1, "f32", 2, False),
+        (W.YOLOV2_16, (608, 608, 3), "5x5/8/2x2", 1, "bf16", 3, True),
     ]
-    for layers, hwc, tiling, batch, dtype, seed in cases:
-        print(f"[no-alloc] {len(layers)} layers {hwc} {tiling} batch={batch} {dtype}", flush=True)
-        assert M.Plan(layers, hwc, tiling).workspace_size(batch, dtype) <= M.MAFAT_STATIC_WORKSPACE_MIB << 20
+    for layers, hwc, tiling, batch, dtype, seed, reuse in cases:
+        print(f"[no-alloc] {len(layers)} layers {hwc} {tiling} batch={batch} {dtype} row_reuse={reuse}", flush=True)
+        plan = M.Plan(layers, hwc, tiling, packed_weights=True, row_reuse=reuse)
+        assert plan.workspace_size(batch, dtype) <= M.MAFAT_STATIC_WORKSPACE_MIB << 20
         p = W.make_inputs(layers, *hwc, batch, seed, dtype)
-        plan = M.Plan(layers, hwc, tiling, packed_weights=True)
         net = M.Network(plan, p, batch, dtype)
         x = net.input_tensor(p["x"])
         ref = net.run(x).clone()
