@@ -492,6 +492,22 @@ int mafat_get_config_balanced(const mafat_layer* layers, int32_t n_layers, int32
                               int32_t* out_grid1, int32_t* out_grid2, int64_t* out_pred,
                               int32_t* out_fits);
 
+/* mafat_get_config with every candidate planned with plan_flags (those of
+ * mafat_plan_create_flags: MAFAT_PLAN_ROW_REUSE, MAFAT_PLAN_STAGE_PARTITION,
+ * MAFAT_PLAN_PACKED_WEIGHTS) and, if balanced is nonzero, with its groups'
+ * balanced tile boundaries as mafat_get_config_balanced.  With
+ * MAFAT_PLAN_ROW_REUSE and a device model this is the search under a
+ * device-memory limit for the data-reuse execution of section 3 (tile rows
+ * in order, no halo recompute), whose memory is its row bands.  Same
+ * arguments, outputs and errors as mafat_get_config_balanced, plus those of
+ * mafat_plan_create_flags for the flags. */
+int mafat_get_config_flags(const mafat_layer* layers, int32_t n_layers, int32_t in_h, int32_t in_w,
+                           int32_t in_c, int32_t model, int32_t batch, int32_t dtype, int64_t bias_bytes,
+                           int64_t limit_bytes, const int32_t* cuts, int32_t n_cuts, const int32_t* grids,
+                           int32_t n_grids, int32_t second_grid, int32_t plan_flags, int32_t balanced,
+                           int32_t* out_cut, int32_t* out_grid1, int32_t* out_grid2, int64_t* out_pred,
+                           int32_t* out_fits);
+
 /* Error reporting of this library (no counterpart in the paper).
  * Static text of a status code. */
 const char* mafat_status_string(int status);

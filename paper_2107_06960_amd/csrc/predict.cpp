@@ -29,7 +29,8 @@
 // one group), for each cut the first-group grids t x t in the given order,
 // the second group on a fixed grid; the first configuration whose predicted
 // memory plus the bias is below the limit is returned, else the last one
-// tried.
+// tried.  mafat_get_config_flags plans the candidates with plan flags (row
+// reuse: the device models then give its row bands).
 #include <algorithm>
 #include <cmath>
 #include <new>
@@ -138,8 +139,8 @@ namespace {
 int get_config(const mafat_layer* layers, int32_t n_layers, int32_t in_h, int32_t in_w, int32_t in_c,
                int32_t model, int32_t batch, int32_t dtype, int64_t bias_bytes, int64_t limit_bytes,
                const int32_t* cuts, int32_t n_cuts, const int32_t* grids, int32_t n_grids, int32_t second_grid,
-               bool balanced, int32_t* out_cut, int32_t* out_grid1, int32_t* out_grid2, int64_t* out_pred,
-               int32_t* out_fits) {
+               int32_t flags, bool balanced, int32_t* out_cut, int32_t* out_grid1, int32_t* out_grid2,
+               int64_t* out_pred, int32_t* out_fits) {
   clear_error();
   if (!layers || !cuts || !grids || n_cuts < 1 || n_grids < 1 || second_grid < 1 || !out_cut || !out_grid1 ||
       !out_grid2) {
@@ -171,9 +172,10 @@ int get_config(const mafat_layer* layers, int32_t n_layers, int32_t in_h, int32_
         }
         if (rc == MAFAT_OK)
           rc = mafat_plan_create_bounds(layers, n_layers, in_h, in_w, in_c, starts, ng, rows, rows, rb.data(),
-                                        cb.data(), 0, &plan);
+                                        cb.data(), flags, &plan);
       } else {
-        rc = mafat_plan_create(layers, n_layers, in_h, in_w, in_c, starts, split ? 2 : 1, rows, rows, &plan);
+        rc = mafat_plan_create_flags(layers, n_layers, in_h, in_w, in_c, starts, split ? 2 : 1, rows, rows, flags,
+                                     &plan);
       }
       if (rc != MAFAT_OK) return rc;  // mafat_last_error() names the problem
       int64_t pred = 0;
@@ -206,7 +208,7 @@ extern "C" int mafat_get_config(const mafat_layer* layers, int32_t n_layers, int
                                 int32_t n_grids, int32_t second_grid, int32_t* out_cut, int32_t* out_grid1,
                                 int32_t* out_grid2, int64_t* out_pred, int32_t* out_fits) {
   return get_config(layers, n_layers, in_h, in_w, in_c, model, batch, dtype, bias_bytes, limit_bytes, cuts, n_cuts,
-                    grids, n_grids, second_grid, false, out_cut, out_grid1, out_grid2, out_pred, out_fits);
+                    grids, n_grids, second_grid, 0, false, out_cut, out_grid1, out_grid2, out_pred, out_fits);
 }
 
 extern "C" int mafat_get_config_balanced(const mafat_layer* layers, int32_t n_layers, int32_t in_h,
@@ -218,7 +220,25 @@ extern "C" int mafat_get_config_balanced(const mafat_layer* layers, int32_t n_la
                                          int32_t* out_fits) {
   try {
     return get_config(layers, n_layers, in_h, in_w, in_c, model, batch, dtype, bias_bytes, limit_bytes, cuts,
-                      n_cuts, grids, n_grids, second_grid, true, out_cut, out_grid1, out_grid2, out_pred, out_fits);
+                      n_cuts, grids, n_grids, second_grid, 0, true, out_cut, out_grid1, out_grid2, out_pred,
+                      out_fits);
+  } catch (const std::bad_alloc&) {
+    set_error("host allocation failed");
+    return MAFAT_ENOMEM;
+  }
+}
+
+extern "C" int mafat_get_config_flags(const mafat_layer* layers, int32_t n_layers, int32_t in_h, int32_t in_w,
+                                      int32_t in_c, int32_t model, int32_t batch, int32_t dtype,
+                                      int64_t bias_bytes, int64_t limit_bytes, const int32_t* cuts,
+                                      int32_t n_cuts, const int32_t* grids, int32_t n_grids,
+                                      int32_t second_grid, int32_t plan_flags, int32_t balanced,
+                                      int32_t* out_cut, int32_t* out_grid1, int32_t* out_grid2,
+                                      int64_t* out_pred, int32_t* out_fits) {
+  try {
+    return get_config(layers, n_layers, in_h, in_w, in_c, model, batch, dtype, bias_bytes, limit_bytes, cuts,
+                      n_cuts, grids, n_grids, second_grid, plan_flags, balanced != 0, out_cut, out_grid1, out_grid2,
+                      out_pred, out_fits);
   } catch (const std::bad_alloc&) {
     set_error("host allocation failed");
     return MAFAT_ENOMEM;

@@ -40,7 +40,7 @@ EXPORTS = ("mafat_plan_create", "mafat_plan_create_flags", "mafat_plan_create_bo
            "mafat_plan_stage_fused", "mafat_plan_stage_kernel", "mafat_plan_set_tile_batch",
            "mafat_workspace_size", "mafat_run_group", "mafat_run_group_timed", "mafat_run_stage", "mafat_run_network",
            "mafat_run_network_static",
-           "mafat_predict_mem", "mafat_get_config", "mafat_get_config_balanced", "mafat_status_string",
+           "mafat_predict_mem", "mafat_get_config", "mafat_get_config_balanced", "mafat_get_config_flags", "mafat_status_string",
            "mafat_last_error")
 
 
@@ -110,6 +110,8 @@ def lib():
         L.mafat_get_config.argtypes = [ctypes.POINTER(mafat_layer), i32, i32, i32, i32, i32, i32, i32, i64, i64,
                                        i32p, i32, i32p, i32, i32, i32p, i32p, i32p, i64p, i32p]
         L.mafat_get_config_balanced.argtypes = L.mafat_get_config.argtypes
+        a = list(L.mafat_get_config.argtypes)
+        L.mafat_get_config_flags.argtypes = a[:15] + [i32, i32] + a[15:]
         L.mafat_status_string.argtypes = [ctypes.c_int]
         L.mafat_status_string.restype = ctypes.c_char_p
         L.mafat_last_error.argtypes = []
@@ -331,21 +333,24 @@ def mafat_predict_mem(plan, model, batch, dtype):
 
 
 def mafat_get_config(layers, in_hwc, limit_bytes, model="paper", batch=1, dtype="f32", bias_bytes=0,
-                     cuts=(16, 12, 8), grids=(1, 2, 3, 4, 5), second_grid=2, balanced=False):
+                     cuts=(16, 12, 8), grids=(1, 2, 3, 4, 5), second_grid=2, balanced=False, flags=0):
     """Algorithm 2 (balanced=True: mafat_get_config_balanced, every
-    candidate with balanced tile boundaries).  Returns (tiling spec in the
-    paper's notation, prediction + bias, fits)."""
+    candidate with balanced tile boundaries; flags: plan flags of every
+    candidate, mafat_get_config_flags).  Returns (tiling spec in the paper's
+    notation, prediction + bias, fits)."""
     h, w, c = in_hwc
     cc = (ctypes.c_int32 * len(cuts))(*cuts)
     gg = (ctypes.c_int32 * len(grids))(*grids)
     oc, o1, o2, fits = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
     pred = ctypes.c_int64()
-    name = "mafat_get_config_balanced" if balanced else "mafat_get_config"
-    _check(name,
-           getattr(lib(), name)(_layer_array(layers), len(layers), h, w, c, MEM_MODELS.get(model, model), batch,
-                                DTYPES.get(dtype, dtype), int(bias_bytes), int(limit_bytes), cc, len(cuts), gg,
-                                len(grids), second_grid, ctypes.byref(oc), ctypes.byref(o1), ctypes.byref(o2),
-                                ctypes.byref(pred), ctypes.byref(fits)))
+    head = (_layer_array(layers), len(layers), h, w, c, MEM_MODELS.get(model, model), batch, DTYPES.get(dtype, dtype),
+            int(bias_bytes), int(limit_bytes), cc, len(cuts), gg, len(grids), second_grid)
+    tail = (ctypes.byref(oc), ctypes.byref(o1), ctypes.byref(o2), ctypes.byref(pred), ctypes.byref(fits))
+    if flags:
+        _check("mafat_get_config_flags", lib().mafat_get_config_flags(*head, int(flags), int(bool(balanced)), *tail))
+    else:
+        name = "mafat_get_config_balanced" if balanced else "mafat_get_config"
+        _check(name, getattr(lib(), name)(*head, *tail))
     if oc.value >= len(layers):
         spec = f"{o1.value}x{o1.value}/NoCut"
     else:

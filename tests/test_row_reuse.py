@@ -341,3 +341,28 @@ def test_gpu_row_reuse_random_stacks(orc):
         ref = orc.forward_layers(layers, h, w, 32, p["x"], p)
         assert not np.isnan(out).any()
         assert normwise_err(out, ref) <= TOL[dtype], k
+
+
+def test_library_search_with_row_reuse(M):
+    # Algorithm 2 over candidates planned with row reuse (mafat_get_config_flags)
+    # = the first candidate, in the paper's order, whose row-reuse plan's
+    # device-model prediction plus the bias is below the limit
+    layers, hwc = W.YOLOV2_16, (608, 608, 3)
+    order = [(16, t) for t in (1, 2, 3, 4, 5)] + [(c, t) for c in (12, 8) for t in (1, 2, 3, 4, 5)]
+    spec = lambda cut, t: f"{t}x{t}/NoCut" if cut == 16 else f"{t}x{t}/{cut}/2x2"
+    pred = {k: M.Plan(layers, hwc, spec(*k), row_reuse=True).predict_mem("device", 1, "bf16") for k in order}
+    for mib in (8, 12, 13, 14, 16, 20, 40):
+        got, p, fits = M.mafat_get_config(layers, hwc, mib << 20, model="device", dtype="bf16",
+                                          flags=M.MAFAT_PLAN_ROW_REUSE)
+        first = next((k for k in order if pred[k] < (mib << 20)), None)
+        if first is None:
+            assert not fits and got == spec(*order[-1]), mib
+        else:
+            assert fits and got == spec(*first) and p == pred[first], (mib, got, first)
+    # with balanced boundaries too
+    got, p, fits = M.mafat_get_config(layers, hwc, 14 << 20, model="device", dtype="bf16",
+                                      flags=M.MAFAT_PLAN_ROW_REUSE, balanced=True)
+    assert fits and p < 14 << 20
+    with pytest.raises(M.MafatError):
+        M.mafat_get_config(layers, hwc, 14 << 20, model="device", flags=M.MAFAT_PLAN_ROW_REUSE |
+                           M.MAFAT_PLAN_STAGE_PARTITION)
