@@ -616,7 +616,7 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
 #ifdef MAFAT_TUNING
         if (std::getenv("MAFAT_WG_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH || kind == K_CONV_RGB_MFMA)) {
           static long long wt[2][8192];
-          hipStreamSynchronize(stream);
+          (void)hipStreamSynchronize(stream);
           if (kind == K_CONV_RING) mafat_debug_wg_ring(&wt[0][0]);
           else if (kind == K_CONV_PATCH) mafat_debug_wg_patch(&wt[0][0]);
           else mafat_debug_wg_rgb(&wt[0][0]);
@@ -636,7 +636,7 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         }
         if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH)) {
           long long tr[3][64];
-          hipStreamSynchronize(stream);
+          (void)hipStreamSynchronize(stream);
           if (kind == K_CONV_RING) mafat_debug_ring_trace(&tr[0][0]);
           else mafat_debug_patch_trace(&tr[0][0]);
           std::fprintf(stderr, "RTRACE stage %d-%d %dx%d kg%d ns%d grid %d\n", S.first, S.last, shape.bm, shape.bn,
@@ -655,7 +655,7 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         }
         if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_MFMA || kind == K_CONV_RGB_MFMA)) {
           long long tr[4][64];
-          hipStreamSynchronize(stream);
+          (void)hipStreamSynchronize(stream);
           mafat_debug_trace(&tr[0][0]);
           std::fprintf(stderr, "TRACE stage %d-%d tile %dx%d depth %d grid %d\n", S.first, S.last,
                        shape.bm, shape.bn, shape.depth, A.total_blocks);
