@@ -4,17 +4,20 @@
  * boundary test of the GPU suite (tests/test_gpu_c_caller.py).
  *
  * Usage: mafat_c_caller DIR
- *   DIR/config.txt   "in_h in_w in_c batch dtype n_layers n_groups", then one
- *                    line "op c_out f s p act" per layer, then one line
- *                    "group_start rows cols" per group
+ *   DIR/config.txt   "in_h in_w in_c batch dtype n_layers n_groups flags", then
+ *                    one line "op c_out f s p act" per layer, then one line
+ *                    "group_start rows cols" per group (flags: the plan flags
+ *                    of mafat_plan_create_flags, 0 for mafat_plan_create)
  *   DIR/x.bin        the input, NHWC, batch frames, in the run dtype
  *   DIR/w<l>.bin     conv layer l's weights [c_out][f][f][c_in] in the dtype
  *   DIR/s<l>.bin     its float32 scale, DIR/b<l>.bin its float32 bias
  * Writes DIR/y.bin (the network output, in the dtype) and DIR/regions.txt
  * (every group's tile regions as mafat_plan_regions reports them).
  *
- * Steps: plan, workspace size, caller-owned device buffers (hipMalloc),
- * mafat_run_network on a stream of its own, then the same network group by
+ * Steps: plan, workspace size, caller-owned device buffers (hipMalloc), the
+ * weights of every layer that the plan packs repacked by mafat_pack_weights
+ * into buffers of mafat_packed_weights_size bytes, mafat_run_network on a
+ * stream of its own, then the same network group by
  * group through mafat_run_group into a second output, which must equal the
  * first bit for bit; a workspace one byte too small must be refused with
  * MAFAT_EWORKSPACE and a message, before any launch.  Exit status 0 on
@@ -82,10 +85,10 @@ int main(int argc, char** argv) {
   snprintf(path, sizeof(path), "%s/config.txt", dir);
   FILE* cf = fopen(path, "r");
   if (!cf) { fprintf(stderr, "mafat_c_caller: cannot open %s\n", path); return 1; }
-  int in_h, in_w, in_c, batch, dtype, nl, ng;
+  int in_h, in_w, in_c, batch, dtype, nl, ng, flags;
   mafat_layer layers[MAXL];
   int32_t gs[MAXG], rows[MAXG], cols[MAXG];
-  int ok = fscanf(cf, "%d %d %d %d %d %d %d", &in_h, &in_w, &in_c, &batch, &dtype, &nl, &ng) == 7 &&
+  int ok = fscanf(cf, "%d %d %d %d %d %d %d %d", &in_h, &in_w, &in_c, &batch, &dtype, &nl, &ng, &flags) == 8 &&
            nl >= 1 && nl <= MAXL && ng >= 1 && ng <= MAXG;
   for (int l = 0; ok && l < nl; ++l) {
     mafat_layer* L = &layers[l];
@@ -97,7 +100,8 @@ int main(int argc, char** argv) {
   const size_t esz = dtype == MAFAT_BF16 ? 2 : 4;
 
   mafat_plan* plan = NULL;
-  int rc = mafat_plan_create(layers, nl, in_h, in_w, in_c, gs, ng, rows, cols, &plan);
+  int rc = flags ? mafat_plan_create_flags(layers, nl, in_h, in_w, in_c, gs, ng, rows, cols, flags, &plan)
+                 : mafat_plan_create(layers, nl, in_h, in_w, in_c, gs, ng, rows, cols, &plan);
   if (rc != MAFAT_OK) return fail("mafat_plan_create", rc);
 
   /* shapes: the input of every layer, the output of the last and of every group */
@@ -163,6 +167,22 @@ int main(int argc, char** argv) {
   hipStream_t stream;
   if (!hip_ok(hipStreamCreate(&stream), "hipStreamCreate")) return 1;
 
+  /* layers whose weights the plan takes packed: repack them on the stream */
+  void* wk[MAXL];
+  for (int l = 0; l < nl; ++l) {
+    wk[l] = NULL;
+    if (layers[l].op != MAFAT_CONV) continue;
+    size_t pb = 0;
+    if ((rc = mafat_packed_weights_size(plan, l, dtype, &pb)) != MAFAT_OK) return fail("mafat_packed_weights_size", rc);
+    if (pb == 0) continue;
+    void* packed = NULL;
+    if (!hip_ok(hipMalloc(&packed, pb), "hipMalloc packed weights")) return 1;
+    if ((rc = mafat_pack_weights(plan, l, dtype, w[l], packed, stream)) != MAFAT_OK)
+      return fail("mafat_pack_weights", rc);
+    wk[l] = w[l];
+    w[l] = packed;
+  }
+
   /* a workspace one byte short is refused before anything is enqueued */
   if (ws_bytes > 0) {
     rc = mafat_run_network(plan, batch, dtype, x, y, cuts, (const void* const*)w, (const float* const*)sc,
@@ -205,10 +225,11 @@ int main(int argc, char** argv) {
   free(hy);
   free(hy2);
   hipStreamDestroy(stream);
-  for (int l = 0; l < nl; ++l) { hipFree(w[l]); hipFree(sc[l]); hipFree(bi[l]); }
+  for (int l = 0; l < nl; ++l) { hipFree(w[l]); hipFree(wk[l]); hipFree(sc[l]); hipFree(bi[l]); }
   for (int g = 0; g + 1 < ng; ++g) { hipFree(cuts[g]); hipFree(cuts2[g]); }
   hipFree(x); hipFree(y); hipFree(y2); hipFree(ws);
   mafat_plan_destroy(plan);
-  printf("mafat_c_caller: ok (%d layers, %d groups, batch %d, %s)\n", nl, ng, batch, dtype == MAFAT_BF16 ? "bf16" : "f32");
+  printf("mafat_c_caller: ok (%d layers, %d groups, batch %d, %s, flags %d)\n", nl, ng, batch,
+         dtype == MAFAT_BF16 ? "bf16" : "f32", flags);
   return 0;
 }

@@ -1,5 +1,6 @@
 """The C ABI from a plain C program (tests/c_caller/mafat_c_caller.c, built
-by __graft_entry__.build()): plan, regions, workspace size, caller-owned
+by __graft_entry__.build()): plan (with plan flags: packed weights repacked
+by mafat_pack_weights, row reuse), regions, workspace size, caller-owned
 hipMalloc buffers, mafat_run_network and mafat_run_group on a stream of its
 own, the short-workspace error -- no Python or torch in that process.  Its
 regions must equal the oracle's and its output the oracle's forward within
@@ -33,9 +34,11 @@ def _write(d, name, a, dtype):
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("dtype,batch,tiling", [("f32", 1, "3x3/8/2x2"), ("bf16", 2, "5x5/8/2x2"),
-                                               ("bf16", 1, "2x2/4/3x3/12/1x1")])
-def test_c_caller(orc, tmp_path, dtype, batch, tiling):
+@pytest.mark.parametrize("dtype,batch,tiling,flags", [("f32", 1, "3x3/8/2x2", 0), ("bf16", 2, "5x5/8/2x2", 0),
+                                                     ("bf16", 1, "2x2/4/3x3/12/1x1", 0),
+                                                     ("bf16", 1, "5x5/8/2x2", 6),    # row reuse, packed weights
+                                                     ("f32", 2, "3x3/NoCut", 4)])    # row reuse
+def test_c_caller(orc, tmp_path, dtype, batch, tiling, flags):
     require_gpu()
     assert os.path.exists(EXE), f"{EXE} is missing: run __graft_entry__.build() first"
     layers, (h, w, c) = W.YOLOV2_16, (96, 96, 3)
@@ -43,7 +46,7 @@ def test_c_caller(orc, tmp_path, dtype, batch, tiling):
     p = W.make_inputs(layers, h, w, c, batch, 71, dtype)
     d = str(tmp_path)
     with open(os.path.join(d, "config.txt"), "w") as f:
-        f.write(f"{h} {w} {c} {batch} {1 if dtype == 'bf16' else 0} {len(layers)} {len(gs)}\n")
+        f.write(f"{h} {w} {c} {batch} {1 if dtype == 'bf16' else 0} {len(layers)} {len(gs)} {flags}\n")
         for L in layers:
             f.write(f"{OPS[L['op']]} {int(L.get('c_out', 0))} {L['f']} {L['s']} {L['p']} {ACTS[L.get('act', W.LINEAR)]}\n")
         for g in range(len(gs)):
@@ -54,7 +57,7 @@ def test_c_caller(orc, tmp_path, dtype, batch, tiling):
             _write(d, f"w{k}.bin", p["w"][k], dtype)
             np.ascontiguousarray(p["scale"][k], dtype=np.float32).tofile(os.path.join(d, f"s{k}.bin"))
             np.ascontiguousarray(p["bias"][k], dtype=np.float32).tofile(os.path.join(d, f"b{k}.bin"))
-    print(f"[c caller] {h}x{w}x{c} {tiling} batch={batch} {dtype}", flush=True)
+    print(f"[c caller] {h}x{w}x{c} {tiling} batch={batch} {dtype} flags={flags}", flush=True)
     r = subprocess.run([EXE, d], capture_output=True, text=True, timeout=120)
     print(r.stdout.strip(), r.stderr.strip()[-2000:], flush=True)
     assert r.returncode == 0, r.stderr
