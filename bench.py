@@ -992,6 +992,12 @@ def main():
             sp, sms = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch,
                                           wl.dtype, params["x"], packed=True, tile_batch=1)
             res["tiles_in_sequence"] = {"peak_mem_mib": round(sp / 2 ** 20, 2), "ms_per_step": round(sms, 5)}
+            # Row reuse: tile rows in order, every stage output computed once
+            # into row bands (its time from the headline's loop above).
+            rp, _ = measure_peak_memory(M, wl.layers, (wl.h, wl.w, wl.c), wl.tiling, params, wl.batch,
+                                        wl.dtype, params["x"], packed=True, reuse=True)
+            res["row_reuse"] = {"peak_mem_mib": round(rp / 2 ** 20, 2),
+                                "ms_per_step": round(reuse_ms, 5) if reuse_ms is not None else None}
 
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, params, sum(plan.macs(g)[0] for g in range(ng)))
