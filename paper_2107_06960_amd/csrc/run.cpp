@@ -400,6 +400,72 @@ WorkspaceLayout workspace_layout(const mafat_plan& P, const Group& G, int batch,
 
 namespace {
 
+#ifdef MAFAT_TUNING
+// Tuning builds only: per-workgroup spans (MAFAT_WG_DUMP) and the phase
+// stamps of three workgroups (MAFAT_TRACE_DUMP) of the launch just
+// enqueued, printed to stderr (the stream is synchronised first).
+void dump_launch_trace(int kind, const Stage& S, const MfmaShape& shape, const StageArgs& A,
+                       hipStream_t stream) {
+  if (std::getenv("MAFAT_WG_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH || kind == K_CONV_RGB_MFMA)) {
+    static long long wt[2][8192];
+    (void)hipStreamSynchronize(stream);
+    if (kind == K_CONV_RING) mafat_debug_wg_ring(&wt[0][0]);
+    else if (kind == K_CONV_PATCH) mafat_debug_wg_patch(&wt[0][0]);
+    else mafat_debug_wg_rgb(&wt[0][0]);
+    const int n = std::min(A.total_blocks, 8192);
+    std::vector<long long> d(n);
+    long long s0 = wt[0][0], s1 = wt[0][0], e0 = wt[1][0], e1 = wt[1][0];
+    for (int b = 0; b < n; ++b) {
+      s0 = std::min(s0, wt[0][b]); s1 = std::max(s1, wt[0][b]);
+      e0 = std::min(e0, wt[1][b]); e1 = std::max(e1, wt[1][b]);
+      d[b] = wt[1][b] - wt[0][b];
+    }
+    std::sort(d.begin(), d.end());
+    std::fprintf(stderr, "WGSPAN stage %d-%d kind %d grid %d: span %lld ns, starts %lld, first end %lld, "
+                 "dur p10 %lld p50 %lld p90 %lld max %lld ns\n", S.first, S.last, kind, A.total_blocks,
+                 (e1 - s0) * 10, (s1 - s0) * 10, (e0 - s0) * 10, d[n / 10] * 10, d[n / 2] * 10,
+                 d[(9 * n) / 10] * 10, d.back() * 10);
+  }
+  if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH)) {
+    long long tr[3][64];
+    (void)hipStreamSynchronize(stream);
+    if (kind == K_CONV_RING) mafat_debug_ring_trace(&tr[0][0]);
+    else mafat_debug_patch_trace(&tr[0][0]);
+    std::fprintf(stderr, "RTRACE stage %d-%d %dx%d kg%d ns%d grid %d\n", S.first, S.last, shape.bm, shape.bn,
+                 shape.kg, shape.depth, A.total_blocks);
+    for (int w = 0; w < 3; ++w) {
+      std::fprintf(stderr, "  wg%d slots 6-9: %lld %lld %lld %lld\n", w, (tr[w][6] - tr[w][0]) * 10,
+                   (tr[w][7] - tr[w][0]) * 10, (tr[w][8] - tr[w][0]) * 10, (tr[w][9] - tr[w][0]) * 10);
+      std::fprintf(stderr, "  wg%d decode +%lld staged +%lld loopend +%lld end +%lld iters:", w,
+                   (tr[w][1] - tr[w][0]) * 10, (tr[w][6] - tr[w][0]) * 10, (tr[w][4] - tr[w][0]) * 10,
+                   (tr[w][5] - tr[w][0]) * 10);
+      for (int k = 8; k < 44; ++k) std::fprintf(stderr, " %lld", (tr[w][k] - tr[w][0]) * 10);
+      std::fprintf(stderr, "\n");
+    }
+    std::fprintf(stderr, "  start spread: mid-first %lld last-first %lld ns\n", (tr[1][0] - tr[0][0]) * 10,
+                 (tr[2][0] - tr[0][0]) * 10);
+  }
+  if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_MFMA || kind == K_CONV_RGB_MFMA)) {
+    long long tr[4][64];
+    (void)hipStreamSynchronize(stream);
+    mafat_debug_trace(&tr[0][0]);
+    std::fprintf(stderr, "TRACE stage %d-%d tile %dx%d depth %d grid %d\n", S.first, S.last,
+                 shape.bm, shape.bn, shape.depth, A.total_blocks);
+    for (int w = 0; w < 3; ++w) {
+      std::fprintf(stderr, "  wg%d decoded +%lld addr +%lld issued +%lld lstored +%lld barrier +%lld loop +%lld end +%lld steps:", w,
+                   (tr[w][4] - tr[w][0]) * 10, (tr[w][5] - tr[w][0]) * 10, (tr[w][6] - tr[w][0]) * 10,
+                   (tr[w][7] - tr[w][0]) * 10, (tr[w][1] - tr[w][0]) * 10, (tr[w][2] - tr[w][0]) * 10,
+                   (tr[w][3] - tr[w][0]) * 10);
+      for (int k = 8; k < 20; ++k) std::fprintf(stderr, " %lld", (tr[w][k] - tr[w][0]) * 10);
+      std::fprintf(stderr, " | remap +%lld divs +%lld prefix +%lld", (tr[w][60] - tr[w][0]) * 10,
+                   (tr[w][61] - tr[w][0]) * 10, (tr[w][62] - tr[w][0]) * 10);
+      std::fprintf(stderr, "\n");
+    }
+    std::fprintf(stderr, "  start spread wg-last minus wg0: %lld ns\n", (tr[1][0] - tr[0][0]) * 10);
+  }
+}
+#endif
+
 // Runs stages [s_begin, s_end) of group g: per tile batch (all tiles
 // unless the plan sets fewer), every stage in order, a stage as one launch
 // per 64 tiles; a fused pair whose two stages are both in the range as one
@@ -614,63 +680,7 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         if (e != hipSuccess)
           return fail(MAFAT_EHIP, std::string("stage launch failed: ") + hipGetErrorString(e));
 #ifdef MAFAT_TUNING
-        if (std::getenv("MAFAT_WG_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH || kind == K_CONV_RGB_MFMA)) {
-          static long long wt[2][8192];
-          (void)hipStreamSynchronize(stream);
-          if (kind == K_CONV_RING) mafat_debug_wg_ring(&wt[0][0]);
-          else if (kind == K_CONV_PATCH) mafat_debug_wg_patch(&wt[0][0]);
-          else mafat_debug_wg_rgb(&wt[0][0]);
-          const int n = std::min(A.total_blocks, 8192);
-          std::vector<long long> d(n);
-          long long s0 = wt[0][0], s1 = wt[0][0], e0 = wt[1][0], e1 = wt[1][0];
-          for (int b = 0; b < n; ++b) {
-            s0 = std::min(s0, wt[0][b]); s1 = std::max(s1, wt[0][b]);
-            e0 = std::min(e0, wt[1][b]); e1 = std::max(e1, wt[1][b]);
-            d[b] = wt[1][b] - wt[0][b];
-          }
-          std::sort(d.begin(), d.end());
-          std::fprintf(stderr, "WGSPAN stage %d-%d kind %d grid %d: span %lld ns, starts %lld, first end %lld, "
-                       "dur p10 %lld p50 %lld p90 %lld max %lld ns\n", S.first, S.last, kind, A.total_blocks,
-                       (e1 - s0) * 10, (s1 - s0) * 10, (e0 - s0) * 10, d[n / 10] * 10, d[n / 2] * 10,
-                       d[(9 * n) / 10] * 10, d.back() * 10);
-        }
-        if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_RING || kind == K_CONV_PATCH)) {
-          long long tr[3][64];
-          (void)hipStreamSynchronize(stream);
-          if (kind == K_CONV_RING) mafat_debug_ring_trace(&tr[0][0]);
-          else mafat_debug_patch_trace(&tr[0][0]);
-          std::fprintf(stderr, "RTRACE stage %d-%d %dx%d kg%d ns%d grid %d\n", S.first, S.last, shape.bm, shape.bn,
-                       shape.kg, shape.depth, A.total_blocks);
-          for (int w = 0; w < 3; ++w) {
-            std::fprintf(stderr, "  wg%d slots 6-9: %lld %lld %lld %lld\n", w, (tr[w][6] - tr[w][0]) * 10,
-                         (tr[w][7] - tr[w][0]) * 10, (tr[w][8] - tr[w][0]) * 10, (tr[w][9] - tr[w][0]) * 10);
-            std::fprintf(stderr, "  wg%d decode +%lld staged +%lld loopend +%lld end +%lld iters:", w,
-                         (tr[w][1] - tr[w][0]) * 10, (tr[w][6] - tr[w][0]) * 10, (tr[w][4] - tr[w][0]) * 10,
-                         (tr[w][5] - tr[w][0]) * 10);
-            for (int k = 8; k < 44; ++k) std::fprintf(stderr, " %lld", (tr[w][k] - tr[w][0]) * 10);
-            std::fprintf(stderr, "\n");
-          }
-          std::fprintf(stderr, "  start spread: mid-first %lld last-first %lld ns\n", (tr[1][0] - tr[0][0]) * 10,
-                       (tr[2][0] - tr[0][0]) * 10);
-        }
-        if (std::getenv("MAFAT_TRACE_DUMP") && (kind == K_CONV_MFMA || kind == K_CONV_RGB_MFMA)) {
-          long long tr[4][64];
-          (void)hipStreamSynchronize(stream);
-          mafat_debug_trace(&tr[0][0]);
-          std::fprintf(stderr, "TRACE stage %d-%d tile %dx%d depth %d grid %d\n", S.first, S.last,
-                       shape.bm, shape.bn, shape.depth, A.total_blocks);
-          for (int w = 0; w < 3; ++w) {
-            std::fprintf(stderr, "  wg%d decoded +%lld addr +%lld issued +%lld lstored +%lld barrier +%lld loop +%lld end +%lld steps:", w,
-                         (tr[w][4] - tr[w][0]) * 10, (tr[w][5] - tr[w][0]) * 10, (tr[w][6] - tr[w][0]) * 10,
-                         (tr[w][7] - tr[w][0]) * 10, (tr[w][1] - tr[w][0]) * 10, (tr[w][2] - tr[w][0]) * 10,
-                         (tr[w][3] - tr[w][0]) * 10);
-            for (int k = 8; k < 20; ++k) std::fprintf(stderr, " %lld", (tr[w][k] - tr[w][0]) * 10);
-            std::fprintf(stderr, " | remap +%lld divs +%lld prefix +%lld", (tr[w][60] - tr[w][0]) * 10,
-                         (tr[w][61] - tr[w][0]) * 10, (tr[w][62] - tr[w][0]) * 10);
-            std::fprintf(stderr, "\n");
-          }
-          std::fprintf(stderr, "  start spread wg-last minus wg0: %lld ns\n", (tr[1][0] - tr[0][0]) * 10);
-        }
+        dump_launch_trace(kind, S, shape, A, stream);
 #endif
       }
       started[static_cast<size_t>(s - s_begin)] = launched ? 1 : 0;
