@@ -366,3 +366,19 @@ def test_library_search_with_row_reuse(M):
     with pytest.raises(M.MafatError):
         M.mafat_get_config(layers, hwc, 14 << 20, model="device", flags=M.MAFAT_PLAN_ROW_REUSE |
                            M.MAFAT_PLAN_STAGE_PARTITION)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gpu_row_reuse_wide_rows(orc, dtype):
+    """Tile rows of more tiles than one launch describes (70 per row: two
+    launches per stage and row), three rows, batch 2."""
+    require_gpu()
+    layers, (h, w, c) = W.TINY, (40, 600, 3)
+    gs, rows, cols = [0], [3], [70]
+    print(f"[row reuse] {h}x{w}x{c} 3x70 batch=2 {dtype}", flush=True)
+    p = W.make_inputs(layers, h, w, c, 2, seed=43, dtype=dtype)
+    out = run_gpu(layers, h, w, c, p, (gs, rows, cols), 2, dtype, want_cuts=False, reuse=True)
+    ref = orc.forward_layers(layers, h, w, c, p["x"], p)
+    assert not np.isnan(out).any()
+    assert normwise_err(out, ref) <= TOL[dtype]
