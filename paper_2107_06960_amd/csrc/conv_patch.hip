@@ -81,8 +81,8 @@ MAFAT_WG_TRACE_DECL(g_wg_patch)
 #define MAFAT_PTRACE(slot_)                                                                      \
   do {                                                                                           \
     if (threadIdx.x == 0 && (slot_) < 64 &&                                                      \
-        (blockIdx.x == 0 || blockIdx.x == gridDim.x / 2 || blockIdx.x == gridDim.x - 1))         \
-      g_patch_trace[blockIdx.x == 0 ? 0 : (blockIdx.x == gridDim.x - 1 ? 2 : 1)][(slot_)] =      \
+        (blockIdx.x == 0 || blockIdx.x == a.total_blocks / 2 || blockIdx.x == a.total_blocks - 1))         \
+      g_patch_trace[blockIdx.x == 0 ? 0 : (blockIdx.x == a.total_blocks - 1 ? 2 : 1)][(slot_)] =      \
           wall_clock64();                                                                        \
   } while (0)
 #else
@@ -145,6 +145,10 @@ __device__ __forceinline__ int patch_key(int py) { return ((py & 1) << 1) | ((py
 template <int BR, int BC, int BM, int BN, int WGM, int WGN, int NS, bool POOL, int N2 = 0, bool PRE = false>
 __global__ __launch_bounds__(64 * WGM * WGN) __attribute__((amdgpu_waves_per_eu(PRE ? MAFAT_PRE_WAVES : 1)))
 void conv_patch_kernel(const StageArgs a) {
+  if (__builtin_expect(blockIdx.y != 0, 0)) {  // the second grid row: carried band copies (row reuse)
+    carried_copies();
+    return;
+  }
   constexpr int NWAVE = WGM * WGN;
   constexpr int WM = BM / WGM, WN = BN / WGN, MT = WM / 16, NT = WN / 16;
   constexpr int PR = BR + 2, PC = BC + 2;
@@ -823,7 +827,7 @@ void conv_patch_kernel(const StageArgs a) {
 
 template <bool POOL>
 hipError_t launch_patch_p(const MfmaShape& sh, const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
-  const dim3 grid(static_cast<unsigned>(args.total_blocks));
+  const dim3 grid(static_cast<unsigned>(args.total_blocks), args.copy_blocks > 0 ? 2u : 1u);
 #define MAFAT_PATCH(br_, bc_, bm_, bn_, wgm_, wgn_, ns_)                                               \
   if (sh.br == (br_) && sh.bc == (bc_) && sh.bm == (bm_) && sh.bn == (bn_) && sh.wgm == (wgm_) &&      \
       sh.wgn == (wgn_) && sh.depth == (ns_)) {                                                        \
@@ -845,7 +849,7 @@ hipError_t launch_patch_p(const MfmaShape& sh, const StageArgs& args, hipStream_
 hipError_t launch_conv_patch_fused(const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
   if (args.total_blocks <= 0) return hipSuccess;
   if (args.cout != 128 || (args.cout2 != 64 && args.cout2 != 32)) return hipErrorInvalidValue;
-  const dim3 grid(static_cast<unsigned>(args.total_blocks));
+  const dim3 grid(static_cast<unsigned>(args.total_blocks), args.copy_blocks > 0 ? 2u : 1u);
   if (args.cout2 == 64)
     hipExtLaunchKernelGGL((conv_patch_kernel<8, 16, 128, 128, 4, 2, 1, false, 64>), grid, dim3(512), 0, stream,
                           ev.start, ev.stop, 0, args);
@@ -862,7 +866,7 @@ hipError_t launch_conv_patch_first(const MfmaShape& sh, const StageArgs& args, h
   if (sh.br == (br_) && sh.bc == (bc_) && sh.bm == (bm_) && sh.bn == 64 && sh.wgm == (wgm_) &&            \
       sh.wgn == (wgn_)) {                                                                                 \
     hipExtLaunchKernelGGL((conv_patch_kernel<br_, bc_, bm_, 64, wgm_, wgn_, 1, true, 0, true>),           \
-                          dim3(static_cast<unsigned>(args.total_blocks)), dim3(64 * (wgm_) * (wgn_)), 0,  \
+                          dim3(static_cast<unsigned>(args.total_blocks), args.copy_blocks > 0 ? 2u : 1u), dim3(64 * (wgm_) * (wgn_)), 0,  \
                           stream, ev.start, ev.stop, 0, args);                                            \
     return hipGetLastError();                                                                             \
   }

@@ -58,8 +58,8 @@ MAFAT_WG_TRACE_DECL(g_wg_ring)
 #define MAFAT_RTRACE(slot_)                                                                      \
   do {                                                                                           \
     if (threadIdx.x == 0 && (slot_) < 64 &&                                                      \
-        (blockIdx.x == 0 || blockIdx.x == gridDim.x / 2 || blockIdx.x == gridDim.x - 1))         \
-      g_ring_trace[blockIdx.x == 0 ? 0 : (blockIdx.x == gridDim.x - 1 ? 2 : 1)][(slot_)] =       \
+        (blockIdx.x == 0 || blockIdx.x == a.total_blocks / 2 || blockIdx.x == a.total_blocks - 1))         \
+      g_ring_trace[blockIdx.x == 0 ? 0 : (blockIdx.x == a.total_blocks - 1 ? 2 : 1)][(slot_)] =       \
           wall_clock64();                                                                        \
   } while (0)
 #else
@@ -99,6 +99,10 @@ __device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "mem
 
 template <int F, int BM, int BN, int WGM, int WGN, int KG, int NS, int KORD, bool POOL>
 __global__ __launch_bounds__(64 * WGM * WGN * KG) void conv_ring_kernel(const StageArgs a) {
+  if (__builtin_expect(blockIdx.y != 0, 0)) {  // the second grid row: carried band copies (row reuse)
+    carried_copies();
+    return;
+  }
   constexpr int NWAVE = WGM * WGN * KG;
   constexpr int P = (F - 1) / 2;
   constexpr int WM = BM / WGM, WN = BN / WGN, MT = WM / 16, NT = WN / 16;
@@ -405,7 +409,7 @@ __global__ __launch_bounds__(64 * WGM * WGN * KG) void conv_ring_kernel(const St
 
 template <int F, bool POOL>
 hipError_t launch_ring_fp(const MfmaShape& sh, const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
-  const dim3 grid(static_cast<unsigned>(args.total_blocks));
+  const dim3 grid(static_cast<unsigned>(args.total_blocks), args.copy_blocks > 0 ? 2u : 1u);
 #define MAFAT_RING(bm_, bn_, wgm_, wgn_, kg_, ns_, ko_)                                             \
   if (sh.bm == (bm_) && sh.bn == (bn_) && sh.wgm == (wgm_) && sh.wgn == (wgn_) && sh.kg == (kg_) && \
       sh.depth == (ns_) && sh.kord == (ko_)) {                                                     \

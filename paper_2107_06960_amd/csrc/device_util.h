@@ -124,6 +124,36 @@ __device__ __forceinline__ BlockPos decode_block(const StageArgs& a, KTile* tile
   return p;
 }
 
+// Row reuse take-over copies carried by a launch (StageArgs::copy_*): a
+// launch that carries copies has a second grid row (blockIdx.y = 1) of
+// total_blocks workgroups, whose first copy_blocks copy 16 bytes per thread
+// and step and the rest return at once; the first row computes as always,
+// its test of blockIdx.y needing no memory access.  The copy table is read
+// through the argument segment (a dynamic index into the by-value copy
+// would go through private memory).
+__device__ __forceinline__ void carried_copies() {
+  const StageArgs* ka = (const StageArgs*)__builtin_amdgcn_kernarg_segment_ptr();
+  const int cb = static_cast<int>(blockIdx.x);
+  if (cb >= ka->copy_blocks) return;
+  const int n = ka->ncopy;
+  int64_t per_frame = 0;
+  for (int k = 0; k < n; ++k) per_frame += ka->copy_bytes[k] >> 4;
+  const int64_t total = per_frame * ka->copy_frames;
+  const int64_t step = static_cast<int64_t>(ka->copy_blocks) * blockDim.x;
+  for (int64_t u = static_cast<int64_t>(cb) * blockDim.x + threadIdx.x; u < total; u += step) {
+    const int64_t f = u / per_frame;
+    int64_t r = u - f * per_frame;
+    int k = 0;
+    while (k + 1 < n && r >= (ka->copy_bytes[k] >> 4)) {
+      r -= ka->copy_bytes[k] >> 4;
+      ++k;
+    }
+    unsigned char* fb = ka->copy_base + f * ka->copy_fstride;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(fb + ka->copy_src[k] + (r << 4));
+    *reinterpret_cast<u32x4*>(fb + ka->copy_dst[k] + (r << 4)) = v;
+  }
+}
+
 // Output pixel of row m of a tile's GEMM.  Without a fused pool the rows run
 // over the computed rectangle in row-major order; with one, every 4
 // consecutive rows are one 2x2 pool window (the rectangle has even origin and

@@ -19,6 +19,9 @@ struct KTile {
   int32_t src_off, dst_off;  // element offsets within one frame's buffer
 };
 
+// Band take-over copies one stage launch carries (row reuse).
+constexpr int kMaxCarriedCopies = 4;
+
 struct StageArgs {
   const void* src;
   void* dst;
@@ -52,6 +55,18 @@ struct StageArgs {
   const float* scale0;
   const float* bias0;
   int32_t act0, in_h0, in_w0;
+  // Row reuse: band take-over copies carried by this launch.  With
+  // copy_blocks > 0 the grid has a second row (blockIdx.y = 1) of
+  // total_blocks workgroups, of which the first copy_blocks (at most
+  // total_blocks) compute nothing: for each of copy_frames frames
+  // (copy_fstride bytes apart from copy_base) they move copy_bytes[k] bytes
+  // from byte offset copy_src[k] to copy_dst[k].  Offsets and lengths are
+  // multiples of 16; no range overlaps another or anything the launch's own
+  // workgroups read or write.
+  unsigned char* copy_base;
+  int64_t copy_fstride;
+  int64_t copy_src[kMaxCarriedCopies], copy_dst[kMaxCarriedCopies], copy_bytes[kMaxCarriedCopies];
+  int32_t copy_blocks, ncopy, copy_frames;
   int32_t mblk_prefix[kMaxTilesPerLaunch + 1];
   KTile tiles[kMaxTilesPerLaunch];
 };

@@ -34,9 +34,9 @@ __device__ long long g_trace[4][64];
 MAFAT_WG_TRACE_DECL(g_wg_rgb)
 #define MAFAT_TRACE(slot_)                                                                     \
   do {                                                                                         \
-    if (threadIdx.x == 0 && (blockIdx.x == 0 || blockIdx.x == gridDim.x - 1 ||                 \
-                             blockIdx.x == gridDim.x / 2) && (slot_) < 64)                     \
-      g_trace[blockIdx.x == 0 ? 0 : (blockIdx.x == gridDim.x - 1 ? 1 : 2)][(slot_)] = wall_clock64(); \
+    if (threadIdx.x == 0 && (blockIdx.x == 0 || blockIdx.x == a.total_blocks - 1 ||            \
+                             blockIdx.x == a.total_blocks / 2) && (slot_) < 64)                     \
+      g_trace[blockIdx.x == 0 ? 0 : (blockIdx.x == a.total_blocks - 1 ? 1 : 2)][(slot_)] = wall_clock64(); \
   } while (0)
 #else
 #define MAFAT_TRACE(slot_) do {} while (0)
@@ -142,6 +142,10 @@ __device__ __forceinline__ void store_direct(const f32x4 (&acc)[BN / 32][BM / 32
 // below 2^31 within a frame's source buffer and the weights (host-checked).
 template <int DT, int F, int BM, int BN, bool POOL, int DEPTH, int KG>
 __global__ __launch_bounds__(256 * KG) void conv_mfma_kernel(const StageArgs a) {
+  if (__builtin_expect(blockIdx.y != 0, 0)) {  // the second grid row: carried band copies (row reuse)
+    carried_copies();
+    return;
+  }
   using T = typename Elt<DT>::T;
   constexpr int ESZ = static_cast<int>(sizeof(T));
   constexpr int P = (F - 1) / 2;
@@ -379,6 +383,10 @@ __global__ __launch_bounds__(256 * KG) void conv_mfma_kernel(const StageArgs a) 
 // padding, taken from the stage arguments (a.f, a.s, a.p).
 template <int DT, int F, bool POOL>
 __global__ __launch_bounds__(256) void conv_direct_kernel(const StageArgs a) {
+  if (__builtin_expect(blockIdx.y != 0, 0)) {  // the second grid row: carried band copies (row reuse)
+    carried_copies();
+    return;
+  }
   using T = typename Elt<DT>::T;
   const int f = F > 0 ? F : a.f;
   const int st = F > 0 ? 1 : a.s;
@@ -459,6 +467,10 @@ __global__ __launch_bounds__(256) void conv_direct_kernel(const StageArgs a) {
 template <int DT, bool POOL>
 __global__ __launch_bounds__(256) 
 void conv_rgb_kernel(const StageArgs a) {
+  if (__builtin_expect(blockIdx.y != 0, 0)) {  // the second grid row: carried band copies (row reuse)
+    carried_copies();
+    return;
+  }
   using T = typename Elt<DT>::T;
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
   constexpr int Q = POOL ? 2 : 1;   // output pixels per thread along each axis
@@ -608,6 +620,10 @@ void conv_rgb_kernel(const StageArgs a) {
 // Requires c_out = 16 * NJ, c_in = 3, f = 3, s = 1, p = 1 (host-checked).
 template <bool POOL, int NJ>
 __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
+  if (__builtin_expect(blockIdx.y != 0, 0)) {  // the second grid row: carried band copies (row reuse)
+    carried_copies();
+    return;
+  }
   typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
   typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
   constexpr int BR = kRgbBlockRows, BC = kRgbBlockCols;  // conv outputs per block, even
@@ -805,6 +821,10 @@ __global__ __launch_bounds__(256) void conv_rgb_mfma_kernel(const StageArgs a) {
 // coordinates.
 template <int DT>
 __global__ __launch_bounds__(256) void pool_kernel(const StageArgs a) {
+  if (__builtin_expect(blockIdx.y != 0, 0)) {  // the second grid row: carried band copies (row reuse)
+    carried_copies();
+    return;
+  }
   using T = typename Elt<DT>::T;
   KTile tl;
   const BlockPos bp = decode_block(a, &tl);
@@ -828,7 +848,7 @@ __global__ __launch_bounds__(256) void pool_kernel(const StageArgs a) {
 
 template <int DT, int F, bool POOL, int DEPTH>
 hipError_t launch_mfma(MfmaShape sh, const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
-  const dim3 grid(static_cast<unsigned>(args.total_blocks));
+  const dim3 grid(static_cast<unsigned>(args.total_blocks), args.copy_blocks > 0 ? 2u : 1u);
 #define MAFAT_SHAPE(bm_, bn_, kg_)                                                             \
   if (sh.bm == (bm_) && sh.bn == (bn_) && sh.kg == (kg_)) {                                    \
     hipExtLaunchKernelGGL((conv_mfma_kernel<DT, F, bm_, bn_, POOL, DEPTH, kg_>), grid, dim3(256 * (kg_)), 0, \
@@ -844,7 +864,7 @@ hipError_t launch_mfma(MfmaShape sh, const StageArgs& args, hipStream_t stream, 
 
 template <int DT, int F, bool POOL>
 hipError_t launch_conv(int kind, MfmaShape sh, const StageArgs& args, hipStream_t stream, LaunchEvents ev) {
-  const dim3 grid(static_cast<unsigned>(args.total_blocks)), block(256);
+  const dim3 grid(static_cast<unsigned>(args.total_blocks), args.copy_blocks > 0 ? 2u : 1u), block(256);
   if (kind == K_CONV_DIRECT) {
     hipExtLaunchKernelGGL((conv_direct_kernel<DT, F, POOL>), grid, block, 0, stream, ev.start, ev.stop, 0, args);
     return hipGetLastError();
@@ -880,7 +900,7 @@ template <int DT>
 hipError_t launch_dt(int kind, int f, bool pool, MfmaShape sh, const StageArgs& args,
                      hipStream_t stream, LaunchEvents ev) {
   if (kind == K_POOL) {
-    hipExtLaunchKernelGGL((pool_kernel<DT>), dim3(static_cast<unsigned>(args.total_blocks)), dim3(256),
+    hipExtLaunchKernelGGL((pool_kernel<DT>), dim3(static_cast<unsigned>(args.total_blocks), args.copy_blocks > 0 ? 2u : 1u), dim3(256),
                           0, stream, ev.start, ev.stop, 0, args);
     return hipGetLastError();
   }

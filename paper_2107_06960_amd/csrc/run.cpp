@@ -515,38 +515,80 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
   const int K = G.tile_batch;
   const int64_t bstride = G.partition ? G.scratch_elems : static_cast<int64_t>(K) * G.scratch_elems;
   std::vector<char> started(static_cast<size_t>(s_end - s_begin), 0);  // start event recorded
+  // Row reuse: the take-over copy of stage s's band into row i, and which
+  // launch carries it: launches are numbered within a row; carrier[s] >= 0:
+  // that launch of row i - 1 (the first after the band's reader, which
+  // neither reads nor writes it); -1: row i's first launch (it reads the
+  // group input and writes another band); -2: a copy launch of its own.
+  const int ns_all = static_cast<int>(G.stages.size());
+  std::vector<int> launch_of(static_cast<size_t>(ns_all), 0), carrier(static_cast<size_t>(ns_all), -2);
+  int nlaunch = 0;
+  struct BandCopy { int64_t src, dst, bytes; bool aligned; };
+  auto band_copy = [&](int s, int i, BandCopy* c) {
+    const Stage& S = G.stages[static_cast<size_t>(s)];
+    if (bands.base[static_cast<size_t>(s)][0] < 0) return false;
+    const int lo = S.band_lo[static_cast<size_t>(i)], prev_lo = S.band_lo[static_cast<size_t>(i - 1)];
+    const int n_rows = S.row_b[static_cast<size_t>(i)] - lo;
+    if (n_rows <= 0) return false;
+    const int64_t row_elems = static_cast<int64_t>(S.out_w) * S.cout, e = static_cast<int64_t>(esz);
+    c->src = (bands.base[static_cast<size_t>(s)][(i - 1) & 1] + (lo - prev_lo) * row_elems) * e;
+    c->dst = bands.base[static_cast<size_t>(s)][i & 1] * e;
+    c->bytes = n_rows * row_elems * e;
+    c->aligned = ((c->src | c->dst | c->bytes | (scr_frame * e)) & 15) == 0;
+    return true;
+  };
+  auto run_copies = [&](const std::vector<BandCopy>& cs) {
+    BandCopyArgs C;
+    std::memset(&C, 0, sizeof(C));
+    C.fstride = scr_frame * static_cast<int64_t>(esz);
+    for (size_t k = 0; k < cs.size(); ++k) {
+      C.src[C.ncopy] = cs[k].src;
+      C.dst[C.ncopy] = cs[k].dst;
+      C.bytes[C.ncopy] = cs[k].bytes;
+      if (++C.ncopy == kMaxBandCopies || k + 1 == cs.size()) {
+        const hipError_t e = launch_band_copy(ws, C, batch, stream);
+        if (e != hipSuccess) return fail(MAFAT_EHIP, std::string("band copy failed: ") + hipGetErrorString(e));
+        C.ncopy = 0;
+      }
+    }
+    return static_cast<int>(MAFAT_OK);
+  };
+  if (G.reuse) {
+    for (int s = s_begin; s < s_end; ++s) {
+      const bool fz = stage_config(*plan, G, G.stages[static_cast<size_t>(s)], batch, dtype).fuse > 0 &&
+                      s + 1 < s_end;
+      launch_of[static_cast<size_t>(s)] = nlaunch;
+      if (fz) launch_of[static_cast<size_t>(++s)] = nlaunch;
+      ++nlaunch;
+    }
+    for (int s = 0; s + 1 < ns_all; ++s) {
+      if (bands.base[static_cast<size_t>(s)][0] < 0) continue;
+      const int reader = launch_of[static_cast<size_t>(s + 1)];
+      carrier[static_cast<size_t>(s)] = (reader + 1 < nlaunch) ? reader + 1
+                                        : (launch_of[static_cast<size_t>(s)] != 0 ? -1 : -2);
+    }
+  }
   for (int b0 = 0; b0 < G.ntiles; b0 += K) {
     const int b1 = std::min(G.ntiles, b0 + K);
     const bool last_batch = b1 >= G.ntiles;
-    // Row reuse: batch = tile row i (K = the grid's columns).  Each band
-    // this row writes into first takes over, from row i - 1's band, the
-    // rows above row i's own that the next stage reads (within one buffer
-    // the two row ranges do not overlap).
+    // Row reuse: batch = tile row `row` (K = the grid's columns).  Each band
+    // the row writes into first takes over, from the previous row's band,
+    // the rows above its own that the next stage reads (within one buffer
+    // the two row ranges do not overlap).  The copies ride in launches that
+    // neither read nor write the band (carrier[]); the rest, and any the
+    // kernels cannot carry, run as one copy launch before the row.
     const int row = b0 / std::max(K, 1);
+    std::vector<BandCopy> first_copies;  // carried by this row's first launch
     if (G.reuse && row > 0) {
-      BandCopyArgs C;
-      std::memset(&C, 0, sizeof(C));
-      C.fstride = scr_frame * static_cast<int64_t>(esz);
-      for (int s = 0; s + 1 < static_cast<int>(G.stages.size()); ++s) {
-        const Stage& S = G.stages[s];
-        if (bands.base[static_cast<size_t>(s)][0] < 0) continue;
-        const int lo = S.band_lo[static_cast<size_t>(row)], prev_lo = S.band_lo[static_cast<size_t>(row - 1)];
-        const int n_rows = S.row_b[static_cast<size_t>(row)] - lo;
-        if (n_rows <= 0) continue;
-        const int64_t row_elems = static_cast<int64_t>(S.out_w) * S.cout;
-        C.src[C.ncopy] = (bands.base[static_cast<size_t>(s)][(row - 1) & 1] + (lo - prev_lo) * row_elems) * esz;
-        C.dst[C.ncopy] = bands.base[static_cast<size_t>(s)][row & 1] * static_cast<int64_t>(esz);
-        C.bytes[C.ncopy] = n_rows * row_elems * static_cast<int64_t>(esz);
-        if (++C.ncopy == kMaxBandCopies) {
-          const hipError_t e = launch_band_copy(ws, C, batch, stream);
-          if (e != hipSuccess) return fail(MAFAT_EHIP, std::string("band copy failed: ") + hipGetErrorString(e));
-          C.ncopy = 0;
-        }
+      std::vector<BandCopy> own;
+      for (int s = 0; s + 1 < ns_all; ++s) {
+        BandCopy c;
+        if (!band_copy(s, row, &c)) continue;
+        if (carrier[static_cast<size_t>(s)] == -1 && c.aligned) first_copies.push_back(c);
+        else if (carrier[static_cast<size_t>(s)] < 0 || !c.aligned) own.push_back(c);
       }
-      if (C.ncopy > 0) {
-        const hipError_t e = launch_band_copy(ws, C, batch, stream);
-        if (e != hipSuccess) return fail(MAFAT_EHIP, std::string("band copy failed: ") + hipGetErrorString(e));
-      }
+      const int rc = run_copies(own);
+      if (rc != MAFAT_OK) return rc;
     }
     // A fused pair never writes the buffer it reads: inside a group its
     // input and output would be the same ping-pong scratch buffer (stages
@@ -555,8 +597,23 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
     // batch run with the two scratch buffers swapped.
     bool swapped = false;
     auto eff = [&](int buf) { return (swapped && buf >= 0) ? 1 - buf : buf; };
+    int launch = -1;
     for (int s = s_begin; s < s_end; ++s) {
+      ++launch;
       const Stage& S = G.stages[s];
+      // take-over copies this launch carries: its row's (first launch) and
+      // the next row's whose band this launch leaves alone
+      std::vector<BandCopy> carry;
+      if (G.reuse) {
+        if (launch == 0) carry = first_copies;
+        if (row + 1 < G.rows)
+          for (int sb = 0; sb + 1 < ns_all; ++sb) {
+            BandCopy c;
+            if (carrier[static_cast<size_t>(sb)] == launch && band_copy(sb, row + 1, &c)) {
+              if (c.aligned) carry.push_back(c);
+            }
+          }
+      }
       hipEvent_t ev_start = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin)]) : nullptr;
       hipEvent_t ev_stop = events ? static_cast<hipEvent_t>(events[2 * (s - s_begin) + 1]) : nullptr;
       bool launched = started[static_cast<size_t>(s - s_begin)] != 0;
@@ -656,6 +713,34 @@ int run_group_impl(const mafat_plan* plan, int g, int s_begin, int s_end, int ba
         A.total_blocks = static_cast<int32_t>(blocks);
         const bool last_chunk = last_batch && t1 >= b1;
         const LaunchEvents lev{launched ? nullptr : ev_start, last_chunk ? ev_stop : nullptr};
+        // carried copies: in the first chunk of the launch, as extra
+        // workgroups; those that do not fit (or a launch with nothing to
+        // compute) get a copy launch of their own here
+        A.copy_blocks = A.ncopy = 0;
+        if (t0 == b0 && !carry.empty()) {
+          std::vector<BandCopy> rest;
+          int64_t units = 0;
+          for (const BandCopy& c : carry) {
+            if (A.total_blocks > 0 && A.ncopy < kMaxCarriedCopies) {
+              A.copy_src[A.ncopy] = c.src;
+              A.copy_dst[A.ncopy] = c.dst;
+              A.copy_bytes[A.ncopy] = c.bytes;
+              ++A.ncopy;
+              units += c.bytes / 16;
+            } else {
+              rest.push_back(c);
+            }
+          }
+          if (A.ncopy > 0) {
+            A.copy_base = static_cast<unsigned char*>(ws);
+            A.copy_fstride = scr_frame * static_cast<int64_t>(esz);
+            A.copy_frames = batch;
+            A.copy_blocks = static_cast<int32_t>(
+                std::min<int64_t>(std::min<int64_t>((units * batch + 255) / 256, 64), A.total_blocks));
+          }
+          const int rc = run_copies(rest);
+          if (rc != MAFAT_OK) return rc;
+        }
         hipError_t e;
         if (A.total_blocks <= 0) {
           e = hipSuccess;
