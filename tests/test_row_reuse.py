@@ -382,3 +382,21 @@ def test_gpu_row_reuse_wide_rows(orc, dtype):
     ref = orc.forward_layers(layers, h, w, c, p["x"], p)
     assert not np.isnan(out).any()
     assert normwise_err(out, ref) <= TOL[dtype]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_gpu_row_reuse_odd_channels(orc, dtype):
+    """Channel counts whose band rows are not whole 16-byte pieces (3, 5, 7
+    channels): the take-over copies then run as copy launches of their own
+    (2-byte pieces) instead of riding in a stage launch."""
+    require_gpu()
+    layers = [W.conv(5, 3), W.conv(7, 3), W.maxpool(2, 2, 0), W.conv(3, 3), W.conv(5, 1)]
+    h, w, c = 45, 37, 3
+    gs, rows, cols = [0, 3], [4, 3], [2, 1]
+    print(f"[row reuse] odd channels {h}x{w}x{c} batch=2 {dtype}", flush=True)
+    p = W.make_inputs(layers, h, w, c, 2, seed=47, dtype=dtype)
+    out = run_gpu(layers, h, w, c, p, (gs, rows, cols), 2, dtype, want_cuts=False, reuse=True)
+    ref = orc.forward_layers(layers, h, w, c, p["x"], p)
+    assert not np.isnan(out).any()
+    assert normwise_err(out, ref) <= TOL[dtype]
